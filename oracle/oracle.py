@@ -1,0 +1,158 @@
+"""Python access to the CPU oracle (``carve_oracle.c``) for the chunked CARVE layer.
+
+TEST INFRASTRUCTURE ONLY.  This module (and the C library it wraps) may be
+imported only by ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline
+leg of ``bench.py``.  It shares no code with the HIP path and never imports
+the product package.
+
+All arrays are converted to contiguous float64 before the call; layouts are
+those documented in ``carve_oracle.h`` ([B,T,H,D] token tensors,
+[B,H,Dv,Dk] states, shared [R,Dv] / [Dk,R] / [Dv,R] parameters).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "carve_oracle.c")
+_LIB = os.path.join(_HERE, "libcarve_oracle.so")
+
+_lib = None
+
+
+class _Dims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in ("B", "T", "H", "Dk", "Dv", "R", "L")]
+
+
+def build() -> str:
+    """Compile the oracle with gcc (IEEE double, no FMA contraction)."""
+    tmp = _LIB + ".tmp"
+    cmd = ["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-ffp-contract=off",
+           "-fno-fast-math", "-Wall", "-o", tmp, _SRC, "-lm", "-lpthread"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    P = ctypes.POINTER(ctypes.c_double)
+    D = ctypes.POINTER(_Dims)
+    lib.cref_fwd_serial.argtypes = [D] + [P] * 17 + [ctypes.c_int]
+    lib.cref_fwd_chunked.argtypes = [D] + [P] * 17 + [ctypes.c_int]
+    lib.cref_baseline_fwd.argtypes = [D] + [P] * 10 + [ctypes.c_int]
+    lib.cref_bwd.argtypes = [D] + [P] * 26 + [ctypes.c_int]
+    for f in (lib.cref_fwd_serial, lib.cref_fwd_chunked, lib.cref_baseline_fwd, lib.cref_bwd):
+        f.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _f64(x):
+    if x is None:
+        return None
+    return np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+
+
+def _ptr(x):
+    if x is None:
+        return ctypes.POINTER(ctypes.c_double)()
+    return x.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def dims_of(inp, L):
+    B, T, H, Dk = inp["q"].shape
+    Dv = inp["v"].shape[-1]
+    R = inp["Ub"].shape[0]
+    return _Dims(B, T, H, Dk, Dv, R, L)
+
+
+def default_threads():
+    return max(1, os.cpu_count() or 1)
+
+
+def _check(st, name):
+    if st != 0:
+        raise ValueError(f"oracle {name} returned {st}")
+
+
+def _fwd(fn_name, inp, L, want_chunks, want_gates, nthreads):
+    lib = _load()
+    d = dims_of(inp, L)
+    a = {k: _f64(inp.get(k)) for k in ("q", "k", "v", "beta", "g", "bx", "wx", "Ub", "Uw", "Vb", "Vw", "S0")}
+    B, T, H, Dk, Dv = d.B, d.T, d.H, d.Dk, d.Dv
+    o = np.zeros((B, T, H, Dv))
+    S_T = np.zeros((B, H, Dv, Dk))
+    S_chunks = np.zeros((B, H, T // L, Dv, Dk)) if want_chunks else None
+    gb = np.zeros((B, T, H, Dk)) if want_gates else None
+    gw = np.zeros((B, T, H, Dv)) if want_gates else None
+    fn = getattr(lib, fn_name)
+    st = fn(ctypes.byref(d), *[_ptr(a[k]) for k in ("q", "k", "v", "beta", "g", "bx", "wx",
+                                                       "Ub", "Uw", "Vb", "Vw", "S0")],
+            _ptr(o), _ptr(S_T), _ptr(S_chunks), _ptr(gb), _ptr(gw),
+            nthreads if nthreads else default_threads())
+    _check(st, fn_name)
+    out = {"o": o, "S_T": S_T}
+    if want_chunks:
+        out["S_chunks"] = S_chunks
+    if want_gates:
+        out["gate_b"] = gb
+        out["gate_w"] = gw
+    return out
+
+
+def fwd_serial(inp, L, want_chunks=False, want_gates=False, nthreads=None):
+    """Token-serial definition of the layer (Eq. carve_state, staleness rule of Alg. carve_fwd)."""
+    return _fwd("cref_fwd_serial", inp, L, want_chunks, want_gates, nthreads)
+
+
+def fwd_chunked(inp, L, want_chunks=False, want_gates=False, nthreads=None):
+    """Chunked WY form of the same layer (Sec. WY-form intra-chunk solve)."""
+    return _fwd("cref_fwd_chunked", inp, L, want_chunks, want_gates, nthreads)
+
+
+def baseline_fwd(inp, L=None, nthreads=None):
+    """Memory-blind key-axis gated delta recurrence (gates from bx, wx only)."""
+    lib = _load()
+    d = dims_of(inp, L if L else inp["q"].shape[1])
+    a = {k: _f64(inp.get(k)) for k in ("q", "k", "v", "beta", "g", "bx", "wx", "S0")}
+    o = np.zeros((d.B, d.T, d.H, d.Dv))
+    S_T = np.zeros((d.B, d.H, d.Dv, d.Dk))
+    st = lib.cref_baseline_fwd(ctypes.byref(d), *[_ptr(a[k]) for k in ("q", "k", "v", "beta", "g",
+                                                                     "bx", "wx", "S0")],
+                               _ptr(o), _ptr(S_T), nthreads if nthreads else default_threads())
+    _check(st, "cref_baseline_fwd")
+    return {"o": o, "S_T": S_T}
+
+
+def bwd(inp, L, dO, dS_T=None, nthreads=None):
+    """Exact reverse mode of ``fwd_serial`` for the loss <dO, o> + <dS_T, S_T>."""
+    lib = _load()
+    d = dims_of(inp, L)
+    a = {k: _f64(inp.get(k)) for k in ("q", "k", "v", "beta", "g", "bx", "wx", "Ub", "Uw", "Vb", "Vw", "S0")}
+    dO = _f64(dO)
+    dS_T = _f64(dS_T)
+    B, T, H, Dk, Dv, R = d.B, d.T, d.H, d.Dk, d.Dv, d.R
+    out = {
+        "dq": np.zeros((B, T, H, Dk)), "dk": np.zeros((B, T, H, Dk)), "dv": np.zeros((B, T, H, Dv)),
+        "dbeta": np.zeros((B, T, H)), "dg": np.zeros((B, T, H, Dk)), "dbx": np.zeros((B, T, H, Dk)),
+        "dwx": np.zeros((B, T, H, Dv)), "dUb": np.zeros((R, Dv)), "dUw": np.zeros((R, Dv)),
+        "dVb": np.zeros((Dk, R)), "dVw": np.zeros((Dv, R)), "dS0": np.zeros((B, H, Dv, Dk)),
+    }
+    st = lib.cref_bwd(ctypes.byref(d), *[_ptr(a[k]) for k in ("q", "k", "v", "beta", "g", "bx", "wx",
+                                                            "Ub", "Uw", "Vb", "Vw", "S0")],
+                      _ptr(dO), _ptr(dS_T),
+                      *[_ptr(out[k]) for k in ("dq", "dk", "dv", "dbeta", "dg", "dbx", "dwx",
+                                               "dUb", "dUw", "dVb", "dVw", "dS0")],
+                      nthreads if nthreads else default_threads())
+    _check(st, "cref_bwd")
+    return out

@@ -1,0 +1,382 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+None of these tests compares the oracle with itself through a retyped copy of
+its recurrence: each checks a closed form, an invariant, an exact special
+case, the paper's own worked numbers (tests/golden/), or finite differences.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import oracle as orc
+from paper_2606_27229_amd.inputs import WORKLOADS, Workload, make_inputs
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _f64(inp):
+    return {k: (None if v is None else np.asarray(v, dtype=np.float64)) for k, v in inp.items()}
+
+
+def _rel(a, b):
+    return float(np.max(np.abs(a - b)) / max(np.max(np.abs(b)), 1e-300))
+
+
+def _small(**kw):
+    base = dict(name="pin", B=2, H=2, T=128, Dk=16, Dv=12, L=16, R=3, dtype="f32", mu=2.0,
+                s0=0.3, u_std=0.3)
+    base.update(kw)
+    return Workload(**base)
+
+
+# --------------------------------------------------------------------------
+# chunked WY form == token-serial definition (Sec. WY-form intra-chunk solve:
+# the WY form is an exact reformulation; Table exactness "chunk mode vs
+# sequential")
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("L", [1, 8, 16, 32, 64, 128])
+@pytest.mark.parametrize("erase_heavy", [False, True])
+def test_chunked_equals_serial(L, erase_heavy):
+    w = _small(T=256, L=L)
+    inp = make_inputs(w, seed=11 + L, bx_mean=0.0 if erase_heavy else None)
+    a = orc.fwd_serial(inp, L, want_chunks=True)
+    b = orc.fwd_chunked(inp, L, want_chunks=True)
+    for key in ("o", "S_T", "S_chunks"):
+        assert np.all(np.isfinite(b[key]))
+        assert _rel(b[key], a[key]) < 1e-12, key
+
+
+def test_chunked_equals_serial_rectangular_and_paper_shapes():
+    for w in (WORKLOADS["tiny_fp32"].with_(u_std=0.3), _small(Dk=32, Dv=8, R=5, L=32, T=96)):
+        inp = make_inputs(w, seed=5)
+        a = orc.fwd_serial(inp, w.L)
+        b = orc.fwd_chunked(inp, w.L)
+        assert _rel(b["o"], a["o"]) < 1e-12
+        assert _rel(b["S_T"], a["S_T"]) < 1e-12
+
+
+# --------------------------------------------------------------------------
+# zero-initialised content projections => bit-identical to the memory-blind
+# baseline (Sec. content-aware gates, "bit-identical ... at step 0";
+# Table exactness "CARVE vs GDN-2 baseline at init")
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("which", ["U", "V"])
+def test_zero_content_is_bit_identical_to_memory_blind(which):
+    w = WORKLOADS["tiny_fp32"].with_(s0=0.2)
+    inp = make_inputs(w, seed=0)
+    if which == "U":
+        inp["Ub"] = np.zeros_like(inp["Ub"])
+        inp["Uw"] = np.zeros_like(inp["Uw"])
+    else:
+        inp["Vb"] = np.zeros_like(inp["Vb"])
+        inp["Vw"] = np.zeros_like(inp["Vw"])
+    a = orc.fwd_serial(inp, w.L)
+    base = orc.baseline_fwd(inp)
+    assert np.array_equal(a["o"], base["o"])
+    assert np.array_equal(a["S_T"], base["S_T"])
+
+
+def test_zero_content_makes_chunk_length_irrelevant():
+    """Without a content term nothing reads the chunk-boundary state, so the
+    result cannot depend on L (bitwise)."""
+    w = _small(T=128)
+    inp = make_inputs(w, seed=4, zero_content=True)
+    ref = orc.fwd_serial(inp, 1)
+    for L in (8, 32, 128):
+        out = orc.fwd_serial(inp, L)
+        assert np.array_equal(out["o"], ref["o"])
+        assert np.array_equal(out["S_T"], ref["S_T"])
+
+
+def test_content_term_changes_result():
+    """Negative control: with non-zero content projections the chunk length
+    matters (staleness), so the pins above are not vacuous."""
+    w = _small(T=128)
+    inp = make_inputs(w, seed=4)
+    a = orc.fwd_serial(inp, 8)["o"]
+    b = orc.fwd_serial(inp, 64)["o"]
+    assert _rel(a, b) > 1e-3
+
+
+# --------------------------------------------------------------------------
+# split call == full call, bitwise (Table exactness "chunk-by-chunk vs full
+# call"); requires chunk 0 to fold S0
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("fn", [orc.fwd_serial, orc.fwd_chunked])
+def test_split_call_is_bitwise(fn):
+    w = _small(T=128, L=16, s0=0.5)
+    inp = make_inputs(w, seed=9)
+    full = fn(inp, 16)
+    T1 = 48
+    first = {k: (v[:, :T1] if (v is not None and v.ndim >= 3 and v.shape[1] == 128) else v)
+             for k, v in inp.items()}
+    second = {k: (v[:, T1:] if (v is not None and v.ndim >= 3 and v.shape[1] == 128) else v)
+              for k, v in inp.items()}
+    r1 = fn(first, 16)
+    second["S0"] = r1["S_T"]
+    r2 = fn(second, 16)
+    assert np.array_equal(np.concatenate([r1["o"], r2["o"]], axis=1), full["o"])
+    assert np.array_equal(r2["S_T"], full["S_T"])
+
+
+# --------------------------------------------------------------------------
+# delta-rule capacity (Thm. memory capacity): with no decay, no erase, full
+# write, beta = 1 and orthonormal keys, d_k sequential writes from S0 = 0
+# store every association exactly: S = sum_i v_i k_i^T and S k_i = v_i.
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("fn", [orc.fwd_serial, orc.fwd_chunked])
+def test_delta_rule_capacity_closed_form(fn):
+    d, dv, L = 8, 5, 4
+    T = d
+    rng = np.random.default_rng(1)
+    inp = {
+        "q": np.eye(d)[None, :, None, :].copy(),            # query = key_t
+        "k": np.eye(d)[None, :, None, :].copy(),            # keys = standard basis
+        "v": rng.standard_normal((1, T, 1, dv)),
+        "beta": np.ones((1, T, 1)),
+        "g": np.zeros((1, T, 1, d)),
+        "bx": np.full((1, T, 1, d), -1e4),                  # erase gate = 0
+        "wx": np.full((1, T, 1, dv), 1e4),                  # write gate = 1
+        "Ub": np.zeros((2, dv)), "Uw": np.zeros((2, dv)),
+        "Vb": np.zeros((d, 2)), "Vw": np.zeros((dv, 2)), "S0": None,
+    }
+    out = fn(inp, L)
+    V = inp["v"][0, :, 0, :]
+    assert np.array_equal(out["S_T"][0, 0], V.T)                # S = sum v_i e_i^T
+    assert np.array_equal(out["o"][0, :, 0, :], V)              # read-out right after each write
+    Q = rng.standard_normal((d,))
+    assert np.allclose(out["S_T"][0, 0] @ Q, V.T @ Q, rtol=0, atol=1e-14)
+
+
+# --------------------------------------------------------------------------
+# single write into empty memory (App. proof of scalar write sufficiency):
+# S = beta (w * v) k^T and the read-out with q = k is beta w v ||k||^2.
+# --------------------------------------------------------------------------
+def test_single_write_worked_example():
+    ex = json.load(open(os.path.join(GOLDEN, "scalar_write_example.json")))
+    kw = np.array(ex["k_w"]); vw = np.array(ex["v_w"]); wxv = np.array(ex["wx"]); beta = ex["beta"]
+    d, dv = kw.size, vw.size
+    inp = {
+        "q": kw[None, None, None, :], "k": kw[None, None, None, :], "v": vw[None, None, None, :],
+        "beta": np.array([[[beta]]]), "g": np.zeros((1, 1, 1, d)), "bx": np.zeros((1, 1, 1, d)),
+        "wx": wxv[None, None, None, :],
+        "Ub": np.ones((2, dv)), "Uw": np.ones((2, dv)),       # empty memory: the fold is 0
+        "Vb": np.ones((d, 2)), "Vw": np.ones((dv, 2)), "S0": None,
+    }
+    w = 1.0 / (1.0 + np.exp(-wxv))
+    for fn in (orc.fwd_serial, orc.fwd_chunked):
+        out = fn(inp, 1)
+        np.testing.assert_allclose(out["S_T"][0, 0], beta * np.outer(w * vw, kw), rtol=1e-15, atol=0)
+        np.testing.assert_allclose(out["o"][0, 0, 0], beta * w * vw * float(kw @ kw), rtol=1e-15)
+
+
+# --------------------------------------------------------------------------
+# folded content read-out, staleness rule and erase/write placement, pinned by
+# hand-built cases whose answer is a scalar closed form.
+# --------------------------------------------------------------------------
+def _sig(z):
+    return 1.0 / (1.0 + math.exp(-z))
+
+
+@pytest.mark.parametrize("fn", [orc.fwd_serial, orc.fwd_chunked])
+def test_content_erase_gate_closed_form(fn):
+    """No writes (k = 0); S0 = s e1 e1^T; every query = e1.  Then only S[0,0]
+    = sigma evolves.  The erase content signal of chunk c is
+    tanh(Ub[:,0] * sigma_hat_c) with sigma_hat_c frozen at the chunk start
+    (Eq. content_readout, fold of the chunk-boundary state), so within a chunk
+    the retention a_c = e^g * sigmoid(-(bx + Vb[0,:] . tanh(Ub[:,0] sigma_hat_c)))
+    is constant and sigma_hat_{c+1} = sigma_hat_c * a_c^L."""
+    d, dv, R, L, nch = 3, 2, 2, 4, 3
+    T = L * nch
+    s0, g0, bx0 = 2.0, -0.05, -1.0
+    Ub = np.array([[0.7, 5.0], [-0.4, 3.0]])        # column 0 is what the read-out sees
+    Uw = np.array([[9.0, 9.0], [9.0, 9.0]])         # must not influence the erase gate
+    Vb = np.array([[1.5, -2.0], [7.0, 7.0], [7.0, 7.0]])
+    Vw = np.zeros((dv, R))
+    e1 = np.zeros(d); e1[0] = 1.0
+    inp = {
+        "q": np.tile(e1, (1, T, 1, 1)), "k": np.zeros((1, T, 1, d)), "v": np.ones((1, T, 1, dv)),
+        "beta": np.ones((1, T, 1)), "g": np.full((1, T, 1, d), g0), "bx": np.full((1, T, 1, d), bx0),
+        "wx": np.zeros((1, T, 1, dv)), "Ub": Ub, "Uw": Uw, "Vb": Vb, "Vw": Vw,
+        "S0": np.zeros((1, 1, dv, d)),
+    }
+    inp["S0"][0, 0, 0, 0] = s0
+    out = fn(inp, L, want_gates=True)
+    sig_hat = s0
+    for c in range(nch):
+        zb = bx0 + sum(Vb[0, r] * math.tanh(Ub[r, 0] * sig_hat) for r in range(R))
+        a = math.exp(g0) * _sig(-zb)
+        for i in range(L):
+            t = c * L + i
+            assert out["gate_b"][0, t, 0, 0] == pytest.approx(_sig(zb), rel=1e-14)
+            assert out["o"][0, t, 0, 0] == pytest.approx(sig_hat * a ** (i + 1), rel=1e-13)
+        sig_hat = sig_hat * a ** L
+    assert out["S_T"][0, 0, 0, 0] == pytest.approx(sig_hat, rel=1e-13)
+    assert np.count_nonzero(out["S_T"]) == 1
+
+
+@pytest.mark.parametrize("fn", [orc.fwd_serial, orc.fwd_chunked])
+def test_content_write_gate_and_undecayed_prediction(fn):
+    """One token, S0 = s e1 e1^T, k = q = e1.  The write gate reads
+    Uw S0 q = s Uw[:,0] through Vw; the prediction uses the undecayed S0
+    (boxed Eq. carve_state) and w scales v only (Alg. WYChunkDelta step 3):
+       S1[:,0] = s a e1 + beta (w * v - s e1),   o = S1[:,0]."""
+    d, dv, R = 3, 3, 2
+    s, beta, g0, bx0 = 1.5, 0.8, -0.2, 0.3
+    Ub = np.array([[0.5, 1.0, 1.0], [-0.3, 1.0, 1.0]])
+    Uw = np.array([[0.9, 2.0, 2.0], [0.2, 2.0, 2.0]])
+    Vb = np.array([[0.4, -0.6], [1.0, 1.0], [1.0, 1.0]])
+    Vw = np.array([[1.0, -0.5], [0.3, 0.7], [-1.2, 0.1]])
+    v = np.array([0.7, -1.1, 2.0]); wx = np.array([0.2, -0.4, 0.6])
+    e1 = np.array([1.0, 0.0, 0.0])
+    inp = {
+        "q": e1[None, None, None], "k": e1[None, None, None], "v": v[None, None, None],
+        "beta": np.array([[[beta]]]), "g": np.full((1, 1, 1, d), g0), "bx": np.full((1, 1, 1, d), bx0),
+        "wx": wx[None, None, None], "Ub": Ub, "Uw": Uw, "Vb": Vb, "Vw": Vw,
+        "S0": np.zeros((1, 1, dv, d)),
+    }
+    inp["S0"][0, 0, 0, 0] = s
+    out = fn(inp, 1, want_gates=True)
+    tw = np.tanh(s * Uw[:, 0])
+    w = 1.0 / (1.0 + np.exp(-(wx + Vw @ tw)))
+    zb0 = bx0 + Vb[0] @ np.tanh(s * Ub[:, 0])
+    a = math.exp(g0) * _sig(-zb0)
+    col = beta * (w * v)
+    col[0] += s * a - beta * s
+    np.testing.assert_allclose(out["gate_w"][0, 0, 0], w, rtol=1e-14)
+    np.testing.assert_allclose(out["o"][0, 0, 0], col, rtol=1e-13)
+    np.testing.assert_allclose(out["S_T"][0, 0][:, 0], col, rtol=1e-13)
+
+
+# --------------------------------------------------------------------------
+# Thm. Lyapunov stability, the paper's worked ratio (tests/golden)
+# --------------------------------------------------------------------------
+def test_lyapunov_contraction_example():
+    ex = json.load(open(os.path.join(GOLDEN, "lyapunov_contraction.json")))
+    b, decay, rho = ex["erase_gate"], ex["decay_factor"], ex["rho"]
+    d, dv, T = 4, 3, 10
+    rng = np.random.default_rng(2)
+    S0 = rng.standard_normal((1, 1, dv, d))
+    inp = {
+        "q": rng.standard_normal((1, T, 1, d)), "k": np.zeros((1, T, 1, d)),
+        "v": rng.standard_normal((1, T, 1, dv)), "beta": np.ones((1, T, 1)),
+        "g": np.full((1, T, 1, d), math.log(decay)),
+        "bx": np.full((1, T, 1, d), math.log(b / (1 - b))),
+        "wx": np.zeros((1, T, 1, dv)), "Ub": np.zeros((2, dv)), "Uw": np.zeros((2, dv)),
+        "Vb": np.zeros((d, 2)), "Vw": np.zeros((dv, 2)), "S0": S0,
+    }
+    for fn in (orc.fwd_serial, orc.fwd_chunked):
+        out = fn(inp, 5)
+        ratio = (np.linalg.norm(out["S_T"]) / np.linalg.norm(S0)) ** (1.0 / T)
+        assert ratio == pytest.approx(rho, rel=1e-12)
+
+
+def test_lyapunov_step_bound():
+    """Per step ||S_t|| <= max(alpha) ||S_{t-1}|| + ||beta e k^T|| (triangle step
+    of the Lyapunov proof), checked on one-token calls chained through S0."""
+    w = _small(B=1, H=1, T=1, L=1, s0=0.5)
+    base = make_inputs(w.with_(T=24), seed=8)
+    S = base["S0"]
+    for t in range(24):
+        x = {k: (v[:, t:t + 1] if (v is not None and v.ndim >= 3 and v.shape[1] == 24) else v)
+             for k, v in base.items()}
+        x["S0"] = S
+        out = orc.fwd_serial(x, 1, want_gates=True)
+        Sn = out["S_T"]
+        alpha = np.exp(x["g"][0, 0, 0]) * (1 - out["gate_b"][0, 0, 0])
+        e = out["gate_w"][0, 0, 0] * x["v"][0, 0, 0] - S[0, 0] @ x["k"][0, 0, 0]
+        bound = alpha.max() * np.linalg.norm(S) + abs(x["beta"][0, 0, 0]) * np.linalg.norm(e) * np.linalg.norm(x["k"][0, 0, 0])
+        assert np.linalg.norm(Sn) <= bound * (1 + 1e-12)
+        S = Sn
+
+
+# --------------------------------------------------------------------------
+# affine state carry without content (key-axis part of Thm. gradient flow):
+# with Ub = Uw = 0 the map S0 -> (o, S_T) is affine, so superposition holds.
+# --------------------------------------------------------------------------
+def test_affine_superposition_without_content():
+    w = _small(T=32, L=8, s0=0.0, mu=4.0)
+    inp = make_inputs(w, seed=6, zero_content=True)
+    rng = np.random.default_rng(3)
+    Sa = rng.standard_normal((w.B, w.H, w.Dv, w.Dk))
+    Sb = rng.standard_normal((w.B, w.H, w.Dv, w.Dk))
+
+    def run(S0):
+        x = dict(inp); x["S0"] = S0
+        return orc.fwd_chunked(x, 8)
+
+    f0, fa, fb, fab = run(None), run(Sa), run(Sb), run(Sa + Sb)
+    for key in ("o", "S_T"):
+        lhs = fab[key] - fb[key]
+        rhs = fa[key] - f0[key]
+        scale = max(np.max(np.abs(fab[key])), np.max(np.abs(fa[key])))
+        assert np.max(np.abs(rhs)) > 1e-3 * scale          # S0 still matters at the end
+        assert np.max(np.abs(lhs - rhs)) < 1e-13 * scale
+
+
+# --------------------------------------------------------------------------
+# backward == derivative of the forward (central differences, double)
+# --------------------------------------------------------------------------
+GRADS = [("q", "dq"), ("k", "dk"), ("v", "dv"), ("beta", "dbeta"), ("g", "dg"), ("bx", "dbx"),
+         ("wx", "dwx"), ("Ub", "dUb"), ("Uw", "dUw"), ("Vb", "dVb"), ("Vw", "dVw"), ("S0", "dS0")]
+
+
+def _loss(x, L):
+    o = orc.fwd_serial(x, L)
+    return float(np.sum(o["o"] * x["dO"]) + np.sum(o["S_T"] * x["dS_T"]))
+
+
+@pytest.mark.parametrize("L,T,Dk,Dv,R", [(8, 32, 8, 6, 3), (16, 64, 16, 16, 4), (4, 16, 5, 7, 2)])
+def test_backward_directional_finite_differences(L, T, Dk, Dv, R):
+    w = Workload("fd", B=1, H=2, T=T, Dk=Dk, Dv=Dv, L=L, R=R, dtype="f32", mu=2.0, s0=0.3, u_std=0.4)
+    inp = _f64(make_inputs(w, seed=L + Dk, dS_T=True))
+    gr = orc.bwd(inp, L, inp["dO"], inp["dS_T"])
+    rng = np.random.default_rng(L)
+    h = 1e-6
+    for name, gname in GRADS:
+        dirn = rng.standard_normal(inp[name].shape)
+        xp = dict(inp); xp[name] = inp[name] + h * dirn
+        xm = dict(inp); xm[name] = inp[name] - h * dirn
+        fd = (_loss(xp, L) - _loss(xm, L)) / (2 * h)
+        an = float(np.sum(gr[gname] * dirn))
+        assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-3), (name, fd, an)
+
+
+def test_backward_coordinate_finite_differences():
+    w = Workload("fd", B=1, H=1, T=16, Dk=6, Dv=5, L=4, R=2, dtype="f32", mu=2.0, s0=0.3, u_std=0.5)
+    inp = _f64(make_inputs(w, seed=77, dS_T=True))
+    gr = orc.bwd(inp, 4, inp["dO"], inp["dS_T"])
+    rng = np.random.default_rng(5)
+    h = 1e-6
+    checked = 0
+    for name, gname in GRADS:
+        flat = inp[name].reshape(-1)
+        for idx in rng.choice(flat.size, size=min(4, flat.size), replace=False):
+            xp = dict(inp); xp[name] = inp[name].copy(); xp[name].reshape(-1)[idx] += h
+            xm = dict(inp); xm[name] = inp[name].copy(); xm[name].reshape(-1)[idx] -= h
+            fd = (_loss(xp, 4) - _loss(xm, 4)) / (2 * h)
+            an = gr[gname].reshape(-1)[idx]
+            assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-2), (name, idx, fd, an)
+            checked += 1
+    assert checked >= 32
+
+
+def test_backward_without_dST_and_S0():
+    """NULL dS_T and S0 mean zeros."""
+    w = Workload("fd", B=1, H=1, T=16, Dk=4, Dv=4, L=4, R=2, dtype="f32", mu=2.0, u_std=0.3)
+    inp = _f64(make_inputs(w, seed=1))
+    a = orc.bwd(inp, 4, inp["dO"], None)
+    x = dict(inp); x["S0"] = np.zeros((1, 1, 4, 4))
+    b = orc.bwd(x, 4, inp["dO"], np.zeros((1, 1, 4, 4)))
+    for key in a:
+        assert np.array_equal(a[key], b[key]), key
+
+
+def test_oracle_rejects_bad_shapes():
+    w = _small(T=24, L=16)
+    inp = make_inputs(w, seed=0)
+    with pytest.raises(ValueError):
+        orc.fwd_serial(inp, 16)
