@@ -1,0 +1,126 @@
+/*
+ * carve.h -- C ABI of libcarve: the chunked CARVE layer (arXiv 2606.27229)
+ * forward and backward on AMD Instinct MI355X (gfx950).
+ *
+ * What the library computes (one layer, every batch element b and head h,
+ * recurrent state S in R^{Dv x Dk}):
+ *
+ *   Sec. 4, Eq. carve_state (boxed): per token t
+ *       S_t = S_{t-1} diag(exp g_t) diag(1 - b_t) + beta_t (w_t * v_t - S_{t-1} k_t) k_t^T
+ *       o_t = S_t q_t
+ *     with key-axis decay g_t (log domain, <= 0) and erase gate b_t, a
+ *     per-token write strength beta_t, and a value-axis write gate w_t that
+ *     scales v_t only (Alg. WYChunkDelta step 3).
+ *   Sec. 4.2, Eq. content_readout / erase_gate: the gates of every token of
+ *     chunk c (tokens [cL, (c+1)L)) read the state carried out of chunk c-1
+ *     (S0 for chunk 0), folded once per chunk:
+ *       F = [Ub; Uw] S_{c-1}           (2R x Dk)
+ *       tau_b = tanh(F_b q_t), tau_w = tanh(F_w q_t)
+ *       b_t = sigmoid(bx_t + Vb tau_b),  w_t = sigmoid(wx_t + Vw tau_w)
+ *   Sec. 6.2, Alg. WYChunkDelta: evaluated chunk-parallel in WY form (one
+ *     shared unit-lower-triangular solve per chunk, Thm. chunkability).
+ *   App. Alg. backward / megakernel_bwd: the exact gradient of
+ *       loss = <dO, o> + <dS_T, S_T>
+ *     with respect to every input, including the chunk-boundary "glue"
+ *     through the folded read-out and the parameter gradients reduced over
+ *     batch, heads and chunks.
+ *
+ * Conventions
+ *   - All tensors are dense, row-major and live in DEVICE memory owned by
+ *     the caller.  Token tensors are [B, T, H, D] (q, k, bx, g: D = Dk;
+ *     v, wx, o: D = Dv); beta is [B, T, H]; states are [B, H, Dv, Dk];
+ *     S_chunks is [B, H, T/L, Dv, Dk] and holds the state at the start of
+ *     every chunk; Ub, Uw are [R, Dv]; Vb is [Dk, R]; Vw is [Dv, R].
+ *     Ub, Uw, Vb, Vw are shared by all heads.
+ *   - dtype (CARVE_F32 or CARVE_BF16) is the element type of q, k, v, beta,
+ *     bx, wx, o, dO and of dq, dk, dv, dbeta, dbx, dwx.  g, the parameters,
+ *     the states and dg, dUb, dUw, dVb, dVw, dS0, dS_T are always f32.  All
+ *     arithmetic is f32 (bf16 operands on the matrix cores in bf16 mode).
+ *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the
+ *     default stream) and never synchronises.  The return value reports
+ *     argument validation and launch errors only.
+ *   - Outputs are overwritten, never accumulated (parameter gradients too).
+ *   - The library allocates no device memory and keeps no state between
+ *     calls except the cached kernel attributes; concurrent calls on
+ *     different streams must use different workspaces.
+ *   - Supported shapes: Dk == Dv in {32, 64, 128}; 1 <= R <= 64;
+ *     L in {16, 32, 64, 128} (f32 with Dk = 128: L in {16, 32, 64, 128} is
+ *     run in 16-token WY tiles); T a positive multiple of L; B, H >= 1.
+ *     Other shapes return CARVE_ERR_UNSUPPORTED (or CARVE_ERR_SHAPE when
+ *     T % L != 0 or a size is non-positive).
+ *   - Every pointer must be 16-byte aligned (CARVE_ERR_ALIGN).
+ *   - Inputs are assumed finite with g <= 0; NaN/Inf propagate.  Numerical
+ *     range: within any 16 consecutive tokens of a chunk the summed log
+ *     retention g - softplus(z_b) of a key channel must stay above about
+ *     -80 (the WY tiles factor e^{-(16-token log retention)} in f32).
+ */
+#ifndef CARVE_H
+#define CARVE_H
+
+#include <stddef.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { CARVE_F32 = 0, CARVE_BF16 = 1 } carve_dtype_t;
+
+typedef struct {
+  int B, T, H, Dk, Dv, R, L;
+  carve_dtype_t dtype;
+} carve_dims_t;
+
+enum {
+  CARVE_OK = 0,
+  CARVE_ERR_NULL = -1,        /* a required pointer is NULL */
+  CARVE_ERR_SHAPE = -2,       /* non-positive size or T % L != 0 */
+  CARVE_ERR_UNSUPPORTED = -3, /* valid but not built: see "Supported shapes" */
+  CARVE_ERR_ALIGN = -4,       /* a pointer is not 16-byte aligned */
+  CARVE_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than carve_workspace_size */
+  CARVE_ERR_HIP = -6          /* a HIP runtime call failed */
+};
+
+/* Bytes of device workspace the forward (for_backward = 0) or the backward
+ * (for_backward = 1) needs for these dims; 0 means none.  Returns 0 for
+ * dims that fail validation.  The workspace holds per-(batch, head) partial
+ * parameter gradients and the WY-tile start states of one chunk. */
+size_t carve_workspace_size(const carve_dims_t* d, int for_backward);
+
+/* Forward (Alg. carve_fwd with the WY solve of Alg. WYChunkDelta).
+ * In:  q, k [B,T,H,Dk]; v [B,T,H,Dv]; beta [B,T,H]; g [B,T,H,Dk] (f32);
+ *      bx [B,T,H,Dk]; wx [B,T,H,Dv]; Ub, Uw, Vb, Vw (f32);
+ *      S0 [B,H,Dv,Dk] f32 or NULL (= zeros).
+ * Out: o [B,T,H,Dv]; S_T [B,H,Dv,Dk] or NULL; S_chunks [B,H,T/L,Dv,Dk] or
+ *      NULL (needed by carve_chunk_bwd).
+ * workspace may be NULL when carve_workspace_size(d, 0) == 0. */
+int carve_chunk_fwd(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                    const void* beta, const float* g, const void* bx, const void* wx,
+                    const float* Ub, const float* Uw, const float* Vb, const float* Vw,
+                    const float* S0, void* o, float* S_T, float* S_chunks, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream);
+
+/* Backward of carve_chunk_fwd for loss <dO, o> + <dS_T, S_T>.
+ * In:  the forward inputs; S_chunks as written by carve_chunk_fwd on the
+ *      same inputs; dO [B,T,H,Dv]; dS_T [B,H,Dv,Dk] f32 or NULL (= zeros).
+ * Out: dq, dk [B,T,H,Dk]; dv [B,T,H,Dv]; dbeta [B,T,H]; dg [B,T,H,Dk] f32;
+ *      dbx [B,T,H,Dk]; dwx [B,T,H,Dv]; dUb, dUw [R,Dv]; dVb [Dk,R];
+ *      dVw [Dv,R]; dS0 [B,H,Dv,Dk] or NULL.  (S0 itself is not needed: the
+ *      chunk-start states are read from S_chunks.)
+ * The parameter gradients are reduced over batch, heads and chunks in a
+ * fixed order, so reruns are bitwise identical. */
+int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                    const void* beta, const float* g, const void* bx, const void* wx,
+                    const float* Ub, const float* Uw, const float* Vb, const float* Vw,
+                    const float* S_chunks, const void* dO, const float* dS_T, void* dq, void* dk,
+                    void* dv, void* dbeta, float* dg, void* dbx, void* dwx, float* dUb,
+                    float* dUw, float* dVb, float* dVw, float* dS0, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream);
+
+/* Static description of a status code. */
+const char* carve_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CARVE_H */

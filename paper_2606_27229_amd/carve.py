@@ -1,0 +1,169 @@
+"""Thin Python binding of libcarve (C ABI in include/carve.h).
+
+Argument marshalling only: tensors are allocated with PyTorch on the GPU,
+their device pointers and the current HIP stream are handed to the C entry
+points, and every step of the layer runs in the HIP kernels.  There is no
+fallback: if libcarve.so is missing or a tensor is not a contiguous GPU
+tensor of the right dtype, the call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcarve.so")
+
+CARVE_F32, CARVE_BF16 = 0, 1
+SYMBOLS = ("carve_chunk_fwd", "carve_chunk_bwd", "carve_workspace_size", "carve_status_string")
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int), ("T", ctypes.c_int), ("H", ctypes.c_int), ("Dk", ctypes.c_int),
+                ("Dv", ctypes.c_int), ("R", ctypes.c_int), ("L", ctypes.c_int), ("dtype", ctypes.c_int)]
+
+
+class CarveError(RuntimeError):
+    def __init__(self, fn, status, msg):
+        super().__init__(f"{fn} failed with status {status}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libcarve.so (no GPU needed).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None and path == LIB_PATH:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} not found: build it with paper_2606_27229_amd.build.build()")
+    lib = ctypes.CDLL(path)
+    vp, fp, sz = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t
+    D = ctypes.POINTER(Dims)
+    lib.carve_workspace_size.argtypes = [D, ctypes.c_int]
+    lib.carve_workspace_size.restype = sz
+    lib.carve_status_string.argtypes = [ctypes.c_int]
+    lib.carve_status_string.restype = ctypes.c_char_p
+    lib.carve_chunk_fwd.argtypes = [D] + [vp] * 7 + [fp] * 5 + [vp, fp, fp, vp, sz, vp]
+    lib.carve_chunk_fwd.restype = ctypes.c_int
+    lib.carve_chunk_bwd.argtypes = [D] + [vp] * 7 + [fp] * 5 + [vp, fp] + [vp] * 12 + [vp, sz, vp]
+    lib.carve_chunk_bwd.restype = ctypes.c_int
+    if path == LIB_PATH:
+        _lib = lib
+    return lib
+
+
+def status_string(st: int) -> str:
+    return load_library().carve_status_string(st).decode()
+
+
+def make_dims(B, T, H, Dk, Dv, R, L, dtype) -> Dims:
+    return Dims(B, T, H, Dk, Dv, R, L, CARVE_BF16 if dtype == torch.bfloat16 else CARVE_F32)
+
+
+def workspace_size(dims: Dims, backward: bool) -> int:
+    return int(load_library().carve_workspace_size(ctypes.byref(dims), 1 if backward else 0))
+
+
+def _ptr(t, name, dtype=None, shape=None):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _check(fn, st):
+    if st != 0:
+        raise CarveError(fn, st, status_string(st))
+
+
+def chunk_fwd(q, k, v, beta, g, bx, wx, Ub, Uw, Vb, Vw, S0=None, *, L=64, want_chunks=True,
+              want_state=True, out=None, stream=None):
+    """Forward of the chunked CARVE layer.
+
+    Shapes: q, k, bx, g [B,T,H,Dk]; v, wx [B,T,H,Dv]; beta [B,T,H]; Ub, Uw [R,Dv];
+    Vb [Dk,R]; Vw [Dv,R]; S0 [B,H,Dv,Dk] or None.  Returns (o, S_T, S_chunks).
+    ``out`` may hold preallocated {"o", "S_T", "S_chunks"} tensors.
+    """
+    lib = load_library()
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    R = Ub.shape[0]
+    dt = q.dtype
+    f32 = torch.float32
+    dims = make_dims(B, T, H, Dk, Dv, R, L, dt)
+    out = dict(out or {})
+    o = out.get("o")
+    if o is None:
+        o = torch.empty((B, T, H, Dv), dtype=dt, device=q.device)
+    S_T = out.get("S_T") if "S_T" in out else (torch.empty((B, H, Dv, Dk), dtype=f32, device=q.device) if want_state else None)
+    S_chunks = out.get("S_chunks") if "S_chunks" in out else (
+        torch.empty((B, H, T // L, Dv, Dk), dtype=f32, device=q.device) if want_chunks else None)
+    st = lib.carve_chunk_fwd(
+        ctypes.byref(dims), _ptr(q, "q", dt, (B, T, H, Dk)), _ptr(k, "k", dt, (B, T, H, Dk)),
+        _ptr(v, "v", dt, (B, T, H, Dv)), _ptr(beta, "beta", dt, (B, T, H)), _ptr(g, "g", f32, (B, T, H, Dk)),
+        _ptr(bx, "bx", dt, (B, T, H, Dk)), _ptr(wx, "wx", dt, (B, T, H, Dv)),
+        _ptr(Ub, "Ub", f32, (R, Dv)), _ptr(Uw, "Uw", f32, (R, Dv)), _ptr(Vb, "Vb", f32, (Dk, R)),
+        _ptr(Vw, "Vw", f32, (Dv, R)), _ptr(S0, "S0", f32, (B, H, Dv, Dk)),
+        _ptr(o, "o", dt, (B, T, H, Dv)), _ptr(S_T, "S_T", f32), _ptr(S_chunks, "S_chunks", f32),
+        None, 0, _stream(stream))
+    _check("carve_chunk_fwd", st)
+    return o, S_T, S_chunks
+
+
+def chunk_bwd(q, k, v, beta, g, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO, dS_T=None, *, L=64,
+              want_dS0=True, out=None, workspace=None, stream=None):
+    """Backward of the chunked CARVE layer for loss <dO, o> + <dS_T, S_T>.
+
+    Returns a dict with dq, dk, dv, dbeta, dg, dbx, dwx, dUb, dUw, dVb, dVw, dS0.
+    """
+    lib = load_library()
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    R = Ub.shape[0]
+    dt = q.dtype
+    f32 = torch.float32
+    dev = q.device
+    dims = make_dims(B, T, H, Dk, Dv, R, L, dt)
+    res = dict(out or {})
+    spec = {"dq": ((B, T, H, Dk), dt), "dk": ((B, T, H, Dk), dt), "dv": ((B, T, H, Dv), dt),
+            "dbeta": ((B, T, H), dt), "dg": ((B, T, H, Dk), f32), "dbx": ((B, T, H, Dk), dt),
+            "dwx": ((B, T, H, Dv), dt), "dUb": ((R, Dv), f32), "dUw": ((R, Dv), f32),
+            "dVb": ((Dk, R), f32), "dVw": ((Dv, R), f32)}
+    if want_dS0:
+        spec["dS0"] = ((B, H, Dv, Dk), f32)
+    for name, (shape, dtype) in spec.items():
+        if res.get(name) is None:
+            res[name] = torch.empty(shape, dtype=dtype, device=dev)
+    ws_bytes = workspace_size(dims, True)
+    if workspace is None and ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    ws_ptr = _ptr(workspace, "workspace") if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    st = lib.carve_chunk_bwd(
+        ctypes.byref(dims), _ptr(q, "q", dt, (B, T, H, Dk)), _ptr(k, "k", dt, (B, T, H, Dk)),
+        _ptr(v, "v", dt, (B, T, H, Dv)), _ptr(beta, "beta", dt, (B, T, H)), _ptr(g, "g", f32, (B, T, H, Dk)),
+        _ptr(bx, "bx", dt, (B, T, H, Dk)), _ptr(wx, "wx", dt, (B, T, H, Dv)),
+        _ptr(Ub, "Ub", f32, (R, Dv)), _ptr(Uw, "Uw", f32, (R, Dv)), _ptr(Vb, "Vb", f32, (Dk, R)),
+        _ptr(Vw, "Vw", f32, (Dv, R)), _ptr(S_chunks, "S_chunks", f32, (B, H, T // L, Dv, Dk)),
+        _ptr(dO, "dO", dt, (B, T, H, Dv)), _ptr(dS_T, "dS_T", f32, (B, H, Dv, Dk)),
+        *[_ptr(res[n], n) for n in ("dq", "dk", "dv", "dbeta", "dg", "dbx", "dwx", "dUb", "dUw", "dVb", "dVw")],
+        _ptr(res.get("dS0"), "dS0"), ws_ptr, ws_len, _stream(stream))
+    _check("carve_chunk_bwd", st)
+    return res

@@ -1,0 +1,176 @@
+// carve_abi.hip -- the C ABI of libcarve: argument validation, workspace
+// sizing, kernel selection and launch.  No allocation, no synchronisation.
+#include <stdint.h>
+
+#include "carve_kernels.h"
+
+using namespace carve;
+
+namespace {
+
+constexpr size_t kMaxLds = 160 * 1024;
+
+int round_rp(int R) { return (R + 31) / 32 * 32; }
+
+size_t esize(carve_dtype_t dt) { return dt == CARVE_BF16 ? 2 : 4; }
+
+int check_dims(const carve_dims_t* d) {
+  if (!d) return CARVE_ERR_NULL;
+  if (d->B <= 0 || d->T <= 0 || d->H <= 0 || d->Dk <= 0 || d->Dv <= 0 || d->R <= 0 || d->L <= 0)
+    return CARVE_ERR_SHAPE;
+  if (d->dtype != CARVE_F32 && d->dtype != CARVE_BF16) return CARVE_ERR_UNSUPPORTED;
+  if (d->T % d->L != 0) return CARVE_ERR_SHAPE;
+  if (d->Dk != d->Dv) return CARVE_ERR_UNSUPPORTED;
+  if (d->Dk != 32 && d->Dk != 64 && d->Dk != 128) return CARVE_ERR_UNSUPPORTED;
+  if (d->R > 64) return CARVE_ERR_UNSUPPORTED;
+  if (d->L != 16 && d->L != 32 && d->L != 64 && d->L != 128) return CARVE_ERR_UNSUPPORTED;
+  // the grid is B*H workgroups and offsets are computed in size_t
+  if ((long long)d->B * d->H > (1LL << 30)) return CARVE_ERR_UNSUPPORTED;
+  return CARVE_OK;
+}
+
+// largest WY tile (<= 64, dividing L) whose LDS layout fits
+int pick_lw(const carve_dims_t* d, bool bwd) {
+  const int RP = round_rp(d->R);
+  for (int lw = 64; lw >= 16; lw /= 2) {
+    if (lw > d->L || d->L % lw) continue;
+    const size_t need = bwd ? bwd_lds_bytes(d->dtype, d->Dk, lw, RP) : fwd_lds_bytes(d->dtype, d->Dk, lw, RP);
+    if (need <= kMaxLds) return lw;
+  }
+  return 0;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+struct Range {
+  const void* p;
+  size_t bytes;
+};
+
+bool overlap(const Range& a, const Range& b) {
+  if (!a.p || !b.p || a.bytes == 0 || b.bytes == 0) return false;
+  const uintptr_t a0 = (uintptr_t)a.p, a1 = a0 + a.bytes, b0 = (uintptr_t)b.p, b1 = b0 + b.bytes;
+  return a0 < b1 && b0 < a1;
+}
+
+bool any_overlap(const Range* outs, int nout, const Range* ins, int nin) {
+  for (int i = 0; i < nout; ++i) {
+    for (int j = 0; j < nin; ++j)
+      if (overlap(outs[i], ins[j])) return true;
+    for (int j = i + 1; j < nout; ++j)
+      if (overlap(outs[i], outs[j])) return true;
+  }
+  return false;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* carve_status_string(int status) {
+  switch (status) {
+    case CARVE_OK: return "ok";
+    case CARVE_ERR_NULL: return "a required pointer is NULL";
+    case CARVE_ERR_SHAPE: return "invalid shape (non-positive size or T not a multiple of L)";
+    case CARVE_ERR_UNSUPPORTED: return "unsupported configuration (dtype, head size, rank or chunk length)";
+    case CARVE_ERR_ALIGN: return "a pointer is not 16-byte aligned";
+    case CARVE_ERR_WORKSPACE: return "workspace missing or too small";
+    case CARVE_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+size_t carve_workspace_size(const carve_dims_t* d, int for_backward) {
+  if (check_dims(d) != CARVE_OK) return 0;
+  if (!for_backward) return 0;
+  const int lw = pick_lw(d, true);
+  if (!lw) return 0;
+  const size_t nbh = (size_t)d->B * d->H;
+  size_t bytes = nbh * part_floats(d->R, d->Dk) * 4;
+  const int msub = d->L / lw;
+  if (msub > 1) bytes += nbh * (size_t)msub * d->Dv * d->Dk * 4;
+  return (bytes + 255) & ~(size_t)255;
+}
+
+int carve_chunk_fwd(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                    const void* beta, const float* g, const void* bx, const void* wx,
+                    const float* Ub, const float* Uw, const float* Vb, const float* Vw,
+                    const float* S0, void* o, float* S_T, float* S_chunks, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  int st = check_dims(d);
+  if (st) return st;
+  if (!q || !k || !v || !beta || !g || !bx || !wx || !Ub || !Uw || !Vb || !Vw || !o) return CARVE_ERR_NULL;
+  const void* ptrs[] = {q, k, v, beta, g, bx, wx, Ub, Uw, Vb, Vw, S0, o, S_T, S_chunks};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return CARVE_ERR_ALIGN;
+  const size_t es = esize(d->dtype);
+  const size_t ntok = (size_t)d->B * d->T * d->H;
+  const size_t nst = (size_t)d->B * d->H * d->Dv * d->Dk;
+  const Range ins[] = {{q, ntok * d->Dk * es}, {k, ntok * d->Dk * es}, {v, ntok * d->Dv * es},
+                       {beta, ntok * es}, {g, ntok * d->Dk * 4}, {bx, ntok * d->Dk * es},
+                       {wx, ntok * d->Dv * es}, {Ub, (size_t)d->R * d->Dv * 4},
+                       {Uw, (size_t)d->R * d->Dv * 4}, {Vb, (size_t)d->Dk * d->R * 4},
+                       {Vw, (size_t)d->Dv * d->R * 4}, {S0, nst * 4}};
+  const Range outs[] = {{o, ntok * d->Dv * es}, {S_T, nst * 4}, {S_chunks, nst * (d->T / d->L) * 4}};
+  if (any_overlap(outs, 3, ins, 12)) return CARVE_ERR_UNSUPPORTED;
+  const int lw = pick_lw(d, false);
+  if (!lw) return CARVE_ERR_UNSUPPORTED;
+  FwdArgs a;
+  a.q = q; a.k = k; a.v = v; a.beta = beta; a.bx = bx; a.wx = wx;
+  a.g = g; a.Ub = Ub; a.Uw = Uw; a.Vb = Vb; a.Vw = Vw; a.S0 = S0;
+  a.o = o; a.S_T = S_T; a.S_chunks = S_chunks;
+  a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = round_rp(d->R); a.L = d->L;
+  return launch_fwd(a, d->dtype, d->Dk, lw, stream);
+}
+
+int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                    const void* beta, const float* g, const void* bx, const void* wx,
+                    const float* Ub, const float* Uw, const float* Vb, const float* Vw,
+                    const float* S_chunks, const void* dO, const float* dS_T, void* dq, void* dk,
+                    void* dv, void* dbeta, float* dg, void* dbx, void* dwx, float* dUb,
+                    float* dUw, float* dVb, float* dVw, float* dS0, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream) {
+  int st = check_dims(d);
+  if (st) return st;
+  if (!q || !k || !v || !beta || !g || !bx || !wx || !Ub || !Uw || !Vb || !Vw || !S_chunks || !dO ||
+      !dq || !dk || !dv || !dbeta || !dg || !dbx || !dwx || !dUb || !dUw || !dVb || !dVw)
+    return CARVE_ERR_NULL;
+  const void* ptrs[] = {q, k, v, beta, g, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO, dS_T, dq, dk, dv,
+                        dbeta, dg, dbx, dwx, dUb, dUw, dVb, dVw, dS0, workspace};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return CARVE_ERR_ALIGN;
+  const size_t need = carve_workspace_size(d, 1);
+  if (need && (!workspace || workspace_bytes < need)) return CARVE_ERR_WORKSPACE;
+  const size_t es = esize(d->dtype);
+  const size_t ntok = (size_t)d->B * d->T * d->H;
+  const size_t nst = (size_t)d->B * d->H * d->Dv * d->Dk;
+  const size_t RDv = (size_t)d->R * d->Dv * 4;
+  const Range ins[] = {{q, ntok * d->Dk * es}, {k, ntok * d->Dk * es}, {v, ntok * d->Dv * es},
+                       {beta, ntok * es}, {g, ntok * d->Dk * 4}, {bx, ntok * d->Dk * es},
+                       {wx, ntok * d->Dv * es}, {Ub, RDv}, {Uw, RDv}, {Vb, RDv}, {Vw, RDv},
+                       {S_chunks, nst * (d->T / d->L) * 4}, {dO, ntok * d->Dv * es},
+                       {dS_T, nst * 4}, {workspace, need}};
+  const Range outs[] = {{dq, ntok * d->Dk * es}, {dk, ntok * d->Dk * es}, {dv, ntok * d->Dv * es},
+                        {dbeta, ntok * es}, {dg, ntok * d->Dk * 4}, {dbx, ntok * d->Dk * es},
+                        {dwx, ntok * d->Dv * es}, {dUb, RDv}, {dUw, RDv}, {dVb, RDv},
+                        {dVw, RDv}, {dS0, nst * 4}};
+  if (any_overlap(outs, 12, ins, 15)) return CARVE_ERR_UNSUPPORTED;
+  const int lw = pick_lw(d, true);
+  if (!lw) return CARVE_ERR_UNSUPPORTED;
+  BwdArgs a;
+  a.q = q; a.k = k; a.v = v; a.beta = beta; a.bx = bx; a.wx = wx;
+  a.g = g; a.Ub = Ub; a.Uw = Uw; a.Vb = Vb; a.Vw = Vw; a.S_chunks = S_chunks;
+  a.dO = dO; a.dS_T = dS_T;
+  a.dq = dq; a.dk = dk; a.dv = dv; a.dbeta = dbeta; a.dbx = dbx; a.dwx = dwx; a.dg = dg; a.dS0 = dS0;
+  a.part = reinterpret_cast<float*>(workspace);
+  const size_t nbh = (size_t)d->B * d->H;
+  a.substates = (d->L / lw > 1) ? a.part + nbh * part_floats(d->R, d->Dk) : nullptr;
+  a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = round_rp(d->R); a.L = d->L;
+  st = launch_bwd(a, d->dtype, d->Dk, lw, stream);
+  if (st) return st;
+  return launch_param_reduce(a.part, (int)nbh, d->R, d->Dk, dUb, dUw, dVb, dVw, stream);
+}
+
+}  // extern "C"

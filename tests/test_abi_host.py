@@ -1,0 +1,87 @@
+"""Host-side checks of the C ABI: the library loads, exports every symbol
+include/carve.h declares, and validation errors come back before any HIP
+call (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_27229_amd import carve
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_symbols():
+    text = open(os.path.join(ROOT, "include", "carve.h")).read()
+    decl = r"^\s*(?:const\s+char\s*\*|int|size_t|void)\s*(carve_[a-z_]+)\s*\("
+    return sorted(set(re.findall(decl, text, flags=re.M)))
+
+
+def test_header_declares_the_binding_symbols():
+    assert sorted(carve.SYMBOLS) == _declared_symbols()
+
+
+def test_library_exports_every_declared_symbol():
+    lib = carve.load_library()
+    for name in _declared_symbols():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    lib = carve.load_library()
+    for st in range(0, -7, -1):
+        assert lib.carve_status_string(st)
+    assert carve.status_string(0) == "ok"
+
+
+def _dims(**kw):
+    base = dict(B=1, T=128, H=2, Dk=64, Dv=64, R=16, L=64, dtype=carve.CARVE_BF16)
+    base.update(kw)
+    return carve.Dims(**base)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=100), -2), (dict(B=0), -2), (dict(Dk=48, Dv=48), -3), (dict(Dk=64, Dv=32), -3),
+    (dict(R=65), -3), (dict(L=8, T=128), -3), (dict(dtype=7), -3),
+])
+def test_forward_validation(kw, expect):
+    lib = carve.load_library()
+    d = _dims(**kw)
+    fake = ctypes.c_void_p(4096)  # never dereferenced: validation fails first
+    st = lib.carve_chunk_fwd(ctypes.byref(d), *([fake] * 12), fake, None, None, None, 0, None)
+    assert st == expect
+
+
+def test_forward_null_and_alignment():
+    lib = carve.load_library()
+    d = _dims()
+    fake = ctypes.c_void_p(4096)
+    st = lib.carve_chunk_fwd(ctypes.byref(d), None, *([fake] * 11), fake, None, None, None, 0, None)
+    assert st == -1
+    bad = ctypes.c_void_p(4096 + 4)
+    st = lib.carve_chunk_fwd(ctypes.byref(d), bad, *([fake] * 11), fake, None, None, None, 0, None)
+    assert st == -4
+
+
+def test_backward_workspace_checks():
+    lib = carve.load_library()
+    d = _dims()
+    need = lib.carve_workspace_size(ctypes.byref(d), 1)
+    assert need > 0
+    assert lib.carve_workspace_size(ctypes.byref(_dims(T=100)), 1) == 0
+    # distinct fake addresses far apart so no range overlaps
+    ptrs = [ctypes.c_void_p(1 << 40 | (i << 32)) for i in range(28)]
+    st = lib.carve_chunk_bwd(ctypes.byref(d), *ptrs[:26], None, 0, None)
+    assert st == -5
+    st = lib.carve_chunk_bwd(ctypes.byref(d), *ptrs[:26], ptrs[26], need - 1, None)
+    assert st == -5
+
+
+def test_aliasing_output_rejected():
+    lib = carve.load_library()
+    d = _dims()
+    ptrs = [ctypes.c_void_p(1 << 40 | (i << 32)) for i in range(16)]
+    args = ptrs[:12] + [ptrs[0]]  # o aliases q
+    st = lib.carve_chunk_fwd(ctypes.byref(d), *args, None, None, None, 0, None)
+    assert st == -3

@@ -1,0 +1,138 @@
+"""Forward parity of the HIP path (through the C ABI) against the CPU oracle.
+
+Bars: f32 inputs max-rel <= 1e-4; bf16 inputs (f32 state / accumulation)
+max-rel <= 2e-2, on o, S_T and the chunk-boundary states.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as orc
+from paper_2606_27229_amd import carve
+from paper_2606_27229_amd.inputs import WORKLOADS, Workload, make_inputs
+from tests.gpu_util import host, max_rel, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def run_gpu_fwd(w, inp, L=None):
+    L = L or w.L
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    x = to_gpu(inp, dt)
+    o, S_T, S_chunks = carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"],
+                                       x["Ub"], x["Uw"], x["Vb"], x["Vw"], x["S0"], L=L)
+    torch.cuda.synchronize()
+    return {"o": host(o), "S_T": host(S_T), "S_chunks": host(S_chunks)}
+
+
+def check_fwd(w, inp, L=None, tol=None):
+    L = L or w.L
+    tol = tol or TOL[w.dtype]
+    ref = orc.fwd_serial(inp, L, want_chunks=True)
+    got = run_gpu_fwd(w, inp, L)
+    errs = {key: max_rel(got[key], ref[key]) for key in ("o", "S_T", "S_chunks")}
+    for key, e in errs.items():
+        assert np.all(np.isfinite(got[key])), key
+        assert e <= tol, (key, e, errs)
+    return errs, got, ref
+
+
+def _w(**kw):
+    base = dict(name="t", B=1, H=2, T=128, Dk=32, Dv=32, L=32, R=4, dtype="f32", mu=2.0, s0=0.3, u_std=0.3)
+    base.update(kw)
+    return Workload(**base)
+
+
+def test_tiny_fp32_workload():
+    w = WORKLOADS["tiny_fp32"]
+    print("case tiny_fp32", flush=True)
+    check_fwd(w, make_inputs(w, seed=0))
+    check_fwd(w, make_inputs(w, seed=0, zero_content=True))
+
+
+@pytest.mark.parametrize("D", [32, 64])
+@pytest.mark.parametrize("L", [16, 32, 64, 128])
+def test_fp32_shapes_content_amplified(D, L):
+    w = _w(Dk=D, Dv=D, L=L, T=256, R=5)
+    print(f"case fp32 D={D} L={L}", flush=True)
+    check_fwd(w, make_inputs(w, seed=D + L))
+
+
+def test_fp32_d128():
+    w = _w(Dk=128, Dv=128, L=64, T=128, R=32)
+    print("case fp32 D=128", flush=True)
+    check_fwd(w, make_inputs(w, seed=3))
+
+
+@pytest.mark.parametrize("L", [16, 32, 64, 128])
+def test_bf16_d128_content_amplified(L):
+    w = _w(Dk=128, Dv=128, L=L, T=256, R=32, dtype="bf16", mu=3.0, s0=0.0)
+    print(f"case bf16 D=128 L={L}", flush=True)
+    check_fwd(w, make_inputs(w, seed=L))
+
+
+@pytest.mark.parametrize("D", [32, 64])
+def test_bf16_small_heads(D):
+    w = _w(Dk=D, Dv=D, L=64, T=192, R=16, dtype="bf16", mu=3.0)
+    print(f"case bf16 D={D}", flush=True)
+    check_fwd(w, make_inputs(w, seed=D))
+
+
+def test_layer_fp32_workload_forward():
+    w = WORKLOADS["layer_fp32"]
+    print("case layer_fp32", flush=True)
+    check_fwd(w, make_inputs(w, seed=1))
+
+
+def test_erase_heavy_bf16():
+    w = _w(Dk=128, Dv=128, L=128, T=256, R=32, dtype="bf16", mu=3.0, s0=0.0)
+    print("case erase-heavy", flush=True)
+    check_fwd(w, make_inputs(w, seed=7, bx_mean=0.0))
+
+
+def test_content_term_is_visible_on_gpu():
+    """Negative control: with content projections of scale 1 the outputs move
+    by far more than the tolerance, so a broken fold cannot pass parity."""
+    w = _w(Dk=128, Dv=128, L=64, T=256, R=32, dtype="bf16", mu=3.0, s0=0.0, u_std=1.0)
+    inp = make_inputs(w, seed=11)
+    _, got, _ = check_fwd(w, inp)
+    inp0 = dict(inp)
+    inp0["Ub"] = np.zeros_like(inp["Ub"])
+    inp0["Uw"] = np.zeros_like(inp["Uw"])
+    got0 = run_gpu_fwd(w, inp0)
+    assert max_rel(got["o"], got0["o"]) >= 10 * TOL["bf16"]
+
+
+def test_determinism_and_overwrite():
+    w = _w(Dk=128, Dv=128, L=64, T=128, R=32, dtype="bf16", mu=3.0)
+    inp = make_inputs(w, seed=5)
+    x = to_gpu(inp, torch.bfloat16)
+    outs = []
+    for poison in (float("nan"), 7.0):
+        o = torch.full((w.B, w.T, w.H, w.Dv), poison, dtype=torch.bfloat16, device="cuda")
+        st = torch.full((w.B, w.H, w.Dv, w.Dk), poison, device="cuda")
+        sc = torch.full((w.B, w.H, w.T // w.L, w.Dv, w.Dk), poison, device="cuda")
+        carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
+                        x["Vb"], x["Vw"], x["S0"], L=w.L, out={"o": o, "S_T": st, "S_chunks": sc})
+        torch.cuda.synchronize()
+        outs.append((host(o), host(st), host(sc)))
+    for a, b in zip(outs[0], outs[1]):
+        assert np.all(np.isfinite(a))
+        assert np.array_equal(a, b)
+
+
+def test_split_call_matches_full_call():
+    """Chunk-by-chunk calls chained through S0 equal one full call (bitwise)."""
+    w = _w(Dk=64, Dv=64, L=32, T=256, R=16, dtype="f32")
+    inp = make_inputs(w, seed=2)
+    full = run_gpu_fwd(w, inp)
+    T1 = 96
+    first = {kk: (vv[:, :T1] if (vv is not None and vv.ndim >= 3 and vv.shape[1] == w.T) else vv) for kk, vv in inp.items()}
+    second = {kk: (vv[:, T1:] if (vv is not None and vv.ndim >= 3 and vv.shape[1] == w.T) else vv) for kk, vv in inp.items()}
+    r1 = run_gpu_fwd(w.with_(T=T1), first)
+    second["S0"] = r1["S_T"]
+    r2 = run_gpu_fwd(w.with_(T=w.T - T1), second)
+    assert np.array_equal(np.concatenate([r1["o"], r2["o"]], axis=1), full["o"])
+    assert np.array_equal(r2["S_T"], full["S_T"])
