@@ -33,6 +33,7 @@ def check_fwd(w, inp, L=None, tol=None):
     ref = orc.fwd_serial(inp, L, want_chunks=True)
     got = run_gpu_fwd(w, inp, L)
     errs = {key: max_rel(got[key], ref[key]) for key in ("o", "S_T", "S_chunks")}
+    print("max-rel errors:", {key: float("%.3g" % e) for key, e in errs.items()}, flush=True)
     for key, e in errs.items():
         assert np.all(np.isfinite(got[key])), key
         assert e <= tol, (key, e, errs)
