@@ -1,0 +1,210 @@
+#!/usr/bin/env python3
+"""Benchmark: chunked CARVE layer forward + backward on one MI355X.
+
+One step = carve_chunk_fwd + carve_chunk_bwd over one batch of the 1.3B-scale
+layer (B=4, H=16, T=4096, d_k=d_v=128, r=32, L=64, bf16 token tensors, f32
+state and accumulation), inputs already resident in HBM.  Prints ONE JSON
+line with tokens/s, the roofline of the dominant kernel and the CPU oracle
+timed on a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--L 64]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "layer fwd+bwd tokens/s, H=16 d=128 T=4096 L=64 bf16; % MFMA peak"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+KERNEL_SOURCES = ("paper_2606_27229_amd/csrc/carve_fwd.hip", "paper_2606_27229_amd/csrc/carve_bwd.hip",
+                  "paper_2606_27229_amd/csrc/carve_dev.h", "paper_2606_27229_amd/csrc/carve_kernels.h")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer_1p3b_T4096.json")
+
+
+def algorithmic_counts(B, T, H, d, R, L):
+    """Algorithmic bytes and flops per call, per kernel (inputs/outputs once).
+
+    Bytes per token-head (bf16 token tensors, f32 g and states):
+      forward  reads q,k,v (3*2d) + g (4d) + bx,wx (2*2d) + beta (2), writes
+               o (2d) + chunk-start states (4 d^2 / L)
+      backward reads the forward inputs + dO (2d) + chunk-start states, writes
+               dq,dk,dv (3*2d) + dg (4d) + dbx,dwx (2*2d) + dbeta (2)
+    Flops per token-head (multiply-add = 2): forward
+      2 * (2 r d^2 / L + 3 d^2 + 4 r d + 5/2 L d + L^2 / 6), backward 2x forward.
+    """
+    th = B * T * H
+    fwd_bytes = (3 * 2 * d + 4 * d + 2 * 2 * d + 2) + (2 * d + 4 * d * d / L)
+    bwd_bytes = (3 * 2 * d + 4 * d + 2 * 2 * d + 2) + 2 * d + 4 * d * d / L + (3 * 2 * d + 4 * d + 2 * 2 * d + 2)
+    fwd_mac = 2 * R * d * d / L + 3 * d * d + 4 * R * d + 2.5 * L * d + L * L / 6.0
+    return {
+        "fwd_bytes": fwd_bytes * th, "bwd_bytes": bwd_bytes * th,
+        "fwd_flops": 2 * fwd_mac * th, "bwd_flops": 4 * fwd_mac * th,
+    }
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel):
+    """HBM bytes per launch measured with rocprofv3 counters, if they were taken
+    on the current kernel sources; None otherwise."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    return None if k is None else k.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, L, seed):
+    """Time the CPU oracle (fwd + exact bwd) on one batch element of the workload."""
+    from oracle import oracle as orc
+    from paper_2606_27229_amd.inputs import make_inputs
+
+    ws = w.with_(B=1)
+    inp = make_inputs(ws, seed=seed)
+    threads = max(1, min(16, os.cpu_count() or 1, ws.B * ws.H))
+    t0 = time.perf_counter()
+    orc.fwd_serial(inp, L, nthreads=threads)
+    t1 = time.perf_counter()
+    orc.bwd(inp, L, inp["dO"], None, nthreads=threads)
+    t2 = time.perf_counter()
+    tokens = ws.B * ws.T   # layer tokens (all heads) in the sample
+    return {"value": tokens / (t2 - t0), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"B=1 of {w.B}, all {w.H} heads, T={w.T}, L={L}: token-serial forward + exact "
+                      f"reverse-mode backward in double, fwd {t1 - t0:.2f} s, bwd {t2 - t1:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--L", type=int, default=64)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the layer shards over (batch, head) with no exchange "
+              "except a 64 KB parameter-gradient all-reduce, which this build does not run; "
+              "use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2606_27229_amd import carve
+    from paper_2606_27229_amd.inputs import HEADLINE, WORKLOADS, make_inputs
+
+    w = WORKLOADS[HEADLINE].with_(L=args.L)
+    L = w.L
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    inp = make_inputs(w, seed=4)
+    x = {}
+    for key, val in inp.items():
+        if val is None:
+            x[key] = None
+            continue
+        t = torch.from_numpy(np.ascontiguousarray(val))
+        if key not in ("g", "Ub", "Uw", "Vb", "Vw", "S0", "dS_T"):
+            t = t.to(torch.bfloat16)
+        x[key] = t.to(dev)
+    B, T, H, d, R = w.B, w.T, w.H, w.Dk, w.R
+    f32, bf = torch.float32, torch.bfloat16
+    fwd_out = {"o": torch.empty((B, T, H, d), dtype=bf, device=dev),
+               "S_T": torch.empty((B, H, d, d), dtype=f32, device=dev),
+               "S_chunks": torch.empty((B, H, T // L, d, d), dtype=f32, device=dev)}
+    bwd_out = {"dq": torch.empty((B, T, H, d), dtype=bf, device=dev),
+               "dk": torch.empty((B, T, H, d), dtype=bf, device=dev),
+               "dv": torch.empty((B, T, H, d), dtype=bf, device=dev),
+               "dbeta": torch.empty((B, T, H), dtype=bf, device=dev),
+               "dg": torch.empty((B, T, H, d), dtype=f32, device=dev),
+               "dbx": torch.empty((B, T, H, d), dtype=bf, device=dev),
+               "dwx": torch.empty((B, T, H, d), dtype=bf, device=dev),
+               "dUb": torch.empty((R, d), dtype=f32, device=dev), "dUw": torch.empty((R, d), dtype=f32, device=dev),
+               "dVb": torch.empty((d, R), dtype=f32, device=dev), "dVw": torch.empty((d, R), dtype=f32, device=dev),
+               "dS0": torch.empty((B, H, d, d), dtype=f32, device=dev)}
+    dims = carve.make_dims(B, T, H, d, d, R, L, bf)
+    ws = torch.empty(max(carve.workspace_size(dims, True), 16), dtype=torch.uint8, device=dev)
+
+    def fwd():
+        carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
+                        x["Vb"], x["Vw"], x["S0"], L=L, out=fwd_out)
+
+    def bwd():
+        carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
+                        x["Vb"], x["Vw"], fwd_out["S_chunks"], x["dO"], None, L=L, out=bwd_out,
+                        workspace=ws)
+
+    for _ in range(args.warmup):
+        fwd()
+        bwd()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        ev[s][0].record(stream)
+        fwd()
+        ev[s][1].record(stream)
+        bwd()
+        ev[s][2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    fwd_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
+    bwd_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
+    ms_per_step = wall * 1e3 / args.steps
+    tokens = B * T
+    cnt = algorithmic_counts(B, T, H, d, R, L)
+
+    dominant = "carve_bwd_kernel" if bwd_ms >= fwd_ms else "carve_fwd_kernel"
+    dom_ms = bwd_ms if dominant == "carve_bwd_kernel" else fwd_ms
+    dom_bytes = cnt["bwd_bytes"] if dominant == "carve_bwd_kernel" else cnt["fwd_bytes"]
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    layer_tflops = (cnt["fwd_flops"] + cnt["bwd_flops"]) / (ms_per_step * 1e-3) / 1e12
+    res = {
+        "metric": METRIC,
+        "value": tokens / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "H": H, "T": T, "Dk": d, "Dv": d, "R": R, "L": L,
+                   "token_dtype": "bf16", "state_dtype": "f32"},
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": load_traffic(dominant),
+                     "algorithmic_bytes_per_launch": dom_bytes, "avg_launch_ms": dom_ms},
+        "kernels_ms": {"carve_fwd_kernel": fwd_ms, "carve_bwd_kernel+param_reduce": bwd_ms},
+        "mfma_peak_frac": layer_tflops / BF16_PEAK_TFLOPS,
+        "layer_tflops": layer_tflops,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, L, seed=4)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

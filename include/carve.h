@@ -44,10 +44,11 @@
  *     calls except the cached kernel attributes; concurrent calls on
  *     different streams must use different workspaces.
  *   - Supported shapes: Dk == Dv in {32, 64, 128}; 1 <= R <= 64;
- *     L in {16, 32, 64, 128} (f32 with Dk = 128: L in {16, 32, 64, 128} is
- *     run in 16-token WY tiles); T a positive multiple of L; B, H >= 1.
- *     Other shapes return CARVE_ERR_UNSUPPORTED (or CARVE_ERR_SHAPE when
- *     T % L != 0 or a size is non-positive).
+ *     L in {16, 32, 64, 128}; T a positive multiple of L; B, H >= 1.
+ *     Not built: f32 token tensors with Dk = 128; the backward with R > 32
+ *     at Dk = 128 (bf16) or at Dk = 64 (f32).  These, and other shapes,
+ *     return CARVE_ERR_UNSUPPORTED (CARVE_ERR_SHAPE when T % L != 0 or a
+ *     size is non-positive).
  *   - Every pointer must be 16-byte aligned (CARVE_ERR_ALIGN).
  *   - Inputs are assumed finite with g <= 0; NaN/Inf propagate.  Numerical
  *     range: within any 16 consecutive tokens of a chunk the summed log

@@ -2,8 +2,11 @@
 //
 // One workgroup per (batch, head) runs the whole sequence as a persistent
 // loop over gate chunks of L tokens (Alg. carve_fwd).  The recurrent state
-// S (Dv x Dk, f32) stays in registers for the whole call: wave w owns key
-// columns [16w, 16w+16) of S for every value row, in the MFMA result layout.
+// S (Dv x Dk, f32) stays in registers for the whole call: wave w owns the key
+// column tiles [w*CPW, (w+1)*CPW) of S (16 columns each) for every value row,
+// in the MFMA result layout.  The shared parameters are staged in LDS once,
+// and the token inputs of the next WY tile are fetched into registers while
+// the current tile computes.
 //
 // Per gate chunk c (state S_hat = S at the chunk start, Eq. content_readout):
 //   F = [Ub; Uw] S_hat            fold, read straight from the S registers
@@ -33,21 +36,25 @@
 namespace carve {
 
 template <typename T, int D, int LW>
-__global__ void __launch_bounds__(D * 4) carve_fwd_kernel(FwdArgs a) {
+__global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
   typedef Mma<T> M;
-  constexpr int NW = D / 16;      // waves; wave w owns key-column tile w
-  constexpr int NT = NW * 64;
-  constexpr int NB = LW / 16;     // 16-token blocks per WY tile
-  constexpr int NIT = D / 16;     // value-row tiles
+  constexpr int NT = fwd_threads(D);
+  constexpr int NW = NT / 64;         // waves
+  constexpr int NCT = D / 16;         // 16-column tiles of S (key side) / of the value side
+  constexpr int CPW = NCT / NW;       // column tiles per wave
+  constexpr int NB = LW / 16;         // 16-token blocks per WY tile
+  constexpr int NIT = D / 16;         // value-row tiles
   constexpr int KS = M::KS, KPL = M::KPL;
   constexpr int LK = lk_of<T, LW>();  // padded token extent of the K = LW products
+  constexpr int VEC = 16 / sizeof(T); // elements per 16-byte vector
+  constexpr int NVT = LW * D / VEC;                // 16-byte vectors of a q (or k) tile
+  constexpr int NQV = (NVT + NT - 1) / NT;         // per thread
   const int RP = a.RP, R2 = 2 * a.RP, R = a.R;
   const int H = a.H, Tn = a.T, L = a.L;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
   const int bh = blockIdx.x, b = bh / H, h = bh % H;
-  const int nch = Tn / L, msub = L / LW;
-  const size_t rowstride = (size_t)H * D;  // elements between consecutive tokens
+  const int nch = Tn / L, msub = L / LW, ntiles = Tn / LW;
 
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const FwdLds lay = fwd_lds<T, D, LW>(RP);
@@ -57,15 +64,18 @@ __global__ void __launch_bounds__(D * 4) carve_fwd_kernel(FwdArgs a) {
   T* sKi = reinterpret_cast<T*>(smem + lay.Ki);
   T* sF = reinterpret_cast<T*>(smem + lay.F);
   T* sTau = reinterpret_cast<T*>(smem + lay.Tau);
-  T* sTb = sTau;                                  // alias: T (bf16/f32), after tau is dead
+  T* sTb = sTau;                                  // alias: T, after tau is dead
   T* sKhT = reinterpret_cast<T*>(smem + lay.KhT);
   float* sA = reinterpret_cast<float*>(smem + lay.A);
-  T* sRT = sQ;                                    // alias: R^T [D][LW]
-  T* sUT = sK;                                    // alias: u^T [D][LW]
-  T* sP = sKi;                                    // alias: P [LW][LW]
+  T* sRT = sQ;                                    // alias: R^T [D][LK]
+  T* sUT = sK;                                    // alias: u^T [D][LK]
+  T* sP = sKi;                                    // alias: P [LW][LK]
   float* sBase = reinterpret_cast<float*>(smem + lay.Base);   // [NB][D]  e^{base_ti}
   float* sCf = reinterpret_cast<float*>(smem + lay.Cf);       // [NB*NB][D] e^{base_ti - base_si}
   float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);   // [LW]
+  T* sU = reinterpret_cast<T*>(smem + lay.Ucat);              // [2RP][D] padded [Ub; Uw]
+  T* sVb = reinterpret_cast<T*>(smem + lay.Vb);               // [D][RP]
+  T* sVw = reinterpret_cast<T*>(smem + lay.Vw);               // [D][RP]
 
   const T* __restrict__ q = reinterpret_cast<const T*>(a.q);
   const T* __restrict__ k = reinterpret_cast<const T*>(a.k);
@@ -73,78 +83,126 @@ __global__ void __launch_bounds__(D * 4) carve_fwd_kernel(FwdArgs a) {
   const T* __restrict__ bx = reinterpret_cast<const T*>(a.bx);
   const T* __restrict__ wx = reinterpret_cast<const T*>(a.wx);
   const T* __restrict__ beta = reinterpret_cast<const T*>(a.beta);
+  const float* __restrict__ gl = a.g;
   T* __restrict__ o = reinterpret_cast<T*>(a.o);
 
-  // ---- state registers: S[16*it + 4g + r][16w + c] -------------------------
-  f32x4 S[NIT];
-  const size_t soff = (size_t)bh * D * D;
-  for (int it = 0; it < NIT; ++it) {
-    for (int r = 0; r < 4; ++r)
-      S[it][r] = a.S0 ? a.S0[soff + (size_t)(16 * it + 4 * g + r) * D + 16 * w + c] : 0.0f;
-    store_tile(sS, D, 16 * it, 16 * w, S[it], lane);
+  // ---- shared parameters -> LDS (zero padded to RP) ------------------------
+  for (int x = tid; x < R2 * D; x += NT) {
+    const int rr = x / D, i = x % D;
+    float u = 0.0f;
+    if (rr < R) u = a.Ub[(size_t)rr * D + i];
+    else if (rr >= RP && rr < RP + R) u = a.Uw[(size_t)(rr - RP) * D + i];
+    sU[x] = (T)u;
   }
+  for (int x = tid; x < D * RP; x += NT) {
+    const int j = x / RP, rr = x % RP;
+    sVb[x] = (T)(rr < R ? a.Vb[(size_t)j * R + rr] : 0.0f);
+    sVw[x] = (T)(rr < R ? a.Vw[(size_t)j * R + rr] : 0.0f);
+  }
+
+  // ---- state registers: S[cq][it][r] = S[16*it + 4g + r][16*(w*CPW+cq) + c] ----
+  f32x4 S[CPW][NIT];
+  const size_t soff = (size_t)bh * D * D;
+  for (int cq = 0; cq < CPW; ++cq) {
+    const int col = 16 * (w * CPW + cq) + c;
+    for (int it = 0; it < NIT; ++it) {
+      for (int r = 0; r < 4; ++r)
+        S[cq][it][r] = a.S0 ? a.S0[soff + (size_t)(16 * it + 4 * g + r) * D + col] : 0.0f;
+      store_tile(sS, D, 16 * it, 16 * (w * CPW + cq), S[cq][it], lane);
+    }
+  }
+
+  // ---- prefetch registers for the next WY tile ---------------------------
+  f32x4 pq[NQV], pk[NQV];
+  float pbx[CPW][NB][4], pg[CPW][NB][4], pwx[CPW][NB][4], pv[CPW][NB][4];
+  float pbeta = 0.0f;
+  auto prefetch_qk = [&](int tile) {
+    const size_t tb = ((size_t)b * Tn + (size_t)tile * LW) * H + h;
+    for (int u = 0; u < NQV; ++u) {
+      const int x = tid + u * NT;
+      if (NVT % NT != 0 && x >= NVT) break;
+      const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;
+      const size_t gofs = (tb + (size_t)t * H) * D + j;
+      pq[u] = *reinterpret_cast<const f32x4*>(q + gofs);
+      pk[u] = *reinterpret_cast<const f32x4*>(k + gofs);
+    }
+    if (tid < LW) pbeta = to_f(beta[tb + (size_t)tid * H]);
+  };
+  auto prefetch_gates = [&](int tile) {
+    const size_t tb = ((size_t)b * Tn + (size_t)tile * LW) * H + h;
+    for (int cq = 0; cq < CPW; ++cq) {
+      const int col = 16 * (w * CPW + cq) + c;
+      for (int ti = 0; ti < NB; ++ti)
+        for (int r = 0; r < 4; ++r) {
+          const size_t e = (tb + (size_t)(16 * ti + 4 * g + r) * H) * D + col;
+          pbx[cq][ti][r] = to_f(bx[e]);
+          pg[cq][ti][r] = gl[e];
+          pwx[cq][ti][r] = to_f(wx[e]);
+          pv[cq][ti][r] = to_f(v[e]);
+        }
+    }
+  };
+  prefetch_qk(0);
+  prefetch_gates(0);
 
   for (int ch = 0; ch < nch; ++ch) {
     if (a.S_chunks) {
       float* dst = a.S_chunks + ((size_t)bh * nch + ch) * D * D;
-      for (int it = 0; it < NIT; ++it)
-        for (int r = 0; r < 4; ++r) dst[(size_t)(16 * it + 4 * g + r) * D + 16 * w + c] = S[it][r];
+      for (int cq = 0; cq < CPW; ++cq) {
+        const int col = 16 * (w * CPW + cq) + c;
+        for (int it = 0; it < NIT; ++it)
+          for (int r = 0; r < 4; ++r) dst[(size_t)(16 * it + 4 * g + r) * D + col] = S[cq][it][r];
+      }
     }
     for (int m = 0; m < msub; ++m) {
-      const int t0 = ch * L + m * LW;
+      const int tile = ch * msub + m;
+      const int t0 = tile * LW;
       const size_t tokbase = ((size_t)b * Tn + t0) * H + h;   // token row index of t0
 
-      // ---- P0: q, k tiles and beta -------------------------------------------
-      {
-        constexpr int VEC = 16 / sizeof(T);
-        constexpr int NV = LW * D / VEC;
-        for (int x = tid; x < NV; x += NT) {
-          const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;
-          const size_t gofs = (tokbase + (size_t)t * H) * D + j;
-          *reinterpret_cast<f32x4*>(sQ + t * D + j) = *reinterpret_cast<const f32x4*>(q + gofs);
-          *reinterpret_cast<f32x4*>(sK + t * D + j) = *reinterpret_cast<const f32x4*>(k + gofs);
-        }
-        for (int t = tid; t < LW; t += NT) sBeta[t] = to_f(beta[tokbase + (size_t)t * H]);
+      // ---- P0: q, k tiles and beta from the prefetch registers -------------
+      for (int u = 0; u < NQV; ++u) {
+        const int x = tid + u * NT;
+        if (NVT % NT != 0 && x >= NVT) break;
+        const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;
+        *reinterpret_cast<f32x4*>(sQ + t * D + j) = pq[u];
+        *reinterpret_cast<f32x4*>(sK + t * D + j) = pk[u];
       }
+      if (tid < LW) sBeta[tid] = pbeta;
+      if (tile + 1 < ntiles) prefetch_qk(tile + 1);
       // ---- P1: fold F = [Ub;Uw] S_hat from the state registers ---------------
       if (m == 0) {
-        for (int rt = 0; rt < R2 / 16; ++rt) {
-          const int rr = 16 * rt + c;  // padded row of [Ub;Uw] this lane supplies as B
-          const float* urow = nullptr;
-          if (rr < R) urow = a.Ub + (size_t)rr * D;
-          else if (rr >= RP && rr < RP + R) urow = a.Uw + (size_t)(rr - RP) * D;
-          f32x4 acc = zero4();
-          if constexpr (KPL == 8) {
-            for (int ks = 0; ks < D / 32; ++ks) {
-              typename M::frag af, bfg;
-              for (int e = 0; e < 4; ++e) {
-                af[e] = (T)S[2 * ks][e];
-                af[4 + e] = (T)S[2 * ks + 1][e];
+        for (int cq = 0; cq < CPW; ++cq) {
+          const int ct = w * CPW + cq;
+          for (int rt = 0; rt < R2 / 16; ++rt) {
+            const T* urow = sU + (16 * rt + c) * D;  // B row this lane supplies
+            f32x4 acc = zero4();
+            if constexpr (KPL == 8) {
+              for (int ks = 0; ks < D / 32; ++ks) {
+                typename M::frag af, bfg;
+                const T* p = urow + 32 * ks + 4 * g;
+                for (int e = 0; e < 4; ++e) {
+                  af[e] = (T)S[cq][2 * ks][e];
+                  af[4 + e] = (T)S[cq][2 * ks + 1][e];
+                  bfg[e] = p[e];
+                  bfg[4 + e] = p[16 + e];
+                }
+                acc = M::mma(af, bfg, acc);
               }
-              const int i0 = 32 * ks + 4 * g;
-              for (int e = 0; e < 4; ++e) {
-                bfg[e] = (T)(urow ? urow[i0 + e] : 0.0f);
-                bfg[4 + e] = (T)(urow ? urow[i0 + 16 + e] : 0.0f);
-              }
-              acc = M::mma(af, bfg, acc);
+            } else {
+              for (int it = 0; it < NIT; ++it)
+                for (int r4 = 0; r4 < 4; ++r4) acc = M::mma((T)S[cq][it][r4], urow[16 * it + 4 * g + r4], acc);
             }
-          } else {
-            for (int it = 0; it < NIT; ++it)
-              for (int r4 = 0; r4 < 4; ++r4) {
-                const float bv = urow ? urow[16 * it + 4 * g + r4] : 0.0f;
-                acc = M::mma((T)S[it][r4], (T)bv, acc);
-              }
+            // acc = F^T[j = 16ct + 4g + r][16rt + c]  ->  sF[r][j]
+            store_tile_t(sF, D, 16 * ct, 16 * rt, acc, lane);
           }
-          // acc = F^T[j = 16w + 4g + r][16rt + c]  ->  sF[r][j]
-          store_tile_t(sF, D, 16 * w, 16 * rt, acc, lane);
         }
       }
       __syncthreads();
 
       // ---- P2: tau = tanh(Q F^T) -> sTau [LW][2RP] ----------------------------
       {
-        const int ntiles = NB * (R2 / 16);
-        for (int x = w; x < ntiles; x += NW) {
+        const int ntl = NB * (R2 / 16);
+        for (int x = w; x < ntl; x += NW) {
           const int ti = x / (R2 / 16), rt = x % (R2 / 16);
           f32x4 acc = zero4();
           for (int ks = 0; ks < D / KS; ++ks) {
@@ -157,46 +215,43 @@ __global__ void __launch_bounds__(D * 4) carve_fwd_kernel(FwdArgs a) {
       }
       __syncthreads();
 
-      // ---- P3: gate logits; P4: key-side retention factors ---------------------
-      float ell[NB][4];
-      float wv[NB][4];
-      {
-        const int jj = 16 * w + c;  // key column (erase side) and value column (write side)
+      // ---- P3: gate logits (key side: l; value side: w*v) --------------------
+      float ell[CPW][NB][4];
+      float wv[CPW][NB][4];
+      for (int cq = 0; cq < CPW; ++cq) {
+        const int ct = w * CPW + cq;
+        const T* vbrow = sVb + (16 * ct + c) * RP;
+        const T* vwrow = sVw + (16 * ct + c) * RP;
         for (int ti = 0; ti < NB; ++ti) {
           f32x4 accB = zero4(), accW = zero4();
           for (int ks = 0; ks < RP / KS; ++ks) {
             const int r0 = ks * KS + g * KPL;
-            float vb[KPL], vw[KPL];
-            for (int e = 0; e < KPL; ++e) {
-              const int rr = r0 + e;
-              vb[e] = rr < R ? a.Vb[(size_t)jj * R + rr] : 0.0f;
-              vw[e] = rr < R ? a.Vw[(size_t)jj * R + rr] : 0.0f;
-            }
             const int arow = (16 * ti + c) * R2;
-            accB = M::mma(M::load(sTau + arow + r0), M::from_f32(vb), accB);
-            accW = M::mma(M::load(sTau + arow + RP + r0), M::from_f32(vw), accW);
+            accB = M::mma(M::load(sTau + arow + r0), M::load(vbrow + r0), accB);
+            accW = M::mma(M::load(sTau + arow + RP + r0), M::load(vwrow + r0), accW);
           }
           for (int r = 0; r < 4; ++r) {
-            const int t = 16 * ti + 4 * g + r;
-            const size_t e = (tokbase + (size_t)t * H) * D + jj;
-            const float zb = to_f(bx[e]) + accB[r];
-            ell[ti][r] = a.g[e] - softplus_f(zb);
-            const float wg = sigmoid_f(to_f(wx[e]) + accW[r]);
-            wv[ti][r] = wg * to_f(v[e]);
+            const float zb = pbx[cq][ti][r] + accB[r];
+            ell[cq][ti][r] = pg[cq][ti][r] - softplus_f(zb);
+            wv[cq][ti][r] = sigmoid_f(pwx[cq][ti][r] + accW[r]) * pv[cq][ti][r];
           }
         }
       }
-      float gamma_col;  // e^{Lam_{LW-1}} for key column 16w + c
-      {
-        const int jj = 16 * w + c;
-        float base = 0.0f;        // Lam at the end of the previous block
+      if (tile + 1 < ntiles) prefetch_gates(tile + 1);
+
+      // ---- P4: key-side retention factors --------------------------------------
+      float gamma_col[CPW];  // e^{Lam_{LW-1}} for key column 16(w*CPW+cq) + c
+      for (int cq = 0; cq < CPW; ++cq) {
+        const int ct = w * CPW + cq;
+        const int jj = 16 * ct + c;
+        float base = 0.0f;  // Lam at the end of the previous block
         float bases[NB];
         for (int ti = 0; ti < NB; ++ti) {
           float p[4];
-          p[0] = ell[ti][0];
-          p[1] = p[0] + ell[ti][1];
-          p[2] = p[1] + ell[ti][2];
-          p[3] = p[2] + ell[ti][3];
+          p[0] = ell[cq][ti][0];
+          p[1] = p[0] + ell[cq][ti][1];
+          p[2] = p[1] + ell[cq][ti][2];
+          p[3] = p[2] + ell[cq][ti][3];
           float incl = p[3];
           float y = __shfl_up(incl, 16);
           if (g >= 1) incl += y;
@@ -223,19 +278,19 @@ __global__ void __launch_bounds__(D * 4) carve_fwd_kernel(FwdArgs a) {
             sQ[t * D + jj] = (T)(qv * E[r]);
             Ki[r] *= kv;
             sKi[t * D + jj] = (T)Ki[r];
+            ell[cq][ti][r] = Ki[r];  // keep k e^{-Lam_rel}
           }
           bases[ti] = base;
-          ell[ti][0] = Ki[0]; ell[ti][1] = Ki[1]; ell[ti][2] = Ki[2]; ell[ti][3] = Ki[3];  // keep k*Kinv
           base += btot;
         }
         const float lam_end = base;  // Lam_{LW-1}
-        gamma_col = fast_exp(lam_end);
+        gamma_col[cq] = fast_exp(lam_end);
         for (int ti = 0; ti < NB; ++ti) {
           // Khat^T[j][s] = Kinv_s e^{Lam_end - base_si}
           const float f = fast_exp(lam_end - bases[ti]);
           f32x4 kh;
-          for (int r = 0; r < 4; ++r) kh[r] = ell[ti][r] * f;
-          store_tile_t(sKhT, LK, 16 * ti, 16 * w, kh, lane);
+          for (int r = 0; r < 4; ++r) kh[r] = ell[cq][ti][r] * f;
+          store_tile_t(sKhT, LK, 16 * ti, 16 * ct, kh, lane);
           if (g == 0) {
             sBase[ti * D + jj] = fast_exp(bases[ti]);
             for (int si = 0; si < ti; ++si) sCf[(ti * NB + si) * D + jj] = fast_exp(bases[ti] - bases[si]);
@@ -271,18 +326,21 @@ __global__ void __launch_bounds__(D * 4) carve_fwd_kernel(FwdArgs a) {
           Pkeep[slot] = accP;
         }
       }
-      f32x4 XK[NB], XQ[NB];
-      for (int ti = 0; ti < NB; ++ti) {
-        f32x4 ak = zero4(), aq = zero4();
-        for (int ks = 0; ks < D / KS; ++ks) {
-          const int kofs = ks * KS + g * KPL;
-          const typename M::frag sb = M::load(sS + (16 * w + c) * D + kofs);
-          const float* sc = sBase + ti * D + kofs;
-          ak = M::mma(M::load_scaled(sK + (16 * ti + c) * D + kofs, sc), sb, ak);
-          aq = M::mma(M::load_scaled(sQ + (16 * ti + c) * D + kofs, sc), sb, aq);
+      f32x4 XK[CPW][NB], XQ[CPW][NB];
+      for (int cq = 0; cq < CPW; ++cq) {
+        const int ct = w * CPW + cq;
+        for (int ti = 0; ti < NB; ++ti) {
+          f32x4 ak = zero4(), aq = zero4();
+          for (int ks = 0; ks < D / KS; ++ks) {
+            const int kofs = ks * KS + g * KPL;
+            const typename M::frag sb = M::load(sS + (16 * ct + c) * D + kofs);
+            const float* sc = sBase + ti * D + kofs;
+            ak = M::mma(M::load_scaled(sK + (16 * ti + c) * D + kofs, sc), sb, ak);
+            aq = M::mma(M::load_scaled(sQ + (16 * ti + c) * D + kofs, sc), sb, aq);
+          }
+          XK[cq][ti] = ak;
+          XQ[cq][ti] = aq;
         }
-        XK[ti] = ak;
-        XQ[ti] = aq;
       }
       __syncthreads();
       // epilogues into the aliased buffers
@@ -310,27 +368,36 @@ __global__ void __launch_bounds__(D * 4) carve_fwd_kernel(FwdArgs a) {
             sKhT[rr * LK + cc] = (T)0.0f;
           }
         }
-        for (int ti = 0; ti < NB; ++ti) {
-          f32x4 rv;
-          for (int r = 0; r < 4; ++r) {
-            const int t = 16 * ti + 4 * g + r;
-            rv[r] = sBeta[t] * (wv[ti][r] - XK[ti][r]);
+        for (int cq = 0; cq < CPW; ++cq)
+          for (int ti = 0; ti < NB; ++ti) {
+            f32x4 rv;
+            for (int r = 0; r < 4; ++r) rv[r] = sBeta[16 * ti + 4 * g + r] * (wv[cq][ti][r] - XK[cq][ti][r]);
+            store_tile_t(sRT, LK, 16 * ti, 16 * (w * CPW + cq), rv, lane);
           }
-          store_tile_t(sRT, LK, 16 * ti, 16 * w, rv, lane);
-        }
       }
       __syncthreads();
 
       // ---- P6: T = (I + A)^{-1} -----------------------------------------------
       if (w == 0 && g < NB) {
-        // diagonal block g: column c by forward substitution
-        float x[16];
+        // diagonal block g: column c by forward substitution, A rows in registers
         const float* Ab = sA + (16 * g) * LW + 16 * g;
+        float arow[16][16];
+#pragma unroll
+        for (int t = 1; t < 16; ++t)
+#pragma unroll
+          for (int s4 = 0; s4 < (t + 3) / 4; ++s4) {
+            const f32x4 v4 = *reinterpret_cast<const f32x4*>(Ab + t * LW + 4 * s4);
+            arow[t][4 * s4] = v4[0];
+            arow[t][4 * s4 + 1] = v4[1];
+            arow[t][4 * s4 + 2] = v4[2];
+            arow[t][4 * s4 + 3] = v4[3];
+          }
+        float x[16];
 #pragma unroll
         for (int t = 0; t < 16; ++t) {
           float acc = (t == c) ? 1.0f : 0.0f;
 #pragma unroll
-          for (int s = 0; s < t; ++s) acc -= Ab[t * LW + s] * x[s];
+          for (int s = 0; s < t; ++s) acc -= arow[t][s] * x[s];
           x[t] = acc;
         }
         float* Aw = sA + (16 * g) * LW + 16 * g;
@@ -368,46 +435,59 @@ __global__ void __launch_bounds__(D * 4) carve_fwd_kernel(FwdArgs a) {
       }
 
       // ---- P7: u = T R -> sUT -----------------------------------------------
-      for (int ti = 0; ti < NB; ++ti) {
-        f32x4 acc = zero4();
-        const int kmax = (16 * (ti + 1) + KS - 1) / KS;
-        for (int ks = 0; ks < kmax; ++ks) {
-          const int kofs = ks * KS + g * KPL;
-          acc = M::mma(M::load(sTb + (16 * ti + c) * LK + kofs), M::load(sRT + (16 * w + c) * LK + kofs), acc);
+      for (int cq = 0; cq < CPW; ++cq) {
+        const int ct = w * CPW + cq;
+        for (int ti = 0; ti < NB; ++ti) {
+          f32x4 acc = zero4();
+          const int kmax = (16 * (ti + 1) + KS - 1) / KS;
+          for (int ks = 0; ks < kmax; ++ks) {
+            const int kofs = ks * KS + g * KPL;
+            acc = M::mma(M::load(sTb + (16 * ti + c) * LK + kofs), M::load(sRT + (16 * ct + c) * LK + kofs), acc);
+          }
+          store_tile_t(sUT, LK, 16 * ti, 16 * ct, acc, lane);
         }
-        store_tile_t(sUT, LK, 16 * ti, 16 * w, acc, lane);
       }
       __syncthreads();
 
       // ---- P8: outputs and state carry --------------------------------------
-      for (int ti = 0; ti < NB; ++ti) {
-        f32x4 acc = XQ[ti];
-        const int kmax = (16 * (ti + 1) + KS - 1) / KS;
-        for (int ks = 0; ks < kmax; ++ks) {
-          const int kofs = ks * KS + g * KPL;
-          acc = M::mma(M::load(sP + (16 * ti + c) * LK + kofs), M::load(sUT + (16 * w + c) * LK + kofs), acc);
-        }
-        for (int r = 0; r < 4; ++r) {
-          const int t = 16 * ti + 4 * g + r;
-          o[(tokbase + (size_t)t * H) * D + 16 * w + c] = (T)acc[r];
+      for (int cq = 0; cq < CPW; ++cq) {
+        const int ct = w * CPW + cq;
+        for (int ti = 0; ti < NB; ++ti) {
+          f32x4 acc = XQ[cq][ti];
+          const int kmax = (16 * (ti + 1) + KS - 1) / KS;
+          for (int ks = 0; ks < kmax; ++ks) {
+            const int kofs = ks * KS + g * KPL;
+            acc = M::mma(M::load(sP + (16 * ti + c) * LK + kofs), M::load(sUT + (16 * ct + c) * LK + kofs), acc);
+          }
+          for (int r = 0; r < 4; ++r) {
+            const int t = 16 * ti + 4 * g + r;
+            o[(tokbase + (size_t)t * H) * D + 16 * ct + c] = (T)acc[r];
+          }
         }
       }
-      for (int it = 0; it < NIT; ++it) {
-        f32x4 acc;
-        for (int r = 0; r < 4; ++r) acc[r] = S[it][r] * gamma_col;
-        for (int ks = 0; ks < LK / KS; ++ks) {
-          const int kofs = ks * KS + g * KPL;
-          acc = M::mma(M::load(sUT + (16 * it + c) * LK + kofs), M::load(sKhT + (16 * w + c) * LK + kofs), acc);
+      for (int cq = 0; cq < CPW; ++cq) {
+        const int ct = w * CPW + cq;
+        for (int it = 0; it < NIT; ++it) {
+          f32x4 acc;
+          for (int r = 0; r < 4; ++r) acc[r] = S[cq][it][r] * gamma_col[cq];
+          for (int ks = 0; ks < LK / KS; ++ks) {
+            const int kofs = ks * KS + g * KPL;
+            acc = M::mma(M::load(sUT + (16 * it + c) * LK + kofs), M::load(sKhT + (16 * ct + c) * LK + kofs), acc);
+          }
+          S[cq][it] = acc;
         }
-        S[it] = acc;
-        store_tile(sS, D, 16 * it, 16 * w, acc, lane);
       }
-      __syncthreads();
+      __syncthreads();  // every wave is done reading sS (P5) and the aliases
+      for (int cq = 0; cq < CPW; ++cq)
+        for (int it = 0; it < NIT; ++it) store_tile(sS, D, 16 * it, 16 * (w * CPW + cq), S[cq][it], lane);
     }
   }
   if (a.S_T) {
-    for (int it = 0; it < NIT; ++it)
-      for (int r = 0; r < 4; ++r) a.S_T[soff + (size_t)(16 * it + 4 * g + r) * D + 16 * w + c] = S[it][r];
+    for (int cq = 0; cq < CPW; ++cq) {
+      const int col = 16 * (w * CPW + cq) + c;
+      for (int it = 0; it < NIT; ++it)
+        for (int r = 0; r < 4; ++r) a.S_T[soff + (size_t)(16 * it + 4 * g + r) * D + col] = S[cq][it][r];
+    }
   }
 }
 
@@ -425,7 +505,7 @@ static int launch_fwd_t(const FwdArgs& a, hipStream_t stream) {
       return CARVE_ERR_HIP;
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(D * 4), lay.total, stream, a);
+  hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(fwd_threads(D)), lay.total, stream, a);
   return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
 }
 

@@ -16,8 +16,11 @@ struct FwdArgs {
 };
 
 struct FwdLds {
-  size_t S, Q, K, Ki, F, Tau, KhT, A, Base, Cf, Beta, total;
+  size_t S, Q, K, Ki, F, Tau, KhT, A, Base, Cf, Beta, Ucat, Vb, Vw, total;
 };
+
+// threads of a forward workgroup: up to four waves (one per SIMD)
+__host__ __device__ constexpr int fwd_threads(int D) { return (D / 16 < 4 ? D / 16 : 4) * 64; }
 
 __host__ __device__ constexpr size_t lds_round(size_t x) { return (x + 15) & ~(size_t)15; }
 __host__ __device__ constexpr size_t lds_max(size_t a, size_t b) { return a > b ? a : b; }
@@ -47,6 +50,9 @@ __host__ __device__ constexpr FwdLds fwd_lds(int RP) {
   l.Base = off; off += lds_round((size_t)NB * D * 4);
   l.Cf = off;   off += lds_round((size_t)NB * NB * D * 4);
   l.Beta = off; off += lds_round((size_t)LW * 4);
+  l.Ucat = off; off += lds_round((size_t)2 * RP * D * e);
+  l.Vb = off;   off += lds_round((size_t)D * RP * e);
+  l.Vw = off;   off += lds_round((size_t)D * RP * e);
   l.total = off;
   return l;
 }
