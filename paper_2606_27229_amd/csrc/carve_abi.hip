@@ -12,6 +12,29 @@ constexpr size_t kMaxLds = 160 * 1024;
 
 int round_rp(int R) { return (R + 31) / 32 * 32; }
 
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// backward workspace: per-(b,h) parameter partials | WY-tile start states |
+// packed [Ub; Uw] | its transpose
+struct BwdWs {
+  size_t part, substates, up, ut, total;
+};
+
+BwdWs bwd_workspace_layout(const carve_dims_t* d, int lw) {
+  BwdWs l{};
+  const size_t nbh = (size_t)d->B * d->H;
+  const size_t es = d->dtype == CARVE_BF16 ? 2 : 4;
+  const size_t R2 = 2 * (size_t)round_rp(d->R);
+  const int msub = d->L / lw;
+  size_t off = 0;
+  l.part = off;      off += align256(nbh * part_floats(d->R, d->Dk) * 4);
+  l.substates = off; off += msub > 1 ? align256(nbh * (size_t)msub * d->Dv * d->Dk * 4) : 0;
+  l.up = off;        off += align256(R2 * d->Dk * es);
+  l.ut = off;        off += align256(R2 * d->Dk * es);
+  l.total = off;
+  return l;
+}
+
 size_t esize(carve_dtype_t dt) { return dt == CARVE_BF16 ? 2 : 4; }
 
 int check_dims(const carve_dims_t* d) {
@@ -85,11 +108,7 @@ size_t carve_workspace_size(const carve_dims_t* d, int for_backward) {
   if (!for_backward) return 0;
   const int lw = pick_lw(d, true);
   if (!lw) return 0;
-  const size_t nbh = (size_t)d->B * d->H;
-  size_t bytes = nbh * part_floats(d->R, d->Dk) * 4;
-  const int msub = d->L / lw;
-  if (msub > 1) bytes += nbh * (size_t)msub * d->Dv * d->Dk * 4;
-  return (bytes + 255) & ~(size_t)255;
+  return bwd_workspace_layout(d, lw).total;
 }
 
 int carve_chunk_fwd(const carve_dims_t* d, const void* q, const void* k, const void* v,
@@ -164,9 +183,13 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
   a.g = g; a.Ub = Ub; a.Uw = Uw; a.Vb = Vb; a.Vw = Vw; a.S_chunks = S_chunks;
   a.dO = dO; a.dS_T = dS_T;
   a.dq = dq; a.dk = dk; a.dv = dv; a.dbeta = dbeta; a.dbx = dbx; a.dwx = dwx; a.dg = dg; a.dS0 = dS0;
-  a.part = reinterpret_cast<float*>(workspace);
+  const BwdWs wl = bwd_workspace_layout(d, lw);
+  char* wsb = reinterpret_cast<char*>(workspace);
+  a.part = reinterpret_cast<float*>(wsb + wl.part);
+  a.substates = (d->L / lw > 1) ? reinterpret_cast<float*>(wsb + wl.substates) : nullptr;
+  a.Up = wsb + wl.up;
+  a.UT = wsb + wl.ut;
   const size_t nbh = (size_t)d->B * d->H;
-  a.substates = (d->L / lw > 1) ? a.part + nbh * part_floats(d->R, d->Dk) : nullptr;
   a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = round_rp(d->R); a.L = d->L;
   st = launch_bwd(a, d->dtype, d->Dk, lw, stream);
   if (st) return st;

@@ -133,20 +133,65 @@ __device__ __forceinline__ f32x4 mma_regB(f32x4 acc, const T* a_row, const f32x4
   return acc;
 }
 
-template <typename T, int D>
-__global__ void __launch_bounds__(D * 4) carve_bwd_kernel(BwdArgs a) {
+// Column c of (I + A)^{-1} for a 16x16 strictly lower A (row stride lda) by
+// forward substitution; the rows of A are read one ahead of their use.
+__device__ __forceinline__ void unit_lower_inverse_column(const float* A, int lda, int c, float* x) {
+  f32x4 cur[4], nxt[4];
+#pragma unroll
+  for (int s4 = 0; s4 < 4; ++s4) cur[s4] = *reinterpret_cast<const f32x4*>(A + 1 * lda + 4 * s4);
+  x[0] = (c == 0) ? 1.0f : 0.0f;
+#pragma unroll
+  for (int t = 1; t < 16; ++t) {
+    if (t + 1 < 16) {
+#pragma unroll
+      for (int s4 = 0; s4 < 4; ++s4) nxt[s4] = *reinterpret_cast<const f32x4*>(A + (t + 1) * lda + 4 * s4);
+    }
+    float acc = (t == c) ? 1.0f : 0.0f;
+#pragma unroll
+    for (int s = 0; s < t; ++s) acc -= cur[s >> 2][s & 3] * x[s];
+    x[t] = acc;
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) cur[s4] = nxt[s4];
+  }
+}
+
+// Pack [Ub; Uw] once per call into the workspace, zero padded to RP rows per
+// half, in both orientations: Up [2RP][D] and UT [D][2RP] (token dtype).
+template <typename T>
+__global__ void carve_pack_u_kernel(const float* __restrict__ Ub, const float* __restrict__ Uw, int R, int RP,
+                                    int D, T* __restrict__ Up, T* __restrict__ UT) {
+  const int x = blockIdx.x * blockDim.x + threadIdx.x;
+  const int R2 = 2 * RP;
+  if (x >= R2 * D) return;
+  const int rr = x / D, i = x % D;
+  float u = 0.0f;
+  if (rr < R) u = Ub[(size_t)rr * D + i];
+  else if (rr >= RP && rr < RP + R) u = Uw[(size_t)(rr - RP) * D + i];
+  Up[x] = (T)u;
+  UT[(size_t)i * R2 + rr] = (T)u;
+}
+
+template <typename T, int D, int RP>
+__global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
   typedef Mma<T> M;
-  constexpr int NW = D / 16;
-  constexpr int NT = NW * 64;
+  constexpr int NT = bwd_threads(D);
+  constexpr int NW = NT / 64;
+  constexpr int NCT = D / 16;
+  constexpr int CPW = NCT / NW;       // column tiles per wave
   constexpr int NIT = D / 16;
   constexpr int KS = M::KS, KPL = M::KPL;
-  const int RP = a.RP, R2 = 2 * a.RP, R = a.R;
+  constexpr int R2 = 2 * RP;
+  constexpr int NRT = R2 / 16;        // 16-row tiles of [Ub; Uw]
+  constexpr int NVT = RP / 16;        // 16-column tiles of Vb / Vw
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int NQV = (BLW * D / VEC + NT - 1) / NT;
+  constexpr int NGT = (2 * NVT + NW - 1) / NW;  // dtau tiles per wave
+  const int R = a.R;
   const int H = a.H, Tn = a.T, L = a.L;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
   const int bh = blockIdx.x, b = bh / H, h = bh % H;
   const int nch = Tn / L, msub = L / BLW;
-  const int jj = 16 * w + c;  // this lane's key column / value column
 
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const BwdLds lay = bwd_lds<T, D>(RP);
@@ -196,541 +241,669 @@ __global__ void __launch_bounds__(D * 4) carve_bwd_kernel(BwdArgs a) {
   const T* __restrict__ wx = reinterpret_cast<const T*>(a.wx);
   const T* __restrict__ beta = reinterpret_cast<const T*>(a.beta);
   const T* __restrict__ dO = reinterpret_cast<const T*>(a.dO);
-  T* __restrict__ dq = reinterpret_cast<T*>(a.dq);
-  T* __restrict__ dk = reinterpret_cast<T*>(a.dk);
-  T* __restrict__ dv = reinterpret_cast<T*>(a.dv);
-  T* __restrict__ dbeta = reinterpret_cast<T*>(a.dbeta);
-  T* __restrict__ dbx = reinterpret_cast<T*>(a.dbx);
-  T* __restrict__ dwx = reinterpret_cast<T*>(a.dwx);
-
+  const T* __restrict__ Up = reinterpret_cast<const T*>(a.Up);
+  const T* __restrict__ UT = reinterpret_cast<const T*>(a.UT);
+  // token tensors addressed from this (batch, head)'s first element with 32-bit
+  // offsets t * rs + column (rs = H * D elements between consecutive tokens)
+  const size_t bh0 = ((size_t)b * Tn * H + h) * D;
+  const size_t bh1 = (size_t)b * Tn * H + h;
+  const int rs = H * D;
+  q += bh0; k += bh0; v += bh0; bx += bh0; wx += bh0; dO += bh0; beta += bh1;
+  const float* __restrict__ gl = a.g + bh0;
+  float* __restrict__ dgo = a.dg + bh0;
+  T* __restrict__ dq = reinterpret_cast<T*>(a.dq) + bh0;
+  T* __restrict__ dk = reinterpret_cast<T*>(a.dk) + bh0;
+  T* __restrict__ dv = reinterpret_cast<T*>(a.dv) + bh0;
+  T* __restrict__ dbeta = reinterpret_cast<T*>(a.dbeta) + bh1;
+  T* __restrict__ dbx = reinterpret_cast<T*>(a.dbx) + bh0;
+  T* __restrict__ dwx = reinterpret_cast<T*>(a.dwx) + bh0;
   const size_t soff = (size_t)bh * D * D;
-  float* part = a.part + (size_t)bh * part_floats(R, D);
-  float* pUb = part;
-  float* pUw = part + (size_t)R * D;
-  float* pVb = part + (size_t)2 * R * D;
-  float* pVw = part + (size_t)3 * R * D;
-  // clear the dUcat entries this lane accumulates at every chunk start
-  for (int rt = 0; rt < R2 / 16; ++rt)
-    for (int r = 0; r < 4; ++r) {
-      const int rr = 16 * rt + 4 * g + r;
-      if (rr < R) pUb[(size_t)rr * D + jj] = 0.0f;
-      else if (rr >= RP && rr < RP + R) pUw[(size_t)(rr - RP) * D + jj] = 0.0f;
-    }
 
-  f32x4 S[NIT], dS[NIT], dF[8], dVb[4], dVw[4];  // R2/16 <= 8, RP/16 <= 4
-  for (int it = 0; it < NIT; ++it)
-    for (int r = 0; r < 4; ++r)
-      dS[it][r] = a.dS_T ? a.dS_T[soff + (size_t)(16 * it + 4 * g + r) * D + jj] : 0.0f;
-  for (int x = 0; x < 4; ++x) {
-    dVb[x] = zero4();
-    dVw[x] = zero4();
+  // ---- constant operand fragments of Vb, Vw -------------------------------------
+  // z = x + tau V^T: B[k = r][n = j] = V[j][r]  (per owned column tile, RP/KS steps)
+  typename M::frag fVb[CPW][RP / KS], fVw[CPW][RP / KS];
+  for (int cq = 0; cq < CPW; ++cq) {
+    const int col = 16 * (w * CPW + cq) + c;
+    for (int ks = 0; ks < RP / KS; ++ks) {
+      float vb[KPL], vw[KPL];
+      for (int e = 0; e < KPL; ++e) {
+        const int rr = ks * KS + g * KPL + e;
+        vb[e] = rr < R ? a.Vb[(size_t)col * R + rr] : 0.0f;
+        vw[e] = rr < R ? a.Vw[(size_t)col * R + rr] : 0.0f;
+      }
+      fVb[cq][ks] = M::from_f32(vb);
+      fVw[cq][ks] = M::from_f32(vw);
+    }
+  }
+  // dtau = dz V: B[k = j][n = r] = V[j][r] for the dtau tiles this wave owns
+  typename M::frag fVt[NGT][D / KS];
+  for (int gi = 0; gi < NGT; ++gi) {
+    const int x = w + gi * NW;
+    const int half = x / NVT, rt = x % NVT;
+    const float* Vm = half ? a.Vw : a.Vb;
+    const int col = 16 * rt + c;
+    for (int ks = 0; ks < D / KS; ++ks) {
+      float vb[KPL];
+      for (int e = 0; e < KPL; ++e) {
+        const int j = ks * KS + g * KPL + e;
+        vb[e] = (x < 2 * NVT && col < R) ? Vm[(size_t)j * R + col] : 0.0f;
+      }
+      fVt[gi][ks] = M::from_f32(vb);
+    }
   }
 
-  for (int ch = nch - 1; ch >= 0; --ch) {
-    const float* Shat = a.S_chunks + ((size_t)bh * nch + ch) * D * D;
+  // ---- persistent registers --------------------------------------------------------
+  // S[cq][it][r] = S[16 it + 4g + r][16(w CPW + cq) + c] (tile start state), dS the
+  // gradient of the tile end state, dF the fold gradient of the current chunk,
+  // dU / dVb / dVw this (batch, head)'s parameter-gradient partials.
+  f32x4 S[CPW][NIT], dS[CPW][NIT], dF[CPW][NRT], dU[CPW][NRT], dVb[CPW][NVT], dVw[CPW][NVT];
+  for (int cq = 0; cq < CPW; ++cq) {
+    const int col = 16 * (w * CPW + cq) + c;
     for (int it = 0; it < NIT; ++it)
-      for (int r = 0; r < 4; ++r) S[it][r] = Shat[(size_t)(16 * it + 4 * g + r) * D + jj];
-    for (int x = 0; x < 8; ++x) dF[x] = zero4();
-    // fold F = [Ub; Uw] S_hat -> sF [R2][D]
-    __syncthreads();
-    for (int rt = 0; rt < R2 / 16; ++rt) {
-      const int rr = 16 * rt + c;
-      const float* urow = nullptr;
-      if (rr < R) urow = a.Ub + (size_t)rr * D;
-      else if (rr >= RP && rr < RP + R) urow = a.Uw + (size_t)(rr - RP) * D;
-      f32x4 acc = zero4();
-      if constexpr (KPL == 8) {
-        for (int ks = 0; ks < D / 32; ++ks) {
-          typename M::frag af, bfg;
-          const int i0 = 32 * ks + 4 * g;
-          for (int e = 0; e < 4; ++e) {
-            af[e] = (T)S[2 * ks][e];
-            af[4 + e] = (T)S[2 * ks + 1][e];
-            bfg[e] = (T)(urow ? urow[i0 + e] : 0.0f);
-            bfg[4 + e] = (T)(urow ? urow[i0 + 16 + e] : 0.0f);
-          }
-          acc = M::mma(af, bfg, acc);
-        }
-      } else {
-        for (int it = 0; it < NIT; ++it)
-          for (int r4 = 0; r4 < 4; ++r4) {
-            const float bv = urow ? urow[16 * it + 4 * g + r4] : 0.0f;
-            acc = M::mma((T)S[it][r4], (T)bv, acc);
-          }
+      for (int r = 0; r < 4; ++r) {
+        const size_t e = soff + (size_t)(16 * it + 4 * g + r) * D + col;
+        dS[cq][it][r] = a.dS_T ? a.dS_T[e] : 0.0f;
+        S[cq][it][r] = a.S_chunks[((size_t)bh * nch + nch - 1) * D * D + (16 * it + 4 * g + r) * D + col];
       }
-      store_tile_t(sF, D, 16 * w, 16 * rt, acc, lane);
+    for (int x = 0; x < NRT; ++x) dU[cq][x] = zero4();
+    for (int x = 0; x < NVT; ++x) {
+      dVb[cq][x] = zero4();
+      dVw[cq][x] = zero4();
+    }
+  }
+
+  // ---- per-tile input prefetch ----------------------------------------------------
+  f32x4 pq[NQV], pk[NQV], pdo[NQV];
+  float cq_[CPW][4], ck_[CPW][4], cbx[CPW][4], cg[CPW][4], cwx[CPW][4], cv[CPW][4];
+  float pbeta = 0.0f;
+#define CARVE_BWD_PREFETCH(T0_, WANT_DO_)                                                \
+  do {                                                                                   \
+    const int t0_ = (T0_);                                                               \
+    for (int u = 0; u < NQV; ++u) {                                                      \
+      const int x = tid + u * NT;                                                        \
+      if ((BLW * D / VEC) % NT != 0 && x >= BLW * D / VEC) break;                        \
+      const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;                            \
+      const int gofs = (t0_ + t) * rs + j;                                               \
+      pq[u] = *reinterpret_cast<const f32x4*>(q + gofs);                                 \
+      pk[u] = *reinterpret_cast<const f32x4*>(k + gofs);                                 \
+      if (WANT_DO_) pdo[u] = *reinterpret_cast<const f32x4*>(dO + gofs);                 \
+    }                                                                                    \
+    if (tid < BLW) pbeta = to_f(beta[(t0_ + tid) * H]);                                  \
+    for (int cq = 0; cq < CPW; ++cq) {                                                   \
+      const int col_ = 16 * (w * CPW + cq) + c;                                          \
+      for (int r = 0; r < 4; ++r) {                                                      \
+        const int e_ = (t0_ + 4 * g + r) * rs + col_;                                    \
+        cq_[cq][r] = to_f(q[e_]);                                                        \
+        ck_[cq][r] = to_f(k[e_]);                                                        \
+        cbx[cq][r] = to_f(bx[e_]);                                                       \
+        cg[cq][r] = gl[e_];                                                              \
+        cwx[cq][r] = to_f(wx[e_]);                                                       \
+        cv[cq][r] = to_f(v[e_]);                                                         \
+      }                                                                                  \
+    }                                                                                    \
+  } while (0)
+
+  // the tile steps of a chunk: forward tiles 0..msub-2 (recompute the tile start
+  // states), then backward tiles msub-1..0
+  const int nsteps = 2 * msub - 1;
+#define CARVE_STEP_IS_BWD(ST_) ((ST_) >= msub - 1)
+#define CARVE_STEP_TILE(ST_) (CARVE_STEP_IS_BWD(ST_) ? (2 * msub - 2 - (ST_)) : (ST_))
+  CARVE_BWD_PREFETCH((nch - 1) * L + CARVE_STEP_TILE(0) * BLW, CARVE_STEP_IS_BWD(0));
+
+  for (int ch = nch - 1; ch >= 0; --ch) {
+    for (int cq = 0; cq < CPW; ++cq)
+      for (int x = 0; x < NRT; ++x) dF[cq][x] = zero4();
+    __syncthreads();
+    // ---- fold F = [Ub; Uw] S_hat -> sF [R2][D] (S holds S_hat here) -------------
+    for (int cq = 0; cq < CPW; ++cq) {
+      const int ct = w * CPW + cq;
+      typename M::frag sa[NIT / 2 > 0 ? NIT / 2 : 1];
+      if constexpr (KPL == 8)
+        for (int ks = 0; ks < NIT / 2; ++ks)
+          for (int e = 0; e < 4; ++e) {
+            sa[ks][e] = (T)S[cq][2 * ks][e];
+            sa[ks][4 + e] = (T)S[cq][2 * ks + 1][e];
+          }
+      for (int rt = 0; rt < NRT; ++rt) {
+        const T* urow = Up + (size_t)(16 * rt + c) * D;
+        f32x4 acc = zero4();
+        if constexpr (KPL == 8) {
+          for (int ks = 0; ks < D / 32; ++ks) {
+            typename M::frag bfg;
+            const T* p = urow + 32 * ks + 4 * g;
+            const bf16x4 lo = *reinterpret_cast<const bf16x4*>(p);
+            const bf16x4 hi = *reinterpret_cast<const bf16x4*>(p + 16);
+            for (int e = 0; e < 4; ++e) {
+              bfg[e] = lo[e];
+              bfg[4 + e] = hi[e];
+            }
+            acc = M::mma(sa[ks], bfg, acc);
+          }
+        } else {
+          for (int it = 0; it < NIT; ++it)
+            for (int r4 = 0; r4 < 4; ++r4) acc = M::mma(S[cq][it][r4], urow[16 * it + 4 * g + r4], acc);
+        }
+        store_tile_t(sF, D, 16 * ct, 16 * rt, acc, lane);
+      }
     }
 
-    // pass 0: forward tiles 0..msub-2 recompute the tile start states;
-    // pass 1: backward tiles msub-1..0
-    for (int pass = (msub > 1 ? 0 : 1); pass < 2; ++pass) {
-      const bool bwd = pass == 1;
-      const int mcount = bwd ? msub : msub - 1;
-      for (int mi = 0; mi < mcount; ++mi) {
-        const int m = bwd ? (msub - 1 - mi) : mi;
-        const int t0 = ch * L + m * BLW;
-        const size_t tokbase = ((size_t)b * Tn + t0) * H + h;
-        if (bwd && msub > 1) {
-          const float* src = (m == 0) ? Shat : a.substates + ((size_t)bh * msub + m) * D * D;
-          for (int it = 0; it < NIT; ++it)
-            for (int r = 0; r < 4; ++r) S[it][r] = src[(size_t)(16 * it + 4 * g + r) * D + jj];
-        }
-        __syncthreads();  // previous users of the transient buffers are done
-        // ---- B0: loads --------------------------------------------------------
-        {
-          constexpr int VEC = 16 / sizeof(T);
-          constexpr int NV = BLW * D / VEC;
-          for (int x = tid; x < NV; x += NT) {
-            const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;
-            const size_t gofs = (tokbase + (size_t)t * H) * D + j;
-            *reinterpret_cast<f32x4*>(sQ + t * D + j) = *reinterpret_cast<const f32x4*>(q + gofs);
-            *reinterpret_cast<f32x4*>(sK + t * D + j) = *reinterpret_cast<const f32x4*>(k + gofs);
-            if (bwd) {
-              const f32x4 raw = *reinterpret_cast<const f32x4*>(dO + gofs);
-              *reinterpret_cast<f32x4*>(sdO + t * D + j) = raw;
-              const T* rv = reinterpret_cast<const T*>(&raw);
-              for (int e = 0; e < VEC; ++e) sdOT[(j + e) * BLW + t] = rv[e];
-            }
-          }
-          if (tid < BLW) sBeta[tid] = to_f(beta[tokbase + (size_t)tid * H]);
-          for (int it = 0; it < NIT; ++it) {
-            store_tile(sS, D, 16 * it, 16 * w, S[it], lane);
-            if (bwd) store_tile(sdS, D, 16 * it, 16 * w, dS[it], lane);
-          }
-        }
-        __syncthreads();
-        // ---- R1: tau = tanh(Q F^T) --------------------------------------------
-        for (int rt = w; rt < R2 / 16; rt += NW) {
-          f32x4 acc = zero4();
-          for (int ks = 0; ks < D / KS; ++ks) {
-            const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load(sQ + c * D + kofs), M::load(sF + (16 * rt + c) * D + kofs), acc);
-          }
-          for (int r = 0; r < 4; ++r) acc[r] = tanh_f(acc[r]);
-          store_tile(sTau, R2, 0, 16 * rt, acc, lane);
-        }
-        __syncthreads();
-        // ---- R2: gates and retention factors ------------------------------------
-        float qv[4], kv[4], E[4], Ep[4], en[4], bgt[4], wgt[4], vv[4], wv[4];
-        float gam;
-        {
-          f32x4 accB = zero4(), accW = zero4();
-          for (int ks = 0; ks < RP / KS; ++ks) {
-            const int r0 = ks * KS + g * KPL;
-            float vb[KPL], vw[KPL];
-            for (int e = 0; e < KPL; ++e) {
-              const int rr = r0 + e;
-              vb[e] = rr < R ? a.Vb[(size_t)jj * R + rr] : 0.0f;
-              vw[e] = rr < R ? a.Vw[(size_t)jj * R + rr] : 0.0f;
-            }
-            accB = M::mma(M::load(sTau + c * R2 + r0), M::from_f32(vb), accB);
-            accW = M::mma(M::load(sTau + c * R2 + RP + r0), M::from_f32(vw), accW);
-          }
-          float p[4];
-          for (int r = 0; r < 4; ++r) {
-            const int t = 4 * g + r;
-            const size_t e = (tokbase + (size_t)t * H) * D + jj;
-            const float zb = to_f(bx[e]) + accB[r];
-            p[r] = a.g[e] - softplus_f(zb);
-            bgt[r] = sigmoid_f(zb);
-            wgt[r] = sigmoid_f(to_f(wx[e]) + accW[r]);
-            vv[r] = to_f(v[e]);
-            wv[r] = wgt[r] * vv[r];
-            qv[r] = to_f(sQ[t * D + jj]);
-            kv[r] = to_f(sK[t * D + jj]);
-          }
-          p[1] += p[0];
-          p[2] += p[1];
-          p[3] += p[2];
-          float incl = p[3];
-          float y = __shfl_up(incl, 16);
-          if (g >= 1) incl += y;
-          y = __shfl_up(incl, 32);
-          if (g >= 2) incl += y;
-          const float excl = incl - p[3];
-          const float lam_end = __shfl(incl, 48 + c);
-          for (int r = 0; r < 4; ++r) {
-            const float lam = excl + p[r];
-            E[r] = fast_exp(lam);
-            en[r] = fast_exp(-lam);
-          }
-          const float eprev = __shfl_up(E[3], 16);
-          Ep[0] = g == 0 ? 1.0f : eprev;
-          Ep[1] = E[0];
-          Ep[2] = E[1];
-          Ep[3] = E[2];
-          gam = fast_exp(lam_end);
-          f32x4 vK, vQ, vKi, vKh;
-          for (int r = 0; r < 4; ++r) {
-            const int t = 4 * g + r;
-            vK[r] = kv[r] * Ep[r];
-            vQ[r] = qv[r] * E[r];
-            vKi[r] = kv[r] * en[r];
-            vKh[r] = vKi[r] * gam;
-            sK[t * D + jj] = (T)vK[r];
-            sQ[t * D + jj] = (T)vQ[r];
-            sKi[t * D + jj] = (T)vKi[r];
-          }
-          store_tile_t(sKT, BLW, 0, 16 * w, vK, lane);
-          store_tile_t(sQT, BLW, 0, 16 * w, vQ, lane);
-          store_tile_t(sKiT, BLW, 0, 16 * w, vKi, lane);
-          if (!bwd) store_tile_t(sKhT, BLW, 0, 16 * w, vKh, lane);
-          if (g == 0) sGam[jj] = gam;
-        }
-        __syncthreads();
-        // ---- R3: A, D, P and Ktil S^T --------------------------------------------
-        if (w == 0) {
-          f32x4 accA = zero4(), accP = zero4();
-          for (int ks = 0; ks < D / KS; ++ks) {
-            const int kofs = ks * KS + g * KPL;
-            const typename M::frag kb = M::load(sKi + c * D + kofs);
-            accA = M::mma(M::load(sK + c * D + kofs), kb, accA);
-            accP = M::mma(M::load(sQ + c * D + kofs), kb, accP);
-          }
-          f32x4 pv;
-          for (int r = 0; r < 4; ++r) {
-            const int t = 4 * g + r;
-            const float dval = (c < t) ? accA[r] : 0.0f;
-            sDm[t * BLW + c] = dval;
-            sA[t * BLW + c] = sBeta[t] * dval;
-            pv[r] = (c <= t) ? accP[r] : 0.0f;
-          }
-          store_tile_t(sPT, BLW, 0, 0, pv, lane);
-        }
-        float Eerr[4];
-        {
-          f32x4 acc = zero4();
-          for (int ks = 0; ks < D / KS; ++ks) {
-            const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load(sK + c * D + kofs), M::load(sS + (16 * w + c) * D + kofs), acc);
-          }
-          f32x4 rv;
-          for (int r = 0; r < 4; ++r) {
-            Eerr[r] = wv[r] - acc[r];
-            rv[r] = sBeta[4 * g + r] * Eerr[r];
-          }
-          store_tile_t(sRT, BLW, 0, 16 * w, rv, lane);
-        }
-        __syncthreads();
-        // ---- R4: T = (I + A)^{-1}; du = Khat dS'^T + P^T dO ----------------------
-        if (w == 0 && g == 0) {
-          float x[16];
-#pragma unroll
-          for (int t = 0; t < 16; ++t) {
-            float acc = (t == c) ? 1.0f : 0.0f;
-#pragma unroll
-            for (int s = 0; s < t; ++s) acc -= sA[t * BLW + s] * x[s];
-            x[t] = acc;
-          }
-#pragma unroll
-          for (int t = 0; t < 16; ++t) {
-            sTb[t * BLW + c] = (T)x[t];
-            sTbT[c * BLW + t] = (T)x[t];
-          }
-        }
-        if (bwd) {
-          f32x4 acc = zero4();
-          for (int ks = 0; ks < D / KS; ++ks) {
-            const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load_scaled(sKi + c * D + kofs, sGam + kofs), M::load(sdS + (16 * w + c) * D + kofs), acc);
-          }
-          acc = mma_k16<T>(acc, sPT + c * BLW, sdOT + (16 * w + c) * BLW, g);
-          store_tile_t(sduT, BLW, 0, 16 * w, acc, lane);
-        }
-        __syncthreads();
-        // ---- R5: u = T R; dR = T^T du ---------------------------------------------
-        float dzw[4];
-        {
-          const f32x4 u = mma_k16<T>(zero4(), sTb + c * BLW, sRT + (16 * w + c) * BLW, g);
+    for (int st = 0; st < nsteps; ++st) {
+      const bool bwd = CARVE_STEP_IS_BWD(st);
+      const int m = CARVE_STEP_TILE(st);
+      // re-derive the lane coordinates inside the loop so per-lane addresses are
+      // formed next to their use instead of being hoisted out of the loops
+      int lane_ = threadIdx.x & 63;
+      asm volatile("" : "+v"(lane_));
+      const int g = lane_ >> 4, c = lane_ & 15, lane = lane_;
+      const int t0 = ch * L + m * BLW;
+      __syncthreads();  // previous users of the transient buffers are done
+      // ---- B0: tile inputs from the prefetch registers --------------------------
+      float qv[CPW][4], kv[CPW][4], bxv[CPW][4], gv[CPW][4], wxv[CPW][4], vv[CPW][4];
+      {
+        for (int u = 0; u < NQV; ++u) {
+          const int x = tid + u * NT;
+          if ((BLW * D / VEC) % NT != 0 && x >= BLW * D / VEC) break;
+          const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;
+          *reinterpret_cast<f32x4*>(sQ + t * D + j) = pq[u];
+          *reinterpret_cast<f32x4*>(sK + t * D + j) = pk[u];
           if (bwd) {
-            store_tile(sU, D, 0, 16 * w, u, lane);
-            const f32x4 dR = mma_k16<T>(zero4(), sTbT + c * BLW, sduT + (16 * w + c) * BLW, g);
-            f32x4 dE, dzv;
-            for (int r = 0; r < 4; ++r) {
-              const int t = 4 * g + r;
-              dE[r] = sBeta[t] * dR[r];
-              float db = dR[r] * Eerr[r];
-              db += __shfl_xor(db, 1);
-              db += __shfl_xor(db, 2);
-              db += __shfl_xor(db, 4);
-              db += __shfl_xor(db, 8);
-              if (c == 0) sDb[w * BLW + t] = db;
-              const float dwv = dE[r] * vv[r];
-              const size_t e = (tokbase + (size_t)t * H) * D + jj;
-              dv[e] = (T)(dE[r] * wgt[r]);
-              dzw[r] = dwv * wgt[r] * (1.0f - wgt[r]);
-              dwx[e] = (T)dzw[r];
-              dzv[r] = dzw[r];
-            }
-            store_tile(sdR, D, 0, 16 * w, dR, lane);
-            store_tile(sdE, D, 0, 16 * w, dE, lane);
-            store_tile_t(sdET, BLW, 0, 16 * w, dE, lane);
-            store_tile(sdzw, D, 0, 16 * w, dzv, lane);
-          } else {
-            store_tile_t(sUT, BLW, 0, 16 * w, u, lane);
+            *reinterpret_cast<f32x4*>(sdO + t * D + j) = pdo[u];
+            const T* rv = reinterpret_cast<const T*>(&pdo[u]);
+            for (int e = 0; e < VEC; ++e) sdOT[(j + e) * BLW + t] = rv[e];
           }
         }
-        __syncthreads();
-        if (!bwd) {
-          // forward tile: S <- S diag(gam) + u^T Khat, park it for the backward tiles
-          float* dst = a.substates + ((size_t)bh * msub + m + 1) * D * D;
+        if (tid < BLW) sBeta[tid] = pbeta;
+        for (int cq = 0; cq < CPW; ++cq)
+          for (int r = 0; r < 4; ++r) {
+            qv[cq][r] = cq_[cq][r];
+            kv[cq][r] = ck_[cq][r];
+            bxv[cq][r] = cbx[cq][r];
+            gv[cq][r] = cg[cq][r];
+            wxv[cq][r] = cwx[cq][r];
+            vv[cq][r] = cv[cq][r];
+          }
+        // next tile step (this chunk or the previous one)
+        {
+          int nch_ = ch, nst = st + 1;
+          if (nst == nsteps) { nch_ = ch - 1; nst = 0; }
+          if (nch_ >= 0) CARVE_BWD_PREFETCH(nch_ * L + CARVE_STEP_TILE(nst) * BLW, CARVE_STEP_IS_BWD(nst));
+        }
+        for (int cq = 0; cq < CPW; ++cq)
           for (int it = 0; it < NIT; ++it) {
-            f32x4 acc;
-            for (int r = 0; r < 4; ++r) acc[r] = S[it][r] * gam;
-            acc = mma_k16<T>(acc, sUT + (16 * it + c) * BLW, sKhT + (16 * w + c) * BLW, g);
-            S[it] = acc;
-            for (int r = 0; r < 4; ++r) dst[(size_t)(16 * it + 4 * g + r) * D + jj] = acc[r];
+            store_tile(sS, D, 16 * it, 16 * (w * CPW + cq), S[cq][it], lane);
+            if (bwd) store_tile(sdS, D, 16 * it, 16 * (w * CPW + cq), dS[cq][it], lane);
           }
-          continue;
+      }
+      __syncthreads();
+      // ---- R1: tau = tanh(Q F^T) --------------------------------------------------
+      for (int rt = w; rt < NRT; rt += NW) {
+        f32x4 acc = zero4();
+        for (int ks = 0; ks < D / KS; ++ks) {
+          const int kofs = ks * KS + g * KPL;
+          acc = M::mma(M::load(sQ + c * D + kofs), M::load(sF + (16 * rt + c) * D + kofs), acc);
         }
-        // ---- G3: dKtil = -dE S, dQtil = dO S, dKhat = u dS'; dP, dA -------------
-        f32x4 dKt = mma_regB<T, NIT>(zero4(), sdE + c * D, S, g);
-        for (int r = 0; r < 4; ++r) dKt[r] = -dKt[r];
-        f32x4 dQt = mma_regB<T, NIT>(zero4(), sdO + c * D, S, g);
-        f32x4 dKh = mma_regB<T, NIT>(zero4(), sU + c * D, dS, g);
-        float cs = 0.0f;  // colsum(S * dS') for column jj
-        for (int it = 0; it < NIT; ++it)
-          for (int r = 0; r < 4; ++r) cs += S[it][r] * dS[it][r];
-        cs += __shfl_xor(cs, 16);
-        cs += __shfl_xor(cs, 32);
-        if (w == 0) {
+        for (int r = 0; r < 4; ++r) acc[r] = tanh_f(acc[r]);
+        store_tile(sTau, R2, 0, 16 * rt, acc, lane);
+      }
+      __syncthreads();
+      // ---- R2: gates and retention factors ------------------------------------------
+      float E[CPW][4], Ep[CPW][4], en[CPW][4], bgt[CPW][4], wgt[CPW][4], wv[CPW][4];
+      float gam[CPW];
+      for (int cq = 0; cq < CPW; ++cq) {
+        const int ct = w * CPW + cq;
+        const int jj = 16 * ct + c;
+        f32x4 accB = zero4(), accW = zero4();
+        for (int ks = 0; ks < RP / KS; ++ks) {
+          const int r0 = ks * KS + g * KPL;
+          accB = M::mma(M::load(sTau + c * R2 + r0), fVb[cq][ks], accB);
+          accW = M::mma(M::load(sTau + c * R2 + RP + r0), fVw[cq][ks], accW);
+        }
+        float p[4];
+        for (int r = 0; r < 4; ++r) {
+          const float zb = bxv[cq][r] + accB[r];
+          p[r] = gv[cq][r] - softplus_f(zb);
+          bgt[cq][r] = sigmoid_f(zb);
+          wgt[cq][r] = sigmoid_f(wxv[cq][r] + accW[r]);
+          wv[cq][r] = wgt[cq][r] * vv[cq][r];
+        }
+        p[1] += p[0];
+        p[2] += p[1];
+        p[3] += p[2];
+        float incl = p[3];
+        float y = __shfl_up(incl, 16);
+        if (g >= 1) incl += y;
+        y = __shfl_up(incl, 32);
+        if (g >= 2) incl += y;
+        const float excl = incl - p[3];
+        const float lam_end = __shfl(incl, 48 + c);
+        for (int r = 0; r < 4; ++r) {
+          const float lam = excl + p[r];
+          E[cq][r] = fast_exp(lam);
+          en[cq][r] = fast_exp(-lam);
+        }
+        const float eprev = __shfl_up(E[cq][3], 16);
+        Ep[cq][0] = g == 0 ? 1.0f : eprev;
+        Ep[cq][1] = E[cq][0];
+        Ep[cq][2] = E[cq][1];
+        Ep[cq][3] = E[cq][2];
+        gam[cq] = fast_exp(lam_end);
+        f32x4 vK, vQ, vKi, vKh;
+        for (int r = 0; r < 4; ++r) {
+          const int t = 4 * g + r;
+          vK[r] = kv[cq][r] * Ep[cq][r];
+          vQ[r] = qv[cq][r] * E[cq][r];
+          vKi[r] = kv[cq][r] * en[cq][r];
+          vKh[r] = vKi[r] * gam[cq];
+          sK[t * D + jj] = (T)vK[r];
+          sQ[t * D + jj] = (T)vQ[r];
+          sKi[t * D + jj] = (T)vKi[r];
+        }
+        store_tile_t(sKT, BLW, 0, 16 * ct, vK, lane);
+        store_tile_t(sQT, BLW, 0, 16 * ct, vQ, lane);
+        store_tile_t(sKiT, BLW, 0, 16 * ct, vKi, lane);
+        if (!bwd) store_tile_t(sKhT, BLW, 0, 16 * ct, vKh, lane);
+        if (g == 0) sGam[jj] = gam[cq];
+      }
+      __syncthreads();
+      // ---- R3: A, D, P and Ktil S^T ------------------------------------------------
+      if (w == 0) {
+        f32x4 accA = zero4(), accP = zero4();
+        for (int ks = 0; ks < D / KS; ++ks) {
+          const int kofs = ks * KS + g * KPL;
+          const typename M::frag kb = M::load(sKi + c * D + kofs);
+          accA = M::mma(M::load(sK + c * D + kofs), kb, accA);
+          accP = M::mma(M::load(sQ + c * D + kofs), kb, accP);
+        }
+        f32x4 pv;
+        for (int r = 0; r < 4; ++r) {
+          const int t = 4 * g + r;
+          const float dval = (c < t) ? accA[r] : 0.0f;
+          sDm[t * BLW + c] = dval;
+          sA[t * BLW + c] = sBeta[t] * dval;
+          pv[r] = (c <= t) ? accP[r] : 0.0f;
+        }
+        store_tile_t(sPT, BLW, 0, 0, pv, lane);
+      }
+      float Eerr[CPW][4];
+      for (int cq = 0; cq < CPW; ++cq) {
+        const int ct = w * CPW + cq;
+        f32x4 acc = zero4();
+        for (int ks = 0; ks < D / KS; ++ks) {
+          const int kofs = ks * KS + g * KPL;
+          acc = M::mma(M::load(sK + c * D + kofs), M::load(sS + (16 * ct + c) * D + kofs), acc);
+        }
+        f32x4 rv;
+        for (int r = 0; r < 4; ++r) {
+          Eerr[cq][r] = wv[cq][r] - acc[r];
+          rv[r] = sBeta[4 * g + r] * Eerr[cq][r];
+        }
+        store_tile_t(sRT, BLW, 0, 16 * ct, rv, lane);
+      }
+      __syncthreads();
+      // ---- R4: T = (I + A)^{-1}; du = Khat dS'^T + P^T dO ------------------------------
+      if (w == 0 && g == 0) {
+        float x[16];
+        unit_lower_inverse_column(sA, BLW, c, x);
+#pragma unroll
+        for (int t = 0; t < 16; ++t) {
+          sTb[t * BLW + c] = (T)x[t];
+          sTbT[c * BLW + t] = (T)x[t];
+        }
+      }
+      if (bwd) {
+        for (int cq = 0; cq < CPW; ++cq) {
+          const int ct = w * CPW + cq;
           f32x4 acc = zero4();
           for (int ks = 0; ks < D / KS; ++ks) {
             const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load(sdO + c * D + kofs), M::load(sU + c * D + kofs), acc);
+            acc = M::mma(M::load_scaled(sKi + c * D + kofs, sGam + kofs), M::load(sdS + (16 * ct + c) * D + kofs), acc);
           }
-          for (int r = 0; r < 4; ++r) acc[r] = (c <= 4 * g + r) ? acc[r] : 0.0f;
-          store_tile(sdP, BLW, 0, 0, acc, lane);
-          store_tile_t(sdPT, BLW, 0, 0, acc, lane);
+          acc = mma_k16<T>(acc, sPT + c * BLW, sdOT + (16 * ct + c) * BLW, g);
+          store_tile_t(sduT, BLW, 0, 16 * ct, acc, lane);
         }
-        if (w == (NW > 1 ? 1 : 0)) {
-          f32x4 acc = zero4();
-          for (int ks = 0; ks < D / KS; ++ks) {
-            const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load(sdR + c * D + kofs), M::load(sU + c * D + kofs), acc);
-          }
-          f32x4 ddv;
+      }
+      __syncthreads();
+      // ---- R5: u = T R; dR = T^T du ---------------------------------------------------
+      float dzw[CPW][4];
+      for (int cq = 0; cq < CPW; ++cq) {
+        const int ct = w * CPW + cq;
+        const int jj = 16 * ct + c;
+        const f32x4 u = mma_k16<T>(zero4(), sTb + c * BLW, sRT + (16 * ct + c) * BLW, g);
+        if (bwd) {
+          store_tile(sU, D, 0, 16 * ct, u, lane);
+          const f32x4 dR = mma_k16<T>(zero4(), sTbT + c * BLW, sduT + (16 * ct + c) * BLW, g);
+          f32x4 dE, dzv;
           for (int r = 0; r < 4; ++r) {
             const int t = 4 * g + r;
-            const float dA = (c < t) ? -acc[r] : 0.0f;
-            ddv[r] = sBeta[t] * dA;
-            float db = dA * sDm[t * BLW + c];
+            dE[r] = sBeta[t] * dR[r];
+            float db = dR[r] * Eerr[cq][r];
             db += __shfl_xor(db, 1);
             db += __shfl_xor(db, 2);
             db += __shfl_xor(db, 4);
             db += __shfl_xor(db, 8);
-            if (c == 0) sDb2[t] = db;
+            if (c == 0) sDb[ct * BLW + t] = db;
+            const float dwv = dE[r] * vv[cq][r];
+            const int e = (t0 + t) * rs + jj;
+            dv[e] = (T)(dE[r] * wgt[cq][r]);
+            dzw[cq][r] = dwv * wgt[cq][r] * (1.0f - wgt[cq][r]);
+            dwx[e] = (T)dzw[cq][r];
+            dzv[r] = dzw[cq][r];
           }
-          store_tile(sdD, BLW, 0, 0, ddv, lane);
-          store_tile_t(sdDT, BLW, 0, 0, ddv, lane);
+          store_tile(sdR, D, 0, 16 * ct, dR, lane);
+          store_tile(sdE, D, 0, 16 * ct, dE, lane);
+          store_tile_t(sdET, BLW, 0, 16 * ct, dE, lane);
+          store_tile(sdzw, D, 0, 16 * ct, dzv, lane);
+        } else {
+          store_tile_t(sUT, BLW, 0, 16 * ct, u, lane);
         }
-        __syncthreads();
-        // ---- G5: factored-pair gradients, dLam, gate-logit gradients -------------
-        float dqv[4], dkv[4];
-        {
-          const f32x4 dAq = mma_k16<T>(zero4(), sdD + c * BLW, sKiT + (16 * w + c) * BLW, g);
-          const f32x4 dPq = mma_k16<T>(zero4(), sdP + c * BLW, sKiT + (16 * w + c) * BLW, g);
-          f32x4 dcol = mma_k16<T>(zero4(), sdDT + c * BLW, sKT + (16 * w + c) * BLW, g);
-          dcol = mma_k16<T>(dcol, sdPT + c * BLW, sQT + (16 * w + c) * BLW, g);
-          float aL[4], pL[4], xs = 0.0f;
-          for (int r = 0; r < 4; ++r) {
-            const float gq = dQt[r] * E[r] + E[r] * dPq[r];          // dq from Qtil and P
-            const float gkh = dKh[r] * gam * en[r];                  // dk from Khat
-            const float gkc = en[r] * dcol[r];                       // dk from the column side
-            const float gkr = dKt[r] * Ep[r] + Ep[r] * dAq[r];       // dk from Ktil and the row side of A
-            dqv[r] = gq;
-            dkv[r] = gkr + gkh + gkc;
-            aL[r] = qv[r] * gq - kv[r] * gkc - kv[r] * gkh;
-            pL[r] = kv[r] * gkr;
-            xs += kv[r] * gkh;
-          }
-          xs += __shfl_xor(xs, 16);
-          xs += __shfl_xor(xs, 32);
-          if (g == 3) aL[3] += xs + cs * gam;
-          const float pnext = __shfl_down(pL[0], 16);
-          float dLam[4];
-          dLam[0] = aL[0] + pL[1];
-          dLam[1] = aL[1] + pL[2];
-          dLam[2] = aL[2] + pL[3];
-          dLam[3] = aL[3] + (g < 3 ? pnext : 0.0f);
-          // reverse prefix sums over the 16 rows
-          float sfx[4];
-          sfx[3] = dLam[3];
-          sfx[2] = sfx[3] + dLam[2];
-          sfx[1] = sfx[2] + dLam[1];
-          sfx[0] = sfx[1] + dLam[0];
-          float tot = sfx[0];
-          float z = __shfl_down(tot, 16);
-          if (g <= 2) tot += z;
-          z = __shfl_down(tot, 32);
-          if (g <= 1) tot += z;
-          const float after = tot - sfx[0];  // sum over the rows of later lane groups
-          f32x4 dzb;
-          for (int r = 0; r < 4; ++r) {
-            const int t = 4 * g + r;
-            const float dl = sfx[r] + after;
-            const size_t e = (tokbase + (size_t)t * H) * D + jj;
-            a.dg[e] = dl;
-            dzb[r] = -dl * bgt[r];
-            dbx[e] = (T)dzb[r];
-          }
-          store_tile(sdzb, D, 0, 16 * w, dzb, lane);
-          // dVb += dz_b^T tau_b, dVw += dz_w^T tau_w (A from registers, K = 16 tokens)
-          for (int rt = 0; rt < RP / 16; ++rt) {
-            if constexpr (sizeof(T) == 2) {
-              typename M::frag ab, aw, bb, bw;
-              for (int e = 0; e < 4; ++e) {
-                ab[e] = (T)dzb[e];
-                aw[e] = (T)dzw[e];
-                bb[e] = sTau[(4 * g + e) * R2 + 16 * rt + c];
-                bw[e] = sTau[(4 * g + e) * R2 + RP + 16 * rt + c];
-                ab[4 + e] = (T)0.0f;
-                aw[4 + e] = (T)0.0f;
-                bb[4 + e] = (T)0.0f;
-                bw[4 + e] = (T)0.0f;
-              }
-              dVb[rt] = M::mma(ab, bb, dVb[rt]);
-              dVw[rt] = M::mma(aw, bw, dVw[rt]);
-            } else {
-              for (int r = 0; r < 4; ++r) {
-                dVb[rt] = M::mma(dzb[r], sTau[(4 * g + r) * R2 + 16 * rt + c], dVb[rt]);
-                dVw[rt] = M::mma(dzw[r], sTau[(4 * g + r) * R2 + RP + 16 * rt + c], dVw[rt]);
-              }
-            }
-          }
-        }
-        __syncthreads();
-        // ---- G8: dtau = dz V, dY = dtau (1 - tau^2) ------------------------------
-        for (int x = w; x < 2 * (RP / 16); x += NW) {
-          const int half = x / (RP / 16), rt = x % (RP / 16);
-          const T* arow = (half ? sdzw : sdzb) + c * D;
-          const float* Vm = half ? a.Vw : a.Vb;
-          const int col = 16 * rt + c;  // column of V this lane supplies
-          f32x4 acc = zero4();
-          for (int ks = 0; ks < D / KS; ++ks) {
-            const int j0 = ks * KS + g * KPL;
-            float vb[KPL];
-            for (int e = 0; e < KPL; ++e) vb[e] = col < R ? Vm[(size_t)(j0 + e) * R + col] : 0.0f;
-            acc = M::mma(M::load(arow + j0), M::from_f32(vb), acc);
-          }
-          f32x4 dy;
-          for (int r = 0; r < 4; ++r) {
-            const float tv = to_f(sTau[(4 * g + r) * R2 + half * RP + 16 * rt + c]);
-            dy[r] = acc[r] * (1.0f - tv * tv);
-          }
-          store_tile(sdY, R2, 0, half * RP + 16 * rt, dy, lane);
-          store_tile_t(sdYT, BLW, 0, half * RP + 16 * rt, dy, lane);
-        }
-        __syncthreads();
-        // ---- G9: dq += dY F, outputs, dF += dY^T q, dS <- ... ---------------------
-        {
-          f32x4 acc = zero4();
-          for (int ks = 0; ks < R2 / KS; ++ks) {
-            const int r0 = ks * KS + g * KPL;
-            typename M::frag bfg;
-            if constexpr (KPL == 8) {
-              for (int e = 0; e < 8; ++e) bfg[e] = sF[(r0 + e) * D + jj];
-            } else {
-              bfg = sF[r0 * D + jj];
-            }
-            acc = M::mma(M::load(sdY + c * R2 + r0), bfg, acc);
-          }
-          for (int r = 0; r < 4; ++r) {
-            const int t = 4 * g + r;
-            const size_t e = (tokbase + (size_t)t * H) * D + jj;
-            dq[e] = (T)(dqv[r] + acc[r]);
-            dk[e] = (T)dkv[r];
-          }
-          if (w == 0 && lane < BLW) {
-            float db = sDb2[lane];
-            for (int x = 0; x < NW; ++x) db += sDb[x * BLW + lane];
-            dbeta[tokbase + (size_t)lane * H] = (T)db;
-          }
-          for (int rt = 0; rt < R2 / 16; ++rt) {
-            if constexpr (sizeof(T) == 2) {
-              typename M::frag af, bfg;
-              for (int e = 0; e < 4; ++e) {
-                af[e] = sdYT[(16 * rt + c) * BLW + 4 * g + e];
-                bfg[e] = (T)qv[e];
-                af[4 + e] = (T)0.0f;
-                bfg[4 + e] = (T)0.0f;
-              }
-              dF[rt] = M::mma(af, bfg, dF[rt]);
-            } else {
-              for (int r = 0; r < 4; ++r) dF[rt] = M::mma(sdYT[(16 * rt + c) * BLW + 4 * g + r], qv[r], dF[rt]);
-            }
-          }
+      }
+      __syncthreads();
+      if (!bwd) {
+        // forward tile: S <- S diag(gam) + u^T Khat, park it for the backward tiles
+        f32x4* dst = reinterpret_cast<f32x4*>(a.substates + ((size_t)bh * msub + m + 1) * D * D) + (size_t)tid * CPW * NIT;
+        for (int cq = 0; cq < CPW; ++cq) {
+          const int ct = w * CPW + cq;
           for (int it = 0; it < NIT; ++it) {
-            f32x4 acc1, acc2;
-            for (int r = 0; r < 4; ++r) acc1[r] = dS[it][r] * gam;
-            acc1 = mma_k16<T>(acc1, sdOT + (16 * it + c) * BLW, sQT + (16 * w + c) * BLW, g);
-            acc2 = mma_k16<T>(zero4(), sdET + (16 * it + c) * BLW, sKT + (16 * w + c) * BLW, g);
-            for (int r = 0; r < 4; ++r) dS[it][r] = acc1[r] - acc2[r];
+            f32x4 acc;
+            for (int r = 0; r < 4; ++r) acc[r] = S[cq][it][r] * gam[cq];
+            acc = mma_k16<T>(acc, sUT + (16 * it + c) * BLW, sKhT + (16 * ct + c) * BLW, g);
+            S[cq][it] = acc;
+            if (m + 1 < msub - 1) dst[cq * NIT + it] = acc;  // the last one stays in registers
           }
         }
-      }  // tiles
-    }    // passes
+        continue;
+      }
+      // ---- G3: dKtil = -dE S, dQtil = dO S, dKhat = u dS'; dP, dA -------------------
+      f32x4 dKt[CPW], dQt[CPW], dKh[CPW];
+      float cs[CPW];
+      for (int cq = 0; cq < CPW; ++cq) {
+        dKt[cq] = mma_regB<T, NIT>(zero4(), sdE + c * D, S[cq], g);
+        for (int r = 0; r < 4; ++r) dKt[cq][r] = -dKt[cq][r];
+        dQt[cq] = mma_regB<T, NIT>(zero4(), sdO + c * D, S[cq], g);
+        dKh[cq] = mma_regB<T, NIT>(zero4(), sU + c * D, dS[cq], g);
+        float s_ = 0.0f;  // colsum(S * dS') for this column
+        for (int it = 0; it < NIT; ++it)
+          for (int r = 0; r < 4; ++r) s_ += S[cq][it][r] * dS[cq][it][r];
+        s_ += __shfl_xor(s_, 16);
+        s_ += __shfl_xor(s_, 32);
+        cs[cq] = s_;
+      }
+      // S is dead for this tile: fetch the start state of the next backward tile
+      {
+        const float* src = nullptr;
+        bool lane_major = false;
+        if (m > 0) {
+          if (m - 1 == 0) src = a.S_chunks + ((size_t)bh * nch + ch) * D * D;
+          else {
+            src = a.substates + ((size_t)bh * msub + m - 1) * D * D;
+            lane_major = true;
+          }
+        } else if (ch > 0) {
+          src = a.S_chunks + ((size_t)bh * nch + ch - 1) * D * D;
+        }
+        if (src) {
+          if (lane_major) {
+            const f32x4* sp = reinterpret_cast<const f32x4*>(src) + (size_t)tid * CPW * NIT;
+            for (int cq = 0; cq < CPW; ++cq)
+              for (int it = 0; it < NIT; ++it) S[cq][it] = sp[cq * NIT + it];
+          } else {
+            for (int cq = 0; cq < CPW; ++cq) {
+              const int col = 16 * (w * CPW + cq) + c;
+              for (int it = 0; it < NIT; ++it)
+                for (int r = 0; r < 4; ++r) S[cq][it][r] = src[(size_t)(16 * it + 4 * g + r) * D + col];
+            }
+          }
+        }
+      }
+      if (w == 0) {
+        f32x4 acc = zero4();
+        for (int ks = 0; ks < D / KS; ++ks) {
+          const int kofs = ks * KS + g * KPL;
+          acc = M::mma(M::load(sdO + c * D + kofs), M::load(sU + c * D + kofs), acc);
+        }
+        for (int r = 0; r < 4; ++r) acc[r] = (c <= 4 * g + r) ? acc[r] : 0.0f;
+        store_tile(sdP, BLW, 0, 0, acc, lane);
+        store_tile_t(sdPT, BLW, 0, 0, acc, lane);
+      }
+      if (w == (NW > 1 ? 1 : 0)) {
+        f32x4 acc = zero4();
+        for (int ks = 0; ks < D / KS; ++ks) {
+          const int kofs = ks * KS + g * KPL;
+          acc = M::mma(M::load(sdR + c * D + kofs), M::load(sU + c * D + kofs), acc);
+        }
+        f32x4 ddv;
+        for (int r = 0; r < 4; ++r) {
+          const int t = 4 * g + r;
+          const float dA = (c < t) ? -acc[r] : 0.0f;
+          ddv[r] = sBeta[t] * dA;
+          float db = dA * sDm[t * BLW + c];
+          db += __shfl_xor(db, 1);
+          db += __shfl_xor(db, 2);
+          db += __shfl_xor(db, 4);
+          db += __shfl_xor(db, 8);
+          if (c == 0) sDb2[t] = db;
+        }
+        store_tile(sdD, BLW, 0, 0, ddv, lane);
+        store_tile_t(sdDT, BLW, 0, 0, ddv, lane);
+      }
+      __syncthreads();
+      // ---- G5: factored-pair gradients, dLam, gate-logit gradients -----------------
+      float dqv[CPW][4], dkv[CPW][4], dzb[CPW][4];
+      for (int cq = 0; cq < CPW; ++cq) {
+        const int ct = w * CPW + cq;
+        const int jj = 16 * ct + c;
+        const f32x4 dAq = mma_k16<T>(zero4(), sdD + c * BLW, sKiT + (16 * ct + c) * BLW, g);
+        const f32x4 dPq = mma_k16<T>(zero4(), sdP + c * BLW, sKiT + (16 * ct + c) * BLW, g);
+        f32x4 dcol = mma_k16<T>(zero4(), sdDT + c * BLW, sKT + (16 * ct + c) * BLW, g);
+        dcol = mma_k16<T>(dcol, sdPT + c * BLW, sQT + (16 * ct + c) * BLW, g);
+        float aL[4], pL[4], xs = 0.0f;
+        for (int r = 0; r < 4; ++r) {
+          const float gq = dQt[cq][r] * E[cq][r] + E[cq][r] * dPq[r];   // dq from Qtil and P
+          const float gkh = dKh[cq][r] * gam[cq] * en[cq][r];           // dk from Khat
+          const float gkc = en[cq][r] * dcol[r];                        // dk from the column side
+          const float gkr = dKt[cq][r] * Ep[cq][r] + Ep[cq][r] * dAq[r];  // dk from Ktil and A's row side
+          dqv[cq][r] = gq;
+          dkv[cq][r] = gkr + gkh + gkc;
+          aL[r] = qv[cq][r] * gq - kv[cq][r] * gkc - kv[cq][r] * gkh;
+          pL[r] = kv[cq][r] * gkr;
+          xs += kv[cq][r] * gkh;
+        }
+        xs += __shfl_xor(xs, 16);
+        xs += __shfl_xor(xs, 32);
+        if (g == 3) aL[3] += xs + cs[cq] * gam[cq];
+        const float pnext = __shfl_down(pL[0], 16);
+        float dLam[4];
+        dLam[0] = aL[0] + pL[1];
+        dLam[1] = aL[1] + pL[2];
+        dLam[2] = aL[2] + pL[3];
+        dLam[3] = aL[3] + (g < 3 ? pnext : 0.0f);
+        float sfx[4];
+        sfx[3] = dLam[3];
+        sfx[2] = sfx[3] + dLam[2];
+        sfx[1] = sfx[2] + dLam[1];
+        sfx[0] = sfx[1] + dLam[0];
+        float tot = sfx[0];
+        float z = __shfl_down(tot, 16);
+        if (g <= 2) tot += z;
+        z = __shfl_down(tot, 32);
+        if (g <= 1) tot += z;
+        const float after = tot - sfx[0];
+        f32x4 dzv;
+        for (int r = 0; r < 4; ++r) {
+          const int t = 4 * g + r;
+          const float dl = sfx[r] + after;
+          const int e = (t0 + t) * rs + jj;
+          dgo[e] = dl;
+          dzb[cq][r] = -dl * bgt[cq][r];
+          dbx[e] = (T)dzb[cq][r];
+          dzv[r] = dzb[cq][r];
+        }
+        store_tile(sdzb, D, 0, 16 * ct, dzv, lane);
+        // dVb += dz_b^T tau_b, dVw += dz_w^T tau_w (A from registers, K = 16 tokens)
+        for (int rt = 0; rt < NVT; ++rt) {
+          if constexpr (sizeof(T) == 2) {
+            typename M::frag ab, aw, bb, bw;
+            for (int e = 0; e < 4; ++e) {
+              ab[e] = (T)dzb[cq][e];
+              aw[e] = (T)dzw[cq][e];
+              bb[e] = sTau[(4 * g + e) * R2 + 16 * rt + c];
+              bw[e] = sTau[(4 * g + e) * R2 + RP + 16 * rt + c];
+              ab[4 + e] = (T)0.0f;
+              aw[4 + e] = (T)0.0f;
+              bb[4 + e] = (T)0.0f;
+              bw[4 + e] = (T)0.0f;
+            }
+            dVb[cq][rt] = M::mma(ab, bb, dVb[cq][rt]);
+            dVw[cq][rt] = M::mma(aw, bw, dVw[cq][rt]);
+          } else {
+            for (int r = 0; r < 4; ++r) {
+              dVb[cq][rt] = M::mma(dzb[cq][r], sTau[(4 * g + r) * R2 + 16 * rt + c], dVb[cq][rt]);
+              dVw[cq][rt] = M::mma(dzw[cq][r], sTau[(4 * g + r) * R2 + RP + 16 * rt + c], dVw[cq][rt]);
+            }
+          }
+        }
+      }
+      __syncthreads();
+      // ---- G8: dtau = dz V, dY = dtau (1 - tau^2) ------------------------------------
+      for (int gi = 0; gi < NGT; ++gi) {
+        const int x = w + gi * NW;
+        if (x >= 2 * NVT) break;
+        const int half = x / NVT, rt = x % NVT;
+        const T* arow = (half ? sdzw : sdzb) + c * D;
+        f32x4 acc = zero4();
+        for (int ks = 0; ks < D / KS; ++ks) acc = M::mma(M::load(arow + ks * KS + g * KPL), fVt[gi][ks], acc);
+        f32x4 dy;
+        for (int r = 0; r < 4; ++r) {
+          const float tv = to_f(sTau[(4 * g + r) * R2 + half * RP + 16 * rt + c]);
+          dy[r] = acc[r] * (1.0f - tv * tv);
+        }
+        store_tile(sdY, R2, 0, half * RP + 16 * rt, dy, lane);
+        store_tile_t(sdYT, BLW, 0, half * RP + 16 * rt, dy, lane);
+      }
+      __syncthreads();
+      // ---- G9: dq += dY F, outputs, dF += dY^T q, dS <- ... -----------------------------
+      for (int cq = 0; cq < CPW; ++cq) {
+        const int ct = w * CPW + cq;
+        const int jj = 16 * ct + c;
+        f32x4 acc = zero4();
+        for (int ks = 0; ks < R2 / KS; ++ks) {
+          const int r0 = ks * KS + g * KPL;
+          typename M::frag bfg;
+          if constexpr (KPL == 8) {
+            for (int e = 0; e < 8; ++e) bfg[e] = sF[(r0 + e) * D + jj];
+          } else {
+            bfg = sF[r0 * D + jj];
+          }
+          acc = M::mma(M::load(sdY + c * R2 + r0), bfg, acc);
+        }
+        for (int r = 0; r < 4; ++r) {
+          const int t = 4 * g + r;
+          const int e = (t0 + t) * rs + jj;
+          dq[e] = (T)(dqv[cq][r] + acc[r]);
+          dk[e] = (T)dkv[cq][r];
+        }
+        for (int rt = 0; rt < NRT; ++rt) {
+          if constexpr (sizeof(T) == 2) {
+            typename M::frag af, bfg;
+            for (int e = 0; e < 4; ++e) {
+              af[e] = sdYT[(16 * rt + c) * BLW + 4 * g + e];
+              bfg[e] = (T)qv[cq][e];
+              af[4 + e] = (T)0.0f;
+              bfg[4 + e] = (T)0.0f;
+            }
+            dF[cq][rt] = M::mma(af, bfg, dF[cq][rt]);
+          } else {
+            for (int r = 0; r < 4; ++r)
+              dF[cq][rt] = M::mma(sdYT[(16 * rt + c) * BLW + 4 * g + r], qv[cq][r], dF[cq][rt]);
+          }
+        }
+        for (int it = 0; it < NIT; ++it) {
+          f32x4 acc1, acc2;
+          for (int r = 0; r < 4; ++r) acc1[r] = dS[cq][it][r] * gam[cq];
+          acc1 = mma_k16<T>(acc1, sdOT + (16 * it + c) * BLW, sQT + (16 * ct + c) * BLW, g);
+          acc2 = mma_k16<T>(zero4(), sdET + (16 * it + c) * BLW, sKT + (16 * ct + c) * BLW, g);
+          for (int r = 0; r < 4; ++r) dS[cq][it][r] = acc1[r] - acc2[r];
+        }
+      }
+      if (w == 0 && lane < BLW) {
+        float db = sDb2[lane];
+        for (int x = 0; x < NCT; ++x) db += sDb[x * BLW + lane];
+        dbeta[(t0 + lane) * H] = (T)db;
+      }
+    }  // tile steps
 
-    // ---- chunk start: glue through the folded read-out ------------------------
+    // ---- chunk start: glue through the folded read-out ------------------------------
     __syncthreads();
-    for (int rt = 0; rt < R2 / 16; ++rt) store_tile(sdF, D, 16 * rt, 16 * w, dF[rt], lane);
+    for (int cq = 0; cq < CPW; ++cq)
+      for (int rt = 0; rt < NRT; ++rt) store_tile(sdF, D, 16 * rt, 16 * (w * CPW + cq), dF[cq][rt], lane);
     // dS += [Ub;Uw]^T dF  (contraction over the rows of dF, held in registers)
-    for (int it = 0; it < NIT; ++it) {
-      f32x4 acc = dS[it];
-      const int ii = 16 * it + c;  // value row this lane supplies as A
-      if constexpr (KPL == 8) {
-        for (int ks = 0; ks < R2 / 32; ++ks) {
-          typename M::frag af, bfg;
-          for (int e = 0; e < 8; ++e) {
-            const int rr = 32 * ks + (e < 4 ? 4 * g + e : 16 + 4 * g + e - 4);
-            float uv = 0.0f;
-            if (rr < R) uv = a.Ub[(size_t)rr * D + ii];
-            else if (rr >= RP && rr < RP + R) uv = a.Uw[(size_t)(rr - RP) * D + ii];
-            af[e] = (T)uv;
-            bfg[e] = (T)(e < 4 ? dF[2 * ks][e] : dF[2 * ks + 1][e - 4]);
+    for (int cq = 0; cq < CPW; ++cq)
+      for (int it = 0; it < NIT; ++it) {
+        f32x4 acc = dS[cq][it];
+        const T* urow = UT + (size_t)(16 * it + c) * R2;  // value row this lane supplies as A
+        if constexpr (KPL == 8) {
+          for (int ks = 0; ks < R2 / 32; ++ks) {
+            typename M::frag af, bfg;
+            const bf16x4 lo = *reinterpret_cast<const bf16x4*>(urow + 32 * ks + 4 * g);
+            const bf16x4 hi = *reinterpret_cast<const bf16x4*>(urow + 32 * ks + 16 + 4 * g);
+            for (int e = 0; e < 4; ++e) {
+              af[e] = lo[e];
+              af[4 + e] = hi[e];
+              bfg[e] = (T)dF[cq][2 * ks][e];
+              bfg[4 + e] = (T)dF[cq][2 * ks + 1][e];
+            }
+            acc = M::mma(af, bfg, acc);
           }
-          acc = M::mma(af, bfg, acc);
+        } else {
+          for (int rt = 0; rt < NRT; ++rt)
+            for (int r4 = 0; r4 < 4; ++r4) acc = M::mma(urow[16 * rt + 4 * g + r4], dF[cq][rt][r4], acc);
         }
-      } else {
-        for (int rt = 0; rt < R2 / 16; ++rt)
-          for (int r4 = 0; r4 < 4; ++r4) {
-            const int rr = 16 * rt + 4 * g + r4;
-            float uv = 0.0f;
-            if (rr < R) uv = a.Ub[(size_t)rr * D + ii];
-            else if (rr >= RP && rr < RP + R) uv = a.Uw[(size_t)(rr - RP) * D + ii];
-            acc = M::mma(uv, dF[rt][r4], acc);
-          }
+        dS[cq][it] = acc;
       }
-      dS[it] = acc;
-    }
     __syncthreads();
-    // d[Ub;Uw] += dF S_hat^T  (sS still holds S_hat from the first tile)
-    for (int rt = 0; rt < R2 / 16; ++rt) {
-      f32x4 acc = zero4();
-      for (int ks = 0; ks < D / KS; ++ks) {
-        const int kofs = ks * KS + g * KPL;
-        acc = M::mma(M::load(sdF + (16 * rt + c) * D + kofs), M::load(sS + (16 * w + c) * D + kofs), acc);
-      }
-      for (int r = 0; r < 4; ++r) {
-        const int rr = 16 * rt + 4 * g + r;
-        if (rr < R) pUb[(size_t)rr * D + jj] += acc[r];
-        else if (rr >= RP && rr < RP + R) pUw[(size_t)(rr - RP) * D + jj] += acc[r];
+    // d[Ub;Uw] += dF S_hat^T  (sS still holds S_hat from the chunk's first tile)
+    for (int cq = 0; cq < CPW; ++cq) {
+      const int ct = w * CPW + cq;
+      for (int rt = 0; rt < NRT; ++rt) {
+        f32x4 acc = dU[cq][rt];
+        for (int ks = 0; ks < D / KS; ++ks) {
+          const int kofs = ks * KS + g * KPL;
+          acc = M::mma(M::load(sdF + (16 * rt + c) * D + kofs), M::load(sS + (16 * ct + c) * D + kofs), acc);
+        }
+        dU[cq][rt] = acc;
       }
     }
   }  // chunks
 
   if (a.dS0) {
-    for (int it = 0; it < NIT; ++it)
-      for (int r = 0; r < 4; ++r) a.dS0[soff + (size_t)(16 * it + 4 * g + r) * D + jj] = dS[it][r];
-  }
-  for (int rt = 0; rt < RP / 16; ++rt)
-    for (int r = 0; r < 4; ++r) {
-      const int j = 16 * w + 4 * g + r, col = 16 * rt + c;
-      if (col < R) {
-        pVb[(size_t)j * R + col] = dVb[rt][r];
-        pVw[(size_t)j * R + col] = dVw[rt][r];
-      }
+    for (int cq = 0; cq < CPW; ++cq) {
+      const int col = 16 * (w * CPW + cq) + c;
+      for (int it = 0; it < NIT; ++it)
+        for (int r = 0; r < 4; ++r) a.dS0[soff + (size_t)(16 * it + 4 * g + r) * D + col] = dS[cq][it][r];
     }
+  }
+  float* part = a.part + (size_t)bh * part_floats(R, D);
+  float* pUb = part;
+  float* pUw = part + (size_t)R * D;
+  float* pVb = part + (size_t)2 * R * D;
+  float* pVw = part + (size_t)3 * R * D;
+  for (int cq = 0; cq < CPW; ++cq) {
+    const int ct = w * CPW + cq;
+    for (int rt = 0; rt < NRT; ++rt)
+      for (int r = 0; r < 4; ++r) {
+        const int rr = 16 * rt + 4 * g + r;
+        if (rr < R) pUb[(size_t)rr * D + 16 * ct + c] = dU[cq][rt][r];
+        else if (rr >= RP && rr < RP + R) pUw[(size_t)(rr - RP) * D + 16 * ct + c] = dU[cq][rt][r];
+      }
+    for (int rt = 0; rt < NVT; ++rt)
+      for (int r = 0; r < 4; ++r) {
+        const int j = 16 * ct + 4 * g + r, col = 16 * rt + c;
+        if (col < R) {
+          pVb[(size_t)j * R + col] = dVb[cq][rt][r];
+          pVw[(size_t)j * R + col] = dVw[cq][rt][r];
+        }
+      }
+  }
 }
 
 // Sum the per-(batch, head) partial parameter gradients in a fixed order.
@@ -746,10 +919,10 @@ __global__ void carve_param_reduce_kernel(const float* __restrict__ part, int np
 }
 
 // ---------------------------------------------------------------------------
-template <typename T, int D>
+template <typename T, int D, int RP>
 static int launch_bwd_t(const BwdArgs& a, hipStream_t stream) {
-  const BwdLds lay = bwd_lds<T, D>(a.RP);
-  auto kern = carve_bwd_kernel<T, D>;
+  const BwdLds lay = bwd_lds<T, D>(RP);
+  auto kern = carve_bwd_kernel<T, D, RP>;
   static bool attr_set = false;
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -757,19 +930,30 @@ static int launch_bwd_t(const BwdArgs& a, hipStream_t stream) {
       return CARVE_ERR_HIP;
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(D * 4), lay.total, stream, a);
+  const int n = 2 * RP * D;
+  hipLaunchKernelGGL(carve_pack_u_kernel<T>, dim3((n + 255) / 256), dim3(256), 0, stream, a.Ub, a.Uw, a.R, RP, D,
+                     reinterpret_cast<T*>(const_cast<void*>(a.Up)), reinterpret_cast<T*>(const_cast<void*>(a.UT)));
+  if (hipGetLastError() != hipSuccess) return CARVE_ERR_HIP;
+  hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(bwd_threads(D)), lay.total, stream, a);
   return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
+}
+
+template <typename T, int D>
+static int launch_bwd_r(const BwdArgs& a, hipStream_t s) {
+  if (a.RP == 32) return launch_bwd_t<T, D, 32>(a, s);
+  if (a.RP == 64) return launch_bwd_t<T, D, 64>(a, s);
+  return CARVE_ERR_UNSUPPORTED;
 }
 
 int launch_bwd(const BwdArgs& a, int dtype, int D, int LW, hipStream_t s) {
   if (LW != BLW) return CARVE_ERR_UNSUPPORTED;
   if (dtype == CARVE_BF16) {
-    if (D == 32) return launch_bwd_t<bf16_t, 32>(a, s);
-    if (D == 64) return launch_bwd_t<bf16_t, 64>(a, s);
-    if (D == 128) return launch_bwd_t<bf16_t, 128>(a, s);
+    if (D == 32) return launch_bwd_r<bf16_t, 32>(a, s);
+    if (D == 64) return launch_bwd_r<bf16_t, 64>(a, s);
+    if (D == 128 && a.RP == 32) return launch_bwd_t<bf16_t, 128, 32>(a, s);
   } else {
-    if (D == 32) return launch_bwd_t<float, 32>(a, s);
-    if (D == 64) return launch_bwd_t<float, 64>(a, s);
+    if (D == 32) return launch_bwd_r<float, 32>(a, s);
+    if (D == 64 && a.RP == 32) return launch_bwd_t<float, 64, 32>(a, s);
   }
   return CARVE_ERR_UNSUPPORTED;
 }

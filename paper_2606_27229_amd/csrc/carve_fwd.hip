@@ -83,8 +83,14 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
   const T* __restrict__ bx = reinterpret_cast<const T*>(a.bx);
   const T* __restrict__ wx = reinterpret_cast<const T*>(a.wx);
   const T* __restrict__ beta = reinterpret_cast<const T*>(a.beta);
-  const float* __restrict__ gl = a.g;
-  T* __restrict__ o = reinterpret_cast<T*>(a.o);
+  // token tensors addressed from this (batch, head)'s first element with 32-bit
+  // offsets t * rs + column (rs = H * D elements between consecutive tokens)
+  const size_t bh0 = ((size_t)b * Tn * H + h) * D;
+  const size_t bh1 = (size_t)b * Tn * H + h;
+  const int rs = H * D;
+  q += bh0; k += bh0; v += bh0; bx += bh0; wx += bh0; beta += bh1;
+  const float* __restrict__ gl = a.g + bh0;
+  T* __restrict__ o = reinterpret_cast<T*>(a.o) + bh0;
 
   // ---- shared parameters -> LDS (zero padded to RP) ------------------------
   for (int x = tid; x < R2 * D; x += NT) {
@@ -116,34 +122,36 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
   f32x4 pq[NQV], pk[NQV];
   float pbx[CPW][NB][4], pg[CPW][NB][4], pwx[CPW][NB][4], pv[CPW][NB][4];
   float pbeta = 0.0f;
-  auto prefetch_qk = [&](int tile) {
-    const size_t tb = ((size_t)b * Tn + (size_t)tile * LW) * H + h;
-    for (int u = 0; u < NQV; ++u) {
-      const int x = tid + u * NT;
-      if (NVT % NT != 0 && x >= NVT) break;
-      const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;
-      const size_t gofs = (tb + (size_t)t * H) * D + j;
-      pq[u] = *reinterpret_cast<const f32x4*>(q + gofs);
-      pk[u] = *reinterpret_cast<const f32x4*>(k + gofs);
-    }
-    if (tid < LW) pbeta = to_f(beta[tb + (size_t)tid * H]);
-  };
-  auto prefetch_gates = [&](int tile) {
-    const size_t tb = ((size_t)b * Tn + (size_t)tile * LW) * H + h;
-    for (int cq = 0; cq < CPW; ++cq) {
-      const int col = 16 * (w * CPW + cq) + c;
-      for (int ti = 0; ti < NB; ++ti)
-        for (int r = 0; r < 4; ++r) {
-          const size_t e = (tb + (size_t)(16 * ti + 4 * g + r) * H) * D + col;
-          pbx[cq][ti][r] = to_f(bx[e]);
-          pg[cq][ti][r] = gl[e];
-          pwx[cq][ti][r] = to_f(wx[e]);
-          pv[cq][ti][r] = to_f(v[e]);
-        }
-    }
-  };
-  prefetch_qk(0);
-  prefetch_gates(0);
+#define CARVE_FWD_PREFETCH_QK(TILE_)                                                    \
+  do {                                                                                  \
+    const int tt0_ = (TILE_) * LW;                                                      \
+    for (int u = 0; u < NQV; ++u) {                                                     \
+      const int x = tid + u * NT;                                                       \
+      if (NVT % NT != 0 && x >= NVT) break;                                             \
+      const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;                           \
+      const int gofs = (tt0_ + t) * rs + j;                                             \
+      pq[u] = *reinterpret_cast<const f32x4*>(q + gofs);                                \
+      pk[u] = *reinterpret_cast<const f32x4*>(k + gofs);                                \
+    }                                                                                   \
+    if (tid < LW) pbeta = to_f(beta[(tt0_ + tid) * H]);                                 \
+  } while (0)
+#define CARVE_FWD_PREFETCH_GATES(TILE_)                                                 \
+  do {                                                                                  \
+    const int tt0_ = (TILE_) * LW;                                                      \
+    for (int cq = 0; cq < CPW; ++cq) {                                                  \
+      const int col_ = 16 * (w * CPW + cq) + c;                                         \
+      for (int ti = 0; ti < NB; ++ti)                                                   \
+        for (int r = 0; r < 4; ++r) {                                                   \
+          const int e_ = (tt0_ + 16 * ti + 4 * g + r) * rs + col_;                      \
+          pbx[cq][ti][r] = to_f(bx[e_]);                                                \
+          pg[cq][ti][r] = gl[e_];                                                       \
+          pwx[cq][ti][r] = to_f(wx[e_]);                                                \
+          pv[cq][ti][r] = to_f(v[e_]);                                                  \
+        }                                                                               \
+    }                                                                                   \
+  } while (0)
+  CARVE_FWD_PREFETCH_QK(0);
+  CARVE_FWD_PREFETCH_GATES(0);
 
   for (int ch = 0; ch < nch; ++ch) {
     if (a.S_chunks) {
@@ -157,7 +165,6 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
     for (int m = 0; m < msub; ++m) {
       const int tile = ch * msub + m;
       const int t0 = tile * LW;
-      const size_t tokbase = ((size_t)b * Tn + t0) * H + h;   // token row index of t0
 
       // ---- P0: q, k tiles and beta from the prefetch registers -------------
       for (int u = 0; u < NQV; ++u) {
@@ -168,7 +175,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
         *reinterpret_cast<f32x4*>(sK + t * D + j) = pk[u];
       }
       if (tid < LW) sBeta[tid] = pbeta;
-      if (tile + 1 < ntiles) prefetch_qk(tile + 1);
+      if (tile + 1 < ntiles) CARVE_FWD_PREFETCH_QK(tile + 1);
       // ---- P1: fold F = [Ub;Uw] S_hat from the state registers ---------------
       if (m == 0) {
         for (int cq = 0; cq < CPW; ++cq) {
@@ -237,7 +244,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
           }
         }
       }
-      if (tile + 1 < ntiles) prefetch_gates(tile + 1);
+      if (tile + 1 < ntiles) CARVE_FWD_PREFETCH_GATES(tile + 1);
 
       // ---- P4: key-side retention factors --------------------------------------
       float gamma_col[CPW];  // e^{Lam_{LW-1}} for key column 16(w*CPW+cq) + c
@@ -461,7 +468,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
           }
           for (int r = 0; r < 4; ++r) {
             const int t = 16 * ti + 4 * g + r;
-            o[(tokbase + (size_t)t * H) * D + 16 * ct + c] = (T)acc[r];
+            o[(t0 + t) * rs + 16 * ct + c] = (T)acc[r];
           }
         }
       }

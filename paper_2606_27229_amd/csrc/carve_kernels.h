@@ -21,6 +21,8 @@ struct FwdLds {
 
 // threads of a forward workgroup: up to four waves (one per SIMD)
 __host__ __device__ constexpr int fwd_threads(int D) { return (D / 16 < 4 ? D / 16 : 4) * 64; }
+// threads of a backward workgroup: one wave per 16-column tile of the state
+__host__ __device__ constexpr int bwd_threads(int D) { return (D / 16) * 64; }
 
 __host__ __device__ constexpr size_t lds_round(size_t x) { return (x + 15) & ~(size_t)15; }
 __host__ __device__ constexpr size_t lds_max(size_t a, size_t b) { return a > b ? a : b; }
@@ -72,6 +74,8 @@ struct BwdArgs {
   float* dS0;
   float* part;       // per-(b,h) partial parameter gradients (workspace)
   float* substates;  // per-(b,h) WY-tile start states inside one gate chunk (workspace)
+  const void* Up;    // [2RP][D] packed [Ub; Uw] (token dtype, workspace)
+  const void* UT;    // [D][2RP] its transpose (token dtype, workspace)
   int B, T, H, R, RP, L;
 };
 
