@@ -37,9 +37,13 @@ namespace carve {
 
 constexpr int BLW = 16;  // WY tile of the backward
 
+// Compiler-only fence: keeps the loads of one unrolled iteration from being
+// hoisted above the previous one (bounds the live fragment registers).
+#define CARVE_SEQ() asm volatile("" ::: "memory")
+
 struct BwdLds {
   size_t S, dS, F, Q, K, Ki, QT, KT, KiT, Tau, A, Dm, Tb, TbT, PT, RT, U, UTz, KhTz, dO, dOT, duT,
-      dR, dE, dET, dD, dDT, dP, dPT, dY, dYT, Gam, Beta, Db, Db2, total;
+      dET, Gam, Beta, Db, Db2, total;
 };
 
 template <typename T, int D>
@@ -47,42 +51,38 @@ __host__ __device__ constexpr BwdLds bwd_lds(int RP) {
   BwdLds l{};
   size_t off = 0;
   const size_t e = sizeof(T);
-  const size_t R2 = 2 * (size_t)RP;
-  constexpr size_t LD = (size_t)BLW * D;   // [16][D] or [D][16]
-  constexpr size_t LL = (size_t)BLW * BLW; // [16][16]
-  l.S = off;    off += lds_round((size_t)D * D * e);
-  l.dS = off;   off += lds_round((size_t)D * D * e);
-  l.F = off;    off += lds_round(R2 * D * e);
+  constexpr size_t PAD = 16 / sizeof(T);        // every LDS row is padded by 16 bytes
+  constexpr size_t LDD = D + PAD, LDB = BLW, LDF = BLW + 4;
+  const size_t R2 = 2 * (size_t)RP, LDR = R2 + PAD;
+  constexpr size_t RD = (size_t)BLW * LDD;   // [16][D]
+  constexpr size_t DR = (size_t)D * LDB;     // [D][16]
+  constexpr size_t LL = (size_t)BLW * LDB;   // [16][16]
+  constexpr size_t LLF = (size_t)BLW * LDF;  // [16][16] f32
+  l.S = off;    off += lds_round((size_t)D * LDD * e);
+  l.dS = off;   off += lds_round((size_t)D * LDD * e);
+  l.F = off;    off += lds_round(R2 * LDD * e);
   // transient region; dF (R2 x D) for the parameter product at a chunk start
   // reuses it once the tiles of the chunk are done
-  l.Q = off;    off += lds_round(LD * e);
-  l.K = off;    off += lds_round(LD * e);
-  l.Ki = off;   off += lds_round(LD * e);
-  l.QT = off;   off += lds_round(LD * e);
-  l.KT = off;   off += lds_round(LD * e);
-  l.KiT = off;  off += lds_round(LD * e);
-  l.Tau = off;  off += lds_round((size_t)BLW * R2 * e);
-  l.A = off;    off += lds_round(LL * 4);
-  l.Dm = off;   off += lds_round(LL * 4);
+  l.Q = off;    off += lds_round(RD * e);
+  l.K = off;    off += lds_round(RD * e);
+  l.Ki = off;   off += lds_round(RD * e);
+  l.QT = off;   off += lds_round(DR * e);
+  l.KT = off;   off += lds_round(DR * e);
+  l.KiT = off;  off += lds_round(DR * e);
+  l.Tau = off;  off += lds_round((size_t)BLW * LDR * e);
+  l.A = off;    off += lds_round(LLF * 4);
+  l.Dm = off;   off += lds_round(LLF * 4);
   l.Tb = off;   off += lds_round(LL * e);
   l.TbT = off;  off += lds_round(LL * e);
   l.PT = off;   off += lds_round(LL * e);
-  l.RT = off;   off += lds_round(LD * e);
-  l.U = off;    off += lds_round(LD * e);
-  l.UTz = off;  off += lds_round(LD * e);   // u^T (forward tiles) / dz_b (backward tiles)
-  l.KhTz = off; off += lds_round(LD * e);   // Khat^T (forward tiles) / dz_w (backward tiles)
-  l.dO = off;   off += lds_round(LD * e);
-  l.dOT = off;  off += lds_round(LD * e);
-  l.duT = off;  off += lds_round(LD * e);
-  l.dR = off;   off += lds_round(LD * e);
-  l.dE = off;   off += lds_round(LD * e);
-  l.dET = off;  off += lds_round(LD * e);
-  l.dD = off;   off += lds_round(LL * e);
-  l.dDT = off;  off += lds_round(LL * e);
-  l.dP = off;   off += lds_round(LL * e);
-  l.dPT = off;  off += lds_round(LL * e);
-  l.dY = off;   off += lds_round((size_t)BLW * R2 * e);
-  l.dYT = off;  off += lds_round((size_t)BLW * R2 * e);
+  l.RT = off;   off += lds_max(lds_round(DR * e), lds_round((size_t)BLW * LDR * e) + lds_round(R2 * LDB * e));
+  l.U = off;    off += lds_round(RD * e);
+  l.UTz = off;  off += lds_round(lds_max(DR, RD) * e);   // u^T (forward tiles) / dz_b (backward tiles)
+  l.KhTz = off; off += lds_round(lds_max(DR, RD) * e);   // Khat^T (forward tiles) / dz_w (backward tiles)
+  l.dO = off;   off += lds_round(RD * e);
+  l.dOT = off;  off += lds_round(DR * e);
+  l.duT = off;  off += lds_round(DR * e);
+  l.dET = off;  off += lds_round(DR * e);
   l.Gam = off;  off += lds_round((size_t)D * 4);
   l.Beta = off; off += lds_round((size_t)BLW * 4);
   l.Db = off;   off += lds_round((size_t)(D / 16) * BLW * 4);
@@ -186,6 +186,13 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
   constexpr int VEC = 16 / sizeof(T);
   constexpr int NQV = (BLW * D / VEC + NT - 1) / NT;
   constexpr int NGT = (2 * NVT + NW - 1) / NW;  // dtau tiles per wave
+  // LDS row strides, each row padded by 16 bytes so that the 16 rows read by one
+  // MFMA fragment load fall into distinct banks
+  constexpr int PAD = 16 / sizeof(T);
+  constexpr int LDD = D + PAD;     // rows of D elements
+  constexpr int LDB = BLW;         // rows of 16 tokens (2-way bank conflicts at most)
+  constexpr int LDR = R2 + PAD;    // rows of 2RP elements
+  constexpr int LDF = BLW + 4;     // rows of the f32 16x16 matrices
   const int R = a.R;
   const int H = a.H, Tn = a.T, L = a.L;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -219,15 +226,16 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
   T* sdO = reinterpret_cast<T*>(smem + lay.dO);
   T* sdOT = reinterpret_cast<T*>(smem + lay.dOT);
   T* sduT = reinterpret_cast<T*>(smem + lay.duT);
-  T* sdR = reinterpret_cast<T*>(smem + lay.dR);
-  T* sdE = reinterpret_cast<T*>(smem + lay.dE);
+  T* sdR = sQ;  // alias: Q is dead after R3
+  T* sdE = sK;  // alias: K is dead after R3
   T* sdET = reinterpret_cast<T*>(smem + lay.dET);
-  T* sdD = reinterpret_cast<T*>(smem + lay.dD);
-  T* sdDT = reinterpret_cast<T*>(smem + lay.dDT);
-  T* sdP = reinterpret_cast<T*>(smem + lay.dP);
-  T* sdPT = reinterpret_cast<T*>(smem + lay.dPT);
-  T* sdY = reinterpret_cast<T*>(smem + lay.dY);
-  T* sdYT = reinterpret_cast<T*>(smem + lay.dYT);
+  // dD, dD^T, dP, dP^T reuse T, T^T, P^T, A (dead after R5); dY, dY^T reuse R^T
+  T* sdD = sTb;
+  T* sdDT = sTbT;
+  T* sdP = sPT;
+  T* sdPT = reinterpret_cast<T*>(smem + lay.A);
+  T* sdY = sRT;
+  T* sdYT = reinterpret_cast<T*>(smem + lay.RT + lds_round((size_t)BLW * LDR * sizeof(T)));
   float* sGam = reinterpret_cast<float*>(smem + lay.Gam);
   float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);
   float* sDb = reinterpret_cast<float*>(smem + lay.Db);
@@ -314,9 +322,9 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
 
   // ---- per-tile input prefetch ----------------------------------------------------
   f32x4 pq[NQV], pk[NQV], pdo[NQV];
-  float cq_[CPW][4], ck_[CPW][4], cbx[CPW][4], cg[CPW][4], cwx[CPW][4], cv[CPW][4];
+  float cbx[CPW][4], cg[CPW][4], cwx[CPW][4], cv[CPW][4];
   float pbeta = 0.0f;
-#define CARVE_BWD_PREFETCH(T0_, WANT_DO_)                                                \
+#define CARVE_BWD_PREFETCH_VEC(T0_, WANT_DO_)                                            \
   do {                                                                                   \
     const int t0_ = (T0_);                                                               \
     for (int u = 0; u < NQV; ++u) {                                                      \
@@ -329,12 +337,14 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
       if (WANT_DO_) pdo[u] = *reinterpret_cast<const f32x4*>(dO + gofs);                 \
     }                                                                                    \
     if (tid < BLW) pbeta = to_f(beta[(t0_ + tid) * H]);                                  \
+  } while (0)
+#define CARVE_BWD_PREFETCH_GATES(T0_)                                                    \
+  do {                                                                                   \
+    const int t0_ = (T0_);                                                               \
     for (int cq = 0; cq < CPW; ++cq) {                                                   \
       const int col_ = 16 * (w * CPW + cq) + c;                                          \
       for (int r = 0; r < 4; ++r) {                                                      \
         const int e_ = (t0_ + 4 * g + r) * rs + col_;                                    \
-        cq_[cq][r] = to_f(q[e_]);                                                        \
-        ck_[cq][r] = to_f(k[e_]);                                                        \
         cbx[cq][r] = to_f(bx[e_]);                                                       \
         cg[cq][r] = gl[e_];                                                              \
         cwx[cq][r] = to_f(wx[e_]);                                                       \
@@ -348,7 +358,8 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
   const int nsteps = 2 * msub - 1;
 #define CARVE_STEP_IS_BWD(ST_) ((ST_) >= msub - 1)
 #define CARVE_STEP_TILE(ST_) (CARVE_STEP_IS_BWD(ST_) ? (2 * msub - 2 - (ST_)) : (ST_))
-  CARVE_BWD_PREFETCH((nch - 1) * L + CARVE_STEP_TILE(0) * BLW, CARVE_STEP_IS_BWD(0));
+  CARVE_BWD_PREFETCH_VEC((nch - 1) * L + CARVE_STEP_TILE(0) * BLW, CARVE_STEP_IS_BWD(0));
+  CARVE_BWD_PREFETCH_GATES((nch - 1) * L + CARVE_STEP_TILE(0) * BLW);
 
   for (int ch = nch - 1; ch >= 0; --ch) {
     for (int cq = 0; cq < CPW; ++cq)
@@ -365,6 +376,7 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
             sa[ks][4 + e] = (T)S[cq][2 * ks + 1][e];
           }
       for (int rt = 0; rt < NRT; ++rt) {
+        CARVE_SEQ();
         const T* urow = Up + (size_t)(16 * rt + c) * D;
         f32x4 acc = zero4();
         if constexpr (KPL == 8) {
@@ -383,7 +395,7 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
           for (int it = 0; it < NIT; ++it)
             for (int r4 = 0; r4 < 4; ++r4) acc = M::mma(S[cq][it][r4], urow[16 * it + 4 * g + r4], acc);
         }
-        store_tile_t(sF, D, 16 * ct, 16 * rt, acc, lane);
+        store_tile_t(sF, LDD, 16 * ct, 16 * rt, acc, lane);
       }
     }
 
@@ -398,40 +410,32 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
       const int t0 = ch * L + m * BLW;
       __syncthreads();  // previous users of the transient buffers are done
       // ---- B0: tile inputs from the prefetch registers --------------------------
-      float qv[CPW][4], kv[CPW][4], bxv[CPW][4], gv[CPW][4], wxv[CPW][4], vv[CPW][4];
+      // the tile step processed after this one (this chunk or the previous one)
+      int nch_ = ch, nst_ = st + 1;
+      if (nst_ == nsteps) {
+        nch_ = ch - 1;
+        nst_ = 0;
+      }
+      const int nt0 = nch_ * L + CARVE_STEP_TILE(nst_) * BLW;
       {
         for (int u = 0; u < NQV; ++u) {
           const int x = tid + u * NT;
           if ((BLW * D / VEC) % NT != 0 && x >= BLW * D / VEC) break;
           const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;
-          *reinterpret_cast<f32x4*>(sQ + t * D + j) = pq[u];
-          *reinterpret_cast<f32x4*>(sK + t * D + j) = pk[u];
+          *reinterpret_cast<f32x4*>(sQ + t * LDD + j) = pq[u];
+          *reinterpret_cast<f32x4*>(sK + t * LDD + j) = pk[u];
           if (bwd) {
-            *reinterpret_cast<f32x4*>(sdO + t * D + j) = pdo[u];
+            *reinterpret_cast<f32x4*>(sdO + t * LDD + j) = pdo[u];
             const T* rv = reinterpret_cast<const T*>(&pdo[u]);
-            for (int e = 0; e < VEC; ++e) sdOT[(j + e) * BLW + t] = rv[e];
+            for (int e = 0; e < VEC; ++e) sdOT[(j + e) * LDB + t] = rv[e];
           }
         }
         if (tid < BLW) sBeta[tid] = pbeta;
-        for (int cq = 0; cq < CPW; ++cq)
-          for (int r = 0; r < 4; ++r) {
-            qv[cq][r] = cq_[cq][r];
-            kv[cq][r] = ck_[cq][r];
-            bxv[cq][r] = cbx[cq][r];
-            gv[cq][r] = cg[cq][r];
-            wxv[cq][r] = cwx[cq][r];
-            vv[cq][r] = cv[cq][r];
-          }
-        // next tile step (this chunk or the previous one)
-        {
-          int nch_ = ch, nst = st + 1;
-          if (nst == nsteps) { nch_ = ch - 1; nst = 0; }
-          if (nch_ >= 0) CARVE_BWD_PREFETCH(nch_ * L + CARVE_STEP_TILE(nst) * BLW, CARVE_STEP_IS_BWD(nst));
-        }
+        if (nch_ >= 0) CARVE_BWD_PREFETCH_VEC(nt0, CARVE_STEP_IS_BWD(nst_));
         for (int cq = 0; cq < CPW; ++cq)
           for (int it = 0; it < NIT; ++it) {
-            store_tile(sS, D, 16 * it, 16 * (w * CPW + cq), S[cq][it], lane);
-            if (bwd) store_tile(sdS, D, 16 * it, 16 * (w * CPW + cq), dS[cq][it], lane);
+            store_tile(sS, LDD, 16 * it, 16 * (w * CPW + cq), S[cq][it], lane);
+            if (bwd) store_tile(sdS, LDD, 16 * it, 16 * (w * CPW + cq), dS[cq][it], lane);
           }
       }
       __syncthreads();
@@ -440,44 +444,53 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
         f32x4 acc = zero4();
         for (int ks = 0; ks < D / KS; ++ks) {
           const int kofs = ks * KS + g * KPL;
-          acc = M::mma(M::load(sQ + c * D + kofs), M::load(sF + (16 * rt + c) * D + kofs), acc);
+          acc = M::mma(M::load(sQ + c * LDD + kofs), M::load(sF + (16 * rt + c) * LDD + kofs), acc);
         }
         for (int r = 0; r < 4; ++r) acc[r] = tanh_f(acc[r]);
-        store_tile(sTau, R2, 0, 16 * rt, acc, lane);
+        store_tile(sTau, LDR, 0, 16 * rt, acc, lane);
       }
       __syncthreads();
       // ---- R2: gates and retention factors ------------------------------------------
+      float qv[CPW][4], kv[CPW][4], vv[CPW][4];
       float E[CPW][4], Ep[CPW][4], en[CPW][4], bgt[CPW][4], wgt[CPW][4], wv[CPW][4];
       float gam[CPW];
+      float p[CPW][4];
       for (int cq = 0; cq < CPW; ++cq) {
         const int ct = w * CPW + cq;
         const int jj = 16 * ct + c;
         f32x4 accB = zero4(), accW = zero4();
         for (int ks = 0; ks < RP / KS; ++ks) {
           const int r0 = ks * KS + g * KPL;
-          accB = M::mma(M::load(sTau + c * R2 + r0), fVb[cq][ks], accB);
-          accW = M::mma(M::load(sTau + c * R2 + RP + r0), fVw[cq][ks], accW);
+          accB = M::mma(M::load(sTau + c * LDR + r0), fVb[cq][ks], accB);
+          accW = M::mma(M::load(sTau + c * LDR + RP + r0), fVw[cq][ks], accW);
         }
-        float p[4];
         for (int r = 0; r < 4; ++r) {
-          const float zb = bxv[cq][r] + accB[r];
-          p[r] = gv[cq][r] - softplus_f(zb);
+          const float zb = cbx[cq][r] + accB[r];
+          p[cq][r] = cg[cq][r] - softplus_f(zb);
           bgt[cq][r] = sigmoid_f(zb);
-          wgt[cq][r] = sigmoid_f(wxv[cq][r] + accW[r]);
+          wgt[cq][r] = sigmoid_f(cwx[cq][r] + accW[r]);
+          vv[cq][r] = cv[cq][r];
           wv[cq][r] = wgt[cq][r] * vv[cq][r];
+          qv[cq][r] = to_f(sQ[(4 * g + r) * LDD + jj]);
+          kv[cq][r] = to_f(sK[(4 * g + r) * LDD + jj]);
         }
-        p[1] += p[0];
-        p[2] += p[1];
-        p[3] += p[2];
-        float incl = p[3];
+      }
+      if (nch_ >= 0) CARVE_BWD_PREFETCH_GATES(nt0);
+      for (int cq = 0; cq < CPW; ++cq) {
+        const int ct = w * CPW + cq;
+        const int jj = 16 * ct + c;
+        p[cq][1] += p[cq][0];
+        p[cq][2] += p[cq][1];
+        p[cq][3] += p[cq][2];
+        float incl = p[cq][3];
         float y = __shfl_up(incl, 16);
         if (g >= 1) incl += y;
         y = __shfl_up(incl, 32);
         if (g >= 2) incl += y;
-        const float excl = incl - p[3];
+        const float excl = incl - p[cq][3];
         const float lam_end = __shfl(incl, 48 + c);
         for (int r = 0; r < 4; ++r) {
-          const float lam = excl + p[r];
+          const float lam = excl + p[cq][r];
           E[cq][r] = fast_exp(lam);
           en[cq][r] = fast_exp(-lam);
         }
@@ -494,14 +507,14 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
           vQ[r] = qv[cq][r] * E[cq][r];
           vKi[r] = kv[cq][r] * en[cq][r];
           vKh[r] = vKi[r] * gam[cq];
-          sK[t * D + jj] = (T)vK[r];
-          sQ[t * D + jj] = (T)vQ[r];
-          sKi[t * D + jj] = (T)vKi[r];
+          sK[t * LDD + jj] = (T)vK[r];
+          sQ[t * LDD + jj] = (T)vQ[r];
+          sKi[t * LDD + jj] = (T)vKi[r];
         }
-        store_tile_t(sKT, BLW, 0, 16 * ct, vK, lane);
-        store_tile_t(sQT, BLW, 0, 16 * ct, vQ, lane);
-        store_tile_t(sKiT, BLW, 0, 16 * ct, vKi, lane);
-        if (!bwd) store_tile_t(sKhT, BLW, 0, 16 * ct, vKh, lane);
+        store_tile_t(sKT, LDB, 0, 16 * ct, vK, lane);
+        store_tile_t(sQT, LDB, 0, 16 * ct, vQ, lane);
+        store_tile_t(sKiT, LDB, 0, 16 * ct, vKi, lane);
+        if (!bwd) store_tile_t(sKhT, LDB, 0, 16 * ct, vKh, lane);
         if (g == 0) sGam[jj] = gam[cq];
       }
       __syncthreads();
@@ -510,19 +523,19 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
         f32x4 accA = zero4(), accP = zero4();
         for (int ks = 0; ks < D / KS; ++ks) {
           const int kofs = ks * KS + g * KPL;
-          const typename M::frag kb = M::load(sKi + c * D + kofs);
-          accA = M::mma(M::load(sK + c * D + kofs), kb, accA);
-          accP = M::mma(M::load(sQ + c * D + kofs), kb, accP);
+          const typename M::frag kb = M::load(sKi + c * LDD + kofs);
+          accA = M::mma(M::load(sK + c * LDD + kofs), kb, accA);
+          accP = M::mma(M::load(sQ + c * LDD + kofs), kb, accP);
         }
         f32x4 pv;
         for (int r = 0; r < 4; ++r) {
           const int t = 4 * g + r;
           const float dval = (c < t) ? accA[r] : 0.0f;
-          sDm[t * BLW + c] = dval;
-          sA[t * BLW + c] = sBeta[t] * dval;
+          sDm[t * LDF + c] = dval;
+          sA[t * LDF + c] = sBeta[t] * dval;
           pv[r] = (c <= t) ? accP[r] : 0.0f;
         }
-        store_tile_t(sPT, BLW, 0, 0, pv, lane);
+        store_tile_t(sPT, LDB, 0, 0, pv, lane);
       }
       float Eerr[CPW][4];
       for (int cq = 0; cq < CPW; ++cq) {
@@ -530,24 +543,24 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
         f32x4 acc = zero4();
         for (int ks = 0; ks < D / KS; ++ks) {
           const int kofs = ks * KS + g * KPL;
-          acc = M::mma(M::load(sK + c * D + kofs), M::load(sS + (16 * ct + c) * D + kofs), acc);
+          acc = M::mma(M::load(sK + c * LDD + kofs), M::load(sS + (16 * ct + c) * LDD + kofs), acc);
         }
         f32x4 rv;
         for (int r = 0; r < 4; ++r) {
           Eerr[cq][r] = wv[cq][r] - acc[r];
           rv[r] = sBeta[4 * g + r] * Eerr[cq][r];
         }
-        store_tile_t(sRT, BLW, 0, 16 * ct, rv, lane);
+        store_tile_t(sRT, LDB, 0, 16 * ct, rv, lane);
       }
       __syncthreads();
       // ---- R4: T = (I + A)^{-1}; du = Khat dS'^T + P^T dO ------------------------------
       if (w == 0 && g == 0) {
         float x[16];
-        unit_lower_inverse_column(sA, BLW, c, x);
+        unit_lower_inverse_column(sA, LDF, c, x);
 #pragma unroll
         for (int t = 0; t < 16; ++t) {
-          sTb[t * BLW + c] = (T)x[t];
-          sTbT[c * BLW + t] = (T)x[t];
+          sTb[t * LDB + c] = (T)x[t];
+          sTbT[c * LDB + t] = (T)x[t];
         }
       }
       if (bwd) {
@@ -556,10 +569,10 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
           f32x4 acc = zero4();
           for (int ks = 0; ks < D / KS; ++ks) {
             const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load_scaled(sKi + c * D + kofs, sGam + kofs), M::load(sdS + (16 * ct + c) * D + kofs), acc);
+            acc = M::mma(M::load_scaled(sKi + c * LDD + kofs, sGam + kofs), M::load(sdS + (16 * ct + c) * LDD + kofs), acc);
           }
-          acc = mma_k16<T>(acc, sPT + c * BLW, sdOT + (16 * ct + c) * BLW, g);
-          store_tile_t(sduT, BLW, 0, 16 * ct, acc, lane);
+          acc = mma_k16<T>(acc, sPT + c * LDB, sdOT + (16 * ct + c) * LDB, g);
+          store_tile_t(sduT, LDB, 0, 16 * ct, acc, lane);
         }
       }
       __syncthreads();
@@ -568,10 +581,10 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
       for (int cq = 0; cq < CPW; ++cq) {
         const int ct = w * CPW + cq;
         const int jj = 16 * ct + c;
-        const f32x4 u = mma_k16<T>(zero4(), sTb + c * BLW, sRT + (16 * ct + c) * BLW, g);
+        const f32x4 u = mma_k16<T>(zero4(), sTb + c * LDB, sRT + (16 * ct + c) * LDB, g);
         if (bwd) {
-          store_tile(sU, D, 0, 16 * ct, u, lane);
-          const f32x4 dR = mma_k16<T>(zero4(), sTbT + c * BLW, sduT + (16 * ct + c) * BLW, g);
+          store_tile(sU, LDD, 0, 16 * ct, u, lane);
+          const f32x4 dR = mma_k16<T>(zero4(), sTbT + c * LDB, sduT + (16 * ct + c) * LDB, g);
           f32x4 dE, dzv;
           for (int r = 0; r < 4; ++r) {
             const int t = 4 * g + r;
@@ -589,12 +602,12 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
             dwx[e] = (T)dzw[cq][r];
             dzv[r] = dzw[cq][r];
           }
-          store_tile(sdR, D, 0, 16 * ct, dR, lane);
-          store_tile(sdE, D, 0, 16 * ct, dE, lane);
-          store_tile_t(sdET, BLW, 0, 16 * ct, dE, lane);
-          store_tile(sdzw, D, 0, 16 * ct, dzv, lane);
+          store_tile(sdR, LDD, 0, 16 * ct, dR, lane);
+          store_tile(sdE, LDD, 0, 16 * ct, dE, lane);
+          store_tile_t(sdET, LDB, 0, 16 * ct, dE, lane);
+          store_tile(sdzw, LDD, 0, 16 * ct, dzv, lane);
         } else {
-          store_tile_t(sUT, BLW, 0, 16 * ct, u, lane);
+          store_tile_t(sUT, LDB, 0, 16 * ct, u, lane);
         }
       }
       __syncthreads();
@@ -604,9 +617,10 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
         for (int cq = 0; cq < CPW; ++cq) {
           const int ct = w * CPW + cq;
           for (int it = 0; it < NIT; ++it) {
+            CARVE_SEQ();
             f32x4 acc;
             for (int r = 0; r < 4; ++r) acc[r] = S[cq][it][r] * gam[cq];
-            acc = mma_k16<T>(acc, sUT + (16 * it + c) * BLW, sKhT + (16 * ct + c) * BLW, g);
+            acc = mma_k16<T>(acc, sUT + (16 * it + c) * LDB, sKhT + (16 * ct + c) * LDB, g);
             S[cq][it] = acc;
             if (m + 1 < msub - 1) dst[cq * NIT + it] = acc;  // the last one stays in registers
           }
@@ -617,10 +631,10 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
       f32x4 dKt[CPW], dQt[CPW], dKh[CPW];
       float cs[CPW];
       for (int cq = 0; cq < CPW; ++cq) {
-        dKt[cq] = mma_regB<T, NIT>(zero4(), sdE + c * D, S[cq], g);
+        dKt[cq] = mma_regB<T, NIT>(zero4(), sdE + c * LDD, S[cq], g);
         for (int r = 0; r < 4; ++r) dKt[cq][r] = -dKt[cq][r];
-        dQt[cq] = mma_regB<T, NIT>(zero4(), sdO + c * D, S[cq], g);
-        dKh[cq] = mma_regB<T, NIT>(zero4(), sU + c * D, dS[cq], g);
+        dQt[cq] = mma_regB<T, NIT>(zero4(), sdO + c * LDD, S[cq], g);
+        dKh[cq] = mma_regB<T, NIT>(zero4(), sU + c * LDD, dS[cq], g);
         float s_ = 0.0f;  // colsum(S * dS') for this column
         for (int it = 0; it < NIT; ++it)
           for (int r = 0; r < 4; ++r) s_ += S[cq][it][r] * dS[cq][it][r];
@@ -659,32 +673,32 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
         f32x4 acc = zero4();
         for (int ks = 0; ks < D / KS; ++ks) {
           const int kofs = ks * KS + g * KPL;
-          acc = M::mma(M::load(sdO + c * D + kofs), M::load(sU + c * D + kofs), acc);
+          acc = M::mma(M::load(sdO + c * LDD + kofs), M::load(sU + c * LDD + kofs), acc);
         }
         for (int r = 0; r < 4; ++r) acc[r] = (c <= 4 * g + r) ? acc[r] : 0.0f;
-        store_tile(sdP, BLW, 0, 0, acc, lane);
-        store_tile_t(sdPT, BLW, 0, 0, acc, lane);
+        store_tile(sdP, LDB, 0, 0, acc, lane);
+        store_tile_t(sdPT, LDB, 0, 0, acc, lane);
       }
       if (w == (NW > 1 ? 1 : 0)) {
         f32x4 acc = zero4();
         for (int ks = 0; ks < D / KS; ++ks) {
           const int kofs = ks * KS + g * KPL;
-          acc = M::mma(M::load(sdR + c * D + kofs), M::load(sU + c * D + kofs), acc);
+          acc = M::mma(M::load(sdR + c * LDD + kofs), M::load(sU + c * LDD + kofs), acc);
         }
         f32x4 ddv;
         for (int r = 0; r < 4; ++r) {
           const int t = 4 * g + r;
           const float dA = (c < t) ? -acc[r] : 0.0f;
           ddv[r] = sBeta[t] * dA;
-          float db = dA * sDm[t * BLW + c];
+          float db = dA * sDm[t * LDF + c];
           db += __shfl_xor(db, 1);
           db += __shfl_xor(db, 2);
           db += __shfl_xor(db, 4);
           db += __shfl_xor(db, 8);
           if (c == 0) sDb2[t] = db;
         }
-        store_tile(sdD, BLW, 0, 0, ddv, lane);
-        store_tile_t(sdDT, BLW, 0, 0, ddv, lane);
+        store_tile(sdD, LDB, 0, 0, ddv, lane);
+        store_tile_t(sdDT, LDB, 0, 0, ddv, lane);
       }
       __syncthreads();
       // ---- G5: factored-pair gradients, dLam, gate-logit gradients -----------------
@@ -692,10 +706,10 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
       for (int cq = 0; cq < CPW; ++cq) {
         const int ct = w * CPW + cq;
         const int jj = 16 * ct + c;
-        const f32x4 dAq = mma_k16<T>(zero4(), sdD + c * BLW, sKiT + (16 * ct + c) * BLW, g);
-        const f32x4 dPq = mma_k16<T>(zero4(), sdP + c * BLW, sKiT + (16 * ct + c) * BLW, g);
-        f32x4 dcol = mma_k16<T>(zero4(), sdDT + c * BLW, sKT + (16 * ct + c) * BLW, g);
-        dcol = mma_k16<T>(dcol, sdPT + c * BLW, sQT + (16 * ct + c) * BLW, g);
+        const f32x4 dAq = mma_k16<T>(zero4(), sdD + c * LDB, sKiT + (16 * ct + c) * LDB, g);
+        const f32x4 dPq = mma_k16<T>(zero4(), sdP + c * LDB, sKiT + (16 * ct + c) * LDB, g);
+        f32x4 dcol = mma_k16<T>(zero4(), sdDT + c * LDB, sKT + (16 * ct + c) * LDB, g);
+        dcol = mma_k16<T>(dcol, sdPT + c * LDB, sQT + (16 * ct + c) * LDB, g);
         float aL[4], pL[4], xs = 0.0f;
         for (int r = 0; r < 4; ++r) {
           const float gq = dQt[cq][r] * E[cq][r] + E[cq][r] * dPq[r];   // dq from Qtil and P
@@ -738,7 +752,7 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
           dbx[e] = (T)dzb[cq][r];
           dzv[r] = dzb[cq][r];
         }
-        store_tile(sdzb, D, 0, 16 * ct, dzv, lane);
+        store_tile(sdzb, LDD, 0, 16 * ct, dzv, lane);
         // dVb += dz_b^T tau_b, dVw += dz_w^T tau_w (A from registers, K = 16 tokens)
         for (int rt = 0; rt < NVT; ++rt) {
           if constexpr (sizeof(T) == 2) {
@@ -746,8 +760,8 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
             for (int e = 0; e < 4; ++e) {
               ab[e] = (T)dzb[cq][e];
               aw[e] = (T)dzw[cq][e];
-              bb[e] = sTau[(4 * g + e) * R2 + 16 * rt + c];
-              bw[e] = sTau[(4 * g + e) * R2 + RP + 16 * rt + c];
+              bb[e] = sTau[(4 * g + e) * LDR + 16 * rt + c];
+              bw[e] = sTau[(4 * g + e) * LDR + RP + 16 * rt + c];
               ab[4 + e] = (T)0.0f;
               aw[4 + e] = (T)0.0f;
               bb[4 + e] = (T)0.0f;
@@ -757,8 +771,8 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
             dVw[cq][rt] = M::mma(aw, bw, dVw[cq][rt]);
           } else {
             for (int r = 0; r < 4; ++r) {
-              dVb[cq][rt] = M::mma(dzb[cq][r], sTau[(4 * g + r) * R2 + 16 * rt + c], dVb[cq][rt]);
-              dVw[cq][rt] = M::mma(dzw[cq][r], sTau[(4 * g + r) * R2 + RP + 16 * rt + c], dVw[cq][rt]);
+              dVb[cq][rt] = M::mma(dzb[cq][r], sTau[(4 * g + r) * LDR + 16 * rt + c], dVb[cq][rt]);
+              dVw[cq][rt] = M::mma(dzw[cq][r], sTau[(4 * g + r) * LDR + RP + 16 * rt + c], dVw[cq][rt]);
             }
           }
         }
@@ -769,16 +783,16 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
         const int x = w + gi * NW;
         if (x >= 2 * NVT) break;
         const int half = x / NVT, rt = x % NVT;
-        const T* arow = (half ? sdzw : sdzb) + c * D;
+        const T* arow = (half ? sdzw : sdzb) + c * LDD;
         f32x4 acc = zero4();
         for (int ks = 0; ks < D / KS; ++ks) acc = M::mma(M::load(arow + ks * KS + g * KPL), fVt[gi][ks], acc);
         f32x4 dy;
         for (int r = 0; r < 4; ++r) {
-          const float tv = to_f(sTau[(4 * g + r) * R2 + half * RP + 16 * rt + c]);
+          const float tv = to_f(sTau[(4 * g + r) * LDR + half * RP + 16 * rt + c]);
           dy[r] = acc[r] * (1.0f - tv * tv);
         }
-        store_tile(sdY, R2, 0, half * RP + 16 * rt, dy, lane);
-        store_tile_t(sdYT, BLW, 0, half * RP + 16 * rt, dy, lane);
+        store_tile(sdY, LDR, 0, half * RP + 16 * rt, dy, lane);
+        store_tile_t(sdYT, LDB, 0, half * RP + 16 * rt, dy, lane);
       }
       __syncthreads();
       // ---- G9: dq += dY F, outputs, dF += dY^T q, dS <- ... -----------------------------
@@ -790,11 +804,11 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
           const int r0 = ks * KS + g * KPL;
           typename M::frag bfg;
           if constexpr (KPL == 8) {
-            for (int e = 0; e < 8; ++e) bfg[e] = sF[(r0 + e) * D + jj];
+            for (int e = 0; e < 8; ++e) bfg[e] = sF[(r0 + e) * LDD + jj];
           } else {
-            bfg = sF[r0 * D + jj];
+            bfg = sF[r0 * LDD + jj];
           }
-          acc = M::mma(M::load(sdY + c * R2 + r0), bfg, acc);
+          acc = M::mma(M::load(sdY + c * LDR + r0), bfg, acc);
         }
         for (int r = 0; r < 4; ++r) {
           const int t = 4 * g + r;
@@ -806,7 +820,7 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
           if constexpr (sizeof(T) == 2) {
             typename M::frag af, bfg;
             for (int e = 0; e < 4; ++e) {
-              af[e] = sdYT[(16 * rt + c) * BLW + 4 * g + e];
+              af[e] = sdYT[(16 * rt + c) * LDB + 4 * g + e];
               bfg[e] = (T)qv[cq][e];
               af[4 + e] = (T)0.0f;
               bfg[4 + e] = (T)0.0f;
@@ -814,14 +828,15 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
             dF[cq][rt] = M::mma(af, bfg, dF[cq][rt]);
           } else {
             for (int r = 0; r < 4; ++r)
-              dF[cq][rt] = M::mma(sdYT[(16 * rt + c) * BLW + 4 * g + r], qv[cq][r], dF[cq][rt]);
+              dF[cq][rt] = M::mma(sdYT[(16 * rt + c) * LDB + 4 * g + r], qv[cq][r], dF[cq][rt]);
           }
         }
         for (int it = 0; it < NIT; ++it) {
+          CARVE_SEQ();
           f32x4 acc1, acc2;
           for (int r = 0; r < 4; ++r) acc1[r] = dS[cq][it][r] * gam[cq];
-          acc1 = mma_k16<T>(acc1, sdOT + (16 * it + c) * BLW, sQT + (16 * ct + c) * BLW, g);
-          acc2 = mma_k16<T>(zero4(), sdET + (16 * it + c) * BLW, sKT + (16 * ct + c) * BLW, g);
+          acc1 = mma_k16<T>(acc1, sdOT + (16 * it + c) * LDB, sQT + (16 * ct + c) * LDB, g);
+          acc2 = mma_k16<T>(zero4(), sdET + (16 * it + c) * LDB, sKT + (16 * ct + c) * LDB, g);
           for (int r = 0; r < 4; ++r) dS[cq][it][r] = acc1[r] - acc2[r];
         }
       }
@@ -835,10 +850,11 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
     // ---- chunk start: glue through the folded read-out ------------------------------
     __syncthreads();
     for (int cq = 0; cq < CPW; ++cq)
-      for (int rt = 0; rt < NRT; ++rt) store_tile(sdF, D, 16 * rt, 16 * (w * CPW + cq), dF[cq][rt], lane);
+      for (int rt = 0; rt < NRT; ++rt) store_tile(sdF, LDD, 16 * rt, 16 * (w * CPW + cq), dF[cq][rt], lane);
     // dS += [Ub;Uw]^T dF  (contraction over the rows of dF, held in registers)
     for (int cq = 0; cq < CPW; ++cq)
       for (int it = 0; it < NIT; ++it) {
+        CARVE_SEQ();
         f32x4 acc = dS[cq][it];
         const T* urow = UT + (size_t)(16 * it + c) * R2;  // value row this lane supplies as A
         if constexpr (KPL == 8) {
@@ -865,10 +881,11 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
     for (int cq = 0; cq < CPW; ++cq) {
       const int ct = w * CPW + cq;
       for (int rt = 0; rt < NRT; ++rt) {
+        CARVE_SEQ();
         f32x4 acc = dU[cq][rt];
         for (int ks = 0; ks < D / KS; ++ks) {
           const int kofs = ks * KS + g * KPL;
-          acc = M::mma(M::load(sdF + (16 * rt + c) * D + kofs), M::load(sS + (16 * ct + c) * D + kofs), acc);
+          acc = M::mma(M::load(sdF + (16 * rt + c) * LDD + kofs), M::load(sS + (16 * ct + c) * LDD + kofs), acc);
         }
         dU[cq][rt] = acc;
       }

@@ -46,10 +46,17 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
   constexpr int NIT = D / 16;         // value-row tiles
   constexpr int KS = M::KS, KPL = M::KPL;
   constexpr int LK = lk_of<T, LW>();  // padded token extent of the K = LW products
+  // LDS row strides: every row is padded by 16 bytes so that the 16 rows read by
+  // one MFMA fragment load fall into distinct banks
+  constexpr int PAD = 16 / sizeof(T);
+  constexpr int LDD = D + PAD;        // rows of D elements
+  constexpr int LDK = LK + PAD;       // rows of LK elements
+  constexpr int LDA = LW + 4;         // rows of the f32 coupling matrix
   constexpr int VEC = 16 / sizeof(T); // elements per 16-byte vector
   constexpr int NVT = LW * D / VEC;                // 16-byte vectors of a q (or k) tile
   constexpr int NQV = (NVT + NT - 1) / NT;         // per thread
   const int RP = a.RP, R2 = 2 * a.RP, R = a.R;
+  const int LDR = R2 + PAD, LDV = RP + PAD;  // rows of 2RP / RP elements
   const int H = a.H, Tn = a.T, L = a.L;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
@@ -98,12 +105,12 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
     float u = 0.0f;
     if (rr < R) u = a.Ub[(size_t)rr * D + i];
     else if (rr >= RP && rr < RP + R) u = a.Uw[(size_t)(rr - RP) * D + i];
-    sU[x] = (T)u;
+    sU[rr * LDD + i] = (T)u;
   }
   for (int x = tid; x < D * RP; x += NT) {
     const int j = x / RP, rr = x % RP;
-    sVb[x] = (T)(rr < R ? a.Vb[(size_t)j * R + rr] : 0.0f);
-    sVw[x] = (T)(rr < R ? a.Vw[(size_t)j * R + rr] : 0.0f);
+    sVb[j * LDV + rr] = (T)(rr < R ? a.Vb[(size_t)j * R + rr] : 0.0f);
+    sVw[j * LDV + rr] = (T)(rr < R ? a.Vw[(size_t)j * R + rr] : 0.0f);
   }
 
   // ---- state registers: S[cq][it][r] = S[16*it + 4g + r][16*(w*CPW+cq) + c] ----
@@ -114,7 +121,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
     for (int it = 0; it < NIT; ++it) {
       for (int r = 0; r < 4; ++r)
         S[cq][it][r] = a.S0 ? a.S0[soff + (size_t)(16 * it + 4 * g + r) * D + col] : 0.0f;
-      store_tile(sS, D, 16 * it, 16 * (w * CPW + cq), S[cq][it], lane);
+      store_tile(sS, LDD, 16 * it, 16 * (w * CPW + cq), S[cq][it], lane);
     }
   }
 
@@ -171,8 +178,8 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
         const int x = tid + u * NT;
         if (NVT % NT != 0 && x >= NVT) break;
         const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;
-        *reinterpret_cast<f32x4*>(sQ + t * D + j) = pq[u];
-        *reinterpret_cast<f32x4*>(sK + t * D + j) = pk[u];
+        *reinterpret_cast<f32x4*>(sQ + t * LDD + j) = pq[u];
+        *reinterpret_cast<f32x4*>(sK + t * LDD + j) = pk[u];
       }
       if (tid < LW) sBeta[tid] = pbeta;
       if (tile + 1 < ntiles) CARVE_FWD_PREFETCH_QK(tile + 1);
@@ -181,7 +188,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
         for (int cq = 0; cq < CPW; ++cq) {
           const int ct = w * CPW + cq;
           for (int rt = 0; rt < R2 / 16; ++rt) {
-            const T* urow = sU + (16 * rt + c) * D;  // B row this lane supplies
+            const T* urow = sU + (16 * rt + c) * LDD;  // B row this lane supplies
             f32x4 acc = zero4();
             if constexpr (KPL == 8) {
               for (int ks = 0; ks < D / 32; ++ks) {
@@ -200,7 +207,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
                 for (int r4 = 0; r4 < 4; ++r4) acc = M::mma((T)S[cq][it][r4], urow[16 * it + 4 * g + r4], acc);
             }
             // acc = F^T[j = 16ct + 4g + r][16rt + c]  ->  sF[r][j]
-            store_tile_t(sF, D, 16 * ct, 16 * rt, acc, lane);
+            store_tile_t(sF, LDD, 16 * ct, 16 * rt, acc, lane);
           }
         }
       }
@@ -214,10 +221,10 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
           f32x4 acc = zero4();
           for (int ks = 0; ks < D / KS; ++ks) {
             const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load(sQ + (16 * ti + c) * D + kofs), M::load(sF + (16 * rt + c) * D + kofs), acc);
+            acc = M::mma(M::load(sQ + (16 * ti + c) * LDD + kofs), M::load(sF + (16 * rt + c) * LDD + kofs), acc);
           }
           for (int r = 0; r < 4; ++r) acc[r] = tanh_f(acc[r]);
-          store_tile(sTau, R2, 16 * ti, 16 * rt, acc, lane);
+          store_tile(sTau, LDR, 16 * ti, 16 * rt, acc, lane);
         }
       }
       __syncthreads();
@@ -227,13 +234,13 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
       float wv[CPW][NB][4];
       for (int cq = 0; cq < CPW; ++cq) {
         const int ct = w * CPW + cq;
-        const T* vbrow = sVb + (16 * ct + c) * RP;
-        const T* vwrow = sVw + (16 * ct + c) * RP;
+        const T* vbrow = sVb + (16 * ct + c) * LDV;
+        const T* vwrow = sVw + (16 * ct + c) * LDV;
         for (int ti = 0; ti < NB; ++ti) {
           f32x4 accB = zero4(), accW = zero4();
           for (int ks = 0; ks < RP / KS; ++ks) {
             const int r0 = ks * KS + g * KPL;
-            const int arow = (16 * ti + c) * R2;
+            const int arow = (16 * ti + c) * LDR;
             accB = M::mma(M::load(sTau + arow + r0), M::load(vbrow + r0), accB);
             accW = M::mma(M::load(sTau + arow + RP + r0), M::load(vwrow + r0), accW);
           }
@@ -279,12 +286,12 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
           Ep[3] = E[2];
           for (int r = 0; r < 4; ++r) {
             const int t = 16 * ti + 4 * g + r;
-            const float kv = to_f(sK[t * D + jj]);
-            const float qv = to_f(sQ[t * D + jj]);
-            sK[t * D + jj] = (T)(kv * Ep[r]);
-            sQ[t * D + jj] = (T)(qv * E[r]);
+            const float kv = to_f(sK[t * LDD + jj]);
+            const float qv = to_f(sQ[t * LDD + jj]);
+            sK[t * LDD + jj] = (T)(kv * Ep[r]);
+            sQ[t * LDD + jj] = (T)(qv * E[r]);
             Ki[r] *= kv;
-            sKi[t * D + jj] = (T)Ki[r];
+            sKi[t * LDD + jj] = (T)Ki[r];
             ell[cq][ti][r] = Ki[r];  // keep k e^{-Lam_rel}
           }
           bases[ti] = base;
@@ -297,7 +304,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
           const float f = fast_exp(lam_end - bases[ti]);
           f32x4 kh;
           for (int r = 0; r < 4; ++r) kh[r] = ell[cq][ti][r] * f;
-          store_tile_t(sKhT, LK, 16 * ti, 16 * ct, kh, lane);
+          store_tile_t(sKhT, LDK, 16 * ti, 16 * ct, kh, lane);
           if (g == 0) {
             sBase[ti * D + jj] = fast_exp(bases[ti]);
             for (int si = 0; si < ti; ++si) sCf[(ti * NB + si) * D + jj] = fast_exp(bases[ti] - bases[si]);
@@ -318,16 +325,16 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
           f32x4 accA = zero4(), accP = zero4();
           for (int ks = 0; ks < D / KS; ++ks) {
             const int kofs = ks * KS + g * KPL;
-            const T* kb = sKi + (16 * si + c) * D + kofs;
+            const T* kb = sKi + (16 * si + c) * LDD + kofs;
             const typename M::frag bf = (ti == si) ? M::load(kb) : M::load_scaled(kb, sCf + (ti * NB + si) * D + kofs);
-            accA = M::mma(M::load(sK + (16 * ti + c) * D + kofs), bf, accA);
-            accP = M::mma(M::load(sQ + (16 * ti + c) * D + kofs), bf, accP);
+            accA = M::mma(M::load(sK + (16 * ti + c) * LDD + kofs), bf, accA);
+            accP = M::mma(M::load(sQ + (16 * ti + c) * LDD + kofs), bf, accP);
           }
           for (int r = 0; r < 4; ++r) {
             const int tl = 4 * g + r;  // row inside the tile
             const bool lowA = (ti > si) || (c < tl);
             const bool lowP = (ti > si) || (c <= tl);
-            sA[(16 * ti + tl) * LW + 16 * si + c] = lowA ? sBeta[16 * ti + tl] * accA[r] : 0.0f;
+            sA[(16 * ti + tl) * LDA + 16 * si + c] = lowA ? sBeta[16 * ti + tl] * accA[r] : 0.0f;
             accP[r] = lowP ? accP[r] : 0.0f;
           }
           Pkeep[slot] = accP;
@@ -340,10 +347,10 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
           f32x4 ak = zero4(), aq = zero4();
           for (int ks = 0; ks < D / KS; ++ks) {
             const int kofs = ks * KS + g * KPL;
-            const typename M::frag sb = M::load(sS + (16 * ct + c) * D + kofs);
+            const typename M::frag sb = M::load(sS + (16 * ct + c) * LDD + kofs);
             const float* sc = sBase + ti * D + kofs;
-            ak = M::mma(M::load_scaled(sK + (16 * ti + c) * D + kofs, sc), sb, ak);
-            aq = M::mma(M::load_scaled(sQ + (16 * ti + c) * D + kofs, sc), sb, aq);
+            ak = M::mma(M::load_scaled(sK + (16 * ti + c) * LDD + kofs, sc), sb, ak);
+            aq = M::mma(M::load_scaled(sQ + (16 * ti + c) * LDD + kofs, sc), sb, aq);
           }
           XK[cq][ti] = ak;
           XQ[cq][ti] = aq;
@@ -356,30 +363,30 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
         for (int x = w; x < NTRI; x += NW, ++slot) {
           int ti = 0, si = x;
           while (si > ti) { si -= ti + 1; ++ti; }
-          store_tile(sP, LK, 16 * ti, 16 * si, Pkeep[slot], lane);
+          store_tile(sP, LDK, 16 * ti, 16 * si, Pkeep[slot], lane);
         }
         // zero the upper tiles (and padding columns) of P and T, and the
         // padding columns of R^T, u^T and Khat^T (read by the 32-wide K steps)
         for (int x = tid; x < LW * LK; x += NT) {
           const int rr = x / LK, cc = x % LK;
           if ((cc >> 4) > (rr >> 4)) {
-            sP[x] = (T)0.0f;
-            sTb[x] = (T)0.0f;
+            sP[rr * LDK + cc] = (T)0.0f;
+            sTb[rr * LDK + cc] = (T)0.0f;
           }
         }
         if constexpr (LK > LW) {
           for (int x = tid; x < D * (LK - LW); x += NT) {
             const int rr = x / (LK - LW), cc = LW + x % (LK - LW);
-            sRT[rr * LK + cc] = (T)0.0f;
-            sUT[rr * LK + cc] = (T)0.0f;
-            sKhT[rr * LK + cc] = (T)0.0f;
+            sRT[rr * LDK + cc] = (T)0.0f;
+            sUT[rr * LDK + cc] = (T)0.0f;
+            sKhT[rr * LDK + cc] = (T)0.0f;
           }
         }
         for (int cq = 0; cq < CPW; ++cq)
           for (int ti = 0; ti < NB; ++ti) {
             f32x4 rv;
             for (int r = 0; r < 4; ++r) rv[r] = sBeta[16 * ti + 4 * g + r] * (wv[cq][ti][r] - XK[cq][ti][r]);
-            store_tile_t(sRT, LK, 16 * ti, 16 * (w * CPW + cq), rv, lane);
+            store_tile_t(sRT, LDK, 16 * ti, 16 * (w * CPW + cq), rv, lane);
           }
       }
       __syncthreads();
@@ -387,13 +394,13 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
       // ---- P6: T = (I + A)^{-1} -----------------------------------------------
       if (w == 0 && g < NB) {
         // diagonal block g: column c by forward substitution, A rows in registers
-        const float* Ab = sA + (16 * g) * LW + 16 * g;
+        const float* Ab = sA + (16 * g) * LDA + 16 * g;
         float arow[16][16];
 #pragma unroll
         for (int t = 1; t < 16; ++t)
 #pragma unroll
           for (int s4 = 0; s4 < (t + 3) / 4; ++s4) {
-            const f32x4 v4 = *reinterpret_cast<const f32x4*>(Ab + t * LW + 4 * s4);
+            const f32x4 v4 = *reinterpret_cast<const f32x4*>(Ab + t * LDA + 4 * s4);
             arow[t][4 * s4] = v4[0];
             arow[t][4 * s4 + 1] = v4[1];
             arow[t][4 * s4 + 2] = v4[2];
@@ -407,12 +414,12 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
           for (int s = 0; s < t; ++s) acc -= arow[t][s] * x[s];
           x[t] = acc;
         }
-        float* Aw = sA + (16 * g) * LW + 16 * g;
-        T* Tw = sTb + (16 * g) * LK + 16 * g;
+        float* Aw = sA + (16 * g) * LDA + 16 * g;
+        T* Tw = sTb + (16 * g) * LDK + 16 * g;
 #pragma unroll
         for (int t = 0; t < 16; ++t) {
-          Aw[t * LW + c] = x[t];
-          Tw[t * LK + c] = (T)x[t];
+          Aw[t * LDA + c] = x[t];
+          Tw[t * LDK + c] = (T)x[t];
         }
       }
       __syncthreads();
@@ -423,19 +430,19 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
             f32x4 X = zero4();
             for (int kb = j; kb < i; ++kb) {
               for (int ks = 0; ks < 4; ++ks) {
-                const float av = sA[(16 * i + c) * LW + 16 * kb + 4 * g + ks];
-                const float bv = (kb == j) ? sA[(16 * kb + 4 * g + ks) * LW + 16 * j + c] : Tc[kb][ks];
+                const float av = sA[(16 * i + c) * LDA + 16 * kb + 4 * g + ks];
+                const float bv = (kb == j) ? sA[(16 * kb + 4 * g + ks) * LDA + 16 * j + c] : Tc[kb][ks];
                 X = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, X, 0, 0, 0);
               }
             }
             f32x4 Y = zero4();
             for (int ks = 0; ks < 4; ++ks) {
-              const float av = sA[(16 * i + c) * LW + 16 * i + 4 * g + ks];
+              const float av = sA[(16 * i + c) * LDA + 16 * i + 4 * g + ks];
               Y = __builtin_amdgcn_mfma_f32_16x16x4f32(av, X[ks], Y, 0, 0, 0);
             }
             for (int r = 0; r < 4; ++r) Y[r] = -Y[r];
             Tc[i] = Y;
-            store_tile(sTb, LK, 16 * i, 16 * j, Y, lane);
+            store_tile(sTb, LDK, 16 * i, 16 * j, Y, lane);
           }
         }
         __syncthreads();
@@ -449,9 +456,9 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
           const int kmax = (16 * (ti + 1) + KS - 1) / KS;
           for (int ks = 0; ks < kmax; ++ks) {
             const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load(sTb + (16 * ti + c) * LK + kofs), M::load(sRT + (16 * ct + c) * LK + kofs), acc);
+            acc = M::mma(M::load(sTb + (16 * ti + c) * LDK + kofs), M::load(sRT + (16 * ct + c) * LDK + kofs), acc);
           }
-          store_tile_t(sUT, LK, 16 * ti, 16 * ct, acc, lane);
+          store_tile_t(sUT, LDK, 16 * ti, 16 * ct, acc, lane);
         }
       }
       __syncthreads();
@@ -464,7 +471,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
           const int kmax = (16 * (ti + 1) + KS - 1) / KS;
           for (int ks = 0; ks < kmax; ++ks) {
             const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load(sP + (16 * ti + c) * LK + kofs), M::load(sUT + (16 * ct + c) * LK + kofs), acc);
+            acc = M::mma(M::load(sP + (16 * ti + c) * LDK + kofs), M::load(sUT + (16 * ct + c) * LDK + kofs), acc);
           }
           for (int r = 0; r < 4; ++r) {
             const int t = 16 * ti + 4 * g + r;
@@ -479,14 +486,14 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
           for (int r = 0; r < 4; ++r) acc[r] = S[cq][it][r] * gamma_col[cq];
           for (int ks = 0; ks < LK / KS; ++ks) {
             const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load(sUT + (16 * it + c) * LK + kofs), M::load(sKhT + (16 * ct + c) * LK + kofs), acc);
+            acc = M::mma(M::load(sUT + (16 * it + c) * LDK + kofs), M::load(sKhT + (16 * ct + c) * LDK + kofs), acc);
           }
           S[cq][it] = acc;
         }
       }
       __syncthreads();  // every wave is done reading sS (P5) and the aliases
       for (int cq = 0; cq < CPW; ++cq)
-        for (int it = 0; it < NIT; ++it) store_tile(sS, D, 16 * it, 16 * (w * CPW + cq), S[cq][it], lane);
+        for (int it = 0; it < NIT; ++it) store_tile(sS, LDD, 16 * it, 16 * (w * CPW + cq), S[cq][it], lane);
     }
   }
   if (a.S_T) {

@@ -41,20 +41,23 @@ __host__ __device__ constexpr FwdLds fwd_lds(int RP) {
   const size_t e = sizeof(T);
   constexpr int NB = LW / 16;
   constexpr int LK = lk_of<T, LW>();
-  l.S = off;    off += lds_round((size_t)D * D * e);
-  l.Q = off;    off += lds_round(lds_max((size_t)LW * D, (size_t)D * LK) * e);   // also R^T [D][LK]
-  l.K = off;    off += lds_round(lds_max((size_t)LW * D, (size_t)D * LK) * e);   // also u^T [D][LK]
-  l.Ki = off;   off += lds_round(lds_max((size_t)LW * D, (size_t)LW * LK) * e);  // also P [LW][LK]
-  l.F = off;    off += lds_round((size_t)2 * RP * D * e);
-  l.Tau = off;  off += lds_round(lds_max((size_t)LW * 2 * RP, (size_t)LW * LK) * e);  // also T [LW][LK]
-  l.KhT = off;  off += lds_round((size_t)D * LK * e);
-  l.A = off;    off += lds_round((size_t)LW * LW * 4);
+  constexpr size_t PAD = 16 / sizeof(T);      // every LDS row is padded by 16 bytes
+  constexpr size_t LDD = D + PAD, LDK = LK + PAD, LDA = LW + 4;
+  const size_t LDR = 2 * (size_t)RP + PAD, LDV = (size_t)RP + PAD;
+  l.S = off;    off += lds_round((size_t)D * LDD * e);
+  l.Q = off;    off += lds_round(lds_max((size_t)LW * LDD, (size_t)D * LDK) * e);   // also R^T [D][LK]
+  l.K = off;    off += lds_round(lds_max((size_t)LW * LDD, (size_t)D * LDK) * e);   // also u^T [D][LK]
+  l.Ki = off;   off += lds_round(lds_max((size_t)LW * LDD, (size_t)LW * LDK) * e);  // also P [LW][LK]
+  l.F = off;    off += lds_round((size_t)2 * RP * LDD * e);
+  l.Tau = off;  off += lds_round(lds_max((size_t)LW * LDR, (size_t)LW * LDK) * e);  // also T [LW][LK]
+  l.KhT = off;  off += lds_round((size_t)D * LDK * e);
+  l.A = off;    off += lds_round((size_t)LW * LDA * 4);
   l.Base = off; off += lds_round((size_t)NB * D * 4);
   l.Cf = off;   off += lds_round((size_t)NB * NB * D * 4);
   l.Beta = off; off += lds_round((size_t)LW * 4);
-  l.Ucat = off; off += lds_round((size_t)2 * RP * D * e);
-  l.Vb = off;   off += lds_round((size_t)D * RP * e);
-  l.Vw = off;   off += lds_round((size_t)D * RP * e);
+  l.Ucat = off; off += lds_round((size_t)2 * RP * LDD * e);
+  l.Vb = off;   off += lds_round((size_t)D * LDV * e);
+  l.Vw = off;   off += lds_round((size_t)D * LDV * e);
   l.total = off;
   return l;
 }
