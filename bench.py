@@ -98,6 +98,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--L", type=int, default=64)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain elementwise copy of 1 GiB (reads 1 GiB, writes 1 GiB) "
+                         "five times: the reference kernel for scaling the HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the layer shards over (batch, head) with no exchange "
@@ -110,6 +113,16 @@ def main():
 
     from paper_2606_27229_amd import carve
     from paper_2606_27229_amd.inputs import HEADLINE, WORKLOADS, make_inputs
+
+    if args.copy_calibration:
+        n = 1 << 30
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration": {"read_bytes": n, "write_bytes": n, "launches": 5}}), flush=True)
+        return
 
     w = WORKLOADS[HEADLINE].with_(L=args.L)
     L = w.L

@@ -47,8 +47,10 @@ int check_dims(const carve_dims_t* d) {
   if (d->Dk != 32 && d->Dk != 64 && d->Dk != 128) return CARVE_ERR_UNSUPPORTED;
   if (d->R > 64) return CARVE_ERR_UNSUPPORTED;
   if (d->L != 16 && d->L != 32 && d->L != 64 && d->L != 128) return CARVE_ERR_UNSUPPORTED;
-  // the grid is B*H workgroups and offsets are computed in size_t
+  // the grid is B*H workgroups; inside one (batch, head) the kernels address
+  // token tensors with 32-bit offsets
   if ((long long)d->B * d->H > (1LL << 30)) return CARVE_ERR_UNSUPPORTED;
+  if ((long long)d->T * d->H * (d->Dk > d->Dv ? d->Dk : d->Dv) >= (1LL << 31)) return CARVE_ERR_UNSUPPORTED;
   return CARVE_OK;
 }
 

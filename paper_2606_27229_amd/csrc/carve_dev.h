@@ -82,6 +82,99 @@ struct Mma<float> {
   static __device__ __forceinline__ frag zero() { return 0.0f; }
 };
 
+// ---- K16 "quad" operands --------------------------------------------------
+// The kernels issue their products on K16 (and paired K32) matrix-core steps.
+// For one 16x16 output tile and one 16-wide slice of the contraction index k:
+//   lane l = 16 g + c supplies A[m = c][k = 4g .. 4g+3]  and  B[k = 4g .. 4g+3][n = c]
+//   and receives C[m = 4g + i][n = c], i = 0..3.
+// So an accumulator tile X held in registers is directly a B operand whose K is
+// X's row index, and an A operand representing X^T.  LDS operands are read as
+// 4-element quads either along a row ("natural": lane c reads row c) or across
+// four rows ("transposed": lane c reads column c), the latter with the gfx950
+// transposing LDS read for 16-bit data.
+template <typename T>
+struct Quad;
+
+template <>
+struct Quad<bf16_t> {
+  typedef bf16x4 q;
+  static __device__ __forceinline__ q ld(const bf16_t* p) { return *reinterpret_cast<const bf16x4*>(p); }
+  // lane (g, c) receives buf[r0 + 4g + e][c0 + c], e = 0..3
+  static __device__ __forceinline__ q ld_tr(const bf16_t* buf, int ld, int r0, int c0, int g, int c) {
+    typedef short short4_ __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) short4_ lds_s4;
+    const bf16_t* p = buf + (r0 + 4 * g + (c >> 2)) * ld + c0 + 4 * (c & 3);
+    const short4_ v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(p));
+    return __builtin_bit_cast(bf16x4, v);
+  }
+  static __device__ __forceinline__ void st(bf16_t* p, q v) { *reinterpret_cast<bf16x4*>(p) = v; }
+  static __device__ __forceinline__ q cvt(f32x4 x) {
+    q o;
+    o[0] = (bf16_t)x[0]; o[1] = (bf16_t)x[1]; o[2] = (bf16_t)x[2]; o[3] = (bf16_t)x[3];
+    return o;
+  }
+  static __device__ __forceinline__ f32x4 f32(q x) {
+    f32x4 o = {(float)x[0], (float)x[1], (float)x[2], (float)x[3]};
+    return o;
+  }
+  static __device__ __forceinline__ f32x4 mma16(q a, q b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+  }
+  // two K16 slices in one K32 step (the same slice pairing on both sides)
+  static __device__ __forceinline__ f32x4 mma32(q a0, q a1, q b0, q b1, f32x4 c) {
+    const bf16x8 a = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+    const bf16x8 b = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <>
+struct Quad<float> {
+  typedef f32x4 q;
+  static __device__ __forceinline__ q ld(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+  static __device__ __forceinline__ q ld_tr(const float* buf, int ld, int r0, int c0, int g, int c) {
+    const float* p = buf + (r0 + 4 * g) * ld + c0 + c;
+    q o = {p[0], p[ld], p[2 * ld], p[3 * ld]};
+    return o;
+  }
+  static __device__ __forceinline__ void st(float* p, q v) { *reinterpret_cast<f32x4*>(p) = v; }
+  static __device__ __forceinline__ q cvt(f32x4 x) { return x; }
+  static __device__ __forceinline__ f32x4 f32(q x) { return x; }
+  static __device__ __forceinline__ f32x4 mma16(q a, q b, f32x4 c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], c, 0, 0, 0);
+    return c;
+  }
+  static __device__ __forceinline__ f32x4 mma32(q a0, q a1, q b0, q b1, f32x4 c) {
+    return mma16(a1, b1, mma16(a0, b0, c));
+  }
+};
+
+// global 4-element vector of the token dtype <-> f32x4
+__device__ __forceinline__ f32x4 gload4(const bf16_t* p) {
+  const bf16x4 v = *reinterpret_cast<const bf16x4*>(p);
+  f32x4 o = {(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+  return o;
+}
+__device__ __forceinline__ f32x4 gload4(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+
+// DPP helpers inside rows of 16 lanes
+// x of the lane one to the left in its row; the first lane of a row gets fill
+__device__ __forceinline__ float row_shr1(float x, float fill) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, fill), __builtin_bit_cast(int, x),
+                                                               0x111, 0xf, 0xf, false));
+}
+// inclusive prefix sum over the 16 lanes of each row
+__device__ __forceinline__ float row_scan(float x) {
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x111, 0xf, 0xf, false));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x112, 0xf, 0xf, false));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x114, 0xf, 0xf, false));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x118, 0xf, 0xf, false));
+  return x;
+}
+
 __device__ __forceinline__ f32x4 zero4() {
   f32x4 z = {0.f, 0.f, 0.f, 0.f};
   return z;

@@ -1,32 +1,33 @@
 // carve_fwd.hip -- chunked CARVE forward on gfx950.
 //
-// One workgroup per (batch, head) runs the whole sequence as a persistent
-// loop over gate chunks of L tokens (Alg. carve_fwd).  The recurrent state
-// S (Dv x Dk, f32) stays in registers for the whole call: wave w owns the key
-// column tiles [w*CPW, (w+1)*CPW) of S (16 columns each) for every value row,
-// in the MFMA result layout.  The shared parameters are staged in LDS once,
-// and the token inputs of the next WY tile are fetched into registers while
-// the current tile computes.
+// One workgroup per (batch, head) runs the whole sequence as a persistent loop
+// over gate chunks of L tokens (Alg. carve_fwd).  Wave w of the workgroup owns
+// the 16-wide tile w of the value axis AND the 16-wide tile w of the key axis:
+//   * the state lives in registers as S^T tiles (rows = key index j, columns =
+//     the wave's 16 value rows v), in the matrix-core result layout, for the
+//     whole call;
+//   * everything on the value side (predictions, WY solve products, outputs,
+//     state update) is wave-local, so the token-serial part of a chunk runs
+//     without barriers;
+//   * the key-side gate arithmetic of a chunk (erase gate, log retention, its
+//     prefix sums and the decayed keys/queries) runs on the wave's key tile.
 //
-// Per gate chunk c (state S_hat = S at the chunk start, Eq. content_readout):
-//   F = [Ub; Uw] S_hat            fold, read straight from the S registers
-// and then per WY tile of LW <= L tokens (the WY form of Sec. 6.2 applied to
-// consecutive sub-blocks of the chunk; the gates of every sub-block use the
-// same F, so this is the same computation as one L-token solve):
-//   tau = tanh(Q F^T), z_b = bx + tau_b Vb^T, z_w = wx + tau_w Vw^T
-//   l = g - softplus(z_b) (log of exp(g)(1-b)), w = sigmoid(z_w)
-//   Lam = prefix sums of l inside the tile, handled per 16-token block:
-//     E_t = e^{Lam_t - base}, E'_t = e^{Lam_{t-1} - base}, Kinv_t = k_t e^{base - Lam_t}
-//     with base = Lam at the end of the previous 16-block.
-//   A_ts = beta_t sum_j k_t k_s e^{Lam_{t-1}-Lam_s}   (s < t), built per 16x16
-//          tile as (k*E')_t . (Kinv_s * e^{base_ti - base_si}) so that no factor
-//          exceeds e^{(16-token log retention)} (Eq. M_coupling, re-derived)
-//   P_ts = sum_j q_t k_s e^{Lam_t - Lam_s}              (s <= t), same tiles
-//   T = (I + A)^{-1}   16x16 diagonal blocks by forward substitution, the
-//                      off-diagonal blocks by block substitution on MFMA
-//   R = beta (w*v - Ktil S^T), Ktil_t = k_t e^{Lam_{t-1}};  u = T R
-//   O = Qtil S^T + P u, Qtil_t = q_t e^{Lam_t}
-//   S <- S diag(e^{Lam_{LW-1}}) + u^T Khat, Khat_s = k_s e^{Lam_{LW-1} - Lam_s}
+// Per gate chunk c with start state S_hat (Eq. content_readout):
+//   F = [Ub; Uw] S_hat                         (fold, once per chunk)
+//   tau = tanh(q F^T), z_b = bx + tau_b Vb^T, z_w = wx + tau_w Vw^T
+//   l = g - softplus(z_b) = log(exp(g) (1 - b)), w = sigmoid(z_w)
+// and then, for consecutive 16-token blocks (the WY form of Sec. 6.2 applied
+// block by block; every block of the chunk uses the same gates' F), with
+// lam = prefix sums of l inside the block (lam_{-1} = 0), state S at the block
+// start and u the WY "pseudo values":
+//   Kt_t = k_t e^{lam_{t-1}},  Qt_t = q_t e^{lam_t},  Ki_s = k_s e^{-lam_s}
+//   A_ts = beta_t Kt_t . Ki_s (s < t),  P_ts = Qt_t . Ki_s (s <= t)
+//   T = (I + A)^{-1},  R_t = beta_t (w_t * v_t - S Kt_t),  u = T R
+//   o_t = S Qt_t + sum_s P_ts u_s
+//   S <- (S + sum_s u_s Ki_s^T) diag(e^{lam_15})
+// which is the recurrence of Eq. carve_state rewritten exactly (the factor
+// e^{-lam} undoes the block's decay up to token s).  A 16-token block keeps
+// every factor within e^{-(16-token log retention)}.
 //
 // Precondition (not checked): within any 16-token block the log retention
 // summed over the block stays above about -80 per key channel, so that
@@ -35,483 +36,325 @@
 
 namespace carve {
 
-template <typename T, int D, int LW>
+template <typename T, int D, int LW, int RP>
 __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
-  typedef Mma<T> M;
+  typedef Quad<T> Qd;
+  typedef typename Qd::q quad;
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
   constexpr int NT = fwd_threads(D);
-  constexpr int NW = NT / 64;         // waves
-  constexpr int NCT = D / 16;         // 16-column tiles of S (key side) / of the value side
-  constexpr int CPW = NCT / NW;       // column tiles per wave
-  constexpr int NB = LW / 16;         // 16-token blocks per WY tile
-  constexpr int NIT = D / 16;         // value-row tiles
-  constexpr int KS = M::KS, KPL = M::KPL;
-  constexpr int LK = lk_of<T, LW>();  // padded token extent of the K = LW products
-  // LDS row strides: every row is padded by 16 bytes so that the 16 rows read by
-  // one MFMA fragment load fall into distinct banks
+  constexpr int NW = NT / 64;          // waves == 16-wide tiles of the key / value axis
+  constexpr int NJT = D / 16;
+  constexpr int NB = LW / 16;          // 16-token blocks per sub-chunk
+  constexpr int R2 = 2 * RP;
+  constexpr int NRT = R2 / 16;         // 16-row tiles of [Ub; Uw] and of F
   constexpr int PAD = 16 / sizeof(T);
-  constexpr int LDD = D + PAD;        // rows of D elements
-  constexpr int LDK = LK + PAD;       // rows of LK elements
-  constexpr int LDA = LW + 4;         // rows of the f32 coupling matrix
-  constexpr int VEC = 16 / sizeof(T); // elements per 16-byte vector
-  constexpr int NVT = LW * D / VEC;                // 16-byte vectors of a q (or k) tile
-  constexpr int NQV = (NVT + NT - 1) / NT;         // per thread
-  const int RP = a.RP, R2 = 2 * a.RP, R = a.R;
-  const int LDR = R2 + PAD, LDV = RP + PAD;  // rows of 2RP / RP elements
-  const int H = a.H, Tn = a.T, L = a.L;
+  constexpr int LDD = D + PAD, LDR = R2 + PAD, LDB = 16 + PAD;
+  constexpr int VEC = 16 / sizeof(T);          // token elements per 16-byte vector
+  constexpr int NVQ = LW * D / VEC;            // 16-byte vectors of a q tile
+  constexpr int NQV = (NVQ + NT - 1) / NT;     // per thread
+  static_assert(NW == NJT, "one wave per 16-wide tile");
+  static_assert(D % 32 == 0, "K32 steps over the key / value axis");
+
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
+  const int H = a.H, Tn = a.T, L = a.L, R = a.R;
   const int bh = blockIdx.x, b = bh / H, h = bh % H;
   const int nch = Tn / L, msub = L / LW, ntiles = Tn / LW;
 
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const FwdLds lay = fwd_lds<T, D, LW>(RP);
-  T* sS = reinterpret_cast<T*>(smem + lay.S);
-  T* sQ = reinterpret_cast<T*>(smem + lay.Q);
-  T* sK = reinterpret_cast<T*>(smem + lay.K);
-  T* sKi = reinterpret_cast<T*>(smem + lay.Ki);
-  T* sF = reinterpret_cast<T*>(smem + lay.F);
-  T* sTau = reinterpret_cast<T*>(smem + lay.Tau);
-  T* sTb = sTau;                                  // alias: T, after tau is dead
-  T* sKhT = reinterpret_cast<T*>(smem + lay.KhT);
-  float* sA = reinterpret_cast<float*>(smem + lay.A);
-  T* sRT = sQ;                                    // alias: R^T [D][LK]
-  T* sUT = sK;                                    // alias: u^T [D][LK]
-  T* sP = sKi;                                    // alias: P [LW][LK]
-  float* sBase = reinterpret_cast<float*>(smem + lay.Base);   // [NB][D]  e^{base_ti}
-  float* sCf = reinterpret_cast<float*>(smem + lay.Cf);       // [NB*NB][D] e^{base_ti - base_si}
-  float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);   // [LW]
-  T* sU = reinterpret_cast<T*>(smem + lay.Ucat);              // [2RP][D] padded [Ub; Uw]
-  T* sVb = reinterpret_cast<T*>(smem + lay.Vb);               // [D][RP]
-  T* sVw = reinterpret_cast<T*>(smem + lay.Vw);               // [D][RP]
+  constexpr FwdLds lay = fwd_lds<T, D, LW, RP>();
+  T* sU = reinterpret_cast<T*>(smem + lay.U);      // [2RP][LDD]  [Ub; 0; Uw; 0]
+  T* sQ = reinterpret_cast<T*>(smem + lay.Q);      // [LW][LDD]   raw q
+  T* sF = reinterpret_cast<T*>(smem + lay.F);      // [2RP][LDD]  F
+  T* sTau = reinterpret_cast<T*>(smem + lay.Tau);  // [LW][LDR]   tau (b half | w half)
+  float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);
+  T* sS = reinterpret_cast<T*>(smem + lay.S);      // [D][LDD]    S_hat[v][j] (chunk start)
+  T* sKt = reinterpret_cast<T*>(smem + lay.Kt);    // [LW][LDD]
+  T* sQt = reinterpret_cast<T*>(smem + lay.Qt);    // [LW][LDD]
+  T* sKi = reinterpret_cast<T*>(smem + lay.Ki);    // [LW][LDD]
+  float* sGam = reinterpret_cast<float*>(smem + lay.Gam);  // [NB][D]     e^{lam_15}
+  float* sAT = reinterpret_cast<float*>(smem + lay.AT);    // [NB][16][20] A^T per block
+  T* sTm = reinterpret_cast<T*>(smem + lay.Tm);            // [NB][16][LDB] T per block
+  T* sP = reinterpret_cast<T*>(smem + lay.P);              // [NB][16][LDB] P per block
 
-  const T* __restrict__ q = reinterpret_cast<const T*>(a.q);
-  const T* __restrict__ k = reinterpret_cast<const T*>(a.k);
-  const T* __restrict__ v = reinterpret_cast<const T*>(a.v);
-  const T* __restrict__ bx = reinterpret_cast<const T*>(a.bx);
-  const T* __restrict__ wx = reinterpret_cast<const T*>(a.wx);
-  const T* __restrict__ beta = reinterpret_cast<const T*>(a.beta);
   // token tensors addressed from this (batch, head)'s first element with 32-bit
   // offsets t * rs + column (rs = H * D elements between consecutive tokens)
   const size_t bh0 = ((size_t)b * Tn * H + h) * D;
   const size_t bh1 = (size_t)b * Tn * H + h;
   const int rs = H * D;
-  q += bh0; k += bh0; v += bh0; bx += bh0; wx += bh0; beta += bh1;
+  const T* __restrict__ q = reinterpret_cast<const T*>(a.q) + bh0;
+  const T* __restrict__ k = reinterpret_cast<const T*>(a.k) + bh0;
+  const T* __restrict__ v = reinterpret_cast<const T*>(a.v) + bh0;
+  const T* __restrict__ bx = reinterpret_cast<const T*>(a.bx) + bh0;
+  const T* __restrict__ wx = reinterpret_cast<const T*>(a.wx) + bh0;
+  const T* __restrict__ beta = reinterpret_cast<const T*>(a.beta) + bh1;
   const float* __restrict__ gl = a.g + bh0;
   T* __restrict__ o = reinterpret_cast<T*>(a.o) + bh0;
 
-  // ---- shared parameters -> LDS (zero padded to RP) ------------------------
+  // ---- shared parameters ------------------------------------------------------
   for (int x = tid; x < R2 * D; x += NT) {
     const int rr = x / D, i = x % D;
     float u = 0.0f;
-    if (rr < R) u = a.Ub[(size_t)rr * D + i];
-    else if (rr >= RP && rr < RP + R) u = a.Uw[(size_t)(rr - RP) * D + i];
+    if (rr < R) u = a.Ub[rr * D + i];
+    else if (rr >= RP && rr < RP + R) u = a.Uw[(rr - RP) * D + i];
     sU[rr * LDD + i] = (T)u;
   }
-  for (int x = tid; x < D * RP; x += NT) {
-    const int j = x / RP, rr = x % RP;
-    sVb[j * LDV + rr] = (T)(rr < R ? a.Vb[(size_t)j * R + rr] : 0.0f);
-    sVw[j * LDV + rr] = (T)(rr < R ? a.Vw[(size_t)j * R + rr] : 0.0f);
-  }
-
-  // ---- state registers: S[cq][it][r] = S[16*it + 4g + r][16*(w*CPW+cq) + c] ----
-  f32x4 S[CPW][NIT];
-  const size_t soff = (size_t)bh * D * D;
-  for (int cq = 0; cq < CPW; ++cq) {
-    const int col = 16 * (w * CPW + cq) + c;
-    for (int it = 0; it < NIT; ++it) {
-      for (int r = 0; r < 4; ++r)
-        S[cq][it][r] = a.S0 ? a.S0[soff + (size_t)(16 * it + 4 * g + r) * D + col] : 0.0f;
-      store_tile(sS, LDD, 16 * it, 16 * (w * CPW + cq), S[cq][it], lane);
+  // Vb / Vw as constant operand quads: lane (g, c) holds V[16 w + c][16 ks + 4 g + e]
+  quad fVb[RP / 16], fVw[RP / 16];
+  for (int ks = 0; ks < RP / 16; ++ks) {
+    f32x4 tb, tw;
+    for (int e = 0; e < 4; ++e) {
+      const int r = 16 * ks + 4 * g + e;
+      tb[e] = r < R ? a.Vb[(16 * w + c) * R + r] : 0.0f;
+      tw[e] = r < R ? a.Vw[(16 * w + c) * R + r] : 0.0f;
     }
+    fVb[ks] = Qd::cvt(tb);
+    fVw[ks] = Qd::cvt(tw);
+  }
+  // identity operand: lane (g, c) holds I[4 g + e][c]
+  quad fI;
+  {
+    f32x4 t;
+    for (int e = 0; e < 4; ++e) t[e] = (4 * g + e == c) ? 1.0f : 0.0f;
+    fI = Qd::cvt(t);
   }
 
-  // ---- prefetch registers for the next WY tile ---------------------------
-  f32x4 pq[NQV], pk[NQV];
-  float pbx[CPW][NB][4], pg[CPW][NB][4], pwx[CPW][NB][4], pv[CPW][NB][4];
-  float pbeta = 0.0f;
-#define CARVE_FWD_PREFETCH_QK(TILE_)                                                    \
+  // ---- state: St[jt][i] = S[v = 16 w + c][j = 16 jt + 4 g + i] ---------------
+  f32x4 St[NJT];
+  const size_t soff = (size_t)bh * D * D;
+  for (int jt = 0; jt < NJT; ++jt)
+    St[jt] = a.S0 ? gload4(a.S0 + soff + (16 * w + c) * D + 16 * jt + 4 * g) : zero4();
+
+  // ---- prefetch registers for the next sub-chunk ------------------------------
+  u32x4 pq[NQV];
+  T pbeta = (T)0.0f;
+  quad pbx[NB], pk[NB], pwx[NB], pv[NB];
+  f32x4 pg[NB];
+#define CARVE_FWD_PREFETCH_Q(TILE_)                                                     \
   do {                                                                                  \
     const int tt0_ = (TILE_) * LW;                                                      \
-    for (int u = 0; u < NQV; ++u) {                                                     \
-      const int x = tid + u * NT;                                                       \
-      if (NVT % NT != 0 && x >= NVT) break;                                             \
-      const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;                           \
-      const int gofs = (tt0_ + t) * rs + j;                                             \
-      pq[u] = *reinterpret_cast<const f32x4*>(q + gofs);                                \
-      pk[u] = *reinterpret_cast<const f32x4*>(k + gofs);                                \
+    for (int u_ = 0; u_ < NQV; ++u_) {                                                  \
+      const int x_ = tid + u_ * NT;                                                     \
+      if (NVQ % NT != 0 && x_ >= NVQ) break;                                            \
+      const int t_ = x_ / (D / VEC), j_ = (x_ % (D / VEC)) * VEC;                       \
+      pq[u_] = *reinterpret_cast<const u32x4*>(q + (tt0_ + t_) * rs + j_);              \
     }                                                                                   \
-    if (tid < LW) pbeta = to_f(beta[(tt0_ + tid) * H]);                                 \
+    if (tid < LW) pbeta = beta[(tt0_ + tid) * H];                                       \
   } while (0)
 #define CARVE_FWD_PREFETCH_GATES(TILE_)                                                 \
   do {                                                                                  \
     const int tt0_ = (TILE_) * LW;                                                      \
-    for (int cq = 0; cq < CPW; ++cq) {                                                  \
-      const int col_ = 16 * (w * CPW + cq) + c;                                         \
-      for (int ti = 0; ti < NB; ++ti)                                                   \
-        for (int r = 0; r < 4; ++r) {                                                   \
-          const int e_ = (tt0_ + 16 * ti + 4 * g + r) * rs + col_;                      \
-          pbx[cq][ti][r] = to_f(bx[e_]);                                                \
-          pg[cq][ti][r] = gl[e_];                                                       \
-          pwx[cq][ti][r] = to_f(wx[e_]);                                                \
-          pv[cq][ti][r] = to_f(v[e_]);                                                  \
-        }                                                                               \
+    for (int bb_ = 0; bb_ < NB; ++bb_) {                                                \
+      const int e_ = (tt0_ + 16 * bb_ + c) * rs + 16 * w + 4 * g;                       \
+      pbx[bb_] = Qd::ld(bx + e_);                                                       \
+      pk[bb_] = Qd::ld(k + e_);                                                         \
+      pwx[bb_] = Qd::ld(wx + e_);                                                       \
+      pv[bb_] = Qd::ld(v + e_);                                                         \
+      pg[bb_] = *reinterpret_cast<const f32x4*>(gl + e_);                               \
     }                                                                                   \
   } while (0)
-  CARVE_FWD_PREFETCH_QK(0);
+  CARVE_FWD_PREFETCH_Q(0);
   CARVE_FWD_PREFETCH_GATES(0);
 
+  int tile = 0;
   for (int ch = 0; ch < nch; ++ch) {
-    if (a.S_chunks) {
-      float* dst = a.S_chunks + ((size_t)bh * nch + ch) * D * D;
-      for (int cq = 0; cq < CPW; ++cq) {
-        const int col = 16 * (w * CPW + cq) + c;
-        for (int it = 0; it < NIT; ++it)
-          for (int r = 0; r < 4; ++r) dst[(size_t)(16 * it + 4 * g + r) * D + col] = S[cq][it][r];
-      }
-    }
-    for (int m = 0; m < msub; ++m) {
-      const int tile = ch * msub + m;
+    for (int m = 0; m < msub; ++m, ++tile) {
       const int t0 = tile * LW;
 
-      // ---- P0: q, k tiles and beta from the prefetch registers -------------
+      // ---- P0: stage q and beta; chunk start state ----------------------------
+      if (m == 0) {
+        if (a.S_chunks) {
+          float* dst = a.S_chunks + ((size_t)bh * nch + ch) * D * D + (16 * w + c) * D + 4 * g;
+          for (int jt = 0; jt < NJT; ++jt) *reinterpret_cast<f32x4*>(dst + 16 * jt) = St[jt];
+        }
+        for (int jt = 0; jt < NJT; ++jt) Qd::st(sS + (16 * w + c) * LDD + 16 * jt + 4 * g, Qd::cvt(St[jt]));
+      }
       for (int u = 0; u < NQV; ++u) {
         const int x = tid + u * NT;
-        if (NVT % NT != 0 && x >= NVT) break;
+        if (NVQ % NT != 0 && x >= NVQ) break;
         const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;
-        *reinterpret_cast<f32x4*>(sQ + t * LDD + j) = pq[u];
-        *reinterpret_cast<f32x4*>(sK + t * LDD + j) = pk[u];
+        *reinterpret_cast<u32x4*>(sQ + t * LDD + j) = pq[u];
       }
-      if (tid < LW) sBeta[tid] = pbeta;
-      if (tile + 1 < ntiles) CARVE_FWD_PREFETCH_QK(tile + 1);
-      // ---- P1: fold F = [Ub;Uw] S_hat from the state registers ---------------
+      if (tid < LW) sBeta[tid] = (float)pbeta;
+      if (tile + 1 < ntiles) CARVE_FWD_PREFETCH_Q(tile + 1);
+      __syncthreads();
+
+      // ---- P1: fold F^T[j][r] = sum_v S_hat[v][j] U[r][v] (key tile w) -------
       if (m == 0) {
-        for (int cq = 0; cq < CPW; ++cq) {
-          const int ct = w * CPW + cq;
-          for (int rt = 0; rt < R2 / 16; ++rt) {
-            const T* urow = sU + (16 * rt + c) * LDD;  // B row this lane supplies
-            f32x4 acc = zero4();
-            if constexpr (KPL == 8) {
-              for (int ks = 0; ks < D / 32; ++ks) {
-                typename M::frag af, bfg;
-                const T* p = urow + 32 * ks + 4 * g;
-                for (int e = 0; e < 4; ++e) {
-                  af[e] = (T)S[cq][2 * ks][e];
-                  af[4 + e] = (T)S[cq][2 * ks + 1][e];
-                  bfg[e] = p[e];
-                  bfg[4 + e] = p[16 + e];
-                }
-                acc = M::mma(af, bfg, acc);
-              }
-            } else {
-              for (int it = 0; it < NIT; ++it)
-                for (int r4 = 0; r4 < 4; ++r4) acc = M::mma((T)S[cq][it][r4], urow[16 * it + 4 * g + r4], acc);
-            }
-            // acc = F^T[j = 16ct + 4g + r][16rt + c]  ->  sF[r][j]
-            store_tile_t(sF, LDD, 16 * ct, 16 * rt, acc, lane);
-          }
-        }
-      }
-      __syncthreads();
-
-      // ---- P2: tau = tanh(Q F^T) -> sTau [LW][2RP] ----------------------------
-      {
-        const int ntl = NB * (R2 / 16);
-        for (int x = w; x < ntl; x += NW) {
-          const int ti = x / (R2 / 16), rt = x % (R2 / 16);
+        for (int rt = 0; rt < NRT; ++rt) {
           f32x4 acc = zero4();
-          for (int ks = 0; ks < D / KS; ++ks) {
-            const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load(sQ + (16 * ti + c) * LDD + kofs), M::load(sF + (16 * rt + c) * LDD + kofs), acc);
+          for (int vp = 0; vp < D / 32; ++vp) {
+            const quad a0 = Qd::ld_tr(sS, LDD, 32 * vp, 16 * w, g, c);
+            const quad a1 = Qd::ld_tr(sS, LDD, 32 * vp + 16, 16 * w, g, c);
+            const T* ur = sU + (16 * rt + c) * LDD + 32 * vp + 4 * g;
+            acc = Qd::mma32(a0, a1, Qd::ld(ur), Qd::ld(ur + 16), acc);
           }
-          for (int r = 0; r < 4; ++r) acc[r] = tanh_f(acc[r]);
-          store_tile(sTau, LDR, 16 * ti, 16 * rt, acc, lane);
-        }
-      }
-      __syncthreads();
-
-      // ---- P3: gate logits (key side: l; value side: w*v) --------------------
-      float ell[CPW][NB][4];
-      float wv[CPW][NB][4];
-      for (int cq = 0; cq < CPW; ++cq) {
-        const int ct = w * CPW + cq;
-        const T* vbrow = sVb + (16 * ct + c) * LDV;
-        const T* vwrow = sVw + (16 * ct + c) * LDV;
-        for (int ti = 0; ti < NB; ++ti) {
-          f32x4 accB = zero4(), accW = zero4();
-          for (int ks = 0; ks < RP / KS; ++ks) {
-            const int r0 = ks * KS + g * KPL;
-            const int arow = (16 * ti + c) * LDR;
-            accB = M::mma(M::load(sTau + arow + r0), M::load(vbrow + r0), accB);
-            accW = M::mma(M::load(sTau + arow + RP + r0), M::load(vwrow + r0), accW);
-          }
-          for (int r = 0; r < 4; ++r) {
-            const float zb = pbx[cq][ti][r] + accB[r];
-            ell[cq][ti][r] = pg[cq][ti][r] - softplus_f(zb);
-            wv[cq][ti][r] = sigmoid_f(pwx[cq][ti][r] + accW[r]) * pv[cq][ti][r];
-          }
-        }
-      }
-      if (tile + 1 < ntiles) CARVE_FWD_PREFETCH_GATES(tile + 1);
-
-      // ---- P4: key-side retention factors --------------------------------------
-      float gamma_col[CPW];  // e^{Lam_{LW-1}} for key column 16(w*CPW+cq) + c
-      for (int cq = 0; cq < CPW; ++cq) {
-        const int ct = w * CPW + cq;
-        const int jj = 16 * ct + c;
-        float base = 0.0f;  // Lam at the end of the previous block
-        float bases[NB];
-        for (int ti = 0; ti < NB; ++ti) {
-          float p[4];
-          p[0] = ell[cq][ti][0];
-          p[1] = p[0] + ell[cq][ti][1];
-          p[2] = p[1] + ell[cq][ti][2];
-          p[3] = p[2] + ell[cq][ti][3];
-          float incl = p[3];
-          float y = __shfl_up(incl, 16);
-          if (g >= 1) incl += y;
-          y = __shfl_up(incl, 32);
-          if (g >= 2) incl += y;
-          const float excl = incl - p[3];
-          const float btot = __shfl(incl, 48 + c);   // block log retention
-          float E[4], Ep[4], Ki[4];
-          for (int r = 0; r < 4; ++r) {
-            const float lrel = excl + p[r];
-            E[r] = fast_exp(lrel);
-            Ki[r] = fast_exp(-lrel);
-          }
-          const float Eprev = __shfl_up(E[3], 16);
-          Ep[0] = g == 0 ? 1.0f : Eprev;
-          Ep[1] = E[0];
-          Ep[2] = E[1];
-          Ep[3] = E[2];
-          for (int r = 0; r < 4; ++r) {
-            const int t = 16 * ti + 4 * g + r;
-            const float kv = to_f(sK[t * LDD + jj]);
-            const float qv = to_f(sQ[t * LDD + jj]);
-            sK[t * LDD + jj] = (T)(kv * Ep[r]);
-            sQ[t * LDD + jj] = (T)(qv * E[r]);
-            Ki[r] *= kv;
-            sKi[t * LDD + jj] = (T)Ki[r];
-            ell[cq][ti][r] = Ki[r];  // keep k e^{-Lam_rel}
-          }
-          bases[ti] = base;
-          base += btot;
-        }
-        const float lam_end = base;  // Lam_{LW-1}
-        gamma_col[cq] = fast_exp(lam_end);
-        for (int ti = 0; ti < NB; ++ti) {
-          // Khat^T[j][s] = Kinv_s e^{Lam_end - base_si}
-          const float f = fast_exp(lam_end - bases[ti]);
-          f32x4 kh;
-          for (int r = 0; r < 4; ++r) kh[r] = ell[cq][ti][r] * f;
-          store_tile_t(sKhT, LDK, 16 * ti, 16 * ct, kh, lane);
-          if (g == 0) {
-            sBase[ti * D + jj] = fast_exp(bases[ti]);
-            for (int si = 0; si < ti; ++si) sCf[(ti * NB + si) * D + jj] = fast_exp(bases[ti] - bases[si]);
-          }
-        }
-      }
-      __syncthreads();
-
-      // ---- P5: A, P (lower 16x16 tiles) and Ktil S^T, Qtil S^T ------------------
-      constexpr int NTRI = NB * (NB + 1) / 2;
-      constexpr int PPW = (NTRI + NW - 1) / NW;
-      f32x4 Pkeep[PPW];
-      {
-        int slot = 0;
-        for (int x = w; x < NTRI; x += NW, ++slot) {
-          int ti = 0, si = x;
-          while (si > ti) { si -= ti + 1; ++ti; }
-          f32x4 accA = zero4(), accP = zero4();
-          for (int ks = 0; ks < D / KS; ++ks) {
-            const int kofs = ks * KS + g * KPL;
-            const T* kb = sKi + (16 * si + c) * LDD + kofs;
-            const typename M::frag bf = (ti == si) ? M::load(kb) : M::load_scaled(kb, sCf + (ti * NB + si) * D + kofs);
-            accA = M::mma(M::load(sK + (16 * ti + c) * LDD + kofs), bf, accA);
-            accP = M::mma(M::load(sQ + (16 * ti + c) * LDD + kofs), bf, accP);
-          }
-          for (int r = 0; r < 4; ++r) {
-            const int tl = 4 * g + r;  // row inside the tile
-            const bool lowA = (ti > si) || (c < tl);
-            const bool lowP = (ti > si) || (c <= tl);
-            sA[(16 * ti + tl) * LDA + 16 * si + c] = lowA ? sBeta[16 * ti + tl] * accA[r] : 0.0f;
-            accP[r] = lowP ? accP[r] : 0.0f;
-          }
-          Pkeep[slot] = accP;
-        }
-      }
-      f32x4 XK[CPW][NB], XQ[CPW][NB];
-      for (int cq = 0; cq < CPW; ++cq) {
-        const int ct = w * CPW + cq;
-        for (int ti = 0; ti < NB; ++ti) {
-          f32x4 ak = zero4(), aq = zero4();
-          for (int ks = 0; ks < D / KS; ++ks) {
-            const int kofs = ks * KS + g * KPL;
-            const typename M::frag sb = M::load(sS + (16 * ct + c) * LDD + kofs);
-            const float* sc = sBase + ti * D + kofs;
-            ak = M::mma(M::load_scaled(sK + (16 * ti + c) * LDD + kofs, sc), sb, ak);
-            aq = M::mma(M::load_scaled(sQ + (16 * ti + c) * LDD + kofs, sc), sb, aq);
-          }
-          XK[cq][ti] = ak;
-          XQ[cq][ti] = aq;
-        }
-      }
-      __syncthreads();
-      // epilogues into the aliased buffers
-      {
-        int slot = 0;
-        for (int x = w; x < NTRI; x += NW, ++slot) {
-          int ti = 0, si = x;
-          while (si > ti) { si -= ti + 1; ++ti; }
-          store_tile(sP, LDK, 16 * ti, 16 * si, Pkeep[slot], lane);
-        }
-        // zero the upper tiles (and padding columns) of P and T, and the
-        // padding columns of R^T, u^T and Khat^T (read by the 32-wide K steps)
-        for (int x = tid; x < LW * LK; x += NT) {
-          const int rr = x / LK, cc = x % LK;
-          if ((cc >> 4) > (rr >> 4)) {
-            sP[rr * LDK + cc] = (T)0.0f;
-            sTb[rr * LDK + cc] = (T)0.0f;
-          }
-        }
-        if constexpr (LK > LW) {
-          for (int x = tid; x < D * (LK - LW); x += NT) {
-            const int rr = x / (LK - LW), cc = LW + x % (LK - LW);
-            sRT[rr * LDK + cc] = (T)0.0f;
-            sUT[rr * LDK + cc] = (T)0.0f;
-            sKhT[rr * LDK + cc] = (T)0.0f;
-          }
-        }
-        for (int cq = 0; cq < CPW; ++cq)
-          for (int ti = 0; ti < NB; ++ti) {
-            f32x4 rv;
-            for (int r = 0; r < 4; ++r) rv[r] = sBeta[16 * ti + 4 * g + r] * (wv[cq][ti][r] - XK[cq][ti][r]);
-            store_tile_t(sRT, LDK, 16 * ti, 16 * (w * CPW + cq), rv, lane);
-          }
-      }
-      __syncthreads();
-
-      // ---- P6: T = (I + A)^{-1} -----------------------------------------------
-      if (w == 0 && g < NB) {
-        // diagonal block g: column c by forward substitution, A rows in registers
-        const float* Ab = sA + (16 * g) * LDA + 16 * g;
-        float arow[16][16];
-#pragma unroll
-        for (int t = 1; t < 16; ++t)
-#pragma unroll
-          for (int s4 = 0; s4 < (t + 3) / 4; ++s4) {
-            const f32x4 v4 = *reinterpret_cast<const f32x4*>(Ab + t * LDA + 4 * s4);
-            arow[t][4 * s4] = v4[0];
-            arow[t][4 * s4 + 1] = v4[1];
-            arow[t][4 * s4 + 2] = v4[2];
-            arow[t][4 * s4 + 3] = v4[3];
-          }
-        float x[16];
-#pragma unroll
-        for (int t = 0; t < 16; ++t) {
-          float acc = (t == c) ? 1.0f : 0.0f;
-#pragma unroll
-          for (int s = 0; s < t; ++s) acc -= arow[t][s] * x[s];
-          x[t] = acc;
-        }
-        float* Aw = sA + (16 * g) * LDA + 16 * g;
-        T* Tw = sTb + (16 * g) * LDK + 16 * g;
-#pragma unroll
-        for (int t = 0; t < 16; ++t) {
-          Aw[t * LDA + c] = x[t];
-          Tw[t * LDK + c] = (T)x[t];
-        }
-      }
-      __syncthreads();
-      if constexpr (NB > 1) {
-        for (int j = w; j < NB - 1; j += NW) {
-          f32x4 Tc[NB];
-          for (int i = j + 1; i < NB; ++i) {
-            f32x4 X = zero4();
-            for (int kb = j; kb < i; ++kb) {
-              for (int ks = 0; ks < 4; ++ks) {
-                const float av = sA[(16 * i + c) * LDA + 16 * kb + 4 * g + ks];
-                const float bv = (kb == j) ? sA[(16 * kb + 4 * g + ks) * LDA + 16 * j + c] : Tc[kb][ks];
-                X = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, X, 0, 0, 0);
-              }
-            }
-            f32x4 Y = zero4();
-            for (int ks = 0; ks < 4; ++ks) {
-              const float av = sA[(16 * i + c) * LDA + 16 * i + 4 * g + ks];
-              Y = __builtin_amdgcn_mfma_f32_16x16x4f32(av, X[ks], Y, 0, 0, 0);
-            }
-            for (int r = 0; r < 4; ++r) Y[r] = -Y[r];
-            Tc[i] = Y;
-            store_tile(sTb, LDK, 16 * i, 16 * j, Y, lane);
-          }
+          Qd::st(sF + (16 * rt + c) * LDD + 16 * w + 4 * g, Qd::cvt(acc));
         }
         __syncthreads();
       }
 
-      // ---- P7: u = T R -> sUT -----------------------------------------------
-      for (int cq = 0; cq < CPW; ++cq) {
-        const int ct = w * CPW + cq;
-        for (int ti = 0; ti < NB; ++ti) {
-          f32x4 acc = zero4();
-          const int kmax = (16 * (ti + 1) + KS - 1) / KS;
-          for (int ks = 0; ks < kmax; ++ks) {
-            const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load(sTb + (16 * ti + c) * LDK + kofs), M::load(sRT + (16 * ct + c) * LDK + kofs), acc);
-          }
-          store_tile_t(sUT, LDK, 16 * ti, 16 * ct, acc, lane);
+      // ---- P2: tau^T[r][t] = tanh(F[r] . q_t) -> sTau[t][r] -------------------
+      for (int x = w; x < NRT * NB; x += NW) {
+        const int rt = x % NRT, bb = x / NRT;
+        f32x4 acc = zero4();
+        for (int jp = 0; jp < D / 32; ++jp) {
+          const T* fr = sF + (16 * rt + c) * LDD + 32 * jp + 4 * g;
+          const T* qr = sQ + (16 * bb + c) * LDD + 32 * jp + 4 * g;
+          acc = Qd::mma32(Qd::ld(fr), Qd::ld(fr + 16), Qd::ld(qr), Qd::ld(qr + 16), acc);
+        }
+        for (int i = 0; i < 4; ++i) acc[i] = tanh_f(acc[i]);
+        Qd::st(sTau + (16 * bb + c) * LDR + 16 * rt + 4 * g, Qd::cvt(acc));
+      }
+      __syncthreads();
+
+      // ---- P3: gates ------------------------------------------------------------
+      // key side, key tile w: lane (g, c) of block bb holds t = 16 bb + c and
+      // j = 16 w + 4 g + i (i = 0..3); the prefix sums run along the 16 lanes
+      // of a row
+      for (int bb = 0; bb < NB; ++bb) {
+        f32x4 z = zero4();
+        for (int ks = 0; ks < RP / 16; ++ks)
+          z = Qd::mma16(fVb[ks], Qd::ld(sTau + (16 * bb + c) * LDR + 16 * ks + 4 * g), z);
+        const f32x4 bxv = Qd::f32(pbx[bb]), kv = Qd::f32(pk[bb]), gv = pg[bb];
+        const f32x4 qv = Qd::f32(Qd::ld(sQ + (16 * bb + c) * LDD + 16 * w + 4 * g));
+        f32x4 kt, qt, ki, gam;
+        for (int i = 0; i < 4; ++i) {
+          const float ell = gv[i] - softplus_f(z[i] + bxv[i]);
+          const float lam = row_scan(ell);
+          const float E = fast_exp(lam);
+          const float Ep = row_shr1(E, 1.0f);
+          kt[i] = kv[i] * Ep;
+          qt[i] = qv[i] * E;
+          ki[i] = kv[i] * fast_exp(-lam);
+          gam[i] = E;
+        }
+        const int ro = (16 * bb + c) * LDD + 16 * w + 4 * g;
+        Qd::st(sKt + ro, Qd::cvt(kt));
+        Qd::st(sQt + ro, Qd::cvt(qt));
+        Qd::st(sKi + ro, Qd::cvt(ki));
+        if (c == 15) *reinterpret_cast<f32x4*>(sGam + bb * D + 16 * w + 4 * g) = gam;
+      }
+      // value side, value tile w: rows t = 16 bb + 4 g + i, column v = 16 w + c
+      f32x4 wv[NB];
+      for (int bb = 0; bb < NB; ++bb) {
+        f32x4 z = zero4();
+        for (int ks = 0; ks < RP / 16; ++ks)
+          z = Qd::mma16(Qd::ld(sTau + (16 * bb + c) * LDR + RP + 16 * ks + 4 * g), fVw[ks], z);
+        z = Qd::mma16(pwx[bb], fI, z);                   // + wx, moved into this layout
+        const f32x4 vv = Qd::mma16(pv[bb], fI, zero4());
+        for (int i = 0; i < 4; ++i) wv[bb][i] = sigmoid_f(z[i]) * vv[i];
+      }
+      if (tile + 1 < ntiles) CARVE_FWD_PREFETCH_GATES(tile + 1);
+      __syncthreads();
+
+      // ---- P4: A^T and P of every block ---------------------------------------
+      for (int x = w; x < 2 * NB; x += NW) {
+        const bool isP = x >= NB;
+        const int bb = isP ? x - NB : x;
+        const T* ar = (isP ? sKi : sKt) + (16 * bb + c) * LDD + 4 * g;
+        const T* br = (isP ? sQt : sKi) + (16 * bb + c) * LDD + 4 * g;
+        f32x4 acc = zero4();
+        for (int jp = 0; jp < D / 32; ++jp)
+          acc = Qd::mma32(Qd::ld(ar + 32 * jp), Qd::ld(ar + 32 * jp + 16), Qd::ld(br + 32 * jp),
+                          Qd::ld(br + 32 * jp + 16), acc);
+        if (!isP) {
+          // acc[i] = Kt_{t=4g+i} . Ki_{s=c}
+          const f32x4 bt = *reinterpret_cast<const f32x4*>(sBeta + 16 * bb + 4 * g);
+          f32x4 av;
+          for (int i = 0; i < 4; ++i) av[i] = (c < 4 * g + i) ? bt[i] * acc[i] : 0.0f;
+          *reinterpret_cast<f32x4*>(sAT + (bb * 16 + c) * 20 + 4 * g) = av;
+        } else {
+          // acc[i] = Ki_{s=4g+i} . Qt_{t=c}
+          f32x4 pv4;
+          for (int i = 0; i < 4; ++i) pv4[i] = (4 * g + i <= c) ? acc[i] : 0.0f;
+          Qd::st(sP + (bb * 16 + c) * LDB + 4 * g, Qd::cvt(pv4));
         }
       }
       __syncthreads();
 
-      // ---- P8: outputs and state carry --------------------------------------
-      for (int cq = 0; cq < CPW; ++cq) {
-        const int ct = w * CPW + cq;
-        for (int ti = 0; ti < NB; ++ti) {
-          f32x4 acc = XQ[cq][ti];
-          const int kmax = (16 * (ti + 1) + KS - 1) / KS;
-          for (int ks = 0; ks < kmax; ++ks) {
-            const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load(sP + (16 * ti + c) * LDK + kofs), M::load(sUT + (16 * ct + c) * LDK + kofs), acc);
+      // ---- P5: T = (I + A)^{-1} per block; first block's state products --------
+      quad sb[NJT];
+      for (int jt = 0; jt < NJT; ++jt) sb[jt] = Qd::cvt(St[jt]);
+      f32x4 XK = zero4(), XQ = zero4();
+#define CARVE_FWD_XKQ(BB_)                                                               \
+  do {                                                                                   \
+    XK = zero4();                                                                        \
+    XQ = zero4();                                                                        \
+    const T* kr_ = sKt + (16 * (BB_) + c) * LDD + 4 * g;                                 \
+    const T* qr_ = sQt + (16 * (BB_) + c) * LDD + 4 * g;                                 \
+    for (int jp_ = 0; jp_ < NJT / 2; ++jp_) {                                            \
+      XK = Qd::mma32(Qd::ld(kr_ + 32 * jp_), Qd::ld(kr_ + 32 * jp_ + 16), sb[2 * jp_],   \
+                     sb[2 * jp_ + 1], XK);                                               \
+      XQ = Qd::mma32(Qd::ld(qr_ + 32 * jp_), Qd::ld(qr_ + 32 * jp_ + 16), sb[2 * jp_],   \
+                     sb[2 * jp_ + 1], XQ);                                               \
+    }                                                                                    \
+  } while (0)
+      if (w == NW - 1) {
+        // lane (g, c): block g, row c of T, by substitution on
+        //   T[c][s] = delta(c, s) - sum_{t > s} T[c][t] A[t][s],  s = 15 .. 0
+        if (g < NB) {
+          const float* Ab = sAT + g * 16 * 20;
+          float x[16];
+#pragma unroll
+          for (int s = 15; s >= 0; --s) {
+            float acc0 = (s == c) ? 1.0f : 0.0f, acc1 = 0.0f;
+#pragma unroll
+            for (int t = s + 1; t < 16; ++t) {
+              if ((t - s) & 1) acc0 -= x[t] * Ab[s * 20 + t];
+              else acc1 -= x[t] * Ab[s * 20 + t];
+            }
+            x[s] = acc0 + acc1;
           }
-          for (int r = 0; r < 4; ++r) {
-            const int t = 16 * ti + 4 * g + r;
-            o[(t0 + t) * rs + 16 * ct + c] = (T)acc[r];
+          T* tr = sTm + (g * 16 + c) * LDB;
+#pragma unroll
+          for (int s4 = 0; s4 < 4; ++s4) {
+            f32x4 t4 = {x[4 * s4], x[4 * s4 + 1], x[4 * s4 + 2], x[4 * s4 + 3]};
+            Qd::st(tr + 4 * s4, Qd::cvt(t4));
           }
         }
       }
-      for (int cq = 0; cq < CPW; ++cq) {
-        const int ct = w * CPW + cq;
-        for (int it = 0; it < NIT; ++it) {
-          f32x4 acc;
-          for (int r = 0; r < 4; ++r) acc[r] = S[cq][it][r] * gamma_col[cq];
-          for (int ks = 0; ks < LK / KS; ++ks) {
-            const int kofs = ks * KS + g * KPL;
-            acc = M::mma(M::load(sUT + (16 * it + c) * LDK + kofs), M::load(sKhT + (16 * ct + c) * LDK + kofs), acc);
-          }
-          S[cq][it] = acc;
+      CARVE_FWD_XKQ(0);
+      __syncthreads();
+
+      // ---- P6: token-serial blocks on the value tile (no barriers) --------------
+      for (int bb = 0; bb < NB; ++bb) {
+        if (bb > 0) CARVE_FWD_XKQ(bb);
+        const f32x4 bt = *reinterpret_cast<const f32x4*>(sBeta + 16 * bb + 4 * g);
+        f32x4 rr;
+        for (int i = 0; i < 4; ++i) rr[i] = bt[i] * (wv[bb][i] - XK[i]);
+        const f32x4 u = Qd::mma16(Qd::ld(sTm + (bb * 16 + c) * LDB + 4 * g), Qd::cvt(rr), zero4());
+        const quad uq = Qd::cvt(u);
+        const f32x4 O = Qd::mma16(Qd::ld(sP + (bb * 16 + c) * LDB + 4 * g), uq, XQ);
+        // o^T through the identity: lane (g, c) gets o[t = c][v = 4 g + i]
+        const f32x4 Ot = Qd::mma16(Qd::cvt(O), fI, zero4());
+        Qd::st(o + (t0 + 16 * bb + c) * rs + 16 * w + 4 * g, Qd::cvt(Ot));
+        for (int jt = 0; jt < NJT; ++jt) {
+          const f32x4 acc = Qd::mma16(Qd::ld_tr(sKi, LDD, 16 * bb, 16 * jt, g, c), uq, St[jt]);
+          const f32x4 gm = *reinterpret_cast<const f32x4*>(sGam + bb * D + 16 * jt + 4 * g);
+          for (int i = 0; i < 4; ++i) St[jt][i] = acc[i] * gm[i];
+          sb[jt] = Qd::cvt(St[jt]);
         }
       }
-      __syncthreads();  // every wave is done reading sS (P5) and the aliases
-      for (int cq = 0; cq < CPW; ++cq)
-        for (int it = 0; it < NIT; ++it) store_tile(sS, LDD, 16 * it, 16 * (w * CPW + cq), S[cq][it], lane);
+#undef CARVE_FWD_XKQ
+      __syncthreads();  // the next sub-chunk overwrites sQ, sBeta and region X
     }
   }
   if (a.S_T) {
-    for (int cq = 0; cq < CPW; ++cq) {
-      const int col = 16 * (w * CPW + cq) + c;
-      for (int it = 0; it < NIT; ++it)
-        for (int r = 0; r < 4; ++r) a.S_T[soff + (size_t)(16 * it + 4 * g + r) * D + col] = S[cq][it][r];
-    }
+    float* dst = a.S_T + soff + (16 * w + c) * D + 4 * g;
+    for (int jt = 0; jt < NJT; ++jt) *reinterpret_cast<f32x4*>(dst + 16 * jt) = St[jt];
   }
+#undef CARVE_FWD_PREFETCH_Q
+#undef CARVE_FWD_PREFETCH_GATES
 }
 
 // ---------------------------------------------------------------------------
 // host-side launch
 // ---------------------------------------------------------------------------
-template <typename T, int D, int LW>
+template <typename T, int D, int LW, int RP>
 static int launch_fwd_t(const FwdArgs& a, hipStream_t stream) {
-  const FwdLds lay = fwd_lds<T, D, LW>(a.RP);
-  auto kern = carve_fwd_kernel<T, D, LW>;
+  constexpr FwdLds lay = fwd_lds<T, D, LW, RP>();
+  auto kern = carve_fwd_kernel<T, D, LW, RP>;
   static bool attr_set = false;  // per instantiation
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -523,14 +366,25 @@ static int launch_fwd_t(const FwdArgs& a, hipStream_t stream) {
   return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
 }
 
+template <typename T, int D, int RP>
+static int launch_fwd_l(const FwdArgs& a, int LW, hipStream_t s) {
+  if (LW == 16) return launch_fwd_t<T, D, 16, RP>(a, s);
+  if (LW == 32) return launch_fwd_t<T, D, 32, RP>(a, s);
+  if (LW == 64) return launch_fwd_t<T, D, 64, RP>(a, s);
+  return CARVE_ERR_UNSUPPORTED;
+}
+
 template <typename T>
 static int launch_fwd_d(const FwdArgs& a, int D, int LW, hipStream_t s) {
-#define CARVE_FWD_CASE(DD, LL) \
-  if (D == DD && LW == LL) return launch_fwd_t<T, DD, LL>(a, s);
-  CARVE_FWD_CASE(32, 16) CARVE_FWD_CASE(32, 32) CARVE_FWD_CASE(32, 64)
-  CARVE_FWD_CASE(64, 16) CARVE_FWD_CASE(64, 32) CARVE_FWD_CASE(64, 64)
-  CARVE_FWD_CASE(128, 16) CARVE_FWD_CASE(128, 32) CARVE_FWD_CASE(128, 64)
-#undef CARVE_FWD_CASE
+  if (a.RP == 32) {
+    if (D == 32) return launch_fwd_l<T, 32, 32>(a, LW, s);
+    if (D == 64) return launch_fwd_l<T, 64, 32>(a, LW, s);
+    if (D == 128) return launch_fwd_l<T, 128, 32>(a, LW, s);
+  } else if (a.RP == 64) {
+    if (D == 32) return launch_fwd_l<T, 32, 64>(a, LW, s);
+    if (D == 64) return launch_fwd_l<T, 64, 64>(a, LW, s);
+    if (D == 128) return launch_fwd_l<T, 128, 64>(a, LW, s);
+  }
   return CARVE_ERR_UNSUPPORTED;
 }
 
@@ -539,15 +393,30 @@ int launch_fwd(const FwdArgs& a, int dtype, int D, int LW, hipStream_t s) {
   return launch_fwd_d<float>(a, D, LW, s);
 }
 
-size_t fwd_lds_bytes(int dtype, int D, int LW, int RP) {
-#define CARVE_LDS_CASE(DD, LL)                                                              \
-  if (D == DD && LW == LL)                                                                  \
-    return dtype == CARVE_BF16 ? fwd_lds<bf16_t, DD, LL>(RP).total : fwd_lds<float, DD, LL>(RP).total;
-  CARVE_LDS_CASE(32, 16) CARVE_LDS_CASE(32, 32) CARVE_LDS_CASE(32, 64)
-  CARVE_LDS_CASE(64, 16) CARVE_LDS_CASE(64, 32) CARVE_LDS_CASE(64, 64)
-  CARVE_LDS_CASE(128, 16) CARVE_LDS_CASE(128, 32) CARVE_LDS_CASE(128, 64)
-#undef CARVE_LDS_CASE
+template <typename T, int D, int RP>
+static size_t fwd_lds_l(int LW) {
+  if (LW == 16) return fwd_lds<T, D, 16, RP>().total;
+  if (LW == 32) return fwd_lds<T, D, 32, RP>().total;
+  if (LW == 64) return fwd_lds<T, D, 64, RP>().total;
   return (size_t)-1;
+}
+
+template <typename T>
+static size_t fwd_lds_d(int D, int LW, int RP) {
+  if (RP == 32) {
+    if (D == 32) return fwd_lds_l<T, 32, 32>(LW);
+    if (D == 64) return fwd_lds_l<T, 64, 32>(LW);
+    if (D == 128) return fwd_lds_l<T, 128, 32>(LW);
+  } else if (RP == 64) {
+    if (D == 32) return fwd_lds_l<T, 32, 64>(LW);
+    if (D == 64) return fwd_lds_l<T, 64, 64>(LW);
+    if (D == 128) return fwd_lds_l<T, 128, 64>(LW);
+  }
+  return (size_t)-1;
+}
+
+size_t fwd_lds_bytes(int dtype, int D, int LW, int RP) {
+  return dtype == CARVE_BF16 ? fwd_lds_d<bf16_t>(D, LW, RP) : fwd_lds_d<float>(D, LW, RP);
 }
 
 }  // namespace carve

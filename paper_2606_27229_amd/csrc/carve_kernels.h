@@ -15,12 +15,9 @@ struct FwdArgs {
   int B, T, H, R, RP, L;
 };
 
-struct FwdLds {
-  size_t S, Q, K, Ki, F, Tau, KhT, A, Base, Cf, Beta, Ucat, Vb, Vw, total;
-};
-
-// threads of a forward workgroup: up to four waves (one per SIMD)
-__host__ __device__ constexpr int fwd_threads(int D) { return (D / 16 < 4 ? D / 16 : 4) * 64; }
+// threads of a forward workgroup: one wave per 16-wide tile of the key (and
+// value) axis
+__host__ __device__ constexpr int fwd_threads(int D) { return (D / 16) * 64; }
 // threads of a backward workgroup: one wave per 16-column tile of the state
 __host__ __device__ constexpr int bwd_threads(int D) { return (D / 16) * 64; }
 
@@ -34,30 +31,38 @@ __host__ __device__ constexpr int lk_of() {
   return (sizeof(T) == 2 && LW < 32) ? 32 : LW;
 }
 
-template <typename T, int D, int LW>
-__host__ __device__ constexpr FwdLds fwd_lds(int RP) {
+// Forward LDS layout for one sub-chunk of LW tokens (NB = LW / 16 blocks).
+// Every row is padded by 16 bytes.  Region X holds the bf16 copy of the chunk
+// start state while the fold runs and the per-token key-side operands after.
+struct FwdLds {
+  size_t U, Q, F, Tau, Beta, X, S, Kt, Qt, Ki, Gam, AT, Tm, P, total;
+};
+
+template <typename T, int D, int LW, int RP>
+__host__ __device__ constexpr FwdLds fwd_lds() {
   FwdLds l{};
-  size_t off = 0;
   const size_t e = sizeof(T);
-  constexpr int NB = LW / 16;
-  constexpr int LK = lk_of<T, LW>();
-  constexpr size_t PAD = 16 / sizeof(T);      // every LDS row is padded by 16 bytes
-  constexpr size_t LDD = D + PAD, LDK = LK + PAD, LDA = LW + 4;
-  const size_t LDR = 2 * (size_t)RP + PAD, LDV = (size_t)RP + PAD;
-  l.S = off;    off += lds_round((size_t)D * LDD * e);
-  l.Q = off;    off += lds_round(lds_max((size_t)LW * LDD, (size_t)D * LDK) * e);   // also R^T [D][LK]
-  l.K = off;    off += lds_round(lds_max((size_t)LW * LDD, (size_t)D * LDK) * e);   // also u^T [D][LK]
-  l.Ki = off;   off += lds_round(lds_max((size_t)LW * LDD, (size_t)LW * LDK) * e);  // also P [LW][LK]
-  l.F = off;    off += lds_round((size_t)2 * RP * LDD * e);
-  l.Tau = off;  off += lds_round(lds_max((size_t)LW * LDR, (size_t)LW * LDK) * e);  // also T [LW][LK]
-  l.KhT = off;  off += lds_round((size_t)D * LDK * e);
-  l.A = off;    off += lds_round((size_t)LW * LDA * 4);
-  l.Base = off; off += lds_round((size_t)NB * D * 4);
-  l.Cf = off;   off += lds_round((size_t)NB * NB * D * 4);
-  l.Beta = off; off += lds_round((size_t)LW * 4);
-  l.Ucat = off; off += lds_round((size_t)2 * RP * LDD * e);
-  l.Vb = off;   off += lds_round((size_t)D * LDV * e);
-  l.Vw = off;   off += lds_round((size_t)D * LDV * e);
+  constexpr size_t NB = LW / 16;
+  constexpr size_t PAD = 16 / sizeof(T);
+  constexpr size_t LDD = D + PAD, LDR = 2 * RP + PAD, LDB = 16 + PAD;
+  size_t off = 0;
+  l.U = off;    off += lds_round(2 * RP * LDD * e);
+  l.Q = off;    off += lds_round(LW * LDD * e);
+  l.F = off;    off += lds_round(2 * RP * LDD * e);
+  l.Tau = off;  off += lds_round(LW * LDR * e);
+  l.Beta = off; off += lds_round(LW * 4);
+  l.X = off;
+  size_t x = 0;
+  l.Kt = off + x;  x += lds_round(LW * LDD * e);
+  l.Qt = off + x;  x += lds_round(LW * LDD * e);
+  l.Ki = off + x;  x += lds_round(LW * LDD * e);
+  l.Gam = off + x; x += lds_round(NB * D * 4);
+  l.AT = off + x;  x += lds_round(NB * 16 * 20 * 4);
+  l.Tm = off + x;  x += lds_round(NB * 16 * LDB * e);
+  l.P = off + x;   x += lds_round(NB * 16 * LDB * e);
+  l.S = off;
+  x = lds_max(x, lds_round(D * LDD * e));
+  off += x;
   l.total = off;
   return l;
 }

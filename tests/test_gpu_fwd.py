@@ -61,10 +61,16 @@ def test_fp32_shapes_content_amplified(D, L):
     check_fwd(w, make_inputs(w, seed=D + L))
 
 
-def test_fp32_d128_is_rejected():
-    """f32 token tensors are built for head sizes up to 64 (the f32 workloads);
-    d = 128 in f32 does not fit the LDS layout and must fail loudly."""
+def test_fp32_d128():
     w = _w(Dk=128, Dv=128, L=64, T=128, R=32)
+    print("case fp32 D=128 R=32", flush=True)
+    check_fwd(w, make_inputs(w, seed=35))
+
+
+def test_fp32_d128_rank64_is_rejected():
+    """f32 token tensors with d = 128 and rank > 32 do not fit the LDS layout
+    and must fail loudly."""
+    w = _w(Dk=128, Dv=128, L=64, T=128, R=64)
     with pytest.raises(carve.CarveError) as err:
         run_gpu_fwd(w, make_inputs(w, seed=3))
     assert err.value.status == -3
