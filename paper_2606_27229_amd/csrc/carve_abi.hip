@@ -14,23 +14,21 @@ int round_rp(int R) { return (R + 31) / 32 * 32; }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// backward workspace: per-(b,h) parameter partials | WY-tile start states |
-// packed [Ub; Uw] | its transpose
+// backward workspace: d[Ub; Uw] partials per (b,h, chunk split) | dVb, dVw
+// partials per (b,h, token split) | chunk records of the recompute
 struct BwdWs {
-  size_t part, substates, up, ut, total;
+  size_t part, partV, rec, total;
 };
 
-BwdWs bwd_workspace_layout(const carve_dims_t* d, int lw) {
+BwdWs bwd_workspace_layout(const carve_dims_t* d) {
   BwdWs l{};
   const size_t nbh = (size_t)d->B * d->H;
   const size_t es = d->dtype == CARVE_BF16 ? 2 : 4;
-  const size_t R2 = 2 * (size_t)round_rp(d->R);
-  const int msub = d->L / lw;
+  const size_t nch = (size_t)(d->T / d->L);
   size_t off = 0;
-  l.part = off;      off += align256(nbh * part_floats(d->R, d->Dk) * 4);
-  l.substates = off; off += msub > 1 ? align256(nbh * (size_t)msub * d->Dv * d->Dk * 4) : 0;
-  l.up = off;        off += align256(R2 * d->Dk * es);
-  l.ut = off;        off += align256(R2 * d->Dk * es);
+  l.part = off;  off += align256(nbh * kUSplit * part_floats(d->R, d->Dk) * 4);
+  l.partV = off; off += align256(nbh * kVSplit * part_floats(d->R, d->Dk) * 4);
+  l.rec = off;   off += align256(nbh * nch * chunk_rec(es, d->Dk, d->L, round_rp(d->R)).total);
   l.total = off;
   return l;
 }
@@ -54,13 +52,14 @@ int check_dims(const carve_dims_t* d) {
   return CARVE_OK;
 }
 
-// largest WY tile (<= 64, dividing L) whose LDS layout fits
+// largest forward sub-chunk (<= 64 tokens, dividing L) whose LDS layout fits;
+// for the backward also the adjoint kernel's layout must fit
 int pick_lw(const carve_dims_t* d, bool bwd) {
   const int RP = round_rp(d->R);
+  if (bwd && bwd_lds_bytes(d->dtype, d->Dk, 16, RP) > kMaxLds) return 0;
   for (int lw = 64; lw >= 16; lw /= 2) {
     if (lw > d->L || d->L % lw) continue;
-    const size_t need = bwd ? bwd_lds_bytes(d->dtype, d->Dk, lw, RP) : fwd_lds_bytes(d->dtype, d->Dk, lw, RP);
-    if (need <= kMaxLds) return lw;
+    if (fwd_lds_bytes(d->dtype, d->Dk, lw, RP) <= kMaxLds) return lw;
   }
   return 0;
 }
@@ -108,9 +107,8 @@ const char* carve_status_string(int status) {
 size_t carve_workspace_size(const carve_dims_t* d, int for_backward) {
   if (check_dims(d) != CARVE_OK) return 0;
   if (!for_backward) return 0;
-  const int lw = pick_lw(d, true);
-  if (!lw) return 0;
-  return bwd_workspace_layout(d, lw).total;
+  if (!pick_lw(d, true)) return 0;
+  return bwd_workspace_layout(d).total;
 }
 
 int carve_chunk_fwd(const carve_dims_t* d, const void* q, const void* k, const void* v,
@@ -180,22 +178,42 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
   if (any_overlap(outs, 12, ins, 15)) return CARVE_ERR_UNSUPPORTED;
   const int lw = pick_lw(d, true);
   if (!lw) return CARVE_ERR_UNSUPPORTED;
+  const BwdWs wl = bwd_workspace_layout(d);
+  char* wsb = reinterpret_cast<char*>(workspace);
+  const int RP = round_rp(d->R);
+  // 1. chunk-parallel recompute -> chunk records
+  FwdArgs f;
+  f.q = q; f.k = k; f.v = v; f.beta = beta; f.bx = bx; f.wx = wx;
+  f.g = g; f.Ub = Ub; f.Uw = Uw; f.Vb = Vb; f.Vw = Vw; f.S0 = nullptr;
+  f.o = nullptr; f.S_T = nullptr; f.S_chunks = const_cast<float*>(S_chunks);
+  f.rec = wsb + wl.rec;
+  f.B = d->B; f.T = d->T; f.H = d->H; f.R = d->R; f.RP = RP; f.L = d->L;
+  st = launch_fwd_rec(f, d->dtype, d->Dk, lw, stream);
+  if (st) return st;
+  // 2. adjoint
   BwdArgs a;
   a.q = q; a.k = k; a.v = v; a.beta = beta; a.bx = bx; a.wx = wx;
   a.g = g; a.Ub = Ub; a.Uw = Uw; a.Vb = Vb; a.Vw = Vw; a.S_chunks = S_chunks;
   a.dO = dO; a.dS_T = dS_T;
   a.dq = dq; a.dk = dk; a.dv = dv; a.dbeta = dbeta; a.dbx = dbx; a.dwx = dwx; a.dg = dg; a.dS0 = dS0;
-  const BwdWs wl = bwd_workspace_layout(d, lw);
-  char* wsb = reinterpret_cast<char*>(workspace);
   a.part = reinterpret_cast<float*>(wsb + wl.part);
-  a.substates = (d->L / lw > 1) ? reinterpret_cast<float*>(wsb + wl.substates) : nullptr;
-  a.Up = wsb + wl.up;
-  a.UT = wsb + wl.ut;
-  const size_t nbh = (size_t)d->B * d->H;
-  a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = round_rp(d->R); a.L = d->L;
+  a.partV = reinterpret_cast<float*>(wsb + wl.partV);
+  a.rec = wsb + wl.rec;
+  a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = RP; a.L = d->L;
   st = launch_bwd(a, d->dtype, d->Dk, lw, stream);
   if (st) return st;
-  return launch_param_reduce(a.part, (int)nbh, d->R, d->Dk, dUb, dUw, dVb, dVw, stream);
+  // 3. dVb, dVw from dbx, dwx and tau
+  st = launch_bwd_vparam(a, d->dtype, d->Dk, stream);
+  if (st) return st;
+  // 4. d[Ub; Uw] from the per-chunk dF
+  st = launch_bwd_uparam(a, d->dtype, d->Dk, stream);
+  if (st) return st;
+  // 5. fixed-order reductions of the partials
+  const int nbh = d->B * d->H;
+  const size_t RD = (size_t)d->R * d->Dk;
+  st = launch_param_reduce(a.part, nbh * kUSplit, RD, dUb, dUw, stream);
+  if (st) return st;
+  return launch_param_reduce(a.partV, nbh * kVSplit, RD, dVb, dVw, stream);
 }
 
 }  // extern "C"

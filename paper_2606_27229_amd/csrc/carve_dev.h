@@ -166,6 +166,19 @@ __device__ __forceinline__ float row_shr1(float x, float fill) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, fill), __builtin_bit_cast(int, x),
                                                                0x111, 0xf, 0xf, false));
 }
+// x of the lane one to the right in its row; the last lane of a row gets fill
+__device__ __forceinline__ float row_shl1(float x, float fill) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, fill), __builtin_bit_cast(int, x),
+                                                               0x101, 0xf, 0xf, false));
+}
+// inclusive suffix sum over the 16 lanes of each row
+__device__ __forceinline__ float row_suffix(float x) {
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x101, 0xf, 0xf, false));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x102, 0xf, 0xf, false));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x104, 0xf, 0xf, false));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x108, 0xf, 0xf, false));
+  return x;
+}
 // inclusive prefix sum over the 16 lanes of each row
 __device__ __forceinline__ float row_scan(float x) {
   x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x111, 0xf, 0xf, false));
@@ -218,6 +231,13 @@ __device__ __forceinline__ float sigmoid_f(float z) { return fast_rcp(1.0f + fas
 // log(1 + e^z) without overflow
 __device__ __forceinline__ float softplus_f(float z) {
   return fmaxf(z, 0.0f) + __logf(1.0f + fast_exp(-fabsf(z)));
+}
+// softplus(z) = log(1 + e^z) and sigmoid(z) from one exponential
+__device__ __forceinline__ void softplus_sigmoid(float z, float& sp, float& sig) {
+  const float e = fast_exp(-fabsf(z));
+  const float r = fast_rcp(1.0f + e);
+  sp = fmaxf(z, 0.0f) + __logf(1.0f + e);
+  sig = z >= 0.0f ? r : e * r;
 }
 // tanh with a short odd series near 0 (the exp form cancels there)
 __device__ __forceinline__ float tanh_f(float y) {

@@ -36,7 +36,10 @@
 
 namespace carve {
 
-template <typename T, int D, int LW, int RP>
+// REC = false: the forward of the whole sequence, one workgroup per (batch, head).
+// REC = true: recompute for the backward, one workgroup per (batch, head,
+// chunk) starting from S_chunks; writes the chunk record instead of outputs.
+template <typename T, int D, int LW, int RP, bool REC>
 __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
   typedef Quad<T> Qd;
   typedef typename Qd::q quad;
@@ -58,8 +61,10 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
   const int H = a.H, Tn = a.T, L = a.L, R = a.R;
-  const int bh = blockIdx.x, b = bh / H, h = bh % H;
-  const int nch = Tn / L, msub = L / LW, ntiles = Tn / LW;
+  const int nch = Tn / L, msub = L / LW;
+  const int bh = REC ? blockIdx.x / nch : blockIdx.x, b = bh / H, h = bh % H;
+  const int ch0 = REC ? blockIdx.x % nch : 0, ch1 = REC ? ch0 + 1 : nch;
+  const int ntiles = ch1 * msub;   // prefetch bound (exclusive)
 
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr FwdLds lay = fwd_lds<T, D, LW, RP>();
@@ -122,8 +127,20 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
   // ---- state: St[jt][i] = S[v = 16 w + c][j = 16 jt + 4 g + i] ---------------
   f32x4 St[NJT];
   const size_t soff = (size_t)bh * D * D;
-  for (int jt = 0; jt < NJT; ++jt)
-    St[jt] = a.S0 ? gload4(a.S0 + soff + (16 * w + c) * D + 16 * jt + 4 * g) : zero4();
+  if (REC) {
+    const float* src = a.S_chunks + ((size_t)bh * nch + ch0) * D * D + (16 * w + c) * D + 16 * 0 + 4 * g;
+    for (int jt = 0; jt < NJT; ++jt) St[jt] = gload4(src + 16 * jt);
+  } else {
+    for (int jt = 0; jt < NJT; ++jt)
+      St[jt] = a.S0 ? gload4(a.S0 + soff + (16 * w + c) * D + 16 * jt + 4 * g) : zero4();
+  }
+  // chunk record of this workgroup (REC)
+  char* rec = nullptr;
+  ChunkRec cr{};
+  if (REC) {
+    cr = chunk_rec(sizeof(T), D, L, RP);
+    rec = reinterpret_cast<char*>(a.rec) + ((size_t)bh * nch + ch0) * cr.total;
+  }
 
   // ---- prefetch registers for the next sub-chunk ------------------------------
   u32x4 pq[NQV];
@@ -153,17 +170,17 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
       pg[bb_] = *reinterpret_cast<const f32x4*>(gl + e_);                               \
     }                                                                                   \
   } while (0)
-  CARVE_FWD_PREFETCH_Q(0);
-  CARVE_FWD_PREFETCH_GATES(0);
+  CARVE_FWD_PREFETCH_Q(ch0 * msub);
+  CARVE_FWD_PREFETCH_GATES(ch0 * msub);
 
-  int tile = 0;
-  for (int ch = 0; ch < nch; ++ch) {
+  int tile = ch0 * msub;
+  for (int ch = ch0; ch < ch1; ++ch) {
     for (int m = 0; m < msub; ++m, ++tile) {
       const int t0 = tile * LW;
 
       // ---- P0: stage q and beta; chunk start state ----------------------------
       if (m == 0) {
-        if (a.S_chunks) {
+        if (!REC && a.S_chunks) {
           float* dst = a.S_chunks + ((size_t)bh * nch + ch) * D * D + (16 * w + c) * D + 4 * g;
           for (int jt = 0; jt < NJT; ++jt) *reinterpret_cast<f32x4*>(dst + 16 * jt) = St[jt];
         }
@@ -190,6 +207,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
             acc = Qd::mma32(a0, a1, Qd::ld(ur), Qd::ld(ur + 16), acc);
           }
           Qd::st(sF + (16 * rt + c) * LDD + 16 * w + 4 * g, Qd::cvt(acc));
+          if (REC) Qd::st(reinterpret_cast<T*>(rec + cr.F) + (16 * rt + c) * D + 16 * w + 4 * g, Qd::cvt(acc));
         }
         __syncthreads();
       }
@@ -205,6 +223,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
         }
         for (int i = 0; i < 4; ++i) acc[i] = tanh_f(acc[i]);
         Qd::st(sTau + (16 * bb + c) * LDR + 16 * rt + 4 * g, Qd::cvt(acc));
+        if (REC) Qd::st(reinterpret_cast<T*>(rec + cr.Tau) + (m * LW + 16 * bb + c) * R2 + 16 * rt + 4 * g, Qd::cvt(acc));
       }
       __syncthreads();
 
@@ -233,7 +252,10 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
         Qd::st(sKt + ro, Qd::cvt(kt));
         Qd::st(sQt + ro, Qd::cvt(qt));
         Qd::st(sKi + ro, Qd::cvt(ki));
-        if (c == 15) *reinterpret_cast<f32x4*>(sGam + bb * D + 16 * w + 4 * g) = gam;
+        if (c == 15) {
+          *reinterpret_cast<f32x4*>(sGam + bb * D + 16 * w + 4 * g) = gam;
+          if (REC) *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(rec + cr.Gam) + (m * NB + bb) * D + 16 * w + 4 * g) = gam;
+        }
       }
       // value side, value tile w: rows t = 16 bb + 4 g + i, column v = 16 w + c
       f32x4 wv[NB];
@@ -269,6 +291,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
           f32x4 pv4;
           for (int i = 0; i < 4; ++i) pv4[i] = (4 * g + i <= c) ? acc[i] : 0.0f;
           Qd::st(sP + (bb * 16 + c) * LDB + 4 * g, Qd::cvt(pv4));
+          if (REC) Qd::st(reinterpret_cast<T*>(rec + cr.P) + ((m * NB + bb) * 16 + c) * 16 + 4 * g, Qd::cvt(pv4));
         }
       }
       __syncthreads();
@@ -286,8 +309,9 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
     for (int jp_ = 0; jp_ < NJT / 2; ++jp_) {                                            \
       XK = Qd::mma32(Qd::ld(kr_ + 32 * jp_), Qd::ld(kr_ + 32 * jp_ + 16), sb[2 * jp_],   \
                      sb[2 * jp_ + 1], XK);                                               \
-      XQ = Qd::mma32(Qd::ld(qr_ + 32 * jp_), Qd::ld(qr_ + 32 * jp_ + 16), sb[2 * jp_],   \
-                     sb[2 * jp_ + 1], XQ);                                               \
+      if (!REC)                                                                          \
+        XQ = Qd::mma32(Qd::ld(qr_ + 32 * jp_), Qd::ld(qr_ + 32 * jp_ + 16), sb[2 * jp_], \
+                       sb[2 * jp_ + 1], XQ);                                             \
     }                                                                                    \
   } while (0)
       if (w == NW - 1) {
@@ -311,6 +335,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
           for (int s4 = 0; s4 < 4; ++s4) {
             f32x4 t4 = {x[4 * s4], x[4 * s4 + 1], x[4 * s4 + 2], x[4 * s4 + 3]};
             Qd::st(tr + 4 * s4, Qd::cvt(t4));
+            if (REC) Qd::st(reinterpret_cast<T*>(rec + cr.Tm) + ((m * NB + g) * 16 + c) * 16 + 4 * s4, Qd::cvt(t4));
           }
         }
       }
@@ -320,15 +345,21 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
       // ---- P6: token-serial blocks on the value tile (no barriers) --------------
       for (int bb = 0; bb < NB; ++bb) {
         if (bb > 0) CARVE_FWD_XKQ(bb);
+        if (REC) {
+          T* sv = reinterpret_cast<T*>(rec + cr.S) + ((size_t)(m * NB + bb) * NT + tid) * 4 * NJT;
+          for (int jt = 0; jt < NJT; ++jt) Qd::st(sv + 4 * jt, sb[jt]);
+        }
         const f32x4 bt = *reinterpret_cast<const f32x4*>(sBeta + 16 * bb + 4 * g);
         f32x4 rr;
         for (int i = 0; i < 4; ++i) rr[i] = bt[i] * (wv[bb][i] - XK[i]);
         const f32x4 u = Qd::mma16(Qd::ld(sTm + (bb * 16 + c) * LDB + 4 * g), Qd::cvt(rr), zero4());
         const quad uq = Qd::cvt(u);
-        const f32x4 O = Qd::mma16(Qd::ld(sP + (bb * 16 + c) * LDB + 4 * g), uq, XQ);
-        // o^T through the identity: lane (g, c) gets o[t = c][v = 4 g + i]
-        const f32x4 Ot = Qd::mma16(Qd::cvt(O), fI, zero4());
-        Qd::st(o + (t0 + 16 * bb + c) * rs + 16 * w + 4 * g, Qd::cvt(Ot));
+        if (!REC) {
+          const f32x4 O = Qd::mma16(Qd::ld(sP + (bb * 16 + c) * LDB + 4 * g), uq, XQ);
+          // o^T through the identity: lane (g, c) gets o[t = c][v = 4 g + i]
+          const f32x4 Ot = Qd::mma16(Qd::cvt(O), fI, zero4());
+          Qd::st(o + (t0 + 16 * bb + c) * rs + 16 * w + 4 * g, Qd::cvt(Ot));
+        }
         for (int jt = 0; jt < NJT; ++jt) {
           const f32x4 acc = Qd::mma16(Qd::ld_tr(sKi, LDD, 16 * bb, 16 * jt, g, c), uq, St[jt]);
           const f32x4 gm = *reinterpret_cast<const f32x4*>(sGam + bb * D + 16 * jt + 4 * g);
@@ -340,7 +371,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
       __syncthreads();  // the next sub-chunk overwrites sQ, sBeta and region X
     }
   }
-  if (a.S_T) {
+  if (!REC && a.S_T) {
     float* dst = a.S_T + soff + (16 * w + c) * D + 4 * g;
     for (int jt = 0; jt < NJT; ++jt) *reinterpret_cast<f32x4*>(dst + 16 * jt) = St[jt];
   }
@@ -351,10 +382,10 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
 // ---------------------------------------------------------------------------
 // host-side launch
 // ---------------------------------------------------------------------------
-template <typename T, int D, int LW, int RP>
+template <typename T, int D, int LW, int RP, bool REC>
 static int launch_fwd_t(const FwdArgs& a, hipStream_t stream) {
   constexpr FwdLds lay = fwd_lds<T, D, LW, RP>();
-  auto kern = carve_fwd_kernel<T, D, LW, RP>;
+  auto kern = carve_fwd_kernel<T, D, LW, RP, REC>;
   static bool attr_set = false;  // per instantiation
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -362,35 +393,41 @@ static int launch_fwd_t(const FwdArgs& a, hipStream_t stream) {
       return CARVE_ERR_HIP;
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(fwd_threads(D)), lay.total, stream, a);
+  const int grid = REC ? a.B * a.H * (a.T / a.L) : a.B * a.H;
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(fwd_threads(D)), lay.total, stream, a);
   return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
 }
 
-template <typename T, int D, int RP>
+template <typename T, int D, int RP, bool REC>
 static int launch_fwd_l(const FwdArgs& a, int LW, hipStream_t s) {
-  if (LW == 16) return launch_fwd_t<T, D, 16, RP>(a, s);
-  if (LW == 32) return launch_fwd_t<T, D, 32, RP>(a, s);
-  if (LW == 64) return launch_fwd_t<T, D, 64, RP>(a, s);
+  if (LW == 16) return launch_fwd_t<T, D, 16, RP, REC>(a, s);
+  if (LW == 32) return launch_fwd_t<T, D, 32, RP, REC>(a, s);
+  if (LW == 64) return launch_fwd_t<T, D, 64, RP, REC>(a, s);
   return CARVE_ERR_UNSUPPORTED;
 }
 
-template <typename T>
+template <typename T, bool REC>
 static int launch_fwd_d(const FwdArgs& a, int D, int LW, hipStream_t s) {
   if (a.RP == 32) {
-    if (D == 32) return launch_fwd_l<T, 32, 32>(a, LW, s);
-    if (D == 64) return launch_fwd_l<T, 64, 32>(a, LW, s);
-    if (D == 128) return launch_fwd_l<T, 128, 32>(a, LW, s);
+    if (D == 32) return launch_fwd_l<T, 32, 32, REC>(a, LW, s);
+    if (D == 64) return launch_fwd_l<T, 64, 32, REC>(a, LW, s);
+    if (D == 128) return launch_fwd_l<T, 128, 32, REC>(a, LW, s);
   } else if (a.RP == 64) {
-    if (D == 32) return launch_fwd_l<T, 32, 64>(a, LW, s);
-    if (D == 64) return launch_fwd_l<T, 64, 64>(a, LW, s);
-    if (D == 128) return launch_fwd_l<T, 128, 64>(a, LW, s);
+    if (D == 32) return launch_fwd_l<T, 32, 64, REC>(a, LW, s);
+    if (D == 64) return launch_fwd_l<T, 64, 64, REC>(a, LW, s);
+    if (D == 128) return launch_fwd_l<T, 128, 64, REC>(a, LW, s);
   }
   return CARVE_ERR_UNSUPPORTED;
 }
 
 int launch_fwd(const FwdArgs& a, int dtype, int D, int LW, hipStream_t s) {
-  if (dtype == CARVE_BF16) return launch_fwd_d<bf16_t>(a, D, LW, s);
-  return launch_fwd_d<float>(a, D, LW, s);
+  if (dtype == CARVE_BF16) return launch_fwd_d<bf16_t, false>(a, D, LW, s);
+  return launch_fwd_d<float, false>(a, D, LW, s);
+}
+
+int launch_fwd_rec(const FwdArgs& a, int dtype, int D, int LW, hipStream_t s) {
+  if (dtype == CARVE_BF16) return launch_fwd_d<bf16_t, true>(a, D, LW, s);
+  return launch_fwd_d<float, true>(a, D, LW, s);
 }
 
 template <typename T, int D, int RP>

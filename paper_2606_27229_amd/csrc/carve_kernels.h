@@ -12,8 +12,37 @@ struct FwdArgs {
   const float *g, *Ub, *Uw, *Vb, *Vw, *S0;  // f32
   void* o;
   float *S_T, *S_chunks;
+  void* rec;     // chunk records (recompute mode of the backward)
   int B, T, H, R, RP, L;
 };
+
+// Per-(batch, head, chunk) record written by the chunk-parallel recompute of
+// the backward and read by its adjoint kernel (byte offsets, 256-aligned):
+//   F   [2RP][D]   token dtype   folded read-out of the chunk start state
+//   Tau [L][2RP]   token dtype   tanh(q F^T)
+//   Tm  [L/16][16][16]           T = (I + A)^{-1} of every 16-token block
+//   P   [L/16][16][16]           P of every block
+//   Gam [L/16][D]  f32           block retention e^{lam_15}
+//   S   [L/16][D*D]              block start states, wave layout (lane-major)
+//   dF  [2RP][D]   f32           written by the adjoint: the chunk's gradient of F
+struct ChunkRec {
+  size_t F, Tau, Tm, P, Gam, S, dF, total;
+};
+__host__ __device__ constexpr size_t rec_align(size_t x) { return (x + 255) & ~(size_t)255; }
+__host__ __device__ constexpr ChunkRec chunk_rec(size_t e, int D, int L, int RP) {
+  ChunkRec r{};
+  const size_t nbc = L / 16;
+  size_t off = 0;
+  r.F = off;   off += rec_align(2 * (size_t)RP * D * e);
+  r.Tau = off; off += rec_align((size_t)L * 2 * RP * e);
+  r.Tm = off;  off += rec_align(nbc * 256 * e);
+  r.P = off;   off += rec_align(nbc * 256 * e);
+  r.Gam = off; off += rec_align(nbc * D * 4);
+  r.S = off;   off += rec_align(nbc * (size_t)D * D * e);
+  r.dF = off;  off += rec_align(2 * (size_t)RP * D * 4);
+  r.total = off;
+  return r;
+}
 
 // threads of a forward workgroup: one wave per 16-wide tile of the key (and
 // value) axis
@@ -68,6 +97,8 @@ __host__ __device__ constexpr FwdLds fwd_lds() {
 }
 
 int launch_fwd(const FwdArgs& a, int dtype, int D, int LW, hipStream_t s);
+// chunk-parallel forward recompute that writes the chunk records (a.rec)
+int launch_fwd_rec(const FwdArgs& a, int dtype, int D, int LW, hipStream_t s);
 size_t fwd_lds_bytes(int dtype, int D, int LW, int RP);
 
 // ---- backward -----------------------------------------------------------------
@@ -80,19 +111,62 @@ struct BwdArgs {
   void *dq, *dk, *dv, *dbeta, *dbx, *dwx;
   float* dg;
   float* dS0;
-  float* part;       // per-(b,h) partial parameter gradients (workspace)
-  float* substates;  // per-(b,h) WY-tile start states inside one gate chunk (workspace)
-  const void* Up;    // [2RP][D] packed [Ub; Uw] (token dtype, workspace)
-  const void* UT;    // [D][2RP] its transpose (token dtype, workspace)
+  float* part;    // per-(b,h, chunk split) partial d[Ub; Uw] (workspace)
+  float* partV;   // per-(b,h,split) partial dVb, dVw (workspace)
+  const void* rec;  // chunk records of the recompute (workspace)
   int B, T, H, R, RP, L;
 };
 
+// token splits of the Vb / Vw gradient kernel and chunk splits of the [Ub; Uw]
+// gradient kernel (per (batch, head))
+constexpr int kVSplit = 16;
+constexpr int kUSplit = 16;
+
+// LDS layout of the adjoint kernel (one 16-token block at a time)
+struct BwdLds {
+  size_t F, VbT, VwT, Tau, Tm, P, Gam, Beta, Dbeta, Kt, Qt, Ki, Sx, dSx, dOT, uT, dRT, dzwT, dzb, dY, total;
+};
+
+template <typename T, int D, int RP>
+__host__ __device__ constexpr BwdLds bwd_lds() {
+  BwdLds l{};
+  const size_t e = sizeof(T);
+  constexpr size_t NW = D / 16;
+  constexpr size_t PAD = 16 / sizeof(T);
+  constexpr size_t LDD = D + PAD, LDR = 2 * RP + PAD, LDB = 16 + PAD;
+  size_t off = 0;
+  l.F = off;     off += lds_round(2 * RP * LDD * e);
+  l.VbT = off;   off += lds_round(RP * LDD * e);
+  l.VwT = off;   off += lds_round(RP * LDD * e);
+  l.Tau = off;   off += lds_round(16 * LDR * e);
+  l.Tm = off;    off += lds_round(16 * LDB * e);
+  l.P = off;     off += lds_round(16 * LDB * e);
+  l.Gam = off;   off += lds_round(D * 4);
+  l.Beta = off;  off += lds_round(16 * 4);
+  l.Dbeta = off; off += lds_round(NW * 16 * 4);
+  l.Kt = off;    off += lds_round(16 * LDD * e);
+  l.Qt = off;    off += lds_round(16 * LDD * e);
+  l.Ki = off;    off += lds_round(16 * LDD * e);
+  l.Sx = off;    off += lds_round(D * LDD * e);
+  l.dSx = off;   off += lds_round(D * lds_max(LDD, 2 * LDR) * e);
+  l.dOT = off;   off += lds_round(D * LDB * e);
+  l.uT = off;    off += lds_round(D * LDB * e);
+  l.dRT = off;   off += lds_round(D * LDB * e);
+  l.dzwT = off;  off += lds_round(D * LDB * e);
+  l.dzb = off;   off += lds_round(16 * LDD * e);
+  l.dY = off;    off += lds_round(16 * LDR * e);
+  l.total = off;
+  return l;
+}
+
 int launch_bwd(const BwdArgs& a, int dtype, int D, int LW, hipStream_t s);
 size_t bwd_lds_bytes(int dtype, int D, int LW, int RP);
-int launch_param_reduce(const float* part, int nparts, int R, int D, float* dUb, float* dUw,
-                        float* dVb, float* dVw, hipStream_t s);
+int launch_bwd_vparam(const BwdArgs& a, int dtype, int D, hipStream_t s);
+int launch_bwd_uparam(const BwdArgs& a, int dtype, int D, hipStream_t s);
+// sum nparts records of 2 * half floats into dst0 (first half) and dst1
+int launch_param_reduce(const float* part, int nparts, size_t half, float* dst0, float* dst1, hipStream_t s);
 
-// size of one per-(b,h) partial-gradient record: dUb, dUw [R][D], dVb, dVw [D][R]
-__host__ __device__ constexpr size_t part_floats(int R, int D) { return (size_t)4 * R * D; }
+// floats of one partial-gradient record: d[Ub; Uw] ([R][D] twice) or dVb, dVw ([D][R] twice)
+__host__ __device__ constexpr size_t part_floats(int R, int D) { return (size_t)2 * R * D; }
 
 }  // namespace carve
