@@ -115,25 +115,14 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
     sVbT[rr * LDD + j] = (T)(rr < R ? a.Vb[j * R + rr] : 0.0f);
     sVwT[rr * LDD + j] = (T)(rr < R ? a.Vw[j * R + rr] : 0.0f);
   }
-  // constant operand quads: lane (g, c) holds Vb[16 w + c][16 ks + 4 g + e] and
-  // Vw[16 w + c][16 ks + 4 g + e]
-  quad fVb[NRB], fVw[NRB];
-  for (int ks = 0; ks < NRB; ++ks) {
-    f32x4 tb, tw;
-    for (int e = 0; e < 4; ++e) {
-      const int r = 16 * ks + 4 * g + e;
-      tb[e] = r < R ? a.Vb[(16 * w + c) * R + r] : 0.0f;
-      tw[e] = r < R ? a.Vw[(16 * w + c) * R + r] : 0.0f;
-    }
-    fVb[ks] = Qd::cvt(tb);
-    fVw[ks] = Qd::cvt(tw);
-  }
-  quad fI;
-  {
-    f32x4 t;
-    for (int e = 0; e < 4; ++e) t[e] = (4 * g + e == c) ? 1.0f : 0.0f;
-    fI = Qd::cvt(t);
-  }
+  // Vb / Vw operand quads (lane (g, c): V[16 w + c][16 ks + 4 g + e]) are read
+  // from sVbT / sVwT with the transposing load where needed; the identity
+  // operand (lane (g, c): I[4 g + e][c]) is rebuilt where needed.
+#define CARVE_FVB(KS_) Qd::ld_tr(sVbT, LDD, 16 * (KS_), 16 * w, g, c)
+#define CARVE_FVW(KS_) Qd::ld_tr(sVwT, LDD, 16 * (KS_), 16 * w, g, c)
+#define CARVE_FI() Qd::cvt(f32x4{4 * g == c ? 1.0f : 0.0f, 4 * g + 1 == c ? 1.0f : 0.0f, \
+                                 4 * g + 2 == c ? 1.0f : 0.0f, 4 * g + 3 == c ? 1.0f : 0.0f})
+  __syncthreads();
 
   // ---- persistent accumulators --------------------------------------------------
   const size_t soff = (size_t)bh * D * D;
@@ -155,6 +144,14 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
     }
 #pragma unroll 1
     for (int bc = nbc - 1; bc >= 0; --bc) {
+      // opaque copies of the lane coordinates: values derived from them
+      // (addresses, masks) are recomputed in every block instead of being
+      // hoisted out of the loops and kept live (which would spill)
+      int tid_ = tid, g_ = g, c_ = c, w_ = w;
+      asm volatile("" : "+v"(tid_), "+v"(g_), "+v"(c_), "+v"(w_));
+      const int tid = tid_, g = g_, c = c_, w = w_;
+      const int lane = tid & 63;
+      (void)lane;
       const int tb = ch * L + 16 * bc;   // first token of the block
       const int e0 = (tb + c) * rs + 16 * w + 4 * g;
 
@@ -182,16 +179,18 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
         const T* sv = reinterpret_cast<const T*>(rc + cr.S) + ((size_t)bc * NT + tid) * 4 * NJT;
         for (int jt = 0; jt < NJT; ++jt) sbq[jt] = Qd::ld(sv + 4 * jt);
       }
-      f32x4 kv, qv, E, Ei, sig;
+      // key-side factors kept for the adjoint in the token dtype (quads)
+      quad kq, qq, Eq, Eiq, sigq;
       {
         const T* tau = reinterpret_cast<const T*>(rc + cr.Tau) + (16 * bc + c) * R2 + 4 * g;
         f32x4 z = zero4();
-        for (int ks = 0; ks < NRB; ++ks) z = Qd::mma16(fVb[ks], Qd::ld(tau + 16 * ks), z);
+        for (int ks = 0; ks < NRB; ++ks) z = Qd::mma16(CARVE_FVB(ks), Qd::ld(tau + 16 * ks), z);
         const f32x4 bxv = Qd::f32(Qd::ld(bx + e0));
         const f32x4 gv = *reinterpret_cast<const f32x4*>(gl + e0);
-        kv = Qd::f32(Qd::ld(k + e0));
-        qv = Qd::f32(Qd::ld(q + e0));
-        f32x4 kt, qt, ki;
+        kq = Qd::ld(k + e0);
+        qq = Qd::ld(q + e0);
+        const f32x4 kv = Qd::f32(kq), qv = Qd::f32(qq);
+        f32x4 kt, qt, ki, E, Ei, sig;
         for (int i = 0; i < 4; ++i) {
           float sp, sg;
           softplus_sigmoid(z[i] + bxv[i], sp, sg);
@@ -203,6 +202,9 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
           qt[i] = qv[i] * E[i];
           ki[i] = kv[i] * Ei[i];
         }
+        Eq = Qd::cvt(E);
+        Eiq = Qd::cvt(Ei);
+        sigq = Qd::cvt(sig);
         const int ro = c * LDD + 16 * w + 4 * g;
         Qd::st(sKt + ro, Qd::cvt(kt));
         Qd::st(sQt + ro, Qd::cvt(qt));
@@ -217,14 +219,14 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
 
       // -- BV: value-side adjoint (value tile w, rows t = 4 g + i, column v = 16 w + c)
       {
-        const f32x4 vv = Qd::mma16(vq, fI, zero4());
-        const f32x4 dOc = Qd::mma16(dOq, fI, zero4());
+        const f32x4 vv = Qd::mma16(vq, CARVE_FI(), zero4());
+        const f32x4 dOc = Qd::mma16(dOq, CARVE_FI(), zero4());
         f32x4 wgt;
         {
           f32x4 zw = zero4();
           for (int ks = 0; ks < NRB; ++ks)
-            zw = Qd::mma16(Qd::ld(sTau + c * LDR + RP + 16 * ks + 4 * g), fVw[ks], zw);
-          zw = Qd::mma16(wxq, fI, zw);
+            zw = Qd::mma16(Qd::ld(sTau + c * LDR + RP + 16 * ks + 4 * g), CARVE_FVW(ks), zw);
+          zw = Qd::mma16(wxq, CARVE_FI(), zw);
           for (int i = 0; i < 4; ++i) wgt[i] = sigmoid_f(zw[i]);
         }
         f32x4 XK = zero4();
@@ -270,9 +272,9 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
           dvv[i] = dwv[i] * wgt[i];
           dzw[i] = dwv[i] * vv[i] * wgt[i] * (1.0f - wgt[i]);
         }
-        Qd::st(dv + e0, Qd::cvt(Qd::mma16(Qd::cvt(dvv), fI, zero4())));
+        Qd::st(dv + e0, Qd::cvt(Qd::mma16(Qd::cvt(dvv), CARVE_FI(), zero4())));
         const quad dzwq = Qd::cvt(dzw);
-        Qd::st(dwx + e0, Qd::cvt(Qd::mma16(dzwq, fI, zero4())));
+        Qd::st(dwx + e0, Qd::cvt(Qd::mma16(dzwq, CARVE_FI(), zero4())));
         // beta gradient, value part: sum over v of dR (w v - S Kt)
         f32x4 pr;
         for (int i = 0; i < 4; ++i) pr[i] = row_scan(dR[i] * rm[i]);
@@ -289,6 +291,7 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
       // -- BKA: key-side adjoint (key tile w; C rows j = 16 w + 4 g + i, column t = c)
       f32x4 dqp;
       {
+        const f32x4 kv = Qd::f32(kq), qv = Qd::f32(qq), E = Qd::f32(Eq), Ei = Qd::f32(Eiq), sig = Qd::f32(sigq);
         f32x4 dKt = zero4(), dQt = zero4(), dKi = zero4(), dA = zero4(), dP = zero4();
         float dgs = 0.0f;   // sum_v dS'[v][j] S[v][j] for j = 16 w + c (partial over this lane's v)
         for (int kp = 0; kp < NJT / 2; ++kp) {
@@ -351,8 +354,8 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
             for (int i = 0; i < 4; ++i) dbeta[(tb + 4 * g + i) * H] = (T)db[i];
           }
         }
-        const quad bdAT = Qd::cvt(Qd::mma16(Qd::cvt(bdA), fI, zero4()));   // rows s, columns t
-        const quad dPT = Qd::cvt(Qd::mma16(Qd::cvt(dP), fI, zero4()));
+        const quad bdAT = Qd::cvt(Qd::mma16(Qd::cvt(bdA), CARVE_FI(), zero4()));   // rows s, columns t
+        const quad dPT = Qd::cvt(Qd::mma16(Qd::cvt(dP), CARVE_FI(), zero4()));
         const quad KiT = Qd::ld_tr(sKi, LDD, 0, 16 * w, g, c);
         dKt = Qd::mma16(KiT, bdAT, dKt);
         dKi = Qd::mma32(Qd::ld_tr(sKt, LDD, 0, 16 * w, g, c), Qd::ld_tr(sQt, LDD, 0, 16 * w, g, c), Qd::cvt(bdA),
@@ -410,7 +413,7 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
           acc = Qd::mma32(Qd::ld_tr(sF, LDD, 32 * rp, 16 * w, g, c), Qd::ld_tr(sF, LDD, 32 * rp + 16, 16 * w, g, c),
                           Qd::ld(sdY + c * LDR + 32 * rp + 4 * g), Qd::ld(sdY + c * LDR + 32 * rp + 16 + 4 * g), acc);
         Qd::st(dq + e0, Qd::cvt(acc));
-        const quad qT = Qd::cvt(Qd::mma16(Qd::cvt(qv), fI, zero4()));   // q[t = 4g + i][j = 16 w + c]
+        const quad qT = Qd::cvt(Qd::mma16(qq, CARVE_FI(), zero4()));   // q[t = 4g + i][j = 16 w + c]
         for (int rt = 0; rt < NRT; ++rt) dF[rt] = Qd::mma16(Qd::ld_tr(sdY, LDR, 0, 16 * rt, g, c), qT, dF[rt]);
       }
       // the next block (BK1) rewrites sTau, sTm, sP, sGam, sBeta, sSx, sdSx and the
@@ -577,15 +580,36 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_vparam_kernel(BwdArg
     }
 }
 
-// Sum nparts partial records (2 * half floats each) in a fixed order.
-__global__ void carve_param_reduce_kernel(const float* __restrict__ part, int nparts, size_t half, float* dst0,
-                                          float* dst1) {
-  const size_t x = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (x >= 2 * half) return;
+// Sum nparts partial records (2 * half floats each) in a fixed order: thread
+// (x, y) of a 64 x 4 block sums records y, y + 4, ... of element x, then the
+// four partial sums are added in order y = 0..3.
+__global__ void __launch_bounds__(256) carve_param_reduce_kernel(const float* __restrict__ part, int nparts,
+                                                                 size_t half, float* dst0, float* dst1) {
+  __shared__ float red[4][64];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const size_t x = (size_t)blockIdx.x * 64 + tx;
+  const size_t n = 2 * half;
   float s = 0.0f;
-  for (int p = 0; p < nparts; ++p) s += part[(size_t)p * 2 * half + x];
-  if (x < half) dst0[x] = s;
-  else dst1[x - half] = s;
+  if (x < n) {
+    const float* p = part + x;
+    int q = ty;
+    for (; q + 12 < nparts; q += 16) {
+      const float a0 = p[(size_t)q * n], a1 = p[(size_t)(q + 4) * n];
+      const float a2 = p[(size_t)(q + 8) * n], a3 = p[(size_t)(q + 12) * n];
+      s += a0;
+      s += a1;
+      s += a2;
+      s += a3;
+    }
+    for (; q < nparts; q += 4) s += p[(size_t)q * n];
+  }
+  red[ty][tx] = s;
+  __syncthreads();
+  if (ty == 0 && x < n) {
+    const float t = ((red[0][tx] + red[1][tx]) + red[2][tx]) + red[3][tx];
+    if (x < half) dst0[x] = t;
+    else dst1[x - half] = t;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -696,9 +720,8 @@ int launch_bwd_uparam(const BwdArgs& a, int dtype, int D, hipStream_t s) {
 }
 
 int launch_param_reduce(const float* part, int nparts, size_t half, float* dst0, float* dst1, hipStream_t s) {
-  const int threads = 256;
-  const int blocks = (int)((2 * half + threads - 1) / threads);
-  hipLaunchKernelGGL(carve_param_reduce_kernel, dim3(blocks), dim3(threads), 0, s, part, nparts, half, dst0, dst1);
+  const int blocks = (int)((2 * half + 63) / 64);
+  hipLaunchKernelGGL(carve_param_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, nparts, half, dst0, dst1);
   return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
 }
 
