@@ -142,6 +142,20 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
         *reinterpret_cast<u32x4*>(sF + rr * LDD + j) = *reinterpret_cast<const u32x4*>(src + rr * D + j);
       }
     }
+    // pending dq / dF update of the last processed block (its BQ step)
+    f32x4 pdqp = zero4();
+    quad pqq = Qd::cvt(zero4());
+    int pe0 = 0;
+#define CARVE_BWD_BQ()                                                                        \
+  do {                                                                                        \
+    f32x4 acc_ = pdqp;                                                                        \
+    for (int rp = 0; rp < R2 / 32; ++rp)                                                      \
+      acc_ = Qd::mma32(Qd::ld_tr(sF, LDD, 32 * rp, 16 * w, g, c), Qd::ld_tr(sF, LDD, 32 * rp + 16, 16 * w, g, c), \
+                       Qd::ld(sdY + c * LDR + 32 * rp + 4 * g), Qd::ld(sdY + c * LDR + 32 * rp + 16 + 4 * g), acc_); \
+    Qd::st(dq + pe0, Qd::cvt(acc_));                                                          \
+    const quad qT_ = Qd::cvt(Qd::mma16(pqq, CARVE_FI(), zero4()));   /* q[t = 4g + i][j = 16 w + c] */ \
+    for (int rt = 0; rt < NRT; ++rt) dF[rt] = Qd::mma16(Qd::ld_tr(sdY, LDR, 0, 16 * rt, g, c), qT_, dF[rt]); \
+  } while (0)
 #pragma unroll 1
     for (int bc = nbc - 1; bc >= 0; --bc) {
       // opaque copies of the lane coordinates: values derived from them
@@ -155,47 +169,72 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
       const int tb = ch * L + 16 * bc;   // first token of the block
       const int e0 = (tb + c) * rs + 16 * w + 4 * g;
 
-      // -- BK1: stage the block record; recompute the key side; S, dS' -> LDS ---
+      // -- BK1 (a): this block's global data ---------------------------------------
+      constexpr int NTAU = 16 * R2 / VEC;   // 16-byte vectors of the block's tau
+      constexpr int NTV = (NTAU + NT - 1) / NT;
+      u32x4 ltau[NTV];
+      quad ltm, lpm;
+      f32x4 lgam;
+      T lbeta = (T)0.0f;
       {
         const T* tau = reinterpret_cast<const T*>(rc + cr.Tau) + 16 * bc * R2;
-        for (int x = tid; x < 16 * R2 / VEC; x += NT) {
-          const int t = x / (R2 / VEC), r = (x % (R2 / VEC)) * VEC;
-          *reinterpret_cast<u32x4*>(sTau + t * LDR + r) = *reinterpret_cast<const u32x4*>(tau + t * R2 + r);
+        for (int u = 0; u < NTV; ++u) {
+          const int x = tid + u * NT;
+          if (x < NTAU) ltau[u] = *reinterpret_cast<const u32x4*>(tau + x * VEC);
         }
         if (tid < 64) {
-          const T* tm = reinterpret_cast<const T*>(rc + cr.Tm) + bc * 256 + 4 * tid;
-          const T* pm = reinterpret_cast<const T*>(rc + cr.P) + bc * 256 + 4 * tid;
-          const int t = tid >> 2, s4 = 4 * (tid & 3);
-          Qd::st(sTm + t * LDB + s4, Qd::ld(tm));
-          Qd::st(sP + t * LDB + s4, Qd::ld(pm));
+          ltm = Qd::ld(reinterpret_cast<const T*>(rc + cr.Tm) + bc * 256 + 4 * tid);
+          lpm = Qd::ld(reinterpret_cast<const T*>(rc + cr.P) + bc * 256 + 4 * tid);
         }
-        if (tid < D / 4)
-          *reinterpret_cast<f32x4*>(sGam + 4 * tid) =
-              *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(rc + cr.Gam) + bc * D + 4 * tid);
-        if (tid < 16) sBeta[tid] = (float)beta[(tb + tid) * H];
+        if (tid < D / 4) lgam = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(rc + cr.Gam) + bc * D + 4 * tid);
+        if (tid < 16) lbeta = beta[(tb + tid) * H];
       }
       quad sbq[NJT];   // block start state, wave layout: S[16 w + c][16 jt + 4 g + e]
       {
         const T* sv = reinterpret_cast<const T*>(rc + cr.S) + ((size_t)bc * NT + tid) * 4 * NJT;
         for (int jt = 0; jt < NJT; ++jt) sbq[jt] = Qd::ld(sv + 4 * jt);
       }
-      // key-side factors kept for the adjoint in the token dtype (quads)
-      quad kq, qq, Eq, Eiq, sigq;
+      quad ltq[NRB];
       {
-        const T* tau = reinterpret_cast<const T*>(rc + cr.Tau) + (16 * bc + c) * R2 + 4 * g;
+        const T* tq = reinterpret_cast<const T*>(rc + cr.Tau) + (16 * bc + c) * R2 + 4 * g;
+        for (int ks = 0; ks < NRB; ++ks) ltq[ks] = Qd::ld(tq + 16 * ks);
+      }
+      const quad lbx = Qd::ld(bx + e0);
+      const f32x4 lg = *reinterpret_cast<const f32x4*>(gl + e0);
+      const quad kq = Qd::ld(k + e0), qq = Qd::ld(q + e0);
+      const quad wxq = Qd::ld(wx + e0), vq = Qd::ld(v + e0), dOq = Qd::ld(dO + e0);
+
+      // -- BQ of the previous block (overlaps the loads above) -------------------
+      if (bc < nbc - 1) CARVE_BWD_BQ();
+
+      // -- BK1 (c): stage the block record; recompute the key side; S, dS' -> LDS
+      for (int u = 0; u < NTV; ++u) {
+        const int x = tid + u * NT;
+        if (x < NTAU) {
+          const int t = x / (R2 / VEC), r = (x % (R2 / VEC)) * VEC;
+          *reinterpret_cast<u32x4*>(sTau + t * LDR + r) = ltau[u];
+        }
+      }
+      if (tid < 64) {
+        const int t = tid >> 2, s4 = 4 * (tid & 3);
+        Qd::st(sTm + t * LDB + s4, ltm);
+        Qd::st(sP + t * LDB + s4, lpm);
+      }
+      if (tid < D / 4) *reinterpret_cast<f32x4*>(sGam + 4 * tid) = lgam;
+      if (tid < 16) sBeta[tid] = (float)lbeta;
+      // key-side factors kept for the adjoint in the token dtype (quads)
+      quad Eq, Eiq, sigq;
+      {
         f32x4 z = zero4();
-        for (int ks = 0; ks < NRB; ++ks) z = Qd::mma16(CARVE_FVB(ks), Qd::ld(tau + 16 * ks), z);
-        const f32x4 bxv = Qd::f32(Qd::ld(bx + e0));
-        const f32x4 gv = *reinterpret_cast<const f32x4*>(gl + e0);
-        kq = Qd::ld(k + e0);
-        qq = Qd::ld(q + e0);
+        for (int ks = 0; ks < NRB; ++ks) z = Qd::mma16(CARVE_FVB(ks), ltq[ks], z);
+        const f32x4 bxv = Qd::f32(lbx);
         const f32x4 kv = Qd::f32(kq), qv = Qd::f32(qq);
         f32x4 kt, qt, ki, E, Ei, sig;
         for (int i = 0; i < 4; ++i) {
           float sp, sg;
           softplus_sigmoid(z[i] + bxv[i], sp, sg);
           sig[i] = sg;
-          const float lam = row_scan(gv[i] - sp);
+          const float lam = row_scan(lg[i] - sp);
           E[i] = fast_exp(lam);
           Ei[i] = fast_exp(-lam);
           kt[i] = kv[i] * row_shr1(E[i], 1.0f);
@@ -210,7 +249,6 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
         Qd::st(sQt + ro, Qd::cvt(qt));
         Qd::st(sKi + ro, Qd::cvt(ki));
       }
-      const quad wxq = Qd::ld(wx + e0), vq = Qd::ld(v + e0), dOq = Qd::ld(dO + e0);
       for (int jt = 0; jt < NJT; ++jt) {
         Qd::st(sSx + (16 * w + c) * LDD + 16 * jt + 4 * g, sbq[jt]);
         Qd::st(sdSx + (16 * w + c) * LDD + 16 * jt + 4 * g, Qd::cvt(dSt[jt]));
@@ -406,20 +444,12 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
       }
       __syncthreads();
 
-      // -- BQ: dq = dQt e^{lam} + F^T dY^T (key tile), dF += dY^T q ---------------
-      {
-        f32x4 acc = dqp;
-        for (int rp = 0; rp < R2 / 32; ++rp)
-          acc = Qd::mma32(Qd::ld_tr(sF, LDD, 32 * rp, 16 * w, g, c), Qd::ld_tr(sF, LDD, 32 * rp + 16, 16 * w, g, c),
-                          Qd::ld(sdY + c * LDR + 32 * rp + 4 * g), Qd::ld(sdY + c * LDR + 32 * rp + 16 + 4 * g), acc);
-        Qd::st(dq + e0, Qd::cvt(acc));
-        const quad qT = Qd::cvt(Qd::mma16(qq, CARVE_FI(), zero4()));   // q[t = 4g + i][j = 16 w + c]
-        for (int rt = 0; rt < NRT; ++rt) dF[rt] = Qd::mma16(Qd::ld_tr(sdY, LDR, 0, 16 * rt, g, c), qT, dF[rt]);
-      }
-      // the next block (BK1) rewrites sTau, sTm, sP, sGam, sBeta, sSx, sdSx and the
-      // key-side buffers, all last read before the barrier above; sdY is read just
-      // now and rewritten only after two more barriers
+      // BQ of this block runs at the top of the next block (or before the glue)
+      pdqp = dqp;
+      pqq = qq;
+      pe0 = e0;
     }
+    CARVE_BWD_BQ();
 
     // ---- glue: dS += [Ub; Uw]^T dF; dF is parked in the chunk record for
     // d[Ub; Uw] += dF S_hat^T (carve_bwd_uparam_kernel).  dF enters the product
@@ -464,6 +494,7 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
     }
   }  // chunks
 
+#undef CARVE_BWD_BQ
   if (a.dS0) {
     float* dst = a.dS0 + soff + (16 * w + c) * D + 4 * g;
     for (int jt = 0; jt < NJT; ++jt) *reinterpret_cast<f32x4*>(dst + 16 * jt) = dSt[jt];
