@@ -1,0 +1,88 @@
+"""Parity at the full workload sizes, in the launch configuration the benchmark
+times (the whole batch and all heads in one call), on sampled (batch, head)
+slices.
+
+Every output of a slice (o, S_T, S_chunks and the token gradients, dS0 too)
+depends only on that slice's inputs and the shared parameters, so the oracle
+runs on the sampled slices alone.  The parameter gradients are sums over all
+slices: the upstream gradients dO and dS_T are zeroed outside the sampled
+slices, which makes every other slice's contribution exactly zero, so the
+full-size parameter gradients of the GPU must equal the oracle's sum over the
+sampled slices.
+
+Bar: bf16 inputs with f32 state and accumulation, max-rel <= 2e-2 per tensor.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as orc
+from paper_2606_27229_amd import carve
+from paper_2606_27229_amd.inputs import CHUNK_SWEEP, WORKLOADS, make_inputs
+from tests.gpu_util import host, max_rel, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+TOKEN_KEYS = ("q", "k", "v", "beta", "g", "bx", "wx", "dO")
+TOKEN_GRADS = ("dq", "dk", "dv", "dbeta", "dg", "dbx", "dwx")
+PARAM_GRADS = ("dUb", "dUw", "dVb", "dVw")
+
+CASES = [("layer_1p3b_T2048", 64), ("long_seq_T16384", 64)] + [("layer_1p3b_T4096", L) for L in CHUNK_SWEEP]
+
+
+def _slice(inp, b, h):
+    out = {}
+    for key, val in inp.items():
+        if val is None:
+            out[key] = None
+        elif key in TOKEN_KEYS:
+            out[key] = np.ascontiguousarray(val[b:b + 1, :, h:h + 1])
+        elif key in ("S0", "dS_T"):
+            out[key] = np.ascontiguousarray(val[b:b + 1, h:h + 1])
+        else:
+            out[key] = val
+    return out
+
+
+@pytest.mark.parametrize("name,L", CASES)
+def test_full_size_sampled(name, L):
+    w = WORKLOADS[name].with_(L=L)
+    print(f"case {name} L={L}: B={w.B} H={w.H} T={w.T}", flush=True)
+    inp = make_inputs(w, seed=100 + L, dS_T=True)
+    samples = [(0, 0), (w.B - 1, w.H - 1)]
+    keep = np.zeros((w.B, w.H), dtype=bool)
+    for b, h in samples:
+        keep[b, h] = True
+    inp["dO"] = inp["dO"] * keep[:, None, :, None]
+    inp["dS_T"] = inp["dS_T"] * keep[:, :, None, None]
+
+    x = to_gpu(inp, torch.bfloat16)
+    o, S_T, S_chunks = carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"],
+                                       x["Uw"], x["Vb"], x["Vw"], x["S0"], L=L)
+    gr = carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
+                         x["Vb"], x["Vw"], S_chunks, x["dO"], x["dS_T"], L=L)
+    torch.cuda.synchronize()
+    del x
+
+    ref_params = {key: 0.0 for key in PARAM_GRADS}
+    errs = {}
+    for b, h in samples:
+        s = _slice(inp, b, h)
+        rf = orc.fwd_serial(s, L, want_chunks=True)
+        rb = orc.bwd(s, L, s["dO"], s["dS_T"])
+        got = {"o": host(o[b:b + 1, :, h:h + 1]), "S_T": host(S_T[b:b + 1, h:h + 1]),
+               "S_chunks": host(S_chunks[b:b + 1, h:h + 1])}
+        for key in ("o", "S_T", "S_chunks"):
+            errs[f"{key}[{b},{h}]"] = max_rel(got[key], rf[key])
+        for key in TOKEN_GRADS:
+            g_ = host(gr[key][b:b + 1, :, h:h + 1])
+            errs[f"{key}[{b},{h}]"] = max_rel(g_, rb[key])
+        errs[f"dS0[{b},{h}]"] = max_rel(host(gr["dS0"][b:b + 1, h:h + 1]), rb["dS0"])
+        for key in PARAM_GRADS:
+            ref_params[key] = ref_params[key] + rb[key]
+    for key in PARAM_GRADS:
+        errs[key] = max_rel(host(gr[key]), ref_params[key])
+    print("max-rel errors:", {k: float("%.3g" % e) for k, e in errs.items()}, flush=True)
+    bad = {k: e for k, e in errs.items() if not e <= TOL}
+    assert not bad, bad
