@@ -64,6 +64,16 @@ int pick_lw(const carve_dims_t* d, bool bwd) {
   return 0;
 }
 
+// largest WY block (<= 64 tokens, dividing L) whose chain-forward LDS layout fits
+int pick_wb(const carve_dims_t* d) {
+  const int RP = round_rp(d->R);
+  for (int wb = 64; wb >= 16; wb /= 2) {
+    if (wb > d->L || d->L % wb) continue;
+    if (chain_lds_bytes(d->dtype, d->Dk, wb, RP) <= kMaxLds) return wb;
+  }
+  return 0;
+}
+
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 struct Range {
@@ -134,14 +144,15 @@ int carve_chunk_fwd(const carve_dims_t* d, const void* q, const void* k, const v
                        {Vw, (size_t)d->Dv * d->R * 4}, {S0, nst * 4}};
   const Range outs[] = {{o, ntok * d->Dv * es}, {S_T, nst * 4}, {S_chunks, nst * (d->T / d->L) * 4}};
   if (any_overlap(outs, 3, ins, 12)) return CARVE_ERR_UNSUPPORTED;
-  const int lw = pick_lw(d, false);
-  if (!lw) return CARVE_ERR_UNSUPPORTED;
+  const int wb = pick_wb(d);
+  if (!wb) return CARVE_ERR_UNSUPPORTED;
   FwdArgs a;
   a.q = q; a.k = k; a.v = v; a.beta = beta; a.bx = bx; a.wx = wx;
   a.g = g; a.Ub = Ub; a.Uw = Uw; a.Vb = Vb; a.Vw = Vw; a.S0 = S0;
   a.o = o; a.S_T = S_T; a.S_chunks = S_chunks;
   a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = round_rp(d->R); a.L = d->L;
-  return launch_fwd(a, d->dtype, d->Dk, lw, stream);
+  a.rec = nullptr;
+  return launch_chain_fwd(a, d->dtype, d->Dk, wb, stream);
 }
 
 int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const void* v,

@@ -191,8 +191,8 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
       }
       quad sbq[NJT];   // block start state, wave layout: S[16 w + c][16 jt + 4 g + e]
       {
-        const T* sv = reinterpret_cast<const T*>(rc + cr.S) + ((size_t)bc * NT + tid) * 4 * NJT;
-        for (int jt = 0; jt < NJT; ++jt) sbq[jt] = Qd::ld(sv + 4 * jt);
+        const T* sv = reinterpret_cast<const T*>(rc + cr.S) + (size_t)bc * NJT * NT * 4 + tid * 4;
+        for (int jt = 0; jt < NJT; ++jt) sbq[jt] = Qd::ld(sv + (size_t)jt * NT * 4);
       }
       quad ltq[NRB];
       {
@@ -502,11 +502,12 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
 }
 
 // d[Ub; Uw][r][v] = sum over the chunks of one split of sum_j dF[r][j] S_hat[v][j];
-// wave w owns value tile w (S_hat read in the wave layout of the chunk record).
+// wave w owns value tile w (S_hat read in the thread layout of the chunk record).
 template <typename T, int D, int RP>
 __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_uparam_kernel(BwdArgs a) {
   typedef Quad<T> Qd;
   typedef typename Qd::q quad;
+  constexpr int NT = bwd_threads(D);
   constexpr int NJT = D / 16;
   constexpr int R2 = 2 * RP;
   constexpr int NRT = R2 / 16;
@@ -523,10 +524,10 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_uparam_kernel(BwdArg
   const int c0 = split * per, c1 = c0 + per < nch ? c0 + per : nch;
   for (int ch = c0; ch < c1; ++ch) {
     const char* rc = recb + (size_t)ch * cr.total;
-    const T* sv = reinterpret_cast<const T*>(rc + cr.S) + (size_t)tid * 4 * NJT;
+    const T* sv = reinterpret_cast<const T*>(rc + cr.S) + (size_t)tid * 4;
     const float* dFr = reinterpret_cast<const float*>(rc + cr.dF);
     quad sb[NJT];
-    for (int jt = 0; jt < NJT; ++jt) sb[jt] = Qd::ld(sv + 4 * jt);
+    for (int jt = 0; jt < NJT; ++jt) sb[jt] = Qd::ld(sv + (size_t)jt * NT * 4);
     for (int rt = 0; rt < NRT; ++rt)
       for (int jt = 0; jt < NJT; ++jt)
       {

@@ -346,8 +346,9 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
       for (int bb = 0; bb < NB; ++bb) {
         if (bb > 0) CARVE_FWD_XKQ(bb);
         if (REC) {
-          T* sv = reinterpret_cast<T*>(rec + cr.S) + ((size_t)(m * NB + bb) * NT + tid) * 4 * NJT;
-          for (int jt = 0; jt < NJT; ++jt) Qd::st(sv + 4 * jt, sb[jt]);
+          // coalesced: quad jt of every thread is contiguous over the threads
+          T* sv = reinterpret_cast<T*>(rec + cr.S) + (size_t)(m * NB + bb) * NJT * NT * 4 + tid * 4;
+          for (int jt = 0; jt < NJT; ++jt) Qd::st(sv + (size_t)jt * NT * 4, sb[jt]);
         }
         const f32x4 bt = *reinterpret_cast<const f32x4*>(sBeta + 16 * bb + 4 * g);
         f32x4 rr;

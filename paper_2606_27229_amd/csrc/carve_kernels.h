@@ -23,7 +23,8 @@ struct FwdArgs {
 //   Tm  [L/16][16][16]           T = (I + A)^{-1} of every 16-token block
 //   P   [L/16][16][16]           P of every block
 //   Gam [L/16][D]  f32           block retention e^{lam_15}
-//   S   [L/16][D*D]              block start states, wave layout (lane-major)
+//   S   [L/16][D/16][threads][4]  block start states: quad jt of thread tid
+//                                 (S[16 w + c][16 jt + 4 g + e]), contiguous over threads
 //   dF  [2RP][D]   f32           written by the adjoint: the chunk's gradient of F
 struct ChunkRec {
   size_t F, Tau, Tm, P, Gam, S, dF, total;
@@ -49,6 +50,9 @@ __host__ __device__ constexpr ChunkRec chunk_rec(size_t e, int D, int L, int RP)
 __host__ __device__ constexpr int fwd_threads(int D) { return (D / 16) * 64; }
 // threads of a backward workgroup: one wave per 16-column tile of the state
 __host__ __device__ constexpr int bwd_threads(int D) { return (D / 16) * 64; }
+
+// LDS per workgroup on gfx950
+constexpr size_t kMaxLdsBytes = 160 * 1024;
 
 __host__ __device__ constexpr size_t lds_round(size_t x) { return (x + 15) & ~(size_t)15; }
 __host__ __device__ constexpr size_t lds_max(size_t a, size_t b) { return a > b ? a : b; }
@@ -95,6 +99,45 @@ __host__ __device__ constexpr FwdLds fwd_lds() {
   l.total = off;
   return l;
 }
+
+// LDS layout of the chain forward for one WY block of WB tokens (NB = WB / 16
+// token tiles).  Rows are padded by 16 bytes.  Region X holds the chunk start
+// state while the fold reads it, then the block's raw erase logits (Bx) and the
+// decayed keys Kt; Ki holds the block's raw keys until the gates turn them
+// into Ki in place.
+struct ChainLds {
+  size_t U, X, Kt, Bx, Ki, F, Q, Tau, A, P, AdT, TmT, Rho, Beta, total;
+};
+
+template <typename T, int D, int WB, int RP>
+__host__ __device__ constexpr ChainLds chain_lds() {
+  ChainLds l{};
+  const size_t e = sizeof(T);
+  constexpr size_t NB = WB / 16;
+  constexpr size_t PAD = 16 / sizeof(T);
+  constexpr size_t LDD = D + PAD, LDR = 2 * RP + PAD, LDW = WB + PAD, LDB = 16 + PAD;
+  size_t off = 0;
+  l.U = off;    off += lds_round(2 * RP * LDD * e);
+  l.X = off;    off += lds_round(lds_max(D * LDD * e, 2 * lds_round(WB * LDD * e)));
+  l.Kt = l.X;
+  l.Bx = l.X + lds_round(WB * LDD * e);
+  l.Ki = off;   off += lds_round(WB * LDD * e);
+  l.F = off;    off += lds_round(2 * RP * LDD * e);
+  l.Q = off;    off += lds_round(WB * LDD * e);
+  l.Tau = off;  off += lds_round(WB * LDR * e);
+  l.A = off;    off += lds_round(WB * LDW * e);
+  l.P = off;    off += lds_round(WB * LDW * e);
+  l.AdT = off;  off += lds_round(NB * 16 * 20 * 4);
+  l.TmT = off;  off += lds_round(NB * 16 * LDB * e);
+  l.Rho = off;  off += lds_round(D * 4);
+  l.Beta = off; off += lds_round(2 * WB * 4);
+  l.total = off;
+  return l;
+}
+
+// forward of the whole sequence (one workgroup per (batch, head)), WY blocks of WB tokens
+int launch_chain_fwd(const FwdArgs& a, int dtype, int D, int WB, hipStream_t s);
+size_t chain_lds_bytes(int dtype, int D, int WB, int RP);
 
 int launch_fwd(const FwdArgs& a, int dtype, int D, int LW, hipStream_t s);
 // chunk-parallel forward recompute that writes the chunk records (a.rec)
