@@ -43,8 +43,11 @@ namespace carve {
 // hoisted above the previous one (bounds the number of live operand registers).
 #define CARVE_SEQ() asm volatile("" ::: "memory")
 
+// one workgroup per CU (its LDS layout), so two waves per SIMD: the full
+// register file of a wave is available
 template <typename T, int D, int RP>
-__global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
+__global__ void __launch_bounds__(bwd_threads(D)) __attribute__((amdgpu_waves_per_eu(1, 2)))
+carve_bwd_kernel(BwdArgs a) {
   typedef Quad<T> Qd;
   typedef typename Qd::q quad;
   typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
@@ -460,14 +463,18 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_kernel(BwdArgs a) {
       float* dFr = reinterpret_cast<float*>(const_cast<char*>(rc) + cr.dF);
       // [Ub; Uw] operand quads, lane (g, c): U[16 rt + 4 g + e][16 w + c]; the
       // opaque column keeps these loads inside the chunk loop (short live range)
+      // (rows past R are zero: clamped unconditional loads times a mask, so the
+      // sixteen loads are issued back to back and waited for once)
       quad fU[NRT];
       int col = 16 * w + c;
       asm volatile("" : "+v"(col));
       for (int rt = 0; rt < NRT; ++rt) {
+        const float* src = rt < RP / 16 ? a.Ub : a.Uw;
         f32x4 tu;
         for (int e = 0; e < 4; ++e) {
-          const int rr = 16 * rt + 4 * g + e;
-          tu[e] = rr < R ? a.Ub[rr * D + col] : (rr >= RP && rr < RP + R) ? a.Uw[(rr - RP) * D + col] : 0.0f;
+          const int rl = 16 * (rt % (RP / 16)) + 4 * g + e;
+          const float x = src[(rl < R ? rl : R - 1) * D + col];
+          tu[e] = rl < R ? x : 0.0f;
         }
         fU[rt] = Qd::cvt(tu);
       }

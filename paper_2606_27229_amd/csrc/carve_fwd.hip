@@ -40,7 +40,8 @@ namespace carve {
 // REC = true: recompute for the backward, one workgroup per (batch, head,
 // chunk) starting from S_chunks; writes the chunk record instead of outputs.
 template <typename T, int D, int LW, int RP, bool REC>
-__global__ void __launch_bounds__(fwd_threads(D)) carve_fwd_kernel(FwdArgs a) {
+__global__ void __launch_bounds__(fwd_threads(D)) __attribute__((amdgpu_waves_per_eu(1, 2)))
+carve_fwd_kernel(FwdArgs a) {
   typedef Quad<T> Qd;
   typedef typename Qd::q quad;
   typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
