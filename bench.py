@@ -24,28 +24,34 @@ sys.path.insert(0, ROOT)
 METRIC = "layer fwd+bwd tokens/s, H=16 d=128 T=4096 L=64 bf16; % MFMA peak"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
-KERNEL_SOURCES = ("paper_2606_27229_amd/csrc/carve_fwd.hip", "paper_2606_27229_amd/csrc/carve_bwd.hip",
-                  "paper_2606_27229_amd/csrc/carve_dev.h", "paper_2606_27229_amd/csrc/carve_kernels.h")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer_1p3b_T4096.json")
+KERNEL_SOURCES = ("paper_2606_27229_amd/csrc/carve_fwd_chain.hip", "paper_2606_27229_amd/csrc/carve_fwd.hip",
+                  "paper_2606_27229_amd/csrc/carve_bwd.hip", "paper_2606_27229_amd/csrc/carve_dev.h",
+                  "paper_2606_27229_amd/csrc/carve_kernels.h")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer_1p3b_T4096_L64.json")
 
 
 def algorithmic_counts(B, T, H, d, R, L):
-    """Algorithmic bytes and flops per call, per kernel (inputs/outputs once).
+    """Algorithmic bytes and flops per call (every input and output once).
 
     Bytes per token-head (bf16 token tensors, f32 g and states):
-      forward  reads q,k,v (3*2d) + g (4d) + bx,wx (2*2d) + beta (2), writes
-               o (2d) + chunk-start states (4 d^2 / L)
-      backward reads the forward inputs + dO (2d) + chunk-start states, writes
-               dq,dk,dv (3*2d) + dg (4d) + dbx,dwx (2*2d) + dbeta (2)
+      forward kernel   reads q, k, v (3*2d) + g (4d) + bx, wx (2*2d) + beta (2);
+                       writes o (2d) + chunk-start states (4 d^2 / L)
+      adjoint kernel   reads the forward inputs + dO (2d); writes dq, dk, dv
+                       (3*2d) + dg (4d) + dbx, dwx (2*2d) + dbeta (2)
+      whole backward   the adjoint's bytes + the chunk-start states it needs
+                       (4 d^2 / L, read by the recompute)
     Flops per token-head (multiply-add = 2): forward
       2 * (2 r d^2 / L + 3 d^2 + 4 r d + 5/2 L d + L^2 / 6), backward 2x forward.
     """
     th = B * T * H
-    fwd_bytes = (3 * 2 * d + 4 * d + 2 * 2 * d + 2) + (2 * d + 4 * d * d / L)
-    bwd_bytes = (3 * 2 * d + 4 * d + 2 * 2 * d + 2) + 2 * d + 4 * d * d / L + (3 * 2 * d + 4 * d + 2 * 2 * d + 2)
+    inputs = 3 * 2 * d + 4 * d + 2 * 2 * d + 2
+    grads = 3 * 2 * d + 4 * d + 2 * 2 * d + 2
+    states = 4 * d * d / L
     fwd_mac = 2 * R * d * d / L + 3 * d * d + 4 * R * d + 2.5 * L * d + L * L / 6.0
     return {
-        "fwd_bytes": fwd_bytes * th, "bwd_bytes": bwd_bytes * th,
+        "fwd_bytes": (inputs + 2 * d + states) * th,
+        "adjoint_bytes": (inputs + 2 * d + grads) * th,
+        "bwd_bytes": (inputs + 2 * d + grads + states) * th,
         "fwd_flops": 2 * fwd_mac * th, "bwd_flops": 4 * fwd_mac * th,
     }
 
@@ -72,23 +78,81 @@ def load_traffic(kernel):
     return None if k is None else k.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, L, seed):
-    """Time the CPU oracle (fwd + exact bwd) on one batch element of the workload."""
+TRAFFIC_KERNELS = {"carve_chain_fwd_kernel": "carve_chain_fwd_kernel", "carve_bwd_kernel": "16carve_bwd_kernel"}
+
+
+def _pmc_per_dispatch(run_dir, counter):
+    """{kernel name: [counter value per dispatch]} from a rocprofv3 --pmc csv run."""
+    import csv
+    import glob
+    vals = {}
+    for path in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for row in csv.DictReader(f):
+                if row["Counter_Name"] != counter:
+                    continue
+                key = (row["Kernel_Name"], row["Dispatch_Id"])
+                vals[key] = vals.get(key, 0.0) + float(row["Counter_Value"])
+    out = {}
+    for (name, _), v in vals.items():
+        out.setdefault(name, []).append(v)
+    return out
+
+
+def traffic_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir):
+    """Scale the FETCH_SIZE / WRITE_SIZE counters (KiB per dispatch) by what they
+    read for a plain copy of known size and write the per-launch HBM traffic of
+    the headline kernels to TRAFFIC_FILE, tagged with the kernel-source hash."""
+    n_copy = 1 << 30
+
+    def copy_factor(d, counter):
+        per = _pmc_per_dispatch(d, counter)
+        big = max((sum(v) / len(v), name) for name, v in per.items())
+        return n_copy / (big[0] * 1024.0), big[1]
+
+    ff, copy_name = copy_factor(copy_fetch_dir, "FETCH_SIZE")
+    wf, _ = copy_factor(copy_write_dir, "WRITE_SIZE")
+    fetch = _pmc_per_dispatch(fetch_dir, "FETCH_SIZE")
+    write = _pmc_per_dispatch(write_dir, "WRITE_SIZE")
+    rec = {"source_hash": kernel_source_hash(), "copy_kernel": copy_name,
+           "fetch_factor": ff, "write_factor": wf, "kernels": {}}
+    for key, pat in TRAFFIC_KERNELS.items():
+        fv = [v for name, vs in fetch.items() if pat in name for v in vs]
+        wv = [v for name, vs in write.items() if pat in name for v in vs]
+        if not fv or not wv:
+            continue
+        fb = sum(fv) / len(fv) * 1024.0 * ff
+        wb = sum(wv) / len(wv) * 1024.0 * wf
+        rec["kernels"][key] = {"fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+                               "hbm_bytes_per_launch": fb + wb, "dispatches": len(fv)}
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec), flush=True)
+
+
+def cpu_baseline(w, L, seed, target_s=12.0):
+    """Time the CPU oracle (token-serial forward + exact backward, double) on the
+    whole workload batch, repeated until about target_s seconds of CPU work."""
     from oracle import oracle as orc
     from paper_2606_27229_amd.inputs import make_inputs
 
-    ws = w.with_(B=1)
-    inp = make_inputs(ws, seed=seed)
-    threads = max(1, min(16, os.cpu_count() or 1, ws.B * ws.H))
-    t0 = time.perf_counter()
-    orc.fwd_serial(inp, L, nthreads=threads)
-    t1 = time.perf_counter()
-    orc.bwd(inp, L, inp["dO"], None, nthreads=threads)
-    t2 = time.perf_counter()
-    tokens = ws.B * ws.T   # layer tokens (all heads) in the sample
-    return {"value": tokens / (t2 - t0), "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"B=1 of {w.B}, all {w.H} heads, T={w.T}, L={L}: token-serial forward + exact "
-                      f"reverse-mode backward in double, fwd {t1 - t0:.2f} s, bwd {t2 - t1:.2f} s"}
+    inp = make_inputs(w, seed=seed)
+    threads = max(1, min(16, os.cpu_count() or 1, w.B * w.H))
+    reps, t_f, t_b = 0, 0.0, 0.0
+    while reps == 0 or t_f + t_b < target_s:
+        t0 = time.perf_counter()
+        orc.fwd_serial(inp, L, nthreads=threads)
+        t1 = time.perf_counter()
+        orc.bwd(inp, L, inp["dO"], None, nthreads=threads)
+        t2 = time.perf_counter()
+        t_f += t1 - t0
+        t_b += t2 - t1
+        reps += 1
+    tokens = reps * w.B * w.T   # layer tokens (all heads) processed
+    return {"value": tokens / (t_f + t_b), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} x the whole batch (B={w.B}, H={w.H}, T={w.T}, L={L}): token-serial forward + "
+                      f"exact reverse-mode backward in double on {threads} threads, fwd {t_f:.1f} s, "
+                      f"bwd {t_b:.1f} s"}
 
 
 def main():
@@ -98,10 +162,16 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--L", type=int, default=64)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                    help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of this benchmark and of "
+                         "--copy-calibration into the traffic record read by the roofline (no GPU needed)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain elementwise copy of 1 GiB (reads 1 GiB, writes 1 GiB) "
                          "five times: the reference kernel for scaling the HBM byte counters")
     args = ap.parse_args()
+    if args.traffic_summary:
+        traffic_summary(*args.traffic_summary)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: the layer shards over (batch, head) with no exchange "
               "except a 64 KB parameter-gradient all-reduce, which this build does not run; "
@@ -170,26 +240,42 @@ def main():
         bwd()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    # launch-boundary events recorded by the library: forward 1 kernel, backward 6
+    NF, NB = 2, 7
+    ev_f = [[torch.cuda.Event(enable_timing=True) for _ in range(NF)] for _ in range(args.steps)]
+    ev_b = [[torch.cuda.Event(enable_timing=True) for _ in range(NB)] for _ in range(args.steps)]
+    for e in [x for row in ev_f + ev_b for x in row]:
+        e.record(stream)            # create the device events up front
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for s in range(args.steps):
-        ev[s][0].record(stream)
+    for s_ in range(args.steps):
+        carve.profile_events(ev_f[s_])
         fwd()
-        ev[s][1].record(stream)
+        carve.profile_events(ev_b[s_])
         bwd()
-        ev[s][2].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    fwd_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
-    bwd_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
     ms_per_step = wall * 1e3 / args.steps
+
+    def avg(rows, i):
+        return sum(r[i].elapsed_time(r[i + 1]) for r in rows) / len(rows)
+
+    bwd_names = ["carve_fwd_kernel<recompute>", "carve_bwd_kernel", "carve_bwd_vparam_kernel",
+                 "carve_bwd_uparam_kernel", "carve_param_reduce_kernel[dU]", "carve_param_reduce_kernel[dV]"]
+    kernels_ms = {"carve_chain_fwd_kernel": avg(ev_f, 0)}
+    for i, name in enumerate(bwd_names):
+        kernels_ms[name] = avg(ev_b, i)
+    fwd_ms = kernels_ms["carve_chain_fwd_kernel"]
+    bwd_ms = sum(r[0].elapsed_time(r[NB - 1]) for r in ev_b) / args.steps
     tokens = B * T
     cnt = algorithmic_counts(B, T, H, d, R, L)
 
-    dominant = "carve_bwd_kernel" if bwd_ms >= fwd_ms else "carve_fwd_kernel"
-    dom_ms = bwd_ms if dominant == "carve_bwd_kernel" else fwd_ms
-    dom_bytes = cnt["bwd_bytes"] if dominant == "carve_bwd_kernel" else cnt["fwd_bytes"]
+    alg = {"carve_chain_fwd_kernel": cnt["fwd_bytes"], "carve_bwd_kernel": cnt["adjoint_bytes"]}
+    dominant = max(alg, key=lambda k_: kernels_ms[k_])
+    dom_ms = kernels_ms[dominant]
+    dom_bytes = alg[dominant]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    traffic = load_traffic(dominant)
     layer_tflops = (cnt["fwd_flops"] + cnt["bwd_flops"]) / (ms_per_step * 1e-3) / 1e12
     res = {
         "metric": METRIC,
@@ -208,9 +294,13 @@ def main():
                    "token_dtype": "bf16", "state_dtype": "f32"},
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": load_traffic(dominant),
+                     "traffic": None if traffic is None else traffic / (dom_ms * 1e-3) / 1e9,
+                     "traffic_bytes_per_launch": traffic,
                      "algorithmic_bytes_per_launch": dom_bytes, "avg_launch_ms": dom_ms},
-        "kernels_ms": {"carve_fwd_kernel": fwd_ms, "carve_bwd_kernel+param_reduce": bwd_ms},
+        "kernels_ms": kernels_ms,
+        "fwd_call_ms": fwd_ms,
+        "bwd_call_ms": bwd_ms,
+        "layer_hbm_frac": (cnt["fwd_bytes"] + cnt["bwd_bytes"]) / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "mfma_peak_frac": layer_tflops / BF16_PEAK_TFLOPS,
         "layer_tflops": layer_tflops,
     }

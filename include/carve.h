@@ -45,15 +45,19 @@
  *     different streams must use different workspaces.
  *   - Supported shapes: Dk == Dv in {32, 64, 128}; 1 <= R <= 64;
  *     L in {16, 32, 64, 128}; T a positive multiple of L; B, H >= 1.
- *     Not built: f32 token tensors with Dk = 128; the backward with R > 32
- *     at Dk = 128 (bf16) or at Dk = 64 (f32).  These, and other shapes,
- *     return CARVE_ERR_UNSUPPORTED (CARVE_ERR_SHAPE when T % L != 0 or a
- *     size is non-positive).
+ *     Not built (their LDS layouts exceed 160 KB): the forward with f32
+ *     token tensors at Dk = 128 and R > 32; the backward with f32 token
+ *     tensors at Dk = 128, and with R > 32 at Dk = 128 (bf16) or Dk = 64
+ *     (f32).  These, and other shapes, return CARVE_ERR_UNSUPPORTED
+ *     (CARVE_ERR_SHAPE when T % L != 0 or a size is non-positive).
  *   - Every pointer must be 16-byte aligned (CARVE_ERR_ALIGN).
  *   - Inputs are assumed finite with g <= 0; NaN/Inf propagate.  Numerical
- *     range: within any 16 consecutive tokens of a chunk the summed log
- *     retention g - softplus(z_b) of a key channel must stay above about
- *     -80 (the WY tiles factor e^{-(16-token log retention)} in f32).
+ *     range (log retention l = g - softplus(z_b) per key channel): the
+ *     forward evaluates WY blocks of up to 64 tokens of a chunk with factors
+ *     up to e^{|sum of l over the block| / 2}, so that sum must stay above
+ *     about -170; the backward evaluates 16-token tiles with factors up to
+ *     e^{|sum of l over the tile|}, so any 16 consecutive tokens must sum
+ *     above about -80.
  */
 #ifndef CARVE_H
 #define CARVE_H
@@ -117,6 +121,20 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
                     void* dv, void* dbeta, float* dg, void* dbx, void* dwx, float* dUb,
                     float* dUw, float* dVb, float* dVw, float* dS0, void* workspace,
                     size_t workspace_bytes, hipStream_t stream);
+
+/* Measurement hook (not part of the computation).  Arms the next
+ * carve_chunk_fwd / carve_chunk_bwd call made on the calling thread to record
+ * events[0] on its stream before its first kernel launch and events[i] after
+ * its i-th launch (the forward makes 1 launch; the backward 6: recompute,
+ * adjoint, dVb/dVw partials, d[Ub;Uw] partials, two fixed-order reductions),
+ * up to `capacity` events.  `events` are hipEvent_t handles created by the
+ * caller (hipEventCreate) and owned by the caller; the handles are copied
+ * here (the array may be freed after this call) and the events are only
+ * recorded, never synchronised.  The hook covers exactly one call and is
+ * cleared when that call returns, whatever its status; capacity 0 disarms
+ * it.  Returns CARVE_ERR_NULL for a NULL array with capacity > 0 or a
+ * negative capacity, CARVE_ERR_UNSUPPORTED for capacity > 16. */
+int carve_profile_events(hipEvent_t* events, int capacity);
 
 /* Static description of a status code. */
 const char* carve_status_string(int status);

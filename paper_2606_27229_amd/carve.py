@@ -17,7 +17,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libcarve.so")
 
 CARVE_F32, CARVE_BF16 = 0, 1
-SYMBOLS = ("carve_chunk_fwd", "carve_chunk_bwd", "carve_workspace_size", "carve_status_string")
+SYMBOLS = ("carve_chunk_fwd", "carve_chunk_bwd", "carve_workspace_size", "carve_status_string",
+           "carve_profile_events")
 
 
 class Dims(ctypes.Structure):
@@ -52,6 +53,8 @@ def load_library(path: str = LIB_PATH):
     lib.carve_chunk_fwd.restype = ctypes.c_int
     lib.carve_chunk_bwd.argtypes = [D] + [vp] * 7 + [fp] * 5 + [vp, fp] + [vp] * 12 + [vp, sz, vp]
     lib.carve_chunk_bwd.restype = ctypes.c_int
+    lib.carve_profile_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]
+    lib.carve_profile_events.restype = ctypes.c_int
     if path == LIB_PATH:
         _lib = lib
     return lib
@@ -59,6 +62,14 @@ def load_library(path: str = LIB_PATH):
 
 def status_string(st: int) -> str:
     return load_library().carve_status_string(st).decode()
+
+
+def profile_events(events) -> None:
+    """Arm the next chunk_fwd / chunk_bwd call on this thread to record the
+    given torch.cuda.Event objects at its kernel-launch boundaries (measurement
+    only).  The events must already exist on the device (record each once)."""
+    arr = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+    _check("carve_profile_events", load_library().carve_profile_events(arr, len(events)))
 
 
 def make_dims(B, T, H, Dk, Dv, R, L, dtype) -> Dims:

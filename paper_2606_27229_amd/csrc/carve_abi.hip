@@ -76,6 +76,23 @@ int pick_wb(const carve_dims_t* d) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// launch-boundary events of the next call on this thread (carve_profile_events);
+// the handles are copied when the hook is armed
+constexpr int kMaxProfEvents = 16;
+thread_local hipEvent_t g_prof_events[kMaxProfEvents];
+thread_local int g_prof_capacity = 0;
+thread_local int g_prof_count = 0;
+
+void prof_mark(hipStream_t stream) {
+  if (g_prof_count < g_prof_capacity) hipEventRecord(g_prof_events[g_prof_count++], stream);
+}
+
+// the hook covers exactly one call: it is cleared when that call returns,
+// whatever its status
+struct ProfClear {
+  ~ProfClear() { g_prof_capacity = 0; }
+};
+
 struct Range {
   const void* p;
   size_t bytes;
@@ -114,6 +131,16 @@ const char* carve_status_string(int status) {
   }
 }
 
+int carve_profile_events(hipEvent_t* events, int capacity) {
+  g_prof_capacity = 0;
+  if (capacity < 0 || (capacity > 0 && !events)) return CARVE_ERR_NULL;
+  if (capacity > kMaxProfEvents) return CARVE_ERR_UNSUPPORTED;
+  for (int i = 0; i < capacity; ++i) g_prof_events[i] = events[i];
+  g_prof_capacity = capacity;
+  g_prof_count = 0;
+  return CARVE_OK;
+}
+
 size_t carve_workspace_size(const carve_dims_t* d, int for_backward) {
   if (check_dims(d) != CARVE_OK) return 0;
   if (!for_backward) return 0;
@@ -128,6 +155,7 @@ int carve_chunk_fwd(const carve_dims_t* d, const void* q, const void* k, const v
                     size_t workspace_bytes, hipStream_t stream) {
   (void)workspace;
   (void)workspace_bytes;
+  ProfClear pc;
   int st = check_dims(d);
   if (st) return st;
   if (!q || !k || !v || !beta || !g || !bx || !wx || !Ub || !Uw || !Vb || !Vw || !o) return CARVE_ERR_NULL;
@@ -152,7 +180,10 @@ int carve_chunk_fwd(const carve_dims_t* d, const void* q, const void* k, const v
   a.o = o; a.S_T = S_T; a.S_chunks = S_chunks;
   a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = round_rp(d->R); a.L = d->L;
   a.rec = nullptr;
-  return launch_chain_fwd(a, d->dtype, d->Dk, wb, stream);
+  prof_mark(stream);
+  st = launch_chain_fwd(a, d->dtype, d->Dk, wb, stream);
+  prof_mark(stream);
+  return st;
 }
 
 int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const void* v,
@@ -162,6 +193,7 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
                     void* dv, void* dbeta, float* dg, void* dbx, void* dwx, float* dUb,
                     float* dUw, float* dVb, float* dVw, float* dS0, void* workspace,
                     size_t workspace_bytes, hipStream_t stream) {
+  ProfClear pc;
   int st = check_dims(d);
   if (st) return st;
   if (!q || !k || !v || !beta || !g || !bx || !wx || !Ub || !Uw || !Vb || !Vw || !S_chunks || !dO ||
@@ -199,8 +231,10 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
   f.o = nullptr; f.S_T = nullptr; f.S_chunks = const_cast<float*>(S_chunks);
   f.rec = wsb + wl.rec;
   f.B = d->B; f.T = d->T; f.H = d->H; f.R = d->R; f.RP = RP; f.L = d->L;
+  prof_mark(stream);
   st = launch_fwd_rec(f, d->dtype, d->Dk, lw, stream);
   if (st) return st;
+  prof_mark(stream);
   // 2. adjoint
   BwdArgs a;
   a.q = q; a.k = k; a.v = v; a.beta = beta; a.bx = bx; a.wx = wx;
@@ -213,18 +247,24 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
   a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = RP; a.L = d->L;
   st = launch_bwd(a, d->dtype, d->Dk, lw, stream);
   if (st) return st;
+  prof_mark(stream);
   // 3. dVb, dVw from dbx, dwx and tau
   st = launch_bwd_vparam(a, d->dtype, d->Dk, stream);
   if (st) return st;
+  prof_mark(stream);
   // 4. d[Ub; Uw] from the per-chunk dF
   st = launch_bwd_uparam(a, d->dtype, d->Dk, stream);
   if (st) return st;
+  prof_mark(stream);
   // 5. fixed-order reductions of the partials
   const int nbh = d->B * d->H;
   const size_t RD = (size_t)d->R * d->Dk;
   st = launch_param_reduce(a.part, nbh * kUSplit, RD, dUb, dUw, stream);
   if (st) return st;
-  return launch_param_reduce(a.partV, nbh * kVSplit, RD, dVb, dVw, stream);
+  prof_mark(stream);
+  st = launch_param_reduce(a.partV, nbh * kVSplit, RD, dVb, dVw, stream);
+  prof_mark(stream);
+  return st;
 }
 
 }  // extern "C"
