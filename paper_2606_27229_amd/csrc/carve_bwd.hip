@@ -135,20 +135,74 @@ carve_bwd_kernel(BwdArgs a) {
   f32x4 dF[NRT];                  // dF[r = 16 rt + 4 g + i][j = 16 w + c]
   for (int rt = 0; rt < NRT; ++rt) dF[rt] = zero4();
 
-  for (int ch = nch - 1; ch >= 0; --ch) {
-    const char* rc = recb + (size_t)ch * cr.total;
-    // F of the chunk -> LDS
-    {
-      const T* src = reinterpret_cast<const T*>(rc + cr.F);
-      for (int x = tid; x < R2 * D / VEC; x += NT) {
-        const int rr = x / (D / VEC), j = (x % (D / VEC)) * VEC;
-        *reinterpret_cast<u32x4*>(sF + rr * LDD + j) = *reinterpret_cast<const u32x4*>(src + rr * D + j);
-      }
+  // ---- prefetch registers: the next block to process (reverse order) and, at
+  // the last block of a chunk, the fold F of the next chunk.  Every block
+  // starts with one wait for all of this wave's memory operations, issued at
+  // least a block earlier.
+  constexpr int NTAU = 16 * R2 / VEC;   // 16-byte vectors of a block's tau
+  constexpr int NTV = (NTAU + NT - 1) / NT;
+  constexpr int NFV = (R2 * D / VEC + NT - 1) / NT;   // 16-byte vectors of F per thread
+  u32x4 ptau[NTV], pF[NFV];
+  quad ptm, ppm, psbq[NJT], ptq[NRB], pbx, pkq, pqq2, pwxq, pvq, pdOq;
+  f32x4 pgam, pg;
+  T pbeta = (T)0.0f;
+#define CARVE_BWD_LOAD(GB_)                                                                   \
+  do {                                                                                        \
+    const int ch_ = (GB_) / nbc, bc_ = (GB_) % nbc;                                           \
+    const char* rc_ = recb + (size_t)ch_ * cr.total;                                          \
+    const int tb_ = ch_ * L + 16 * bc_;                                                       \
+    const int e_ = (tb_ + c) * rs + 16 * w + 4 * g;                                           \
+    const T* tau_ = reinterpret_cast<const T*>(rc_ + cr.Tau) + 16 * bc_ * R2;                 \
+    for (int u_ = 0; u_ < NTV; ++u_) {                                                        \
+      const int x_ = tid + u_ * NT;                                                           \
+      if (x_ < NTAU) ptau[u_] = *reinterpret_cast<const u32x4*>(tau_ + x_ * VEC);             \
+    }                                                                                         \
+    if (tid < 64) {                                                                           \
+      ptm = Qd::ld(reinterpret_cast<const T*>(rc_ + cr.Tm) + bc_ * 256 + 4 * tid);            \
+      ppm = Qd::ld(reinterpret_cast<const T*>(rc_ + cr.P) + bc_ * 256 + 4 * tid);             \
+    }                                                                                         \
+    if (tid < D / 4) pgam = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(rc_ + cr.Gam) + bc_ * D + 4 * tid); \
+    if (tid < 16) pbeta = beta[(tb_ + tid) * H];                                              \
+    const T* sv_ = reinterpret_cast<const T*>(rc_ + cr.S) + (size_t)bc_ * NJT * NT * 4 + tid * 4; \
+    for (int jt_ = 0; jt_ < NJT; ++jt_) psbq[jt_] = Qd::ld(sv_ + (size_t)jt_ * NT * 4);        \
+    const T* tq_ = reinterpret_cast<const T*>(rc_ + cr.Tau) + (16 * bc_ + c) * R2 + 4 * g;    \
+    for (int ks_ = 0; ks_ < NRB; ++ks_) ptq[ks_] = Qd::ld(tq_ + 16 * ks_);                    \
+    pbx = Qd::ld(bx + e_);                                                                    \
+    pg = *reinterpret_cast<const f32x4*>(gl + e_);                                            \
+    pkq = Qd::ld(k + e_);                                                                     \
+    pqq2 = Qd::ld(q + e_);                                                                    \
+    pwxq = Qd::ld(wx + e_);                                                                   \
+    pvq = Qd::ld(v + e_);                                                                     \
+    pdOq = Qd::ld(dO + e_);                                                                   \
+  } while (0)
+#define CARVE_BWD_LOADF(CH_)                                                                  \
+  do {                                                                                        \
+    const T* src_ = reinterpret_cast<const T*>(recb + (size_t)(CH_) * cr.total + cr.F);       \
+    for (int u_ = 0; u_ < NFV; ++u_) {                                                        \
+      const int x_ = tid + u_ * NT;                                                           \
+      if (x_ < R2 * D / VEC) pF[u_] = *reinterpret_cast<const u32x4*>(src_ + x_ * VEC);       \
+    }                                                                                         \
+  } while (0)
+  // [Ub; Uw] operand quads of the glue, lane (g, c): U[16 rt + 4 g + e][16 w + c]
+  // (rows past R are zero), loaded once for the whole call
+  quad fU[NRT];
+  for (int rt = 0; rt < NRT; ++rt) {
+    const float* src = rt < RP / 16 ? a.Ub : a.Uw;
+    f32x4 tu;
+    for (int e = 0; e < 4; ++e) {
+      const int rl = 16 * (rt % (RP / 16)) + 4 * g + e;
+      tu[e] = rl < R ? src[rl * D + 16 * w + c] : 0.0f;
     }
-    // pending dq / dF update of the last processed block (its BQ step)
-    f32x4 pdqp = zero4();
-    quad pqq = Qd::cvt(zero4());
-    int pe0 = 0;
+    fU[rt] = Qd::cvt(tu);
+  }
+  const int ngb = nch * nbc;
+  CARVE_BWD_LOAD(ngb - 1);
+  CARVE_BWD_LOADF(nch - 1);
+
+  // pending dq / dF update of the last processed block (its BQ step)
+  f32x4 pdqp = zero4();
+  quad pqq = Qd::cvt(zero4());
+  int pe0 = 0;
 #define CARVE_BWD_BQ()                                                                        \
   do {                                                                                        \
     f32x4 acc_ = pdqp;                                                                        \
@@ -160,7 +214,10 @@ carve_bwd_kernel(BwdArgs a) {
     for (int rt = 0; rt < NRT; ++rt) dF[rt] = Qd::mma16(Qd::ld_tr(sdY, LDR, 0, 16 * rt, g, c), qT_, dF[rt]); \
   } while (0)
 #pragma unroll 1
-    for (int bc = nbc - 1; bc >= 0; --bc) {
+  for (int gb = ngb - 1; gb >= 0; --gb) {
+    const int ch = gb / nbc, bc = gb % nbc;
+    const char* rc = recb + (size_t)ch * cr.total;
+    {
       // opaque copies of the lane coordinates: values derived from them
       // (addresses, masks) are recomputed in every block instead of being
       // hoisted out of the loops and kept live (which would spill)
@@ -172,40 +229,35 @@ carve_bwd_kernel(BwdArgs a) {
       const int tb = ch * L + 16 * bc;   // first token of the block
       const int e0 = (tb + c) * rs + 16 * w + 4 * g;
 
-      // -- BK1 (a): this block's global data ---------------------------------------
-      constexpr int NTAU = 16 * R2 / VEC;   // 16-byte vectors of the block's tau
-      constexpr int NTV = (NTAU + NT - 1) / NT;
+      // -- BK1 (a): this block's data (prefetched a block ago) ------------------------
+      vm_wait_all();
       u32x4 ltau[NTV];
-      quad ltm, lpm;
-      f32x4 lgam;
-      T lbeta = (T)0.0f;
-      {
-        const T* tau = reinterpret_cast<const T*>(rc + cr.Tau) + 16 * bc * R2;
-        for (int u = 0; u < NTV; ++u) {
-          const int x = tid + u * NT;
-          if (x < NTAU) ltau[u] = *reinterpret_cast<const u32x4*>(tau + x * VEC);
-        }
-        if (tid < 64) {
-          ltm = Qd::ld(reinterpret_cast<const T*>(rc + cr.Tm) + bc * 256 + 4 * tid);
-          lpm = Qd::ld(reinterpret_cast<const T*>(rc + cr.P) + bc * 256 + 4 * tid);
-        }
-        if (tid < D / 4) lgam = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(rc + cr.Gam) + bc * D + 4 * tid);
-        if (tid < 16) lbeta = beta[(tb + tid) * H];
-      }
+      for (int u = 0; u < NTV; ++u) ltau[u] = ptau[u];
+      const quad ltm = ptm, lpm = ppm;
+      const f32x4 lgam = pgam;
+      const T lbeta = pbeta;
       quad sbq[NJT];   // block start state, wave layout: S[16 w + c][16 jt + 4 g + e]
-      {
-        const T* sv = reinterpret_cast<const T*>(rc + cr.S) + (size_t)bc * NJT * NT * 4 + tid * 4;
-        for (int jt = 0; jt < NJT; ++jt) sbq[jt] = Qd::ld(sv + (size_t)jt * NT * 4);
-      }
+      for (int jt = 0; jt < NJT; ++jt) sbq[jt] = psbq[jt];
       quad ltq[NRB];
-      {
-        const T* tq = reinterpret_cast<const T*>(rc + cr.Tau) + (16 * bc + c) * R2 + 4 * g;
-        for (int ks = 0; ks < NRB; ++ks) ltq[ks] = Qd::ld(tq + 16 * ks);
+      for (int ks = 0; ks < NRB; ++ks) ltq[ks] = ptq[ks];
+      const quad lbx = pbx;
+      const f32x4 lg = pg;
+      const quad kq = pkq, qq = pqq2;
+      const quad wxq = pwxq, vq = pvq, dOq = pdOq;
+      if (bc == nbc - 1) {
+        // first block of a chunk in reverse order: the chunk's F into LDS (the
+        // previous chunk's last read of sF was before its glue barriers)
+        for (int u = 0; u < NFV; ++u) {
+          const int x = tid + u * NT;
+          if (x < R2 * D / VEC) {
+            const int rr = x / (D / VEC), j = (x % (D / VEC)) * VEC;
+            *reinterpret_cast<u32x4*>(sF + rr * LDD + j) = pF[u];
+          }
+        }
       }
-      const quad lbx = Qd::ld(bx + e0);
-      const f32x4 lg = *reinterpret_cast<const f32x4*>(gl + e0);
-      const quad kq = Qd::ld(k + e0), qq = Qd::ld(q + e0);
-      const quad wxq = Qd::ld(wx + e0), vq = Qd::ld(v + e0), dOq = Qd::ld(dO + e0);
+      // prefetch the next block (and at a chunk's last block the next chunk's F)
+      CARVE_BWD_LOAD(gb > 0 ? gb - 1 : 0);
+      if (bc == 0) CARVE_BWD_LOADF(ch > 0 ? ch - 1 : 0);
 
       // -- BQ of the previous block (overlaps the loads above) -------------------
       if (bc < nbc - 1) CARVE_BWD_BQ();
@@ -452,6 +504,14 @@ carve_bwd_kernel(BwdArgs a) {
       pqq = qq;
       pe0 = e0;
     }
+    if (bc != 0) continue;
+    {
+    // opaque lane coordinates for the glue as well (its LDS addresses are
+    // recomputed here rather than held across the loop)
+    int tid_ = tid, g_ = g, c_ = c, w_ = w;
+    asm volatile("" : "+v"(tid_), "+v"(g_), "+v"(c_), "+v"(w_));
+    const int tid = tid_, g = g_, c = c_, w = w_;
+    (void)tid;
     CARVE_BWD_BQ();
 
     // ---- glue: dS += [Ub; Uw]^T dF; dF is parked in the chunk record for
@@ -461,29 +521,21 @@ carve_bwd_kernel(BwdArgs a) {
       T* sdFh = sdSx;               // [D][LDR]: dF[r][j] stored at (j, r)
       T* sdFl = sdSx + D * LDR;     // [D][LDR]: dF - (dF rounded)
       float* dFr = reinterpret_cast<float*>(const_cast<char*>(rc) + cr.dF);
-      // [Ub; Uw] operand quads, lane (g, c): U[16 rt + 4 g + e][16 w + c]; the
-      // opaque column keeps these loads inside the chunk loop (short live range)
-      // (rows past R are zero: clamped unconditional loads times a mask, so the
-      // sixteen loads are issued back to back and waited for once)
-      quad fU[NRT];
-      int col = 16 * w + c;
-      asm volatile("" : "+v"(col));
-      for (int rt = 0; rt < NRT; ++rt) {
-        const float* src = rt < RP / 16 ? a.Ub : a.Uw;
-        f32x4 tu;
-        for (int e = 0; e < 4; ++e) {
-          const int rl = 16 * (rt % (RP / 16)) + 4 * g + e;
-          const float x = src[(rl < R ? rl : R - 1) * D + col];
-          tu[e] = rl < R ? x : 0.0f;
-        }
-        fU[rt] = Qd::cvt(tu);
-      }
       __syncthreads();  // every wave is done with sdSx and sdY of the last block
       for (int rt = 0; rt < NRT; ++rt) {
         const quad hi = Qd::cvt(dF[rt]);
         Qd::st(sdFh + (16 * w + c) * LDR + 16 * rt + 4 * g, hi);
         Qd::st(sdFl + (16 * w + c) * LDR + 16 * rt + 4 * g, Qd::cvt(dF[rt] - Qd::f32(hi)));
-        for (int i = 0; i < 4; ++i) dFr[(16 * rt + 4 * g + i) * D + 16 * w + c] = dF[rt][i];
+        // dF parked as [r][j]: the tile is transposed on the matrix cores in f32
+        // (an exact product with the identity) so that a lane holds four
+        // consecutive j, one 16-byte store per tile
+        {
+          const float one = 1.0f, zero = 0.0f;
+          f32x4 tT = zero4();
+          for (int kk = 0; kk < 4; ++kk)
+            tT = __builtin_amdgcn_mfma_f32_16x16x4f32(dF[rt][kk], 4 * g + kk == c ? one : zero, tT, 0, 0, 0);
+          *reinterpret_cast<f32x4*>(dFr + (size_t)(16 * rt + c) * D + 16 * w + 4 * g) = tT;
+        }
         dF[rt] = zero4();
       }
       __syncthreads();
@@ -499,9 +551,12 @@ carve_bwd_kernel(BwdArgs a) {
       }
       __syncthreads();
     }
-  }  // chunks
+    }
+  }  // blocks (reverse)
 
 #undef CARVE_BWD_BQ
+#undef CARVE_BWD_LOAD
+#undef CARVE_BWD_LOADF
   if (a.dS0) {
     float* dst = a.dS0 + soff + (16 * w + c) * D + 4 * g;
     for (int jt = 0; jt < NJT; ++jt) *reinterpret_cast<f32x4*>(dst + 16 * jt) = dSt[jt];

@@ -85,3 +85,22 @@ def test_aliasing_output_rejected():
     args = ptrs[:12] + [ptrs[0]]  # o aliases q
     st = lib.carve_chunk_fwd(ctypes.byref(d), *args, None, None, None, 0, None)
     assert st == -3
+
+
+def test_profile_hook_validation():
+    """The measurement hook copies at most 16 handles and rejects bad arguments
+    without touching HIP; capacity 0 disarms it."""
+    lib = carve.load_library()
+    assert lib.carve_profile_events(None, 0) == 0
+    assert lib.carve_profile_events(None, 3) == -1
+    arr = (ctypes.c_void_p * 17)(*([4096] * 17))
+    assert lib.carve_profile_events(arr, -1) == -1
+    assert lib.carve_profile_events(arr, 17) == -3
+    # an armed hook is cleared by the next call even when that call fails in
+    # validation: after a rejected forward, nothing stays armed (the handles
+    # here are fake and would fault if ever recorded)
+    assert lib.carve_profile_events(arr, 2) == 0
+    d = _dims(T=100)
+    fake = ctypes.c_void_p(4096)
+    assert lib.carve_chunk_fwd(ctypes.byref(d), *([fake] * 12), fake, None, None, None, 0, None) == -2
+    assert lib.carve_profile_events(None, 0) == 0
