@@ -24,7 +24,7 @@ sys.path.insert(0, ROOT)
 METRIC = "layer fwd+bwd tokens/s, H=16 d=128 T=4096 L=64 bf16; % MFMA peak"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
-KERNEL_SOURCES = ("paper_2606_27229_amd/csrc/carve_fwd_chain.hip", "paper_2606_27229_amd/csrc/carve_fwd.hip",
+KERNEL_SOURCES = ("paper_2606_27229_amd/csrc/carve_fwd_chain.hip", "paper_2606_27229_amd/csrc/carve_rec.h",
                   "paper_2606_27229_amd/csrc/carve_bwd.hip", "paper_2606_27229_amd/csrc/carve_dev.h",
                   "paper_2606_27229_amd/csrc/carve_kernels.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer_1p3b_T4096_L64.json")
@@ -36,10 +36,11 @@ def algorithmic_counts(B, T, H, d, R, L):
     Bytes per token-head (bf16 token tensors, f32 g and states):
       forward kernel   reads q, k, v (3*2d) + g (4d) + bx, wx (2*2d) + beta (2);
                        writes o (2d) + chunk-start states (4 d^2 / L)
-      adjoint kernel   reads the forward inputs + dO (2d); writes dq, dk, dv
+      adjoint          reads the forward inputs + dO (2d); writes dq, dk, dv
                        (3*2d) + dg (4d) + dbx, dwx (2*2d) + dbeta (2)
-      whole backward   the adjoint's bytes + the chunk-start states it needs
-                       (4 d^2 / L, read by the recompute)
+      backward         the adjoint's bytes + the chunk-start states it needs
+                       (4 d^2 / L, read by the recompute); the fused
+                       recompute + adjoint kernel is priced at this figure
     Flops per token-head (multiply-add = 2): forward
       2 * (2 r d^2 / L + 3 d^2 + 4 r d + 5/2 L d + L^2 / 6), backward 2x forward.
     """
@@ -78,7 +79,7 @@ def load_traffic(kernel):
     return None if k is None else k.get("hbm_bytes_per_launch")
 
 
-TRAFFIC_KERNELS = {"carve_chain_fwd_kernel": "carve_chain_fwd_kernel", "carve_bwd_kernel": "16carve_bwd_kernel"}
+TRAFFIC_KERNELS = {"carve_chain_fwd_kernel": "carve_chain_fwd_kernel", "carve_bwd_fused_kernel": "carve_bwd_fused_kernel"}
 
 
 def _pmc_per_dispatch(run_dir, counter):
@@ -260,7 +261,7 @@ def main():
     def avg(rows, i):
         return sum(r[i].elapsed_time(r[i + 1]) for r in rows) / len(rows)
 
-    bwd_names = ["carve_fwd_kernel<recompute>", "carve_bwd_kernel", "carve_bwd_vparam_kernel",
+    bwd_names = ["carve_sync_clear_kernel", "carve_bwd_fused_kernel", "carve_bwd_vparam_kernel",
                  "carve_bwd_uparam_kernel", "carve_param_reduce_kernel[dU]", "carve_param_reduce_kernel[dV]"]
     kernels_ms = {"carve_chain_fwd_kernel": avg(ev_f, 0)}
     for i, name in enumerate(bwd_names):
@@ -270,7 +271,7 @@ def main():
     tokens = B * T
     cnt = algorithmic_counts(B, T, H, d, R, L)
 
-    alg = {"carve_chain_fwd_kernel": cnt["fwd_bytes"], "carve_bwd_kernel": cnt["adjoint_bytes"]}
+    alg = {"carve_chain_fwd_kernel": cnt["fwd_bytes"], "carve_bwd_fused_kernel": cnt["bwd_bytes"]}
     dominant = max(alg, key=lambda k_: kernels_ms[k_])
     dom_ms = kernels_ms[dominant]
     dom_bytes = alg[dominant]

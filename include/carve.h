@@ -88,8 +88,10 @@ enum {
 
 /* Bytes of device workspace the forward (for_backward = 0) or the backward
  * (for_backward = 1) needs for these dims; 0 means none.  Returns 0 for
- * dims that fail validation.  The workspace holds per-(batch, head) partial
- * parameter gradients and the WY-tile start states of one chunk. */
+ * dims that fail validation.  The workspace holds the per-chunk records of
+ * the recompute (fold, tau, WY factors and block start states), the partial
+ * parameter gradients and the chunk ready flags of the fused recompute +
+ * adjoint launch. */
 size_t carve_workspace_size(const carve_dims_t* d, int for_backward);
 
 /* Forward (Alg. carve_fwd with the WY solve of Alg. WYChunkDelta).
@@ -125,8 +127,9 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
 /* Measurement hook (not part of the computation).  Arms the next
  * carve_chunk_fwd / carve_chunk_bwd call made on the calling thread to record
  * events[0] on its stream before its first kernel launch and events[i] after
- * its i-th launch (the forward makes 1 launch; the backward 6: recompute,
- * adjoint, dVb/dVw partials, d[Ub;Uw] partials, two fixed-order reductions),
+ * its i-th launch (the forward makes 1 launch; the backward 6: clear of the
+ * chunk ready flags, chunk recompute fused with the adjoint, dVb/dVw
+ * partials, d[Ub;Uw] partials, two fixed-order reductions),
  * up to `capacity` events.  `events` are hipEvent_t handles created by the
  * caller (hipEventCreate) and owned by the caller; the handles are copied
  * here (the array may be freed after this call) and the events are only

@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libcarve.so")
-SOURCES = ["carve_abi.hip", "carve_fwd_chain.hip", "carve_fwd.hip", "carve_bwd.hip"]
+SOURCES = ["carve_abi.hip", "carve_fwd_chain.hip", "carve_bwd.hip"]
 
 BUILD = os.path.join(HERE, "_build")
 HIPCC_FLAGS = [

@@ -15,9 +15,10 @@ int round_rp(int R) { return (R + 31) / 32 * 32; }
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // backward workspace: d[Ub; Uw] partials per (b,h, chunk split) | dVb, dVw
-// partials per (b,h, token split) | chunk records of the recompute
+// partials per (b,h, token split) | chunk records of the recompute | ready
+// flags and ticket counter of the fused recompute + adjoint launch
 struct BwdWs {
-  size_t part, partV, rec, total;
+  size_t part, partV, rec, sync, total;
 };
 
 BwdWs bwd_workspace_layout(const carve_dims_t* d) {
@@ -29,6 +30,7 @@ BwdWs bwd_workspace_layout(const carve_dims_t* d) {
   l.part = off;  off += align256(nbh * kUSplit * part_floats(d->R, d->Dk) * 4);
   l.partV = off; off += align256(nbh * kVSplit * part_floats(d->R, d->Dk) * 4);
   l.rec = off;   off += align256(nbh * nch * chunk_rec(es, d->Dk, d->L, round_rp(d->R)).total);
+  l.sync = off;  off += align256(sync_ints(nbh, nch) * sizeof(int));
   l.total = off;
   return l;
 }
@@ -52,16 +54,24 @@ int check_dims(const carve_dims_t* d) {
   return CARVE_OK;
 }
 
-// largest forward sub-chunk (<= 64 tokens, dividing L) whose LDS layout fits;
-// for the backward also the adjoint kernel's layout must fit
-int pick_lw(const carve_dims_t* d, bool bwd) {
+// largest recompute sub-chunk (<= 64 tokens, dividing L) for which the LDS
+// layout of the fused recompute + adjoint launch fits
+int pick_lw(const carve_dims_t* d) {
   const int RP = round_rp(d->R);
-  if (bwd && bwd_lds_bytes(d->dtype, d->Dk, 16, RP) > kMaxLds) return 0;
   for (int lw = 64; lw >= 16; lw /= 2) {
     if (lw > d->L || d->L % lw) continue;
-    if (fwd_lds_bytes(d->dtype, d->Dk, lw, RP) <= kMaxLds) return lw;
+    if (bwd_lds_bytes(d->dtype, d->Dk, lw, RP) <= kMaxLds) return lw;
   }
   return 0;
+}
+
+// compute units of the current device (the fused backward sizes its grid by it)
+int device_cus(int* cus) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return CARVE_ERR_HIP;
+  if (hipDeviceGetAttribute(cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return CARVE_ERR_HIP;
+  if (*cus < 1) *cus = 1;
+  return CARVE_OK;
 }
 
 // largest WY block (<= 64 tokens, dividing L) whose chain-forward LDS layout fits
@@ -144,7 +154,7 @@ int carve_profile_events(hipEvent_t* events, int capacity) {
 size_t carve_workspace_size(const carve_dims_t* d, int for_backward) {
   if (check_dims(d) != CARVE_OK) return 0;
   if (!for_backward) return 0;
-  if (!pick_lw(d, true)) return 0;
+  if (!pick_lw(d)) return 0;
   return bwd_workspace_layout(d).total;
 }
 
@@ -219,23 +229,21 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
                         {dwx, ntok * d->Dv * es}, {dUb, RDv}, {dUw, RDv}, {dVb, RDv},
                         {dVw, RDv}, {dS0, nst * 4}};
   if (any_overlap(outs, 12, ins, 15)) return CARVE_ERR_UNSUPPORTED;
-  const int lw = pick_lw(d, true);
+  const int lw = pick_lw(d);
   if (!lw) return CARVE_ERR_UNSUPPORTED;
+  int cus = 0;
+  st = device_cus(&cus);
+  if (st) return st;
   const BwdWs wl = bwd_workspace_layout(d);
   char* wsb = reinterpret_cast<char*>(workspace);
   const int RP = round_rp(d->R);
-  // 1. chunk-parallel recompute -> chunk records
+  // 1-2. chunk-parallel recompute -> chunk records, overlapped with the adjoint
   FwdArgs f;
   f.q = q; f.k = k; f.v = v; f.beta = beta; f.bx = bx; f.wx = wx;
   f.g = g; f.Ub = Ub; f.Uw = Uw; f.Vb = Vb; f.Vw = Vw; f.S0 = nullptr;
   f.o = nullptr; f.S_T = nullptr; f.S_chunks = const_cast<float*>(S_chunks);
   f.rec = wsb + wl.rec;
   f.B = d->B; f.T = d->T; f.H = d->H; f.R = d->R; f.RP = RP; f.L = d->L;
-  prof_mark(stream);
-  st = launch_fwd_rec(f, d->dtype, d->Dk, lw, stream);
-  if (st) return st;
-  prof_mark(stream);
-  // 2. adjoint
   BwdArgs a;
   a.q = q; a.k = k; a.v = v; a.beta = beta; a.bx = bx; a.wx = wx;
   a.g = g; a.Ub = Ub; a.Uw = Uw; a.Vb = Vb; a.Vw = Vw; a.S_chunks = S_chunks;
@@ -245,7 +253,12 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
   a.partV = reinterpret_cast<float*>(wsb + wl.partV);
   a.rec = wsb + wl.rec;
   a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = RP; a.L = d->L;
-  st = launch_bwd(a, d->dtype, d->Dk, lw, stream);
+  int* sync = reinterpret_cast<int*>(wsb + wl.sync);
+  prof_mark(stream);
+  st = launch_sync_clear(sync, sync_ints((size_t)d->B * d->H, (size_t)(d->T / d->L)), stream);
+  if (st) return st;
+  prof_mark(stream);
+  st = launch_bwd_fused(f, a, sync, cus, d->dtype, d->Dk, lw, stream);
   if (st) return st;
   prof_mark(stream);
   // 3. dVb, dVw from dbx, dwx and tau

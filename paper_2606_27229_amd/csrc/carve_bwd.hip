@@ -1,12 +1,17 @@
 // carve_bwd.hip -- chunked CARVE backward on gfx950 (App. Alg. backward).
 //
 // The backward runs as a sequence of launches on one stream:
-//   1. the forward kernel in recompute mode (carve_fwd.hip), one workgroup per
-//      (batch, head, chunk): starting from S_chunks it recomputes every chunk
-//      independently and writes a chunk record (F, tau, T and P of every
-//      16-token block, the block retentions and the block start states);
-//   2. carve_bwd_kernel below: one workgroup per (batch, head) walks the chunks
-//      and their 16-token blocks in reverse and carries the state gradient;
+//   1. carve_sync_clear_kernel: zeroes the chunk ready flags and the ticket
+//      counter of step 2 (a fill kernel, so the sequence may be graph-captured);
+//   2. carve_bwd_fused_kernel: two kinds of workgroup in one grid.
+//      Recompute workgroups (rec_chunk, carve_rec.h) recompute chunks
+//      independently from S_chunks, latest chunks first, and write a chunk
+//      record each (F, tau, T and P of every 16-token block, the block
+//      retentions and the block start states), then raise that chunk's ready
+//      flag.  Adjoint workgroups (bwd_adjoint below), one per (batch, head),
+//      walk the chunks and their 16-token blocks in reverse, carry the state
+//      gradient and wait for a chunk's flag before reading its record, so the
+//      recompute runs on the compute units the adjoint leaves idle, ahead of it;
 //   3. carve_bwd_vparam_kernel: dVb, dVw from dbx, dwx and tau, split over
 //      tokens;
 //   4. carve_bwd_uparam_kernel: d[Ub; Uw] from the per-chunk dF (parked in the
@@ -35,19 +40,54 @@
 //   dtau = [dz_b Vb, dz_w Vw],  dY = dtau (1 - tau^2),  dF += dY^T q
 // and at the chunk start the folded read-out closes the chain ("glue"):
 //   dS += [Ub; Uw]^T dF,   d[Ub; Uw] += dF S_hat^T.
-#include "carve_kernels.h"
+#include "carve_rec.h"
 
 namespace carve {
+
+// Bound of the ready-flag wait: 2^20 polls (each a few device-scope loads and a
+// short sleep; about a second in all).  A chunk is recomputed in tens of
+// microseconds by a workgroup that never waits, so the bound is not reached in
+// a correct launch; if it is, the waiting wave poisons its state gradient with
+// NaN (every gradient of earlier tokens then comes out NaN) and waits no more.
+constexpr int kReadySpinLimit = 1 << 20;
+// chunks whose flags one wait inspects (need, need - 1, ...)
+constexpr int kReadyWindow = 8;
+
+// Wait until chunk `need`'s flag is raised (flags are raised with release
+// stores at agent scope) and return the lowest chunk lo such that the flags of
+// chunks lo .. need, within a window of kReadyWindow chunks, were all seen
+// raised; one acquire fence then covers all of them, so a wave pays for one
+// cache invalidation per window instead of one per chunk.  Every lane reads
+// every flag itself.  Returns need + 1 if the bound ran out.
+__device__ __forceinline__ int acquire_ready(const int* rdy, const int need) {
+  for (int n = 0; n < kReadySpinLimit; ++n) {
+    int f[kReadyWindow];
+#pragma unroll
+    for (int i = 0; i < kReadyWindow; ++i)
+      f[i] = need - i >= 0 ? __hip_atomic_load(rdy + need - i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+    if (f[0] != 0) {
+      int lo = need;
+#pragma unroll
+      for (int i = 1; i < kReadyWindow; ++i) {
+        if (f[i] == 0) break;
+        lo = need - i;
+      }
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      return lo;
+    }
+    __builtin_amdgcn_s_sleep(2);
+  }
+  return need + 1;
+}
 
 // Compiler-only fence: keeps the LDS loads of one loop iteration from being
 // hoisted above the previous one (bounds the number of live operand registers).
 #define CARVE_SEQ() asm volatile("" ::: "memory")
 
-// one workgroup per CU (its LDS layout), so two waves per SIMD: the full
-// register file of a wave is available
+// Adjoint of (batch, head) bh.  ready[bh * nch + ch] is raised when chunk ch's
+// record is complete; smem is the workgroup's dynamic LDS (BwdLds layout).
 template <typename T, int D, int RP>
-__global__ void __launch_bounds__(bwd_threads(D)) __attribute__((amdgpu_waves_per_eu(1, 2)))
-carve_bwd_kernel(BwdArgs a) {
+__device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char* smem, const int* ready) {
   typedef Quad<T> Qd;
   typedef typename Qd::q quad;
   typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
@@ -65,10 +105,9 @@ carve_bwd_kernel(BwdArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
   const int H = a.H, Tn = a.T, L = a.L, R = a.R;
-  const int bh = blockIdx.x, b = bh / H, h = bh % H;
+  const int b = bh / H, h = bh % H;
   const int nch = Tn / L, nbc = L / 16;
 
-  extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr BwdLds lay = bwd_lds<T, D, RP>();
   T* sF = reinterpret_cast<T*>(smem + lay.F);        // [2RP][LDD]   F of the chunk
   T* sVbT = reinterpret_cast<T*>(smem + lay.VbT);    // [RP][LDD]    Vb^T
@@ -196,6 +235,24 @@ carve_bwd_kernel(BwdArgs a) {
     fU[rt] = Qd::cvt(tu);
   }
   const int ngb = nch * nbc;
+  const int* rdy = ready + (size_t)bh * nch;
+  // chunks >= acq_lo have been acquired by this wave; acq_lo = -1 after a wait
+  // ran out of its bound (never in a correct launch)
+  int acq_lo = nch;
+#define CARVE_BWD_READY(CH_)                                                                  \
+  do {                                                                                        \
+    if ((CH_) < acq_lo) {                                                                     \
+      const int lo_ = acquire_ready(rdy, (CH_));                                              \
+      if (lo_ > (CH_)) {                                                                      \
+        acq_lo = -1;                                                                          \
+        for (int jt_ = 0; jt_ < NJT; ++jt_) dSt[jt_] = f32x4{__builtin_nanf(""), __builtin_nanf(""), \
+                                                             __builtin_nanf(""), __builtin_nanf("")}; \
+      } else {                                                                                \
+        acq_lo = lo_;                                                                         \
+      }                                                                                       \
+    }                                                                                         \
+  } while (0)
+  CARVE_BWD_READY(nch - 1);
   CARVE_BWD_LOAD(ngb - 1);
   CARVE_BWD_LOADF(nch - 1);
 
@@ -255,7 +312,9 @@ carve_bwd_kernel(BwdArgs a) {
           }
         }
       }
-      // prefetch the next block (and at a chunk's last block the next chunk's F)
+      // prefetch the next block (and at a chunk's last block the next chunk's
+      // F, once the recompute has published that chunk's record)
+      if (bc == 0 && ch > 0) CARVE_BWD_READY(ch - 1);
       CARVE_BWD_LOAD(gb > 0 ? gb - 1 : 0);
       if (bc == 0) CARVE_BWD_LOADF(ch > 0 ? ch - 1 : 0);
 
@@ -555,6 +614,7 @@ carve_bwd_kernel(BwdArgs a) {
   }  // blocks (reverse)
 
 #undef CARVE_BWD_BQ
+#undef CARVE_BWD_READY
 #undef CARVE_BWD_LOAD
 #undef CARVE_BWD_LOADF
   if (a.dS0) {
@@ -706,61 +766,142 @@ __global__ void __launch_bounds__(256) carve_param_reduce_kernel(const float* __
   }
 }
 
+// Zero the synchronisation area of the fused launch (ready flags, ticket).
+__global__ void __launch_bounds__(256) carve_sync_clear_kernel(int* __restrict__ sync, int n) {
+  const int x = blockIdx.x * 256 + threadIdx.x;
+  if (x < n) sync[x] = 0;
+}
+
+// Chunk recompute and adjoint in one grid of nrec + B*H workgroups.  Roles go
+// by arrival: each workgroup draws a ticket from the counter in sync; the first
+// nrec tickets recompute, the rest run the adjoint of (batch, head) ticket -
+// nrec.  A workgroup with a recompute ticket is already running and never
+// waits, so every flag an adjoint workgroup waits for is raised in finite time
+// whatever order the hardware dispatches the grid in.  Recompute items are
+// taken latest chunk first (the order in which the adjoint needs them): item
+// i is chunk nch - 1 - i / (B*H) of (batch, head) i % (B*H).
+template <typename T, int D, int LW, int RP>
+__global__ void __launch_bounds__(bwd_threads(D)) __attribute__((amdgpu_waves_per_eu(1, 2)))
+carve_bwd_fused_kernel(FwdArgs f, BwdArgs a, int nrec, int* sync) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int nbh = a.B * a.H, nch = a.T / a.L;
+  const int nitems = nbh * nch;
+  int* ready = sync;
+  if (threadIdx.x == 0)
+    reinterpret_cast<int*>(smem)[0] =
+        __hip_atomic_fetch_add(sync + nitems, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  const int ticket = __builtin_amdgcn_readfirstlane(reinterpret_cast<const int*>(smem)[0]);
+  __syncthreads();
+  if (ticket < nrec) {
+    for (int item = ticket; item < nitems; item += nrec) {
+      const int ch = nch - 1 - item / nbh, bh = item % nbh;
+      rec_chunk<T, D, LW, RP>(f, bh, ch, smem);
+      // every wave's record stores are complete before the barrier; the
+      // release store (agent scope) then writes them back for other XCDs
+      vm_wait_all();
+      __syncthreads();
+      if (threadIdx.x == 0)
+        __hip_atomic_store(ready + (size_t)bh * nch + ch, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  } else {
+    bwd_adjoint<T, D, RP>(a, ticket - nrec, smem, ready);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // host-side launch
 // ---------------------------------------------------------------------------
-template <typename T, int D, int RP>
-static int launch_bwd_t(const BwdArgs& a, hipStream_t stream) {
-  constexpr BwdLds lay = bwd_lds<T, D, RP>();
-  auto kern = carve_bwd_kernel<T, D, RP>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lay.total) != hipSuccess)
-      return CARVE_ERR_HIP;
-    attr_set = true;
+template <typename T, int D, int LW, int RP>
+__host__ __device__ constexpr size_t fused_lds() {
+  return lds_max(rec_lds<T, D, LW, RP>().total, bwd_lds<T, D, RP>().total);
+}
+
+template <typename T, int D, int LW, int RP>
+static int launch_fused_t(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, hipStream_t stream) {
+  constexpr size_t lds = fused_lds<T, D, LW, RP>();
+  if constexpr (lds > kMaxLdsBytes) {
+    return CARVE_ERR_UNSUPPORTED;
+  } else {
+    auto kern = carve_bwd_fused_kernel<T, D, LW, RP>;
+    static bool attr_set = false;  // per instantiation
+    if (!attr_set) {
+      if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)lds) != hipSuccess)
+        return CARVE_ERR_HIP;
+      attr_set = true;
+    }
+    // the adjoint workgroups take B*H compute units (one workgroup per CU: the
+    // LDS layout); the recompute gets the rest, or the whole device first when
+    // fewer than a quarter would remain
+    const int nbh = a.B * a.H;
+    const long long nitems = (long long)nbh * (a.T / a.L);
+    long long nrec = cus - nbh;
+    if (nrec < cus / 4) nrec = cus;
+    if (nrec > nitems) nrec = nitems;
+    if (nrec < 1) nrec = 1;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(nrec + nbh)), dim3(bwd_threads(D)), lds, stream, f, a, (int)nrec, sync);
+    return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
   }
-  hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(bwd_threads(D)), lay.total, stream, a);
-  return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
+}
+
+template <typename T, int D, int RP>
+static int launch_fused_l(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, int LW, hipStream_t s) {
+  if (LW == 16) return launch_fused_t<T, D, 16, RP>(f, a, sync, cus, s);
+  if (LW == 32) return launch_fused_t<T, D, 32, RP>(f, a, sync, cus, s);
+  if (LW == 64) return launch_fused_t<T, D, 64, RP>(f, a, sync, cus, s);
+  return CARVE_ERR_UNSUPPORTED;
 }
 
 template <typename T>
-static int launch_bwd_d(const BwdArgs& a, int D, hipStream_t s) {
+static int launch_fused_d(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, int D, int LW, hipStream_t s) {
   if (a.RP == 32) {
-    if (D == 32) return launch_bwd_t<T, 32, 32>(a, s);
-    if (D == 64) return launch_bwd_t<T, 64, 32>(a, s);
-    if (D == 128) return launch_bwd_t<T, 128, 32>(a, s);
+    if (D == 32) return launch_fused_l<T, 32, 32>(f, a, sync, cus, LW, s);
+    if (D == 64) return launch_fused_l<T, 64, 32>(f, a, sync, cus, LW, s);
+    if (D == 128) return launch_fused_l<T, 128, 32>(f, a, sync, cus, LW, s);
   } else if (a.RP == 64) {
-    if (D == 32) return launch_bwd_t<T, 32, 64>(a, s);
-    if (D == 64) return launch_bwd_t<T, 64, 64>(a, s);
-    if (D == 128) return launch_bwd_t<T, 128, 64>(a, s);
+    if (D == 32) return launch_fused_l<T, 32, 64>(f, a, sync, cus, LW, s);
+    if (D == 64) return launch_fused_l<T, 64, 64>(f, a, sync, cus, LW, s);
+    if (D == 128) return launch_fused_l<T, 128, 64>(f, a, sync, cus, LW, s);
   }
   return CARVE_ERR_UNSUPPORTED;
 }
 
-int launch_bwd(const BwdArgs& a, int dtype, int D, int LW, hipStream_t s) {
-  (void)LW;
-  if (dtype == CARVE_BF16) return launch_bwd_d<bf16_t>(a, D, s);
-  return launch_bwd_d<float>(a, D, s);
+int launch_sync_clear(int* sync, size_t n, hipStream_t s) {
+  hipLaunchKernelGGL(carve_sync_clear_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, sync, (int)n);
+  return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
+}
+
+int launch_bwd_fused(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, int dtype, int D, int LW,
+                     hipStream_t s) {
+  if (dtype == CARVE_BF16) return launch_fused_d<bf16_t>(f, a, sync, cus, D, LW, s);
+  return launch_fused_d<float>(f, a, sync, cus, D, LW, s);
+}
+
+template <typename T, int D, int RP>
+static size_t fused_lds_l(int LW) {
+  if (LW == 16) return fused_lds<T, D, 16, RP>();
+  if (LW == 32) return fused_lds<T, D, 32, RP>();
+  if (LW == 64) return fused_lds<T, D, 64, RP>();
+  return (size_t)-1;
 }
 
 template <typename T>
-static size_t bwd_lds_d(int D, int RP) {
+static size_t fused_lds_d(int D, int LW, int RP) {
   if (RP == 32) {
-    if (D == 32) return bwd_lds<T, 32, 32>().total;
-    if (D == 64) return bwd_lds<T, 64, 32>().total;
-    if (D == 128) return bwd_lds<T, 128, 32>().total;
+    if (D == 32) return fused_lds_l<T, 32, 32>(LW);
+    if (D == 64) return fused_lds_l<T, 64, 32>(LW);
+    if (D == 128) return fused_lds_l<T, 128, 32>(LW);
   } else if (RP == 64) {
-    if (D == 32) return bwd_lds<T, 32, 64>().total;
-    if (D == 64) return bwd_lds<T, 64, 64>().total;
-    if (D == 128) return bwd_lds<T, 128, 64>().total;
+    if (D == 32) return fused_lds_l<T, 32, 64>(LW);
+    if (D == 64) return fused_lds_l<T, 64, 64>(LW);
+    if (D == 128) return fused_lds_l<T, 128, 64>(LW);
   }
   return (size_t)-1;
 }
 
 size_t bwd_lds_bytes(int dtype, int D, int LW, int RP) {
-  (void)LW;
-  return dtype == CARVE_BF16 ? bwd_lds_d<bf16_t>(D, RP) : bwd_lds_d<float>(D, RP);
+  return dtype == CARVE_BF16 ? fused_lds_d<bf16_t>(D, LW, RP) : fused_lds_d<float>(D, LW, RP);
 }
 
 template <typename T, int D, int RP>

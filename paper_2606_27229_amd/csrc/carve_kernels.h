@@ -64,16 +64,16 @@ __host__ __device__ constexpr int lk_of() {
   return (sizeof(T) == 2 && LW < 32) ? 32 : LW;
 }
 
-// Forward LDS layout for one sub-chunk of LW tokens (NB = LW / 16 blocks).
-// Every row is padded by 16 bytes.  Region X holds the bf16 copy of the chunk
-// start state while the fold runs and the per-token key-side operands after.
-struct FwdLds {
-  size_t U, Q, F, Tau, Beta, X, S, Kt, Qt, Ki, Gam, AT, Tm, P, total;
+// LDS layout of the chunk recompute for one sub-chunk of LW tokens (NB = LW / 16
+// blocks).  Every row is padded by 16 bytes.  Region X holds the copy of the
+// chunk start state while the fold runs and the per-token key-side operands after.
+struct RecLds {
+  size_t U, Q, F, Tau, Beta, X, S, Kt, Qt, Ki, Gam, AT, Tm, total;
 };
 
 template <typename T, int D, int LW, int RP>
-__host__ __device__ constexpr FwdLds fwd_lds() {
-  FwdLds l{};
+__host__ __device__ constexpr RecLds rec_lds() {
+  RecLds l{};
   const size_t e = sizeof(T);
   constexpr size_t NB = LW / 16;
   constexpr size_t PAD = 16 / sizeof(T);
@@ -92,7 +92,6 @@ __host__ __device__ constexpr FwdLds fwd_lds() {
   l.Gam = off + x; x += lds_round(NB * D * 4);
   l.AT = off + x;  x += lds_round(NB * 16 * 20 * 4);
   l.Tm = off + x;  x += lds_round(NB * 16 * LDB * e);
-  l.P = off + x;   x += lds_round(NB * 16 * LDB * e);
   l.S = off;
   x = lds_max(x, lds_round(D * LDD * e));
   off += x;
@@ -139,10 +138,6 @@ __host__ __device__ constexpr ChainLds chain_lds() {
 int launch_chain_fwd(const FwdArgs& a, int dtype, int D, int WB, hipStream_t s);
 size_t chain_lds_bytes(int dtype, int D, int WB, int RP);
 
-int launch_fwd(const FwdArgs& a, int dtype, int D, int LW, hipStream_t s);
-// chunk-parallel forward recompute that writes the chunk records (a.rec)
-int launch_fwd_rec(const FwdArgs& a, int dtype, int D, int LW, hipStream_t s);
-size_t fwd_lds_bytes(int dtype, int D, int LW, int RP);
 
 // ---- backward -----------------------------------------------------------------
 struct BwdArgs {
@@ -202,8 +197,18 @@ __host__ __device__ constexpr BwdLds bwd_lds() {
   return l;
 }
 
-int launch_bwd(const BwdArgs& a, int dtype, int D, int LW, hipStream_t s);
+// Chunk recompute and adjoint in one launch (see carve_bwd.hip).  f carries the
+// forward inputs, S_chunks and the chunk records (f.rec == a.rec); sync points
+// at sync_ints(B * H, T / L) ints of workspace, zeroed by launch_sync_clear
+// on the same stream before; cus is the device's compute-unit count.
+int launch_bwd_fused(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, int dtype, int D, int LW,
+                     hipStream_t s);
+int launch_sync_clear(int* sync, size_t n, hipStream_t s);
+// LDS bytes of the fused launch with LW-token recompute sub-chunks
 size_t bwd_lds_bytes(int dtype, int D, int LW, int RP);
+// ints of the synchronisation area: one ready flag per chunk, the ticket
+// counter that assigns the workgroup roles, padding
+__host__ __device__ constexpr size_t sync_ints(size_t nbh, size_t nch) { return nbh * nch + 4; }
 int launch_bwd_vparam(const BwdArgs& a, int dtype, int D, hipStream_t s);
 int launch_bwd_uparam(const BwdArgs& a, int dtype, int D, hipStream_t s);
 // sum nparts records of 2 * half floats into dst0 (first half) and dst1

@@ -1,0 +1,345 @@
+// carve_rec.h -- chunk recompute of the CARVE backward on gfx950.
+//
+// rec_chunk() recomputes one gate chunk of one (batch, head) from its start
+// state (S_chunks, written by the forward) and writes the chunk record that the
+// adjoint reads (ChunkRec): the fold F, tau, and T, P, the retention and the
+// start state of every 16-token WY block.  Every chunk is independent, so the
+// recompute is chunk-parallel.  Wave w of the workgroup owns the 16-wide tile w
+// of the value axis and the 16-wide tile w of the key axis:
+//   * the state lives in registers as S^T tiles (rows = key index j, columns =
+//     the wave's 16 value rows v), in the matrix-core result layout;
+//   * everything on the value side (predictions, WY solve, state update) is
+//     wave-local, so the token-serial part of a sub-chunk runs without barriers;
+//   * the key-side gate arithmetic (erase gate, log retention, its prefix sums
+//     and the decayed keys/queries) runs on the wave's key tile.
+//
+// Per gate chunk with start state S_hat (Eq. content_readout):
+//   F = [Ub; Uw] S_hat                         (fold, once per chunk)
+//   tau = tanh(q F^T), z_b = bx + tau_b Vb^T, z_w = wx + tau_w Vw^T
+//   l = g - softplus(z_b) = log(exp(g) (1 - b)), w = sigmoid(z_w)
+// and then, for consecutive 16-token blocks (the WY form of Sec. 6.2 applied
+// block by block; every block of the chunk uses the same F), with lam = prefix
+// sums of l inside the block (lam_{-1} = 0), state S at the block start and u
+// the WY "pseudo values":
+//   Kt_t = k_t e^{lam_{t-1}},  Ki_s = k_s e^{-lam_s},  Qt_t = q_t e^{lam_t}
+//   A_ts = beta_t Kt_t . Ki_s (s < t),  P_ts = Qt_t . Ki_s (s <= t)
+//   T = (I + A)^{-1},  R_t = beta_t (w_t * v_t - S Kt_t),  u = T R
+//   S <- (S + sum_s u_s Ki_s^T) diag(e^{lam_15})
+// which is the recurrence of Eq. carve_state rewritten exactly.  A 16-token
+// block keeps every factor within e^{-(16-token log retention)}.
+//
+// Precondition (not checked): within any 16-token block the log retention
+// summed over the block stays above about -80 per key channel, so that
+// e^{-(block log retention)} is finite in f32.
+#pragma once
+#include "carve_kernels.h"
+
+namespace carve {
+
+// One chunk ch0 of (batch, head) bh; LW-token sub-chunks (LW | L).  smem is the
+// workgroup's dynamic LDS (RecLds layout).  Ends with a workgroup barrier, so
+// the caller may reuse the LDS at once; the record stores may still be in
+// flight.
+template <typename T, int D, int LW, int RP>
+__device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const int ch0, char* smem) {
+  typedef Quad<T> Qd;
+  typedef typename Qd::q quad;
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  constexpr int NT = fwd_threads(D);
+  constexpr int NW = NT / 64;          // waves == 16-wide tiles of the key / value axis
+  constexpr int NJT = D / 16;
+  constexpr int NB = LW / 16;          // 16-token blocks per sub-chunk
+  constexpr int R2 = 2 * RP;
+  constexpr int NRT = R2 / 16;         // 16-row tiles of [Ub; Uw] and of F
+  constexpr int PAD = 16 / sizeof(T);
+  constexpr int LDD = D + PAD, LDR = R2 + PAD, LDB = 16 + PAD;
+  constexpr int VEC = 16 / sizeof(T);          // token elements per 16-byte vector
+  constexpr int NVQ = LW * D / VEC;            // 16-byte vectors of a q tile
+  constexpr int NQV = (NVQ + NT - 1) / NT;     // per thread
+  static_assert(NW == NJT, "one wave per 16-wide tile");
+  static_assert(D % 32 == 0, "K32 steps over the key / value axis");
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int g = lane >> 4, c = lane & 15;
+  const int H = a.H, Tn = a.T, L = a.L, R = a.R;
+  const int nch = Tn / L, msub = L / LW;
+  const int b = bh / H, h = bh % H;
+
+  constexpr RecLds lay = rec_lds<T, D, LW, RP>();
+  T* sU = reinterpret_cast<T*>(smem + lay.U);      // [2RP][LDD]  [Ub; 0; Uw; 0]
+  T* sQ = reinterpret_cast<T*>(smem + lay.Q);      // [LW][LDD]   raw q
+  T* sF = reinterpret_cast<T*>(smem + lay.F);      // [2RP][LDD]  F
+  T* sTau = reinterpret_cast<T*>(smem + lay.Tau);  // [LW][LDR]   tau (b half | w half)
+  float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);
+  T* sS = reinterpret_cast<T*>(smem + lay.S);      // [D][LDD]    S_hat[v][j] (chunk start)
+  T* sKt = reinterpret_cast<T*>(smem + lay.Kt);    // [LW][LDD]
+  T* sQt = reinterpret_cast<T*>(smem + lay.Qt);    // [LW][LDD]
+  T* sKi = reinterpret_cast<T*>(smem + lay.Ki);    // [LW][LDD]
+  float* sGam = reinterpret_cast<float*>(smem + lay.Gam);  // [NB][D]     e^{lam_15}
+  float* sAT = reinterpret_cast<float*>(smem + lay.AT);    // [NB][16][20] A^T per block
+  T* sTm = reinterpret_cast<T*>(smem + lay.Tm);            // [NB][16][LDB] T per block
+
+  // token tensors addressed from this (batch, head)'s first element with 32-bit
+  // offsets t * rs + column (rs = H * D elements between consecutive tokens)
+  const size_t bh0 = ((size_t)b * Tn * H + h) * D;
+  const size_t bh1 = (size_t)b * Tn * H + h;
+  const int rs = H * D;
+  const T* __restrict__ q = reinterpret_cast<const T*>(a.q) + bh0;
+  const T* __restrict__ k = reinterpret_cast<const T*>(a.k) + bh0;
+  const T* __restrict__ v = reinterpret_cast<const T*>(a.v) + bh0;
+  const T* __restrict__ bx = reinterpret_cast<const T*>(a.bx) + bh0;
+  const T* __restrict__ wx = reinterpret_cast<const T*>(a.wx) + bh0;
+  const T* __restrict__ beta = reinterpret_cast<const T*>(a.beta) + bh1;
+  const float* __restrict__ gl = a.g + bh0;
+
+  // ---- shared parameters ------------------------------------------------------
+  for (int x = tid; x < R2 * D; x += NT) {
+    const int rr = x / D, i = x % D;
+    float u = 0.0f;
+    if (rr < R) u = a.Ub[rr * D + i];
+    else if (rr >= RP && rr < RP + R) u = a.Uw[(rr - RP) * D + i];
+    sU[rr * LDD + i] = (T)u;
+  }
+  // Vb / Vw as constant operand quads: lane (g, c) holds V[16 w + c][16 ks + 4 g + e]
+  quad fVb[RP / 16], fVw[RP / 16];
+  for (int ks = 0; ks < RP / 16; ++ks) {
+    f32x4 tb, tw;
+    for (int e = 0; e < 4; ++e) {
+      const int r = 16 * ks + 4 * g + e;
+      tb[e] = r < R ? a.Vb[(16 * w + c) * R + r] : 0.0f;
+      tw[e] = r < R ? a.Vw[(16 * w + c) * R + r] : 0.0f;
+    }
+    fVb[ks] = Qd::cvt(tb);
+    fVw[ks] = Qd::cvt(tw);
+  }
+  // identity operand: lane (g, c) holds I[4 g + e][c]
+  quad fI;
+  {
+    f32x4 t;
+    for (int e = 0; e < 4; ++e) t[e] = (4 * g + e == c) ? 1.0f : 0.0f;
+    fI = Qd::cvt(t);
+  }
+
+  // ---- state: St[jt][i] = S[v = 16 w + c][j = 16 jt + 4 g + i] ---------------
+  f32x4 St[NJT];
+  {
+    const float* src = a.S_chunks + ((size_t)bh * nch + ch0) * D * D + (16 * w + c) * D + 4 * g;
+    for (int jt = 0; jt < NJT; ++jt) St[jt] = gload4(src + 16 * jt);
+  }
+  const ChunkRec cr = chunk_rec(sizeof(T), D, L, RP);
+  char* rec = reinterpret_cast<char*>(a.rec) + ((size_t)bh * nch + ch0) * cr.total;
+
+  // ---- prefetch registers for the next sub-chunk ------------------------------
+  u32x4 pq[NQV];
+  T pbeta = (T)0.0f;
+  quad pbx[NB], pk[NB], pwx[NB], pv[NB];
+  f32x4 pg[NB];
+#define CARVE_REC_PREFETCH_Q(TILE_)                                                     \
+  do {                                                                                  \
+    const int tt0_ = (TILE_) * LW;                                                      \
+    for (int u_ = 0; u_ < NQV; ++u_) {                                                  \
+      const int x_ = tid + u_ * NT;                                                     \
+      if (NVQ % NT != 0 && x_ >= NVQ) break;                                            \
+      const int t_ = x_ / (D / VEC), j_ = (x_ % (D / VEC)) * VEC;                       \
+      pq[u_] = *reinterpret_cast<const u32x4*>(q + (tt0_ + t_) * rs + j_);              \
+    }                                                                                   \
+    if (tid < LW) pbeta = beta[(tt0_ + tid) * H];                                       \
+  } while (0)
+#define CARVE_REC_PREFETCH_GATES(TILE_)                                                 \
+  do {                                                                                  \
+    const int tt0_ = (TILE_) * LW;                                                      \
+    for (int bb_ = 0; bb_ < NB; ++bb_) {                                                \
+      const int e_ = (tt0_ + 16 * bb_ + c) * rs + 16 * w + 4 * g;                       \
+      pbx[bb_] = Qd::ld(bx + e_);                                                       \
+      pk[bb_] = Qd::ld(k + e_);                                                         \
+      pwx[bb_] = Qd::ld(wx + e_);                                                       \
+      pv[bb_] = Qd::ld(v + e_);                                                         \
+      pg[bb_] = *reinterpret_cast<const f32x4*>(gl + e_);                               \
+    }                                                                                   \
+  } while (0)
+  const int tile0 = ch0 * msub, ntiles = tile0 + msub;
+  CARVE_REC_PREFETCH_Q(tile0);
+  CARVE_REC_PREFETCH_GATES(tile0);
+
+  for (int m = 0; m < msub; ++m) {
+    const int tile = tile0 + m;
+
+    // ---- P0: stage q and beta; chunk start state --------------------------------
+    if (m == 0)
+      for (int jt = 0; jt < NJT; ++jt) Qd::st(sS + (16 * w + c) * LDD + 16 * jt + 4 * g, Qd::cvt(St[jt]));
+    for (int u = 0; u < NQV; ++u) {
+      const int x = tid + u * NT;
+      if (NVQ % NT != 0 && x >= NVQ) break;
+      const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;
+      *reinterpret_cast<u32x4*>(sQ + t * LDD + j) = pq[u];
+    }
+    if (tid < LW) sBeta[tid] = (float)pbeta;
+    if (tile + 1 < ntiles) CARVE_REC_PREFETCH_Q(tile + 1);
+    __syncthreads();
+
+    // ---- P1: fold F^T[j][r] = sum_v S_hat[v][j] U[r][v] (key tile w) -----------
+    if (m == 0) {
+      for (int rt = 0; rt < NRT; ++rt) {
+        f32x4 acc = zero4();
+        for (int vp = 0; vp < D / 32; ++vp) {
+          const quad a0 = Qd::ld_tr(sS, LDD, 32 * vp, 16 * w, g, c);
+          const quad a1 = Qd::ld_tr(sS, LDD, 32 * vp + 16, 16 * w, g, c);
+          const T* ur = sU + (16 * rt + c) * LDD + 32 * vp + 4 * g;
+          acc = Qd::mma32(a0, a1, Qd::ld(ur), Qd::ld(ur + 16), acc);
+        }
+        Qd::st(sF + (16 * rt + c) * LDD + 16 * w + 4 * g, Qd::cvt(acc));
+        Qd::st(reinterpret_cast<T*>(rec + cr.F) + (16 * rt + c) * D + 16 * w + 4 * g, Qd::cvt(acc));
+      }
+      __syncthreads();
+    }
+
+    // ---- P2: tau^T[r][t] = tanh(F[r] . q_t) -> sTau[t][r] -----------------------
+    for (int x = w; x < NRT * NB; x += NW) {
+      const int rt = x % NRT, bb = x / NRT;
+      f32x4 acc = zero4();
+      for (int jp = 0; jp < D / 32; ++jp) {
+        const T* fr = sF + (16 * rt + c) * LDD + 32 * jp + 4 * g;
+        const T* qr = sQ + (16 * bb + c) * LDD + 32 * jp + 4 * g;
+        acc = Qd::mma32(Qd::ld(fr), Qd::ld(fr + 16), Qd::ld(qr), Qd::ld(qr + 16), acc);
+      }
+      for (int i = 0; i < 4; ++i) acc[i] = tanh_f(acc[i]);
+      Qd::st(sTau + (16 * bb + c) * LDR + 16 * rt + 4 * g, Qd::cvt(acc));
+      Qd::st(reinterpret_cast<T*>(rec + cr.Tau) + (m * LW + 16 * bb + c) * R2 + 16 * rt + 4 * g, Qd::cvt(acc));
+    }
+    __syncthreads();
+
+    // ---- P3: gates --------------------------------------------------------------
+    // key side, key tile w: lane (g, c) of block bb holds t = 16 bb + c and
+    // j = 16 w + 4 g + i (i = 0..3); the prefix sums run along the 16 lanes of a row
+    for (int bb = 0; bb < NB; ++bb) {
+      f32x4 z = zero4();
+      for (int ks = 0; ks < RP / 16; ++ks)
+        z = Qd::mma16(fVb[ks], Qd::ld(sTau + (16 * bb + c) * LDR + 16 * ks + 4 * g), z);
+      const f32x4 bxv = Qd::f32(pbx[bb]), kv = Qd::f32(pk[bb]), gv = pg[bb];
+      const f32x4 qv = Qd::f32(Qd::ld(sQ + (16 * bb + c) * LDD + 16 * w + 4 * g));
+      f32x4 kt, qt, ki, gam;
+      for (int i = 0; i < 4; ++i) {
+        const float ell = gv[i] - softplus_f(z[i] + bxv[i]);
+        const float lam = row_scan(ell);
+        const float E = fast_exp(lam);
+        const float Ep = row_shr1(E, 1.0f);
+        kt[i] = kv[i] * Ep;
+        qt[i] = qv[i] * E;
+        ki[i] = kv[i] * fast_exp(-lam);
+        gam[i] = E;
+      }
+      const int ro = (16 * bb + c) * LDD + 16 * w + 4 * g;
+      Qd::st(sKt + ro, Qd::cvt(kt));
+      Qd::st(sQt + ro, Qd::cvt(qt));
+      Qd::st(sKi + ro, Qd::cvt(ki));
+      if (c == 15) {
+        *reinterpret_cast<f32x4*>(sGam + bb * D + 16 * w + 4 * g) = gam;
+        *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(rec + cr.Gam) + (m * NB + bb) * D + 16 * w + 4 * g) = gam;
+      }
+    }
+    // value side, value tile w: rows t = 16 bb + 4 g + i, column v = 16 w + c
+    f32x4 wv[NB];
+    for (int bb = 0; bb < NB; ++bb) {
+      f32x4 z = zero4();
+      for (int ks = 0; ks < RP / 16; ++ks)
+        z = Qd::mma16(Qd::ld(sTau + (16 * bb + c) * LDR + RP + 16 * ks + 4 * g), fVw[ks], z);
+      z = Qd::mma16(pwx[bb], fI, z);                   // + wx, moved into this layout
+      const f32x4 vv = Qd::mma16(pv[bb], fI, zero4());
+      for (int i = 0; i < 4; ++i) wv[bb][i] = sigmoid_f(z[i]) * vv[i];
+    }
+    if (tile + 1 < ntiles) CARVE_REC_PREFETCH_GATES(tile + 1);
+    __syncthreads();
+
+    // ---- P4: A^T and P of every block -------------------------------------------
+    for (int x = w; x < 2 * NB; x += NW) {
+      const bool isP = x >= NB;
+      const int bb = isP ? x - NB : x;
+      const T* ar = (isP ? sKi : sKt) + (16 * bb + c) * LDD + 4 * g;
+      const T* br = (isP ? sQt : sKi) + (16 * bb + c) * LDD + 4 * g;
+      f32x4 acc = zero4();
+      for (int jp = 0; jp < D / 32; ++jp)
+        acc = Qd::mma32(Qd::ld(ar + 32 * jp), Qd::ld(ar + 32 * jp + 16), Qd::ld(br + 32 * jp),
+                        Qd::ld(br + 32 * jp + 16), acc);
+      if (!isP) {
+        // acc[i] = Kt_{t=4g+i} . Ki_{s=c}
+        const f32x4 bt = *reinterpret_cast<const f32x4*>(sBeta + 16 * bb + 4 * g);
+        f32x4 av;
+        for (int i = 0; i < 4; ++i) av[i] = (c < 4 * g + i) ? bt[i] * acc[i] : 0.0f;
+        *reinterpret_cast<f32x4*>(sAT + (bb * 16 + c) * 20 + 4 * g) = av;
+      } else {
+        // acc[i] = Ki_{s=4g+i} . Qt_{t=c}
+        f32x4 pv4;
+        for (int i = 0; i < 4; ++i) pv4[i] = (4 * g + i <= c) ? acc[i] : 0.0f;
+        Qd::st(reinterpret_cast<T*>(rec + cr.P) + ((m * NB + bb) * 16 + c) * 16 + 4 * g, Qd::cvt(pv4));
+      }
+    }
+    __syncthreads();
+
+    // ---- P5: T = (I + A)^{-1} per block; first block's state products ------------
+    quad sb[NJT];
+    for (int jt = 0; jt < NJT; ++jt) sb[jt] = Qd::cvt(St[jt]);
+    f32x4 XK = zero4();
+#define CARVE_REC_XK(BB_)                                                                \
+  do {                                                                                   \
+    XK = zero4();                                                                        \
+    const T* kr_ = sKt + (16 * (BB_) + c) * LDD + 4 * g;                                 \
+    for (int jp_ = 0; jp_ < NJT / 2; ++jp_)                                              \
+      XK = Qd::mma32(Qd::ld(kr_ + 32 * jp_), Qd::ld(kr_ + 32 * jp_ + 16), sb[2 * jp_],   \
+                     sb[2 * jp_ + 1], XK);                                               \
+  } while (0)
+    if (w == NW - 1) {
+      // lane (g, c): block g, row c of T, by substitution on
+      //   T[c][s] = delta(c, s) - sum_{t > s} T[c][t] A[t][s],  s = 15 .. 0
+      if (g < NB) {
+        const float* Ab = sAT + g * 16 * 20;
+        float x[16];
+#pragma unroll
+        for (int s = 15; s >= 0; --s) {
+          float acc0 = (s == c) ? 1.0f : 0.0f, acc1 = 0.0f;
+#pragma unroll
+          for (int t = s + 1; t < 16; ++t) {
+            if ((t - s) & 1) acc0 -= x[t] * Ab[s * 20 + t];
+            else acc1 -= x[t] * Ab[s * 20 + t];
+          }
+          x[s] = acc0 + acc1;
+        }
+        T* tr = sTm + (g * 16 + c) * LDB;
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) {
+          f32x4 t4 = {x[4 * s4], x[4 * s4 + 1], x[4 * s4 + 2], x[4 * s4 + 3]};
+          Qd::st(tr + 4 * s4, Qd::cvt(t4));
+          Qd::st(reinterpret_cast<T*>(rec + cr.Tm) + ((m * NB + g) * 16 + c) * 16 + 4 * s4, Qd::cvt(t4));
+        }
+      }
+    }
+    CARVE_REC_XK(0);
+    __syncthreads();
+
+    // ---- P6: token-serial blocks on the value tile (no barriers) ------------------
+    for (int bb = 0; bb < NB; ++bb) {
+      if (bb > 0) CARVE_REC_XK(bb);
+      {
+        // coalesced: quad jt of every thread is contiguous over the threads
+        T* sv = reinterpret_cast<T*>(rec + cr.S) + (size_t)(m * NB + bb) * NJT * NT * 4 + tid * 4;
+        for (int jt = 0; jt < NJT; ++jt) Qd::st(sv + (size_t)jt * NT * 4, sb[jt]);
+      }
+      const f32x4 bt = *reinterpret_cast<const f32x4*>(sBeta + 16 * bb + 4 * g);
+      f32x4 rr;
+      for (int i = 0; i < 4; ++i) rr[i] = bt[i] * (wv[bb][i] - XK[i]);
+      const f32x4 u = Qd::mma16(Qd::ld(sTm + (bb * 16 + c) * LDB + 4 * g), Qd::cvt(rr), zero4());
+      const quad uq = Qd::cvt(u);
+      for (int jt = 0; jt < NJT; ++jt) {
+        const f32x4 acc = Qd::mma16(Qd::ld_tr(sKi, LDD, 16 * bb, 16 * jt, g, c), uq, St[jt]);
+        const f32x4 gm = *reinterpret_cast<const f32x4*>(sGam + bb * D + 16 * jt + 4 * g);
+        for (int i = 0; i < 4; ++i) St[jt][i] = acc[i] * gm[i];
+        sb[jt] = Qd::cvt(St[jt]);
+      }
+    }
+#undef CARVE_REC_XK
+    __syncthreads();  // the next sub-chunk (or chunk) overwrites sQ, sBeta and region X
+  }
+#undef CARVE_REC_PREFETCH_Q
+#undef CARVE_REC_PREFETCH_GATES
+}
+
+}  // namespace carve
