@@ -61,10 +61,14 @@ constexpr int kReadyWindow = 8;
 // every flag itself.  Returns need + 1 if the bound ran out.
 __device__ __forceinline__ int acquire_ready(const int* rdy, const int need) {
   for (int n = 0; n < kReadySpinLimit; ++n) {
+    // unconditional loads from clamped indices (issued back to back), masked after
     int f[kReadyWindow];
 #pragma unroll
     for (int i = 0; i < kReadyWindow; ++i)
-      f[i] = need - i >= 0 ? __hip_atomic_load(rdy + need - i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+      f[i] = __hip_atomic_load(rdy + (need - i >= 0 ? need - i : 0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+    for (int i = 1; i < kReadyWindow; ++i)
+      if (need - i < 0) f[i] = 0;
     if (f[0] != 0) {
       int lo = need;
 #pragma unroll
@@ -129,6 +133,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   T* sdzwT = reinterpret_cast<T*>(smem + lay.dzwT);
   T* sdzb = reinterpret_cast<T*>(smem + lay.dzb);    // [16][LDD]    dz_b[t][j]
   T* sdY = reinterpret_cast<T*>(smem + lay.dY);      // [16][LDR]    dY[t][r]
+  T* sStg = reinterpret_cast<T*>(smem + lay.Stage);  // [6][16][D]   token tiles, swizzled
 
   const size_t bh0 = ((size_t)b * Tn * H + h) * D;
   const size_t bh1 = (size_t)b * Tn * H + h;
@@ -182,7 +187,14 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   constexpr int NTV = (NTAU + NT - 1) / NT;
   constexpr int NFV = (R2 * D / VEC + NT - 1) / NT;   // 16-byte vectors of F per thread
   u32x4 ptau[NTV], pF[NFV];
-  quad ptm, ppm, psbq[NJT], ptq[NRB], pbx, pkq, pqq2, pwxq, pvq, pdOq;
+  // token tiles k, q, bx, v, wx, dO of a block: 6 * 16 rows of D elements read
+  // as 16-byte vectors (whole rows, coalesced) and staged through LDS
+  constexpr int NC = D / VEC;                    // 16-byte chunks per row
+  constexpr int NSV = 6 * 16 * NC;               // vectors of the six tiles
+  constexpr int NSTG = (NSV + NT - 1) / NT;      // per thread
+  static_assert((16 * NC) % 64 == 0 || NSV % NT == 0, "tile index uniform per wave");
+  u32x4 pstg[NSTG];
+  quad ptm, ppm, psbq[NJT];
   f32x4 pgam, pg;
   T pbeta = (T)0.0f;
 #define CARVE_BWD_LOAD(GB_)                                                                   \
@@ -204,15 +216,14 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
     if (tid < 16) pbeta = beta[(tb_ + tid) * H];                                              \
     const T* sv_ = reinterpret_cast<const T*>(rc_ + cr.S) + (size_t)bc_ * NJT * NT * 4 + tid * 4; \
     for (int jt_ = 0; jt_ < NJT; ++jt_) psbq[jt_] = Qd::ld(sv_ + (size_t)jt_ * NT * 4);        \
-    const T* tq_ = reinterpret_cast<const T*>(rc_ + cr.Tau) + (16 * bc_ + c) * R2 + 4 * g;    \
-    for (int ks_ = 0; ks_ < NRB; ++ks_) ptq[ks_] = Qd::ld(tq_ + 16 * ks_);                    \
-    pbx = Qd::ld(bx + e_);                                                                    \
+    for (int u_ = 0; u_ < NSTG; ++u_) {                                                       \
+      const int x_ = tid + u_ * NT;                                                           \
+      if (NSV % NT != 0 && x_ >= NSV) break;                                                  \
+      const int s_ = x_ / (16 * NC), t_ = (x_ / NC) % 16, k_ = x_ % NC;                       \
+      const T* src_ = s_ == 0 ? k : s_ == 1 ? q : s_ == 2 ? bx : s_ == 3 ? v : s_ == 4 ? wx : dO; \
+      pstg[u_] = *reinterpret_cast<const u32x4*>(src_ + (tb_ + t_) * rs + k_ * VEC);           \
+    }                                                                                         \
     pg = *reinterpret_cast<const f32x4*>(gl + e_);                                            \
-    pkq = Qd::ld(k + e_);                                                                     \
-    pqq2 = Qd::ld(q + e_);                                                                    \
-    pwxq = Qd::ld(wx + e_);                                                                   \
-    pvq = Qd::ld(v + e_);                                                                     \
-    pdOq = Qd::ld(dO + e_);                                                                   \
   } while (0)
 #define CARVE_BWD_LOADF(CH_)                                                                  \
   do {                                                                                        \
@@ -295,12 +306,9 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       const T lbeta = pbeta;
       quad sbq[NJT];   // block start state, wave layout: S[16 w + c][16 jt + 4 g + e]
       for (int jt = 0; jt < NJT; ++jt) sbq[jt] = psbq[jt];
-      quad ltq[NRB];
-      for (int ks = 0; ks < NRB; ++ks) ltq[ks] = ptq[ks];
-      const quad lbx = pbx;
+      u32x4 lstg[NSTG];
+      for (int u = 0; u < NSTG; ++u) lstg[u] = pstg[u];
       const f32x4 lg = pg;
-      const quad kq = pkq, qq = pqq2;
-      const quad wxq = pwxq, vq = pvq, dOq = pdOq;
       if (bc == nbc - 1) {
         // first block of a chunk in reverse order: the chunk's F into LDS (the
         // previous chunk's last read of sF was before its glue barriers)
@@ -336,6 +344,32 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       }
       if (tid < D / 4) *reinterpret_cast<f32x4*>(sGam + 4 * tid) = lgam;
       if (tid < 16) sBeta[tid] = (float)lbeta;
+      // token tiles -> LDS: 16-byte chunk kk of row t goes to chunk kk ^ (t mod NC)
+      // (a row-dependent swizzle instead of padding: the 16 rows a wave reads in
+      // one quad load fall into distinct banks)
+      for (int u = 0; u < NSTG; ++u) {
+        const int x = tid + u * NT;
+        if (NSV % NT != 0 && x >= NSV) break;
+        const int s_ = x / (16 * NC), t = (x / NC) % 16, kk = x % NC;
+        *reinterpret_cast<u32x4*>(sStg + (s_ * 16 + t) * D + (kk ^ (t & (NC - 1))) * VEC) = lstg[u];
+      }
+      __syncthreads();
+      // this wave's quads of the token tiles (row t = c, elements 16 w + 4 g ..
+      // + 3) and of tau_b; read before the barrier that ends this step, so the
+      // value-side step may overwrite the staging region
+      quad kq, qq, lbx, vq, wxq, dOq, ltq[NRB];
+      {
+        const int by = (16 * w + 4 * g) * (int)sizeof(T);
+        const int off = ((((by >> 4) ^ (c & (NC - 1))) << 4) | (by & 15)) / (int)sizeof(T);
+        const T* r0 = sStg + c * D + off;
+        kq = Qd::ld(r0);
+        qq = Qd::ld(r0 + 16 * D);
+        lbx = Qd::ld(r0 + 32 * D);
+        vq = Qd::ld(r0 + 48 * D);
+        wxq = Qd::ld(r0 + 64 * D);
+        dOq = Qd::ld(r0 + 80 * D);
+        for (int ks = 0; ks < NRB; ++ks) ltq[ks] = Qd::ld(sTau + c * LDR + 16 * ks + 4 * g);
+      }
       // key-side factors kept for the adjoint in the token dtype (quads)
       quad Eq, Eiq, sigq;
       {

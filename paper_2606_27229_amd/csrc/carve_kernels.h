@@ -160,9 +160,13 @@ struct BwdArgs {
 constexpr int kVSplit = 16;
 constexpr int kUSplit = 16;
 
-// LDS layout of the adjoint kernel (one 16-token block at a time)
+// LDS layout of the adjoint kernel (one 16-token block at a time).  The four
+// [value][token] exchange buffers dOT .. dzwT are dead between the end of one
+// block and the value-side step of the next; the block's token tiles (k, q, bx,
+// v, wx, dO: 16 rows each, unpadded, 16-byte chunks XOR-swizzled by row) are
+// staged there (Stage), so the region is at least 6 * 16 * D elements.
 struct BwdLds {
-  size_t F, VbT, VwT, Tau, Tm, P, Gam, Beta, Dbeta, Kt, Qt, Ki, Sx, dSx, dOT, uT, dRT, dzwT, dzb, dY, total;
+  size_t F, VbT, VwT, Tau, Tm, P, Gam, Beta, Dbeta, Kt, Qt, Ki, Sx, dSx, dOT, uT, dRT, dzwT, Stage, dzb, dY, total;
 };
 
 template <typename T, int D, int RP>
@@ -187,10 +191,12 @@ __host__ __device__ constexpr BwdLds bwd_lds() {
   l.Ki = off;    off += lds_round(16 * LDD * e);
   l.Sx = off;    off += lds_round(D * LDD * e);
   l.dSx = off;   off += lds_round(D * lds_max(LDD, 2 * LDR) * e);
+  l.Stage = off;
   l.dOT = off;   off += lds_round(D * LDB * e);
   l.uT = off;    off += lds_round(D * LDB * e);
   l.dRT = off;   off += lds_round(D * LDB * e);
   l.dzwT = off;  off += lds_round(D * LDB * e);
+  off = lds_max(off, l.Stage + lds_round(6 * 16 * D * e));
   l.dzb = off;   off += lds_round(16 * LDD * e);
   l.dY = off;    off += lds_round(16 * LDR * e);
   l.total = off;
