@@ -197,7 +197,19 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   quad ptm, ppm, psbq[NJT];
   f32x4 pgam, pg;
   T pbeta = (T)0.0f;
-#define CARVE_BWD_LOAD(GB_)                                                                   \
+  // The prefetch of a block is issued in two parts during the previous block's
+  // value- and key-side steps (which hardly use the memory pipeline), not at
+  // its top, where issuing it would stall the waves: LOADA (token tiles, tau,
+  // T, P, retention, beta, g) and LOADS (the block start state, once the
+  // current one has had its last use).
+#define CARVE_BWD_LOADS(GB_)                                                                  \
+  do {                                                                                        \
+    const int ch_ = (GB_) / nbc, bc_ = (GB_) % nbc;                                           \
+    const char* rc_ = recb + (size_t)ch_ * cr.total;                                          \
+    const T* sv_ = reinterpret_cast<const T*>(rc_ + cr.S) + (size_t)bc_ * NJT * NT * 4 + tid * 4; \
+    for (int jt_ = 0; jt_ < NJT; ++jt_) psbq[jt_] = Qd::ld(sv_ + (size_t)jt_ * NT * 4);        \
+  } while (0)
+#define CARVE_BWD_LOADA(GB_)                                                                  \
   do {                                                                                        \
     const int ch_ = (GB_) / nbc, bc_ = (GB_) % nbc;                                           \
     const char* rc_ = recb + (size_t)ch_ * cr.total;                                          \
@@ -214,8 +226,6 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
     }                                                                                         \
     if (tid < D / 4) pgam = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(rc_ + cr.Gam) + bc_ * D + 4 * tid); \
     if (tid < 16) pbeta = beta[(tb_ + tid) * H];                                              \
-    const T* sv_ = reinterpret_cast<const T*>(rc_ + cr.S) + (size_t)bc_ * NJT * NT * 4 + tid * 4; \
-    for (int jt_ = 0; jt_ < NJT; ++jt_) psbq[jt_] = Qd::ld(sv_ + (size_t)jt_ * NT * 4);        \
     for (int u_ = 0; u_ < NSTG; ++u_) {                                                       \
       const int x_ = tid + u_ * NT;                                                           \
       if (NSV % NT != 0 && x_ >= NSV) break;                                                  \
@@ -264,7 +274,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
     }                                                                                         \
   } while (0)
   CARVE_BWD_READY(nch - 1);
-  CARVE_BWD_LOAD(ngb - 1);
+  CARVE_BWD_LOADA(ngb - 1);
+  CARVE_BWD_LOADS(ngb - 1);
   CARVE_BWD_LOADF(nch - 1);
 
   // pending dq / dF update of the last processed block (its BQ step)
@@ -320,11 +331,9 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
           }
         }
       }
-      // prefetch the next block (and at a chunk's last block the next chunk's
-      // F, once the recompute has published that chunk's record)
+      // the next block's prefetch (below) reads chunk ch - 1's record at a
+      // chunk's last block: wait until the recompute has published it
       if (bc == 0 && ch > 0) CARVE_BWD_READY(ch - 1);
-      CARVE_BWD_LOAD(gb > 0 ? gb - 1 : 0);
-      if (bc == 0) CARVE_BWD_LOADF(ch > 0 ? ch - 1 : 0);
 
       // -- BQ of the previous block (overlaps the loads above) -------------------
       if (bc < nbc - 1) CARVE_BWD_BQ();
@@ -404,6 +413,10 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       __syncthreads();
 
       // -- BV: value-side adjoint (value tile w, rows t = 4 g + i, column v = 16 w + c)
+      // prefetch (part A) of the next block, and at a chunk's last block the
+      // next chunk's F
+      CARVE_BWD_LOADA(gb > 0 ? gb - 1 : 0);
+      if (bc == 0) CARVE_BWD_LOADF(ch > 0 ? ch - 1 : 0);
       {
         const f32x4 vv = Qd::mma16(vq, CARVE_FI(), zero4());
         const f32x4 dOc = Qd::mma16(dOq, CARVE_FI(), zero4());
@@ -475,6 +488,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       __syncthreads();
 
       // -- BKA: key-side adjoint (key tile w; C rows j = 16 w + 4 g + i, column t = c)
+      // prefetch (part S): the next block's start state (sbq had its last use in BV)
+      CARVE_BWD_LOADS(gb > 0 ? gb - 1 : 0);
       f32x4 dqp;
       {
         const f32x4 kv = Qd::f32(kq), qv = Qd::f32(qq), E = Qd::f32(Eq), Ei = Qd::f32(Eiq), sig = Qd::f32(sigq);
@@ -649,7 +664,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
 
 #undef CARVE_BWD_BQ
 #undef CARVE_BWD_READY
-#undef CARVE_BWD_LOAD
+#undef CARVE_BWD_LOADA
+#undef CARVE_BWD_LOADS
 #undef CARVE_BWD_LOADF
   if (a.dS0) {
     float* dst = a.dS0 + soff + (16 * w + c) * D + 4 * g;
