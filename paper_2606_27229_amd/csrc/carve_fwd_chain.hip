@@ -184,9 +184,21 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       ck[u_] = *reinterpret_cast<const u32x4*>(k + o_);                            \
       cbx[u_] = *reinterpret_cast<const u32x4*>(bx + o_);                          \
     }                                                                              \
+  } while (0)
+  // per-tile operands of the gates (16 token rows of this wave's 16 columns)
+#define CARVE_PREFETCH_G(BLK_)                                                     \
+  do {                                                                             \
+    int cs_ = c, gs_ = g;                                                          \
+    asm volatile("" : "+v"(cs_), "+v"(gs_));                                       \
+    for (int bb_ = 0; bb_ < NB; ++bb_)                                             \
+      pg[bb_] = *reinterpret_cast<const f32x4*>(gl + ((BLK_) * WB + 16 * bb_ + cs_) * rs + 16 * w + 4 * gs_); \
+  } while (0)
+#define CARVE_PREFETCH_VW(BLK_)                                                    \
+  do {                                                                             \
+    int cs_ = c, gs_ = g;                                                          \
+    asm volatile("" : "+v"(cs_), "+v"(gs_));                                       \
     for (int bb_ = 0; bb_ < NB; ++bb_) {                                           \
-      const int e_ = (t0_ + 16 * bb_ + c) * rs + 16 * w + 4 * g;                   \
-      pg[bb_] = *reinterpret_cast<const f32x4*>(gl + e_);                          \
+      const int e_ = ((BLK_) * WB + 16 * bb_ + cs_) * rs + 16 * w + 4 * gs_;      \
       pv[bb_] = Qd::ld(v + e_);                                                    \
       pwx[bb_] = Qd::ld(wx + e_);                                                  \
     }                                                                              \
@@ -201,6 +213,8 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   } while (0)
   CARVE_PREFETCH_Q(0);
   CARVE_PREFETCH_GATES(0);
+  CARVE_PREFETCH_G(0);
+  CARVE_PREFETCH_VW(0);
 
   quad oq[NB];   // o of the previous block, lane (g, c): o[t = 16 bb + c][v = 16 w + 4 g + e]
   int oprev = -1;
@@ -210,20 +224,22 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     const bool cstart = (blk % bpc) == 0;
     const int par = blk & 1;
 
-    // ---- stage: wait for the prefetch; previous output; chunk start state ------
+    // ---- stage: wait for the prefetch; chunk start state --------------------------
+    // The block's global stores and the next block's loads are spread over the
+    // steps that use only LDS and the matrix cores (fold, tau, coupling,
+    // substitution): issued in one burst they would stall every wave behind
+    // the CU's memory pipeline.  Store addresses come from opaque lane
+    // coordinates, recomputed where needed instead of held across the loop.
+#define CARVE_STORE_S(JT0_, JT1_)                                                  \
+    do {                                                                           \
+      if (cstart && a.S_chunks) {                                                  \
+        int cs_ = c, gs_ = g;                                                      \
+        asm volatile("" : "+v"(cs_), "+v"(gs_));                                   \
+        float* dst_ = a.S_chunks + ((size_t)bh * (Tn / L) + blk / bpc) * D * D + (16 * w + cs_) * D + 4 * gs_; \
+        for (int jt_ = (JT0_); jt_ < (JT1_); ++jt_) *reinterpret_cast<f32x4*>(dst_ + 16 * jt_) = St[jt_]; \
+      }                                                                            \
+    } while (0)
     vm_wait_all();
-    {
-      // store addresses from opaque lane coordinates: recomputed here instead of
-      // being hoisted out of the loop and kept live
-      int cs = c, gs = g;
-      asm volatile("" : "+v"(cs), "+v"(gs));
-      if (oprev >= 0)
-        for (int bb = 0; bb < NB; ++bb) Qd::st(o + (oprev + 16 * bb + cs) * rs + 16 * w + 4 * gs, oq[bb]);
-      if (cstart && a.S_chunks) {
-        float* dst = a.S_chunks + ((size_t)bh * (Tn / L) + blk / bpc) * D * D + (16 * w + cs) * D + 4 * gs;
-        for (int jt = 0; jt < NJT; ++jt) *reinterpret_cast<f32x4*>(dst + 16 * jt) = St[jt];
-      }
-    }
     if (cstart) {
       for (int jt = 0; jt < NJT; ++jt) Qd::st(sS + (16 * w + c) * LDD + 16 * jt + 4 * g, Qd::cvt(St[jt]));
     }
@@ -234,6 +250,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       CARVE_PREFETCH_Q(nx);
     }
     __syncthreads();
+    CARVE_STORE_S(0, NJT / 2);
     // raw keys of the block into free LDS (read by the gates)
     CARVE_STAGE_ROWS(sKi, ck);
 
@@ -253,6 +270,12 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     }
     // raw erase logits into region X (the fold is done with the state)
     CARVE_STAGE_ROWS(sBx, cbx);
+    // the previous block's outputs
+    if (oprev >= 0) {
+      int cs = c, gs = g;
+      asm volatile("" : "+v"(cs), "+v"(gs));
+      for (int bb = 0; bb < NB; ++bb) Qd::st(o + (oprev + 16 * bb + cs) * rs + 16 * w + 4 * gs, oq[bb]);
+    }
 
     // ---- tau^T[r][t] = tanh(F[r] . q_t) -> sTau[t][r] ---------------------------
     for (int x = w; x < NRT * NB; x += NW) {
@@ -328,6 +351,8 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     __syncthreads();
 
     // ---- coupling tiles, diagonal inverses, state products ---------------------
+    CARVE_STORE_S(NJT / 2, NJT);
+    CARVE_PREFETCH_G(blk + 1 < nblk ? blk + 1 : blk);
     const float* bcur = sBeta + par * WB;
     if (w == TW) {
       // diagonal tiles of A in f32, stored transposed: sAdT[i][s][t] = A[t][s]
@@ -420,6 +445,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     __syncthreads();
 
     // ---- value tile: blocked substitution for u, outputs, state carry ---------------
+    CARVE_PREFETCH_VW(blk + 1 < nblk ? blk + 1 : blk);
     quad uq[NB];
     for (int i = 0; i < NB; ++i) {
       f32x4 r = RH[i];
@@ -448,6 +474,9 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   }
 #undef CARVE_PREFETCH_Q
 #undef CARVE_PREFETCH_GATES
+#undef CARVE_PREFETCH_G
+#undef CARVE_PREFETCH_VW
+#undef CARVE_STORE_S
 #undef CARVE_STAGE_ROWS
 }
 
