@@ -175,6 +175,10 @@ __device__ __forceinline__ float row_shl1(float x, float fill) {
 __device__ __forceinline__ float row_bcast15(float x) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x15F, 0xf, 0xf, false));
 }
+// x of the neighbouring lane (lane ^ 1)
+__device__ __forceinline__ float lane_xor1(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0xB1, 0xf, 0xf, false));
+}
 // wait until every vector memory operation this wave issued has completed
 __device__ __forceinline__ void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 // inclusive suffix sum over the 16 lanes of each row

@@ -230,13 +230,28 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     // substitution): issued in one burst they would stall every wave behind
     // the CU's memory pipeline.  Store addresses come from opaque lane
     // coordinates, recomputed where needed instead of held across the loop.
+  // The chunk start state goes out in whole 128-byte lines: for the column
+  // tiles 2m and 2m + 1, neighbouring lanes c and c ^ 1 (rows 2r and 2r + 1)
+  // swap one quad each, so that one store writes row 2r (tile 2m from the even
+  // lane, tile 2m + 1 from the odd one) and the next row 2r + 1.  Tiles
+  // [JT0_ / 2 * 2, JT1_ / 2 * 2) are stored.
 #define CARVE_STORE_S(JT0_, JT1_)                                                  \
     do {                                                                           \
       if (cstart && a.S_chunks) {                                                  \
         int cs_ = c, gs_ = g;                                                      \
         asm volatile("" : "+v"(cs_), "+v"(gs_));                                   \
-        float* dst_ = a.S_chunks + ((size_t)bh * (Tn / L) + blk / bpc) * D * D + (16 * w + cs_) * D + 4 * gs_; \
-        for (int jt_ = (JT0_); jt_ < (JT1_); ++jt_) *reinterpret_cast<f32x4*>(dst_ + 16 * jt_) = St[jt_]; \
+        const bool odd_ = (cs_ & 1) != 0;                                          \
+        float* r0_ = a.S_chunks + ((size_t)bh * (Tn / L) + blk / bpc) * D * D + (16 * w + (cs_ & ~1)) * D + 4 * gs_ + (odd_ ? 16 : 0); \
+        for (int m_ = (JT0_) / 2; m_ < (JT1_) / 2; ++m_) {                         \
+          f32x4 st0_, st1_;                                                        \
+          for (int e_ = 0; e_ < 4; ++e_) {                                         \
+            const float rv_ = lane_xor1(odd_ ? St[2 * m_][e_] : St[2 * m_ + 1][e_]); \
+            st0_[e_] = odd_ ? rv_ : St[2 * m_][e_];                                \
+            st1_[e_] = odd_ ? St[2 * m_ + 1][e_] : rv_;                            \
+          }                                                                        \
+          *reinterpret_cast<f32x4*>(r0_ + 32 * m_) = st0_;                         \
+          *reinterpret_cast<f32x4*>(r0_ + D + 32 * m_) = st1_;                     \
+        }                                                                          \
       }                                                                            \
     } while (0)
     vm_wait_all();
