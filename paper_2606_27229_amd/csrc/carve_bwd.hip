@@ -442,13 +442,12 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         // du = Ki dM^T + P^T dO with dM = dS' diag(gam)
         f32x4 du = zero4();
         const T* kir = sKi + c * LDD + 4 * g;
-        const float* gmr = sGam + 4 * g;
-        for (int jp = 0; jp < NJT / 2; ++jp) {
-          const f32x4 g0 = *reinterpret_cast<const f32x4*>(gmr + 32 * jp);
-          const f32x4 g1 = *reinterpret_cast<const f32x4*>(gmr + 32 * jp + 16);
-          du = Qd::mma32(Qd::ld(kir + 32 * jp), Qd::ld(kir + 32 * jp + 16), Qd::cvt(dSt[2 * jp] * g0),
-                         Qd::cvt(dSt[2 * jp + 1] * g1), du);
-        }
+        // dS' (already in LDS for the key side) becomes dM in place: both du and
+        // the state gradient below use dM only
+        for (int jt = 0; jt < NJT; ++jt) dSt[jt] *= *reinterpret_cast<const f32x4*>(sGam + 16 * jt + 4 * g);
+        for (int jp = 0; jp < NJT / 2; ++jp)
+          du = Qd::mma32(Qd::ld(kir + 32 * jp), Qd::ld(kir + 32 * jp + 16), Qd::cvt(dSt[2 * jp]),
+                         Qd::cvt(dSt[2 * jp + 1]), du);
         const quad dOcq = Qd::cvt(dOc);
         du = Qd::mma16(Qd::ld_tr(sP, LDB, 0, 0, g, c), dOcq, du);
         const f32x4 dR = Qd::mma16(Qd::ld_tr(sTm, LDB, 0, 0, g, c), Qd::cvt(du), zero4());
@@ -461,9 +460,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         // state gradient at the block start
         for (int jt = 0; jt < NJT; ++jt) {
           CARVE_SEQ();
-          const f32x4 gm = *reinterpret_cast<const f32x4*>(gmr + 16 * jt);
           dSt[jt] = Qd::mma32(Qd::ld_tr(sQt, LDD, 0, 16 * jt, g, c), Qd::ld_tr(sKt, LDD, 0, 16 * jt, g, c), dOcq,
-                              dXq, dSt[jt] * gm);
+                              dXq, dSt[jt]);
         }
         // value-side token gradients, stored through the identity (4 values per lane)
         f32x4 dvv, dzw;
@@ -495,6 +493,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         const f32x4 kv = Qd::f32(kq), qv = Qd::f32(qq), E = Qd::f32(Eq), Ei = Qd::f32(Eiq), sig = Qd::f32(sigq);
         f32x4 dKt = zero4(), dQt = zero4(), dKi = zero4(), dA = zero4(), dP = zero4();
         float dgs = 0.0f;   // sum_v dS'[v][j] S[v][j] for j = 16 w + c (partial over this lane's v)
+        // one pass over the value axis (32 values per step): every operand tile
+        // is read from LDS once
         for (int kp = 0; kp < NJT / 2; ++kp) {
           CARVE_SEQ();
           const quad s0 = Qd::ld_tr(sSx, LDD, 32 * kp, 16 * w, g, c);
@@ -503,21 +503,14 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
           const quad a1 = Qd::ld_tr(sdSx, LDD, 32 * kp + 16, 16 * w, g, c);
           const quad r0 = Qd::ld_tr(sdRT, LDB, 32 * kp, 0, g, c), r1 = Qd::ld_tr(sdRT, LDB, 32 * kp + 16, 0, g, c);
           const quad o0 = Qd::ld_tr(sdOT, LDB, 32 * kp, 0, g, c), o1 = Qd::ld_tr(sdOT, LDB, 32 * kp + 16, 0, g, c);
+          const quad u0 = Qd::ld_tr(suT, LDB, 32 * kp, 0, g, c), u1 = Qd::ld_tr(suT, LDB, 32 * kp + 16, 0, g, c);
           dKt = Qd::mma32(s0, s1, r0, r1, dKt);
           dQt = Qd::mma32(s0, s1, o0, o1, dQt);
-          const f32x4 x0 = Qd::f32(a0), x1 = Qd::f32(a1), y0 = Qd::f32(s0), y1 = Qd::f32(s1);
-          for (int e = 0; e < 4; ++e) dgs += x0[e] * y0[e] + x1[e] * y1[e];
-        }
-        for (int kp = 0; kp < NJT / 2; ++kp) {
-          CARVE_SEQ();
-          const quad a0 = Qd::ld_tr(sdSx, LDD, 32 * kp, 16 * w, g, c);
-          const quad a1 = Qd::ld_tr(sdSx, LDD, 32 * kp + 16, 16 * w, g, c);
-          const quad r0 = Qd::ld_tr(sdRT, LDB, 32 * kp, 0, g, c), r1 = Qd::ld_tr(sdRT, LDB, 32 * kp + 16, 0, g, c);
-          const quad o0 = Qd::ld_tr(sdOT, LDB, 32 * kp, 0, g, c), o1 = Qd::ld_tr(sdOT, LDB, 32 * kp + 16, 0, g, c);
-          const quad u0 = Qd::ld_tr(suT, LDB, 32 * kp, 0, g, c), u1 = Qd::ld_tr(suT, LDB, 32 * kp + 16, 0, g, c);
           dKi = Qd::mma32(a0, a1, u0, u1, dKi);
           dA = Qd::mma32(r0, r1, u0, u1, dA);
           dP = Qd::mma32(o0, o1, u0, u1, dP);
+          const f32x4 x0 = Qd::f32(a0), x1 = Qd::f32(a1), y0 = Qd::f32(s0), y1 = Qd::f32(s1);
+          for (int e = 0; e < 4; ++e) dgs += x0[e] * y0[e] + x1[e] * y1[e];
         }
         dgs += __shfl_xor(dgs, 16);
         dgs += __shfl_xor(dgs, 32);
