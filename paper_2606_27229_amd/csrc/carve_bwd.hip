@@ -627,16 +627,9 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         const quad hi = Qd::cvt(dF[rt]);
         Qd::st(sdFh + (16 * w + c) * LDR + 16 * rt + 4 * g, hi);
         Qd::st(sdFl + (16 * w + c) * LDR + 16 * rt + 4 * g, Qd::cvt(dF[rt] - Qd::f32(hi)));
-        // dF parked as [r][j]: the tile is transposed on the matrix cores in f32
-        // (an exact product with the identity) so that a lane holds four
-        // consecutive j, one 16-byte store per tile
-        {
-          const float one = 1.0f, zero = 0.0f;
-          f32x4 tT = zero4();
-          for (int kk = 0; kk < 4; ++kk)
-            tT = __builtin_amdgcn_mfma_f32_16x16x4f32(dF[rt][kk], 4 * g + kk == c ? one : zero, tT, 0, 0, 0);
-          *reinterpret_cast<f32x4*>(dFr + (size_t)(16 * rt + c) * D + 16 * w + 4 * g) = tT;
-        }
+        // dF parked as [j][r] (a lane holds four consecutive r of one j: one
+        // 16-byte store per tile); the d[Ub; Uw] kernel transposes it in LDS
+        *reinterpret_cast<f32x4*>(dFr + (size_t)(16 * w + c) * R2 + 16 * rt + 4 * g) = dF[rt];
         dF[rt] = zero4();
       }
       __syncthreads();
@@ -668,6 +661,14 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
 
 // d[Ub; Uw][r][v] = sum over the chunks of one split of sum_j dF[r][j] S_hat[v][j];
 // wave w owns value tile w (S_hat read in the thread layout of the chunk record).
+// Per chunk, dF (parked as [j][r] f32) is read once with whole-row 16-byte loads
+// and staged in LDS as a high and a low token-dtype part ([j][r], padded rows);
+// the matrix-core operand dF[r][j] is then read with the transposing LDS load.
+template <typename T, int D, int RP>
+__host__ __device__ constexpr size_t uparam_lds() {
+  return (sizeof(T) == 2 ? 2 : 1) * (size_t)D * (2 * RP + 16 / sizeof(T)) * sizeof(T);
+}
+
 template <typename T, int D, int RP>
 __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_uparam_kernel(BwdArgs a) {
   typedef Quad<T> Qd;
@@ -676,6 +677,13 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_uparam_kernel(BwdArg
   constexpr int NJT = D / 16;
   constexpr int R2 = 2 * RP;
   constexpr int NRT = R2 / 16;
+  constexpr int LDR = R2 + 16 / sizeof(T);
+  constexpr bool SPLIT = sizeof(T) == 2;       // f32 operands carry dF exactly
+  constexpr int NV = D * R2 / 4;               // 16-byte vectors of dF
+  static_assert(NV % NT == 0, "whole vectors per thread");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  T* sH = reinterpret_cast<T*>(smem);          // [D][LDR] dF rounded to T
+  T* sL = sH + D * LDR;                        // [D][LDR] dF - rounded (bf16 only)
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
   const int Tn = a.T, L = a.L, R = a.R;
@@ -693,14 +701,21 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_uparam_kernel(BwdArg
     const float* dFr = reinterpret_cast<const float*>(rc + cr.dF);
     quad sb[NJT];
     for (int jt = 0; jt < NJT; ++jt) sb[jt] = Qd::ld(sv + (size_t)jt * NT * 4);
+    for (int u = 0; u < NV / NT; ++u) {
+      const int x = tid + u * NT;
+      const int j = x / (R2 / 4), r4 = (x % (R2 / 4)) * 4;
+      const f32x4 v = gload4(dFr + (size_t)j * R2 + r4);
+      const quad hi = Qd::cvt(v);
+      Qd::st(sH + j * LDR + r4, hi);
+      if (SPLIT) Qd::st(sL + j * LDR + r4, Qd::cvt(v - Qd::f32(hi)));
+    }
+    __syncthreads();
     for (int rt = 0; rt < NRT; ++rt)
-      for (int jt = 0; jt < NJT; ++jt)
-      {
-        const f32x4 x = gload4(dFr + (16 * rt + c) * D + 16 * jt + 4 * g);
-        const quad hi = Qd::cvt(x);
-        acc[rt] = Qd::mma16(hi, sb[jt], acc[rt]);
-        acc[rt] = Qd::mma16(Qd::cvt(x - Qd::f32(hi)), sb[jt], acc[rt]);
+      for (int jt = 0; jt < NJT; ++jt) {
+        acc[rt] = Qd::mma16(Qd::ld_tr(sH, LDR, 16 * jt, 16 * rt, g, c), sb[jt], acc[rt]);
+        if (SPLIT) acc[rt] = Qd::mma16(Qd::ld_tr(sL, LDR, 16 * jt, 16 * rt, g, c), sb[jt], acc[rt]);
       }
+    __syncthreads();   // the next chunk overwrites the staged dF
   }
   float* part = a.part + (size_t)blockIdx.x * part_floats(R, D);
   float* pUb = part;
@@ -974,8 +989,13 @@ int launch_bwd_vparam(const BwdArgs& a, int dtype, int D, hipStream_t s) {
 
 template <typename T, int D, int RP>
 static int launch_uparam_t(const BwdArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((carve_bwd_uparam_kernel<T, D, RP>), dim3(a.B * a.H * kUSplit), dim3(bwd_threads(D)), 0, s, a);
-  return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
+  constexpr size_t lds = uparam_lds<T, D, RP>();
+  if constexpr (lds > 64 * 1024) {
+    return CARVE_ERR_UNSUPPORTED;   // only shapes the fused launch rejects first
+  } else {
+    hipLaunchKernelGGL((carve_bwd_uparam_kernel<T, D, RP>), dim3(a.B * a.H * kUSplit), dim3(bwd_threads(D)), lds, s, a);
+    return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
+  }
 }
 
 template <typename T>

@@ -25,7 +25,8 @@ struct FwdArgs {
 //   Gam [L/16][D]  f32           block retention e^{lam_15}
 //   S   [L/16][D/16][threads][4]  block start states: quad jt of thread tid
 //                                 (S[16 w + c][16 jt + 4 g + e]), contiguous over threads
-//   dF  [2RP][D]   f32           written by the adjoint: the chunk's gradient of F
+//   dF  [D][2RP]   f32           written by the adjoint: the chunk's gradient of F,
+//                                 stored transposed (dF[r][j] at (j, r))
 struct ChunkRec {
   size_t F, Tau, Tm, P, Gam, S, dF, total;
 };
