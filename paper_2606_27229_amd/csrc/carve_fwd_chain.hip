@@ -106,6 +106,8 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   T* sTmT = reinterpret_cast<T*>(smem + lay.TmT);          // [NB][16][LDB] T_ii[t][s] at (s, t)
   float* sRho = reinterpret_cast<float*>(smem + lay.Rho);  // [D] e^{rho} = e^{lam_end / 2}
   float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);  // [2][WB] (block parity)
+  constexpr bool SVW = chain_stage_vw<T, D, WB, RP>();
+  T* sVW = reinterpret_cast<T*>(smem + lay.VW);    // [2][WB][D]  v, wx (swizzled; SVW)
 
   const size_t bh0 = ((size_t)b * Tn * H + h) * D;
   const size_t bh1 = (size_t)b * Tn * H + h;
@@ -161,7 +163,8 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   constexpr int NVX = WB * D / VEC;                  // vectors of one [WB][D] tile
   constexpr int NXV = (NVX + NT - 1) / NT;           // per thread
   u32x4 cq[NXV], ck[NXV], cbx[NXV];
-  quad pv[NB], pwx[NB];
+  quad pv[NB], pwx[NB];      // per-tile value-side operands (without SVW)
+  u32x4 cv[NXV], cwx[NXV];   // whole rows of v and wx (with SVW)
   f32x4 pg[NB];
   T pbeta = (T)0.0f;
 #define CARVE_PREFETCH_Q(BLK_)                                                     \
@@ -195,12 +198,38 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   } while (0)
 #define CARVE_PREFETCH_VW(BLK_)                                                    \
   do {                                                                             \
-    int cs_ = c, gs_ = g;                                                          \
-    asm volatile("" : "+v"(cs_), "+v"(gs_));                                       \
-    for (int bb_ = 0; bb_ < NB; ++bb_) {                                           \
-      const int e_ = ((BLK_) * WB + 16 * bb_ + cs_) * rs + 16 * w + 4 * gs_;      \
-      pv[bb_] = Qd::ld(v + e_);                                                    \
-      pwx[bb_] = Qd::ld(wx + e_);                                                  \
+    if constexpr (SVW) {                                                           \
+      const int t0_ = (BLK_) * WB;                                                 \
+      for (int u_ = 0; u_ < NXV; ++u_) {                                           \
+        const int x_ = tid + u_ * NT;                                              \
+        if (NVX % NT != 0 && x_ >= NVX) break;                                     \
+        const int o_ = (t0_ + x_ / (D / VEC)) * rs + (x_ % (D / VEC)) * VEC;       \
+        cv[u_] = *reinterpret_cast<const u32x4*>(v + o_);                          \
+        cwx[u_] = *reinterpret_cast<const u32x4*>(wx + o_);                        \
+      }                                                                            \
+    } else {                                                                       \
+      int cs_ = c, gs_ = g;                                                        \
+      asm volatile("" : "+v"(cs_), "+v"(gs_));                                     \
+      for (int bb_ = 0; bb_ < NB; ++bb_) {                                         \
+        const int e_ = ((BLK_) * WB + 16 * bb_ + cs_) * rs + 16 * w + 4 * gs_;    \
+        pv[bb_] = Qd::ld(v + e_);                                                  \
+        pwx[bb_] = Qd::ld(wx + e_);                                                \
+      }                                                                            \
+    }                                                                              \
+  } while (0)
+  // v / wx rows into VW: 16-byte chunk kk of row t goes to chunk kk ^ (t mod NC)
+  // (a swizzle instead of padding: the 16 rows a wave reads with one quad load
+  // fall into distinct banks)
+  constexpr int NC = D / VEC;                        // 16-byte chunks per row
+#define CARVE_STAGE_VW()                                                           \
+  do {                                                                             \
+    for (int u_ = 0; u_ < NXV; ++u_) {                                             \
+      const int x_ = tid + u_ * NT;                                                \
+      if (NVX % NT != 0 && x_ >= NVX) break;                                       \
+      const int t_ = x_ / NC, kk_ = x_ % NC;                                       \
+      T* d_ = sVW + t_ * D + (kk_ ^ (t_ & (NC - 1))) * VEC;                        \
+      *reinterpret_cast<u32x4*>(d_) = cv[u_];                                      \
+      *reinterpret_cast<u32x4*>(d_ + WB * D) = cwx[u_];                            \
     }                                                                              \
   } while (0)
 #define CARVE_STAGE_ROWS(DST_, SRC_)                                               \
@@ -268,6 +297,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     CARVE_STORE_S(0, NJT / 2);
     // raw keys of the block into free LDS (read by the gates)
     CARVE_STAGE_ROWS(sKi, ck);
+    if constexpr (SVW) CARVE_STAGE_VW();
 
     // ---- fold F^T[j][r] = sum_v S_hat[v][j] U[r][v] (key tile w) --------------
     if (cstart) {
@@ -355,8 +385,16 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       f32x4 z = zero4();
       for (int ks = 0; ks < NRB; ++ks)
         z = Qd::mma16(Qd::ld(sTau + (16 * bb + c) * LDR + RP + 16 * ks + 4 * g), fVw[ks], z);
-      z = Qd::mma16(pwx[bb], fI, z);                   // + wx, moved into this layout
-      const f32x4 vv = Qd::mma16(pv[bb], fI, zero4());
+      quad vq = pv[bb], wxq = pwx[bb];
+      if constexpr (SVW) {
+        // row t = 16 bb + c, elements 16 w + 4 g .. + 3 of the swizzled tiles
+        const int by = (16 * w + 4 * g) * (int)sizeof(T), t = 16 * bb + c;
+        const T* r0 = sVW + t * D + ((((by >> 4) ^ (t & (NC - 1))) << 4) | (by & 15)) / (int)sizeof(T);
+        vq = Qd::ld(r0);
+        wxq = Qd::ld(r0 + WB * D);
+      }
+      z = Qd::mma16(wxq, fI, z);                       // + wx, moved into this layout
+      const f32x4 vv = Qd::mma16(vq, fI, zero4());
       for (int e = 0; e < 4; ++e) wv[bb][e] = sigmoid_f(z[e]) * vv[e];
     }
     {
@@ -492,6 +530,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
 #undef CARVE_PREFETCH_G
 #undef CARVE_PREFETCH_VW
 #undef CARVE_STORE_S
+#undef CARVE_STAGE_VW
 #undef CARVE_STAGE_ROWS
 }
 

@@ -105,12 +105,16 @@ __host__ __device__ constexpr RecLds rec_lds() {
 // state while the fold reads it, then the block's raw erase logits (Bx) and the
 // decayed keys Kt; Ki holds the block's raw keys until the gates turn them
 // into Ki in place.
+// With VW (when the layout still fits), VW holds the block's value-side token
+// tiles (v, wx: WB rows each, unpadded, 16-byte chunks XOR-swizzled by row) from
+// the first barrier of a block to its gates; it overlays A .. TmT, which are
+// written only after the gates.  Without VW those tiles are read per wave.
 struct ChainLds {
-  size_t U, X, Kt, Bx, Ki, F, Q, Tau, A, P, AdT, TmT, Rho, Beta, total;
+  size_t U, X, Kt, Bx, Ki, F, Q, Tau, A, P, AdT, TmT, VW, Rho, Beta, total;
 };
 
-template <typename T, int D, int WB, int RP>
-__host__ __device__ constexpr ChainLds chain_lds() {
+template <typename T, int D, int WB, int RP, bool VW>
+__host__ __device__ constexpr ChainLds chain_lds_v() {
   ChainLds l{};
   const size_t e = sizeof(T);
   constexpr size_t NB = WB / 16;
@@ -129,10 +133,23 @@ __host__ __device__ constexpr ChainLds chain_lds() {
   l.P = off;    off += lds_round(WB * LDW * e);
   l.AdT = off;  off += lds_round(NB * 16 * 20 * 4);
   l.TmT = off;  off += lds_round(NB * 16 * LDB * e);
+  l.VW = l.A;
+  if (VW) off = lds_max(off, l.VW + lds_round(2 * WB * (size_t)D * e));
   l.Rho = off;  off += lds_round(D * 4);
   l.Beta = off; off += lds_round(2 * WB * 4);
   l.total = off;
   return l;
+}
+
+// whether the value-side tiles are staged (the layout with VW fits)
+template <typename T, int D, int WB, int RP>
+__host__ __device__ constexpr bool chain_stage_vw() {
+  return chain_lds_v<T, D, WB, RP, true>().total <= kMaxLdsBytes;
+}
+
+template <typename T, int D, int WB, int RP>
+__host__ __device__ constexpr ChainLds chain_lds() {
+  return chain_lds_v<T, D, WB, RP, chain_stage_vw<T, D, WB, RP>()>();
 }
 
 // forward of the whole sequence (one workgroup per (batch, head)), WY blocks of WB tokens
