@@ -449,11 +449,16 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       }
     } else {
       // off-diagonal tiles of -A and all tiles of P, stored [t][s]; a scalar
-      // loop over this wave's tiles (addresses from opaque lane coordinates)
+      // loop over this wave's tiles (addresses from opaque lane coordinates).
+      // With 8 waves, waves w and w + 4 share a SIMD; the T-wave's partner
+      // takes no tiles, so the substitution gets its SIMD's issue slots.
       int ct = c, gt = g;
       asm volatile("" : "+v"(ct), "+v"(gt));
+      constexpr int NWK = NW == 8 ? NW - 2 : NW - 1;        // tile workers
+      const int wk = (NW == 8 && w > TW - 4) ? w - 1 : w;   // worker index
+      const int xend = (NW == 8 && w == TW - 4) ? 0 : NTA + NTP;
 #pragma unroll 1
-      for (int x = w; x < NTA + NTP; x += TW) {
+      for (int x = wk; x < xend; x += NWK) {
         const bool isA = x < NTA;
         const int y = isA ? x : x - NTA;
         const int i = tri_row(y, isA), j = tri_col(y, isA);
