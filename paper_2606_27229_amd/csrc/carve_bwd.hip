@@ -134,6 +134,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   T* sdzb = reinterpret_cast<T*>(smem + lay.dzb);    // [16][LDD]    dz_b[t][j]
   T* sdY = reinterpret_cast<T*>(smem + lay.dY);      // [16][LDR]    dY[t][r]
   T* sStg = reinterpret_cast<T*>(smem + lay.Stage);  // [6][16][D]   token tiles, swizzled
+  float* sGs = reinterpret_cast<float*>(smem + lay.Stage + lds_round(6 * 16 * D * sizeof(T)));  // [16][D] g
 
   const size_t bh0 = ((size_t)b * Tn * H + h) * D;
   const size_t bh1 = (size_t)b * Tn * H + h;
@@ -194,6 +195,9 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   constexpr int NSTG = (NSV + NT - 1) / NT;      // per thread
   static_assert((16 * NC) % 64 == 0 || NSV % NT == 0, "tile index uniform per wave");
   u32x4 pstg[NSTG];
+  // g of a block: 16 rows of D floats, one 16-byte vector per thread
+  constexpr int NGC = D / 4;                     // 16-byte chunks per g row
+  static_assert(16 * NGC == NT, "one g vector per thread");
   quad ptm, ppm, psbq[NJT];
   f32x4 pgam, pg;
   T pbeta = (T)0.0f;
@@ -233,7 +237,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       const T* src_ = s_ == 0 ? k : s_ == 1 ? q : s_ == 2 ? bx : s_ == 3 ? v : s_ == 4 ? wx : dO; \
       pstg[u_] = *reinterpret_cast<const u32x4*>(src_ + (tb_ + t_) * rs + k_ * VEC);           \
     }                                                                                         \
-    pg = *reinterpret_cast<const f32x4*>(gl + e_);                                            \
+    pg = *reinterpret_cast<const f32x4*>(gl + (tb_ + tid / NGC) * rs + 4 * (tid % NGC));      \
+    (void)e_;                                                                                 \
   } while (0)
 #define CARVE_BWD_LOADF(CH_)                                                                  \
   do {                                                                                        \
@@ -319,7 +324,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       for (int jt = 0; jt < NJT; ++jt) sbq[jt] = psbq[jt];
       u32x4 lstg[NSTG];
       for (int u = 0; u < NSTG; ++u) lstg[u] = pstg[u];
-      const f32x4 lg = pg;
+      const f32x4 lg_row = pg;   // a row vector of g (staged below)
       if (bc == nbc - 1) {
         // first block of a chunk in reverse order: the chunk's F into LDS (the
         // previous chunk's last read of sF was before its glue barriers)
@@ -362,12 +367,18 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         const int s_ = x / (16 * NC), t = (x / NC) % 16, kk = x % NC;
         *reinterpret_cast<u32x4*>(sStg + (s_ * 16 + t) * D + (kk ^ (t & (NC - 1))) * VEC) = lstg[u];
       }
+      {
+        const int t = tid / NGC, kk = tid % NGC;
+        *reinterpret_cast<f32x4*>(sGs + t * D + 4 * (kk ^ (t & (NGC - 1)))) = lg_row;
+      }
       __syncthreads();
       // this wave's quads of the token tiles (row t = c, elements 16 w + 4 g ..
       // + 3) and of tau_b; read before the barrier that ends this step, so the
       // value-side step may overwrite the staging region
       quad kq, qq, lbx, vq, wxq, dOq, ltq[NRB];
+      f32x4 lg;
       {
+        lg = *reinterpret_cast<const f32x4*>(sGs + c * D + 4 * ((4 * w + g) ^ (c & (NGC - 1))));
         const int by = (16 * w + 4 * g) * (int)sizeof(T);
         const int off = ((((by >> 4) ^ (c & (NC - 1))) << 4) | (by & 15)) / (int)sizeof(T);
         const T* r0 = sStg + c * D + off;
@@ -619,14 +630,15 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
     // d[Ub; Uw] += dF S_hat^T (carve_bwd_uparam_kernel).  dF enters the product
     // as a high and a low part so that its f32 accumulation is not rounded away.
     {
-      T* sdFh = sdSx;               // [D][LDR]: dF[r][j] stored at (j, r)
-      T* sdFl = sdSx + D * LDR;     // [D][LDR]: dF - (dF rounded)
+      constexpr int LDF = R2 + 4;   // row stride of the dF parts (LDS layout)
+      T* sdFh = sdSx;               // [D][LDF]: dF[r][j] stored at (j, r)
+      T* sdFl = sdSx + D * LDF;     // [D][LDF]: dF - (dF rounded)
       float* dFr = reinterpret_cast<float*>(const_cast<char*>(rc) + cr.dF);
       __syncthreads();  // every wave is done with sdSx and sdY of the last block
       for (int rt = 0; rt < NRT; ++rt) {
         const quad hi = Qd::cvt(dF[rt]);
-        Qd::st(sdFh + (16 * w + c) * LDR + 16 * rt + 4 * g, hi);
-        Qd::st(sdFl + (16 * w + c) * LDR + 16 * rt + 4 * g, Qd::cvt(dF[rt] - Qd::f32(hi)));
+        Qd::st(sdFh + (16 * w + c) * LDF + 16 * rt + 4 * g, hi);
+        Qd::st(sdFl + (16 * w + c) * LDF + 16 * rt + 4 * g, Qd::cvt(dF[rt] - Qd::f32(hi)));
         // dF parked as [j][r] (a lane holds four consecutive r of one j: one
         // 16-byte store per tile); the d[Ub; Uw] kernel transposes it in LDS
         *reinterpret_cast<f32x4*>(dFr + (size_t)(16 * w + c) * R2 + 16 * rt + 4 * g) = dF[rt];
@@ -637,7 +649,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         CARVE_SEQ();
         f32x4 acc = dSt[jt];
         for (int rp = 0; rp < R2 / 32; ++rp) {
-          const int o = (16 * jt + c) * LDR + 32 * rp + 4 * g;
+          const int o = (16 * jt + c) * LDF + 32 * rp + 4 * g;
           acc = Qd::mma32(Qd::ld(sdFh + o), Qd::ld(sdFh + o + 16), fU[2 * rp], fU[2 * rp + 1], acc);
           acc = Qd::mma32(Qd::ld(sdFl + o), Qd::ld(sdFl + o + 16), fU[2 * rp], fU[2 * rp + 1], acc);
         }

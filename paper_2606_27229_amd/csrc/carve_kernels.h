@@ -181,8 +181,10 @@ constexpr int kUSplit = 16;
 // LDS layout of the adjoint kernel (one 16-token block at a time).  The four
 // [value][token] exchange buffers dOT .. dzwT are dead between the end of one
 // block and the value-side step of the next; the block's token tiles (k, q, bx,
-// v, wx, dO: 16 rows each, unpadded, 16-byte chunks XOR-swizzled by row) are
-// staged there (Stage), so the region is at least 6 * 16 * D elements.
+// v, wx, dO in the token dtype, then g in f32: 16 rows each, unpadded, 16-byte
+// chunks XOR-swizzled by row) are staged there (Stage), so the region holds at
+// least 6 * 16 * D elements plus 16 * D floats.  At a chunk start the glue
+// reuses dSx for dF as a high and a low part ([D][LDF] each).
 struct BwdLds {
   size_t F, VbT, VwT, Tau, Tm, P, Gam, Beta, Dbeta, Kt, Qt, Ki, Sx, dSx, dOT, uT, dRT, dzwT, Stage, dzb, dY, total;
 };
@@ -208,13 +210,14 @@ __host__ __device__ constexpr BwdLds bwd_lds() {
   l.Qt = off;    off += lds_round(16 * LDD * e);
   l.Ki = off;    off += lds_round(16 * LDD * e);
   l.Sx = off;    off += lds_round(D * LDD * e);
-  l.dSx = off;   off += lds_round(D * lds_max(LDD, 2 * LDR) * e);
+  constexpr size_t LDF = 2 * RP + 4;
+  l.dSx = off;   off += lds_round(D * lds_max(LDD, 2 * LDF) * e);
   l.Stage = off;
   l.dOT = off;   off += lds_round(D * LDB * e);
   l.uT = off;    off += lds_round(D * LDB * e);
   l.dRT = off;   off += lds_round(D * LDB * e);
   l.dzwT = off;  off += lds_round(D * LDB * e);
-  off = lds_max(off, l.Stage + lds_round(6 * 16 * D * e));
+  off = lds_max(off, l.Stage + lds_round(6 * 16 * D * e) + lds_round(16 * D * 4));
   l.dzb = off;   off += lds_round(16 * LDD * e);
   l.dY = off;    off += lds_round(16 * LDR * e);
   l.total = off;
