@@ -727,3 +727,55 @@ int cref_bwd(const cref_dims* d, const double* q, const double* k, const double*
   free(a.pUb); free(a.pUw); free(a.pVb); free(a.pVw);
   return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* key-axis decay gate computed from its raw logit (Sec. decay_gate)        */
+/* ------------------------------------------------------------------------ */
+
+/* g = -exp(A) * softplus(f + tau) per key channel (Eq. decay_gate), with the
+ * learned log-amplitudes A and biases tau of head h shared by every token. */
+int cref_decay_gate(const cref_dims* d, const double* f, const double* A, const double* tau, double* g) {
+  int st = check_dims(d);
+  if (st) return st;
+  if (!f || !A || !tau || !g) return -1;
+  for (int b = 0; b < d->B; ++b)
+    for (int t = 0; t < d->T; ++t)
+      for (int h = 0; h < d->H; ++h) {
+        const size_t r = row(d, b, t, h) * d->Dk;
+        for (int j = 0; j < d->Dk; ++j) {
+          const size_t p = (size_t)h * d->Dk + j;
+          g[r + j] = -exp(A[p]) * softplus(f[r + j] + tau[p]);
+        }
+      }
+  return 0;
+}
+
+/* Reverse mode of cref_decay_gate for an incoming gradient dg:
+ *   dg/df = dg/dtau = -exp(A) * sigmoid(f + tau)   (d softplus(z)/dz = sigmoid(z))
+ *   dg/dA = g
+ * df is per token; dA and dtau are summed over batch and tokens in the
+ * order b, t (overwritten, not accumulated). */
+int cref_decay_gate_bwd(const cref_dims* d, const double* f, const double* A, const double* tau,
+                        const double* dg, double* df, double* dA, double* dtau) {
+  int st = check_dims(d);
+  if (st) return st;
+  if (!f || !A || !tau || !dg || !df || !dA || !dtau) return -1;
+  const size_t np = (size_t)d->H * d->Dk;
+  for (size_t p = 0; p < np; ++p) dA[p] = dtau[p] = 0.0;
+  for (int b = 0; b < d->B; ++b)
+    for (int t = 0; t < d->T; ++t)
+      for (int h = 0; h < d->H; ++h) {
+        const size_t r = row(d, b, t, h) * d->Dk;
+        for (int j = 0; j < d->Dk; ++j) {
+          const size_t p = (size_t)h * d->Dk + j;
+          const double z = f[r + j] + tau[p];
+          const double ea = exp(A[p]);
+          const double g = -ea * softplus(z);
+          const double dfz = dg[r + j] * (-ea * sigm(z));
+          df[r + j] = dfz;
+          dtau[p] += dfz;
+          dA[p] += dg[r + j] * g;
+        }
+      }
+  return 0;
+}

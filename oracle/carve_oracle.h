@@ -66,6 +66,16 @@ int cref_bwd(const cref_dims* d, const double* q, const double* k, const double*
              double* dbx, double* dwx, double* dUb, double* dUw, double* dVb,
              double* dVw, double* dS0, int nthreads);
 
+/* Key-axis decay gate from its raw logit (Sec. decay_gate, Eq. decay_gate):
+ * g[b,t,h,j] = -exp(A[h][j]) * softplus(f[b,t,h,j] + tau[h][j]).
+ * f, g : [B, T, H, Dk];  A, tau : [H, Dk]. */
+int cref_decay_gate(const cref_dims* d, const double* f, const double* A, const double* tau, double* g);
+
+/* Its reverse mode: df [B,T,H,Dk] = dg * (-exp(A) sigmoid(f + tau));
+ * dA [H,Dk] = sum over b, t of dg * g;  dtau [H,Dk] = sum over b, t of df. */
+int cref_decay_gate_bwd(const cref_dims* d, const double* f, const double* A, const double* tau,
+                        const double* dg, double* df, double* dA, double* dtau);
+
 #ifdef __cplusplus
 }
 #endif

@@ -51,7 +51,10 @@ def _load():
     lib.cref_fwd_chunked.argtypes = [D] + [P] * 17 + [ctypes.c_int]
     lib.cref_baseline_fwd.argtypes = [D] + [P] * 10 + [ctypes.c_int]
     lib.cref_bwd.argtypes = [D] + [P] * 26 + [ctypes.c_int]
-    for f in (lib.cref_fwd_serial, lib.cref_fwd_chunked, lib.cref_baseline_fwd, lib.cref_bwd):
+    lib.cref_decay_gate.argtypes = [D] + [P] * 4
+    lib.cref_decay_gate_bwd.argtypes = [D] + [P] * 7
+    for f in (lib.cref_fwd_serial, lib.cref_fwd_chunked, lib.cref_baseline_fwd, lib.cref_bwd,
+              lib.cref_decay_gate, lib.cref_decay_gate_bwd):
         f.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -155,4 +158,49 @@ def bwd(inp, L, dO, dS_T=None, nthreads=None):
                                                "dUb", "dUw", "dVb", "dVw", "dS0")],
                       nthreads if nthreads else default_threads())
     _check(st, "cref_bwd")
+    return out
+
+
+def decay_gate(f, A, tau, L=1):
+    """g = -exp(A) * softplus(f + tau) (Eq. decay_gate); f [B,T,H,Dk], A and tau [H,Dk]."""
+    lib = _load()
+    f = _f64(f)
+    B, T, H, Dk = f.shape
+    d = _Dims(B, T, H, Dk, Dk, 1, L)
+    g = np.zeros_like(f)
+    _check(lib.cref_decay_gate(ctypes.byref(d), _ptr(f), _ptr(_f64(A)), _ptr(_f64(tau)), _ptr(g)), "cref_decay_gate")
+    return g
+
+
+def decay_gate_bwd(f, A, tau, dg):
+    """Reverse mode of ``decay_gate``: returns (df, dA, dtau)."""
+    lib = _load()
+    f = _f64(f)
+    B, T, H, Dk = f.shape
+    d = _Dims(B, T, H, Dk, Dk, 1, 1)
+    df = np.zeros_like(f)
+    dA = np.zeros((H, Dk))
+    dtau = np.zeros((H, Dk))
+    _check(lib.cref_decay_gate_bwd(ctypes.byref(d), _ptr(f), _ptr(_f64(A)), _ptr(_f64(tau)), _ptr(_f64(dg)),
+                                   _ptr(df), _ptr(dA), _ptr(dtau)), "cref_decay_gate_bwd")
+    return df, dA, dtau
+
+
+def _with_gate(inp):
+    """The ungated inputs of the gated layer: g from (f, A, tau) by Eq. decay_gate."""
+    out = dict(inp)
+    out["g"] = decay_gate(inp["f"], inp["A"], inp["tau_f"])
+    return out
+
+
+def fwd_gated(inp, L, want_chunks=False, nthreads=None):
+    """The layer with the decay gate computed from its raw logit f (Sec. decay_gate)."""
+    return fwd_serial(_with_gate(inp), L, want_chunks=want_chunks, nthreads=nthreads)
+
+
+def bwd_gated(inp, L, dO, dS_T=None, nthreads=None):
+    """Reverse mode of ``fwd_gated``: the gradients of ``bwd`` with dg replaced by
+    df, dA, dtau (chain rule through Eq. decay_gate)."""
+    out = bwd(_with_gate(inp), L, dO, dS_T, nthreads=nthreads)
+    out["df"], out["dA"], out["dtau"] = decay_gate_bwd(inp["f"], inp["A"], inp["tau_f"], out.pop("dg"))
     return out

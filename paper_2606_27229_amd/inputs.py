@@ -15,6 +15,13 @@ Recipe (distributions of the paper's 1.3B-scale layer inputs, Sec. 4.1):
   Vb     ~ N(0, s_u^2) of shape [Dk, R], Vw of shape [Dv, R]
   S0     = 0, or N(0, s0^2) of shape [B, H, Dv, Dk]
   dO     ~ N(0,1) of shape [B, T, H, Dv];  dS_T = 0 unless asked for
+With the decay gate computed from its raw logit (gated=True; Sec. decay_gate,
+g = -exp(A) softplus(f + tau_f)) three more arrays are drawn after the others
+(so every other array is unchanged) and g is left out:
+  f      ~ N(0,1) of shape [B, T, H, Dk]         token dtype
+  A      ~ N(0, 0.1^2) of shape [H, Dk]          f32 log-amplitudes
+  tau_f  ~ N(-mu, 0.1^2) of shape [H, Dk]        f32 biases
+so that f + tau_f ~ N(-mu, 1.01) and g is close in law to logsigmoid(N(mu,1)).
 Token tensors of a bf16 workload are rounded to bf16 (round to nearest even)
 and the rounded values are what every consumer receives; g, the parameters
 and the states stay f32.
@@ -105,11 +112,12 @@ def _logsigmoid(x):
 
 
 def make_inputs(w: Workload, seed: int = 0, *, zero_content: bool = False,
-                dS_T: bool = False, bx_mean: float | None = None) -> dict:
+                dS_T: bool = False, bx_mean: float | None = None, gated: bool = False) -> dict:
     """Draw one seeded input set for workload ``w``.
 
     zero_content: Ub = Uw = 0 (the memory-blind special case).
     bx_mean:      override the erase-logit location (erase-heavy stress uses 0).
+    gated:        raw decay logits f with per-head A, tau_f instead of g.
     """
     rng = np.random.Generator(np.random.PCG64(seed))
     B, T, H, Dk, Dv, R = w.B, w.T, w.H, w.Dk, w.Dv, w.R
@@ -132,5 +140,12 @@ def make_inputs(w: Workload, seed: int = 0, *, zero_content: bool = False,
     dST = _normal(rng, (B, H, Dv, Dk)) if dS_T else None
     if w.dtype == "bf16":
         q, k, v, beta, bx, wx, dO = (round_bf16(a) for a in (q, k, v, beta, bx, wx, dO))
-    return {"q": q, "k": k, "v": v, "beta": beta, "g": g, "bx": bx, "wx": wx,
-            "Ub": Ub, "Uw": Uw, "Vb": Vb, "Vw": Vw, "S0": S0, "dO": dO, "dS_T": dST}
+    out = {"q": q, "k": k, "v": v, "beta": beta, "g": g, "bx": bx, "wx": wx,
+           "Ub": Ub, "Uw": Uw, "Vb": Vb, "Vw": Vw, "S0": S0, "dO": dO, "dS_T": dST}
+    if gated:
+        f = _normal(rng, (B, T, H, Dk))
+        out["A"] = _normal(rng, (H, Dk), std=0.1)
+        out["tau_f"] = _normal(rng, (H, Dk), std=0.1, mean=-w.mu)
+        out["f"] = round_bf16(f) if w.dtype == "bf16" else f
+        out["g"] = None
+    return out

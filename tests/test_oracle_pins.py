@@ -380,3 +380,87 @@ def test_oracle_rejects_bad_shapes():
     inp = make_inputs(w, seed=0)
     with pytest.raises(ValueError):
         orc.fwd_serial(inp, 16)
+
+
+# --------------------------------------------------------------------------
+# decay gate computed from its raw logit (Sec. decay_gate, Eq. decay_gate:
+# g = -exp(A) softplus(f + tau), A and tau per head and key channel)
+# --------------------------------------------------------------------------
+def _gated(w, seed, **kw):
+    return _f64(make_inputs(w, seed=seed, gated=True, **kw))
+
+
+def test_decay_gate_special_values():
+    """softplus(0) = log 2, softplus(z) -> z for large z and -> e^z for very
+    negative z; A = 0 leaves -softplus; the values are checked against numpy's
+    logaddexp(0, z) = log(1 + e^z)."""
+    w = _small(B=1, H=2, T=16, Dk=8)
+    inp = _gated(w, 3)
+    f, A, tau = inp["f"], inp["A"], inp["tau_f"]
+    g = orc.decay_gate(f, A, tau)
+    ref = -np.exp(A)[None, None] * np.logaddexp(0.0, f + tau[None, None])
+    assert _rel(g, ref) < 1e-14
+    assert np.all(g < 0)
+    # f + tau = 0: g = -e^A log 2 exactly up to rounding
+    g0 = orc.decay_gate(-np.broadcast_to(tau, f.shape), A, tau)
+    assert _rel(g0, -np.exp(A)[None, None] * np.log(2.0) * np.ones_like(f)) < 1e-15
+    # large argument: softplus(z) = z + log1p(e^-z)
+    z = np.full_like(f, 40.0)
+    assert _rel(orc.decay_gate(z - tau, np.zeros_like(A), tau), -z) < 1e-15
+    # very negative argument: softplus(z) = e^z to relative 1e-16
+    assert _rel(orc.decay_gate(np.full_like(f, -40.0) - tau, np.zeros_like(A), tau),
+                -np.exp(np.full_like(f, -40.0))) < 1e-12
+
+
+def test_gated_layer_equals_layer_with_activated_decay():
+    """The gated layer is the layer of Eq. carve_state with g from Eq. decay_gate
+    (the activation evaluated here with numpy's logaddexp)."""
+    w = _small(T=64)
+    inp = _gated(w, 11)
+    x = dict(inp)
+    x["g"] = -np.exp(inp["A"])[None, None] * np.logaddexp(0.0, inp["f"] + inp["tau_f"][None, None])
+    a = orc.fwd_gated(inp, 16)
+    b = orc.fwd_serial(x, 16)
+    assert _rel(a["o"], b["o"]) < 1e-13 and _rel(a["S_T"], b["S_T"]) < 1e-13
+
+
+GATED_GRADS = [("f", "df"), ("A", "dA"), ("tau_f", "dtau"), ("q", "dq"), ("bx", "dbx"), ("Ub", "dUb")]
+
+
+def _gated_loss(x, L):
+    o = orc.fwd_gated(x, L)
+    return float(np.sum(o["o"] * x["dO"]) + np.sum(o["S_T"] * x["dS_T"]))
+
+
+@pytest.mark.parametrize("L,T,Dk,Dv,R", [(8, 32, 8, 6, 3), (4, 16, 5, 7, 2)])
+def test_gated_backward_directional_finite_differences(L, T, Dk, Dv, R):
+    """df, dA, dtau (the chain rule through Eq. decay_gate, reduced over batch
+    and tokens for A and tau) against central differences of the loss."""
+    w = Workload("fd", B=2, H=2, T=T, Dk=Dk, Dv=Dv, L=L, R=R, dtype="f32", mu=1.0, s0=0.3, u_std=0.4)
+    inp = _gated(w, L + Dk, dS_T=True)
+    gr = orc.bwd_gated(inp, L, inp["dO"], inp["dS_T"])
+    assert "dg" not in gr
+    rng = np.random.default_rng(L)
+    h = 1e-6
+    for name, gname in GATED_GRADS:
+        dirn = rng.standard_normal(inp[name].shape)
+        xp = dict(inp); xp[name] = inp[name] + h * dirn
+        xm = dict(inp); xm[name] = inp[name] - h * dirn
+        fd = (_gated_loss(xp, L) - _gated_loss(xm, L)) / (2 * h)
+        an = float(np.sum(gr[gname] * dirn))
+        assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-3), (name, fd, an)
+
+
+def test_gated_backward_coordinates_of_A_and_tau():
+    """Every coordinate of dA and dtau against central differences."""
+    w = Workload("fd", B=2, H=2, T=12, Dk=3, Dv=4, L=4, R=2, dtype="f32", mu=1.0, s0=0.2, u_std=0.5)
+    inp = _gated(w, 5, dS_T=True)
+    gr = orc.bwd_gated(inp, 4, inp["dO"], inp["dS_T"])
+    h = 1e-6
+    for name, gname in (("A", "dA"), ("tau_f", "dtau")):
+        for idx in range(inp[name].size):
+            xp = dict(inp); xp[name] = inp[name].copy(); xp[name].reshape(-1)[idx] += h
+            xm = dict(inp); xm[name] = inp[name].copy(); xm[name].reshape(-1)[idx] -= h
+            fd = (_gated_loss(xp, 4) - _gated_loss(xm, 4)) / (2 * h)
+            an = gr[gname].reshape(-1)[idx]
+            assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-2), (name, idx, fd, an)
