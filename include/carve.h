@@ -91,7 +91,7 @@ enum {
  * dims that fail validation.  The workspace holds the per-chunk records of
  * the recompute (fold, tau, WY factors and block start states), the partial
  * parameter gradients and the chunk ready flags of the fused recompute +
- * adjoint launch. */
+ * adjoint launch (the same size for the gated backward). */
 size_t carve_workspace_size(const carve_dims_t* d, int for_backward);
 
 /* Forward (Alg. carve_fwd with the WY solve of Alg. WYChunkDelta).
@@ -124,12 +124,43 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
                     float* dUw, float* dVb, float* dVw, float* dS0, void* workspace,
                     size_t workspace_bytes, hipStream_t stream);
 
+/* The same layer with the key-axis decay computed from its raw logit inside
+ * the kernels (Sec. decay_gate, Eq. decay_gate: "gate-in-kernel" fusion):
+ *     g[b,t,h,j] = -exp(A[h][j]) * softplus(f[b,t,h,j] + tau_f[h][j])
+ * In:  f [B,T,H,Dk] in the call's dtype (the raw decay logit, replacing g);
+ *      A, tau_f [H,Dk] f32: learned log-amplitudes and biases of the gate
+ *      (tau_f is the bias the paper calls tau in Eq. decay_gate, not the
+ *      content read-out tau of Eq. content_readout); the other arguments are
+ *      those of carve_chunk_fwd.  g is never materialised.
+ * The numerical-range precondition applies to the g so formed. */
+int carve_chunk_fwd_gated(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                          const void* beta, const void* f, const float* A, const float* tau_f,
+                          const void* bx, const void* wx, const float* Ub, const float* Uw,
+                          const float* Vb, const float* Vw, const float* S0, void* o, float* S_T,
+                          float* S_chunks, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Backward of carve_chunk_fwd_gated for loss <dO, o> + <dS_T, S_T>.  Outputs
+ * as carve_chunk_bwd, with dg replaced by:
+ *   df [B,T,H,Dk] in the call's dtype: dL/df = dL/dg * (-exp(A)) * sigmoid(f + tau_f);
+ *   dA, dtau [H,Dk] f32: sums over batch and tokens of dL/dg * g and of dL/df,
+ *   reduced in a fixed order (bitwise-reproducible reruns).
+ * The workspace is the one carve_workspace_size(d, 1) reports. */
+int carve_chunk_bwd_gated(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                          const void* beta, const void* f, const float* A, const float* tau_f,
+                          const void* bx, const void* wx, const float* Ub, const float* Uw,
+                          const float* Vb, const float* Vw, const float* S_chunks, const void* dO,
+                          const float* dS_T, void* dq, void* dk, void* dv, void* dbeta, void* df,
+                          float* dA, float* dtau, void* dbx, void* dwx, float* dUb, float* dUw,
+                          float* dVb, float* dVw, float* dS0, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream);
+
 /* Measurement hook (not part of the computation).  Arms the next
  * carve_chunk_fwd / carve_chunk_bwd call made on the calling thread to record
  * events[0] on its stream before its first kernel launch and events[i] after
  * its i-th launch (the forward makes 1 launch; the backward 6: clear of the
  * chunk ready flags, chunk recompute fused with the adjoint, dVb/dVw
- * partials, d[Ub;Uw] partials, two fixed-order reductions),
+ * partials, d[Ub;Uw] partials, two fixed-order reductions; the gated backward
+ * a 7th, the reduction of dA, dtau over the batch),
  * up to `capacity` events.  `events` are hipEvent_t handles created by the
  * caller (hipEventCreate) and owned by the caller; the handles are copied
  * here (the array may be freed after this call) and the events are only

@@ -18,7 +18,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // partials per (b,h, token split) | chunk records of the recompute | ready
 // flags and ticket counter of the fused recompute + adjoint launch
 struct BwdWs {
-  size_t part, partV, rec, sync, total;
+  size_t part, partV, rec, sync, partG, total;
 };
 
 BwdWs bwd_workspace_layout(const carve_dims_t* d) {
@@ -31,6 +31,7 @@ BwdWs bwd_workspace_layout(const carve_dims_t* d) {
   l.partV = off; off += align256(nbh * kVSplit * part_floats(d->R, d->Dk) * 4);
   l.rec = off;   off += align256(nbh * nch * chunk_rec(es, d->Dk, d->L, round_rp(d->R)).total);
   l.sync = off;  off += align256(sync_ints(nbh, nch) * sizeof(int));
+  l.partG = off; off += align256(nbh * 2 * (size_t)d->Dk * 4);   // dA, dtau partials (gated)
   l.total = off;
   return l;
 }
@@ -158,59 +159,80 @@ size_t carve_workspace_size(const carve_dims_t* d, int for_backward) {
   return bwd_workspace_layout(d).total;
 }
 
-int carve_chunk_fwd(const carve_dims_t* d, const void* q, const void* k, const void* v,
-                    const void* beta, const float* g, const void* bx, const void* wx,
-                    const float* Ub, const float* Uw, const float* Vb, const float* Vw,
-                    const float* S0, void* o, float* S_T, float* S_chunks, void* workspace,
-                    size_t workspace_bytes, hipStream_t stream) {
-  (void)workspace;
-  (void)workspace_bytes;
+}  // extern "C"
+
+namespace {
+
+// the decay input: g itself, or its raw logit f with A, tau_f (Eq. decay_gate)
+struct Decay {
+  const float* g;
+  const void* f;
+  const float *A, *tau_f;
+  bool gated() const { return f != nullptr; }
+};
+
+int fwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v, const void* beta,
+             const Decay& dc, const void* bx, const void* wx, const float* Ub, const float* Uw,
+             const float* Vb, const float* Vw, const float* S0, void* o, float* S_T, float* S_chunks,
+             hipStream_t stream) {
   ProfClear pc;
   int st = check_dims(d);
   if (st) return st;
-  if (!q || !k || !v || !beta || !g || !bx || !wx || !Ub || !Uw || !Vb || !Vw || !o) return CARVE_ERR_NULL;
-  const void* ptrs[] = {q, k, v, beta, g, bx, wx, Ub, Uw, Vb, Vw, S0, o, S_T, S_chunks};
+  if (!q || !k || !v || !beta || !bx || !wx || !Ub || !Uw || !Vb || !Vw || !o) return CARVE_ERR_NULL;
+  if (dc.gated() ? (!dc.A || !dc.tau_f) : !dc.g) return CARVE_ERR_NULL;
+  const void* ptrs[] = {q, k, v, beta, dc.g, dc.f, dc.A, dc.tau_f, bx, wx, Ub, Uw, Vb, Vw, S0, o, S_T, S_chunks};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return CARVE_ERR_ALIGN;
   const size_t es = esize(d->dtype);
   const size_t ntok = (size_t)d->B * d->T * d->H;
   const size_t nst = (size_t)d->B * d->H * d->Dv * d->Dk;
+  const size_t HD = (size_t)d->H * d->Dk * 4;
   const Range ins[] = {{q, ntok * d->Dk * es}, {k, ntok * d->Dk * es}, {v, ntok * d->Dv * es},
-                       {beta, ntok * es}, {g, ntok * d->Dk * 4}, {bx, ntok * d->Dk * es},
+                       {beta, ntok * es}, {dc.g, ntok * d->Dk * 4}, {dc.f, ntok * d->Dk * es},
+                       {dc.A, HD}, {dc.tau_f, HD}, {bx, ntok * d->Dk * es},
                        {wx, ntok * d->Dv * es}, {Ub, (size_t)d->R * d->Dv * 4},
                        {Uw, (size_t)d->R * d->Dv * 4}, {Vb, (size_t)d->Dk * d->R * 4},
                        {Vw, (size_t)d->Dv * d->R * 4}, {S0, nst * 4}};
   const Range outs[] = {{o, ntok * d->Dv * es}, {S_T, nst * 4}, {S_chunks, nst * (d->T / d->L) * 4}};
-  if (any_overlap(outs, 3, ins, 12)) return CARVE_ERR_UNSUPPORTED;
+  if (any_overlap(outs, 3, ins, 15)) return CARVE_ERR_UNSUPPORTED;
   const int wb = pick_wb(d);
   if (!wb) return CARVE_ERR_UNSUPPORTED;
   FwdArgs a;
   a.q = q; a.k = k; a.v = v; a.beta = beta; a.bx = bx; a.wx = wx;
-  a.g = g; a.Ub = Ub; a.Uw = Uw; a.Vb = Vb; a.Vw = Vw; a.S0 = S0;
+  a.g = dc.g; a.Ub = Ub; a.Uw = Uw; a.Vb = Vb; a.Vw = Vw; a.S0 = S0;
+  a.f = dc.f; a.A = dc.A; a.tau_f = dc.tau_f;
   a.o = o; a.S_T = S_T; a.S_chunks = S_chunks;
   a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = round_rp(d->R); a.L = d->L;
   a.rec = nullptr;
   prof_mark(stream);
-  st = launch_chain_fwd(a, d->dtype, d->Dk, wb, stream);
+  st = launch_chain_fwd(a, d->dtype, d->Dk, wb, dc.gated(), stream);
   prof_mark(stream);
   return st;
 }
 
-int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const void* v,
-                    const void* beta, const float* g, const void* bx, const void* wx,
-                    const float* Ub, const float* Uw, const float* Vb, const float* Vw,
-                    const float* S_chunks, const void* dO, const float* dS_T, void* dq, void* dk,
-                    void* dv, void* dbeta, float* dg, void* dbx, void* dwx, float* dUb,
-                    float* dUw, float* dVb, float* dVw, float* dS0, void* workspace,
-                    size_t workspace_bytes, hipStream_t stream) {
+// decay gradient: dg, or df with dA, dtau (gated)
+struct DecayGrad {
+  float* dg;
+  void* df;
+  float *dA, *dtau;
+};
+
+int bwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v, const void* beta,
+             const Decay& dc, const void* bx, const void* wx, const float* Ub, const float* Uw,
+             const float* Vb, const float* Vw, const float* S_chunks, const void* dO, const float* dS_T,
+             void* dq, void* dk, void* dv, void* dbeta, const DecayGrad& dd, void* dbx, void* dwx,
+             float* dUb, float* dUw, float* dVb, float* dVw, float* dS0, void* workspace,
+             size_t workspace_bytes, hipStream_t stream) {
   ProfClear pc;
   int st = check_dims(d);
   if (st) return st;
-  if (!q || !k || !v || !beta || !g || !bx || !wx || !Ub || !Uw || !Vb || !Vw || !S_chunks || !dO ||
-      !dq || !dk || !dv || !dbeta || !dg || !dbx || !dwx || !dUb || !dUw || !dVb || !dVw)
+  if (!q || !k || !v || !beta || !bx || !wx || !Ub || !Uw || !Vb || !Vw || !S_chunks || !dO ||
+      !dq || !dk || !dv || !dbeta || !dbx || !dwx || !dUb || !dUw || !dVb || !dVw)
     return CARVE_ERR_NULL;
-  const void* ptrs[] = {q, k, v, beta, g, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO, dS_T, dq, dk, dv,
-                        dbeta, dg, dbx, dwx, dUb, dUw, dVb, dVw, dS0, workspace};
+  if (dc.gated() ? (!dc.A || !dc.tau_f || !dd.df || !dd.dA || !dd.dtau) : (!dc.g || !dd.dg)) return CARVE_ERR_NULL;
+  const void* ptrs[] = {q, k, v, beta, dc.g, dc.f, dc.A, dc.tau_f, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO, dS_T,
+                        dq, dk, dv, dbeta, dd.dg, dd.df, dd.dA, dd.dtau, dbx, dwx, dUb, dUw, dVb, dVw, dS0,
+                        workspace};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return CARVE_ERR_ALIGN;
   const size_t need = carve_workspace_size(d, 1);
@@ -219,16 +241,19 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
   const size_t ntok = (size_t)d->B * d->T * d->H;
   const size_t nst = (size_t)d->B * d->H * d->Dv * d->Dk;
   const size_t RDv = (size_t)d->R * d->Dv * 4;
+  const size_t HD = (size_t)d->H * d->Dk * 4;
   const Range ins[] = {{q, ntok * d->Dk * es}, {k, ntok * d->Dk * es}, {v, ntok * d->Dv * es},
-                       {beta, ntok * es}, {g, ntok * d->Dk * 4}, {bx, ntok * d->Dk * es},
+                       {beta, ntok * es}, {dc.g, ntok * d->Dk * 4}, {dc.f, ntok * d->Dk * es},
+                       {dc.A, HD}, {dc.tau_f, HD}, {bx, ntok * d->Dk * es},
                        {wx, ntok * d->Dv * es}, {Ub, RDv}, {Uw, RDv}, {Vb, RDv}, {Vw, RDv},
                        {S_chunks, nst * (d->T / d->L) * 4}, {dO, ntok * d->Dv * es},
                        {dS_T, nst * 4}, {workspace, need}};
   const Range outs[] = {{dq, ntok * d->Dk * es}, {dk, ntok * d->Dk * es}, {dv, ntok * d->Dv * es},
-                        {dbeta, ntok * es}, {dg, ntok * d->Dk * 4}, {dbx, ntok * d->Dk * es},
+                        {dbeta, ntok * es}, {dd.dg, ntok * d->Dk * 4}, {dd.df, ntok * d->Dk * es},
+                        {dd.dA, HD}, {dd.dtau, HD}, {dbx, ntok * d->Dk * es},
                         {dwx, ntok * d->Dv * es}, {dUb, RDv}, {dUw, RDv}, {dVb, RDv},
                         {dVw, RDv}, {dS0, nst * 4}};
-  if (any_overlap(outs, 12, ins, 15)) return CARVE_ERR_UNSUPPORTED;
+  if (any_overlap(outs, 15, ins, 18)) return CARVE_ERR_UNSUPPORTED;
   const int lw = pick_lw(d);
   if (!lw) return CARVE_ERR_UNSUPPORTED;
   int cus = 0;
@@ -240,17 +265,21 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
   // 1-2. chunk-parallel recompute -> chunk records, overlapped with the adjoint
   FwdArgs f;
   f.q = q; f.k = k; f.v = v; f.beta = beta; f.bx = bx; f.wx = wx;
-  f.g = g; f.Ub = Ub; f.Uw = Uw; f.Vb = Vb; f.Vw = Vw; f.S0 = nullptr;
+  f.g = dc.g; f.Ub = Ub; f.Uw = Uw; f.Vb = Vb; f.Vw = Vw; f.S0 = nullptr;
+  f.f = dc.f; f.A = dc.A; f.tau_f = dc.tau_f;
   f.o = nullptr; f.S_T = nullptr; f.S_chunks = const_cast<float*>(S_chunks);
   f.rec = wsb + wl.rec;
   f.B = d->B; f.T = d->T; f.H = d->H; f.R = d->R; f.RP = RP; f.L = d->L;
   BwdArgs a;
   a.q = q; a.k = k; a.v = v; a.beta = beta; a.bx = bx; a.wx = wx;
-  a.g = g; a.Ub = Ub; a.Uw = Uw; a.Vb = Vb; a.Vw = Vw; a.S_chunks = S_chunks;
+  a.g = dc.g; a.Ub = Ub; a.Uw = Uw; a.Vb = Vb; a.Vw = Vw; a.S_chunks = S_chunks;
+  a.f = dc.f; a.A = dc.A; a.tau_f = dc.tau_f;
   a.dO = dO; a.dS_T = dS_T;
-  a.dq = dq; a.dk = dk; a.dv = dv; a.dbeta = dbeta; a.dbx = dbx; a.dwx = dwx; a.dg = dg; a.dS0 = dS0;
+  a.dq = dq; a.dk = dk; a.dv = dv; a.dbeta = dbeta; a.dbx = dbx; a.dwx = dwx; a.dg = dd.dg; a.dS0 = dS0;
+  a.df = dd.df;
   a.part = reinterpret_cast<float*>(wsb + wl.part);
   a.partV = reinterpret_cast<float*>(wsb + wl.partV);
+  a.partG = reinterpret_cast<float*>(wsb + wl.partG);
   a.rec = wsb + wl.rec;
   a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = RP; a.L = d->L;
   int* sync = reinterpret_cast<int*>(wsb + wl.sync);
@@ -258,7 +287,7 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
   st = launch_sync_clear(sync, sync_ints((size_t)d->B * d->H, (size_t)(d->T / d->L)), stream);
   if (st) return st;
   prof_mark(stream);
-  st = launch_bwd_fused(f, a, sync, cus, d->dtype, d->Dk, lw, stream);
+  st = launch_bwd_fused(f, a, sync, cus, d->dtype, d->Dk, lw, dc.gated(), stream);
   if (st) return st;
   prof_mark(stream);
   // 3. dVb, dVw from dbx, dwx and tau
@@ -276,8 +305,73 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
   if (st) return st;
   prof_mark(stream);
   st = launch_param_reduce(a.partV, nbh * kVSplit, RD, dVb, dVw, stream);
+  if (st) return st;
   prof_mark(stream);
+  // 6. (gated) dA, dtau summed over the batch
+  if (dc.gated()) {
+    st = launch_gate_reduce(a.partG, d->B, d->H, d->Dk, dd.dA, dd.dtau, stream);
+    prof_mark(stream);
+  }
   return st;
+}
+
+}  // namespace
+
+extern "C" {
+
+int carve_chunk_fwd(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                    const void* beta, const float* g, const void* bx, const void* wx,
+                    const float* Ub, const float* Uw, const float* Vb, const float* Vw,
+                    const float* S0, void* o, float* S_T, float* S_chunks, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  return fwd_impl(d, q, k, v, beta, Decay{g, nullptr, nullptr, nullptr}, bx, wx, Ub, Uw, Vb, Vw, S0, o, S_T,
+                  S_chunks, stream);
+}
+
+int carve_chunk_fwd_gated(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                          const void* beta, const void* f, const float* A, const float* tau_f,
+                          const void* bx, const void* wx, const float* Ub, const float* Uw,
+                          const float* Vb, const float* Vw, const float* S0, void* o, float* S_T,
+                          float* S_chunks, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  if (!f) {
+    ProfClear pc;
+    return CARVE_ERR_NULL;
+  }
+  return fwd_impl(d, q, k, v, beta, Decay{nullptr, f, A, tau_f}, bx, wx, Ub, Uw, Vb, Vw, S0, o, S_T, S_chunks,
+                  stream);
+}
+
+int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                    const void* beta, const float* g, const void* bx, const void* wx,
+                    const float* Ub, const float* Uw, const float* Vb, const float* Vw,
+                    const float* S_chunks, const void* dO, const float* dS_T, void* dq, void* dk,
+                    void* dv, void* dbeta, float* dg, void* dbx, void* dwx, float* dUb,
+                    float* dUw, float* dVb, float* dVw, float* dS0, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream) {
+  return bwd_impl(d, q, k, v, beta, Decay{g, nullptr, nullptr, nullptr}, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO,
+                  dS_T, dq, dk, dv, dbeta, DecayGrad{dg, nullptr, nullptr, nullptr}, dbx, dwx, dUb, dUw, dVb,
+                  dVw, dS0, workspace, workspace_bytes, stream);
+}
+
+int carve_chunk_bwd_gated(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                          const void* beta, const void* f, const float* A, const float* tau_f,
+                          const void* bx, const void* wx, const float* Ub, const float* Uw,
+                          const float* Vb, const float* Vw, const float* S_chunks, const void* dO,
+                          const float* dS_T, void* dq, void* dk, void* dv, void* dbeta, void* df,
+                          float* dA, float* dtau, void* dbx, void* dwx, float* dUb, float* dUw,
+                          float* dVb, float* dVw, float* dS0, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream) {
+  if (!f) {
+    ProfClear pc;
+    return CARVE_ERR_NULL;
+  }
+  return bwd_impl(d, q, k, v, beta, Decay{nullptr, f, A, tau_f}, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO, dS_T,
+                  dq, dk, dv, dbeta, DecayGrad{nullptr, df, dA, dtau}, dbx, dwx, dUb, dUw, dVb, dVw, dS0,
+                  workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

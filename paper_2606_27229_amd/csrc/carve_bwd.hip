@@ -90,7 +90,10 @@ __device__ __forceinline__ int acquire_ready(const int* rdy, const int need) {
 
 // Adjoint of (batch, head) bh.  ready[bh * nch + ch] is raised when chunk ch's
 // record is complete; smem is the workgroup's dynamic LDS (BwdLds layout).
-template <typename T, int D, int RP>
+// GATED: g is formed from its staged raw logit f (Eq. decay_gate); the kernel
+// writes df = dg (-exp(A)) sigmoid(f + tau_f) instead of dg and sums dA = dg g
+// and dtau = df over its tokens into a per-(batch, head) partial.
+template <typename T, int D, int RP, bool GATED>
 __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char* smem, const int* ready) {
   typedef Quad<T> Qd;
   typedef typename Qd::q quad;
@@ -146,14 +149,19 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   const T* __restrict__ wx = reinterpret_cast<const T*>(a.wx) + bh0;
   const T* __restrict__ beta = reinterpret_cast<const T*>(a.beta) + bh1;
   const T* __restrict__ dO = reinterpret_cast<const T*>(a.dO) + bh0;
-  const float* __restrict__ gl = a.g + bh0;
+  const float* __restrict__ gl = GATED ? nullptr : a.g + bh0;
+  const T* __restrict__ fl = GATED ? reinterpret_cast<const T*>(a.f) + bh0 : nullptr;
   T* __restrict__ dq = reinterpret_cast<T*>(a.dq) + bh0;
   T* __restrict__ dk = reinterpret_cast<T*>(a.dk) + bh0;
   T* __restrict__ dv = reinterpret_cast<T*>(a.dv) + bh0;
   T* __restrict__ dbx = reinterpret_cast<T*>(a.dbx) + bh0;
   T* __restrict__ dwx = reinterpret_cast<T*>(a.dwx) + bh0;
   T* __restrict__ dbeta = reinterpret_cast<T*>(a.dbeta) + bh1;
-  float* __restrict__ dgo = a.dg + bh0;
+  float* __restrict__ dgo = GATED ? nullptr : a.dg + bh0;
+  T* __restrict__ dfo = GATED ? reinterpret_cast<T*>(a.df) + bh0 : nullptr;
+  float* sGate = reinterpret_cast<float*>(smem + lay.Gate);   // [2][D] -exp(A), tau_f (GATED)
+  float* sGacc = reinterpret_cast<float*>(smem + lay.Gacc);   // [2][D] dA, dtau sums (GATED)
+  T* sFs = reinterpret_cast<T*>(sGs);                          // [16][D] staged f (GATED)
   const ChunkRec cr = chunk_rec(sizeof(T), D, L, RP);
   const char* recb = reinterpret_cast<const char*>(a.rec) + (size_t)bh * nch * cr.total;
 
@@ -166,6 +174,13 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   // Vb / Vw operand quads (lane (g, c): V[16 w + c][16 ks + 4 g + e]) are read
   // from sVbT / sVwT with the transposing load where needed; the identity
   // operand (lane (g, c): I[4 g + e][c]) is rebuilt where needed.
+  if (GATED)
+    for (int x = tid; x < D; x += NT) {
+      sGate[x] = -expf(a.A[h * D + x]);
+      sGate[D + x] = a.tau_f[h * D + x];
+      sGacc[x] = 0.0f;
+      sGacc[D + x] = 0.0f;
+    }
 #define CARVE_FVB(KS_) Qd::ld_tr(sVbT, LDD, 16 * (KS_), 16 * w, g, c)
 #define CARVE_FVW(KS_) Qd::ld_tr(sVwT, LDD, 16 * (KS_), 16 * w, g, c)
 #define CARVE_FI() Qd::cvt(f32x4{4 * g == c ? 1.0f : 0.0f, 4 * g + 1 == c ? 1.0f : 0.0f, \
@@ -200,6 +215,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   static_assert(16 * NGC == NT, "one g vector per thread");
   quad ptm, ppm, psbq[NJT];
   f32x4 pgam, pg;
+  u32x4 pfv;        // a 16-byte vector of the block's f rows (GATED)
   T pbeta = (T)0.0f;
   // The prefetch of a block is issued in two parts during the previous block's
   // value- and key-side steps (which hardly use the memory pipeline), not at
@@ -237,7 +253,11 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       const T* src_ = s_ == 0 ? k : s_ == 1 ? q : s_ == 2 ? bx : s_ == 3 ? v : s_ == 4 ? wx : dO; \
       pstg[u_] = *reinterpret_cast<const u32x4*>(src_ + (tb_ + t_) * rs + k_ * VEC);           \
     }                                                                                         \
-    pg = *reinterpret_cast<const f32x4*>(gl + (tb_ + tid / NGC) * rs + 4 * (tid % NGC));      \
+    if constexpr (GATED) {                                                                    \
+      if (tid < 16 * NC) pfv = *reinterpret_cast<const u32x4*>(fl + (tb_ + tid / NC) * rs + (tid % NC) * VEC); \
+    } else {                                                                                  \
+      pg = *reinterpret_cast<const f32x4*>(gl + (tb_ + tid / NGC) * rs + 4 * (tid % NGC));    \
+    }                                                                                         \
     (void)e_;                                                                                 \
   } while (0)
 #define CARVE_BWD_LOADF(CH_)                                                                  \
@@ -325,6 +345,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       u32x4 lstg[NSTG];
       for (int u = 0; u < NSTG; ++u) lstg[u] = pstg[u];
       const f32x4 lg_row = pg;   // a row vector of g (staged below)
+      const u32x4 lf_row = pfv;  // GATED: a row vector of f
       if (bc == nbc - 1) {
         // first block of a chunk in reverse order: the chunk's F into LDS (the
         // previous chunk's last read of sF was before its glue barriers)
@@ -367,7 +388,12 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         const int s_ = x / (16 * NC), t = (x / NC) % 16, kk = x % NC;
         *reinterpret_cast<u32x4*>(sStg + (s_ * 16 + t) * D + (kk ^ (t & (NC - 1))) * VEC) = lstg[u];
       }
-      {
+      if constexpr (GATED) {
+        if (tid < 16 * NC) {
+          const int t = tid / NC, kk = tid % NC;
+          *reinterpret_cast<u32x4*>(sFs + t * D + (kk ^ (t & (NC - 1))) * VEC) = lf_row;
+        }
+      } else {
         const int t = tid / NGC, kk = tid % NGC;
         *reinterpret_cast<f32x4*>(sGs + t * D + 4 * (kk ^ (t & (NGC - 1)))) = lg_row;
       }
@@ -376,11 +402,20 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       // + 3) and of tau_b; read before the barrier that ends this step, so the
       // value-side step may overwrite the staging region
       quad kq, qq, lbx, vq, wxq, dOq, ltq[NRB];
+      quad lfq;   // GATED: f (row t = c, key channels 16 w + 4 g + e)
       f32x4 lg;
       {
-        lg = *reinterpret_cast<const f32x4*>(sGs + c * D + 4 * ((4 * w + g) ^ (c & (NGC - 1))));
         const int by = (16 * w + 4 * g) * (int)sizeof(T);
         const int off = ((((by >> 4) ^ (c & (NC - 1))) << 4) | (by & 15)) / (int)sizeof(T);
+        if constexpr (GATED) {
+          lfq = Qd::ld(sFs + c * D + off);
+          const f32x4 fv = Qd::f32(lfq);
+          const f32x4 na = *reinterpret_cast<const f32x4*>(sGate + 16 * w + 4 * g);
+          const f32x4 tf = *reinterpret_cast<const f32x4*>(sGate + D + 16 * w + 4 * g);
+          for (int i = 0; i < 4; ++i) lg[i] = na[i] * softplus_f(fv[i] + tf[i]);
+        } else {
+          lg = *reinterpret_cast<const f32x4*>(sGs + c * D + 4 * ((4 * w + g) ^ (c & (NGC - 1))));
+        }
         const T* r0 = sStg + c * D + off;
         kq = Qd::ld(r0);
         qq = Qd::ld(r0 + 16 * D);
@@ -581,7 +616,31 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
           dqp[i] = dQt[i] * E[i];
         }
         Qd::st(dk + e0, Qd::cvt(dkv));
-        *reinterpret_cast<f32x4*>(dgo + e0) = dgv;
+        if constexpr (GATED) {
+          // through Eq. decay_gate: df = dg (-exp(A)) sigmoid(f + tau_f); dA and
+          // dtau collect dg g and df, summed over the block's 16 tokens (the
+          // lanes of a row) and added by lane c = 0 (one owner per channel)
+          const f32x4 fv = Qd::f32(lfq);
+          const f32x4 na = *reinterpret_cast<const f32x4*>(sGate + 16 * w + 4 * g);
+          const f32x4 tf = *reinterpret_cast<const f32x4*>(sGate + D + 16 * w + 4 * g);
+          f32x4 dfv, sA, sT;
+          for (int i = 0; i < 4; ++i) {
+            float sp, sg;
+            softplus_sigmoid(fv[i] + tf[i], sp, sg);
+            dfv[i] = dgv[i] * na[i] * sg;
+            sA[i] = row_suffix(dgv[i] * na[i] * sp);
+            sT[i] = row_suffix(dfv[i]);
+          }
+          Qd::st(dfo + e0, Qd::cvt(dfv));
+          if (c == 0) {
+            f32x4* pa = reinterpret_cast<f32x4*>(sGacc + 16 * w + 4 * g);
+            f32x4* pt = reinterpret_cast<f32x4*>(sGacc + D + 16 * w + 4 * g);
+            *pa = *pa + sA;
+            *pt = *pt + sT;
+          }
+        } else {
+          *reinterpret_cast<f32x4*>(dgo + e0) = dgv;
+        }
         const quad dzbq = Qd::cvt(dzb);
         Qd::st(dbx + e0, dzbq);
         Qd::st(sdzb + c * LDD + 16 * w + 4 * g, dzbq);
@@ -665,6 +724,10 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
 #undef CARVE_BWD_LOADA
 #undef CARVE_BWD_LOADS
 #undef CARVE_BWD_LOADF
+  if constexpr (GATED) {
+    // every update of the sums was made before a barrier of the last block
+    for (int x = tid; x < 2 * D; x += NT) a.partG[(size_t)bh * 2 * D + x] = sGacc[x];
+  }
   if (a.dS0) {
     float* dst = a.dS0 + soff + (16 * w + c) * D + 4 * g;
     for (int jt = 0; jt < NJT; ++jt) *reinterpret_cast<f32x4*>(dst + 16 * jt) = dSt[jt];
@@ -850,7 +913,7 @@ __global__ void __launch_bounds__(256) carve_sync_clear_kernel(int* __restrict__
 // whatever order the hardware dispatches the grid in.  Recompute items are
 // taken latest chunk first (the order in which the adjoint needs them): item
 // i is chunk nch - 1 - i / (B*H) of (batch, head) i % (B*H).
-template <typename T, int D, int LW, int RP>
+template <typename T, int D, int LW, int RP, bool GATED>
 __global__ void __launch_bounds__(bwd_threads(D)) __attribute__((amdgpu_waves_per_eu(1, 2)))
 carve_bwd_fused_kernel(FwdArgs f, BwdArgs a, int nrec, int* sync) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -866,7 +929,7 @@ carve_bwd_fused_kernel(FwdArgs f, BwdArgs a, int nrec, int* sync) {
   if (ticket < nrec) {
     for (int item = ticket; item < nitems; item += nrec) {
       const int ch = nch - 1 - item / nbh, bh = item % nbh;
-      rec_chunk<T, D, LW, RP>(f, bh, ch, smem);
+      rec_chunk<T, D, LW, RP, GATED>(f, bh, ch, smem);
       // every wave's record stores are complete before the barrier; the
       // release store (agent scope) then writes them back for other XCDs
       vm_wait_all();
@@ -875,7 +938,7 @@ carve_bwd_fused_kernel(FwdArgs f, BwdArgs a, int nrec, int* sync) {
         __hip_atomic_store(ready + (size_t)bh * nch + ch, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     }
   } else {
-    bwd_adjoint<T, D, RP>(a, ticket - nrec, smem, ready);
+    bwd_adjoint<T, D, RP, GATED>(a, ticket - nrec, smem, ready);
   }
 }
 
@@ -887,13 +950,13 @@ __host__ __device__ constexpr size_t fused_lds() {
   return lds_max(rec_lds<T, D, LW, RP>().total, bwd_lds<T, D, RP>().total);
 }
 
-template <typename T, int D, int LW, int RP>
+template <typename T, int D, int LW, int RP, bool GATED>
 static int launch_fused_t(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, hipStream_t stream) {
   constexpr size_t lds = fused_lds<T, D, LW, RP>();
   if constexpr (lds > kMaxLdsBytes) {
     return CARVE_ERR_UNSUPPORTED;
   } else {
-    auto kern = carve_bwd_fused_kernel<T, D, LW, RP>;
+    auto kern = carve_bwd_fused_kernel<T, D, LW, RP, GATED>;
     static bool attr_set = false;  // per instantiation
     if (!attr_set) {
       if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -915,24 +978,24 @@ static int launch_fused_t(const FwdArgs& f, const BwdArgs& a, int* sync, int cus
   }
 }
 
-template <typename T, int D, int RP>
+template <typename T, int D, int RP, bool GATED>
 static int launch_fused_l(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, int LW, hipStream_t s) {
-  if (LW == 16) return launch_fused_t<T, D, 16, RP>(f, a, sync, cus, s);
-  if (LW == 32) return launch_fused_t<T, D, 32, RP>(f, a, sync, cus, s);
-  if (LW == 64) return launch_fused_t<T, D, 64, RP>(f, a, sync, cus, s);
+  if (LW == 16) return launch_fused_t<T, D, 16, RP, GATED>(f, a, sync, cus, s);
+  if (LW == 32) return launch_fused_t<T, D, 32, RP, GATED>(f, a, sync, cus, s);
+  if (LW == 64) return launch_fused_t<T, D, 64, RP, GATED>(f, a, sync, cus, s);
   return CARVE_ERR_UNSUPPORTED;
 }
 
-template <typename T>
+template <typename T, bool GATED>
 static int launch_fused_d(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, int D, int LW, hipStream_t s) {
   if (a.RP == 32) {
-    if (D == 32) return launch_fused_l<T, 32, 32>(f, a, sync, cus, LW, s);
-    if (D == 64) return launch_fused_l<T, 64, 32>(f, a, sync, cus, LW, s);
-    if (D == 128) return launch_fused_l<T, 128, 32>(f, a, sync, cus, LW, s);
+    if (D == 32) return launch_fused_l<T, 32, 32, GATED>(f, a, sync, cus, LW, s);
+    if (D == 64) return launch_fused_l<T, 64, 32, GATED>(f, a, sync, cus, LW, s);
+    if (D == 128) return launch_fused_l<T, 128, 32, GATED>(f, a, sync, cus, LW, s);
   } else if (a.RP == 64) {
-    if (D == 32) return launch_fused_l<T, 32, 64>(f, a, sync, cus, LW, s);
-    if (D == 64) return launch_fused_l<T, 64, 64>(f, a, sync, cus, LW, s);
-    if (D == 128) return launch_fused_l<T, 128, 64>(f, a, sync, cus, LW, s);
+    if (D == 32) return launch_fused_l<T, 32, 64, GATED>(f, a, sync, cus, LW, s);
+    if (D == 64) return launch_fused_l<T, 64, 64, GATED>(f, a, sync, cus, LW, s);
+    if (D == 128) return launch_fused_l<T, 128, 64, GATED>(f, a, sync, cus, LW, s);
   }
   return CARVE_ERR_UNSUPPORTED;
 }
@@ -943,9 +1006,35 @@ int launch_sync_clear(int* sync, size_t n, hipStream_t s) {
 }
 
 int launch_bwd_fused(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, int dtype, int D, int LW,
-                     hipStream_t s) {
-  if (dtype == CARVE_BF16) return launch_fused_d<bf16_t>(f, a, sync, cus, D, LW, s);
-  return launch_fused_d<float>(f, a, sync, cus, D, LW, s);
+                     bool gated, hipStream_t s) {
+  if (dtype == CARVE_BF16)
+    return gated ? launch_fused_d<bf16_t, true>(f, a, sync, cus, D, LW, s)
+                 : launch_fused_d<bf16_t, false>(f, a, sync, cus, D, LW, s);
+  return gated ? launch_fused_d<float, true>(f, a, sync, cus, D, LW, s)
+               : launch_fused_d<float, false>(f, a, sync, cus, D, LW, s);
+}
+
+// dA[h][j] and dtau[h][j] as sums over b = 0, 1, ... (in order) of the
+// per-(batch, head) partials (layout [B*H][2][D]); one thread per (h, j)
+__global__ void __launch_bounds__(256) carve_gate_reduce_kernel(const float* __restrict__ partG, int B, int H, int D,
+                                                                float* __restrict__ dA, float* __restrict__ dtau) {
+  const int x = blockIdx.x * 256 + threadIdx.x;
+  if (x >= H * D) return;
+  const int h = x / D, j = x % D;
+  float sa = 0.0f, st = 0.0f;
+  for (int b = 0; b < B; ++b) {
+    const float* p = partG + ((size_t)b * H + h) * 2 * D;
+    sa += p[j];
+    st += p[D + j];
+  }
+  dA[x] = sa;
+  dtau[x] = st;
+}
+
+int launch_gate_reduce(const float* partG, int B, int H, int D, float* dA, float* dtau, hipStream_t s) {
+  hipLaunchKernelGGL(carve_gate_reduce_kernel, dim3((unsigned)((H * D + 255) / 256)), dim3(256), 0, s, partG, B, H, D,
+                     dA, dtau);
+  return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
 }
 
 template <typename T, int D, int RP>

@@ -64,7 +64,10 @@ __host__ __device__ constexpr int tri_col(int x, bool strict) {
 static_assert(tri_row(0, true) == 1 && tri_col(0, true) == 0 && tri_row(5, true) == 3 && tri_col(5, true) == 2, "");
 static_assert(tri_row(0, false) == 0 && tri_row(2, false) == 1 && tri_col(2, false) == 1 && tri_col(9, false) == 3, "");
 
-template <typename T, int D, int WB, int RP>
+// GATED: the decay g is formed in the kernel from its raw logit f (token
+// dtype) as -exp(A) softplus(f + tau_f) (Eq. decay_gate, Sec. decay_gate),
+// with A and tau_f of the head held in LDS.
+template <typename T, int D, int WB, int RP, bool GATED>
 __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs a) {
   typedef Quad<T> Qd;
   typedef typename Qd::q quad;
@@ -108,6 +111,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);  // [2][WB] (block parity)
   constexpr bool SVW = chain_stage_vw<T, D, WB, RP>();
   T* sVW = reinterpret_cast<T*>(smem + lay.VW);    // [2][WB][D]  v, wx (swizzled; SVW)
+  float* sGate = reinterpret_cast<float*>(smem + lay.Gate);  // [2][D] -exp(A), tau_f (GATED)
 
   const size_t bh0 = ((size_t)b * Tn * H + h) * D;
   const size_t bh1 = (size_t)b * Tn * H + h;
@@ -118,10 +122,16 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   const T* __restrict__ bx = reinterpret_cast<const T*>(a.bx) + bh0;
   const T* __restrict__ wx = reinterpret_cast<const T*>(a.wx) + bh0;
   const T* __restrict__ beta = reinterpret_cast<const T*>(a.beta) + bh1;
-  const float* __restrict__ gl = a.g + bh0;
+  const float* __restrict__ gl = GATED ? nullptr : a.g + bh0;
+  const T* __restrict__ fl = GATED ? reinterpret_cast<const T*>(a.f) + bh0 : nullptr;
   T* __restrict__ o = reinterpret_cast<T*>(a.o) + bh0;
 
   // ---- shared parameters ------------------------------------------------------
+  if (GATED)
+    for (int x = tid; x < D; x += NT) {
+      sGate[x] = -expf(a.A[h * D + x]);
+      sGate[D + x] = a.tau_f[h * D + x];
+    }
   for (int x = tid; x < R2 * D; x += NT) {
     const int rr = x / D, i = x % D;
     float u = 0.0f;
@@ -165,7 +175,8 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   u32x4 cq[NXV], ck[NXV], cbx[NXV];
   quad pv[NB], pwx[NB];      // per-tile value-side operands (without SVW)
   u32x4 cv[NXV], cwx[NXV];   // whole rows of v and wx (with SVW)
-  f32x4 pg[NB];
+  f32x4 pg[NB];     // g per tile (ungated)
+  quad pf[NB];      // f per tile (GATED)
   T pbeta = (T)0.0f;
 #define CARVE_PREFETCH_Q(BLK_)                                                     \
   do {                                                                             \
@@ -193,8 +204,11 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   do {                                                                             \
     int cs_ = c, gs_ = g;                                                          \
     asm volatile("" : "+v"(cs_), "+v"(gs_));                                       \
-    for (int bb_ = 0; bb_ < NB; ++bb_)                                             \
-      pg[bb_] = *reinterpret_cast<const f32x4*>(gl + ((BLK_) * WB + 16 * bb_ + cs_) * rs + 16 * w + 4 * gs_); \
+    for (int bb_ = 0; bb_ < NB; ++bb_) {                                           \
+      const int e_ = ((BLK_) * WB + 16 * bb_ + cs_) * rs + 16 * w + 4 * gs_;      \
+      if constexpr (GATED) pf[bb_] = Qd::ld(fl + e_);                              \
+      else pg[bb_] = *reinterpret_cast<const f32x4*>(gl + e_);                     \
+    }                                                                              \
   } while (0)
 #define CARVE_PREFETCH_VW(BLK_)                                                    \
   do {                                                                             \
@@ -346,7 +360,16 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
         f32x4 z = zero4();
         for (int ks = 0; ks < NRB; ++ks)
           z = Qd::mma16(fVb[ks], Qd::ld(sTau + (16 * bb + c) * LDR + 16 * ks + 4 * g), z);
-        const f32x4 bxv = Qd::f32(Qd::ld(sBx + (16 * bb + c) * LDD + 16 * w + 4 * g)), gv = pg[bb];
+        const f32x4 bxv = Qd::f32(Qd::ld(sBx + (16 * bb + c) * LDD + 16 * w + 4 * g));
+        f32x4 gv;
+        if constexpr (GATED) {
+          const f32x4 fv = Qd::f32(pf[bb]);
+          const f32x4 na = *reinterpret_cast<const f32x4*>(sGate + 16 * w + 4 * g);
+          const f32x4 tf = *reinterpret_cast<const f32x4*>(sGate + D + 16 * w + 4 * g);
+          for (int e = 0; e < 4; ++e) gv[e] = na[e] * softplus_f(fv[e] + tf[e]);
+        } else {
+          gv = pg[bb];
+        }
         for (int e = 0; e < 4; ++e) {
           const float ell = gv[e] - softplus_f(z[e] + bxv[e]);
           lam[bb][e] = carry[e] + row_scan(ell);
@@ -542,7 +565,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
 // ---------------------------------------------------------------------------
 // host-side launch
 // ---------------------------------------------------------------------------
-template <typename T, int D, int WB, int RP>
+template <typename T, int D, int WB, int RP, bool GATED>
 static int launch_chain_t(const FwdArgs& a, hipStream_t stream) {
   constexpr ChainLds lay = chain_lds<T, D, WB, RP>();
   if constexpr (lay.total > kMaxLdsBytes) {
@@ -550,7 +573,7 @@ static int launch_chain_t(const FwdArgs& a, hipStream_t stream) {
     (void)stream;
     return CARVE_ERR_UNSUPPORTED;
   } else {
-  auto kern = carve_chain_fwd_kernel<T, D, WB, RP>;
+  auto kern = carve_chain_fwd_kernel<T, D, WB, RP, GATED>;
   static bool attr_set = false;  // per instantiation
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -563,31 +586,32 @@ static int launch_chain_t(const FwdArgs& a, hipStream_t stream) {
   }
 }
 
-template <typename T, int D, int RP>
+template <typename T, int D, int RP, bool GATED>
 static int launch_chain_w(const FwdArgs& a, int WB, hipStream_t s) {
-  if (WB == 16) return launch_chain_t<T, D, 16, RP>(a, s);
-  if (WB == 32) return launch_chain_t<T, D, 32, RP>(a, s);
-  if (WB == 64) return launch_chain_t<T, D, 64, RP>(a, s);
+  if (WB == 16) return launch_chain_t<T, D, 16, RP, GATED>(a, s);
+  if (WB == 32) return launch_chain_t<T, D, 32, RP, GATED>(a, s);
+  if (WB == 64) return launch_chain_t<T, D, 64, RP, GATED>(a, s);
   return CARVE_ERR_UNSUPPORTED;
 }
 
-template <typename T>
+template <typename T, bool GATED>
 static int launch_chain_d(const FwdArgs& a, int D, int WB, hipStream_t s) {
   if (a.RP == 32) {
-    if (D == 32) return launch_chain_w<T, 32, 32>(a, WB, s);
-    if (D == 64) return launch_chain_w<T, 64, 32>(a, WB, s);
-    if (D == 128) return launch_chain_w<T, 128, 32>(a, WB, s);
+    if (D == 32) return launch_chain_w<T, 32, 32, GATED>(a, WB, s);
+    if (D == 64) return launch_chain_w<T, 64, 32, GATED>(a, WB, s);
+    if (D == 128) return launch_chain_w<T, 128, 32, GATED>(a, WB, s);
   } else if (a.RP == 64) {
-    if (D == 32) return launch_chain_w<T, 32, 64>(a, WB, s);
-    if (D == 64) return launch_chain_w<T, 64, 64>(a, WB, s);
-    if (D == 128) return launch_chain_w<T, 128, 64>(a, WB, s);
+    if (D == 32) return launch_chain_w<T, 32, 64, GATED>(a, WB, s);
+    if (D == 64) return launch_chain_w<T, 64, 64, GATED>(a, WB, s);
+    if (D == 128) return launch_chain_w<T, 128, 64, GATED>(a, WB, s);
   }
   return CARVE_ERR_UNSUPPORTED;
 }
 
-int launch_chain_fwd(const FwdArgs& a, int dtype, int D, int WB, hipStream_t s) {
-  if (dtype == CARVE_BF16) return launch_chain_d<bf16_t>(a, D, WB, s);
-  return launch_chain_d<float>(a, D, WB, s);
+int launch_chain_fwd(const FwdArgs& a, int dtype, int D, int WB, bool gated, hipStream_t s) {
+  if (dtype == CARVE_BF16)
+    return gated ? launch_chain_d<bf16_t, true>(a, D, WB, s) : launch_chain_d<bf16_t, false>(a, D, WB, s);
+  return gated ? launch_chain_d<float, true>(a, D, WB, s) : launch_chain_d<float, false>(a, D, WB, s);
 }
 
 template <typename T, int D, int RP>

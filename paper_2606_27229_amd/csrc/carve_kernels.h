@@ -10,6 +10,10 @@ namespace carve {
 struct FwdArgs {
   const void *q, *k, *v, *beta, *bx, *wx;   // token tensors (dtype of the call)
   const float *g, *Ub, *Uw, *Vb, *Vw, *S0;  // f32
+  // decay gate from its raw logit (gated kernels; Eq. decay_gate): f [B,T,H,Dk]
+  // in the token dtype, A and tau_f [H,Dk] f32; g is unused then
+  const void* f;
+  const float *A, *tau_f;
   void* o;
   float *S_T, *S_chunks;
   void* rec;     // chunk records (recompute mode of the backward)
@@ -69,7 +73,7 @@ __host__ __device__ constexpr int lk_of() {
 // blocks).  Every row is padded by 16 bytes.  Region X holds the copy of the
 // chunk start state while the fold runs and the per-token key-side operands after.
 struct RecLds {
-  size_t U, Q, F, Tau, Beta, X, S, Kt, Qt, Ki, Gam, AT, Tm, total;
+  size_t U, Q, F, Tau, Beta, X, S, Kt, Qt, Ki, Gam, AT, Tm, Gate, total;
 };
 
 template <typename T, int D, int LW, int RP>
@@ -96,6 +100,7 @@ __host__ __device__ constexpr RecLds rec_lds() {
   l.S = off;
   x = lds_max(x, lds_round(D * LDD * e));
   off += x;
+  l.Gate = off; off += lds_round(2 * D * 4);   // -exp(A), tau_f of the head (gated)
   l.total = off;
   return l;
 }
@@ -110,7 +115,7 @@ __host__ __device__ constexpr RecLds rec_lds() {
 // the first barrier of a block to its gates; it overlays A .. TmT, which are
 // written only after the gates.  Without VW those tiles are read per wave.
 struct ChainLds {
-  size_t U, X, Kt, Bx, Ki, F, Q, Tau, A, P, AdT, TmT, VW, Rho, Beta, total;
+  size_t U, X, Kt, Bx, Ki, F, Q, Tau, A, P, AdT, TmT, VW, Rho, Beta, Gate, total;
 };
 
 template <typename T, int D, int WB, int RP, bool VW>
@@ -137,6 +142,7 @@ __host__ __device__ constexpr ChainLds chain_lds_v() {
   if (VW) off = lds_max(off, l.VW + lds_round(2 * WB * (size_t)D * e));
   l.Rho = off;  off += lds_round(D * 4);
   l.Beta = off; off += lds_round(2 * WB * 4);
+  l.Gate = off; off += lds_round(2 * D * 4);   // -exp(A), tau_f of the head (gated)
   l.total = off;
   return l;
 }
@@ -153,7 +159,7 @@ __host__ __device__ constexpr ChainLds chain_lds() {
 }
 
 // forward of the whole sequence (one workgroup per (batch, head)), WY blocks of WB tokens
-int launch_chain_fwd(const FwdArgs& a, int dtype, int D, int WB, hipStream_t s);
+int launch_chain_fwd(const FwdArgs& a, int dtype, int D, int WB, bool gated, hipStream_t s);
 size_t chain_lds_bytes(int dtype, int D, int WB, int RP);
 
 
@@ -166,6 +172,12 @@ struct BwdArgs {
   const float* dS_T;
   void *dq, *dk, *dv, *dbeta, *dbx, *dwx;
   float* dg;
+  // gated kernels: decay logit and its parameters, df (token dtype) instead of
+  // dg, per-(b,h) partial dA, dtau ([B*H][2][Dk] f32, workspace)
+  const void* f;
+  const float *A, *tau_f;
+  void* df;
+  float* partG;
   float* dS0;
   float* part;    // per-(b,h, chunk split) partial d[Ub; Uw] (workspace)
   float* partV;   // per-(b,h,split) partial dVb, dVw (workspace)
@@ -185,8 +197,12 @@ constexpr int kUSplit = 16;
 // chunks XOR-swizzled by row) are staged there (Stage), so the region holds at
 // least 6 * 16 * D elements plus 16 * D floats.  At a chunk start the glue
 // reuses dSx for dF as a high and a low part ([D][LDF] each).
+// Gated kernels stage the decay logit f (token dtype) in place of g and keep
+// -exp(A), tau_f of the head (Gate) and the dA, dtau accumulators (Gacc) behind
+// it, inside the area g would take where that is large enough.
 struct BwdLds {
-  size_t F, VbT, VwT, Tau, Tm, P, Gam, Beta, Dbeta, Kt, Qt, Ki, Sx, dSx, dOT, uT, dRT, dzwT, Stage, dzb, dY, total;
+  size_t F, VbT, VwT, Tau, Tm, P, Gam, Beta, Dbeta, Kt, Qt, Ki, Sx, dSx, dOT, uT, dRT, dzwT, Stage, Gate, Gacc,
+      dzb, dY, total;
 };
 
 template <typename T, int D, int RP>
@@ -217,7 +233,12 @@ __host__ __device__ constexpr BwdLds bwd_lds() {
   l.uT = off;    off += lds_round(D * LDB * e);
   l.dRT = off;   off += lds_round(D * LDB * e);
   l.dzwT = off;  off += lds_round(D * LDB * e);
-  off = lds_max(off, l.Stage + lds_round(6 * 16 * D * e) + lds_round(16 * D * 4));
+  {
+    const size_t garea = l.Stage + lds_round(6 * 16 * D * e);      // g, or f then Gate, Gacc
+    l.Gate = garea + lds_round(16 * D * e);
+    l.Gacc = l.Gate + lds_round(2 * D * 4);
+    off = lds_max(off, garea + lds_max(lds_round(16 * D * 4), lds_round(16 * D * e) + 2 * lds_round(2 * D * 4)));
+  }
   l.dzb = off;   off += lds_round(16 * LDD * e);
   l.dY = off;    off += lds_round(16 * LDR * e);
   l.total = off;
@@ -229,7 +250,9 @@ __host__ __device__ constexpr BwdLds bwd_lds() {
 // at sync_ints(B * H, T / L) ints of workspace, zeroed by launch_sync_clear
 // on the same stream before; cus is the device's compute-unit count.
 int launch_bwd_fused(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, int dtype, int D, int LW,
-                     hipStream_t s);
+                     bool gated, hipStream_t s);
+// dA[h][j], dtau[h][j] = sums over b (in order) of the per-(b,h) partials
+int launch_gate_reduce(const float* partG, int B, int H, int D, float* dA, float* dtau, hipStream_t s);
 int launch_sync_clear(int* sync, size_t n, hipStream_t s);
 // LDS bytes of the fused launch with LW-token recompute sub-chunks
 size_t bwd_lds_bytes(int dtype, int D, int LW, int RP);

@@ -40,7 +40,9 @@ namespace carve {
 // workgroup's dynamic LDS (RecLds layout).  Ends with a workgroup barrier, so
 // the caller may reuse the LDS at once; the record stores may still be in
 // flight.
-template <typename T, int D, int LW, int RP>
+// GATED: g is formed from its raw logit f as -exp(A) softplus(f + tau_f)
+// (Eq. decay_gate), A and tau_f of the head held in LDS.
+template <typename T, int D, int LW, int RP, bool GATED>
 __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const int ch0, char* smem) {
   typedef Quad<T> Qd;
   typedef typename Qd::q quad;
@@ -78,6 +80,7 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
   float* sGam = reinterpret_cast<float*>(smem + lay.Gam);  // [NB][D]     e^{lam_15}
   float* sAT = reinterpret_cast<float*>(smem + lay.AT);    // [NB][16][20] A^T per block
   T* sTm = reinterpret_cast<T*>(smem + lay.Tm);            // [NB][16][LDB] T per block
+  float* sGate = reinterpret_cast<float*>(smem + lay.Gate);  // [2][D] -exp(A), tau_f (GATED)
 
   // token tensors addressed from this (batch, head)'s first element with 32-bit
   // offsets t * rs + column (rs = H * D elements between consecutive tokens)
@@ -90,9 +93,15 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
   const T* __restrict__ bx = reinterpret_cast<const T*>(a.bx) + bh0;
   const T* __restrict__ wx = reinterpret_cast<const T*>(a.wx) + bh0;
   const T* __restrict__ beta = reinterpret_cast<const T*>(a.beta) + bh1;
-  const float* __restrict__ gl = a.g + bh0;
+  const float* __restrict__ gl = GATED ? nullptr : a.g + bh0;
+  const T* __restrict__ fl = GATED ? reinterpret_cast<const T*>(a.f) + bh0 : nullptr;
 
   // ---- shared parameters ------------------------------------------------------
+  if (GATED)
+    for (int x = tid; x < D; x += NT) {
+      sGate[x] = -expf(a.A[h * D + x]);
+      sGate[D + x] = a.tau_f[h * D + x];
+    }
   for (int x = tid; x < R2 * D; x += NT) {
     const int rr = x / D, i = x % D;
     float u = 0.0f;
@@ -133,7 +142,8 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
   u32x4 pq[NQV];
   T pbeta = (T)0.0f;
   quad pbx[NB], pk[NB], pwx[NB], pv[NB];
-  f32x4 pg[NB];
+  f32x4 pg[NB];     // g per tile (ungated)
+  quad pf[NB];      // f per tile (GATED)
 #define CARVE_REC_PREFETCH_Q(TILE_)                                                     \
   do {                                                                                  \
     const int tt0_ = (TILE_) * LW;                                                      \
@@ -154,7 +164,8 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
       pk[bb_] = Qd::ld(k + e_);                                                         \
       pwx[bb_] = Qd::ld(wx + e_);                                                       \
       pv[bb_] = Qd::ld(v + e_);                                                         \
-      pg[bb_] = *reinterpret_cast<const f32x4*>(gl + e_);                               \
+      if constexpr (GATED) pf[bb_] = Qd::ld(fl + e_);                                   \
+      else pg[bb_] = *reinterpret_cast<const f32x4*>(gl + e_);                          \
     }                                                                                   \
   } while (0)
   const int tile0 = ch0 * msub, ntiles = tile0 + msub;
@@ -215,7 +226,16 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
       f32x4 z = zero4();
       for (int ks = 0; ks < RP / 16; ++ks)
         z = Qd::mma16(fVb[ks], Qd::ld(sTau + (16 * bb + c) * LDR + 16 * ks + 4 * g), z);
-      const f32x4 bxv = Qd::f32(pbx[bb]), kv = Qd::f32(pk[bb]), gv = pg[bb];
+      const f32x4 bxv = Qd::f32(pbx[bb]), kv = Qd::f32(pk[bb]);
+      f32x4 gv;
+      if constexpr (GATED) {
+        const f32x4 fv = Qd::f32(pf[bb]);
+        const f32x4 na = *reinterpret_cast<const f32x4*>(sGate + 16 * w + 4 * g);
+        const f32x4 tf = *reinterpret_cast<const f32x4*>(sGate + D + 16 * w + 4 * g);
+        for (int i = 0; i < 4; ++i) gv[i] = na[i] * softplus_f(fv[i] + tf[i]);
+      } else {
+        gv = pg[bb];
+      }
       const f32x4 qv = Qd::f32(Qd::ld(sQ + (16 * bb + c) * LDD + 16 * w + 4 * g));
       f32x4 kt, qt, ki, gam;
       for (int i = 0; i < 4; ++i) {

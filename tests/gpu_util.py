@@ -3,7 +3,7 @@ import numpy as np
 import torch
 
 INPUT_KEYS = ("q", "k", "v", "beta", "g", "bx", "wx", "Ub", "Uw", "Vb", "Vw", "S0")
-F32_KEYS = ("g", "Ub", "Uw", "Vb", "Vw", "S0", "dS_T")
+F32_KEYS = ("g", "A", "tau_f", "Ub", "Uw", "Vb", "Vw", "S0", "dS_T")
 
 
 def to_gpu(inp, dtype, device="cuda"):

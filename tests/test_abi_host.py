@@ -104,3 +104,41 @@ def test_profile_hook_validation():
     fake = ctypes.c_void_p(4096)
     assert lib.carve_chunk_fwd(ctypes.byref(d), *([fake] * 12), fake, None, None, None, 0, None) == -2
     assert lib.carve_profile_events(None, 0) == 0
+
+
+def test_gated_forward_validation():
+    """carve_chunk_fwd_gated: NULL f / A / tau_f, bad shapes and misalignment
+    are rejected before any HIP call."""
+    lib = carve.load_library()
+    d = _dims()
+    fake = ctypes.c_void_p(4096)
+    # q, k, v, beta, f, A, tau_f, bx, wx, Ub, Uw, Vb, Vw, S0, o, S_T, S_chunks, ws, bytes, stream
+    args = [fake] * 13 + [None, fake, None, None, None, 0, None]
+    for null_at in (4, 5, 6):   # f, A, tau_f
+        a = list(args)
+        a[null_at] = None
+        assert lib.carve_chunk_fwd_gated(ctypes.byref(d), *a) == -1, null_at
+    assert lib.carve_chunk_fwd_gated(ctypes.byref(_dims(T=100)), *args) == -2
+    a = list(args)
+    a[5] = ctypes.c_void_p(4096 + 4)   # A misaligned
+    assert lib.carve_chunk_fwd_gated(ctypes.byref(d), *a) == -4
+
+
+def test_gated_backward_workspace_and_aliasing():
+    lib = carve.load_library()
+    d = _dims()
+    need = lib.carve_workspace_size(ctypes.byref(d), 1)
+    # distinct fake addresses far apart: 31 tensors before dS0, workspace
+    ptrs = [ctypes.c_void_p(1 << 40 | (i << 32)) for i in range(34)]
+    st = lib.carve_chunk_bwd_gated(ctypes.byref(d), *ptrs[:30], None, 0, None)
+    assert st == -5
+    st = lib.carve_chunk_bwd_gated(ctypes.byref(d), *ptrs[:30], ptrs[30], need - 1, None)
+    assert st == -5
+    a = list(ptrs[:30])
+    a[20] = a[4]          # df aliases f
+    st = lib.carve_chunk_bwd_gated(ctypes.byref(d), *a, ptrs[30], need, None)
+    assert st == -3
+    a = list(ptrs[:30])
+    a[21] = None          # dA missing
+    st = lib.carve_chunk_bwd_gated(ctypes.byref(d), *a, ptrs[30], need, None)
+    assert st == -1
