@@ -30,7 +30,7 @@ KERNEL_SOURCES = ("paper_2606_27229_amd/csrc/carve_fwd_chain.hip", "paper_2606_2
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer_1p3b_T4096_L64.json")
 
 
-def algorithmic_counts(B, T, H, d, R, L):
+def algorithmic_counts(B, T, H, d, R, L, gated=False):
     """Algorithmic bytes and flops per call (every input and output once).
 
     Bytes per token-head (bf16 token tensors, f32 g and states):
@@ -41,12 +41,15 @@ def algorithmic_counts(B, T, H, d, R, L):
       backward         the adjoint's bytes + the chunk-start states it needs
                        (4 d^2 / L, read by the recompute); the fused
                        recompute + adjoint kernel is priced at this figure
+    With the gate-in-kernel decay the f32 g (4d) is replaced by the bf16 logit
+    f (2d) and dg by df (2d); A, tau_f and dA, dtau are per head (negligible).
     Flops per token-head (multiply-add = 2): forward
       2 * (2 r d^2 / L + 3 d^2 + 4 r d + 5/2 L d + L^2 / 6), backward 2x forward.
     """
     th = B * T * H
-    inputs = 3 * 2 * d + 4 * d + 2 * 2 * d + 2
-    grads = 3 * 2 * d + 4 * d + 2 * 2 * d + 2
+    decay = 2 * d if gated else 4 * d
+    inputs = 3 * 2 * d + decay + 2 * 2 * d + 2
+    grads = 3 * 2 * d + decay + 2 * 2 * d + 2
     states = 4 * d * d / L
     fwd_mac = 2 * R * d * d / L + 3 * d * d + 4 * R * d + 2.5 * L * d + L * L / 6.0
     return {
@@ -131,20 +134,22 @@ def traffic_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir):
     print(json.dumps(rec), flush=True)
 
 
-def cpu_baseline(w, L, seed, target_s=12.0):
+def cpu_baseline(w, L, seed, target_s=12.0, gated=False):
     """Time the CPU oracle (token-serial forward + exact backward, double) on the
     whole workload batch, repeated until about target_s seconds of CPU work."""
     from oracle import oracle as orc
     from paper_2606_27229_amd.inputs import make_inputs
 
-    inp = make_inputs(w, seed=seed)
+    inp = make_inputs(w, seed=seed, gated=gated)
     threads = max(1, min(16, os.cpu_count() or 1, w.B * w.H))
+    fwd = orc.fwd_gated if gated else orc.fwd_serial
+    bwd = orc.bwd_gated if gated else orc.bwd
     reps, t_f, t_b = 0, 0.0, 0.0
     while reps == 0 or t_f + t_b < target_s:
         t0 = time.perf_counter()
-        orc.fwd_serial(inp, L, nthreads=threads)
+        fwd(inp, L, nthreads=threads)
         t1 = time.perf_counter()
-        orc.bwd(inp, L, inp["dO"], None, nthreads=threads)
+        bwd(inp, L, inp["dO"], None, nthreads=threads)
         t2 = time.perf_counter()
         t_f += t1 - t0
         t_b += t2 - t1
@@ -163,6 +168,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--L", type=int, default=64)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--gated", action="store_true",
+                    help="the gate-in-kernel variant: the decay is formed in the kernels from its raw "
+                         "logit f (bf16) and per-head A, tau_f (carve_chunk_fwd_gated / _bwd_gated)")
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
                     help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of this benchmark and of "
                          "--copy-calibration into the traffic record read by the roofline (no GPU needed)")
@@ -199,14 +207,15 @@ def main():
     L = w.L
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    inp = make_inputs(w, seed=4)
+    gated = args.gated
+    inp = make_inputs(w, seed=4, gated=gated)
     x = {}
     for key, val in inp.items():
         if val is None:
             x[key] = None
             continue
         t = torch.from_numpy(np.ascontiguousarray(val))
-        if key not in ("g", "Ub", "Uw", "Vb", "Vw", "S0", "dS_T"):
+        if key not in ("g", "A", "tau_f", "Ub", "Uw", "Vb", "Vw", "S0", "dS_T"):
             t = t.to(torch.bfloat16)
         x[key] = t.to(dev)
     B, T, H, d, R = w.B, w.T, w.H, w.Dk, w.R
@@ -224,17 +233,31 @@ def main():
                "dUb": torch.empty((R, d), dtype=f32, device=dev), "dUw": torch.empty((R, d), dtype=f32, device=dev),
                "dVb": torch.empty((d, R), dtype=f32, device=dev), "dVw": torch.empty((d, R), dtype=f32, device=dev),
                "dS0": torch.empty((B, H, d, d), dtype=f32, device=dev)}
+    if gated:
+        del bwd_out["dg"]
+        bwd_out.update({"df": torch.empty((B, T, H, d), dtype=bf, device=dev),
+                        "dA": torch.empty((H, d), dtype=f32, device=dev),
+                        "dtau": torch.empty((H, d), dtype=f32, device=dev)})
     dims = carve.make_dims(B, T, H, d, d, R, L, bf)
     ws = torch.empty(max(carve.workspace_size(dims, True), 16), dtype=torch.uint8, device=dev)
 
     def fwd():
-        carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
-                        x["Vb"], x["Vw"], x["S0"], L=L, out=fwd_out)
+        if gated:
+            carve.chunk_fwd_gated(x["q"], x["k"], x["v"], x["beta"], x["f"], x["A"], x["tau_f"], x["bx"], x["wx"],
+                                  x["Ub"], x["Uw"], x["Vb"], x["Vw"], x["S0"], L=L, out=fwd_out)
+        else:
+            carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
+                            x["Vb"], x["Vw"], x["S0"], L=L, out=fwd_out)
 
     def bwd():
-        carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
-                        x["Vb"], x["Vw"], fwd_out["S_chunks"], x["dO"], None, L=L, out=bwd_out,
-                        workspace=ws)
+        if gated:
+            carve.chunk_bwd_gated(x["q"], x["k"], x["v"], x["beta"], x["f"], x["A"], x["tau_f"], x["bx"], x["wx"],
+                                  x["Ub"], x["Uw"], x["Vb"], x["Vw"], fwd_out["S_chunks"], x["dO"], None, L=L,
+                                  out=bwd_out, workspace=ws)
+        else:
+            carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
+                            x["Vb"], x["Vw"], fwd_out["S_chunks"], x["dO"], None, L=L, out=bwd_out,
+                            workspace=ws)
 
     for _ in range(args.warmup):
         fwd()
@@ -242,7 +265,8 @@ def main():
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     # launch-boundary events recorded by the library: forward 1 kernel, backward 6
-    NF, NB = 2, 7
+    # (7 with the gate-in-kernel decay: the reduction of dA, dtau)
+    NF, NB = 2, (8 if gated else 7)
     ev_f = [[torch.cuda.Event(enable_timing=True) for _ in range(NF)] for _ in range(args.steps)]
     ev_b = [[torch.cuda.Event(enable_timing=True) for _ in range(NB)] for _ in range(args.steps)]
     for e in [x for row in ev_f + ev_b for x in row]:
@@ -263,20 +287,22 @@ def main():
 
     bwd_names = ["carve_sync_clear_kernel", "carve_bwd_fused_kernel", "carve_bwd_vparam_kernel",
                  "carve_bwd_uparam_kernel", "carve_param_reduce_kernel[dU]", "carve_param_reduce_kernel[dV]"]
+    if gated:
+        bwd_names.append("carve_gate_reduce_kernel")
     kernels_ms = {"carve_chain_fwd_kernel": avg(ev_f, 0)}
     for i, name in enumerate(bwd_names):
         kernels_ms[name] = avg(ev_b, i)
     fwd_ms = kernels_ms["carve_chain_fwd_kernel"]
     bwd_ms = sum(r[0].elapsed_time(r[NB - 1]) for r in ev_b) / args.steps
     tokens = B * T
-    cnt = algorithmic_counts(B, T, H, d, R, L)
+    cnt = algorithmic_counts(B, T, H, d, R, L, gated)
 
     alg = {"carve_chain_fwd_kernel": cnt["fwd_bytes"], "carve_bwd_fused_kernel": cnt["bwd_bytes"]}
     dominant = max(alg, key=lambda k_: kernels_ms[k_])
     dom_ms = kernels_ms[dominant]
     dom_bytes = alg[dominant]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-    traffic = load_traffic(dominant)
+    traffic = None if gated else load_traffic(dominant)   # counters were taken on the ungated run
     layer_tflops = (cnt["fwd_flops"] + cnt["bwd_flops"]) / (ms_per_step * 1e-3) / 1e12
     res = {
         "metric": METRIC,
@@ -292,7 +318,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": w.name, "B": B, "H": H, "T": T, "Dk": d, "Dv": d, "R": R, "L": L,
-                   "token_dtype": "bf16", "state_dtype": "f32"},
+                   "token_dtype": "bf16", "state_dtype": "f32",
+                   "decay": "formed in the kernels from f, A, tau_f" if gated else "g input (f32)"},
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": None if traffic is None else traffic / (dom_ms * 1e-3) / 1e9,
@@ -306,7 +333,7 @@ def main():
         "layer_tflops": layer_tflops,
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(w, L, seed=4)
+        res["cpu_baseline"] = cpu_baseline(w, L, seed=4, gated=gated)
     print(json.dumps(res), flush=True)
 
 

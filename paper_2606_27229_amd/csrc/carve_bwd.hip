@@ -92,7 +92,8 @@ __device__ __forceinline__ int acquire_ready(const int* rdy, const int need) {
 // record is complete; smem is the workgroup's dynamic LDS (BwdLds layout).
 // GATED: g is formed from its staged raw logit f (Eq. decay_gate); the kernel
 // writes df = dg (-exp(A)) sigmoid(f + tau_f) instead of dg and sums dA = dg g
-// and dtau = df over its tokens into a per-(batch, head) partial.
+// and dtau = df over its tokens (per lane in registers, reduced once at the
+// end) into a per-(batch, head) partial.
 template <typename T, int D, int RP, bool GATED>
 __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char* smem, const int* ready) {
   typedef Quad<T> Qd;
@@ -160,7 +161,6 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   float* __restrict__ dgo = GATED ? nullptr : a.dg + bh0;
   T* __restrict__ dfo = GATED ? reinterpret_cast<T*>(a.df) + bh0 : nullptr;
   float* sGate = reinterpret_cast<float*>(smem + lay.Gate);   // [2][D] -exp(A), tau_f (GATED)
-  float* sGacc = reinterpret_cast<float*>(smem + lay.Gacc);   // [2][D] dA, dtau sums (GATED)
   T* sFs = reinterpret_cast<T*>(sGs);                          // [16][D] staged f (GATED)
   const ChunkRec cr = chunk_rec(sizeof(T), D, L, RP);
   const char* recb = reinterpret_cast<const char*>(a.rec) + (size_t)bh * nch * cr.total;
@@ -178,8 +178,6 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
     for (int x = tid; x < D; x += NT) {
       sGate[x] = -expf(a.A[h * D + x]);
       sGate[D + x] = a.tau_f[h * D + x];
-      sGacc[x] = 0.0f;
-      sGacc[D + x] = 0.0f;
     }
 #define CARVE_FVB(KS_) Qd::ld_tr(sVbT, LDD, 16 * (KS_), 16 * w, g, c)
 #define CARVE_FVW(KS_) Qd::ld_tr(sVwT, LDD, 16 * (KS_), 16 * w, g, c)
@@ -193,6 +191,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   for (int jt = 0; jt < NJT; ++jt)
     dSt[jt] = a.dS_T ? gload4(a.dS_T + soff + (16 * w + c) * D + 16 * jt + 4 * g) : zero4();
   f32x4 dF[NRT];                  // dF[r = 16 rt + 4 g + i][j = 16 w + c]
+  // GATED: this lane's sums over its tokens of dg g and df (channels 16 w + 4 g + i)
+  f32x4 gaccA = zero4(), gaccT = zero4();
   for (int rt = 0; rt < NRT; ++rt) dF[rt] = zero4();
 
   // ---- prefetch registers: the next block to process (reverse order) and, at
@@ -618,26 +618,19 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         Qd::st(dk + e0, Qd::cvt(dkv));
         if constexpr (GATED) {
           // through Eq. decay_gate: df = dg (-exp(A)) sigmoid(f + tau_f); dA and
-          // dtau collect dg g and df, summed over the block's 16 tokens (the
-          // lanes of a row) and added by lane c = 0 (one owner per channel)
+          // dtau collect dg g and df
           const f32x4 fv = Qd::f32(lfq);
           const f32x4 na = *reinterpret_cast<const f32x4*>(sGate + 16 * w + 4 * g);
           const f32x4 tf = *reinterpret_cast<const f32x4*>(sGate + D + 16 * w + 4 * g);
-          f32x4 dfv, sA, sT;
+          f32x4 dfv;
           for (int i = 0; i < 4; ++i) {
             float sp, sg;
             softplus_sigmoid(fv[i] + tf[i], sp, sg);
             dfv[i] = dgv[i] * na[i] * sg;
-            sA[i] = row_suffix(dgv[i] * na[i] * sp);
-            sT[i] = row_suffix(dfv[i]);
+            gaccA[i] += dgv[i] * na[i] * sp;
+            gaccT[i] += dfv[i];
           }
           Qd::st(dfo + e0, Qd::cvt(dfv));
-          if (c == 0) {
-            f32x4* pa = reinterpret_cast<f32x4*>(sGacc + 16 * w + 4 * g);
-            f32x4* pt = reinterpret_cast<f32x4*>(sGacc + D + 16 * w + 4 * g);
-            *pa = *pa + sA;
-            *pt = *pt + sT;
-          }
         } else {
           *reinterpret_cast<f32x4*>(dgo + e0) = dgv;
         }
@@ -725,8 +718,17 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
 #undef CARVE_BWD_LOADS
 #undef CARVE_BWD_LOADF
   if constexpr (GATED) {
-    // every update of the sums was made before a barrier of the last block
-    for (int x = tid; x < 2 * D; x += NT) a.partG[(size_t)bh * 2 * D + x] = sGacc[x];
+    // the lanes' sums over their tokens, reduced over the 16 lanes of a row
+    // (all tokens of a block) and written by lane c = 0, one owner per channel
+    for (int i = 0; i < 4; ++i) {
+      gaccA[i] = row_suffix(gaccA[i]);
+      gaccT[i] = row_suffix(gaccT[i]);
+    }
+    if (c == 0) {
+      float* dst = a.partG + (size_t)bh * 2 * D + 16 * w + 4 * g;
+      *reinterpret_cast<f32x4*>(dst) = gaccA;
+      *reinterpret_cast<f32x4*>(dst + D) = gaccT;
+    }
   }
   if (a.dS0) {
     float* dst = a.dS0 + soff + (16 * w + c) * D + 4 * g;
