@@ -86,3 +86,56 @@ def test_full_size_sampled(name, L):
     print("max-rel errors:", {k: float("%.3g" % e) for k, e in errs.items()}, flush=True)
     bad = {k: e for k, e in errs.items() if not e <= TOL}
     assert not bad, bad
+
+
+def test_full_size_gated_sampled():
+    """The gate-in-kernel variant at the headline size (B=4 H=16 T=4096 L=64):
+    sampled slices as above; dA and dtau of a head are sums over that head's
+    slices, so with the upstream gradients zeroed outside the samples the
+    sampled heads' rows must equal the slices' oracle rows and every other
+    head's rows must be zero."""
+    w = WORKLOADS["layer_1p3b_T4096"].with_(L=64)
+    L = 64
+    print(f"case gated {w.name} L={L}", flush=True)
+    inp = make_inputs(w, seed=7, dS_T=True, gated=True)
+    samples = [(0, 0), (w.B - 1, w.H - 1)]
+    keep = np.zeros((w.B, w.H), dtype=bool)
+    for b, h in samples:
+        keep[b, h] = True
+    inp["dO"] = inp["dO"] * keep[:, None, :, None]
+    inp["dS_T"] = inp["dS_T"] * keep[:, :, None, None]
+    x = to_gpu(inp, torch.bfloat16)
+    args = (x["q"], x["k"], x["v"], x["beta"], x["f"], x["A"], x["tau_f"], x["bx"], x["wx"],
+            x["Ub"], x["Uw"], x["Vb"], x["Vw"])
+    o, S_T, S_chunks = carve.chunk_fwd_gated(*args, x["S0"], L=L)
+    gr = carve.chunk_bwd_gated(*args, S_chunks, x["dO"], x["dS_T"], L=L)
+    torch.cuda.synchronize()
+    del x
+    errs = {}
+    dA, dtau = host(gr["dA"]), host(gr["dtau"])
+    for b, h in samples:
+        s = {}
+        for key, val in inp.items():
+            if val is None:
+                s[key] = None
+            elif key in TOKEN_KEYS + ("f",):
+                s[key] = np.ascontiguousarray(val[b:b + 1, :, h:h + 1])
+            elif key in ("S0", "dS_T"):
+                s[key] = np.ascontiguousarray(val[b:b + 1, h:h + 1])
+            elif key in ("A", "tau_f"):
+                s[key] = np.ascontiguousarray(val[h:h + 1])
+            else:
+                s[key] = val
+        rf = orc.fwd_gated(s, L, want_chunks=True)
+        rb = orc.bwd_gated(s, L, s["dO"], s["dS_T"])
+        errs[f"o[{b},{h}]"] = max_rel(host(o[b:b + 1, :, h:h + 1]), rf["o"])
+        errs[f"S_chunks[{b},{h}]"] = max_rel(host(S_chunks[b:b + 1, h:h + 1]), rf["S_chunks"])
+        for key in ("dq", "dk", "dv", "dbeta", "df", "dbx", "dwx"):
+            errs[f"{key}[{b},{h}]"] = max_rel(host(gr[key][b:b + 1, :, h:h + 1]), rb[key])
+        errs[f"dA[{h}]"] = max_rel(dA[h:h + 1], rb["dA"])
+        errs[f"dtau[{h}]"] = max_rel(dtau[h:h + 1], rb["dtau"])
+    others = [h for h in range(w.H) if h not in (0, w.H - 1)]
+    assert np.all(dA[others] == 0) and np.all(dtau[others] == 0)
+    print("max-rel errors:", {k: float("%.3g" % e) for k, e in errs.items()}, flush=True)
+    bad = {k: e for k, e in errs.items() if not e <= TOL}
+    assert not bad, bad
