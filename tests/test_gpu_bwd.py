@@ -103,3 +103,21 @@ def test_backward_deterministic():
     b = run_gpu(w, inp)
     for key in GRADS:
         assert np.array_equal(a[key], b[key]), key
+
+
+def test_bf16_many_heads_recompute_first():
+    """B*H = 208 adjoint workgroups at d = 128 (one workgroup per CU): fewer than
+    a quarter of the CUs would remain for the recompute, so the fused launch
+    gives the recompute the whole device first and the adjoint workgroups
+    queue behind it (their roles come by ticket, so nothing waits on a
+    workgroup that is not running)."""
+    w = _w(B=13, H=16, Dk=128, Dv=128, L=16, T=64, R=32, dtype="bf16", mu=3.0, s0=0.1)
+    print("case bf16 D=128 B*H=208", flush=True)
+    check_bwd(w, make_inputs(w, seed=208, dS_T=True))
+
+
+def test_bf16_single_chunk():
+    """T = L: one chunk (the fold reads only S0, the glue runs once)."""
+    w = _w(Dk=128, Dv=128, L=64, T=64, R=32, dtype="bf16", mu=3.0, s0=0.2)
+    print("case bf16 D=128 T=L=64", flush=True)
+    check_bwd(w, make_inputs(w, seed=64, dS_T=True))
