@@ -204,3 +204,43 @@ def bwd_gated(inp, L, dO, dS_T=None, nthreads=None):
     out = bwd(_with_gate(inp), L, dO, dS_T, nthreads=nthreads)
     out["df"], out["dA"], out["dtau"] = decay_gate_bwd(inp["f"], inp["A"], inp["tau_f"], out.pop("dg"))
     return out
+
+
+def scalar_write_inputs(inp):
+    """The inputs of the full layer that define the scalar write gate (Sec. scalar
+    write gate, ablation rows of Table attribution): a per-head logit wx [B,T,H],
+    w_t = sigmoid(wx_t) on every one of the Dv value channels, and no content
+    term on the write side.  The full layer gives exactly that with wx repeated
+    along the value axis and Uw = Vw = 0 (then Vw tau_w = 0 whatever tau_w is).
+    Any Uw, Vw in ``inp`` are ignored."""
+    out = dict(inp)
+    wx = _f64(inp["wx"])
+    Dv = np.shape(inp["v"])[-1]
+    R = np.shape(inp["Ub"])[0]
+    out["wx"] = np.repeat(wx[..., None], Dv, axis=-1)
+    out["Uw"] = np.zeros((R, Dv))
+    out["Vw"] = np.zeros((Dv, R))
+    return out
+
+
+def fwd_sw(inp, L, want_chunks=False, nthreads=None):
+    """The layer with the scalar write gate; the decay is g, or (when ``inp``
+    holds f) formed from f, A, tau_f by Eq. decay_gate."""
+    x = scalar_write_inputs(inp)
+    if inp.get("f") is not None:
+        return fwd_gated(x, L, want_chunks=want_chunks, nthreads=nthreads)
+    return fwd_serial(x, L, want_chunks=want_chunks, nthreads=nthreads)
+
+
+def bwd_sw(inp, L, dO, dS_T=None, nthreads=None):
+    """Reverse mode of ``fwd_sw``: dwx [B,T,H] is the sum over the value
+    channels of the full layer's dwx (the logit is shared by all of them);
+    there is no dUw, dVw.  dg, or df, dA, dtau when ``inp`` holds f."""
+    x = scalar_write_inputs(inp)
+    if inp.get("f") is not None:
+        out = bwd_gated(x, L, dO, dS_T, nthreads=nthreads)
+    else:
+        out = bwd(x, L, dO, dS_T, nthreads=nthreads)
+    out["dwx"] = out["dwx"].sum(axis=-1)
+    del out["dUw"], out["dVw"]
+    return out

@@ -22,6 +22,10 @@ g = -exp(A) softplus(f + tau_f)) three more arrays are drawn after the others
   A      ~ N(0, 0.1^2) of shape [H, Dk]          f32 log-amplitudes
   tau_f  ~ N(-mu, 0.1^2) of shape [H, Dk]        f32 biases
 so that f + tau_f ~ N(-mu, 1.01) and g is close in law to logsigmoid(N(mu,1)).
+With the scalar write gate (scalar_write=True; Sec. scalar write gate) the
+per-head write logit is drawn last (after the gated arrays, if any), replacing
+the per-channel one, and Uw, Vw are left out:
+  wx     ~ N(0,1) of shape [B, T, H]             token dtype
 Token tensors of a bf16 workload are rounded to bf16 (round to nearest even)
 and the rounded values are what every consumer receives; g, the parameters
 and the states stay f32.
@@ -112,12 +116,14 @@ def _logsigmoid(x):
 
 
 def make_inputs(w: Workload, seed: int = 0, *, zero_content: bool = False,
-                dS_T: bool = False, bx_mean: float | None = None, gated: bool = False) -> dict:
+                dS_T: bool = False, bx_mean: float | None = None, gated: bool = False,
+                scalar_write: bool = False) -> dict:
     """Draw one seeded input set for workload ``w``.
 
     zero_content: Ub = Uw = 0 (the memory-blind special case).
     bx_mean:      override the erase-logit location (erase-heavy stress uses 0).
     gated:        raw decay logits f with per-head A, tau_f instead of g.
+    scalar_write: a per-head write logit wx [B,T,H] and no Uw, Vw.
     """
     rng = np.random.Generator(np.random.PCG64(seed))
     B, T, H, Dk, Dv, R = w.B, w.T, w.H, w.Dk, w.Dv, w.R
@@ -148,4 +154,9 @@ def make_inputs(w: Workload, seed: int = 0, *, zero_content: bool = False,
         out["tau_f"] = _normal(rng, (H, Dk), std=0.1, mean=-w.mu)
         out["f"] = round_bf16(f) if w.dtype == "bf16" else f
         out["g"] = None
+    if scalar_write:
+        wxs = _normal(rng, (B, T, H))
+        out["wx"] = round_bf16(wxs) if w.dtype == "bf16" else wxs
+        out["Uw"] = None
+        out["Vw"] = None
     return out

@@ -464,3 +464,115 @@ def test_gated_backward_coordinates_of_A_and_tau():
             fd = (_gated_loss(xp, 4) - _gated_loss(xm, 4)) / (2 * h)
             an = gr[gname].reshape(-1)[idx]
             assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-2), (name, idx, fd, an)
+
+
+# --------------------------------------------------------------------------
+# scalar write gate (Sec. scalar write gate; ablation rows (a), (b) of Table
+# attribution): one logit per (token, head), w = sigmoid(wx) on every value
+# channel, no content term on the write side
+# --------------------------------------------------------------------------
+def _sw(w, seed, **kw):
+    return _f64(make_inputs(w, seed=seed, scalar_write=True, **kw))
+
+
+def test_scalar_write_single_slot_retrieval():
+    """One write into empty memory read with q = k_w (App. proof of Thm. scalar
+    write sufficiency): the read-out is beta sigmoid(wx) ||k_w||^2 v_w, parallel
+    to v_w; the per-channel gate of the same example is not."""
+    ex = json.load(open(os.path.join(GOLDEN, "scalar_write_example.json")))
+    kw = np.array(ex["k_w"]); vw = np.array(ex["v_w"]); beta = ex["beta"]; ws = ex["wx_scalar"]
+    d, dv = kw.size, vw.size
+    inp = {
+        "q": kw[None, None, None, :], "k": kw[None, None, None, :], "v": vw[None, None, None, :],
+        "beta": np.array([[[beta]]]), "g": np.zeros((1, 1, 1, d)), "bx": np.zeros((1, 1, 1, d)),
+        "wx": np.array([[[ws]]]), "Ub": np.ones((2, dv)), "Vb": np.ones((d, 2)), "S0": None,
+    }
+    out = orc.fwd_sw(inp, 1)
+    o = out["o"][0, 0, 0]
+    np.testing.assert_allclose(o, beta * _sig(ws) * float(kw @ kw) * vw, rtol=1e-15)
+    np.testing.assert_allclose(out["S_T"][0, 0], beta * _sig(ws) * np.outer(vw, kw), rtol=1e-15, atol=0)
+    cos = float(o @ vw) / (np.linalg.norm(o) * np.linalg.norm(vw))
+    assert abs(cos - 1.0) < 1e-15
+    full = dict(inp); full["wx"] = np.array(ex["wx"])[None, None, None, :]
+    full["Uw"] = np.ones((2, dv)); full["Vw"] = np.ones((dv, 2))
+    of = orc.fwd_serial(full, 1)["o"][0, 0, 0]
+    assert float(of @ vw) / (np.linalg.norm(of) * np.linalg.norm(vw)) < 0.99
+
+
+def test_scalar_write_content_off_is_memory_blind_baseline():
+    """Row (a) of the ablation (Ub = 0, content off): the memory-blind
+    recurrence (the baseline's separate implementation) with the per-head
+    write logit on every value channel, bit for bit."""
+    w = _small(T=64, L=16, s0=0.2)
+    inp = _sw(w, 4)
+    inp["Ub"] = np.zeros_like(inp["Ub"])
+    a = orc.fwd_sw(inp, 16)
+    x = dict(inp); x["wx"] = np.repeat(inp["wx"][..., None], w.Dv, axis=-1)
+    base = orc.baseline_fwd(x)
+    assert np.array_equal(a["o"], base["o"]) and np.array_equal(a["S_T"], base["S_T"])
+
+
+def test_scalar_write_erase_content_still_acts():
+    """Row (b) (content-aware erase, scalar write): Ub still changes the result."""
+    w = _small(T=64, L=16, s0=0.5)
+    inp = _sw(w, 8)
+    x = dict(inp); x["Ub"] = np.zeros_like(inp["Ub"])
+    a, b = orc.fwd_sw(inp, 16), orc.fwd_sw(x, 16)
+    assert _rel(a["o"], b["o"]) > 1e-4
+
+
+SW_GRADS = [("wx", "dwx"), ("q", "dq"), ("k", "dk"), ("v", "dv"), ("beta", "dbeta"), ("g", "dg"),
+            ("bx", "dbx"), ("Ub", "dUb"), ("Vb", "dVb"), ("S0", "dS0")]
+
+
+def _sw_loss(x, L):
+    o = orc.fwd_sw(x, L)
+    return float(np.sum(o["o"] * x["dO"]) + np.sum(o["S_T"] * x["dS_T"]))
+
+
+@pytest.mark.parametrize("L,T,Dk,Dv,R", [(8, 32, 8, 6, 3), (4, 16, 5, 7, 2)])
+def test_scalar_write_backward_directional_finite_differences(L, T, Dk, Dv, R):
+    w = Workload("fd", B=2, H=2, T=T, Dk=Dk, Dv=Dv, L=L, R=R, dtype="f32", mu=2.0, s0=0.3, u_std=0.4)
+    inp = _sw(w, L + Dv, dS_T=True)
+    gr = orc.bwd_sw(inp, L, inp["dO"], inp["dS_T"])
+    assert gr["dwx"].shape == (2, T, 2) and "dUw" not in gr and "dVw" not in gr
+    rng = np.random.default_rng(L + 1)
+    h = 1e-6
+    for name, gname in SW_GRADS:
+        dirn = rng.standard_normal(inp[name].shape)
+        xp = dict(inp); xp[name] = inp[name] + h * dirn
+        xm = dict(inp); xm[name] = inp[name] - h * dirn
+        fd = (_sw_loss(xp, L) - _sw_loss(xm, L)) / (2 * h)
+        an = float(np.sum(gr[gname] * dirn))
+        assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-3), (name, fd, an)
+
+
+def test_scalar_write_backward_every_logit_coordinate():
+    w = Workload("fd", B=1, H=2, T=8, Dk=4, Dv=6, L=4, R=2, dtype="f32", mu=2.0, s0=0.3, u_std=0.5)
+    inp = _sw(w, 21, dS_T=True)
+    gr = orc.bwd_sw(inp, 4, inp["dO"], inp["dS_T"])
+    h = 1e-6
+    for idx in range(inp["wx"].size):
+        xp = dict(inp); xp["wx"] = inp["wx"].copy(); xp["wx"].reshape(-1)[idx] += h
+        xm = dict(inp); xm["wx"] = inp["wx"].copy(); xm["wx"].reshape(-1)[idx] -= h
+        fd = (_sw_loss(xp, 4) - _sw_loss(xm, 4)) / (2 * h)
+        an = gr["dwx"].reshape(-1)[idx]
+        assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-2), (idx, fd, an)
+
+
+def test_scalar_write_with_decay_gate_backward_finite_differences():
+    """Both deployment options at once: the decay from its raw logit and the
+    scalar write gate."""
+    w = Workload("fd", B=2, H=2, T=16, Dk=6, Dv=5, L=4, R=2, dtype="f32", mu=1.0, s0=0.3, u_std=0.4)
+    inp = _f64(make_inputs(w, seed=9, dS_T=True, gated=True, scalar_write=True))
+    gr = orc.bwd_sw(inp, 4, inp["dO"], inp["dS_T"])
+    assert "dg" not in gr and gr["dwx"].shape == (2, 16, 2)
+    rng = np.random.default_rng(2)
+    h = 1e-6
+    for name, gname in (("wx", "dwx"), ("f", "df"), ("A", "dA"), ("tau_f", "dtau"), ("Ub", "dUb"), ("v", "dv")):
+        dirn = rng.standard_normal(inp[name].shape)
+        xp = dict(inp); xp[name] = inp[name] + h * dirn
+        xm = dict(inp); xm[name] = inp[name] - h * dirn
+        fd = (_sw_loss(xp, 4) - _sw_loss(xm, 4)) / (2 * h)
+        an = float(np.sum(gr[gname] * dirn))
+        assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-3), (name, fd, an)
