@@ -24,13 +24,13 @@ sys.path.insert(0, ROOT)
 METRIC = "layer fwd+bwd tokens/s, H=16 d=128 T=4096 L=64 bf16; % MFMA peak"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
-KERNEL_SOURCES = ("paper_2606_27229_amd/csrc/carve_fwd_chain.hip", "paper_2606_27229_amd/csrc/carve_rec.h",
-                  "paper_2606_27229_amd/csrc/carve_bwd.hip", "paper_2606_27229_amd/csrc/carve_dev.h",
-                  "paper_2606_27229_amd/csrc/carve_kernels.h")
+KERNEL_SOURCES = tuple("paper_2606_27229_amd/csrc/" + f for f in (
+    "carve_fwd_chain.h", "carve_fwd_chain.hip", "carve_rec.h", "carve_bwd.h", "carve_bwd.hip", "carve_dev.h",
+    "carve_kernels.h", "carve_variant.hip"))
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer_1p3b_T4096_L64.json")
 
 
-def algorithmic_counts(B, T, H, d, R, L, gated=False):
+def algorithmic_counts(B, T, H, d, R, L, gated=False, sw=False):
     """Algorithmic bytes and flops per call (every input and output once).
 
     Bytes per token-head (bf16 token tensors, f32 g and states):
@@ -43,15 +43,21 @@ def algorithmic_counts(B, T, H, d, R, L, gated=False):
                        recompute + adjoint kernel is priced at this figure
     With the gate-in-kernel decay the f32 g (4d) is replaced by the bf16 logit
     f (2d) and dg by df (2d); A, tau_f and dA, dtau are per head (negligible).
+    With the scalar write gate wx and dwx are one bf16 value per token-head (2
+    each instead of 2d) and the fold and the content projection lose their
+    write half.
     Flops per token-head (multiply-add = 2): forward
-      2 * (2 r d^2 / L + 3 d^2 + 4 r d + 5/2 L d + L^2 / 6), backward 2x forward.
+      2 * (2 r d^2 / L + 3 d^2 + 4 r d + 5/2 L d + L^2 / 6)
+      (r d^2 / L and 2 r d with the scalar write gate), backward 2x forward.
     """
     th = B * T * H
     decay = 2 * d if gated else 4 * d
-    inputs = 3 * 2 * d + decay + 2 * 2 * d + 2
-    grads = 3 * 2 * d + decay + 2 * 2 * d + 2
+    wxb = 2 if sw else 2 * d
+    inputs = 3 * 2 * d + decay + 2 * d + wxb + 2
+    grads = 3 * 2 * d + decay + 2 * d + wxb + 2
     states = 4 * d * d / L
-    fwd_mac = 2 * R * d * d / L + 3 * d * d + 4 * R * d + 2.5 * L * d + L * L / 6.0
+    rf = 1 if sw else 2       # fold rows per rank unit
+    fwd_mac = rf * R * d * d / L + 3 * d * d + 2 * rf * R * d + 2.5 * L * d + L * L / 6.0
     return {
         "fwd_bytes": (inputs + 2 * d + states) * th,
         "adjoint_bytes": (inputs + 2 * d + grads) * th,
@@ -134,16 +140,19 @@ def traffic_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir):
     print(json.dumps(rec), flush=True)
 
 
-def cpu_baseline(w, L, seed, target_s=12.0, gated=False):
+def cpu_baseline(w, L, seed, target_s=12.0, gated=False, sw=False):
     """Time the CPU oracle (token-serial forward + exact backward, double) on the
     whole workload batch, repeated until about target_s seconds of CPU work."""
     from oracle import oracle as orc
     from paper_2606_27229_amd.inputs import make_inputs
 
-    inp = make_inputs(w, seed=seed, gated=gated)
+    inp = make_inputs(w, seed=seed, gated=gated, scalar_write=sw)
     threads = max(1, min(16, os.cpu_count() or 1, w.B * w.H))
-    fwd = orc.fwd_gated if gated else orc.fwd_serial
-    bwd = orc.bwd_gated if gated else orc.bwd
+    if sw:
+        fwd, bwd = orc.fwd_sw, orc.bwd_sw
+    else:
+        fwd = orc.fwd_gated if gated else orc.fwd_serial
+        bwd = orc.bwd_gated if gated else orc.bwd
     reps, t_f, t_b = 0, 0.0, 0.0
     while reps == 0 or t_f + t_b < target_s:
         t0 = time.perf_counter()
@@ -171,6 +180,9 @@ def main():
     ap.add_argument("--gated", action="store_true",
                     help="the gate-in-kernel variant: the decay is formed in the kernels from its raw "
                          "logit f (bf16) and per-head A, tau_f (carve_chunk_fwd_gated / _bwd_gated)")
+    ap.add_argument("--scalar-write", action="store_true",
+                    help="the scalar write gate: one write logit per token and head, no write-side "
+                         "content (carve_chunk_fwd_sw / _bwd_sw; with --gated, the decay from f)")
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
                     help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of this benchmark and of "
                          "--copy-calibration into the traffic record read by the roofline (no GPU needed)")
@@ -183,7 +195,7 @@ def main():
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: the layer shards over (batch, head) with no exchange "
-              "except a 64 KB parameter-gradient all-reduce, which this build does not run; "
+              "except a 64 KB parameter-gradient all-reduce, which this benchmark does not run; "
               "use --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
@@ -207,8 +219,8 @@ def main():
     L = w.L
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    gated = args.gated
-    inp = make_inputs(w, seed=4, gated=gated)
+    gated, sw = args.gated, args.scalar_write
+    inp = make_inputs(w, seed=4, gated=gated, scalar_write=sw)
     x = {}
     for key, val in inp.items():
         if val is None:
@@ -238,11 +250,18 @@ def main():
         bwd_out.update({"df": torch.empty((B, T, H, d), dtype=bf, device=dev),
                         "dA": torch.empty((H, d), dtype=f32, device=dev),
                         "dtau": torch.empty((H, d), dtype=f32, device=dev)})
+    if sw:
+        del bwd_out["dUw"], bwd_out["dVw"]
+        bwd_out["dwx"] = torch.empty((B, T, H), dtype=bf, device=dev)
+    decay = dict(f=x["f"], A=x["A"], tau_f=x["tau_f"]) if gated else dict(g=x["g"])
     dims = carve.make_dims(B, T, H, d, d, R, L, bf)
     ws = torch.empty(max(carve.workspace_size(dims, True), 16), dtype=torch.uint8, device=dev)
 
     def fwd():
-        if gated:
+        if sw:
+            carve.chunk_fwd_sw(x["q"], x["k"], x["v"], x["beta"], x["bx"], x["wx"], x["Ub"], x["Vb"], x["S0"],
+                               L=L, out=fwd_out, **decay)
+        elif gated:
             carve.chunk_fwd_gated(x["q"], x["k"], x["v"], x["beta"], x["f"], x["A"], x["tau_f"], x["bx"], x["wx"],
                                   x["Ub"], x["Uw"], x["Vb"], x["Vw"], x["S0"], L=L, out=fwd_out)
         else:
@@ -250,7 +269,10 @@ def main():
                             x["Vb"], x["Vw"], x["S0"], L=L, out=fwd_out)
 
     def bwd():
-        if gated:
+        if sw:
+            carve.chunk_bwd_sw(x["q"], x["k"], x["v"], x["beta"], x["bx"], x["wx"], x["Ub"], x["Vb"],
+                               fwd_out["S_chunks"], x["dO"], None, L=L, out=bwd_out, workspace=ws, **decay)
+        elif gated:
             carve.chunk_bwd_gated(x["q"], x["k"], x["v"], x["beta"], x["f"], x["A"], x["tau_f"], x["bx"], x["wx"],
                                   x["Ub"], x["Uw"], x["Vb"], x["Vw"], fwd_out["S_chunks"], x["dO"], None, L=L,
                                   out=bwd_out, workspace=ws)
@@ -295,14 +317,15 @@ def main():
     fwd_ms = kernels_ms["carve_chain_fwd_kernel"]
     bwd_ms = sum(r[0].elapsed_time(r[NB - 1]) for r in ev_b) / args.steps
     tokens = B * T
-    cnt = algorithmic_counts(B, T, H, d, R, L, gated)
+    cnt = algorithmic_counts(B, T, H, d, R, L, gated, sw)
 
     alg = {"carve_chain_fwd_kernel": cnt["fwd_bytes"], "carve_bwd_fused_kernel": cnt["bwd_bytes"]}
     dominant = max(alg, key=lambda k_: kernels_ms[k_])
     dom_ms = kernels_ms[dominant]
     dom_bytes = alg[dominant]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-    traffic = None if gated else load_traffic(dominant)   # counters were taken on the ungated run
+    # the counters were taken on the default variant
+    traffic = None if (gated or sw) else load_traffic(dominant)
     layer_tflops = (cnt["fwd_flops"] + cnt["bwd_flops"]) / (ms_per_step * 1e-3) / 1e12
     res = {
         "metric": METRIC,
@@ -319,7 +342,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": B, "H": H, "T": T, "Dk": d, "Dv": d, "R": R, "L": L,
                    "token_dtype": "bf16", "state_dtype": "f32",
-                   "decay": "formed in the kernels from f, A, tau_f" if gated else "g input (f32)"},
+                   "decay": "formed in the kernels from f, A, tau_f" if gated else "g input (f32)",
+                   "write_gate": "scalar per token and head" if sw else "per value channel, content-aware"},
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": None if traffic is None else traffic / (dom_ms * 1e-3) / 1e9,
@@ -333,7 +357,7 @@ def main():
         "layer_tflops": layer_tflops,
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(w, L, seed=4, gated=gated)
+        res["cpu_baseline"] = cpu_baseline(w, L, seed=4, gated=gated, sw=sw)
     print(json.dumps(res), flush=True)
 
 

@@ -83,7 +83,8 @@ enum {
   CARVE_ERR_UNSUPPORTED = -3, /* valid but not built: see "Supported shapes" */
   CARVE_ERR_ALIGN = -4,       /* a pointer is not 16-byte aligned */
   CARVE_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than carve_workspace_size */
-  CARVE_ERR_HIP = -6          /* a HIP runtime call failed */
+  CARVE_ERR_HIP = -6,         /* a HIP runtime call failed */
+  CARVE_ERR_ARG = -7          /* both of two alternative inputs given (g and f) */
 };
 
 /* Bytes of device workspace the forward (for_backward = 0) or the backward
@@ -153,6 +154,42 @@ int carve_chunk_bwd_gated(const carve_dims_t* d, const void* q, const void* k, c
                           float* dA, float* dtau, void* dbx, void* dwx, float* dUb, float* dUw,
                           float* dVb, float* dVw, float* dS0, void* workspace, size_t workspace_bytes,
                           hipStream_t stream);
+
+/* The layer with the scalar write gate (Sec. scalar write gate, the deployment
+ * variant of the ablation rows "scalar write" of Table attribution): one write
+ * logit per token and head, broadcast over the value channels, and no content
+ * term on the write side:
+ *     w_t = sigmoid(wx[b,t,h]) on every one of the Dv channels,
+ *     b_t = sigmoid(bx_t + Vb tanh(F_b q_t)) with F_b = Ub S_{c-1} (as before).
+ * The fold has R rows instead of 2R; there is no Uw, Vw.
+ * In:  wx [B,T,H] in the call's dtype (replacing the [B,T,H,Dv] logits);
+ *      the decay either as g [B,T,H,Dk] f32 (f = A = tau_f = NULL) or from its
+ *      raw logit as in carve_chunk_fwd_gated (g = NULL; f, A, tau_f given);
+ *      the other arguments are those of carve_chunk_fwd.
+ * Returns CARVE_ERR_NULL when neither g nor f is given, CARVE_ERR_ARG when
+ * both are.  Ub = 0 gives the ablation's row with no content at all. */
+int carve_chunk_fwd_sw(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                       const void* beta, const float* g, const void* f, const float* A,
+                       const float* tau_f, const void* bx, const void* wx, const float* Ub,
+                       const float* Vb, const float* S0, void* o, float* S_T, float* S_chunks,
+                       void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Backward of carve_chunk_fwd_sw for loss <dO, o> + <dS_T, S_T>.  Outputs as
+ * carve_chunk_bwd (dg with the g form; df, dA, dtau as carve_chunk_bwd_gated
+ * with the f form; the other decay outputs may be NULL), except:
+ *   dwx [B,T,H] in the call's dtype: the sum over the value channels of the
+ *   per-channel write-logit gradient, dL/dwx_t = sum_v dL/dw_tv * w_t (1 - w_t);
+ *   no dUw, dVw.
+ * The workspace is the one carve_workspace_size(d, 1) reports; the launch
+ * sequence (and the measurement hook's events) is that of the matching
+ * carve_chunk_bwd or carve_chunk_bwd_gated call. */
+int carve_chunk_bwd_sw(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                       const void* beta, const float* g, const void* f, const float* A,
+                       const float* tau_f, const void* bx, const void* wx, const float* Ub,
+                       const float* Vb, const float* S_chunks, const void* dO, const float* dS_T,
+                       void* dq, void* dk, void* dv, void* dbeta, float* dg, void* df, float* dA,
+                       float* dtau, void* dbx, void* dwx, float* dUb, float* dVb, float* dS0,
+                       void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Measurement hook (not part of the computation).  Arms the next
  * carve_chunk_fwd / carve_chunk_bwd call made on the calling thread to record

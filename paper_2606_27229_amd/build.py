@@ -14,7 +14,11 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libcarve.so")
-SOURCES = ["carve_abi.hip", "carve_fwd_chain.hip", "carve_bwd.hip"]
+# (source, object name, extra flags): carve_variant.hip is compiled once per
+# layer variant (decay given / formed in the kernels x full / scalar write gate)
+SOURCES = [("carve_abi.hip", "carve_abi", []), ("carve_fwd_chain.hip", "carve_fwd_chain", []),
+           ("carve_bwd.hip", "carve_bwd", [])] + [
+    ("carve_variant.hip", f"carve_variant{v}", [f"-DCARVE_VARIANT={v}"]) for v in range(4)]
 
 BUILD = os.path.join(HERE, "_build")
 HIPCC_FLAGS = [
@@ -46,10 +50,10 @@ def build(verbose: bool = False) -> str:
     """Compile every translation unit (in parallel) and link libcarve.so."""
     os.makedirs(BUILD, exist_ok=True)
     objs, cmds = [], []
-    for src in SOURCES:
-        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+    for src, name, extra in SOURCES:
+        obj = os.path.join(BUILD, name + ".o")
         objs.append(obj)
-        cmds.append([hipcc()] + HIPCC_FLAGS + ["-c", "-o", obj, os.path.join(CSRC, src)])
+        cmds.append([hipcc()] + HIPCC_FLAGS + extra + ["-c", "-o", obj, os.path.join(CSRC, src)])
     with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 1)) as ex:
         rcs = list(ex.map(lambda c: _run(c, verbose), cmds))
     if any(rcs):

@@ -18,7 +18,8 @@ LIB_PATH = os.path.join(_HERE, "libcarve.so")
 
 CARVE_F32, CARVE_BF16 = 0, 1
 SYMBOLS = ("carve_chunk_fwd", "carve_chunk_bwd", "carve_chunk_fwd_gated", "carve_chunk_bwd_gated",
-           "carve_workspace_size", "carve_status_string", "carve_profile_events")
+           "carve_chunk_fwd_sw", "carve_chunk_bwd_sw", "carve_workspace_size", "carve_status_string",
+           "carve_profile_events")
 
 
 class Dims(ctypes.Structure):
@@ -58,6 +59,11 @@ def load_library(path: str = LIB_PATH):
     lib.carve_chunk_bwd_gated.argtypes = ([D] + [vp] * 5 + [fp] * 2 + [vp] * 2 + [fp] * 5 + [vp, fp]
                                           + [vp] * 5 + [fp] * 2 + [vp] * 2 + [fp] * 5 + [vp, sz, vp])
     lib.carve_chunk_bwd_gated.restype = ctypes.c_int
+    lib.carve_chunk_fwd_sw.argtypes = [D] + [vp] * 4 + [fp, vp, fp, fp, vp, vp, fp, fp, fp, vp, fp, fp, vp, sz, vp]
+    lib.carve_chunk_fwd_sw.restype = ctypes.c_int
+    lib.carve_chunk_bwd_sw.argtypes = ([D] + [vp] * 4 + [fp, vp, fp, fp, vp, vp, fp, fp, fp, vp, fp]
+                                       + [vp] * 4 + [fp, vp, fp, fp, vp, vp, fp, fp, fp, vp, sz, vp])
+    lib.carve_chunk_bwd_sw.restype = ctypes.c_int
     lib.carve_profile_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]
     lib.carve_profile_events.restype = ctypes.c_int
     if path == LIB_PATH:
@@ -256,4 +262,81 @@ def chunk_bwd_gated(q, k, v, beta, f, A, tau_f, bx, wx, Ub, Uw, Vb, Vw, S_chunks
                                     "dUb", "dUw", "dVb", "dVw")],
         _ptr(res.get("dS0"), "dS0"), ws_ptr, ws_len, _stream(stream))
     _check("carve_chunk_bwd_gated", st)
+    return res
+
+
+def chunk_fwd_sw(q, k, v, beta, bx, wx, Ub, Vb, S0=None, *, g=None, f=None, A=None, tau_f=None, L=64,
+                 want_chunks=True, want_state=True, out=None, stream=None):
+    """Forward with the scalar write gate: wx [B,T,H] (one logit per token and
+    head, w = sigmoid(wx) on every value channel), no Uw, Vw.  The decay is g
+    (f32 [B,T,H,Dk]) or, with g=None, formed in the kernels from f, A, tau_f.
+    Returns (o, S_T, S_chunks)."""
+    lib = load_library()
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    R = Ub.shape[0]
+    dt = q.dtype
+    f32 = torch.float32
+    dims = make_dims(B, T, H, Dk, Dv, R, L, dt)
+    out = dict(out or {})
+    o = out.get("o")
+    if o is None:
+        o = torch.empty((B, T, H, Dv), dtype=dt, device=q.device)
+    S_T = out.get("S_T") if "S_T" in out else (torch.empty((B, H, Dv, Dk), dtype=f32, device=q.device) if want_state else None)
+    S_chunks = out.get("S_chunks") if "S_chunks" in out else (
+        torch.empty((B, H, T // L, Dv, Dk), dtype=f32, device=q.device) if want_chunks else None)
+    st = lib.carve_chunk_fwd_sw(
+        ctypes.byref(dims), _ptr(q, "q", dt, (B, T, H, Dk)), _ptr(k, "k", dt, (B, T, H, Dk)),
+        _ptr(v, "v", dt, (B, T, H, Dv)), _ptr(beta, "beta", dt, (B, T, H)), _ptr(g, "g", f32, (B, T, H, Dk)),
+        _ptr(f, "f", dt, (B, T, H, Dk)), _ptr(A, "A", f32, (H, Dk)), _ptr(tau_f, "tau_f", f32, (H, Dk)),
+        _ptr(bx, "bx", dt, (B, T, H, Dk)), _ptr(wx, "wx", dt, (B, T, H)),
+        _ptr(Ub, "Ub", f32, (R, Dv)), _ptr(Vb, "Vb", f32, (Dk, R)), _ptr(S0, "S0", f32, (B, H, Dv, Dk)),
+        _ptr(o, "o", dt, (B, T, H, Dv)), _ptr(S_T, "S_T", f32), _ptr(S_chunks, "S_chunks", f32),
+        None, 0, _stream(stream))
+    _check("carve_chunk_fwd_sw", st)
+    return o, S_T, S_chunks
+
+
+def chunk_bwd_sw(q, k, v, beta, bx, wx, Ub, Vb, S_chunks, dO, dS_T=None, *, g=None, f=None, A=None, tau_f=None,
+                 L=64, want_dS0=True, out=None, workspace=None, stream=None):
+    """Backward of ``chunk_fwd_sw``: dq, dk, dv, dbeta, dbx, dwx [B,T,H], dUb,
+    dVb, dS0, and dg (g given) or df, dA, dtau (f given)."""
+    lib = load_library()
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    R = Ub.shape[0]
+    dt = q.dtype
+    f32 = torch.float32
+    dev = q.device
+    dims = make_dims(B, T, H, Dk, Dv, R, L, dt)
+    res = dict(out or {})
+    spec = {"dq": ((B, T, H, Dk), dt), "dk": ((B, T, H, Dk), dt), "dv": ((B, T, H, Dv), dt),
+            "dbeta": ((B, T, H), dt), "dbx": ((B, T, H, Dk), dt), "dwx": ((B, T, H), dt),
+            "dUb": ((R, Dv), f32), "dVb": ((Dk, R), f32)}
+    if f is None:
+        spec["dg"] = ((B, T, H, Dk), f32)
+    else:
+        spec.update({"df": ((B, T, H, Dk), dt), "dA": ((H, Dk), f32), "dtau": ((H, Dk), f32)})
+    if want_dS0:
+        spec["dS0"] = ((B, H, Dv, Dk), f32)
+    for name, (shape, dtype) in spec.items():
+        if res.get(name) is None:
+            res[name] = torch.empty(shape, dtype=dtype, device=dev)
+    ws_bytes = workspace_size(dims, True)
+    if workspace is None and ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    ws_ptr = _ptr(workspace, "workspace") if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    st = lib.carve_chunk_bwd_sw(
+        ctypes.byref(dims), _ptr(q, "q", dt, (B, T, H, Dk)), _ptr(k, "k", dt, (B, T, H, Dk)),
+        _ptr(v, "v", dt, (B, T, H, Dv)), _ptr(beta, "beta", dt, (B, T, H)), _ptr(g, "g", f32, (B, T, H, Dk)),
+        _ptr(f, "f", dt, (B, T, H, Dk)), _ptr(A, "A", f32, (H, Dk)), _ptr(tau_f, "tau_f", f32, (H, Dk)),
+        _ptr(bx, "bx", dt, (B, T, H, Dk)), _ptr(wx, "wx", dt, (B, T, H)),
+        _ptr(Ub, "Ub", f32, (R, Dv)), _ptr(Vb, "Vb", f32, (Dk, R)),
+        _ptr(S_chunks, "S_chunks", f32, (B, H, T // L, Dv, Dk)),
+        _ptr(dO, "dO", dt, (B, T, H, Dv)), _ptr(dS_T, "dS_T", f32, (B, H, Dv, Dk)),
+        *[_ptr(res.get(n), n) for n in ("dq", "dk", "dv", "dbeta", "dg", "df", "dA", "dtau", "dbx", "dwx",
+                                        "dUb", "dVb", "dS0")],
+        ws_ptr, ws_len, _stream(stream))
+    _check("carve_chunk_bwd_sw", st)
     return res

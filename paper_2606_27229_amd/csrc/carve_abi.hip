@@ -29,7 +29,8 @@ BwdWs bwd_workspace_layout(const carve_dims_t* d) {
   size_t off = 0;
   l.part = off;  off += align256(nbh * kUSplit * part_floats(d->R, d->Dk) * 4);
   l.partV = off; off += align256(nbh * kVSplit * part_floats(d->R, d->Dk) * 4);
-  l.rec = off;   off += align256(nbh * nch * chunk_rec(es, d->Dk, d->L, round_rp(d->R)).total);
+  // records of the full layer (2RP fold rows); the scalar-write records are smaller
+  l.rec = off;   off += align256(nbh * nch * chunk_rec(es, d->Dk, d->L, 2 * round_rp(d->R)).total);
   l.sync = off;  off += align256(sync_ints(nbh, nch) * sizeof(int));
   l.partG = off; off += align256(nbh * 2 * (size_t)d->Dk * 4);   // dA, dtau partials (gated)
   l.total = off;
@@ -138,6 +139,7 @@ const char* carve_status_string(int status) {
     case CARVE_ERR_ALIGN: return "a pointer is not 16-byte aligned";
     case CARVE_ERR_WORKSPACE: return "workspace missing or too small";
     case CARVE_ERR_HIP: return "HIP runtime error";
+    case CARVE_ERR_ARG: return "conflicting arguments (both or neither of two alternative inputs given)";
     default: return "unknown status";
   }
 }
@@ -171,14 +173,19 @@ struct Decay {
   bool gated() const { return f != nullptr; }
 };
 
+// kernel variant of a call
+int variant_of(const Decay& dc, bool sw) { return (dc.gated() ? kVarGated : 0) | (sw ? kVarScalarW : 0); }
+
+// sw: the scalar write gate (wx [B,T,H], no Uw, Vw)
 int fwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v, const void* beta,
              const Decay& dc, const void* bx, const void* wx, const float* Ub, const float* Uw,
              const float* Vb, const float* Vw, const float* S0, void* o, float* S_T, float* S_chunks,
-             hipStream_t stream) {
+             bool sw, hipStream_t stream) {
   ProfClear pc;
   int st = check_dims(d);
   if (st) return st;
-  if (!q || !k || !v || !beta || !bx || !wx || !Ub || !Uw || !Vb || !Vw || !o) return CARVE_ERR_NULL;
+  if (!q || !k || !v || !beta || !bx || !wx || !Ub || !Vb || !o) return CARVE_ERR_NULL;
+  if (!sw && (!Uw || !Vw)) return CARVE_ERR_NULL;
   if (dc.gated() ? (!dc.A || !dc.tau_f) : !dc.g) return CARVE_ERR_NULL;
   const void* ptrs[] = {q, k, v, beta, dc.g, dc.f, dc.A, dc.tau_f, bx, wx, Ub, Uw, Vb, Vw, S0, o, S_T, S_chunks};
   for (const void* p : ptrs)
@@ -190,7 +197,7 @@ int fwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v,
   const Range ins[] = {{q, ntok * d->Dk * es}, {k, ntok * d->Dk * es}, {v, ntok * d->Dv * es},
                        {beta, ntok * es}, {dc.g, ntok * d->Dk * 4}, {dc.f, ntok * d->Dk * es},
                        {dc.A, HD}, {dc.tau_f, HD}, {bx, ntok * d->Dk * es},
-                       {wx, ntok * d->Dv * es}, {Ub, (size_t)d->R * d->Dv * 4},
+                       {wx, ntok * (sw ? 1 : d->Dv) * es}, {Ub, (size_t)d->R * d->Dv * 4},
                        {Uw, (size_t)d->R * d->Dv * 4}, {Vb, (size_t)d->Dk * d->R * 4},
                        {Vw, (size_t)d->Dv * d->R * 4}, {S0, nst * 4}};
   const Range outs[] = {{o, ntok * d->Dv * es}, {S_T, nst * 4}, {S_chunks, nst * (d->T / d->L) * 4}};
@@ -205,7 +212,7 @@ int fwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v,
   a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = round_rp(d->R); a.L = d->L;
   a.rec = nullptr;
   prof_mark(stream);
-  st = launch_chain_fwd(a, d->dtype, d->Dk, wb, dc.gated(), stream);
+  st = launch_chain_fwd(a, d->dtype, d->Dk, wb, variant_of(dc, sw), stream);
   prof_mark(stream);
   return st;
 }
@@ -222,13 +229,14 @@ int bwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v,
              const float* Vb, const float* Vw, const float* S_chunks, const void* dO, const float* dS_T,
              void* dq, void* dk, void* dv, void* dbeta, const DecayGrad& dd, void* dbx, void* dwx,
              float* dUb, float* dUw, float* dVb, float* dVw, float* dS0, void* workspace,
-             size_t workspace_bytes, hipStream_t stream) {
+             size_t workspace_bytes, bool sw, hipStream_t stream) {
   ProfClear pc;
   int st = check_dims(d);
   if (st) return st;
-  if (!q || !k || !v || !beta || !bx || !wx || !Ub || !Uw || !Vb || !Vw || !S_chunks || !dO ||
-      !dq || !dk || !dv || !dbeta || !dbx || !dwx || !dUb || !dUw || !dVb || !dVw)
+  if (!q || !k || !v || !beta || !bx || !wx || !Ub || !Vb || !S_chunks || !dO ||
+      !dq || !dk || !dv || !dbeta || !dbx || !dwx || !dUb || !dVb)
     return CARVE_ERR_NULL;
+  if (!sw && (!Uw || !Vw || !dUw || !dVw)) return CARVE_ERR_NULL;
   if (dc.gated() ? (!dc.A || !dc.tau_f || !dd.df || !dd.dA || !dd.dtau) : (!dc.g || !dd.dg)) return CARVE_ERR_NULL;
   const void* ptrs[] = {q, k, v, beta, dc.g, dc.f, dc.A, dc.tau_f, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO, dS_T,
                         dq, dk, dv, dbeta, dd.dg, dd.df, dd.dA, dd.dtau, dbx, dwx, dUb, dUw, dVb, dVw, dS0,
@@ -242,16 +250,17 @@ int bwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v,
   const size_t nst = (size_t)d->B * d->H * d->Dv * d->Dk;
   const size_t RDv = (size_t)d->R * d->Dv * 4;
   const size_t HD = (size_t)d->H * d->Dk * 4;
+  const size_t nwx = ntok * (sw ? 1 : d->Dv) * es;   // bytes of wx and of dwx
   const Range ins[] = {{q, ntok * d->Dk * es}, {k, ntok * d->Dk * es}, {v, ntok * d->Dv * es},
                        {beta, ntok * es}, {dc.g, ntok * d->Dk * 4}, {dc.f, ntok * d->Dk * es},
                        {dc.A, HD}, {dc.tau_f, HD}, {bx, ntok * d->Dk * es},
-                       {wx, ntok * d->Dv * es}, {Ub, RDv}, {Uw, RDv}, {Vb, RDv}, {Vw, RDv},
+                       {wx, nwx}, {Ub, RDv}, {Uw, RDv}, {Vb, RDv}, {Vw, RDv},
                        {S_chunks, nst * (d->T / d->L) * 4}, {dO, ntok * d->Dv * es},
                        {dS_T, nst * 4}, {workspace, need}};
   const Range outs[] = {{dq, ntok * d->Dk * es}, {dk, ntok * d->Dk * es}, {dv, ntok * d->Dv * es},
                         {dbeta, ntok * es}, {dd.dg, ntok * d->Dk * 4}, {dd.df, ntok * d->Dk * es},
                         {dd.dA, HD}, {dd.dtau, HD}, {dbx, ntok * d->Dk * es},
-                        {dwx, ntok * d->Dv * es}, {dUb, RDv}, {dUw, RDv}, {dVb, RDv},
+                        {dwx, nwx}, {dUb, RDv}, {dUw, RDv}, {dVb, RDv},
                         {dVw, RDv}, {dS0, nst * 4}};
   if (any_overlap(outs, 15, ins, 18)) return CARVE_ERR_UNSUPPORTED;
   const int lw = pick_lw(d);
@@ -287,24 +296,24 @@ int bwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v,
   st = launch_sync_clear(sync, sync_ints((size_t)d->B * d->H, (size_t)(d->T / d->L)), stream);
   if (st) return st;
   prof_mark(stream);
-  st = launch_bwd_fused(f, a, sync, cus, d->dtype, d->Dk, lw, dc.gated(), stream);
+  st = launch_bwd_fused(f, a, sync, cus, d->dtype, d->Dk, lw, variant_of(dc, sw), stream);
   if (st) return st;
   prof_mark(stream);
-  // 3. dVb, dVw from dbx, dwx and tau
-  st = launch_bwd_vparam(a, d->dtype, d->Dk, stream);
+  // 3. dVb, dVw from dbx, dwx and tau (dVb only with the scalar write gate)
+  st = launch_bwd_vparam(a, d->dtype, d->Dk, sw, stream);
   if (st) return st;
   prof_mark(stream);
-  // 4. d[Ub; Uw] from the per-chunk dF
-  st = launch_bwd_uparam(a, d->dtype, d->Dk, stream);
+  // 4. d[Ub; Uw] from the per-chunk dF (dUb only with the scalar write gate)
+  st = launch_bwd_uparam(a, d->dtype, d->Dk, sw, stream);
   if (st) return st;
   prof_mark(stream);
   // 5. fixed-order reductions of the partials
   const int nbh = d->B * d->H;
   const size_t RD = (size_t)d->R * d->Dk;
-  st = launch_param_reduce(a.part, nbh * kUSplit, RD, dUb, dUw, stream);
+  st = launch_param_reduce(a.part, nbh * kUSplit, RD, dUb, sw ? nullptr : dUw, stream);
   if (st) return st;
   prof_mark(stream);
-  st = launch_param_reduce(a.partV, nbh * kVSplit, RD, dVb, dVw, stream);
+  st = launch_param_reduce(a.partV, nbh * kVSplit, RD, dVb, sw ? nullptr : dVw, stream);
   if (st) return st;
   prof_mark(stream);
   // 6. (gated) dA, dtau summed over the batch
@@ -327,7 +336,7 @@ int carve_chunk_fwd(const carve_dims_t* d, const void* q, const void* k, const v
   (void)workspace;
   (void)workspace_bytes;
   return fwd_impl(d, q, k, v, beta, Decay{g, nullptr, nullptr, nullptr}, bx, wx, Ub, Uw, Vb, Vw, S0, o, S_T,
-                  S_chunks, stream);
+                  S_chunks, false, stream);
 }
 
 int carve_chunk_fwd_gated(const carve_dims_t* d, const void* q, const void* k, const void* v,
@@ -342,7 +351,7 @@ int carve_chunk_fwd_gated(const carve_dims_t* d, const void* q, const void* k, c
     return CARVE_ERR_NULL;
   }
   return fwd_impl(d, q, k, v, beta, Decay{nullptr, f, A, tau_f}, bx, wx, Ub, Uw, Vb, Vw, S0, o, S_T, S_chunks,
-                  stream);
+                  false, stream);
 }
 
 int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const void* v,
@@ -354,7 +363,7 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
                     size_t workspace_bytes, hipStream_t stream) {
   return bwd_impl(d, q, k, v, beta, Decay{g, nullptr, nullptr, nullptr}, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO,
                   dS_T, dq, dk, dv, dbeta, DecayGrad{dg, nullptr, nullptr, nullptr}, dbx, dwx, dUb, dUw, dVb,
-                  dVw, dS0, workspace, workspace_bytes, stream);
+                  dVw, dS0, workspace, workspace_bytes, false, stream);
 }
 
 int carve_chunk_bwd_gated(const carve_dims_t* d, const void* q, const void* k, const void* v,
@@ -371,7 +380,39 @@ int carve_chunk_bwd_gated(const carve_dims_t* d, const void* q, const void* k, c
   }
   return bwd_impl(d, q, k, v, beta, Decay{nullptr, f, A, tau_f}, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO, dS_T,
                   dq, dk, dv, dbeta, DecayGrad{nullptr, df, dA, dtau}, dbx, dwx, dUb, dUw, dVb, dVw, dS0,
-                  workspace, workspace_bytes, stream);
+                  workspace, workspace_bytes, false, stream);
+}
+
+int carve_chunk_fwd_sw(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                       const void* beta, const float* g, const void* f, const float* A,
+                       const float* tau_f, const void* bx, const void* wx, const float* Ub,
+                       const float* Vb, const float* S0, void* o, float* S_T, float* S_chunks,
+                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  if (!g == !f) {
+    ProfClear pc;
+    return g ? CARVE_ERR_ARG : CARVE_ERR_NULL;
+  }
+  const Decay dc = g ? Decay{g, nullptr, nullptr, nullptr} : Decay{nullptr, f, A, tau_f};
+  return fwd_impl(d, q, k, v, beta, dc, bx, wx, Ub, nullptr, Vb, nullptr, S0, o, S_T, S_chunks, true, stream);
+}
+
+int carve_chunk_bwd_sw(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                       const void* beta, const float* g, const void* f, const float* A,
+                       const float* tau_f, const void* bx, const void* wx, const float* Ub,
+                       const float* Vb, const float* S_chunks, const void* dO, const float* dS_T,
+                       void* dq, void* dk, void* dv, void* dbeta, float* dg, void* df, float* dA,
+                       float* dtau, void* dbx, void* dwx, float* dUb, float* dVb, float* dS0,
+                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!g == !f) {
+    ProfClear pc;
+    return g ? CARVE_ERR_ARG : CARVE_ERR_NULL;
+  }
+  const Decay dc = g ? Decay{g, nullptr, nullptr, nullptr} : Decay{nullptr, f, A, tau_f};
+  const DecayGrad dd = g ? DecayGrad{dg, nullptr, nullptr, nullptr} : DecayGrad{nullptr, df, dA, dtau};
+  return bwd_impl(d, q, k, v, beta, dc, bx, wx, Ub, nullptr, Vb, nullptr, S_chunks, dO, dS_T, dq, dk, dv, dbeta, dd,
+                  dbx, dwx, dUb, nullptr, dVb, nullptr, dS0, workspace, workspace_bytes, true, stream);
 }
 
 }  // extern "C"

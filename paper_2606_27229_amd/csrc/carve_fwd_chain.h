@@ -1,0 +1,640 @@
+// carve_fwd_chain.h -- chunked CARVE forward on gfx950: one workgroup per
+// (batch, head) runs the whole sequence as a persistent chain of WY blocks.
+// (Kernel templates; every variant is instantiated in a translation unit of its
+// own, carve_variant.hip.)
+//
+// A gate chunk (L tokens) is evaluated as L / WB WY blocks of WB <= 64 tokens
+// (WB = L for L <= 64).  At the start of every chunk the state S_hat is folded
+// once (Eq. content_readout); every block of the chunk uses the same fold:
+//   F = [Ub; Uw] S_hat,  tau = tanh(q F^T),
+//   z_b = bx + tau_b Vb^T,  z_w = wx + tau_w Vw^T            (Eq. erase_gate)
+//   l = g - softplus(z_b) = log(exp(g) (1 - sigmoid(z_b))),   w = sigmoid(z_w)
+// Inside a block, with lam the prefix sums of l from the block start (lam_{-1}
+// = 0), S the block start state and the WY form of Sec. WY-form intra-chunk
+// solve re-derived from the recurrence of Eq. carve_state, every exponential
+// is taken relative to the per-key-channel reference rho = lam_end / 2 (the
+// middle of the block's log-retention range), so no factor exceeds
+// e^{|lam_end| / 2}:
+//   Kt_t = k_t e^{lam_{t-1} - rho},  Qt_t = q_t e^{lam_t - rho},  Ki_s = k_s e^{rho - lam_s}
+//   A_ts = beta_t Kt_t . Ki_s (s < t),  P_ts = Qt_t . Ki_s (s <= t)
+//   S' = S diag(e^{rho})
+//   u = (I + A)^{-1} beta (w * v - Kt S'^T)                  (corrected values)
+//   o = Qt S'^T + P u
+//   S <- (S' + u^T Ki) diag(e^{rho})          (= S diag(e^{lam_end}) + sum_s u_s k_s^T e^{lam_end - lam_s})
+// The unit-lower-triangular solve is blocked over 16-token tiles: the diagonal
+// tiles are inverted by substitution, the off-diagonal coupling is applied on
+// the matrix cores while walking the tiles in order.
+//
+// Wave w owns the 16-wide tile w of the value axis (state rows, values, u, o)
+// and the 16-wide tile w of the key axis (gate arithmetic, decayed keys).  The
+// state lives in registers in the matrix-core result layout for the whole call.
+//
+// Memory: the next block's token data is loaded into registers while the
+// current block runs (q, k and bx as whole rows, 16 bytes per lane, then
+// staged through LDS; a wave load that touches 16 token rows for 32 bytes
+// each streams at well under half the rate); each block starts with one wait
+// for all of this wave's outstanding memory operations, by then at least half
+// a block old.  The
+// output of a block is stored at the start of the next block, so no wait on
+// the chain ever covers a store that was just issued.
+//
+// With the scalar write gate (kVarScalarW) the fold has the Ub rows only, the
+// write logit of a token is one scalar per head, staged with beta, and w v is
+// that gate times v.
+//
+// Precondition (not checked): inside one WY block the log retention summed
+// over the block stays above about -170 per key channel (factors up to
+// e^{|lam_end| / 2} are formed in f32).
+#pragma once
+#include "carve_kernels.h"
+
+namespace carve {
+
+// Tile x of a row-major enumeration of the lower-triangular tiles (i, j):
+// strict (j < i, starting at i = 1) or inclusive (j <= i).
+__host__ __device__ constexpr int tri_row(int x, bool strict) {
+  int i = strict ? 1 : 0;
+  while (x >= (strict ? i : i + 1)) {
+    x -= strict ? i : i + 1;
+    ++i;
+  }
+  return i;
+}
+__host__ __device__ constexpr int tri_col(int x, bool strict) {
+  int i = strict ? 1 : 0;
+  while (x >= (strict ? i : i + 1)) {
+    x -= strict ? i : i + 1;
+    ++i;
+  }
+  return x;
+}
+static_assert(tri_row(0, true) == 1 && tri_col(0, true) == 0 && tri_row(5, true) == 3 && tri_col(5, true) == 2, "");
+static_assert(tri_row(0, false) == 0 && tri_row(2, false) == 1 && tri_col(2, false) == 1 && tri_col(9, false) == 3, "");
+
+// GATED: the decay g is formed in the kernel from its raw logit f (token
+// dtype) as -exp(A) softplus(f + tau_f) (Eq. decay_gate, Sec. decay_gate),
+// with A and tau_f of the head held in LDS.
+template <typename T, int D, int WB, int RP, int VAR>
+__global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs a) {
+  typedef Quad<T> Qd;
+  typedef typename Qd::q quad;
+  constexpr bool GATED = (VAR & kVarGated) != 0;
+  constexpr bool SW = (VAR & kVarScalarW) != 0;
+  constexpr int NT = fwd_threads(D);
+  constexpr int NW = NT / 64;
+  constexpr int NJT = D / 16;
+  constexpr int NB = WB / 16;
+  constexpr int R2 = fold_rows(RP, VAR);   // rows of the fold
+  constexpr int NRT = R2 / 16;
+  constexpr int NRB = RP / 16;
+  constexpr int PAD = 16 / sizeof(T);
+  constexpr int LDD = D + PAD, LDR = R2 + PAD, LDW = WB + PAD, LDB = 16 + PAD;
+  constexpr int NTA = NB * (NB - 1) / 2;   // off-diagonal tiles of A
+  constexpr int NTP = NB * (NB + 1) / 2;   // tiles of P
+  constexpr int TW = NW - 1;               // the wave that inverts the diagonal tiles
+  static_assert(NW == NJT && NW >= 2, "one wave per 16-wide tile, at least two waves");
+  static_assert(D % 32 == 0, "K32 steps over the key / value axis");
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
+  const int g = lane >> 4, c = lane & 15;
+  const int H = a.H, Tn = a.T, L = a.L, R = a.R;
+  const int nblk = Tn / WB, bpc = L / WB;
+  const int bh = blockIdx.x, b = bh / H, h = bh % H;
+
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  constexpr ChainLds lay = chain_lds<T, D, WB, RP, SW>();
+  T* sU = reinterpret_cast<T*>(smem + lay.U);      // [R2][LDD]   [Ub; 0; Uw; 0] or [Ub; 0]
+  T* sS = reinterpret_cast<T*>(smem + lay.X);      // [D][LDD]    S_hat[v][j]
+  T* sKt = reinterpret_cast<T*>(smem + lay.Kt);    // [WB][LDD]   (aliases sS)
+  T* sBx = reinterpret_cast<T*>(smem + lay.Bx);    // [WB][LDD]   raw bx (aliases sS)
+  T* sKi = reinterpret_cast<T*>(smem + lay.Ki);    // [WB][LDD]   raw k, then Ki
+  T* sF = reinterpret_cast<T*>(smem + lay.F);      // [R2][LDD]   F[r][j]
+  T* sQ = reinterpret_cast<T*>(smem + lay.Q);      // [WB][LDD]   raw q, then Qt
+  T* sTau = reinterpret_cast<T*>(smem + lay.Tau);  // [WB][LDR]   tau[t][r]
+  T* sA = reinterpret_cast<T*>(smem + lay.A);      // [WB][LDW]   -A[t][s] (off-diagonal tiles)
+  T* sP = reinterpret_cast<T*>(smem + lay.P);      // [WB][LDW]   P[t][s]
+  float* sAdT = reinterpret_cast<float*>(smem + lay.AdT);  // [NB][16][20] A_ii[t][s] at (s, t)
+  T* sTmT = reinterpret_cast<T*>(smem + lay.TmT);          // [NB][16][LDB] T_ii[t][s] at (s, t)
+  float* sRho = reinterpret_cast<float*>(smem + lay.Rho);  // [D] e^{rho} = e^{lam_end / 2}
+  float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);  // [2][WB] (block parity)
+  float* sWs = sBeta + 2 * WB;                     // [2][WB] sigmoid(wx) (SW; block parity)
+  constexpr bool SVW = chain_stage_vw<T, D, WB, RP, SW>();
+  T* sVW = reinterpret_cast<T*>(smem + lay.VW);    // [2][WB][D]  v, wx (swizzled; SVW; v only with SW)
+  float* sGate = reinterpret_cast<float*>(smem + lay.Gate);  // [2][D] -exp(A), tau_f (GATED)
+
+  const size_t bh0 = ((size_t)b * Tn * H + h) * D;
+  const size_t bh1 = (size_t)b * Tn * H + h;
+  const int rs = H * D;
+  const T* __restrict__ q = reinterpret_cast<const T*>(a.q) + bh0;
+  const T* __restrict__ k = reinterpret_cast<const T*>(a.k) + bh0;
+  const T* __restrict__ v = reinterpret_cast<const T*>(a.v) + bh0;
+  const T* __restrict__ bx = reinterpret_cast<const T*>(a.bx) + bh0;
+  const T* __restrict__ wx = reinterpret_cast<const T*>(a.wx) + (SW ? bh1 : bh0);
+  const T* __restrict__ beta = reinterpret_cast<const T*>(a.beta) + bh1;
+  const float* __restrict__ gl = GATED ? nullptr : a.g + bh0;
+  const T* __restrict__ fl = GATED ? reinterpret_cast<const T*>(a.f) + bh0 : nullptr;
+  T* __restrict__ o = reinterpret_cast<T*>(a.o) + bh0;
+
+  // ---- shared parameters ------------------------------------------------------
+  if (GATED)
+    for (int x = tid; x < D; x += NT) {
+      sGate[x] = -expf(a.A[h * D + x]);
+      sGate[D + x] = a.tau_f[h * D + x];
+    }
+  for (int x = tid; x < R2 * D; x += NT) {
+    const int rr = x / D, i = x % D;
+    float u = 0.0f;
+    if (rr < R) u = a.Ub[rr * D + i];
+    else if (!SW && rr >= RP && rr < RP + R) u = a.Uw[(rr - RP) * D + i];
+    sU[rr * LDD + i] = (T)u;
+  }
+  // Vb / Vw operand quads, lane (g, c): V[16 w + c][16 ks + 4 g + e]
+  quad fVb[NRB], fVw[NRB];
+  for (int ks = 0; ks < NRB; ++ks) {
+    f32x4 tb, tw;
+    for (int e = 0; e < 4; ++e) {
+      const int r = 16 * ks + 4 * g + e;
+      tb[e] = r < R ? a.Vb[(16 * w + c) * R + r] : 0.0f;
+      tw[e] = (!SW && r < R) ? a.Vw[(16 * w + c) * R + r] : 0.0f;
+    }
+    fVb[ks] = Qd::cvt(tb);
+    fVw[ks] = Qd::cvt(tw);
+  }
+  // identity operand, lane (g, c): I[4 g + e][c]
+  quad fI;
+  {
+    f32x4 t;
+    for (int e = 0; e < 4; ++e) t[e] = (4 * g + e == c) ? 1.0f : 0.0f;
+    fI = Qd::cvt(t);
+  }
+
+  // ---- state: St[jt][e] = S[v = 16 w + c][j = 16 jt + 4 g + e] ----------------
+  f32x4 St[NJT];
+  const size_t soff = (size_t)bh * D * D;
+  for (int jt = 0; jt < NJT; ++jt)
+    St[jt] = a.S0 ? gload4(a.S0 + soff + (16 * w + c) * D + 16 * jt + 4 * g) : zero4();
+
+  // ---- prefetch registers ---------------------------------------------------------
+  // q, k, bx: whole rows, 16 bytes per lane (coalesced), staged through LDS;
+  // g, v, wx: token tile bb as lane (g, c) = token 16 bb + c, elements 16 w + 4 g ..
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  constexpr int VEC = 16 / sizeof(T);                // elements per 16-byte vector
+  constexpr int NVX = WB * D / VEC;                  // vectors of one [WB][D] tile
+  constexpr int NXV = (NVX + NT - 1) / NT;           // per thread
+  u32x4 cq[NXV], ck[NXV], cbx[NXV];
+  quad pv[NB], pwx[NB];      // per-tile value-side operands (without SVW)
+  u32x4 cv[NXV], cwx[NXV];   // whole rows of v and wx (with SVW)
+  f32x4 pg[NB];     // g per tile (ungated)
+  quad pf[NB];      // f per tile (GATED)
+  T pbeta = (T)0.0f, pws = (T)0.0f;   // beta and (SW) the write logit of token lane % WB
+#define CARVE_PREFETCH_Q(BLK_)                                                     \
+  do {                                                                             \
+    const int t0_ = (BLK_) * WB;                                                   \
+    for (int u_ = 0; u_ < NXV; ++u_) {                                             \
+      const int x_ = tid + u_ * NT;                                                \
+      if (NVX % NT != 0 && x_ >= NVX) break;                                       \
+      cq[u_] = *reinterpret_cast<const u32x4*>(q + (t0_ + x_ / (D / VEC)) * rs + (x_ % (D / VEC)) * VEC); \
+    }                                                                              \
+    if (w == 0) {                                                                  \
+      pbeta = beta[(t0_ + (lane % WB)) * H];                                       \
+      if constexpr (SW) pws = wx[(t0_ + (lane % WB)) * H];                         \
+    }                                                                              \
+  } while (0)
+#define CARVE_PREFETCH_GATES(BLK_)                                                 \
+  do {                                                                             \
+    const int t0_ = (BLK_) * WB;                                                   \
+    for (int u_ = 0; u_ < NXV; ++u_) {                                             \
+      const int x_ = tid + u_ * NT;                                                \
+      if (NVX % NT != 0 && x_ >= NVX) break;                                       \
+      const int o_ = (t0_ + x_ / (D / VEC)) * rs + (x_ % (D / VEC)) * VEC;         \
+      ck[u_] = *reinterpret_cast<const u32x4*>(k + o_);                            \
+      cbx[u_] = *reinterpret_cast<const u32x4*>(bx + o_);                          \
+    }                                                                              \
+  } while (0)
+  // per-tile operands of the gates (16 token rows of this wave's 16 columns)
+#define CARVE_PREFETCH_G(BLK_)                                                     \
+  do {                                                                             \
+    int cs_ = c, gs_ = g;                                                          \
+    asm volatile("" : "+v"(cs_), "+v"(gs_));                                       \
+    for (int bb_ = 0; bb_ < NB; ++bb_) {                                           \
+      const int e_ = ((BLK_) * WB + 16 * bb_ + cs_) * rs + 16 * w + 4 * gs_;      \
+      if constexpr (GATED) pf[bb_] = Qd::ld(fl + e_);                              \
+      else pg[bb_] = *reinterpret_cast<const f32x4*>(gl + e_);                     \
+    }                                                                              \
+  } while (0)
+#define CARVE_PREFETCH_VW(BLK_)                                                    \
+  do {                                                                             \
+    if constexpr (SVW) {                                                           \
+      const int t0_ = (BLK_) * WB;                                                 \
+      for (int u_ = 0; u_ < NXV; ++u_) {                                           \
+        const int x_ = tid + u_ * NT;                                              \
+        if (NVX % NT != 0 && x_ >= NVX) break;                                     \
+        const int o_ = (t0_ + x_ / (D / VEC)) * rs + (x_ % (D / VEC)) * VEC;       \
+        cv[u_] = *reinterpret_cast<const u32x4*>(v + o_);                          \
+        if constexpr (!SW) cwx[u_] = *reinterpret_cast<const u32x4*>(wx + o_);     \
+      }                                                                            \
+    } else {                                                                       \
+      int cs_ = c, gs_ = g;                                                        \
+      asm volatile("" : "+v"(cs_), "+v"(gs_));                                     \
+      for (int bb_ = 0; bb_ < NB; ++bb_) {                                         \
+        const int e_ = ((BLK_) * WB + 16 * bb_ + cs_) * rs + 16 * w + 4 * gs_;    \
+        pv[bb_] = Qd::ld(v + e_);                                                  \
+        if constexpr (!SW) pwx[bb_] = Qd::ld(wx + e_);                             \
+      }                                                                            \
+    }                                                                              \
+  } while (0)
+  // v / wx rows into VW: 16-byte chunk kk of row t goes to chunk kk ^ (t mod NC)
+  // (a swizzle instead of padding: the 16 rows a wave reads with one quad load
+  // fall into distinct banks)
+  constexpr int NC = D / VEC;                        // 16-byte chunks per row
+#define CARVE_STAGE_VW()                                                           \
+  do {                                                                             \
+    for (int u_ = 0; u_ < NXV; ++u_) {                                             \
+      const int x_ = tid + u_ * NT;                                                \
+      if (NVX % NT != 0 && x_ >= NVX) break;                                       \
+      const int t_ = x_ / NC, kk_ = x_ % NC;                                       \
+      T* d_ = sVW + t_ * D + (kk_ ^ (t_ & (NC - 1))) * VEC;                        \
+      *reinterpret_cast<u32x4*>(d_) = cv[u_];                                      \
+      if constexpr (!SW) *reinterpret_cast<u32x4*>(d_ + WB * D) = cwx[u_];         \
+    }                                                                              \
+  } while (0)
+#define CARVE_STAGE_ROWS(DST_, SRC_)                                               \
+  do {                                                                             \
+    for (int u_ = 0; u_ < NXV; ++u_) {                                             \
+      const int x_ = tid + u_ * NT;                                                \
+      if (NVX % NT != 0 && x_ >= NVX) break;                                       \
+      *reinterpret_cast<u32x4*>((DST_) + (x_ / (D / VEC)) * LDD + (x_ % (D / VEC)) * VEC) = (SRC_)[u_]; \
+    }                                                                              \
+  } while (0)
+  CARVE_PREFETCH_Q(0);
+  CARVE_PREFETCH_GATES(0);
+  CARVE_PREFETCH_G(0);
+  CARVE_PREFETCH_VW(0);
+
+  quad oq[NB];   // o of the previous block, lane (g, c): o[t = 16 bb + c][v = 16 w + 4 g + e]
+  int oprev = -1;
+
+  for (int blk = 0; blk < nblk; ++blk) {
+    const int t0 = blk * WB;
+    const bool cstart = (blk % bpc) == 0;
+    const int par = blk & 1;
+
+    // ---- stage: wait for the prefetch; chunk start state --------------------------
+    // The block's global stores and the next block's loads are spread over the
+    // steps that use only LDS and the matrix cores (fold, tau, coupling,
+    // substitution): issued in one burst they would stall every wave behind
+    // the CU's memory pipeline.  Store addresses come from opaque lane
+    // coordinates, recomputed where needed instead of held across the loop.
+  // The chunk start state goes out in whole 128-byte lines: for the column
+  // tiles 2m and 2m + 1, neighbouring lanes c and c ^ 1 (rows 2r and 2r + 1)
+  // swap one quad each, so that one store writes row 2r (tile 2m from the even
+  // lane, tile 2m + 1 from the odd one) and the next row 2r + 1.  Tiles
+  // [JT0_ / 2 * 2, JT1_ / 2 * 2) are stored.
+#define CARVE_STORE_S(JT0_, JT1_)                                                  \
+    do {                                                                           \
+      if (cstart && a.S_chunks) {                                                  \
+        int cs_ = c, gs_ = g;                                                      \
+        asm volatile("" : "+v"(cs_), "+v"(gs_));                                   \
+        const bool odd_ = (cs_ & 1) != 0;                                          \
+        float* r0_ = a.S_chunks + ((size_t)bh * (Tn / L) + blk / bpc) * D * D + (16 * w + (cs_ & ~1)) * D + 4 * gs_ + (odd_ ? 16 : 0); \
+        for (int m_ = (JT0_) / 2; m_ < (JT1_) / 2; ++m_) {                         \
+          f32x4 st0_, st1_;                                                        \
+          for (int e_ = 0; e_ < 4; ++e_) {                                         \
+            const float rv_ = lane_xor1(odd_ ? St[2 * m_][e_] : St[2 * m_ + 1][e_]); \
+            st0_[e_] = odd_ ? rv_ : St[2 * m_][e_];                                \
+            st1_[e_] = odd_ ? St[2 * m_ + 1][e_] : rv_;                            \
+          }                                                                        \
+          *reinterpret_cast<f32x4*>(r0_ + 32 * m_) = st0_;                         \
+          *reinterpret_cast<f32x4*>(r0_ + D + 32 * m_) = st1_;                     \
+        }                                                                          \
+      }                                                                            \
+    } while (0)
+    vm_wait_all();
+    if (cstart) {
+      for (int jt = 0; jt < NJT; ++jt) Qd::st(sS + (16 * w + c) * LDD + 16 * jt + 4 * g, Qd::cvt(St[jt]));
+    }
+    CARVE_STAGE_ROWS(sQ, cq);
+    if (w == 0 && lane < WB) {
+      sBeta[par * WB + lane] = (float)pbeta;
+      if constexpr (SW) sWs[par * WB + lane] = sigmoid_f((float)pws);
+    }
+    {
+      const int nx = blk + 1 < nblk ? blk + 1 : blk;
+      CARVE_PREFETCH_Q(nx);
+    }
+    __syncthreads();
+    CARVE_STORE_S(0, NJT / 2);
+    // raw keys of the block into free LDS (read by the gates)
+    CARVE_STAGE_ROWS(sKi, ck);
+    if constexpr (SVW) CARVE_STAGE_VW();
+
+    // ---- fold F^T[j][r] = sum_v S_hat[v][j] U[r][v] (key tile w) --------------
+    if (cstart) {
+      for (int rt = 0; rt < NRT; ++rt) {
+        f32x4 acc = zero4();
+        for (int vp = 0; vp < D / 32; ++vp) {
+          const quad a0 = Qd::ld_tr(sS, LDD, 32 * vp, 16 * w, g, c);
+          const quad a1 = Qd::ld_tr(sS, LDD, 32 * vp + 16, 16 * w, g, c);
+          const T* ur = sU + (16 * rt + c) * LDD + 32 * vp + 4 * g;
+          acc = Qd::mma32(a0, a1, Qd::ld(ur), Qd::ld(ur + 16), acc);
+        }
+        Qd::st(sF + (16 * rt + c) * LDD + 16 * w + 4 * g, Qd::cvt(acc));
+      }
+      __syncthreads();
+    }
+    // raw erase logits into region X (the fold is done with the state)
+    CARVE_STAGE_ROWS(sBx, cbx);
+    // the previous block's outputs
+    if (oprev >= 0) {
+      int cs = c, gs = g;
+      asm volatile("" : "+v"(cs), "+v"(gs));
+      for (int bb = 0; bb < NB; ++bb) Qd::st(o + (oprev + 16 * bb + cs) * rs + 16 * w + 4 * gs, oq[bb]);
+    }
+
+    // ---- tau^T[r][t] = tanh(F[r] . q_t) -> sTau[t][r] ---------------------------
+    for (int x = w; x < NRT * NB; x += NW) {
+      const int rt = x % NRT, bb = x / NRT;
+      f32x4 acc = zero4();
+      for (int jp = 0; jp < D / 32; ++jp) {
+        const T* fr = sF + (16 * rt + c) * LDD + 32 * jp + 4 * g;
+        const T* qr = sQ + (16 * bb + c) * LDD + 32 * jp + 4 * g;
+        acc = Qd::mma32(Qd::ld(fr), Qd::ld(fr + 16), Qd::ld(qr), Qd::ld(qr + 16), acc);
+      }
+      for (int e = 0; e < 4; ++e) acc[e] = tanh_f(acc[e]);
+      Qd::st(sTau + (16 * bb + c) * LDR + 16 * rt + 4 * g, Qd::cvt(acc));
+    }
+    __syncthreads();
+
+    // ---- gates ------------------------------------------------------------------
+    // key side, key tile w: lane (g, c) of tile bb holds token 16 bb + c and keys
+    // j = 16 w + 4 g + e; prefix sums run along the 16 lanes of a row
+    f32x4 lam[NB];
+    {
+      f32x4 carry = zero4();
+      for (int bb = 0; bb < NB; ++bb) {
+        f32x4 z = zero4();
+        for (int ks = 0; ks < NRB; ++ks)
+          z = Qd::mma16(fVb[ks], Qd::ld(sTau + (16 * bb + c) * LDR + 16 * ks + 4 * g), z);
+        const f32x4 bxv = Qd::f32(Qd::ld(sBx + (16 * bb + c) * LDD + 16 * w + 4 * g));
+        f32x4 gv;
+        if constexpr (GATED) {
+          const f32x4 fv = Qd::f32(pf[bb]);
+          const f32x4 na = *reinterpret_cast<const f32x4*>(sGate + 16 * w + 4 * g);
+          const f32x4 tf = *reinterpret_cast<const f32x4*>(sGate + D + 16 * w + 4 * g);
+          for (int e = 0; e < 4; ++e) gv[e] = na[e] * softplus_f(fv[e] + tf[e]);
+        } else {
+          gv = pg[bb];
+        }
+        for (int e = 0; e < 4; ++e) {
+          const float ell = gv[e] - softplus_f(z[e] + bxv[e]);
+          lam[bb][e] = carry[e] + row_scan(ell);
+          carry[e] = row_bcast15(lam[bb][e]);
+        }
+      }
+      f32x4 rho, eRho, fill;
+      for (int e = 0; e < 4; ++e) {
+        rho[e] = 0.5f * carry[e];
+        eRho[e] = fast_exp(rho[e]);
+        fill[e] = fast_exp(-rho[e]);   // e^{lam_{-1} - rho}, lam_{-1} = 0
+      }
+      for (int bb = 0; bb < NB; ++bb) {
+        T* kp = sKi + (16 * bb + c) * LDD + 16 * w + 4 * g;
+        const f32x4 kv = Qd::f32(Qd::ld(kp));
+        T* qp = sQ + (16 * bb + c) * LDD + 16 * w + 4 * g;
+        const f32x4 qv = Qd::f32(Qd::ld(qp));
+        f32x4 kt, qt, ki;
+        for (int e = 0; e < 4; ++e) {
+          const float E = fast_exp(lam[bb][e] - rho[e]);
+          const float Ei = fast_exp(rho[e] - lam[bb][e]);
+          kt[e] = kv[e] * row_shr1(E, fill[e]);
+          qt[e] = qv[e] * E;
+          ki[e] = kv[e] * Ei;
+          fill[e] = row_bcast15(E);
+        }
+        Qd::st(sKt + (16 * bb + c) * LDD + 16 * w + 4 * g, Qd::cvt(kt));
+        Qd::st(qp, Qd::cvt(qt));
+        Qd::st(kp, Qd::cvt(ki));
+      }
+      if (c == 0) *reinterpret_cast<f32x4*>(sRho + 16 * w + 4 * g) = eRho;
+    }
+    // value side, value tile w: rows t = 16 bb + 4 g + e, column v = 16 w + c
+    f32x4 wv[NB];
+    for (int bb = 0; bb < NB; ++bb) {
+      quad vq = pv[bb], wxq;
+      if constexpr (!SW) wxq = pwx[bb];
+      if constexpr (SVW) {
+        // row t = 16 bb + c, elements 16 w + 4 g .. + 3 of the swizzled tiles
+        const int by = (16 * w + 4 * g) * (int)sizeof(T), t = 16 * bb + c;
+        const T* r0 = sVW + t * D + ((((by >> 4) ^ (t & (NC - 1))) << 4) | (by & 15)) / (int)sizeof(T);
+        vq = Qd::ld(r0);
+        if constexpr (!SW) wxq = Qd::ld(r0 + WB * D);
+      }
+      const f32x4 vv = Qd::mma16(vq, fI, zero4());
+      if constexpr (SW) {
+        // one gate per token: rows t = 16 bb + 4 g + e
+        const f32x4 ws = *reinterpret_cast<const f32x4*>(sWs + par * WB + 16 * bb + 4 * g);
+        for (int e = 0; e < 4; ++e) wv[bb][e] = ws[e] * vv[e];
+      } else {
+        f32x4 z = zero4();
+        for (int ks = 0; ks < NRB; ++ks)
+          z = Qd::mma16(Qd::ld(sTau + (16 * bb + c) * LDR + RP + 16 * ks + 4 * g), fVw[ks], z);
+        z = Qd::mma16(wxq, fI, z);                     // + wx, moved into this layout
+        for (int e = 0; e < 4; ++e) wv[bb][e] = sigmoid_f(z[e]) * vv[e];
+      }
+    }
+    {
+      const int nx = blk + 1 < nblk ? blk + 1 : blk;
+      CARVE_PREFETCH_GATES(nx);
+    }
+    __syncthreads();
+
+    // ---- coupling tiles, diagonal inverses, state products ---------------------
+    CARVE_STORE_S(NJT / 2, NJT);
+    CARVE_PREFETCH_G(blk + 1 < nblk ? blk + 1 : blk);
+    const float* bcur = sBeta + par * WB;
+    if (w == TW) {
+      // diagonal tiles of A in f32, stored transposed: sAdT[i][s][t] = A[t][s]
+      for (int i = 0; i < NB; ++i) {
+        f32x4 acc = zero4();   // acc[e] = Kt_{t = 16 i + 4 g + e} . Ki_{s = 16 i + c}
+        const T* kr = sKt + (16 * i + c) * LDD + 4 * g;
+        const T* ir = sKi + (16 * i + c) * LDD + 4 * g;
+        for (int jp = 0; jp < D / 32; ++jp)
+          acc = Qd::mma32(Qd::ld(kr + 32 * jp), Qd::ld(kr + 32 * jp + 16), Qd::ld(ir + 32 * jp),
+                          Qd::ld(ir + 32 * jp + 16), acc);
+        const f32x4 bt = *reinterpret_cast<const f32x4*>(bcur + 16 * i + 4 * g);
+        f32x4 av;
+        for (int e = 0; e < 4; ++e) av[e] = (c < 4 * g + e) ? bt[e] * acc[e] : 0.0f;
+        *reinterpret_cast<f32x4*>(sAdT + (i * 16 + c) * 20 + 4 * g) = av;
+      }
+      // T_ii = (I + A_ii)^{-1}: lane (g, c) computes column s = c of block g by
+      // forward substitution, x[t] = delta(t, c) - sum_{m < t} A[t][m] x[m]
+      if (g < NB) {
+        const float* Ab = sAdT + g * 16 * 20;
+        float acc[16], x[16];
+#pragma unroll
+        for (int t = 0; t < 16; ++t) acc[t] = 0.0f;
+#pragma unroll
+        for (int m = 0; m < 16; ++m) {
+          x[m] = (m == c ? 1.0f : 0.0f) - acc[m];
+          const float* col = Ab + m * 20;   // A[t][m] for t = 0..15
+#pragma unroll
+          for (int t4 = (m + 1) / 4; t4 < 4; ++t4) {
+            const f32x4 a4 = *reinterpret_cast<const f32x4*>(col + 4 * t4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (4 * t4 + e > m) acc[4 * t4 + e] += a4[e] * x[m];
+          }
+        }
+        T* dst = sTmT + (g * 16 + c) * LDB;   // row s = c of T^T: T[t][c], t = 0..15
+#pragma unroll
+        for (int t4 = 0; t4 < 4; ++t4) {
+          const f32x4 v4 = {x[4 * t4], x[4 * t4 + 1], x[4 * t4 + 2], x[4 * t4 + 3]};
+          Qd::st(dst + 4 * t4, Qd::cvt(v4));
+        }
+      }
+    } else {
+      // off-diagonal tiles of -A and all tiles of P, stored [t][s]; a scalar
+      // loop over this wave's tiles (addresses from opaque lane coordinates).
+      // With 8 waves, waves w and w + 4 share a SIMD; the T-wave's partner
+      // takes no tiles, so the substitution gets its SIMD's issue slots.
+      int ct = c, gt = g;
+      asm volatile("" : "+v"(ct), "+v"(gt));
+      constexpr int NWK = NW == 8 ? NW - 2 : NW - 1;        // tile workers
+      const int wk = (NW == 8 && w > TW - 4) ? w - 1 : w;   // worker index
+      const int xend = (NW == 8 && w == TW - 4) ? 0 : NTA + NTP;
+#pragma unroll 1
+      for (int x = wk; x < xend; x += NWK) {
+        const bool isA = x < NTA;
+        const int y = isA ? x : x - NTA;
+        const int i = tri_row(y, isA), j = tri_col(y, isA);
+        // acc[e] = Ki_{s = 16 j + 4 g + e} . X_{t = 16 i + c}, X = Kt (A) or Qt (P)
+        const T* ar = sKi + (16 * j + ct) * LDD + 4 * gt;
+        const T* br = (isA ? sKt : sQ) + (16 * i + ct) * LDD + 4 * gt;
+        f32x4 acc = zero4();
+        for (int jp = 0; jp < D / 32; ++jp)
+          acc = Qd::mma32(Qd::ld(ar + 32 * jp), Qd::ld(ar + 32 * jp + 16), Qd::ld(br + 32 * jp),
+                          Qd::ld(br + 32 * jp + 16), acc);
+        f32x4 val;
+        if (isA) {
+          const float bt = bcur[16 * i + ct];
+          for (int e = 0; e < 4; ++e) val[e] = -bt * acc[e];
+          Qd::st(sA + (16 * i + ct) * LDW + 16 * j + 4 * gt, Qd::cvt(val));
+        } else {
+          for (int e = 0; e < 4; ++e) val[e] = (i > j || 4 * gt + e <= ct) ? acc[e] : 0.0f;
+          Qd::st(sP + (16 * i + ct) * LDW + 16 * j + 4 * gt, Qd::cvt(val));
+        }
+      }
+    }
+    // on the value tile (rows t = 16 bb + 4 g + e, column v): XQ = Qt S^T and the
+    // right-hand side R = beta (w * v - Kt S^T)
+    f32x4 RH[NB], XQ[NB];
+    {
+      quad sb[NJT];   // S' = S diag(e^{rho}) as the B operand
+      for (int jt = 0; jt < NJT; ++jt)
+        sb[jt] = Qd::cvt(St[jt] * *reinterpret_cast<const f32x4*>(sRho + 16 * jt + 4 * g));
+      for (int bb = 0; bb < NB; ++bb) {
+        f32x4 xk = zero4();
+        XQ[bb] = zero4();
+        const T* kr = sKt + (16 * bb + c) * LDD + 4 * g;
+        const T* qr = sQ + (16 * bb + c) * LDD + 4 * g;
+        for (int jp = 0; jp < NJT / 2; ++jp) {
+          xk = Qd::mma32(Qd::ld(kr + 32 * jp), Qd::ld(kr + 32 * jp + 16), sb[2 * jp], sb[2 * jp + 1], xk);
+          XQ[bb] = Qd::mma32(Qd::ld(qr + 32 * jp), Qd::ld(qr + 32 * jp + 16), sb[2 * jp], sb[2 * jp + 1], XQ[bb]);
+        }
+        const f32x4 bt = *reinterpret_cast<const f32x4*>(bcur + 16 * bb + 4 * g);
+        for (int e = 0; e < 4; ++e) RH[bb][e] = bt[e] * (wv[bb][e] - xk[e]);
+      }
+    }
+    __syncthreads();
+
+    // ---- value tile: blocked substitution for u, outputs, state carry ---------------
+    CARVE_PREFETCH_VW(blk + 1 < nblk ? blk + 1 : blk);
+    quad uq[NB];
+    for (int i = 0; i < NB; ++i) {
+      f32x4 r = RH[i];
+      for (int j = 0; j < i; ++j) r = Qd::mma16(Qd::ld(sA + (16 * i + c) * LDW + 16 * j + 4 * g), uq[j], r);
+      const f32x4 u = Qd::mma16(Qd::ld_tr(sTmT + i * 16 * LDB, LDB, 0, 0, g, c), Qd::cvt(r), zero4());
+      uq[i] = Qd::cvt(u);
+      f32x4 O = XQ[i];
+      for (int j = 0; j <= i; ++j) O = Qd::mma16(Qd::ld(sP + (16 * i + c) * LDW + 16 * j + 4 * g), uq[j], O);
+      oq[i] = Qd::cvt(Qd::mma16(Qd::cvt(O), fI, zero4()));
+    }
+    for (int jt = 0; jt < NJT; ++jt) {
+      const f32x4 er = *reinterpret_cast<const f32x4*>(sRho + 16 * jt + 4 * g);
+      f32x4 acc = St[jt] * er;
+      for (int kp = 0; kp < NB / 2; ++kp)
+        acc = Qd::mma32(Qd::ld_tr(sKi, LDD, 32 * kp, 16 * jt, g, c), Qd::ld_tr(sKi, LDD, 32 * kp + 16, 16 * jt, g, c),
+                        uq[2 * kp], uq[2 * kp + 1], acc);
+      if (NB & 1) acc = Qd::mma16(Qd::ld_tr(sKi, LDD, 16 * (NB - 1), 16 * jt, g, c), uq[NB - 1], acc);
+      St[jt] = acc * er;
+    }
+    oprev = t0;
+  }
+  for (int bb = 0; bb < NB; ++bb) Qd::st(o + (oprev + 16 * bb + c) * rs + 16 * w + 4 * g, oq[bb]);
+  if (a.S_T) {
+    float* dst = a.S_T + soff + (16 * w + c) * D + 4 * g;
+    for (int jt = 0; jt < NJT; ++jt) *reinterpret_cast<f32x4*>(dst + 16 * jt) = St[jt];
+  }
+#undef CARVE_PREFETCH_Q
+#undef CARVE_PREFETCH_GATES
+#undef CARVE_PREFETCH_G
+#undef CARVE_PREFETCH_VW
+#undef CARVE_STORE_S
+#undef CARVE_STAGE_VW
+#undef CARVE_STAGE_ROWS
+}
+
+// ---------------------------------------------------------------------------
+// host-side launch (one variant)
+// ---------------------------------------------------------------------------
+template <typename T, int D, int WB, int RP, int VAR>
+static int launch_chain_t(const FwdArgs& a, hipStream_t stream) {
+  constexpr ChainLds lay = chain_lds<T, D, WB, RP, (VAR & kVarScalarW) != 0>();
+  if constexpr (lay.total > kMaxLdsBytes) {
+    (void)a;
+    (void)stream;
+    return CARVE_ERR_UNSUPPORTED;
+  } else {
+  auto kern = carve_chain_fwd_kernel<T, D, WB, RP, VAR>;
+  static bool attr_set = false;  // per instantiation
+  if (!attr_set) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lay.total) != hipSuccess)
+      return CARVE_ERR_HIP;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(fwd_threads(D)), lay.total, stream, a);
+  return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
+  }
+}
+
+template <typename T, int D, int RP, int VAR>
+static int launch_chain_w(const FwdArgs& a, int WB, hipStream_t s) {
+  if (WB == 16) return launch_chain_t<T, D, 16, RP, VAR>(a, s);
+  if (WB == 32) return launch_chain_t<T, D, 32, RP, VAR>(a, s);
+  if (WB == 64) return launch_chain_t<T, D, 64, RP, VAR>(a, s);
+  return CARVE_ERR_UNSUPPORTED;
+}
+
+template <typename T, int VAR>
+static int launch_chain_d(const FwdArgs& a, int D, int WB, hipStream_t s) {
+  if (a.RP == 32) {
+    if (D == 32) return launch_chain_w<T, 32, 32, VAR>(a, WB, s);
+    if (D == 64) return launch_chain_w<T, 64, 32, VAR>(a, WB, s);
+    if (D == 128) return launch_chain_w<T, 128, 32, VAR>(a, WB, s);
+  } else if (a.RP == 64) {
+    if (D == 32) return launch_chain_w<T, 32, 64, VAR>(a, WB, s);
+    if (D == 64) return launch_chain_w<T, 64, 64, VAR>(a, WB, s);
+    if (D == 128) return launch_chain_w<T, 128, 64, VAR>(a, WB, s);
+  }
+  return CARVE_ERR_UNSUPPORTED;
+}
+
+template <int VAR>
+int launch_chain_fwd_var(const FwdArgs& a, int dtype, int D, int WB, hipStream_t s) {
+  if (dtype == CARVE_BF16) return launch_chain_d<bf16_t, VAR>(a, D, WB, s);
+  return launch_chain_d<float, VAR>(a, D, WB, s);
+}
+
+}  // namespace carve

@@ -6,10 +6,25 @@
 
 namespace carve {
 
+// Kernel variants (template argument VAR, a bit set):
+//   kVarGated:   the decay g is formed in the kernels from its raw logit f
+//                (Eq. decay_gate: g = -exp(A) softplus(f + tau_f));
+//   kVarScalarW: the scalar write gate (Sec. scalar write gate): one logit wx
+//                per (token, head), w = sigmoid(wx) on every value channel and
+//                no content term on the write side, so the fold is F = Ub S_hat
+//                (R rows instead of 2R) and there is no Uw, Vw.
+enum : int { kVarGated = 1, kVarScalarW = 2 };
+constexpr int kNumVariants = 4;
+
+// rows of the fold F (and columns of tau) of a variant, R padded to RP:
+// [Ub; 0; Uw; 0], or [Ub; 0] with the scalar write gate
+__host__ __device__ constexpr int fold_rows(int RP, int var) { return (var & kVarScalarW) ? RP : 2 * RP; }
+
 // ---- forward ----------------------------------------------------------------
 struct FwdArgs {
-  const void *q, *k, *v, *beta, *bx, *wx;   // token tensors (dtype of the call)
-  const float *g, *Ub, *Uw, *Vb, *Vw, *S0;  // f32
+  const void *q, *k, *v, *beta, *bx, *wx;   // token tensors (dtype of the call);
+                                            // wx is [B,T,H] with the scalar write gate
+  const float *g, *Ub, *Uw, *Vb, *Vw, *S0;  // f32 (Uw, Vw unused with the scalar write gate)
   // decay gate from its raw logit (gated kernels; Eq. decay_gate): f [B,T,H,Dk]
   // in the token dtype, A and tau_f [H,Dk] f32; g is unused then
   const void* f;
@@ -21,31 +36,32 @@ struct FwdArgs {
 };
 
 // Per-(batch, head, chunk) record written by the chunk-parallel recompute of
-// the backward and read by its adjoint kernel (byte offsets, 256-aligned):
-//   F   [2RP][D]   token dtype   folded read-out of the chunk start state
-//   Tau [L][2RP]   token dtype   tanh(q F^T)
+// the backward and read by its adjoint kernel (byte offsets, 256-aligned); RF
+// is the variant's number of fold rows (fold_rows):
+//   F   [RF][D]    token dtype   folded read-out of the chunk start state
+//   Tau [L][RF]    token dtype   tanh(q F^T)
 //   Tm  [L/16][16][16]           T = (I + A)^{-1} of every 16-token block
 //   P   [L/16][16][16]           P of every block
 //   Gam [L/16][D]  f32           block retention e^{lam_15}
 //   S   [L/16][D/16][threads][4]  block start states: quad jt of thread tid
 //                                 (S[16 w + c][16 jt + 4 g + e]), contiguous over threads
-//   dF  [D][2RP]   f32           written by the adjoint: the chunk's gradient of F,
+//   dF  [D][RF]    f32           written by the adjoint: the chunk's gradient of F,
 //                                 stored transposed (dF[r][j] at (j, r))
 struct ChunkRec {
   size_t F, Tau, Tm, P, Gam, S, dF, total;
 };
 __host__ __device__ constexpr size_t rec_align(size_t x) { return (x + 255) & ~(size_t)255; }
-__host__ __device__ constexpr ChunkRec chunk_rec(size_t e, int D, int L, int RP) {
+__host__ __device__ constexpr ChunkRec chunk_rec(size_t e, int D, int L, int RF) {
   ChunkRec r{};
   const size_t nbc = L / 16;
   size_t off = 0;
-  r.F = off;   off += rec_align(2 * (size_t)RP * D * e);
-  r.Tau = off; off += rec_align((size_t)L * 2 * RP * e);
+  r.F = off;   off += rec_align((size_t)RF * D * e);
+  r.Tau = off; off += rec_align((size_t)L * RF * e);
   r.Tm = off;  off += rec_align(nbc * 256 * e);
   r.P = off;   off += rec_align(nbc * 256 * e);
   r.Gam = off; off += rec_align(nbc * D * 4);
   r.S = off;   off += rec_align(nbc * (size_t)D * D * e);
-  r.dF = off;  off += rec_align(2 * (size_t)RP * D * 4);
+  r.dF = off;  off += rec_align((size_t)RF * D * 4);
   r.total = off;
   return r;
 }
@@ -70,25 +86,27 @@ __host__ __device__ constexpr int lk_of() {
 }
 
 // LDS layout of the chunk recompute for one sub-chunk of LW tokens (NB = LW / 16
-// blocks).  Every row is padded by 16 bytes.  Region X holds the copy of the
-// chunk start state while the fold runs and the per-token key-side operands after.
+// blocks); SW: the scalar write gate (RP fold rows instead of 2RP).  Every row is padded by 16 bytes.  Region X holds
+// the copy of the chunk start state while the fold runs and the per-token
+// key-side operands after.  Beta holds beta, then the scalar write gates.
 struct RecLds {
   size_t U, Q, F, Tau, Beta, X, S, Kt, Qt, Ki, Gam, AT, Tm, Gate, total;
 };
 
-template <typename T, int D, int LW, int RP>
+template <typename T, int D, int LW, int RP, bool SW>
 __host__ __device__ constexpr RecLds rec_lds() {
   RecLds l{};
   const size_t e = sizeof(T);
+  constexpr size_t RF = SW ? RP : 2 * RP;
   constexpr size_t NB = LW / 16;
   constexpr size_t PAD = 16 / sizeof(T);
-  constexpr size_t LDD = D + PAD, LDR = 2 * RP + PAD, LDB = 16 + PAD;
+  constexpr size_t LDD = D + PAD, LDR = RF + PAD, LDB = 16 + PAD;
   size_t off = 0;
-  l.U = off;    off += lds_round(2 * RP * LDD * e);
+  l.U = off;    off += lds_round(RF * LDD * e);
   l.Q = off;    off += lds_round(LW * LDD * e);
-  l.F = off;    off += lds_round(2 * RP * LDD * e);
+  l.F = off;    off += lds_round(RF * LDD * e);
   l.Tau = off;  off += lds_round(LW * LDR * e);
-  l.Beta = off; off += lds_round(LW * 4);
+  l.Beta = off; off += lds_round((SW ? 2 : 1) * LW * 4);
   l.X = off;
   size_t x = 0;
   l.Kt = off + x;  x += lds_round(LW * LDD * e);
@@ -106,7 +124,8 @@ __host__ __device__ constexpr RecLds rec_lds() {
 }
 
 // LDS layout of the chain forward for one WY block of WB tokens (NB = WB / 16
-// token tiles).  Rows are padded by 16 bytes.  Region X holds the chunk start
+// token tiles); SW: the scalar write gate (RP fold rows instead of 2RP).  Rows
+// are padded by 16 bytes.  Region X holds the chunk start
 // state while the fold reads it, then the block's raw erase logits (Bx) and the
 // decayed keys Kt; Ki holds the block's raw keys until the gates turn them
 // into Ki in place.
@@ -114,24 +133,26 @@ __host__ __device__ constexpr RecLds rec_lds() {
 // tiles (v, wx: WB rows each, unpadded, 16-byte chunks XOR-swizzled by row) from
 // the first barrier of a block to its gates; it overlays A .. TmT, which are
 // written only after the gates.  Without VW those tiles are read per wave.
+// Beta holds beta and (scalar write gate) w of the block, for two blocks.
 struct ChainLds {
   size_t U, X, Kt, Bx, Ki, F, Q, Tau, A, P, AdT, TmT, VW, Rho, Beta, Gate, total;
 };
 
-template <typename T, int D, int WB, int RP, bool VW>
+template <typename T, int D, int WB, int RP, bool SW, bool VW>
 __host__ __device__ constexpr ChainLds chain_lds_v() {
   ChainLds l{};
   const size_t e = sizeof(T);
+  constexpr size_t RF = SW ? RP : 2 * RP;
   constexpr size_t NB = WB / 16;
   constexpr size_t PAD = 16 / sizeof(T);
-  constexpr size_t LDD = D + PAD, LDR = 2 * RP + PAD, LDW = WB + PAD, LDB = 16 + PAD;
+  constexpr size_t LDD = D + PAD, LDR = RF + PAD, LDW = WB + PAD, LDB = 16 + PAD;
   size_t off = 0;
-  l.U = off;    off += lds_round(2 * RP * LDD * e);
+  l.U = off;    off += lds_round(RF * LDD * e);
   l.X = off;    off += lds_round(lds_max(D * LDD * e, 2 * lds_round(WB * LDD * e)));
   l.Kt = l.X;
   l.Bx = l.X + lds_round(WB * LDD * e);
   l.Ki = off;   off += lds_round(WB * LDD * e);
-  l.F = off;    off += lds_round(2 * RP * LDD * e);
+  l.F = off;    off += lds_round(RF * LDD * e);
   l.Q = off;    off += lds_round(WB * LDD * e);
   l.Tau = off;  off += lds_round(WB * LDR * e);
   l.A = off;    off += lds_round(WB * LDW * e);
@@ -141,31 +162,36 @@ __host__ __device__ constexpr ChainLds chain_lds_v() {
   l.VW = l.A;
   if (VW) off = lds_max(off, l.VW + lds_round(2 * WB * (size_t)D * e));
   l.Rho = off;  off += lds_round(D * 4);
-  l.Beta = off; off += lds_round(2 * WB * 4);
+  l.Beta = off; off += lds_round((SW ? 4 : 2) * WB * 4);
   l.Gate = off; off += lds_round(2 * D * 4);   // -exp(A), tau_f of the head (gated)
   l.total = off;
   return l;
 }
 
 // whether the value-side tiles are staged (the layout with VW fits)
-template <typename T, int D, int WB, int RP>
+template <typename T, int D, int WB, int RP, bool SW>
 __host__ __device__ constexpr bool chain_stage_vw() {
-  return chain_lds_v<T, D, WB, RP, true>().total <= kMaxLdsBytes;
+  return chain_lds_v<T, D, WB, RP, SW, true>().total <= kMaxLdsBytes;
 }
 
-template <typename T, int D, int WB, int RP>
+template <typename T, int D, int WB, int RP, bool SW>
 __host__ __device__ constexpr ChainLds chain_lds() {
-  return chain_lds_v<T, D, WB, RP, chain_stage_vw<T, D, WB, RP>()>();
+  return chain_lds_v<T, D, WB, RP, SW, chain_stage_vw<T, D, WB, RP, SW>()>();
 }
 
-// forward of the whole sequence (one workgroup per (batch, head)), WY blocks of WB tokens
-int launch_chain_fwd(const FwdArgs& a, int dtype, int D, int WB, bool gated, hipStream_t s);
+// forward of the whole sequence (one workgroup per (batch, head)), WY blocks of
+// WB tokens; launch_chain_fwd dispatches on var to launch_chain_fwd_var<VAR>
+// (each variant is compiled in a translation unit of its own)
+int launch_chain_fwd(const FwdArgs& a, int dtype, int D, int WB, int var, hipStream_t s);
+template <int VAR>
+int launch_chain_fwd_var(const FwdArgs& a, int dtype, int D, int WB, hipStream_t s);
+// LDS bytes of the chain forward with 2RP fold rows (the largest variant)
 size_t chain_lds_bytes(int dtype, int D, int WB, int RP);
 
 
 // ---- backward -----------------------------------------------------------------
 struct BwdArgs {
-  const void *q, *k, *v, *beta, *bx, *wx;
+  const void *q, *k, *v, *beta, *bx, *wx;   // wx (and dwx) [B,T,H] with the scalar write gate
   const float *g, *Ub, *Uw, *Vb, *Vw;
   const float* S_chunks;
   const void* dO;
@@ -190,43 +216,52 @@ struct BwdArgs {
 constexpr int kVSplit = 16;
 constexpr int kUSplit = 16;
 
-// LDS layout of the adjoint kernel (one 16-token block at a time).  The four
-// [value][token] exchange buffers dOT .. dzwT are dead between the end of one
-// block and the value-side step of the next; the block's token tiles (k, q, bx,
-// v, wx, dO in the token dtype, then g in f32: 16 rows each, unpadded, 16-byte
-// chunks XOR-swizzled by row) are staged there (Stage), so the region holds at
-// least 6 * 16 * D elements plus 16 * D floats.  At a chunk start the glue
-// reuses dSx for dF as a high and a low part ([D][LDF] each).
+// LDS layout of the adjoint kernel (one 16-token block at a time); SW: the
+// scalar write gate (RP fold rows instead of 2RP, no Vw).  The four [value][token]
+// exchange buffers dOT .. dzwT are dead between the end of one block and the
+// value-side step of the next; the block's token tiles (k, q, bx, v, dO and,
+// unless the write gate is scalar, wx, in the token dtype, then g in f32: 16
+// rows each, unpadded, 16-byte chunks XOR-swizzled by row) are staged there
+// (Stage), so the region holds at least 6 (5) * 16 * D elements plus 16 * D
+// floats.  At a chunk start the glue reuses dSx for dF as a high and a low
+// part ([D][LDF] each).
 // Gated kernels stage the decay logit f (token dtype) in place of g and keep
-// -exp(A), tau_f of the head (Gate) and the dA, dtau accumulators (Gacc) behind
-// it, inside the area g would take where that is large enough.
+// -exp(A), tau_f of the head (Gate) behind it, inside the area g would take
+// where that is large enough.  Beta holds beta, then the scalar write gates;
+// Dwx the per-wave partial sums of the scalar write gate's gradient.
 struct BwdLds {
-  size_t F, VbT, VwT, Tau, Tm, P, Gam, Beta, Dbeta, Kt, Qt, Ki, Sx, dSx, dOT, uT, dRT, dzwT, Stage, Gate, Gacc,
+  size_t F, VbT, VwT, Tau, Tm, P, Gam, Beta, Dbeta, Dwx, Kt, Qt, Ki, Sx, dSx, dOT, uT, dRT, dzwT, Stage, Gate,
       dzb, dY, total;
 };
 
-template <typename T, int D, int RP>
+// token tiles the adjoint stages per block
+__host__ __device__ constexpr int bwd_stage_tiles(bool SW) { return SW ? 5 : 6; }
+
+template <typename T, int D, int RP, bool SW>
 __host__ __device__ constexpr BwdLds bwd_lds() {
   BwdLds l{};
   const size_t e = sizeof(T);
+  constexpr size_t RF = SW ? RP : 2 * RP;
   constexpr size_t NW = D / 16;
   constexpr size_t PAD = 16 / sizeof(T);
-  constexpr size_t LDD = D + PAD, LDR = 2 * RP + PAD, LDB = 16 + PAD;
+  constexpr size_t LDD = D + PAD, LDR = RF + PAD, LDB = 16 + PAD;
+  constexpr size_t NS = bwd_stage_tiles(SW);
   size_t off = 0;
-  l.F = off;     off += lds_round(2 * RP * LDD * e);
+  l.F = off;     off += lds_round(RF * LDD * e);
   l.VbT = off;   off += lds_round(RP * LDD * e);
-  l.VwT = off;   off += lds_round(RP * LDD * e);
+  l.VwT = off;   off += lds_round((RF - RP) * LDD * e);
   l.Tau = off;   off += lds_round(16 * LDR * e);
   l.Tm = off;    off += lds_round(16 * LDB * e);
   l.P = off;     off += lds_round(16 * LDB * e);
   l.Gam = off;   off += lds_round(D * 4);
-  l.Beta = off;  off += lds_round(16 * 4);
+  l.Beta = off;  off += lds_round((SW ? 32 : 16) * 4);
   l.Dbeta = off; off += lds_round(NW * 16 * 4);
+  l.Dwx = off;   off += SW ? lds_round(NW * 16 * 4) : 0;
   l.Kt = off;    off += lds_round(16 * LDD * e);
   l.Qt = off;    off += lds_round(16 * LDD * e);
   l.Ki = off;    off += lds_round(16 * LDD * e);
   l.Sx = off;    off += lds_round(D * LDD * e);
-  constexpr size_t LDF = 2 * RP + 4;
+  constexpr size_t LDF = RF + 4;
   l.dSx = off;   off += lds_round(D * lds_max(LDD, 2 * LDF) * e);
   l.Stage = off;
   l.dOT = off;   off += lds_round(D * LDB * e);
@@ -234,10 +269,9 @@ __host__ __device__ constexpr BwdLds bwd_lds() {
   l.dRT = off;   off += lds_round(D * LDB * e);
   l.dzwT = off;  off += lds_round(D * LDB * e);
   {
-    const size_t garea = l.Stage + lds_round(6 * 16 * D * e);      // g, or f then Gate, Gacc
+    const size_t garea = l.Stage + lds_round(NS * 16 * D * e);     // g, or f then Gate
     l.Gate = garea + lds_round(16 * D * e);
-    l.Gacc = l.Gate + lds_round(2 * D * 4);
-    off = lds_max(off, garea + lds_max(lds_round(16 * D * 4), lds_round(16 * D * e) + 2 * lds_round(2 * D * 4)));
+    off = lds_max(off, garea + lds_max(lds_round(16 * D * 4), lds_round(16 * D * e) + lds_round(2 * D * 4)));
   }
   l.dzb = off;   off += lds_round(16 * LDD * e);
   l.dY = off;    off += lds_round(16 * LDR * e);
@@ -245,23 +279,36 @@ __host__ __device__ constexpr BwdLds bwd_lds() {
   return l;
 }
 
-// Chunk recompute and adjoint in one launch (see carve_bwd.hip).  f carries the
+// LDS of the fused chunk recompute + adjoint launch
+template <typename T, int D, int LW, int RP, bool SW>
+__host__ __device__ constexpr size_t fused_lds() {
+  return lds_max(rec_lds<T, D, LW, RP, SW>().total, bwd_lds<T, D, RP, SW>().total);
+}
+
+// Chunk recompute and adjoint in one launch (see carve_bwd.h).  f carries the
 // forward inputs, S_chunks and the chunk records (f.rec == a.rec); sync points
 // at sync_ints(B * H, T / L) ints of workspace, zeroed by launch_sync_clear
 // on the same stream before; cus is the device's compute-unit count.
+// launch_bwd_fused dispatches on var to launch_bwd_fused_var<VAR>.
 int launch_bwd_fused(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, int dtype, int D, int LW,
-                     bool gated, hipStream_t s);
+                     int var, hipStream_t s);
+template <int VAR>
+int launch_bwd_fused_var(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, int dtype, int D, int LW,
+                         hipStream_t s);
 // dA[h][j], dtau[h][j] = sums over b (in order) of the per-(b,h) partials
 int launch_gate_reduce(const float* partG, int B, int H, int D, float* dA, float* dtau, hipStream_t s);
 int launch_sync_clear(int* sync, size_t n, hipStream_t s);
-// LDS bytes of the fused launch with LW-token recompute sub-chunks
+// LDS bytes of the fused launch with LW-token recompute sub-chunks and 2RP
+// fold rows (the largest variant)
 size_t bwd_lds_bytes(int dtype, int D, int LW, int RP);
 // ints of the synchronisation area: one ready flag per chunk, the ticket
 // counter that assigns the workgroup roles, padding
 __host__ __device__ constexpr size_t sync_ints(size_t nbh, size_t nch) { return nbh * nch + 4; }
-int launch_bwd_vparam(const BwdArgs& a, int dtype, int D, hipStream_t s);
-int launch_bwd_uparam(const BwdArgs& a, int dtype, int D, hipStream_t s);
-// sum nparts records of 2 * half floats into dst0 (first half) and dst1
+// sw: the scalar write gate (dVb, dUb only; the records hold RP fold rows)
+int launch_bwd_vparam(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s);
+int launch_bwd_uparam(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s);
+// sum nparts records of 2 * half floats into dst0 (first half) and dst1; with
+// dst1 == NULL only the first half is summed
 int launch_param_reduce(const float* part, int nparts, size_t half, float* dst0, float* dst1, hipStream_t s);
 
 // floats of one partial-gradient record: d[Ub; Uw] ([R][D] twice) or dVb, dVw ([D][R] twice)

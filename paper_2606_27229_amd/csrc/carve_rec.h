@@ -28,6 +28,9 @@
 // which is the recurrence of Eq. carve_state rewritten exactly.  A 16-token
 // block keeps every factor within e^{-(16-token log retention)}.
 //
+// With the scalar write gate (kVarScalarW) F = Ub S_hat has R rows and
+// w_t = sigmoid(wx_t) is one scalar per token and head, staged with beta.
+//
 // Precondition (not checked): within any 16-token block the log retention
 // summed over the block stays above about -80 per key channel, so that
 // e^{-(block log retention)} is finite in f32.
@@ -42,17 +45,19 @@ namespace carve {
 // flight.
 // GATED: g is formed from its raw logit f as -exp(A) softplus(f + tau_f)
 // (Eq. decay_gate), A and tau_f of the head held in LDS.
-template <typename T, int D, int LW, int RP, bool GATED>
+template <typename T, int D, int LW, int RP, int VAR>
 __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const int ch0, char* smem) {
   typedef Quad<T> Qd;
   typedef typename Qd::q quad;
   typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  constexpr bool GATED = (VAR & kVarGated) != 0;
+  constexpr bool SW = (VAR & kVarScalarW) != 0;
   constexpr int NT = fwd_threads(D);
   constexpr int NW = NT / 64;          // waves == 16-wide tiles of the key / value axis
   constexpr int NJT = D / 16;
   constexpr int NB = LW / 16;          // 16-token blocks per sub-chunk
-  constexpr int R2 = 2 * RP;
-  constexpr int NRT = R2 / 16;         // 16-row tiles of [Ub; Uw] and of F
+  constexpr int R2 = fold_rows(RP, VAR);
+  constexpr int NRT = R2 / 16;         // 16-row tiles of the fold operand ([Ub; Uw] or Ub) and of F
   constexpr int PAD = 16 / sizeof(T);
   constexpr int LDD = D + PAD, LDR = R2 + PAD, LDB = 16 + PAD;
   constexpr int VEC = 16 / sizeof(T);          // token elements per 16-byte vector
@@ -67,12 +72,12 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
   const int nch = Tn / L, msub = L / LW;
   const int b = bh / H, h = bh % H;
 
-  constexpr RecLds lay = rec_lds<T, D, LW, RP>();
-  T* sU = reinterpret_cast<T*>(smem + lay.U);      // [2RP][LDD]  [Ub; 0; Uw; 0]
+  constexpr RecLds lay = rec_lds<T, D, LW, RP, SW>();
+  T* sU = reinterpret_cast<T*>(smem + lay.U);      // [R2][LDD]   [Ub; 0; Uw; 0] or [Ub; 0]
   T* sQ = reinterpret_cast<T*>(smem + lay.Q);      // [LW][LDD]   raw q
-  T* sF = reinterpret_cast<T*>(smem + lay.F);      // [2RP][LDD]  F
+  T* sF = reinterpret_cast<T*>(smem + lay.F);      // [R2][LDD]   F
   T* sTau = reinterpret_cast<T*>(smem + lay.Tau);  // [LW][LDR]   tau (b half | w half)
-  float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);
+  float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);   // [LW] beta, then [LW] sigmoid(wx) (SW)
   T* sS = reinterpret_cast<T*>(smem + lay.S);      // [D][LDD]    S_hat[v][j] (chunk start)
   T* sKt = reinterpret_cast<T*>(smem + lay.Kt);    // [LW][LDD]
   T* sQt = reinterpret_cast<T*>(smem + lay.Qt);    // [LW][LDD]
@@ -91,7 +96,7 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
   const T* __restrict__ k = reinterpret_cast<const T*>(a.k) + bh0;
   const T* __restrict__ v = reinterpret_cast<const T*>(a.v) + bh0;
   const T* __restrict__ bx = reinterpret_cast<const T*>(a.bx) + bh0;
-  const T* __restrict__ wx = reinterpret_cast<const T*>(a.wx) + bh0;
+  const T* __restrict__ wx = reinterpret_cast<const T*>(a.wx) + (SW ? bh1 : bh0);
   const T* __restrict__ beta = reinterpret_cast<const T*>(a.beta) + bh1;
   const float* __restrict__ gl = GATED ? nullptr : a.g + bh0;
   const T* __restrict__ fl = GATED ? reinterpret_cast<const T*>(a.f) + bh0 : nullptr;
@@ -106,7 +111,7 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
     const int rr = x / D, i = x % D;
     float u = 0.0f;
     if (rr < R) u = a.Ub[rr * D + i];
-    else if (rr >= RP && rr < RP + R) u = a.Uw[(rr - RP) * D + i];
+    else if (!SW && rr >= RP && rr < RP + R) u = a.Uw[(rr - RP) * D + i];
     sU[rr * LDD + i] = (T)u;
   }
   // Vb / Vw as constant operand quads: lane (g, c) holds V[16 w + c][16 ks + 4 g + e]
@@ -116,7 +121,7 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
     for (int e = 0; e < 4; ++e) {
       const int r = 16 * ks + 4 * g + e;
       tb[e] = r < R ? a.Vb[(16 * w + c) * R + r] : 0.0f;
-      tw[e] = r < R ? a.Vw[(16 * w + c) * R + r] : 0.0f;
+      tw[e] = (!SW && r < R) ? a.Vw[(16 * w + c) * R + r] : 0.0f;
     }
     fVb[ks] = Qd::cvt(tb);
     fVw[ks] = Qd::cvt(tw);
@@ -135,12 +140,12 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
     const float* src = a.S_chunks + ((size_t)bh * nch + ch0) * D * D + (16 * w + c) * D + 4 * g;
     for (int jt = 0; jt < NJT; ++jt) St[jt] = gload4(src + 16 * jt);
   }
-  const ChunkRec cr = chunk_rec(sizeof(T), D, L, RP);
+  const ChunkRec cr = chunk_rec(sizeof(T), D, L, R2);
   char* rec = reinterpret_cast<char*>(a.rec) + ((size_t)bh * nch + ch0) * cr.total;
 
   // ---- prefetch registers for the next sub-chunk ------------------------------
   u32x4 pq[NQV];
-  T pbeta = (T)0.0f;
+  T pbeta = (T)0.0f, pws = (T)0.0f;   // beta and (SW) the write logit of token tid
   quad pbx[NB], pk[NB], pwx[NB], pv[NB];
   f32x4 pg[NB];     // g per tile (ungated)
   quad pf[NB];      // f per tile (GATED)
@@ -153,7 +158,10 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
       const int t_ = x_ / (D / VEC), j_ = (x_ % (D / VEC)) * VEC;                       \
       pq[u_] = *reinterpret_cast<const u32x4*>(q + (tt0_ + t_) * rs + j_);              \
     }                                                                                   \
-    if (tid < LW) pbeta = beta[(tt0_ + tid) * H];                                       \
+    if (tid < LW) {                                                                     \
+      pbeta = beta[(tt0_ + tid) * H];                                                   \
+      if constexpr (SW) pws = wx[(tt0_ + tid) * H];                                     \
+    }                                                                                   \
   } while (0)
 #define CARVE_REC_PREFETCH_GATES(TILE_)                                                 \
   do {                                                                                  \
@@ -162,7 +170,7 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
       const int e_ = (tt0_ + 16 * bb_ + c) * rs + 16 * w + 4 * g;                       \
       pbx[bb_] = Qd::ld(bx + e_);                                                       \
       pk[bb_] = Qd::ld(k + e_);                                                         \
-      pwx[bb_] = Qd::ld(wx + e_);                                                       \
+      if constexpr (!SW) pwx[bb_] = Qd::ld(wx + e_);                                    \
       pv[bb_] = Qd::ld(v + e_);                                                         \
       if constexpr (GATED) pf[bb_] = Qd::ld(fl + e_);                                   \
       else pg[bb_] = *reinterpret_cast<const f32x4*>(gl + e_);                          \
@@ -184,7 +192,10 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
       const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;
       *reinterpret_cast<u32x4*>(sQ + t * LDD + j) = pq[u];
     }
-    if (tid < LW) sBeta[tid] = (float)pbeta;
+    if (tid < LW) {
+      sBeta[tid] = (float)pbeta;
+      if constexpr (SW) sBeta[LW + tid] = sigmoid_f((float)pws);
+    }
     if (tile + 1 < ntiles) CARVE_REC_PREFETCH_Q(tile + 1);
     __syncthreads();
 
@@ -260,12 +271,17 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
     // value side, value tile w: rows t = 16 bb + 4 g + i, column v = 16 w + c
     f32x4 wv[NB];
     for (int bb = 0; bb < NB; ++bb) {
-      f32x4 z = zero4();
-      for (int ks = 0; ks < RP / 16; ++ks)
-        z = Qd::mma16(Qd::ld(sTau + (16 * bb + c) * LDR + RP + 16 * ks + 4 * g), fVw[ks], z);
-      z = Qd::mma16(pwx[bb], fI, z);                   // + wx, moved into this layout
       const f32x4 vv = Qd::mma16(pv[bb], fI, zero4());
-      for (int i = 0; i < 4; ++i) wv[bb][i] = sigmoid_f(z[i]) * vv[i];
+      if constexpr (SW) {
+        const f32x4 ws = *reinterpret_cast<const f32x4*>(sBeta + LW + 16 * bb + 4 * g);
+        for (int i = 0; i < 4; ++i) wv[bb][i] = ws[i] * vv[i];
+      } else {
+        f32x4 z = zero4();
+        for (int ks = 0; ks < RP / 16; ++ks)
+          z = Qd::mma16(Qd::ld(sTau + (16 * bb + c) * LDR + RP + 16 * ks + 4 * g), fVw[ks], z);
+        z = Qd::mma16(pwx[bb], fI, z);                 // + wx, moved into this layout
+        for (int i = 0; i < 4; ++i) wv[bb][i] = sigmoid_f(z[i]) * vv[i];
+      }
     }
     if (tile + 1 < ntiles) CARVE_REC_PREFETCH_GATES(tile + 1);
     __syncthreads();

@@ -30,8 +30,9 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings():
     lib = carve.load_library()
-    for st in range(0, -7, -1):
+    for st in range(0, -8, -1):
         assert lib.carve_status_string(st)
+    assert "unknown" not in carve.status_string(-7)
     assert carve.status_string(0) == "ok"
 
 
@@ -142,3 +143,62 @@ def test_gated_backward_workspace_and_aliasing():
     a[21] = None          # dA missing
     st = lib.carve_chunk_bwd_gated(ctypes.byref(d), *a, ptrs[30], need, None)
     assert st == -1
+
+
+def test_scalar_write_forward_validation():
+    """carve_chunk_fwd_sw: exactly one decay form (g, or f with A and tau_f),
+    shapes and alignment are checked before any HIP call."""
+    lib = carve.load_library()
+    d = _dims()
+    fake = ctypes.c_void_p(4096)
+    # q, k, v, beta, g, f, A, tau_f, bx, wx, Ub, Vb, S0, o, S_T, S_chunks, ws, bytes, stream
+    g_form = [fake] * 5 + [None, None, None] + [fake] * 4 + [None, fake, None, None, None, 0, None]
+    f_form = [fake] * 4 + [None] + [fake] * 7 + [None, fake, None, None, None, 0, None]
+    neither = list(g_form); neither[4] = None
+    assert lib.carve_chunk_fwd_sw(ctypes.byref(d), *neither) == -1
+    both = list(f_form); both[4] = fake
+    assert lib.carve_chunk_fwd_sw(ctypes.byref(d), *both) == -7
+    for null_at in (6, 7, 9, 10, 11):   # A, tau_f, wx, Ub, Vb
+        a = list(f_form); a[null_at] = None
+        assert lib.carve_chunk_fwd_sw(ctypes.byref(d), *a) == -1, null_at
+    assert lib.carve_chunk_fwd_sw(ctypes.byref(_dims(T=100)), *g_form) == -2
+    a = list(g_form); a[9] = ctypes.c_void_p(4096 + 2)   # wx misaligned
+    assert lib.carve_chunk_fwd_sw(ctypes.byref(d), *a) == -4
+
+
+def test_scalar_write_backward_validation():
+    lib = carve.load_library()
+    d = _dims()
+    need = lib.carve_workspace_size(ctypes.byref(d), 1)
+    ptrs = [ctypes.c_void_p(1 << 40 | (i << 32)) for i in range(30)]
+    # q k v beta g f A tau bx wx Ub Vb S_chunks dO dS_T dq dk dv dbeta dg df dA dtau dbx dwx dUb dVb dS0
+    g_form = list(ptrs[:28])
+    for i in (5, 6, 7, 20, 21, 22):
+        g_form[i] = None
+    ws = ptrs[28]
+    assert lib.carve_chunk_bwd_sw(ctypes.byref(d), *g_form, None, 0, None) == -5
+    assert lib.carve_chunk_bwd_sw(ctypes.byref(d), *g_form, ws, need - 1, None) == -5
+    a = list(g_form); a[19] = None                     # dg missing
+    assert lib.carve_chunk_bwd_sw(ctypes.byref(d), *a, ws, need, None) == -1
+    a = list(g_form); a[24] = a[15]                    # dwx aliases dq
+    assert lib.carve_chunk_bwd_sw(ctypes.byref(d), *a, ws, need, None) == -3
+    a = list(g_form); a[5] = ptrs[5]                   # g and f both given
+    assert lib.carve_chunk_bwd_sw(ctypes.byref(d), *a, ws, need, None) == -7
+    f_form = list(ptrs[:28]); f_form[4] = None; f_form[19] = None
+    a = list(f_form); a[22] = None                     # dtau missing
+    assert lib.carve_chunk_bwd_sw(ctypes.byref(d), *a, ws, need, None) == -1
+
+
+@pytest.mark.parametrize("D,R,L,dt", [(128, 32, 64, carve.CARVE_BF16), (64, 16, 32, carve.CARVE_F32),
+                                      (32, 40, 16, carve.CARVE_F32)])
+def test_backward_workspace_holds_the_chunk_records(D, R, L, dt):
+    """The backward workspace holds one record per chunk with at least the fold
+    F (2RP x D), tau (L x 2RP) and the block start states (L/16 x D x D) in the
+    token dtype and dF (2RP x D) in f32, RP = R rounded up to 32."""
+    lib = carve.load_library()
+    B, T, H = 2, 4 * L, 3
+    d = carve.Dims(B, T, H, D, D, R, L, dt)
+    e = 2 if dt == carve.CARVE_BF16 else 4
+    RP = (R + 31) // 32 * 32
+    per = 2 * RP * D * e + L * 2 * RP * e + (L // 16) * D * D * e + 2 * RP * D * 4
+    assert lib.carve_workspace_size(ctypes.byref(d), 1) >= B * H * (T // L) * per
