@@ -139,3 +139,43 @@ def test_full_size_gated_sampled():
     print("max-rel errors:", {k: float("%.3g" % e) for k, e in errs.items()}, flush=True)
     bad = {k: e for k, e in errs.items() if not e <= TOL}
     assert not bad, bad
+
+
+def test_full_size_scalar_write_sampled():
+    """The scalar-write-gate variant at the headline size (B=4 H=16 T=4096
+    L=64), sampled slices as above (dwx is one value per token and head)."""
+    w = WORKLOADS["layer_1p3b_T4096"].with_(L=64)
+    L = 64
+    print(f"case scalar write {w.name} L={L}", flush=True)
+    inp = make_inputs(w, seed=8, dS_T=True, scalar_write=True)
+    samples = [(0, 0), (w.B - 1, w.H - 1)]
+    keep = np.zeros((w.B, w.H), dtype=bool)
+    for b, h in samples:
+        keep[b, h] = True
+    inp["dO"] = inp["dO"] * keep[:, None, :, None]
+    inp["dS_T"] = inp["dS_T"] * keep[:, :, None, None]
+    x = to_gpu(inp, torch.bfloat16)
+    args = (x["q"], x["k"], x["v"], x["beta"], x["bx"], x["wx"], x["Ub"], x["Vb"])
+    o, S_T, S_chunks = carve.chunk_fwd_sw(*args, x["S0"], L=L, g=x["g"])
+    gr = carve.chunk_bwd_sw(*args, S_chunks, x["dO"], x["dS_T"], L=L, g=x["g"])
+    torch.cuda.synchronize()
+    del x
+    ref_params = {"dUb": 0.0, "dVb": 0.0}
+    errs = {}
+    for b, h in samples:
+        s = _slice(inp, b, h)
+        rf = orc.fwd_sw(s, L, want_chunks=True)
+        rb = orc.bwd_sw(s, L, s["dO"], s["dS_T"])
+        errs[f"o[{b},{h}]"] = max_rel(host(o[b:b + 1, :, h:h + 1]), rf["o"])
+        errs[f"S_T[{b},{h}]"] = max_rel(host(S_T[b:b + 1, h:h + 1]), rf["S_T"])
+        errs[f"S_chunks[{b},{h}]"] = max_rel(host(S_chunks[b:b + 1, h:h + 1]), rf["S_chunks"])
+        for key in TOKEN_GRADS:
+            errs[f"{key}[{b},{h}]"] = max_rel(host(gr[key][b:b + 1, :, h:h + 1]), rb[key])
+        errs[f"dS0[{b},{h}]"] = max_rel(host(gr["dS0"][b:b + 1, h:h + 1]), rb["dS0"])
+        for key in ref_params:
+            ref_params[key] = ref_params[key] + rb[key]
+    for key in ref_params:
+        errs[key] = max_rel(host(gr[key]), ref_params[key])
+    print("max-rel errors:", {k: float("%.3g" % e) for k, e in errs.items()}, flush=True)
+    bad = {k: e for k, e in errs.items() if not e <= TOL}
+    assert not bad, bad
