@@ -576,3 +576,73 @@ def test_scalar_write_with_decay_gate_backward_finite_differences():
         fd = (_sw_loss(xp, 4) - _sw_loss(xm, 4)) / (2 * h)
         an = float(np.sum(gr[gname] * dirn))
         assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-3), (name, fd, an)
+
+
+# --------------------------------------------------------------------------
+# staleness of the folded read-out (Prop. staleness_bound): inside chunk c the
+# gates read S_{c-1}; per-token exact gating would read S_{t-1}
+# --------------------------------------------------------------------------
+def _state_after(inp, b, h, c, L, m):
+    """S_{cL+m-1} of the chunked run: m tokens of chunk c from its start state,
+    one call whose single chunk folds that start state (m = 0: the start state)."""
+    S = orc.fwd_serial(inp, L, want_chunks=True)["S_chunks"][b, h, c]
+    if m == 0:
+        return S
+    sub = {}
+    for key, val in inp.items():
+        if val is None or key in ("Ub", "Uw", "Vb", "Vw"):
+            sub[key] = val
+        elif key in ("S0", "dS_T"):
+            sub[key] = S[None, None] if key == "S0" else None
+        else:
+            sub[key] = np.ascontiguousarray(val[b:b + 1, c * L:c * L + m, h:h + 1])
+    if "S0" not in sub:
+        sub["S0"] = S[None, None]
+    return orc.fwd_serial(sub, m)["S_T"][0, 0]
+
+
+def test_staleness_bound_of_the_frozen_read_out():
+    """b_{c,t} (read-out of S_{c-1}) against the gate the same token would get
+    from S_{t-1} of the same run: zero at the chunk start, nonzero inside the
+    chunk, and within the Lipschitz bound of Prop. staleness_bound,
+    |b - b_exact| <= 1/4 |Vb|_2 |Ub|_2 |S_{c-1} - S_{t-1}|_F |q_t| (sigma is
+    1/4-Lipschitz, tanh 1-Lipschitz)."""
+    w = Workload("st", B=1, H=1, T=32, Dk=6, Dv=5, L=8, R=3, dtype="f32", mu=1.0, s0=0.5, u_std=0.8)
+    inp = _f64(make_inputs(w, seed=12))
+    L = w.L
+    run = orc.fwd_serial(inp, L, want_gates=True, want_chunks=True)
+    Ub, Vb = inp["Ub"], inp["Vb"]
+    lip = 0.25 * np.linalg.norm(Vb, 2) * np.linalg.norm(Ub, 2)
+    inside = 0
+    for t in range(w.T):
+        c, m = divmod(t, L)
+        S_hat = run["S_chunks"][0, 0, c]
+        S_prev = _state_after(inp, 0, 0, c, L, m)
+        q = inp["q"][0, t, 0]
+        b_exact = 1.0 / (1.0 + np.exp(-(inp["bx"][0, t, 0] + Vb @ np.tanh(Ub @ S_prev @ q))))
+        diff = np.linalg.norm(run["gate_b"][0, t, 0] - b_exact)
+        gap = np.linalg.norm(S_hat - S_prev)
+        if m == 0:
+            assert diff < 1e-14
+        else:
+            assert diff <= lip * gap * np.linalg.norm(q) * (1 + 1e-12) + 1e-15
+            inside += diff > 1e-6
+    assert inside >= w.T // 2
+
+
+def test_chunked_gate_deviation_is_flat_in_L():
+    """Synthetic analog of Table chunkbound row 1: the L-chunked layer against
+    exact per-token gating (L = 1).  At the paper's initial content scale the
+    gate deviation is of order 1e-3 and flat in L: within a factor 1.5 over
+    L = 16..128, the last doubling adding less than the first, as Prop.
+    staleness_bound predicts."""
+    w = Workload("st", B=2, H=4, T=1024, Dk=32, Dv=32, L=16, R=8, dtype="f32", mu=3.0, u_std=0.02)
+    inp = make_inputs(w, seed=2)
+    ex = orc.fwd_serial(inp, 1, want_gates=True)
+    dev = []
+    for L in (16, 32, 64, 128):
+        ch = orc.fwd_serial(inp, L, want_gates=True)
+        dev.append(np.linalg.norm(ch["gate_b"] - ex["gate_b"]) / np.linalg.norm(ex["gate_b"]))
+    assert 1e-5 < dev[0] < 1e-2
+    assert max(dev) < 1.5 * dev[0]
+    assert abs(dev[3] - dev[2]) < dev[1] - dev[0]
