@@ -244,3 +244,59 @@ def bwd_sw(inp, L, dO, dS_T=None, nthreads=None):
     out["dwx"] = out["dwx"].sum(axis=-1)
     del out["dUw"], out["dVw"]
     return out
+
+
+# ---- input activations (Sec. input projections, Fig. carve_block): queries and
+# keys go through SiLU then L2 normalisation over d_k, values through SiLU ----
+L2_EPS = 1e-6   # x / sqrt(|x|^2 + eps); the paper gives no epsilon
+
+
+def silu(x):
+    x = _f64(x)
+    return x / (1.0 + np.exp(-x))
+
+
+def silu_grad(x):
+    x = _f64(x)
+    s = 1.0 / (1.0 + np.exp(-x))
+    return s * (1.0 + x * (1.0 - s))
+
+
+def act_qk(xr):
+    """q = SiLU(q_raw) / sqrt(|SiLU(q_raw)|^2 + eps), per (token, head) over the last axis."""
+    s = silu(xr)
+    return s / np.sqrt(np.sum(s * s, axis=-1, keepdims=True) + L2_EPS)
+
+
+def act_qk_bwd(xr, dy):
+    """Reverse mode of ``act_qk``: with s = SiLU(x), n = sqrt(|s|^2 + eps), y = s / n,
+    ds = (dy - y (y . dy)) / n and dx = ds * SiLU'(x)."""
+    s = silu(xr)
+    n = np.sqrt(np.sum(s * s, axis=-1, keepdims=True) + L2_EPS)
+    y = s / n
+    dy = _f64(dy)
+    ds = (dy - y * np.sum(y * dy, axis=-1, keepdims=True)) / n
+    return ds * silu_grad(xr)
+
+
+def act_inputs(inp):
+    """The layer's q, k, v from the raw projections held in ``inp`` (q, k, v)."""
+    out = dict(inp)
+    out["q"] = act_qk(inp["q"])
+    out["k"] = act_qk(inp["k"])
+    out["v"] = silu(inp["v"])
+    return out
+
+
+def fwd_act(inp, L, want_chunks=False, nthreads=None):
+    """The layer fed the raw projections q, k, v (activations inside the layer)."""
+    return fwd_serial(act_inputs(inp), L, want_chunks=want_chunks, nthreads=nthreads)
+
+
+def bwd_act(inp, L, dO, dS_T=None, nthreads=None):
+    """Reverse mode of ``fwd_act``: dq, dk, dv with respect to the raw projections."""
+    out = bwd(act_inputs(inp), L, dO, dS_T, nthreads=nthreads)
+    out["dq"] = act_qk_bwd(inp["q"], out["dq"])
+    out["dk"] = act_qk_bwd(inp["k"], out["dk"])
+    out["dv"] = out["dv"] * silu_grad(inp["v"])
+    return out

@@ -26,6 +26,10 @@ With the scalar write gate (scalar_write=True; Sec. scalar write gate) the
 per-head write logit is drawn last (after the gated arrays, if any), replacing
 the per-channel one, and Uw, Vw are left out:
   wx     ~ N(0,1) of shape [B, T, H]             token dtype
+With the input activations inside the layer (act=True; SiLU then L2-norm on
+queries and keys, SiLU on values) the raw projections are drawn last and
+replace q, k, v:
+  q, k   ~ N(0,1) of shape [B, T, H, Dk], v ~ N(0,1) of shape [B, T, H, Dv]
 Token tensors of a bf16 workload are rounded to bf16 (round to nearest even)
 and the rounded values are what every consumer receives; g, the parameters
 and the states stay f32.
@@ -117,13 +121,14 @@ def _logsigmoid(x):
 
 def make_inputs(w: Workload, seed: int = 0, *, zero_content: bool = False,
                 dS_T: bool = False, bx_mean: float | None = None, gated: bool = False,
-                scalar_write: bool = False) -> dict:
+                scalar_write: bool = False, act: bool = False) -> dict:
     """Draw one seeded input set for workload ``w``.
 
     zero_content: Ub = Uw = 0 (the memory-blind special case).
     bx_mean:      override the erase-logit location (erase-heavy stress uses 0).
     gated:        raw decay logits f with per-head A, tau_f instead of g.
     scalar_write: a per-head write logit wx [B,T,H] and no Uw, Vw.
+    act:          q, k, v are raw projections (the layer applies the activations).
     """
     rng = np.random.Generator(np.random.PCG64(seed))
     B, T, H, Dk, Dv, R = w.B, w.T, w.H, w.Dk, w.Dv, w.R
@@ -159,4 +164,9 @@ def make_inputs(w: Workload, seed: int = 0, *, zero_content: bool = False,
         out["wx"] = round_bf16(wxs) if w.dtype == "bf16" else wxs
         out["Uw"] = None
         out["Vw"] = None
+    if act:
+        raw = [_normal(rng, (B, T, H, Dk)), _normal(rng, (B, T, H, Dk)), _normal(rng, (B, T, H, Dv))]
+        if w.dtype == "bf16":
+            raw = [round_bf16(a) for a in raw]
+        out["q"], out["k"], out["v"] = raw
     return out

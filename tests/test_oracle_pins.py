@@ -646,3 +646,79 @@ def test_chunked_gate_deviation_is_flat_in_L():
     assert 1e-5 < dev[0] < 1e-2
     assert max(dev) < 1.5 * dev[0]
     assert abs(dev[3] - dev[2]) < dev[1] - dev[0]
+
+
+# --------------------------------------------------------------------------
+# input activations (Sec. input projections, Fig. carve_block): q, k =
+# L2-norm(SiLU(raw)) over d_k, v = SiLU(raw)
+# --------------------------------------------------------------------------
+def test_silu_and_l2_activation_special_values():
+    """SiLU(0) = 0, SiLU'(0) = 1/2, SiLU(x) -> x and SiLU'(x) -> 1 for large x,
+    SiLU(x) -> 0 for very negative x; the activated q, k have unit norm (to the
+    epsilon) and the direction of SiLU(raw); the values equal x * expit(x) of
+    scipy."""
+    from scipy.special import expit
+    x = np.array([0.0, 30.0, -30.0, 1.5, -0.7])
+    assert orc.silu(x)[0] == 0.0 and orc.silu_grad(x)[0] == 0.5
+    assert abs(orc.silu(x)[1] - 30.0) < 1e-11 and abs(orc.silu_grad(x)[1] - 1.0) < 1e-11
+    assert abs(orc.silu(x)[2]) < 1e-11
+    np.testing.assert_allclose(orc.silu(x), x * expit(x), rtol=1e-15, atol=0)
+    rng = np.random.default_rng(0)
+    r = rng.standard_normal((3, 5, 2, 16))
+    y = orc.act_qk(r)
+    n = np.linalg.norm(y, axis=-1)
+    s = r * expit(r)
+    ns = np.linalg.norm(s, axis=-1)
+    np.testing.assert_allclose(n, ns / np.sqrt(ns ** 2 + orc.L2_EPS), rtol=1e-14)
+    np.testing.assert_allclose(y * ns[..., None], s * n[..., None], rtol=1e-12, atol=1e-15)
+
+
+def test_l2_activation_gradient_is_orthogonal_to_the_output_direction():
+    """Scaling SiLU(raw) does not move the normalised output (up to the
+    epsilon), so the gradient with respect to s = SiLU(raw) is orthogonal to
+    s; checked through dx / SiLU'(x)."""
+    rng = np.random.default_rng(1)
+    r = rng.standard_normal((4, 3, 2, 32)) + 1.0
+    dy = rng.standard_normal(r.shape)
+    ds = orc.act_qk_bwd(r, dy) / orc.silu_grad(r)
+    s = orc.silu(r)
+    cos = np.sum(ds * s, axis=-1) / (np.linalg.norm(ds, axis=-1) * np.linalg.norm(s, axis=-1))
+    assert np.max(np.abs(cos)) < 1e-6
+
+
+ACT_GRADS = [("q", "dq"), ("k", "dk"), ("v", "dv"), ("beta", "dbeta"), ("bx", "dbx"), ("Ub", "dUb"), ("S0", "dS0")]
+
+
+def _act_loss(x, L):
+    o = orc.fwd_act(x, L)
+    return float(np.sum(o["o"] * x["dO"]) + np.sum(o["S_T"] * x["dS_T"]))
+
+
+@pytest.mark.parametrize("L,T,Dk,Dv,R", [(8, 32, 8, 6, 3), (4, 16, 5, 7, 2)])
+def test_act_backward_directional_finite_differences(L, T, Dk, Dv, R):
+    w = Workload("fd", B=2, H=2, T=T, Dk=Dk, Dv=Dv, L=L, R=R, dtype="f32", mu=2.0, s0=0.3, u_std=0.4)
+    inp = _f64(make_inputs(w, seed=L + Dk + 1, dS_T=True, act=True))
+    gr = orc.bwd_act(inp, L, inp["dO"], inp["dS_T"])
+    rng = np.random.default_rng(L + 7)
+    h = 1e-6
+    for name, gname in ACT_GRADS:
+        dirn = rng.standard_normal(inp[name].shape)
+        xp = dict(inp); xp[name] = inp[name] + h * dirn
+        xm = dict(inp); xm[name] = inp[name] - h * dirn
+        fd = (_act_loss(xp, L) - _act_loss(xm, L)) / (2 * h)
+        an = float(np.sum(gr[gname] * dirn))
+        assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-3), (name, fd, an)
+
+
+def test_act_backward_coordinates_of_q_k_v():
+    w = Workload("fd", B=1, H=1, T=8, Dk=4, Dv=3, L=4, R=2, dtype="f32", mu=2.0, s0=0.3, u_std=0.5)
+    inp = _f64(make_inputs(w, seed=31, dS_T=True, act=True))
+    gr = orc.bwd_act(inp, 4, inp["dO"], inp["dS_T"])
+    h = 1e-6
+    for name, gname in (("q", "dq"), ("k", "dk"), ("v", "dv")):
+        for idx in range(inp[name].size):
+            xp = dict(inp); xp[name] = inp[name].copy(); xp[name].reshape(-1)[idx] += h
+            xm = dict(inp); xm[name] = inp[name].copy(); xm[name].reshape(-1)[idx] -= h
+            fd = (_act_loss(xp, 4) - _act_loss(xm, 4)) / (2 * h)
+            an = gr[gname].reshape(-1)[idx]
+            assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-2), (name, idx, fd, an)
