@@ -140,15 +140,17 @@ def traffic_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir):
     print(json.dumps(rec), flush=True)
 
 
-def cpu_baseline(w, L, seed, target_s=12.0, gated=False, sw=False):
+def cpu_baseline(w, L, seed, target_s=12.0, gated=False, sw=False, act=False):
     """Time the CPU oracle (token-serial forward + exact backward, double) on the
     whole workload batch, repeated until about target_s seconds of CPU work."""
     from oracle import oracle as orc
     from paper_2606_27229_amd.inputs import make_inputs
 
-    inp = make_inputs(w, seed=seed, gated=gated, scalar_write=sw)
+    inp = make_inputs(w, seed=seed, gated=gated, scalar_write=sw, act=act)
     threads = max(1, min(16, os.cpu_count() or 1, w.B * w.H))
-    if sw:
+    if act:
+        fwd, bwd = orc.fwd_act, orc.bwd_act
+    elif sw:
         fwd, bwd = orc.fwd_sw, orc.bwd_sw
     else:
         fwd = orc.fwd_gated if gated else orc.fwd_serial
@@ -180,6 +182,9 @@ def main():
     ap.add_argument("--gated", action="store_true",
                     help="the gate-in-kernel variant: the decay is formed in the kernels from its raw "
                          "logit f (bf16) and per-head A, tau_f (carve_chunk_fwd_gated / _bwd_gated)")
+    ap.add_argument("--act", action="store_true",
+                    help="the input activations inside the kernels: q, k, v are the raw projections "
+                         "(SiLU, then L2 norm for q, k; carve_chunk_fwd_act / _bwd_act)")
     ap.add_argument("--scalar-write", action="store_true",
                     help="the scalar write gate: one write logit per token and head, no write-side "
                          "content (carve_chunk_fwd_sw / _bwd_sw; with --gated, the decay from f)")
@@ -219,8 +224,11 @@ def main():
     L = w.L
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    gated, sw = args.gated, args.scalar_write
-    inp = make_inputs(w, seed=4, gated=gated, scalar_write=sw)
+    gated, sw, act = args.gated, args.scalar_write, args.act
+    if act and (gated or sw):
+        print("--act runs with the default decay and write gate only", file=sys.stderr)
+        sys.exit(2)
+    inp = make_inputs(w, seed=4, gated=gated, scalar_write=sw, act=act)
     x = {}
     for key, val in inp.items():
         if val is None:
@@ -266,7 +274,7 @@ def main():
                                   x["Ub"], x["Uw"], x["Vb"], x["Vw"], x["S0"], L=L, out=fwd_out)
         else:
             carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
-                            x["Vb"], x["Vw"], x["S0"], L=L, out=fwd_out)
+                            x["Vb"], x["Vw"], x["S0"], L=L, out=fwd_out, act=act)
 
     def bwd():
         if sw:
@@ -279,7 +287,7 @@ def main():
         else:
             carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
                             x["Vb"], x["Vw"], fwd_out["S_chunks"], x["dO"], None, L=L, out=bwd_out,
-                            workspace=ws)
+                            workspace=ws, act=act)
 
     for _ in range(args.warmup):
         fwd()
@@ -288,7 +296,7 @@ def main():
     stream = torch.cuda.current_stream()
     # launch-boundary events recorded by the library: forward 1 kernel, backward 6
     # (7 with the gate-in-kernel decay: the reduction of dA, dtau)
-    NF, NB = 2, (8 if gated else 7)
+    NF, NB = 2, (8 if (gated or act) else 7)
     ev_f = [[torch.cuda.Event(enable_timing=True) for _ in range(NF)] for _ in range(args.steps)]
     ev_b = [[torch.cuda.Event(enable_timing=True) for _ in range(NB)] for _ in range(args.steps)]
     for e in [x for row in ev_f + ev_b for x in row]:
@@ -311,6 +319,8 @@ def main():
                  "carve_bwd_uparam_kernel", "carve_param_reduce_kernel[dU]", "carve_param_reduce_kernel[dV]"]
     if gated:
         bwd_names.append("carve_gate_reduce_kernel")
+    if act:
+        bwd_names.append("carve_act_bwd_kernel")
     kernels_ms = {"carve_chain_fwd_kernel": avg(ev_f, 0)}
     for i, name in enumerate(bwd_names):
         kernels_ms[name] = avg(ev_b, i)
@@ -325,7 +335,7 @@ def main():
     dom_bytes = alg[dominant]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     # the counters were taken on the default variant
-    traffic = None if (gated or sw) else load_traffic(dominant)
+    traffic = None if (gated or sw or act) else load_traffic(dominant)
     layer_tflops = (cnt["fwd_flops"] + cnt["bwd_flops"]) / (ms_per_step * 1e-3) / 1e12
     res = {
         "metric": METRIC,
@@ -343,7 +353,8 @@ def main():
         "config": {"workload": w.name, "B": B, "H": H, "T": T, "Dk": d, "Dv": d, "R": R, "L": L,
                    "token_dtype": "bf16", "state_dtype": "f32",
                    "decay": "formed in the kernels from f, A, tau_f" if gated else "g input (f32)",
-                   "write_gate": "scalar per token and head" if sw else "per value channel, content-aware"},
+                   "write_gate": "scalar per token and head" if sw else "per value channel, content-aware",
+                   "qkv": "raw projections, activations in the kernels" if act else "activated inputs"},
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": None if traffic is None else traffic / (dom_ms * 1e-3) / 1e9,
@@ -357,7 +368,7 @@ def main():
         "layer_tflops": layer_tflops,
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(w, L, seed=4, gated=gated, sw=sw)
+        res["cpu_baseline"] = cpu_baseline(w, L, seed=4, gated=gated, sw=sw, act=act)
     print(json.dumps(res), flush=True)
 
 

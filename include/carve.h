@@ -191,13 +191,40 @@ int carve_chunk_bwd_sw(const carve_dims_t* d, const void* q, const void* k, cons
                        float* dtau, void* dbx, void* dwx, float* dUb, float* dVb, float* dS0,
                        void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* The layer with its input activations inside the kernels (Sec. input
+ * projections, Fig. carve_block, the chunk-local normalisation of
+ * Alg. megakernel fused into the chunk loads):
+ *     q = SiLU(q_raw) / sqrt(|SiLU(q_raw)|^2 + 1e-6)   per (token, head) over Dk,
+ *     k likewise from k_raw, v = SiLU(v_raw).
+ * In:  q, k, v are the raw projections q_raw, k_raw, v_raw (same shapes and
+ *      dtype as in carve_chunk_fwd); every other argument is that of
+ *      carve_chunk_fwd.  The activated q, k, v are never written to memory. */
+int carve_chunk_fwd_act(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                        const void* beta, const float* g, const void* bx, const void* wx,
+                        const float* Ub, const float* Uw, const float* Vb, const float* Vw,
+                        const float* S0, void* o, float* S_T, float* S_chunks, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream);
+
+/* Backward of carve_chunk_fwd_act for loss <dO, o> + <dS_T, S_T>.  Outputs as
+ * carve_chunk_bwd, with dq, dk, dv the gradients with respect to q_raw, k_raw,
+ * v_raw.  The backward makes one more launch than carve_chunk_bwd (the last:
+ * dq, dk taken through the L2 normalisation and SiLU in place). */
+int carve_chunk_bwd_act(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                        const void* beta, const float* g, const void* bx, const void* wx,
+                        const float* Ub, const float* Uw, const float* Vb, const float* Vw,
+                        const float* S_chunks, const void* dO, const float* dS_T, void* dq, void* dk,
+                        void* dv, void* dbeta, float* dg, void* dbx, void* dwx, float* dUb,
+                        float* dUw, float* dVb, float* dVw, float* dS0, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream);
+
 /* Measurement hook (not part of the computation).  Arms the next
  * carve_chunk_fwd / carve_chunk_bwd call made on the calling thread to record
  * events[0] on its stream before its first kernel launch and events[i] after
  * its i-th launch (the forward makes 1 launch; the backward 6: clear of the
  * chunk ready flags, chunk recompute fused with the adjoint, dVb/dVw
  * partials, d[Ub;Uw] partials, two fixed-order reductions; the gated backward
- * a 7th, the reduction of dA, dtau over the batch),
+ * a 7th, the reduction of dA, dtau over the batch; the backward with the
+ * input activations a 7th, the activation gradient of dq, dk),
  * up to `capacity` events.  `events` are hipEvent_t handles created by the
  * caller (hipEventCreate) and owned by the caller; the handles are copied
  * here (the array may be freed after this call) and the events are only

@@ -15,10 +15,11 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libcarve.so")
 # (source, object name, extra flags): carve_variant.hip is compiled once per
-# layer variant (decay given / formed in the kernels x full / scalar write gate)
+# layer variant (decay given / formed in the kernels x full / scalar write
+# gate, and the input activations inside the layer)
 SOURCES = [("carve_abi.hip", "carve_abi", []), ("carve_fwd_chain.hip", "carve_fwd_chain", []),
            ("carve_bwd.hip", "carve_bwd", [])] + [
-    ("carve_variant.hip", f"carve_variant{v}", [f"-DCARVE_VARIANT={v}"]) for v in range(4)]
+    ("carve_variant.hip", f"carve_variant{v}", [f"-DCARVE_VARIANT={v}"]) for v in range(5)]
 
 BUILD = os.path.join(HERE, "_build")
 HIPCC_FLAGS = [

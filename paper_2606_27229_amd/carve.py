@@ -18,8 +18,8 @@ LIB_PATH = os.path.join(_HERE, "libcarve.so")
 
 CARVE_F32, CARVE_BF16 = 0, 1
 SYMBOLS = ("carve_chunk_fwd", "carve_chunk_bwd", "carve_chunk_fwd_gated", "carve_chunk_bwd_gated",
-           "carve_chunk_fwd_sw", "carve_chunk_bwd_sw", "carve_workspace_size", "carve_status_string",
-           "carve_profile_events")
+           "carve_chunk_fwd_sw", "carve_chunk_bwd_sw", "carve_chunk_fwd_act", "carve_chunk_bwd_act",
+           "carve_workspace_size", "carve_status_string", "carve_profile_events")
 
 
 class Dims(ctypes.Structure):
@@ -64,6 +64,10 @@ def load_library(path: str = LIB_PATH):
     lib.carve_chunk_bwd_sw.argtypes = ([D] + [vp] * 4 + [fp, vp, fp, fp, vp, vp, fp, fp, fp, vp, fp]
                                        + [vp] * 4 + [fp, vp, fp, fp, vp, vp, fp, fp, fp, vp, sz, vp])
     lib.carve_chunk_bwd_sw.restype = ctypes.c_int
+    lib.carve_chunk_fwd_act.argtypes = lib.carve_chunk_fwd.argtypes
+    lib.carve_chunk_fwd_act.restype = ctypes.c_int
+    lib.carve_chunk_bwd_act.argtypes = lib.carve_chunk_bwd.argtypes
+    lib.carve_chunk_bwd_act.restype = ctypes.c_int
     lib.carve_profile_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]
     lib.carve_profile_events.restype = ctypes.c_int
     if path == LIB_PATH:
@@ -116,12 +120,14 @@ def _check(fn, st):
 
 
 def chunk_fwd(q, k, v, beta, g, bx, wx, Ub, Uw, Vb, Vw, S0=None, *, L=64, want_chunks=True,
-              want_state=True, out=None, stream=None):
+              want_state=True, out=None, stream=None, act=False):
     """Forward of the chunked CARVE layer.
 
     Shapes: q, k, bx, g [B,T,H,Dk]; v, wx [B,T,H,Dv]; beta [B,T,H]; Ub, Uw [R,Dv];
     Vb [Dk,R]; Vw [Dv,R]; S0 [B,H,Dv,Dk] or None.  Returns (o, S_T, S_chunks).
-    ``out`` may hold preallocated {"o", "S_T", "S_chunks"} tensors.
+    ``out`` may hold preallocated {"o", "S_T", "S_chunks"} tensors.  act=True:
+    q, k, v are the raw projections and the kernels apply SiLU (+ L2 norm for
+    q, k) (carve_chunk_fwd_act).
     """
     lib = load_library()
     B, T, H, Dk = q.shape
@@ -137,7 +143,8 @@ def chunk_fwd(q, k, v, beta, g, bx, wx, Ub, Uw, Vb, Vw, S0=None, *, L=64, want_c
     S_T = out.get("S_T") if "S_T" in out else (torch.empty((B, H, Dv, Dk), dtype=f32, device=q.device) if want_state else None)
     S_chunks = out.get("S_chunks") if "S_chunks" in out else (
         torch.empty((B, H, T // L, Dv, Dk), dtype=f32, device=q.device) if want_chunks else None)
-    st = lib.carve_chunk_fwd(
+    fn = "carve_chunk_fwd_act" if act else "carve_chunk_fwd"
+    st = getattr(lib, fn)(
         ctypes.byref(dims), _ptr(q, "q", dt, (B, T, H, Dk)), _ptr(k, "k", dt, (B, T, H, Dk)),
         _ptr(v, "v", dt, (B, T, H, Dv)), _ptr(beta, "beta", dt, (B, T, H)), _ptr(g, "g", f32, (B, T, H, Dk)),
         _ptr(bx, "bx", dt, (B, T, H, Dk)), _ptr(wx, "wx", dt, (B, T, H, Dv)),
@@ -145,15 +152,16 @@ def chunk_fwd(q, k, v, beta, g, bx, wx, Ub, Uw, Vb, Vw, S0=None, *, L=64, want_c
         _ptr(Vw, "Vw", f32, (Dv, R)), _ptr(S0, "S0", f32, (B, H, Dv, Dk)),
         _ptr(o, "o", dt, (B, T, H, Dv)), _ptr(S_T, "S_T", f32), _ptr(S_chunks, "S_chunks", f32),
         None, 0, _stream(stream))
-    _check("carve_chunk_fwd", st)
+    _check(fn, st)
     return o, S_T, S_chunks
 
 
 def chunk_bwd(q, k, v, beta, g, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO, dS_T=None, *, L=64,
-              want_dS0=True, out=None, workspace=None, stream=None):
+              want_dS0=True, out=None, workspace=None, stream=None, act=False):
     """Backward of the chunked CARVE layer for loss <dO, o> + <dS_T, S_T>.
 
     Returns a dict with dq, dk, dv, dbeta, dg, dbx, dwx, dUb, dUw, dVb, dVw, dS0.
+    act=True: the backward of chunk_fwd(act=True) (gradients of the raw q, k, v).
     """
     lib = load_library()
     B, T, H, Dk = q.shape
@@ -178,7 +186,8 @@ def chunk_bwd(q, k, v, beta, g, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO, dS_T=None,
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     ws_ptr = _ptr(workspace, "workspace") if workspace is not None else None
     ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    st = lib.carve_chunk_bwd(
+    fn = "carve_chunk_bwd_act" if act else "carve_chunk_bwd"
+    st = getattr(lib, fn)(
         ctypes.byref(dims), _ptr(q, "q", dt, (B, T, H, Dk)), _ptr(k, "k", dt, (B, T, H, Dk)),
         _ptr(v, "v", dt, (B, T, H, Dv)), _ptr(beta, "beta", dt, (B, T, H)), _ptr(g, "g", f32, (B, T, H, Dk)),
         _ptr(bx, "bx", dt, (B, T, H, Dk)), _ptr(wx, "wx", dt, (B, T, H, Dv)),
@@ -187,7 +196,7 @@ def chunk_bwd(q, k, v, beta, g, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO, dS_T=None,
         _ptr(dO, "dO", dt, (B, T, H, Dv)), _ptr(dS_T, "dS_T", f32, (B, H, Dv, Dk)),
         *[_ptr(res[n], n) for n in ("dq", "dk", "dv", "dbeta", "dg", "dbx", "dwx", "dUb", "dUw", "dVb", "dVw")],
         _ptr(res.get("dS0"), "dS0"), ws_ptr, ws_len, _stream(stream))
-    _check("carve_chunk_bwd", st)
+    _check(fn, st)
     return res
 
 

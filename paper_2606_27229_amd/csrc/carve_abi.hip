@@ -174,13 +174,16 @@ struct Decay {
 };
 
 // kernel variant of a call
-int variant_of(const Decay& dc, bool sw) { return (dc.gated() ? kVarGated : 0) | (sw ? kVarScalarW : 0); }
+int variant_of(const Decay& dc, bool sw, bool act) {
+  return (dc.gated() ? kVarGated : 0) | (sw ? kVarScalarW : 0) | (act ? kVarAct : 0);
+}
 
-// sw: the scalar write gate (wx [B,T,H], no Uw, Vw)
+// sw: the scalar write gate (wx [B,T,H], no Uw, Vw); act: q, k, v are the raw
+// projections (the kernels apply the input activations)
 int fwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v, const void* beta,
              const Decay& dc, const void* bx, const void* wx, const float* Ub, const float* Uw,
              const float* Vb, const float* Vw, const float* S0, void* o, float* S_T, float* S_chunks,
-             bool sw, hipStream_t stream) {
+             bool sw, bool act, hipStream_t stream) {
   ProfClear pc;
   int st = check_dims(d);
   if (st) return st;
@@ -212,7 +215,7 @@ int fwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v,
   a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = round_rp(d->R); a.L = d->L;
   a.rec = nullptr;
   prof_mark(stream);
-  st = launch_chain_fwd(a, d->dtype, d->Dk, wb, variant_of(dc, sw), stream);
+  st = launch_chain_fwd(a, d->dtype, d->Dk, wb, variant_of(dc, sw, act), stream);
   prof_mark(stream);
   return st;
 }
@@ -229,7 +232,7 @@ int bwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v,
              const float* Vb, const float* Vw, const float* S_chunks, const void* dO, const float* dS_T,
              void* dq, void* dk, void* dv, void* dbeta, const DecayGrad& dd, void* dbx, void* dwx,
              float* dUb, float* dUw, float* dVb, float* dVw, float* dS0, void* workspace,
-             size_t workspace_bytes, bool sw, hipStream_t stream) {
+             size_t workspace_bytes, bool sw, bool act, hipStream_t stream) {
   ProfClear pc;
   int st = check_dims(d);
   if (st) return st;
@@ -296,7 +299,7 @@ int bwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v,
   st = launch_sync_clear(sync, sync_ints((size_t)d->B * d->H, (size_t)(d->T / d->L)), stream);
   if (st) return st;
   prof_mark(stream);
-  st = launch_bwd_fused(f, a, sync, cus, d->dtype, d->Dk, lw, variant_of(dc, sw), stream);
+  st = launch_bwd_fused(f, a, sync, cus, d->dtype, d->Dk, lw, variant_of(dc, sw, act), stream);
   if (st) return st;
   prof_mark(stream);
   // 3. dVb, dVw from dbx, dwx and tau (dVb only with the scalar write gate)
@@ -319,6 +322,12 @@ int bwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v,
   // 6. (gated) dA, dtau summed over the batch
   if (dc.gated()) {
     st = launch_gate_reduce(a.partG, d->B, d->H, d->Dk, dd.dA, dd.dtau, stream);
+    if (st) return st;
+    prof_mark(stream);
+  }
+  // 7. (input activations) dq, dk through the L2 normalisation and SiLU
+  if (act) {
+    st = launch_act_bwd(q, k, dq, dk, (size_t)d->B * d->T * d->H, d->Dk, d->dtype, stream);
     prof_mark(stream);
   }
   return st;
@@ -336,7 +345,7 @@ int carve_chunk_fwd(const carve_dims_t* d, const void* q, const void* k, const v
   (void)workspace;
   (void)workspace_bytes;
   return fwd_impl(d, q, k, v, beta, Decay{g, nullptr, nullptr, nullptr}, bx, wx, Ub, Uw, Vb, Vw, S0, o, S_T,
-                  S_chunks, false, stream);
+                  S_chunks, false, false, stream);
 }
 
 int carve_chunk_fwd_gated(const carve_dims_t* d, const void* q, const void* k, const void* v,
@@ -351,7 +360,7 @@ int carve_chunk_fwd_gated(const carve_dims_t* d, const void* q, const void* k, c
     return CARVE_ERR_NULL;
   }
   return fwd_impl(d, q, k, v, beta, Decay{nullptr, f, A, tau_f}, bx, wx, Ub, Uw, Vb, Vw, S0, o, S_T, S_chunks,
-                  false, stream);
+                  false, false, stream);
 }
 
 int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const void* v,
@@ -363,7 +372,7 @@ int carve_chunk_bwd(const carve_dims_t* d, const void* q, const void* k, const v
                     size_t workspace_bytes, hipStream_t stream) {
   return bwd_impl(d, q, k, v, beta, Decay{g, nullptr, nullptr, nullptr}, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO,
                   dS_T, dq, dk, dv, dbeta, DecayGrad{dg, nullptr, nullptr, nullptr}, dbx, dwx, dUb, dUw, dVb,
-                  dVw, dS0, workspace, workspace_bytes, false, stream);
+                  dVw, dS0, workspace, workspace_bytes, false, false, stream);
 }
 
 int carve_chunk_bwd_gated(const carve_dims_t* d, const void* q, const void* k, const void* v,
@@ -380,7 +389,7 @@ int carve_chunk_bwd_gated(const carve_dims_t* d, const void* q, const void* k, c
   }
   return bwd_impl(d, q, k, v, beta, Decay{nullptr, f, A, tau_f}, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO, dS_T,
                   dq, dk, dv, dbeta, DecayGrad{nullptr, df, dA, dtau}, dbx, dwx, dUb, dUw, dVb, dVw, dS0,
-                  workspace, workspace_bytes, false, stream);
+                  workspace, workspace_bytes, false, false, stream);
 }
 
 int carve_chunk_fwd_sw(const carve_dims_t* d, const void* q, const void* k, const void* v,
@@ -395,7 +404,7 @@ int carve_chunk_fwd_sw(const carve_dims_t* d, const void* q, const void* k, cons
     return g ? CARVE_ERR_ARG : CARVE_ERR_NULL;
   }
   const Decay dc = g ? Decay{g, nullptr, nullptr, nullptr} : Decay{nullptr, f, A, tau_f};
-  return fwd_impl(d, q, k, v, beta, dc, bx, wx, Ub, nullptr, Vb, nullptr, S0, o, S_T, S_chunks, true, stream);
+  return fwd_impl(d, q, k, v, beta, dc, bx, wx, Ub, nullptr, Vb, nullptr, S0, o, S_T, S_chunks, true, false, stream);
 }
 
 int carve_chunk_bwd_sw(const carve_dims_t* d, const void* q, const void* k, const void* v,
@@ -412,7 +421,30 @@ int carve_chunk_bwd_sw(const carve_dims_t* d, const void* q, const void* k, cons
   const Decay dc = g ? Decay{g, nullptr, nullptr, nullptr} : Decay{nullptr, f, A, tau_f};
   const DecayGrad dd = g ? DecayGrad{dg, nullptr, nullptr, nullptr} : DecayGrad{nullptr, df, dA, dtau};
   return bwd_impl(d, q, k, v, beta, dc, bx, wx, Ub, nullptr, Vb, nullptr, S_chunks, dO, dS_T, dq, dk, dv, dbeta, dd,
-                  dbx, dwx, dUb, nullptr, dVb, nullptr, dS0, workspace, workspace_bytes, true, stream);
+                  dbx, dwx, dUb, nullptr, dVb, nullptr, dS0, workspace, workspace_bytes, true, false, stream);
+}
+
+int carve_chunk_fwd_act(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                        const void* beta, const float* g, const void* bx, const void* wx,
+                        const float* Ub, const float* Uw, const float* Vb, const float* Vw,
+                        const float* S0, void* o, float* S_T, float* S_chunks, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  return fwd_impl(d, q, k, v, beta, Decay{g, nullptr, nullptr, nullptr}, bx, wx, Ub, Uw, Vb, Vw, S0, o, S_T,
+                  S_chunks, false, true, stream);
+}
+
+int carve_chunk_bwd_act(const carve_dims_t* d, const void* q, const void* k, const void* v,
+                        const void* beta, const float* g, const void* bx, const void* wx,
+                        const float* Ub, const float* Uw, const float* Vb, const float* Vw,
+                        const float* S_chunks, const void* dO, const float* dS_T, void* dq, void* dk,
+                        void* dv, void* dbeta, float* dg, void* dbx, void* dwx, float* dUb,
+                        float* dUw, float* dVb, float* dVw, float* dS0, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
+  return bwd_impl(d, q, k, v, beta, Decay{g, nullptr, nullptr, nullptr}, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO,
+                  dS_T, dq, dk, dv, dbeta, DecayGrad{dg, nullptr, nullptr, nullptr}, dbx, dwx, dUb, dUw, dVb,
+                  dVw, dS0, workspace, workspace_bytes, false, true, stream);
 }
 
 }  // extern "C"

@@ -46,6 +46,11 @@
 // channel, no write-side content) the fold is Ub S_hat alone, there is no
 // dtau_w, and the gradient of the token's write logit is the sum over the
 // value channels: dwx_t = sum_v d(wv)_tv v_tv w_t (1 - w_t).
+// With the input activations (kVarAct) the token tiles of q, k, v are staged
+// raw; the inverse L2 norms of the block's SiLU(k), SiLU(q) rows are summed
+// while staging, the quads are activated when read, and dv is taken through
+// SiLU' here.  dq and dk leave this kernel as gradients of the activated q, k;
+// carve_act_bwd_kernel takes them through the L2 normalisation and SiLU.
 #pragma once
 #include "carve_rec.h"
 
@@ -108,6 +113,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
   constexpr bool GATED = (VAR & kVarGated) != 0;
   constexpr bool SW = (VAR & kVarScalarW) != 0;
+  constexpr bool ACT = (VAR & kVarAct) != 0;
   constexpr int NT = bwd_threads(D);
   constexpr int NW = NT / 64;
   constexpr int NJT = D / 16;
@@ -125,7 +131,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   const int b = bh / H, h = bh % H;
   const int nch = Tn / L, nbc = L / 16;
 
-  constexpr BwdLds lay = bwd_lds<T, D, RP, SW>();
+  constexpr BwdLds lay = bwd_lds<T, D, RP, VAR>();
   constexpr int NS = bwd_stage_tiles(SW);             // staged token tiles per block
   T* sF = reinterpret_cast<T*>(smem + lay.F);        // [R2][LDD]    F of the chunk
   T* sVbT = reinterpret_cast<T*>(smem + lay.VbT);    // [RP][LDD]    Vb^T
@@ -137,6 +143,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);    // [16] beta, then [16] sigmoid(wx) (SW)
   float* sDbeta = reinterpret_cast<float*>(smem + lay.Dbeta);  // [NW][16]
   float* sDwx = reinterpret_cast<float*>(smem + lay.Dwx);      // [NW][16] (SW)
+  float* sInv = reinterpret_cast<float*>(smem + lay.Inv);      // [2][16] 1/|SiLU(k)|, 1/|SiLU(q)| (ACT)
   T* sKt = reinterpret_cast<T*>(smem + lay.Kt);      // [16][LDD]
   T* sQt = reinterpret_cast<T*>(smem + lay.Qt);      // [16][LDD]
   T* sKi = reinterpret_cast<T*>(smem + lay.Ki);      // [16][LDD]
@@ -220,6 +227,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   constexpr int NSV = NS * 16 * NC;              // vectors of the tiles
   constexpr int NSTG = (NSV + NT - 1) / NT;      // per thread
   static_assert((16 * NC) % 64 == 0 || NSV % NT == 0, "tile index uniform per wave");
+  static_assert(!ACT || (16 * NC) % 64 == 0, "a staged row's chunks in one wave (row sums over lanes)");
   u32x4 pstg[NSTG];
   // g of a block: 16 rows of D floats, one 16-byte vector per thread
   constexpr int NGC = D / 4;                     // 16-byte chunks per g row
@@ -404,6 +412,14 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         if (NSV % NT != 0 && x >= NSV) break;
         const int s_ = x / (16 * NC), t = (x / NC) % 16, kk = x % NC;
         *reinterpret_cast<u32x4*>(sStg + (s_ * 16 + t) * D + (kk ^ (t & (NC - 1))) * VEC) = lstg[u];
+        if constexpr (ACT) {
+          // k (s_ = 0) and q (s_ = 1) rows: the row's NC chunks are in NC
+          // consecutive lanes, and s_ is uniform over a wave
+          if (s_ < 2) {
+            const float inv = act_row_inv_norm<T, NC>(lstg[u]);
+            if (kk == 0) sInv[s_ * 16 + t] = inv;
+          }
+        }
       }
       if constexpr (GATED) {
         if (tid < 16 * NC) {
@@ -419,6 +435,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       // + 3) and of tau_b; read before the barrier that ends this step, so the
       // value-side step may overwrite the staging region
       quad kq, qq, lbx, vq, wxq, dOq, ltq[NRB];
+      quad vraw;  // ACT: the raw value quad (for SiLU' of dv)
       quad lfq;   // GATED: f (row t = c, key channels 16 w + 4 g + e)
       f32x4 lg;
       {
@@ -440,6 +457,12 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         vq = Qd::ld(r0 + 48 * D);
         dOq = Qd::ld(r0 + 64 * D);
         if constexpr (!SW) wxq = Qd::ld(r0 + 80 * D);
+        if constexpr (ACT) {
+          kq = Qd::cvt(silu4(Qd::f32(kq)) * sInv[c]);
+          qq = Qd::cvt(silu4(Qd::f32(qq)) * sInv[16 + c]);
+          vraw = vq;
+          vq = Qd::cvt(silu4(Qd::f32(vq)));
+        }
         for (int ks = 0; ks < NRB; ++ks) ltq[ks] = Qd::ld(sTau + c * LDR + 16 * ks + 4 * g);
       }
       // key-side factors kept for the adjoint in the token dtype (quads)
@@ -534,7 +557,10 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
           dvv[i] = dwv[i] * wgt[i];
           dzw[i] = dwv[i] * vv[i] * wgt[i] * (1.0f - wgt[i]);
         }
-        Qd::st(dv + e0, Qd::cvt(Qd::mma16(Qd::cvt(dvv), CARVE_FI(), zero4())));
+        if constexpr (ACT)
+          Qd::st(dv + e0, Qd::cvt(Qd::mma16(Qd::cvt(dvv), CARVE_FI(), zero4()) * silu_grad4(Qd::f32(vraw))));
+        else
+          Qd::st(dv + e0, Qd::cvt(Qd::mma16(Qd::cvt(dvv), CARVE_FI(), zero4())));
         const quad dzwq = Qd::cvt(dzw);
         if constexpr (SW) {
           // the token's write-logit gradient, partial over this wave's 16 values
@@ -815,7 +841,7 @@ carve_bwd_fused_kernel(FwdArgs f, BwdArgs a, int nrec, int* sync) {
 // ---------------------------------------------------------------------------
 template <typename T, int D, int LW, int RP, int VAR>
 static int launch_fused_t(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, hipStream_t stream) {
-  constexpr size_t lds = fused_lds<T, D, LW, RP, (VAR & kVarScalarW) != 0>();
+  constexpr size_t lds = fused_lds<T, D, LW, RP, VAR>();
   if constexpr (lds > kMaxLdsBytes) {
     return CARVE_ERR_UNSUPPORTED;
   } else {

@@ -176,6 +176,65 @@ __global__ void __launch_bounds__(256) carve_param_reduce_kernel(const float* __
   }
 }
 
+// Reverse mode of the query / key activation (kVarAct), in place: with
+// s = SiLU(raw) over a row of D channels, n = sqrt(|s|^2 + eps) and y = s / n,
+//   d raw = (dy - y (y . dy)) / n * SiLU'(raw).
+// One 16-byte chunk per thread; a row's D / VEC chunks are consecutive threads
+// of one wave, so the two row sums run over those lanes.  blockIdx.y selects
+// q (0) or k (1).
+template <typename T, int D>
+__global__ void __launch_bounds__(256) carve_act_bwd_kernel(const T* __restrict__ qraw, const T* __restrict__ kraw,
+                                                            T* __restrict__ dq, T* __restrict__ dk, size_t rows) {
+  constexpr int VEC = 16 / sizeof(T), NC = D / VEC, N = Chunk16<T>::N;
+  static_assert(256 % NC == 0 && NC <= 64, "rows inside one wave");
+  const T* raw = blockIdx.y ? kraw : qraw;
+  T* dy = blockIdx.y ? dk : dq;
+  const size_t n = rows * NC;
+  const size_t x = (size_t)blockIdx.x * 256 + threadIdx.x;
+  // a row is wholly inside or outside [0, n): lanes past the end work on the
+  // last chunk (every lane takes part in the row sums) and store nothing
+  const size_t xc = x < n ? x : n - 1;
+  float f[N], d[N], sv[N];
+  Chunk16<T>::unpack(*reinterpret_cast<const u32x4_t*>(raw + xc * VEC), f);
+  Chunk16<T>::unpack(*reinterpret_cast<const u32x4_t*>(dy + xc * VEC), d);
+  float ss = 0.0f;
+  for (int i = 0; i < N; ++i) {
+    sv[i] = silu_f(f[i]);
+    ss += sv[i] * sv[i];
+  }
+  const float inv = rsqrtf(group_sum<NC>(ss) + kL2Eps);
+  float dot = 0.0f;
+  for (int i = 0; i < N; ++i) dot += sv[i] * inv * d[i];
+  dot = group_sum<NC>(dot);
+  for (int i = 0; i < N; ++i) d[i] = (d[i] - sv[i] * inv * dot) * inv * silu_grad_f(f[i]);
+  if (x < n) *reinterpret_cast<u32x4_t*>(dy + x * VEC) = Chunk16<T>::pack(d);
+}
+
+template <typename T, int D>
+static int launch_act_bwd_t(const void* qr, const void* kr, void* dq, void* dk, size_t rows, hipStream_t s) {
+  constexpr int NC = D / (16 / sizeof(T));
+  const size_t blocks = (rows * NC + 255) / 256;
+  hipLaunchKernelGGL((carve_act_bwd_kernel<T, D>), dim3((unsigned)blocks, 2), dim3(256), 0, s,
+                     reinterpret_cast<const T*>(qr), reinterpret_cast<const T*>(kr), reinterpret_cast<T*>(dq),
+                     reinterpret_cast<T*>(dk), rows);
+  return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
+}
+
+template <typename T>
+static int launch_act_bwd_d(const void* qr, const void* kr, void* dq, void* dk, size_t rows, int D, hipStream_t s) {
+  if (D == 32) return launch_act_bwd_t<T, 32>(qr, kr, dq, dk, rows, s);
+  if (D == 64) return launch_act_bwd_t<T, 64>(qr, kr, dq, dk, rows, s);
+  if (D == 128) return launch_act_bwd_t<T, 128>(qr, kr, dq, dk, rows, s);
+  return CARVE_ERR_UNSUPPORTED;
+}
+
+int launch_act_bwd(const void* q_raw, const void* k_raw, void* dq, void* dk, size_t rows, int D, int dtype,
+                   hipStream_t s) {
+  if (rows == 0) return CARVE_OK;
+  if (dtype == CARVE_BF16) return launch_act_bwd_d<bf16_t>(q_raw, k_raw, dq, dk, rows, D, s);
+  return launch_act_bwd_d<float>(q_raw, k_raw, dq, dk, rows, D, s);
+}
+
 // Zero the synchronisation area of the fused launch (ready flags, ticket).
 __global__ void __launch_bounds__(256) carve_sync_clear_kernel(int* __restrict__ sync, int n) {
   const int x = blockIdx.x * 256 + threadIdx.x;
@@ -195,6 +254,7 @@ int launch_bwd_fused(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, int
     case kVarScalarW: return launch_bwd_fused_var<kVarScalarW>(f, a, sync, cus, dtype, D, LW, s);
     case kVarGated | kVarScalarW:
       return launch_bwd_fused_var<kVarGated | kVarScalarW>(f, a, sync, cus, dtype, D, LW, s);
+    case kVarAct: return launch_bwd_fused_var<kVarAct>(f, a, sync, cus, dtype, D, LW, s);
     default: return CARVE_ERR_UNSUPPORTED;
   }
 }
@@ -224,9 +284,9 @@ int launch_gate_reduce(const float* partG, int B, int H, int D, float* dA, float
 
 template <typename T, int D, int RP>
 static size_t fused_lds_l(int LW) {
-  if (LW == 16) return fused_lds<T, D, 16, RP, false>();
-  if (LW == 32) return fused_lds<T, D, 32, RP, false>();
-  if (LW == 64) return fused_lds<T, D, 64, RP, false>();
+  if (LW == 16) return fused_lds<T, D, 16, RP, 0>();
+  if (LW == 32) return fused_lds<T, D, 32, RP, 0>();
+  if (LW == 64) return fused_lds<T, D, 64, RP, 0>();
   return (size_t)-1;
 }
 

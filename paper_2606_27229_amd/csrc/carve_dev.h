@@ -257,4 +257,99 @@ __device__ __forceinline__ float tanh_f(float y) {
   return fabsf(y) < 0.125f ? small : big;
 }
 
+// ---- input activations (queries and keys: SiLU then L2 norm; values: SiLU) --
+__device__ __forceinline__ float silu_f(float x) { return x * sigmoid_f(x); }
+// d SiLU / dx = sigmoid(x) (1 + x (1 - sigmoid(x)))
+__device__ __forceinline__ float silu_grad_f(float x) {
+  const float s = sigmoid_f(x);
+  return s * (1.0f + x * (1.0f - s));
+}
+__device__ __forceinline__ f32x4 silu4(f32x4 x) {
+  f32x4 o;
+  for (int e = 0; e < 4; ++e) o[e] = silu_f(x[e]);
+  return o;
+}
+__device__ __forceinline__ f32x4 silu_grad4(f32x4 x) {
+  f32x4 o;
+  for (int e = 0; e < 4; ++e) o[e] = silu_grad_f(x[e]);
+  return o;
+}
+// the L2 normalisation is x / sqrt(|x|^2 + eps)
+constexpr float kL2Eps = 1e-6f;
+
+// sum over aligned groups of N consecutive lanes (N a power of two dividing
+// 64), in every lane of the group; every lane of the wave must take part.
+// Within a row of 16 lanes a DPP butterfly (lane ^ 1, lane ^ 2, then the
+// half-row and row mirrors, which pair each lane with one in the other half);
+// across rows lane shuffles.  Every step adds two values in either order, so
+// all lanes of a group get the bitwise same sum.
+template <int N>
+__device__ __forceinline__ float group_sum(float x) {
+  static_assert(N >= 1 && N <= 64 && (N & (N - 1)) == 0, "power of two up to a wave");
+  if constexpr (N >= 2)
+    x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0xB1, 0xf, 0xf, false));
+  if constexpr (N >= 4)
+    x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x4E, 0xf, 0xf, false));
+  if constexpr (N >= 8)   // row_half_mirror: lane i <-> 7 - i within each half-row
+    x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x141, 0xf, 0xf, false));
+  if constexpr (N >= 16)  // row_mirror: lane i <-> 15 - i within each row
+    x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x140, 0xf, 0xf, false));
+  if constexpr (N >= 32) x += __shfl_xor(x, 16);
+  if constexpr (N >= 64) x += __shfl_xor(x, 32);
+  return x;
+}
+
+// 16 bytes of the token dtype <-> floats
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+template <typename T>
+struct Chunk16;
+template <>
+struct Chunk16<bf16_t> {
+  static constexpr int N = 8;
+  static __device__ __forceinline__ void unpack(u32x4_t v, float* f) {
+    const bf16x8 b = __builtin_bit_cast(bf16x8, v);
+    for (int i = 0; i < 8; ++i) f[i] = (float)b[i];
+  }
+  static __device__ __forceinline__ u32x4_t pack(const float* f) {
+    bf16x8 b;
+    for (int i = 0; i < 8; ++i) b[i] = (bf16_t)f[i];
+    return __builtin_bit_cast(u32x4_t, b);
+  }
+};
+template <>
+struct Chunk16<float> {
+  static constexpr int N = 4;
+  static __device__ __forceinline__ void unpack(u32x4_t v, float* f) {
+    const f32x4 b = __builtin_bit_cast(f32x4, v);
+    for (int i = 0; i < 4; ++i) f[i] = b[i];
+  }
+  static __device__ __forceinline__ u32x4_t pack(const float* f) {
+    const f32x4 b = {f[0], f[1], f[2], f[3]};
+    return __builtin_bit_cast(u32x4_t, b);
+  }
+};
+
+// Sum over a row of SiLU(raw)^2, the row spread as 16-byte chunks over NC
+// consecutive lanes (every lane of the wave must take part); returns
+// 1 / sqrt(sum + eps), in every lane of the row.
+template <typename T, int NC>
+__device__ __forceinline__ float act_row_inv_norm(u32x4_t raw) {
+  float f[Chunk16<T>::N];
+  Chunk16<T>::unpack(raw, f);
+  float ss = 0.0f;
+  for (int i = 0; i < Chunk16<T>::N; ++i) {
+    const float sv = silu_f(f[i]);
+    ss += sv * sv;
+  }
+  return rsqrtf(group_sum<NC>(ss) + kL2Eps);
+}
+// SiLU(raw) * scale of one chunk
+template <typename T>
+__device__ __forceinline__ u32x4_t act_chunk(u32x4_t raw, float scale) {
+  float f[Chunk16<T>::N];
+  Chunk16<T>::unpack(raw, f);
+  for (int i = 0; i < Chunk16<T>::N; ++i) f[i] = silu_f(f[i]) * scale;
+  return Chunk16<T>::pack(f);
+}
+
 }  // namespace carve

@@ -40,7 +40,9 @@
 //
 // With the scalar write gate (kVarScalarW) the fold has the Ub rows only, the
 // write logit of a token is one scalar per head, staged with beta, and w v is
-// that gate times v.
+// that gate times v.  With the input activations (kVarAct) q, k and v arrive
+// raw: the rows of q and k are staged as SiLU(raw) / |SiLU(raw)| (the norm
+// summed over the row's lanes while staging), v as SiLU(raw).
 //
 // Precondition (not checked): inside one WY block the log retention summed
 // over the block stays above about -170 per key channel (factors up to
@@ -80,6 +82,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   typedef typename Qd::q quad;
   constexpr bool GATED = (VAR & kVarGated) != 0;
   constexpr bool SW = (VAR & kVarScalarW) != 0;
+  constexpr bool ACT = (VAR & kVarAct) != 0;
   constexpr int NT = fwd_threads(D);
   constexpr int NW = NT / 64;
   constexpr int NJT = D / 16;
@@ -103,7 +106,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   const int bh = blockIdx.x, b = bh / H, h = bh % H;
 
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  constexpr ChainLds lay = chain_lds<T, D, WB, RP, SW>();
+  constexpr ChainLds lay = chain_lds<T, D, WB, RP, VAR>();
   T* sU = reinterpret_cast<T*>(smem + lay.U);      // [R2][LDD]   [Ub; 0; Uw; 0] or [Ub; 0]
   T* sS = reinterpret_cast<T*>(smem + lay.X);      // [D][LDD]    S_hat[v][j]
   T* sKt = reinterpret_cast<T*>(smem + lay.Kt);    // [WB][LDD]   (aliases sS)
@@ -119,7 +122,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   float* sRho = reinterpret_cast<float*>(smem + lay.Rho);  // [D] e^{rho} = e^{lam_end / 2}
   float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);  // [2][WB] (block parity)
   float* sWs = sBeta + 2 * WB;                     // [2][WB] sigmoid(wx) (SW; block parity)
-  constexpr bool SVW = chain_stage_vw<T, D, WB, RP, SW>();
+  constexpr bool SVW = chain_stage_vw<T, D, WB, RP, VAR>();
   T* sVW = reinterpret_cast<T*>(smem + lay.VW);    // [2][WB][D]  v, wx (swizzled; SVW; v only with SW)
   float* sGate = reinterpret_cast<float*>(smem + lay.Gate);  // [2][D] -exp(A), tau_f (GATED)
 
@@ -182,6 +185,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   constexpr int VEC = 16 / sizeof(T);                // elements per 16-byte vector
   constexpr int NVX = WB * D / VEC;                  // vectors of one [WB][D] tile
   constexpr int NXV = (NVX + NT - 1) / NT;           // per thread
+  static_assert(NVX % 64 == 0, "whole waves of row chunks (the row sums run over lanes)");
   u32x4 cq[NXV], ck[NXV], cbx[NXV];
   quad pv[NB], pwx[NB];      // per-tile value-side operands (without SVW)
   u32x4 cv[NXV], cwx[NXV];   // whole rows of v and wx (with SVW)
@@ -255,16 +259,20 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       if (NVX % NT != 0 && x_ >= NVX) break;                                       \
       const int t_ = x_ / NC, kk_ = x_ % NC;                                       \
       T* d_ = sVW + t_ * D + (kk_ ^ (t_ & (NC - 1))) * VEC;                        \
-      *reinterpret_cast<u32x4*>(d_) = cv[u_];                                      \
+      *reinterpret_cast<u32x4*>(d_) = ACT ? act_chunk<T>(cv[u_], 1.0f) : cv[u_];   \
       if constexpr (!SW) *reinterpret_cast<u32x4*>(d_ + WB * D) = cwx[u_];         \
     }                                                                              \
   } while (0)
-#define CARVE_STAGE_ROWS(DST_, SRC_)                                               \
+  // (L2_: the rows are raw q or k, staged activated; a row's D / VEC chunks
+  // sit in consecutive lanes of one wave, so its norm is a sum over them)
+#define CARVE_STAGE_ROWS(DST_, SRC_, L2_)                                          \
   do {                                                                             \
     for (int u_ = 0; u_ < NXV; ++u_) {                                             \
       const int x_ = tid + u_ * NT;                                                \
       if (NVX % NT != 0 && x_ >= NVX) break;                                       \
-      *reinterpret_cast<u32x4*>((DST_) + (x_ / (D / VEC)) * LDD + (x_ % (D / VEC)) * VEC) = (SRC_)[u_]; \
+      u32x4 r_ = (SRC_)[u_];                                                       \
+      if constexpr (L2_) r_ = act_chunk<T>(r_, act_row_inv_norm<T, D / VEC>(r_));  \
+      *reinterpret_cast<u32x4*>((DST_) + (x_ / (D / VEC)) * LDD + (x_ % (D / VEC)) * VEC) = r_; \
     }                                                                              \
   } while (0)
   CARVE_PREFETCH_Q(0);
@@ -314,7 +322,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     if (cstart) {
       for (int jt = 0; jt < NJT; ++jt) Qd::st(sS + (16 * w + c) * LDD + 16 * jt + 4 * g, Qd::cvt(St[jt]));
     }
-    CARVE_STAGE_ROWS(sQ, cq);
+    CARVE_STAGE_ROWS(sQ, cq, ACT);
     if (w == 0 && lane < WB) {
       sBeta[par * WB + lane] = (float)pbeta;
       if constexpr (SW) sWs[par * WB + lane] = sigmoid_f((float)pws);
@@ -326,7 +334,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     __syncthreads();
     CARVE_STORE_S(0, NJT / 2);
     // raw keys of the block into free LDS (read by the gates)
-    CARVE_STAGE_ROWS(sKi, ck);
+    CARVE_STAGE_ROWS(sKi, ck, ACT);
     if constexpr (SVW) CARVE_STAGE_VW();
 
     // ---- fold F^T[j][r] = sum_v S_hat[v][j] U[r][v] (key tile w) --------------
@@ -344,7 +352,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       __syncthreads();
     }
     // raw erase logits into region X (the fold is done with the state)
-    CARVE_STAGE_ROWS(sBx, cbx);
+    CARVE_STAGE_ROWS(sBx, cbx, false);
     // the previous block's outputs
     if (oprev >= 0) {
       int cs = c, gs = g;
@@ -429,6 +437,8 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
         const T* r0 = sVW + t * D + ((((by >> 4) ^ (t & (NC - 1))) << 4) | (by & 15)) / (int)sizeof(T);
         vq = Qd::ld(r0);
         if constexpr (!SW) wxq = Qd::ld(r0 + WB * D);
+      } else if constexpr (ACT) {
+        vq = Qd::cvt(silu4(Qd::f32(vq)));
       }
       const f32x4 vv = Qd::mma16(vq, fI, zero4());
       if constexpr (SW) {
@@ -590,7 +600,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
 // ---------------------------------------------------------------------------
 template <typename T, int D, int WB, int RP, int VAR>
 static int launch_chain_t(const FwdArgs& a, hipStream_t stream) {
-  constexpr ChainLds lay = chain_lds<T, D, WB, RP, (VAR & kVarScalarW) != 0>();
+  constexpr ChainLds lay = chain_lds<T, D, WB, RP, VAR>();
   if constexpr (lay.total > kMaxLdsBytes) {
     (void)a;
     (void)stream;

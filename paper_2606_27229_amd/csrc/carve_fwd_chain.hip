@@ -11,15 +11,16 @@ int launch_chain_fwd(const FwdArgs& a, int dtype, int D, int WB, int var, hipStr
     case kVarGated: return launch_chain_fwd_var<kVarGated>(a, dtype, D, WB, s);
     case kVarScalarW: return launch_chain_fwd_var<kVarScalarW>(a, dtype, D, WB, s);
     case kVarGated | kVarScalarW: return launch_chain_fwd_var<kVarGated | kVarScalarW>(a, dtype, D, WB, s);
+    case kVarAct: return launch_chain_fwd_var<kVarAct>(a, dtype, D, WB, s);
     default: return CARVE_ERR_UNSUPPORTED;
   }
 }
 
 template <typename T, int D, int RP>
 static size_t chain_lds_w(int WB) {
-  if (WB == 16) return chain_lds<T, D, 16, RP, false>().total;
-  if (WB == 32) return chain_lds<T, D, 32, RP, false>().total;
-  if (WB == 64) return chain_lds<T, D, 64, RP, false>().total;
+  if (WB == 16) return chain_lds<T, D, 16, RP, 0>().total;
+  if (WB == 32) return chain_lds<T, D, 32, RP, 0>().total;
+  if (WB == 64) return chain_lds<T, D, 64, RP, 0>().total;
   return (size_t)-1;
 }
 

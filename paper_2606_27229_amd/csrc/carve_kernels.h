@@ -12,9 +12,13 @@ namespace carve {
 //   kVarScalarW: the scalar write gate (Sec. scalar write gate): one logit wx
 //                per (token, head), w = sigmoid(wx) on every value channel and
 //                no content term on the write side, so the fold is F = Ub S_hat
-//                (R rows instead of 2R) and there is no Uw, Vw.
-enum : int { kVarGated = 1, kVarScalarW = 2 };
-constexpr int kNumVariants = 4;
+//                (R rows instead of 2R) and there is no Uw, Vw;
+//   kVarAct:     q, k, v are the raw projections; the kernels apply the input
+//                activations (Sec. input projections, Fig. carve_block): q, k =
+//                SiLU then L2 normalisation over d_k, v = SiLU.
+// Built: every combination of kVarGated and kVarScalarW, and kVarAct alone.
+enum : int { kVarGated = 1, kVarScalarW = 2, kVarAct = 4 };
+__host__ __device__ constexpr bool var_built(int var) { return var >= 0 && var <= kVarAct; }
 
 // rows of the fold F (and columns of tau) of a variant, R padded to RP:
 // [Ub; 0; Uw; 0], or [Ub; 0] with the scalar write gate
@@ -89,15 +93,17 @@ __host__ __device__ constexpr int lk_of() {
 // blocks); SW: the scalar write gate (RP fold rows instead of 2RP).  Every row is padded by 16 bytes.  Region X holds
 // the copy of the chunk start state while the fold runs and the per-token
 // key-side operands after.  Beta holds beta, then the scalar write gates.
+// Kn (kVarAct) holds per-wave partial sums of the squared activated keys.
 struct RecLds {
-  size_t U, Q, F, Tau, Beta, X, S, Kt, Qt, Ki, Gam, AT, Tm, Gate, total;
+  size_t U, Q, F, Tau, Beta, X, S, Kt, Qt, Ki, Gam, AT, Tm, Gate, Kn, total;
 };
 
-template <typename T, int D, int LW, int RP, bool SW>
+template <typename T, int D, int LW, int RP, int VAR>
 __host__ __device__ constexpr RecLds rec_lds() {
   RecLds l{};
   const size_t e = sizeof(T);
-  constexpr size_t RF = SW ? RP : 2 * RP;
+  constexpr bool SW = (VAR & kVarScalarW) != 0;
+  constexpr size_t RF = fold_rows(RP, VAR);
   constexpr size_t NB = LW / 16;
   constexpr size_t PAD = 16 / sizeof(T);
   constexpr size_t LDD = D + PAD, LDR = RF + PAD, LDB = 16 + PAD;
@@ -119,6 +125,7 @@ __host__ __device__ constexpr RecLds rec_lds() {
   x = lds_max(x, lds_round(D * LDD * e));
   off += x;
   l.Gate = off; off += lds_round(2 * D * 4);   // -exp(A), tau_f of the head (gated)
+  l.Kn = off;   off += (VAR & kVarAct) ? lds_round((D / 16) * LW * 4) : 0;
   l.total = off;
   return l;
 }
@@ -138,11 +145,12 @@ struct ChainLds {
   size_t U, X, Kt, Bx, Ki, F, Q, Tau, A, P, AdT, TmT, VW, Rho, Beta, Gate, total;
 };
 
-template <typename T, int D, int WB, int RP, bool SW, bool VW>
+template <typename T, int D, int WB, int RP, int VAR, bool VW>
 __host__ __device__ constexpr ChainLds chain_lds_v() {
   ChainLds l{};
   const size_t e = sizeof(T);
-  constexpr size_t RF = SW ? RP : 2 * RP;
+  constexpr bool SW = (VAR & kVarScalarW) != 0;
+  constexpr size_t RF = fold_rows(RP, VAR);
   constexpr size_t NB = WB / 16;
   constexpr size_t PAD = 16 / sizeof(T);
   constexpr size_t LDD = D + PAD, LDR = RF + PAD, LDW = WB + PAD, LDB = 16 + PAD;
@@ -169,14 +177,14 @@ __host__ __device__ constexpr ChainLds chain_lds_v() {
 }
 
 // whether the value-side tiles are staged (the layout with VW fits)
-template <typename T, int D, int WB, int RP, bool SW>
+template <typename T, int D, int WB, int RP, int VAR>
 __host__ __device__ constexpr bool chain_stage_vw() {
-  return chain_lds_v<T, D, WB, RP, SW, true>().total <= kMaxLdsBytes;
+  return chain_lds_v<T, D, WB, RP, VAR, true>().total <= kMaxLdsBytes;
 }
 
-template <typename T, int D, int WB, int RP, bool SW>
+template <typename T, int D, int WB, int RP, int VAR>
 __host__ __device__ constexpr ChainLds chain_lds() {
-  return chain_lds_v<T, D, WB, RP, SW, chain_stage_vw<T, D, WB, RP, SW>()>();
+  return chain_lds_v<T, D, WB, RP, VAR, chain_stage_vw<T, D, WB, RP, VAR>()>();
 }
 
 // forward of the whole sequence (one workgroup per (batch, head)), WY blocks of
@@ -185,7 +193,7 @@ __host__ __device__ constexpr ChainLds chain_lds() {
 int launch_chain_fwd(const FwdArgs& a, int dtype, int D, int WB, int var, hipStream_t s);
 template <int VAR>
 int launch_chain_fwd_var(const FwdArgs& a, int dtype, int D, int WB, hipStream_t s);
-// LDS bytes of the chain forward with 2RP fold rows (the largest variant)
+// LDS bytes of the chain forward of the default variant (2RP fold rows)
 size_t chain_lds_bytes(int dtype, int D, int WB, int RP);
 
 
@@ -229,19 +237,22 @@ constexpr int kUSplit = 16;
 // -exp(A), tau_f of the head (Gate) behind it, inside the area g would take
 // where that is large enough.  Beta holds beta, then the scalar write gates;
 // Dwx the per-wave partial sums of the scalar write gate's gradient.
+// Inv (kVarAct) holds the inverse L2 norms of the block's activated keys and
+// queries.
 struct BwdLds {
-  size_t F, VbT, VwT, Tau, Tm, P, Gam, Beta, Dbeta, Dwx, Kt, Qt, Ki, Sx, dSx, dOT, uT, dRT, dzwT, Stage, Gate,
+  size_t F, VbT, VwT, Tau, Tm, P, Gam, Beta, Dbeta, Dwx, Inv, Kt, Qt, Ki, Sx, dSx, dOT, uT, dRT, dzwT, Stage, Gate,
       dzb, dY, total;
 };
 
 // token tiles the adjoint stages per block
 __host__ __device__ constexpr int bwd_stage_tiles(bool SW) { return SW ? 5 : 6; }
 
-template <typename T, int D, int RP, bool SW>
+template <typename T, int D, int RP, int VAR>
 __host__ __device__ constexpr BwdLds bwd_lds() {
   BwdLds l{};
   const size_t e = sizeof(T);
-  constexpr size_t RF = SW ? RP : 2 * RP;
+  constexpr bool SW = (VAR & kVarScalarW) != 0;
+  constexpr size_t RF = fold_rows(RP, VAR);
   constexpr size_t NW = D / 16;
   constexpr size_t PAD = 16 / sizeof(T);
   constexpr size_t LDD = D + PAD, LDR = RF + PAD, LDB = 16 + PAD;
@@ -257,6 +268,7 @@ __host__ __device__ constexpr BwdLds bwd_lds() {
   l.Beta = off;  off += lds_round((SW ? 32 : 16) * 4);
   l.Dbeta = off; off += lds_round(NW * 16 * 4);
   l.Dwx = off;   off += SW ? lds_round(NW * 16 * 4) : 0;
+  l.Inv = off;   off += (VAR & kVarAct) ? lds_round(2 * 16 * 4) : 0;
   l.Kt = off;    off += lds_round(16 * LDD * e);
   l.Qt = off;    off += lds_round(16 * LDD * e);
   l.Ki = off;    off += lds_round(16 * LDD * e);
@@ -280,9 +292,9 @@ __host__ __device__ constexpr BwdLds bwd_lds() {
 }
 
 // LDS of the fused chunk recompute + adjoint launch
-template <typename T, int D, int LW, int RP, bool SW>
+template <typename T, int D, int LW, int RP, int VAR>
 __host__ __device__ constexpr size_t fused_lds() {
-  return lds_max(rec_lds<T, D, LW, RP, SW>().total, bwd_lds<T, D, RP, SW>().total);
+  return lds_max(rec_lds<T, D, LW, RP, VAR>().total, bwd_lds<T, D, RP, VAR>().total);
 }
 
 // Chunk recompute and adjoint in one launch (see carve_bwd.h).  f carries the
@@ -298,8 +310,8 @@ int launch_bwd_fused_var(const FwdArgs& f, const BwdArgs& a, int* sync, int cus,
 // dA[h][j], dtau[h][j] = sums over b (in order) of the per-(b,h) partials
 int launch_gate_reduce(const float* partG, int B, int H, int D, float* dA, float* dtau, hipStream_t s);
 int launch_sync_clear(int* sync, size_t n, hipStream_t s);
-// LDS bytes of the fused launch with LW-token recompute sub-chunks and 2RP
-// fold rows (the largest variant)
+// LDS bytes of the fused launch of the default variant with LW-token
+// recompute sub-chunks (2RP fold rows)
 size_t bwd_lds_bytes(int dtype, int D, int LW, int RP);
 // ints of the synchronisation area: one ready flag per chunk, the ticket
 // counter that assigns the workgroup roles, padding
@@ -310,6 +322,10 @@ int launch_bwd_uparam(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s
 // sum nparts records of 2 * half floats into dst0 (first half) and dst1; with
 // dst1 == NULL only the first half is summed
 int launch_param_reduce(const float* part, int nparts, size_t half, float* dst0, float* dst1, hipStream_t s);
+// kVarAct: turn dq, dk (gradients of the activated q, k, in place, [rows][D]) into
+// the gradients of the raw projections q_raw, k_raw
+int launch_act_bwd(const void* q_raw, const void* k_raw, void* dq, void* dk, size_t rows, int D, int dtype,
+                   hipStream_t s);
 
 // floats of one partial-gradient record: d[Ub; Uw] ([R][D] twice) or dVb, dVw ([D][R] twice)
 __host__ __device__ constexpr size_t part_floats(int R, int D) { return (size_t)2 * R * D; }

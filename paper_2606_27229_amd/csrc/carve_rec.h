@@ -30,6 +30,9 @@
 //
 // With the scalar write gate (kVarScalarW) F = Ub S_hat has R rows and
 // w_t = sigmoid(wx_t) is one scalar per token and head, staged with beta.
+// With the input activations (kVarAct) q, k, v arrive raw: q rows are staged
+// as SiLU(raw) / |SiLU(raw)|; a key's norm is summed from per-wave partials
+// through LDS (each wave holds 16 of its channels); v is SiLU(raw).
 //
 // Precondition (not checked): within any 16-token block the log retention
 // summed over the block stays above about -80 per key channel, so that
@@ -52,6 +55,7 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
   typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
   constexpr bool GATED = (VAR & kVarGated) != 0;
   constexpr bool SW = (VAR & kVarScalarW) != 0;
+  constexpr bool ACT = (VAR & kVarAct) != 0;
   constexpr int NT = fwd_threads(D);
   constexpr int NW = NT / 64;          // waves == 16-wide tiles of the key / value axis
   constexpr int NJT = D / 16;
@@ -65,6 +69,7 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
   constexpr int NQV = (NVQ + NT - 1) / NT;     // per thread
   static_assert(NW == NJT, "one wave per 16-wide tile");
   static_assert(D % 32 == 0, "K32 steps over the key / value axis");
+  static_assert(NVQ % 64 == 0, "whole waves of row chunks (the row sums run over lanes)");
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
@@ -72,7 +77,7 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
   const int nch = Tn / L, msub = L / LW;
   const int b = bh / H, h = bh % H;
 
-  constexpr RecLds lay = rec_lds<T, D, LW, RP, SW>();
+  constexpr RecLds lay = rec_lds<T, D, LW, RP, VAR>();
   T* sU = reinterpret_cast<T*>(smem + lay.U);      // [R2][LDD]   [Ub; 0; Uw; 0] or [Ub; 0]
   T* sQ = reinterpret_cast<T*>(smem + lay.Q);      // [LW][LDD]   raw q
   T* sF = reinterpret_cast<T*>(smem + lay.F);      // [R2][LDD]   F
@@ -86,6 +91,7 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
   float* sAT = reinterpret_cast<float*>(smem + lay.AT);    // [NB][16][20] A^T per block
   T* sTm = reinterpret_cast<T*>(smem + lay.Tm);            // [NB][16][LDB] T per block
   float* sGate = reinterpret_cast<float*>(smem + lay.Gate);  // [2][D] -exp(A), tau_f (GATED)
+  float* sKn = reinterpret_cast<float*>(smem + lay.Kn);      // [NW][LW] partial |SiLU(k)|^2 (ACT)
 
   // token tensors addressed from this (batch, head)'s first element with 32-bit
   // offsets t * rs + column (rs = H * D elements between consecutive tokens)
@@ -190,7 +196,19 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
       const int x = tid + u * NT;
       if (NVQ % NT != 0 && x >= NVQ) break;
       const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;
-      *reinterpret_cast<u32x4*>(sQ + t * LDD + j) = pq[u];
+      u32x4 r = pq[u];
+      if constexpr (ACT) r = act_chunk<T>(r, act_row_inv_norm<T, D / VEC>(r));
+      *reinterpret_cast<u32x4*>(sQ + t * LDD + j) = r;
+    }
+    if constexpr (ACT) {
+      // this wave's part of |SiLU(k)|^2 for every token of the sub-chunk
+      for (int bb = 0; bb < NB; ++bb) {
+        const f32x4 kf = silu4(Qd::f32(pk[bb]));
+        float p = kf[0] * kf[0] + kf[1] * kf[1] + kf[2] * kf[2] + kf[3] * kf[3];
+        p += __shfl_xor(p, 16);
+        p += __shfl_xor(p, 32);
+        if (g == 0) sKn[w * LW + 16 * bb + c] = p;
+      }
     }
     if (tid < LW) {
       sBeta[tid] = (float)pbeta;
@@ -237,7 +255,14 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
       f32x4 z = zero4();
       for (int ks = 0; ks < RP / 16; ++ks)
         z = Qd::mma16(fVb[ks], Qd::ld(sTau + (16 * bb + c) * LDR + 16 * ks + 4 * g), z);
-      const f32x4 bxv = Qd::f32(pbx[bb]), kv = Qd::f32(pk[bb]);
+      const f32x4 bxv = Qd::f32(pbx[bb]);
+      f32x4 kv = Qd::f32(pk[bb]);
+      if constexpr (ACT) {
+        float n2 = 0.0f;
+        for (int ww = 0; ww < NW; ++ww) n2 += sKn[ww * LW + 16 * bb + c];
+        // rounded to the token dtype like the staged keys of the other kernels
+        kv = Qd::f32(Qd::cvt(silu4(kv) * rsqrtf(n2 + kL2Eps)));
+      }
       f32x4 gv;
       if constexpr (GATED) {
         const f32x4 fv = Qd::f32(pf[bb]);
@@ -271,7 +296,7 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
     // value side, value tile w: rows t = 16 bb + 4 g + i, column v = 16 w + c
     f32x4 wv[NB];
     for (int bb = 0; bb < NB; ++bb) {
-      const f32x4 vv = Qd::mma16(pv[bb], fI, zero4());
+      const f32x4 vv = Qd::mma16(ACT ? Qd::cvt(silu4(Qd::f32(pv[bb]))) : pv[bb], fI, zero4());
       if constexpr (SW) {
         const f32x4 ws = *reinterpret_cast<const f32x4*>(sBeta + LW + 16 * bb + 4 * g);
         for (int i = 0; i < 4; ++i) wv[bb][i] = ws[i] * vv[i];
