@@ -94,7 +94,6 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   constexpr int LDD = D + PAD, LDR = R2 + PAD, LDW = WB + PAD, LDB = 16 + PAD;
   constexpr int NTA = NB * (NB - 1) / 2;   // off-diagonal tiles of A
   constexpr int NTP = NB * (NB + 1) / 2;   // tiles of P
-  constexpr int TW = NW - 1;               // the wave that inverts the diagonal tiles
   static_assert(NW == NJT && NW >= 2, "one wave per 16-wide tile, at least two waves");
   static_assert(D % 32 == 0, "K32 steps over the key / value axis");
 
@@ -117,7 +116,6 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   T* sTau = reinterpret_cast<T*>(smem + lay.Tau);  // [WB][LDR]   tau[t][r]
   T* sA = reinterpret_cast<T*>(smem + lay.A);      // [WB][LDW]   -A[t][s] (off-diagonal tiles)
   T* sP = reinterpret_cast<T*>(smem + lay.P);      // [WB][LDW]   P[t][s]
-  float* sAdT = reinterpret_cast<float*>(smem + lay.AdT);  // [NB][16][20] A_ii[t][s] at (s, t)
   T* sTmT = reinterpret_cast<T*>(smem + lay.TmT);          // [NB][16][LDB] T_ii[t][s] at (s, t)
   float* sRho = reinterpret_cast<float*>(smem + lay.Rho);  // [D] e^{rho} = e^{lam_end / 2}
   float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);  // [2][WB] (block parity)
@@ -463,58 +461,55 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     CARVE_STORE_S(NJT / 2, NJT);
     CARVE_PREFETCH_G(blk + 1 < nblk ? blk + 1 : blk);
     const float* bcur = sBeta + par * WB;
-    if (w == TW) {
-      // diagonal tiles of A in f32, stored transposed: sAdT[i][s][t] = A[t][s]
-      for (int i = 0; i < NB; ++i) {
-        f32x4 acc = zero4();   // acc[e] = Kt_{t = 16 i + 4 g + e} . Ki_{s = 16 i + c}
+    // Diagonal 16 x 16 tiles: T_ii = (I + A_ii)^{-1}.  A_ii is strictly lower
+    // triangular, so with M = -A_ii (M^16 = 0)
+    //   T_ii = sum_{k < 16} M^k = (I + M)(I + M^2)(I + M^4)(I + M^8):
+    // eight f32 matrix-core products (M^2, M^4 and their transposes, M^8, then
+    // the three factors), no serial substitution.  An operand used on the left
+    // is held as its transpose in the result layout, so each power is formed
+    // both ways.  NDW waves (one per SIMD) take the diagonal tiles, the others
+    // (all waves when each has a diagonal tile) the off-diagonal ones.
+    constexpr int NDW = NB < NW ? NB : NW;
+    constexpr int NOW = NW > NDW ? NW - NDW : NW;   // off-diagonal workers
+    if (w >= NW - NDW) {
+      typedef Quad<float> Qf;
+      for (int i = NW - 1 - w; i < NB; i += NDW) {
+        f32x4 acc = zero4(), accT = zero4();
         const T* kr = sKt + (16 * i + c) * LDD + 4 * g;
         const T* ir = sKi + (16 * i + c) * LDD + 4 * g;
-        for (int jp = 0; jp < D / 32; ++jp)
-          acc = Qd::mma32(Qd::ld(kr + 32 * jp), Qd::ld(kr + 32 * jp + 16), Qd::ld(ir + 32 * jp),
-                          Qd::ld(ir + 32 * jp + 16), acc);
+        for (int jp = 0; jp < D / 32; ++jp) {
+          const quad k0 = Qd::ld(kr + 32 * jp), k1 = Qd::ld(kr + 32 * jp + 16);
+          const quad i0 = Qd::ld(ir + 32 * jp), i1 = Qd::ld(ir + 32 * jp + 16);
+          acc = Qd::mma32(k0, k1, i0, i1, acc);     // Kt_{t = 16 i + 4 g + e} . Ki_{s = 16 i + c}
+          accT = Qd::mma32(i0, i1, k0, k1, accT);   // Ki_{s = 16 i + 4 g + e} . Kt_{t = 16 i + c}
+        }
         const f32x4 bt = *reinterpret_cast<const f32x4*>(bcur + 16 * i + 4 * g);
-        f32x4 av;
-        for (int e = 0; e < 4; ++e) av[e] = (c < 4 * g + e) ? bt[e] * acc[e] : 0.0f;
-        *reinterpret_cast<f32x4*>(sAdT + (i * 16 + c) * 20 + 4 * g) = av;
-      }
-      // T_ii = (I + A_ii)^{-1}: lane (g, c) computes column s = c of block g by
-      // forward substitution, x[t] = delta(t, c) - sum_{m < t} A[t][m] x[m]
-      if (g < NB) {
-        const float* Ab = sAdT + g * 16 * 20;
-        float acc[16], x[16];
-#pragma unroll
-        for (int t = 0; t < 16; ++t) acc[t] = 0.0f;
-#pragma unroll
-        for (int m = 0; m < 16; ++m) {
-          x[m] = (m == c ? 1.0f : 0.0f) - acc[m];
-          const float* col = Ab + m * 20;   // A[t][m] for t = 0..15
-#pragma unroll
-          for (int t4 = (m + 1) / 4; t4 < 4; ++t4) {
-            const f32x4 a4 = *reinterpret_cast<const f32x4*>(col + 4 * t4);
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (4 * t4 + e > m) acc[4 * t4 + e] += a4[e] * x[m];
-          }
+        const float bc = bcur[16 * i + c];
+        f32x4 mB, mA, I4;   // M in the result layout (M[4g+e][c]) and transposed (M[c][4g+e])
+        for (int e = 0; e < 4; ++e) {
+          mB[e] = (c < 4 * g + e) ? -bt[e] * acc[e] : 0.0f;
+          mA[e] = (4 * g + e < c) ? -bc * accT[e] : 0.0f;
+          I4[e] = (4 * g + e == c) ? 1.0f : 0.0f;
         }
-        T* dst = sTmT + (g * 16 + c) * LDB;   // row s = c of T^T: T[t][c], t = 0..15
-#pragma unroll
-        for (int t4 = 0; t4 < 4; ++t4) {
-          const f32x4 v4 = {x[4 * t4], x[4 * t4 + 1], x[4 * t4 + 2], x[4 * t4 + 3]};
-          Qd::st(dst + 4 * t4, Qd::cvt(v4));
-        }
+        const f32x4 M2 = Qf::mma16(mA, mB, zero4());
+        const f32x4 M2t = Qf::mma16(mB, mA, zero4());
+        const f32x4 M4 = Qf::mma16(M2t, M2, zero4());
+        const f32x4 M4t = Qf::mma16(M2, M2t, zero4());
+        const f32x4 M8 = Qf::mma16(M4t, M4, zero4());
+        const f32x4 W = Qf::mma16(M4t + I4, M8 + I4, zero4());   // (I + M^4)(I + M^8)
+        const f32x4 W2 = Qf::mma16(M2t + I4, W, zero4());        // (I + M^2) W
+        const f32x4 Ti = Qf::mma16(mA + I4, W2, zero4());        // (I + M) W2
+        // T_ii[t = 4g + e][s = c] at (s, t) of sTmT
+        Qd::st(sTmT + (i * 16 + c) * LDB + 4 * g, Qd::cvt(Ti));
       }
-    } else {
+    }
+    if (NOW == NW || w < NOW) {
       // off-diagonal tiles of -A and all tiles of P, stored [t][s]; a scalar
-      // loop over this wave's tiles (addresses from opaque lane coordinates).
-      // With 8 waves, waves w and w + 4 share a SIMD; the T-wave's partner
-      // takes no tiles, so the substitution gets its SIMD's issue slots.
+      // loop over this wave's tiles (addresses from opaque lane coordinates)
       int ct = c, gt = g;
       asm volatile("" : "+v"(ct), "+v"(gt));
-      constexpr int NWK = NW == 8 ? NW - 2 : NW - 1;        // tile workers
-      const int wk = (NW == 8 && w > TW - 4) ? w - 1 : w;   // worker index
-      const int xend = (NW == 8 && w == TW - 4) ? 0 : NTA + NTP;
 #pragma unroll 1
-      for (int x = wk; x < xend; x += NWK) {
+      for (int x = w; x < NTA + NTP; x += NOW) {
         const bool isA = x < NTA;
         const int y = isA ? x : x - NTA;
         const int i = tri_row(y, isA), j = tri_col(y, isA);

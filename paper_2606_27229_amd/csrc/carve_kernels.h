@@ -142,7 +142,7 @@ __host__ __device__ constexpr RecLds rec_lds() {
 // written only after the gates.  Without VW those tiles are read per wave.
 // Beta holds beta and (scalar write gate) w of the block, for two blocks.
 struct ChainLds {
-  size_t U, X, Kt, Bx, Ki, F, Q, Tau, A, P, AdT, TmT, VW, Rho, Beta, Gate, total;
+  size_t U, X, Kt, Bx, Ki, F, Q, Tau, A, P, TmT, VW, Rho, Beta, Gate, total;
 };
 
 template <typename T, int D, int WB, int RP, int VAR, bool VW>
@@ -165,7 +165,6 @@ __host__ __device__ constexpr ChainLds chain_lds_v() {
   l.Tau = off;  off += lds_round(WB * LDR * e);
   l.A = off;    off += lds_round(WB * LDW * e);
   l.P = off;    off += lds_round(WB * LDW * e);
-  l.AdT = off;  off += lds_round(NB * 16 * 20 * 4);
   l.TmT = off;  off += lds_round(NB * 16 * LDB * e);
   l.VW = l.A;
   if (VW) off = lds_max(off, l.VW + lds_round(2 * WB * (size_t)D * e));
