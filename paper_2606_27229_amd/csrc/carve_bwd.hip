@@ -143,34 +143,38 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_vparam_kernel(BwdArg
 }
 
 // Sum nparts partial records (2 * half floats each) in a fixed order: thread
-// (x, y) of a 64 x 4 block sums records y, y + 4, ... of element x, then the
-// four partial sums are added in order y = 0..3.  Elements x < cnt are summed
-// (cnt = 2 * half, or half when there is no dst1).
-__global__ void __launch_bounds__(256) carve_param_reduce_kernel(const float* __restrict__ part, int nparts,
-                                                                 size_t half, size_t cnt, float* dst0,
-                                                                 float* dst1) {
-  __shared__ float red[4][64];
+// (x, y) of a 64 x 16 block sums records y, y + 16, ... of element x (four
+// loads in flight), then the sixteen partial sums are added in order
+// y = 0..15.  Elements x < cnt are summed (cnt = 2 * half, or half when there
+// is no dst1).
+constexpr int kReduceGroups = 16;
+__global__ void __launch_bounds__(64 * kReduceGroups) carve_param_reduce_kernel(const float* __restrict__ part,
+                                                                                int nparts, size_t half, size_t cnt,
+                                                                                float* dst0, float* dst1) {
+  __shared__ float red[kReduceGroups][64];
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   const size_t x = (size_t)blockIdx.x * 64 + tx;
   const size_t n = 2 * half;
   float s = 0.0f;
   if (x < cnt) {
     const float* p = part + x;
+    constexpr int G = kReduceGroups;
     int q = ty;
-    for (; q + 12 < nparts; q += 16) {
-      const float a0 = p[(size_t)q * n], a1 = p[(size_t)(q + 4) * n];
-      const float a2 = p[(size_t)(q + 8) * n], a3 = p[(size_t)(q + 12) * n];
+    for (; q + 3 * G < nparts; q += 4 * G) {
+      const float a0 = p[(size_t)q * n], a1 = p[(size_t)(q + G) * n];
+      const float a2 = p[(size_t)(q + 2 * G) * n], a3 = p[(size_t)(q + 3 * G) * n];
       s += a0;
       s += a1;
       s += a2;
       s += a3;
     }
-    for (; q < nparts; q += 4) s += p[(size_t)q * n];
+    for (; q < nparts; q += G) s += p[(size_t)q * n];
   }
   red[ty][tx] = s;
   __syncthreads();
   if (ty == 0 && x < cnt) {
-    const float t = ((red[0][tx] + red[1][tx]) + red[2][tx]) + red[3][tx];
+    float t = red[0][tx];
+    for (int y = 1; y < kReduceGroups; ++y) t += red[y][tx];
     if (x < half) dst0[x] = t;
     else dst1[x - half] = t;
   }
@@ -377,7 +381,8 @@ int launch_bwd_uparam(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s
 int launch_param_reduce(const float* part, int nparts, size_t half, float* dst0, float* dst1, hipStream_t s) {
   const size_t cnt = dst1 ? 2 * half : half;
   const int blocks = (int)((cnt + 63) / 64);
-  hipLaunchKernelGGL(carve_param_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, nparts, half, cnt, dst0, dst1);
+  hipLaunchKernelGGL(carve_param_reduce_kernel, dim3(blocks), dim3(64 * kReduceGroups), 0, s, part, nparts, half, cnt,
+                     dst0, dst1);
   return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
 }
 
