@@ -26,7 +26,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 KERNEL_SOURCES = tuple("paper_2606_27229_amd/csrc/" + f for f in (
     "carve_fwd_chain.h", "carve_fwd_chain.hip", "carve_rec.h", "carve_bwd.h", "carve_bwd.hip", "carve_dev.h",
-    "carve_kernels.h", "carve_variant.hip"))
+    "carve_kernels.h", "carve_param.h", "carve_variant.hip"))
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer_1p3b_T4096_L64.json")
 
 
