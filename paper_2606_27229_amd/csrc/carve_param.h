@@ -80,13 +80,19 @@ __device__ __forceinline__ void uparam_item(const BwdArgs& a, const int item, ch
 
 // dVb[j][r] = sum_t dz_b[t][j] tau_b[t][r], dVw[v][r] = sum_t dz_w[t][v] tau_w[t][r]
 // over one token split of one (batch, head); wave w owns rows 16 w .. 16 w + 15.
+// The split is walked in steps of TB tokens staged through LDS (whole rows,
+// 16-byte vectors); the next step's rows are loaded into registers while the
+// current one is multiplied.
 // SW: the scalar write gate (dVb only; tau has the b columns only).
 // item = (batch, head) * kVSplit + split; writes partial record `item`.  smem
 // holds vparam_lds bytes; ends with a workgroup barrier.
+template <typename T>
+__host__ __device__ constexpr int vparam_step_tokens() { return sizeof(T) == 2 ? 64 : 32; }
+
 template <typename T, int D, int RP, bool SW>
 __host__ __device__ constexpr size_t vparam_lds() {
-  constexpr size_t PAD = 16 / sizeof(T);
-  return (2 * 16 * (D + PAD) + 16 * ((SW ? RP : 2 * RP) + PAD)) * sizeof(T);
+  constexpr size_t PAD = 16 / sizeof(T), TB = vparam_step_tokens<T>();
+  return (2 * TB * (D + PAD) + TB * ((SW ? RP : 2 * RP) + PAD)) * sizeof(T);
 }
 
 template <typename T, int D, int RP, bool SW>
@@ -99,9 +105,12 @@ __device__ __forceinline__ void vparam_item(const BwdArgs& a, const int item, ch
   constexpr int PAD = 16 / sizeof(T);
   constexpr int LDD = D + PAD, LDR = R2 + PAD;
   constexpr int VEC = 16 / sizeof(T);
-  T* sB = reinterpret_cast<T*>(smem);          // [16][LDD] dz_b of a block
-  T* sW = sB + 16 * LDD;                       // [16][LDD] dz_w of a block
-  T* sTau = sW + 16 * LDD;                     // [16][LDR] tau of the block
+  constexpr int TB = vparam_step_tokens<T>();
+  constexpr int NC = D / VEC, NCR = R2 / VEC;            // 16-byte vectors per token / tau row
+  constexpr int NVT = (TB * NC + NT - 1) / NT, NTT = (TB * NCR + NT - 1) / NT;
+  T* sB = reinterpret_cast<T*>(smem);          // [TB][LDD] dz_b of a step
+  T* sW = sB + TB * LDD;                       // [TB][LDD] dz_w of a step
+  T* sTau = sW + TB * LDD;                     // [TB][LDR] tau of the step
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
@@ -121,26 +130,60 @@ __device__ __forceinline__ void vparam_item(const BwdArgs& a, const int item, ch
   const int nblk = Tn / 16;
   const int per = (nblk + kVSplit - 1) / kVSplit;
   const int blk0 = split * per, blk1 = blk0 + per < nblk ? blk0 + per : nblk;
-  for (int blk = blk0; blk < blk1; ++blk) {
-    const int t0 = 16 * blk, ch = t0 / L, tl = t0 % L;
-    for (int x = tid; x < 16 * D / VEC; x += NT) {
-      const int t = x / (D / VEC), j = (x % (D / VEC)) * VEC;
-      *reinterpret_cast<u32x4*>(sB + t * LDD + j) = *reinterpret_cast<const u32x4*>(dbx + (t0 + t) * rs + j);
-      if constexpr (!SW)
-        *reinterpret_cast<u32x4*>(sW + t * LDD + j) = *reinterpret_cast<const u32x4*>(dwx + (t0 + t) * rs + j);
+  const int t_begin = 16 * blk0, t_end = 16 * blk1;
+  u32x4 pb[NVT], pw[NVT], pt[NTT];
+  // rows of tokens t0 .. t0 + nt - 1 into registers (vector x of a step: token
+  // x / NC, elements (x % NC) * VEC ..; tau rows from the chunk records)
+  auto load = [&](const int t0) {
+    const int nt = t_end - t0 < TB ? t_end - t0 : TB;
+    for (int u = 0; u < NVT; ++u) {
+      const int x = tid + u * NT;
+      if (x < nt * NC) {
+        const int o = (t0 + x / NC) * rs + (x % NC) * VEC;
+        pb[u] = *reinterpret_cast<const u32x4*>(dbx + o);
+        if constexpr (!SW) pw[u] = *reinterpret_cast<const u32x4*>(dwx + o);
+      }
     }
-    const T* tau = reinterpret_cast<const T*>(recb + (size_t)ch * cr.total + cr.Tau) + tl * R2;
-    for (int x = tid; x < 16 * R2 / VEC; x += NT) {
-      const int t = x / (R2 / VEC), r = (x % (R2 / VEC)) * VEC;
-      *reinterpret_cast<u32x4*>(sTau + t * LDR + r) = *reinterpret_cast<const u32x4*>(tau + t * R2 + r);
+    for (int u = 0; u < NTT; ++u) {
+      const int x = tid + u * NT;
+      if (x < nt * NCR) {
+        const int tt = t0 + x / NCR;
+        const T* tau = reinterpret_cast<const T*>(recb + (size_t)(tt / L) * cr.total + cr.Tau);
+        pt[u] = *reinterpret_cast<const u32x4*>(tau + (tt % L) * R2 + (x % NCR) * VEC);
+      }
     }
+  };
+  auto stage = [&](const int t0) {
+    const int nt = t_end - t0 < TB ? t_end - t0 : TB;
+    for (int u = 0; u < NVT; ++u) {
+      const int x = tid + u * NT;
+      if (x < nt * NC) {
+        const int o = (x / NC) * LDD + (x % NC) * VEC;
+        *reinterpret_cast<u32x4*>(sB + o) = pb[u];
+        if constexpr (!SW) *reinterpret_cast<u32x4*>(sW + o) = pw[u];
+      }
+    }
+    for (int u = 0; u < NTT; ++u) {
+      const int x = tid + u * NT;
+      if (x < nt * NCR) *reinterpret_cast<u32x4*>(sTau + (x / NCR) * LDR + (x % NCR) * VEC) = pt[u];
+    }
+  };
+  if (t_begin < t_end) load(t_begin);
+  for (int t0 = t_begin; t0 < t_end; t0 += TB) {
+    stage(t0);
+    if (t0 + TB < t_end) load(t0 + TB);
     __syncthreads();
-    const typename Qd::q ab = Qd::ld_tr(sB, LDD, 0, 16 * w, g, c);   // lane (g, c): dz_b[t = 4g + e][j = 16 w + c]
-    for (int rt = 0; rt < NRB; ++rt) accB[rt] = Qd::mma16(ab, Qd::ld_tr(sTau, LDR, 0, 16 * rt, g, c), accB[rt]);
-    if constexpr (!SW) {
-      const typename Qd::q aw = Qd::ld_tr(sW, LDD, 0, 16 * w, g, c);
+    const int nb = (t_end - t0 < TB ? t_end - t0 : TB) / 16;
+    for (int bb = 0; bb < nb; ++bb) {
+      // lane (g, c): dz_b[t = 16 bb + 4 g + e][j = 16 w + c]
+      const typename Qd::q ab = Qd::ld_tr(sB + bb * 16 * LDD, LDD, 0, 16 * w, g, c);
       for (int rt = 0; rt < NRB; ++rt)
-        accW[rt] = Qd::mma16(aw, Qd::ld_tr(sTau, LDR, 0, RP + 16 * rt, g, c), accW[rt]);
+        accB[rt] = Qd::mma16(ab, Qd::ld_tr(sTau + bb * 16 * LDR, LDR, 0, 16 * rt, g, c), accB[rt]);
+      if constexpr (!SW) {
+        const typename Qd::q aw = Qd::ld_tr(sW + bb * 16 * LDD, LDD, 0, 16 * w, g, c);
+        for (int rt = 0; rt < NRB; ++rt)
+          accW[rt] = Qd::mma16(aw, Qd::ld_tr(sTau + bb * 16 * LDR, LDR, 0, RP + 16 * rt, g, c), accW[rt]);
+      }
     }
     __syncthreads();
   }
