@@ -590,8 +590,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       {
         const f32x4 kv = Qd::f32(kq), qv = Qd::f32(qq), E = Qd::f32(Eq), Ei = Qd::f32(Eiq), sig = Qd::f32(sigq);
         f32x4 dKt = zero4(), dQt = zero4(), dKi = zero4(), dA = zero4(), dP = zero4();
-        // dS'^T S on the key tile: its diagonal is sum_v dS'[v][j] S[v][j]
-        f32x4 dgd = zero4();
+        float dgs = 0.0f;   // sum_v dS'[v][j] S[v][j] for j = 16 w + c (partial over this lane's v)
         // one pass over the value axis (32 values per step): every operand tile
         // is read from LDS once
         for (int kp = 0; kp < NJT / 2; ++kp) {
@@ -608,8 +607,13 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
           dKi = Qd::mma32(a0, a1, u0, u1, dKi);
           dA = Qd::mma32(r0, r1, u0, u1, dA);
           dP = Qd::mma32(o0, o1, u0, u1, dP);
-          dgd = Qd::mma32(a0, a1, s0, s1, dgd);
+          // (on the VALU: one more accumulating product here costs the gated
+          // kernels registers they do not have)
+          const f32x4 x0 = Qd::f32(a0), x1 = Qd::f32(a1), y0 = Qd::f32(s0), y1 = Qd::f32(s1);
+          for (int e = 0; e < 4; ++e) dgs += x0[e] * y0[e] + x1[e] * y1[e];
         }
+        dgs += __shfl_xor(dgs, 16);
+        dgs += __shfl_xor(dgs, 32);
         const float bc_ = sBeta[c];
         const f32x4 bq = *reinterpret_cast<const f32x4*>(sBeta + 4 * g);
         const f32x4 gmj = *reinterpret_cast<const f32x4*>(sGam + 16 * w + 4 * g);
@@ -618,8 +622,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
           // dgam gam = gam (sum_v dS' S + sum_s Ki_s (dS'^T u_s)), reduced over s = the row
           const float kis = kv[i] * Ei[i];
           const float ds = row_scan(kis * dKi[i]);
-          // diagonal entry j = 16 w + 4 g + i: register i of lane (g, 4 g + i)
-          dgg[i] = gmj[i] * (__shfl(dgd[i], 20 * g + i) + __shfl(ds, (lane & 48) | 15));
+          dgg[i] = gmj[i] * (__shfl(dgs, 4 * g + i) + __shfl(ds, (lane & 48) | 15));
           dKt[i] = -bc_ * dKt[i];
           dKi[i] *= gmj[i];
           const bool lowA = c < 4 * g + i, lowP = c <= 4 * g + i;
