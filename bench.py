@@ -178,6 +178,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--L", type=int, default=64)
+    ap.add_argument("--workload", default=None,
+                    help="another bf16 workload of the layer to time (e.g. layer_1p3b_T2048, long_seq_T16384); "
+                         "the default is the headline layer_1p3b_T4096")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--gated", action="store_true",
                     help="the gate-in-kernel variant: the decay is formed in the kernels from its raw "
@@ -220,7 +223,11 @@ def main():
         print(json.dumps({"copy_calibration": {"read_bytes": n, "write_bytes": n, "launches": 5}}), flush=True)
         return
 
-    w = WORKLOADS[HEADLINE].with_(L=args.L)
+    name = args.workload or HEADLINE
+    if name not in WORKLOADS or WORKLOADS[name].dtype != "bf16" or not WORKLOADS[name].backward:
+        print(f"--workload must be one of the bf16 training workloads, got {name}", file=sys.stderr)
+        sys.exit(2)
+    w = WORKLOADS[name].with_(L=args.L)
     L = w.L
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -335,10 +342,24 @@ def main():
     dom_bytes = alg[dominant]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     # the counters were taken on the default variant
-    traffic = None if (gated or sw or act) else load_traffic(dominant)
+    traffic = None if (gated or sw or act or name != HEADLINE or L != 64) else load_traffic(dominant)
     layer_tflops = (cnt["fwd_flops"] + cnt["bwd_flops"]) / (ms_per_step * 1e-3) / 1e12
+    # achievable HBM bandwidth on this device, for context: a plain 1 GiB
+    # device copy (reads 1 GiB, writes 1 GiB), timed after the measured steps
+    csrc_ = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    cdst_ = torch.empty_like(csrc_)
+    cdst_.copy_(csrc_)
+    c0_, c1_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0_.record(stream)
+    for _ in range(5):
+        cdst_.copy_(csrc_)
+    c1_.record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 5 * 2 * (1 << 30) / (c0_.elapsed_time(c1_) * 1e-3) / 1e9
+    del csrc_, cdst_
     res = {
-        "metric": METRIC,
+        "metric": METRIC if (name == HEADLINE and L == 64) else
+                  f"layer fwd+bwd tokens/s, H={H} d={d} T={T} L={L} bf16; % MFMA peak",
         "value": tokens / (ms_per_step * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -366,6 +387,7 @@ def main():
         "layer_hbm_frac": (cnt["fwd_bytes"] + cnt["bwd_bytes"]) / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "mfma_peak_frac": layer_tflops / BF16_PEAK_TFLOPS,
         "layer_tflops": layer_tflops,
+        "hbm_copy_gbs": copy_gbs,
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, L, seed=4, gated=gated, sw=sw, act=act)
