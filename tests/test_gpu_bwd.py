@@ -121,3 +121,21 @@ def test_bf16_single_chunk():
     w = _w(Dk=128, Dv=128, L=64, T=64, R=32, dtype="bf16", mu=3.0, s0=0.2)
     print("case bf16 D=128 T=L=64", flush=True)
     check_bwd(w, make_inputs(w, seed=64, dS_T=True))
+
+
+def test_bf16_odd_shape():
+    """Odd batch, heads and rank, T of three 16-token chunks at d = 64: every
+    (batch, head) offset, the rank padding (R = 7 of 32) and a chunk count
+    that is not a multiple of anything else."""
+    w = _w(B=3, H=5, T=48, Dk=64, Dv=64, L=16, R=7, dtype="bf16", mu=3.0, s0=0.2)
+    print("case bf16 D=64 B=3 H=5 T=48 L=16 R=7", flush=True)
+    check_bwd(w, make_inputs(w, seed=357, dS_T=True))
+
+
+def test_fp32_one_head_long_chunks():
+    """B = H = 1 (one chain, one adjoint workgroup, every other compute unit a
+    recompute workgroup) with 128-token chunks (two 64-token forward blocks per
+    chunk)."""
+    w = _w(B=1, H=1, T=256, Dk=64, Dv=64, L=128, R=16, dtype="f32", mu=2.0, s0=0.3)
+    print("case fp32 D=64 B=H=1 T=256 L=128", flush=True)
+    check_bwd(w, make_inputs(w, seed=11, dS_T=True))
