@@ -140,6 +140,33 @@ def traffic_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir):
     print(json.dumps(rec), flush=True)
 
 
+def counter_summary(run_dirs):
+    """Per-kernel averages of every counter in rocprofv3 --pmc csv runs (one line
+    of JSON per kernel): the value per dispatch, the number of dispatches and,
+    where the csv carries timestamps, the average dispatch duration in us."""
+    import csv
+    import glob
+    acc = {}
+    for run_dir in run_dirs:
+        for path in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
+            with open(path) as f:
+                for row in csv.DictReader(f):
+                    k = acc.setdefault(row["Kernel_Name"], {"dispatch": {}, "grid": row.get("Grid_Size")})
+                    d = k["dispatch"].setdefault((run_dir, row["Dispatch_Id"]), {})
+                    d[row["Counter_Name"]] = d.get(row["Counter_Name"], 0.0) + float(row["Counter_Value"])
+                    if row.get("Start_Timestamp") and row.get("End_Timestamp"):
+                        d["_us"] = (int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) * 1e-3
+    for name, k in sorted(acc.items()):
+        per = {}
+        for d in k["dispatch"].values():
+            for c, v in d.items():
+                per.setdefault(c, []).append(v)
+        out = {c: sum(v) / len(v) for c, v in per.items()}
+        rec = {"kernel": name, "grid": k["grid"], "dispatches": len(k["dispatch"]),
+               "duration_us": out.pop("_us", None), "counters": out}
+        print(json.dumps(rec), flush=True)
+
+
 def cpu_baseline(w, L, seed, target_s=12.0, gated=False, sw=False, act=False):
     """Time the CPU oracle (token-serial forward + exact backward, double) on the
     whole workload batch, repeated until about target_s seconds of CPU work."""
@@ -194,12 +221,17 @@ def main():
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
                     help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of this benchmark and of "
                          "--copy-calibration into the traffic record read by the roofline (no GPU needed)")
+    ap.add_argument("--counter-summary", nargs="+", metavar="PMC_DIR",
+                    help="print per-kernel averages of the counters in rocprofv3 --pmc csv runs (no GPU needed)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain elementwise copy of 1 GiB (reads 1 GiB, writes 1 GiB) "
                          "five times: the reference kernel for scaling the HBM byte counters")
     args = ap.parse_args()
     if args.traffic_summary:
         traffic_summary(*args.traffic_summary)
+        return
+    if args.counter_summary:
+        counter_summary(args.counter_summary)
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: the layer shards over (batch, head) with no exchange "

@@ -100,6 +100,15 @@ __device__ __forceinline__ int acquire_ready(const int* rdy, const int need) {
 // hoisted above the previous one (bounds the number of live operand registers).
 #define CARVE_SEQ() asm volatile("" ::: "memory")
 
+// Transposing read of the S or dS' tile of a block (rows r0 + 4 g + c / 4,
+// columns c0 + 4 (c % 4)): with the hswz128 layout (SXH) from the lane's
+// precomputed offset sxo (row 4 g + c / 4, its swizzle term), else plain.
+template <bool SXH, typename T, int LDSX>
+__device__ __forceinline__ typename Quad<T>::q ld_sx_tile(const T* buf, int r0, int sxo, int c0, int g, int c) {
+  if constexpr (SXH) return Quad<T>::ld_tr_at(buf + r0 * LDSX + sxo);
+  else return Quad<T>::ld_tr(buf, LDSX, r0, c0, g, c);
+}
+
 // Adjoint of (batch, head) bh.  ready[bh * nch + ch] is raised when chunk ch's
 // record is complete; smem is the workgroup's dynamic LDS (BwdLds layout).
 // GATED: g is formed from its staged raw logit f (Eq. decay_gate); the kernel
@@ -122,11 +131,20 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   constexpr int NRB = RP / 16;
   constexpr int PAD = 16 / sizeof(T);
   constexpr int LDD = D + PAD, LDR = R2 + PAD, LDB = 16 + PAD;
+  // bank-conflict-free layouts (QS): Kt, Qt, Ki, VbT, VwT rows of LDK and the
+  // exchange tiles rows of LDX with the quad swizzle (qx), S and dS' rows of
+  // LDSX (SXH, bf16 d = 128: unpadded with hswz128)
+  constexpr bool QS = bwd_qswz<T, VAR>(), SXH = bwd_sx_hswz<T, D, VAR>();
+  constexpr int LDK = bwd_ldk<T, D, VAR>(), LDX = bwd_ldx<T, VAR>(), LDSX = bwd_ldsx<T, D, VAR>();
   constexpr int VEC = 16 / sizeof(T);
   static_assert(NW == NJT, "one wave per 16-wide tile");
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
+  // the quad-swizzle term of row r, and the transposing operand read, of the
+  // tiles laid out with QS
+#define CARVE_QX(R_) (QS ? qswz<T>(R_) : 0)
+#define CARVE_LDTR(B_, LD_, R0_, C0_) (QS ? Qd::ld_tr_sw(B_, LD_, R0_, C0_, g, c) : Qd::ld_tr(B_, LD_, R0_, C0_, g, c))
   const int H = a.H, Tn = a.T, L = a.L, R = a.R;
   const int b = bh / H, h = bh % H;
   const int nch = Tn / L, nbc = L / 16;
@@ -134,8 +152,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   constexpr BwdLds lay = bwd_lds<T, D, RP, VAR>();
   constexpr int NS = bwd_stage_tiles(SW);             // staged token tiles per block
   T* sF = reinterpret_cast<T*>(smem + lay.F);        // [R2][LDD]    F of the chunk
-  T* sVbT = reinterpret_cast<T*>(smem + lay.VbT);    // [RP][LDD]    Vb^T
-  T* sVwT = reinterpret_cast<T*>(smem + lay.VwT);    // [RP][LDD]    Vw^T (not SW)
+  T* sVbT = reinterpret_cast<T*>(smem + lay.VbT);    // [RP][LDK]    Vb^T (quad-swizzled)
+  T* sVwT = reinterpret_cast<T*>(smem + lay.VwT);    // [RP][LDK]    Vw^T (not SW; quad-swizzled)
   T* sTau = reinterpret_cast<T*>(smem + lay.Tau);    // [16][LDR]    tau of the block
   T* sTm = reinterpret_cast<T*>(smem + lay.Tm);      // [16][LDB]    T of the block
   T* sP = reinterpret_cast<T*>(smem + lay.P);        // [16][LDB]    P of the block
@@ -144,12 +162,12 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   float* sDbeta = reinterpret_cast<float*>(smem + lay.Dbeta);  // [NW][16]
   float* sDwx = reinterpret_cast<float*>(smem + lay.Dwx);      // [NW][16] (SW)
   float* sInv = reinterpret_cast<float*>(smem + lay.Inv);      // [2][16] 1/|SiLU(k)|, 1/|SiLU(q)| (ACT)
-  T* sKt = reinterpret_cast<T*>(smem + lay.Kt);      // [16][LDD]
-  T* sQt = reinterpret_cast<T*>(smem + lay.Qt);      // [16][LDD]
-  T* sKi = reinterpret_cast<T*>(smem + lay.Ki);      // [16][LDD]
-  T* sSx = reinterpret_cast<T*>(smem + lay.Sx);      // [D][LDD]     S[v][j] (block start)
-  T* sdSx = reinterpret_cast<T*>(smem + lay.dSx);    // [D][LDD]     dS'[v][j]; glue: dF at (j, r)
-  T* sdOT = reinterpret_cast<T*>(smem + lay.dOT);    // [D][LDB]     [value][token] exchange
+  T* sKt = reinterpret_cast<T*>(smem + lay.Kt);      // [16][LDK]    (quad-swizzled)
+  T* sQt = reinterpret_cast<T*>(smem + lay.Qt);      // [16][LDK]
+  T* sKi = reinterpret_cast<T*>(smem + lay.Ki);      // [16][LDK]
+  T* sSx = reinterpret_cast<T*>(smem + lay.Sx);      // [D][LDSX]    S[v][j] (block start)
+  T* sdSx = reinterpret_cast<T*>(smem + lay.dSx);    // [D][LDSX]    dS'[v][j]; glue: dF at (j, r)
+  T* sdOT = reinterpret_cast<T*>(smem + lay.dOT);    // [D][LDX]     [value][token] exchange (quad-swizzled)
   T* suT = reinterpret_cast<T*>(smem + lay.uT);
   T* sdRT = reinterpret_cast<T*>(smem + lay.dRT);
   T* sdzwT = reinterpret_cast<T*>(smem + lay.dzwT);
@@ -186,8 +204,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   // ---- shared parameters ------------------------------------------------------
   for (int x = tid; x < RP * D; x += NT) {
     const int rr = x / D, j = x % D;
-    sVbT[rr * LDD + j] = (T)(rr < R ? a.Vb[j * R + rr] : 0.0f);
-    if constexpr (!SW) sVwT[rr * LDD + j] = (T)(rr < R ? a.Vw[j * R + rr] : 0.0f);
+    sVbT[rr * LDK + (j ^ CARVE_QX(rr))] = (T)(rr < R ? a.Vb[j * R + rr] : 0.0f);
+    if constexpr (!SW) sVwT[rr * LDK + (j ^ CARVE_QX(rr))] = (T)(rr < R ? a.Vw[j * R + rr] : 0.0f);
   }
   // Vb / Vw operand quads (lane (g, c): V[16 w + c][16 ks + 4 g + e]) are read
   // from sVbT / sVwT with the transposing load where needed; the identity
@@ -197,8 +215,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       sGate[x] = -expf(a.A[h * D + x]);
       sGate[D + x] = a.tau_f[h * D + x];
     }
-#define CARVE_FVB(KS_) Qd::ld_tr(sVbT, LDD, 16 * (KS_), 16 * w, g, c)
-#define CARVE_FVW(KS_) Qd::ld_tr(sVwT, LDD, 16 * (KS_), 16 * w, g, c)
+#define CARVE_FVB(KS_) CARVE_LDTR(sVbT, LDK, 16 * (KS_), 16 * w)
+#define CARVE_FVW(KS_) CARVE_LDTR(sVwT, LDK, 16 * (KS_), 16 * w)
 #define CARVE_FI() Qd::cvt(f32x4{4 * g == c ? 1.0f : 0.0f, 4 * g + 1 == c ? 1.0f : 0.0f, \
                                  4 * g + 2 == c ? 1.0f : 0.0f, 4 * g + 3 == c ? 1.0f : 0.0f})
   __syncthreads();
@@ -487,14 +505,19 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         Eq = Qd::cvt(E);
         Eiq = Qd::cvt(Ei);
         sigq = Qd::cvt(sig);
-        const int ro = c * LDD + 16 * w + 4 * g;
+        const int ro = c * LDK + 16 * w + ((4 * g) ^ CARVE_QX(c));
         Qd::st(sKt + ro, Qd::cvt(kt));
         Qd::st(sQt + ro, Qd::cvt(qt));
         Qd::st(sKi + ro, Qd::cvt(ki));
       }
-      for (int jt = 0; jt < NJT; ++jt) {
-        Qd::st(sSx + (16 * w + c) * LDD + 16 * jt + 4 * g, sbq[jt]);
-        Qd::st(sdSx + (16 * w + c) * LDD + 16 * jt + 4 * g, Qd::cvt(dSt[jt]));
+      {
+        // row 16 w + c: its swizzle term depends on c only
+        const int hx = SXH ? hswz128(c) : 0;
+        for (int jt = 0; jt < NJT; ++jt) {
+          const int o = (16 * w + c) * LDSX + ((16 * jt + 4 * g) ^ hx);
+          Qd::st(sSx + o, sbq[jt]);
+          Qd::st(sdSx + o, Qd::cvt(dSt[jt]));
+        }
       }
       __syncthreads();
 
@@ -517,7 +540,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
           for (int i = 0; i < 4; ++i) wgt[i] = sigmoid_f(zw[i]);
         }
         f32x4 XK = zero4();
-        const T* kr = sKt + c * LDD + 4 * g;
+        const T* kr = sKt + c * LDK + ((4 * g) ^ CARVE_QX(c));
         for (int jp = 0; jp < NJT / 2; ++jp)
           XK = Qd::mma32(Qd::ld(kr + 32 * jp), Qd::ld(kr + 32 * jp + 16), sbq[2 * jp], sbq[2 * jp + 1], XK);
         const f32x4 bt = *reinterpret_cast<const f32x4*>(sBeta + 4 * g);
@@ -529,7 +552,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         const f32x4 u = Qd::mma16(Qd::ld(sTm + c * LDB + 4 * g), Qd::cvt(rr), zero4());
         // du = Ki dM^T + P^T dO with dM = dS' diag(gam)
         f32x4 du = zero4();
-        const T* kir = sKi + c * LDD + 4 * g;
+        const T* kir = sKi + c * LDK + ((4 * g) ^ CARVE_QX(c));
         // dS' (already in LDS for the key side) becomes dM in place: both du and
         // the state gradient below use dM only
         for (int jt = 0; jt < NJT; ++jt) dSt[jt] *= *reinterpret_cast<const f32x4*>(sGam + 16 * jt + 4 * g);
@@ -548,7 +571,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         // state gradient at the block start
         for (int jt = 0; jt < NJT; ++jt) {
           CARVE_SEQ();
-          dSt[jt] = Qd::mma32(Qd::ld_tr(sQt, LDD, 0, 16 * jt, g, c), Qd::ld_tr(sKt, LDD, 0, 16 * jt, g, c), dOcq,
+          dSt[jt] = Qd::mma32(CARVE_LDTR(sQt, LDK, 0, 16 * jt), CARVE_LDTR(sKt, LDK, 0, 16 * jt), dOcq,
                               dXq, dSt[jt]);
         }
         // value-side token gradients, stored through the identity (4 values per lane)
@@ -575,7 +598,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         for (int i = 0; i < 4; ++i) pr[i] = row_scan(dR[i] * rm[i]);
         if (c == 15) *reinterpret_cast<f32x4*>(sDbeta + w * 16 + 4 * g) = pr;
         // exchange, [value][token] layout
-        const int xo = (16 * w + c) * LDB + 4 * g;
+        const int xo = (16 * w + c) * LDX + ((4 * g) ^ CARVE_QX(c));
         Qd::st(sdRT + xo, Qd::cvt(dR));
         Qd::st(sdOT + xo, dOcq);
         Qd::st(suT + xo, Qd::cvt(u));
@@ -593,15 +616,19 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         float dgs = 0.0f;   // sum_v dS'[v][j] S[v][j] for j = 16 w + c (partial over this lane's v)
         // one pass over the value axis (32 values per step): every operand tile
         // is read from LDS once
+        // S, dS' rows 32 kp + 4 g + c / 4 (+ 16): the swizzle term is that of
+        // row 4 g + c / 4 for every kp
+        const int sxo = SXH ? (4 * g + (c >> 2)) * LDSX + ((16 * w + 4 * (c & 3)) ^ hswz128(4 * g + (c >> 2))) : 0;
+#define CARVE_LDSX(B_, R0_) ld_sx_tile<SXH, T, LDSX>(B_, R0_, sxo, 16 * w, g, c)
         for (int kp = 0; kp < NJT / 2; ++kp) {
           CARVE_SEQ();
-          const quad s0 = Qd::ld_tr(sSx, LDD, 32 * kp, 16 * w, g, c);
-          const quad s1 = Qd::ld_tr(sSx, LDD, 32 * kp + 16, 16 * w, g, c);
-          const quad a0 = Qd::ld_tr(sdSx, LDD, 32 * kp, 16 * w, g, c);
-          const quad a1 = Qd::ld_tr(sdSx, LDD, 32 * kp + 16, 16 * w, g, c);
-          const quad r0 = Qd::ld_tr(sdRT, LDB, 32 * kp, 0, g, c), r1 = Qd::ld_tr(sdRT, LDB, 32 * kp + 16, 0, g, c);
-          const quad o0 = Qd::ld_tr(sdOT, LDB, 32 * kp, 0, g, c), o1 = Qd::ld_tr(sdOT, LDB, 32 * kp + 16, 0, g, c);
-          const quad u0 = Qd::ld_tr(suT, LDB, 32 * kp, 0, g, c), u1 = Qd::ld_tr(suT, LDB, 32 * kp + 16, 0, g, c);
+          const quad s0 = CARVE_LDSX(sSx, 32 * kp);
+          const quad s1 = CARVE_LDSX(sSx, 32 * kp + 16);
+          const quad a0 = CARVE_LDSX(sdSx, 32 * kp);
+          const quad a1 = CARVE_LDSX(sdSx, 32 * kp + 16);
+          const quad r0 = CARVE_LDTR(sdRT, LDX, 32 * kp, 0), r1 = CARVE_LDTR(sdRT, LDX, 32 * kp + 16, 0);
+          const quad o0 = CARVE_LDTR(sdOT, LDX, 32 * kp, 0), o1 = CARVE_LDTR(sdOT, LDX, 32 * kp + 16, 0);
+          const quad u0 = CARVE_LDTR(suT, LDX, 32 * kp, 0), u1 = CARVE_LDTR(suT, LDX, 32 * kp + 16, 0);
           dKt = Qd::mma32(s0, s1, r0, r1, dKt);
           dQt = Qd::mma32(s0, s1, o0, o1, dQt);
           dKi = Qd::mma32(a0, a1, u0, u1, dKi);
@@ -633,8 +660,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         // beta gradient: A part (dA . A0 summed over s) plus the value partials
         if (w == 0) {
           f32x4 A0 = zero4();
-          const T* kr = sKt + c * LDD + 4 * g;
-          const T* kir = sKi + c * LDD + 4 * g;
+          const T* kr = sKt + c * LDK + ((4 * g) ^ CARVE_QX(c));
+          const T* kir = sKi + c * LDK + ((4 * g) ^ CARVE_QX(c));
           for (int jp = 0; jp < NJT / 2; ++jp)
             A0 = Qd::mma32(Qd::ld(kr + 32 * jp), Qd::ld(kr + 32 * jp + 16), Qd::ld(kir + 32 * jp),
                            Qd::ld(kir + 32 * jp + 16), A0);
@@ -661,9 +688,9 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         }
         const quad bdAT = Qd::cvt(Qd::mma16(Qd::cvt(bdA), CARVE_FI(), zero4()));   // rows s, columns t
         const quad dPT = Qd::cvt(Qd::mma16(Qd::cvt(dP), CARVE_FI(), zero4()));
-        const quad KiT = Qd::ld_tr(sKi, LDD, 0, 16 * w, g, c);
+        const quad KiT = CARVE_LDTR(sKi, LDK, 0, 16 * w);
         dKt = Qd::mma16(KiT, bdAT, dKt);
-        dKi = Qd::mma32(Qd::ld_tr(sKt, LDD, 0, 16 * w, g, c), Qd::ld_tr(sQt, LDD, 0, 16 * w, g, c), Qd::cvt(bdA),
+        dKi = Qd::mma32(CARVE_LDTR(sKt, LDK, 0, 16 * w), CARVE_LDTR(sQt, LDK, 0, 16 * w), Qd::cvt(bdA),
                         Qd::cvt(dP), dKi);
         dQt = Qd::mma16(KiT, dPT, dQt);
         // elementwise: lane (g, c) holds j = 16 w + 4 g + i, t = c
@@ -710,16 +737,16 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         const int rt = x % NRB, side = x / NRB;
         f32x4 acc = zero4();
         if (side == 0) {
-          const T* ar = sVbT + (16 * rt + c) * LDD + 4 * g;
+          const T* ar = sVbT + (16 * rt + c) * LDK + ((4 * g) ^ CARVE_QX(c));
           const T* br = sdzb + c * LDD + 4 * g;
           for (int jp = 0; jp < NJT / 2; ++jp)
             acc = Qd::mma32(Qd::ld(ar + 32 * jp), Qd::ld(ar + 32 * jp + 16), Qd::ld(br + 32 * jp),
                             Qd::ld(br + 32 * jp + 16), acc);
         } else {
-          const T* ar = sVwT + (16 * rt + c) * LDD + 4 * g;
+          const T* ar = sVwT + (16 * rt + c) * LDK + ((4 * g) ^ CARVE_QX(c));
           for (int vp = 0; vp < NJT / 2; ++vp)
-            acc = Qd::mma32(Qd::ld(ar + 32 * vp), Qd::ld(ar + 32 * vp + 16), Qd::ld_tr(sdzwT, LDB, 32 * vp, 0, g, c),
-                            Qd::ld_tr(sdzwT, LDB, 32 * vp + 16, 0, g, c), acc);
+            acc = Qd::mma32(Qd::ld(ar + 32 * vp), Qd::ld(ar + 32 * vp + 16), CARVE_LDTR(sdzwT, LDX, 32 * vp, 0),
+                            CARVE_LDTR(sdzwT, LDX, 32 * vp + 16, 0), acc);
         }
         const int ro = side * RP + 16 * rt + 4 * g;
         const f32x4 tau = Qd::f32(Qd::ld(sTau + c * LDR + ro));
@@ -778,6 +805,9 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   }  // blocks (reverse)
 
 #undef CARVE_BWD_BQ
+#undef CARVE_QX
+#undef CARVE_LDTR
+#undef CARVE_LDSX
 #undef CARVE_BWD_READY
 #undef CARVE_BWD_LOADA
 #undef CARVE_BWD_LOADS

@@ -107,6 +107,19 @@ struct Quad<bf16_t> {
     const short4_ v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(p));
     return __builtin_bit_cast(bf16x4, v);
   }
+  // ld_tr on a quad-swizzled tile (qswz below); r0 a multiple of 16, so the
+  // swizzle term of every row this lane touches is g
+  static __device__ __forceinline__ q ld_tr_sw(const bf16_t* buf, int ld, int r0, int c0, int g, int c) {
+    return ld_tr_at(buf + (r0 + 4 * g + (c >> 2)) * ld + c0 + 4 * ((c & 3) ^ g));
+  }
+  // transposing read with the lane's own address (lane (g, c) names row
+  // r0 + 4 g + c / 4, quad c % 4 of the 16 columns)
+  static __device__ __forceinline__ q ld_tr_at(const bf16_t* p) {
+    typedef short short4_ __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) short4_ lds_s4;
+    const short4_ v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(p));
+    return __builtin_bit_cast(bf16x4, v);
+  }
   static __device__ __forceinline__ void st(bf16_t* p, q v) { *reinterpret_cast<bf16x4*>(p) = v; }
   static __device__ __forceinline__ q cvt(f32x4 x) {
     q o;
@@ -137,6 +150,10 @@ struct Quad<float> {
     q o = {p[0], p[ld], p[2 * ld], p[3 * ld]};
     return o;
   }
+  // f32 tiles are not swizzled (qswz<float> is 0)
+  static __device__ __forceinline__ q ld_tr_sw(const float* buf, int ld, int r0, int c0, int g, int c) {
+    return ld_tr(buf, ld, r0, c0, g, c);
+  }
   static __device__ __forceinline__ void st(float* p, q v) { *reinterpret_cast<f32x4*>(p) = v; }
   static __device__ __forceinline__ q cvt(f32x4 x) { return x; }
   static __device__ __forceinline__ f32x4 f32(q x) { return x; }
@@ -151,6 +168,31 @@ struct Quad<float> {
     return mma16(a1, b1, mma16(a0, b0, c));
   }
 };
+
+// ---- bank-conflict-free bf16 operand tiles -----------------------------------
+// The LDS serves 8-byte lane accesses in groups: reads (row-wise or
+// transposing) 32 lanes at a time against a 256-byte bank window, writes 16
+// lanes at a time against a 128-byte window.  A row-major bf16 tile is read and
+// written in three quad (8-byte) patterns: 16 rows x 2 quads (row-wise read),
+// 8 rows x 4 quads (transposing read) and 16 rows x 1 quad (write of a result
+// tile).  Row padding alone cannot make all three conflict-free.  With a row
+// stride of x quads, x = 4 (mod 8), and quad q of row r stored at quad
+// q ^ ((r >> 2) & 3), all three are: the XOR spreads the rows that the stride
+// maps to one window position.  The term only touches the quad index's two low
+// bits, so offsets along a row stay additive.
+// qswz<T>(r): the element-index XOR of row r (f32 tiles: none).
+template <typename T>
+__device__ __forceinline__ int qswz(int r) {
+  return sizeof(T) == 2 ? ((r >> 2) & 3) << 2 : 0;
+}
+// The same three patterns on unpadded 256-byte bf16 rows (128 elements, 32
+// quads): quad q of row r at quad q ^ hq(r mod 16), hq linear over the bits of
+// r with images 4, 8, 17, 2.  hq mod 16 is a bijection of the 16 rows (writes),
+// and {1, 2, 4, 8, 17} is a basis of the quad index (both reads).
+// hswz128(r): the element-index XOR of row r.
+__device__ __forceinline__ int hswz128(int r) {
+  return (((r & 1) ? 4 : 0) ^ ((r & 2) ? 8 : 0) ^ ((r & 4) ? 17 : 0) ^ ((r & 8) ? 2 : 0)) << 2;
+}
 
 // global 4-element vector of the token dtype <-> f32x4
 __device__ __forceinline__ f32x4 gload4(const bf16_t* p) {

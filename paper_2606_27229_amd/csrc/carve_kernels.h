@@ -246,6 +246,25 @@ struct BwdLds {
 // token tiles the adjoint stages per block
 __host__ __device__ constexpr int bwd_stage_tiles(bool SW) { return SW ? 5 : 6; }
 
+// Whether the adjoint lays its bf16 operand tiles out bank-conflict-free (the
+// quad swizzle qswz).  Not in the gated kernels: their extra live state leaves
+// no registers for it (it raises their spills and costs more than it saves).
+template <typename T, int VAR>
+__host__ __device__ constexpr bool bwd_qswz() { return sizeof(T) == 2 && !(VAR & kVarGated); }
+// Row strides (elements): Kt, Qt, Ki, VbT, VwT (the quad swizzle needs a stride
+// of 4 (mod 8) quads; otherwise a 16-byte pad) ...
+template <typename T, int D, int VAR>
+__host__ __device__ constexpr int bwd_ldk() { return bwd_qswz<T, VAR>() ? D + 16 : D + 16 / (int)sizeof(T); }
+// ... the [value][token] exchange tiles ...
+template <typename T, int VAR>
+__host__ __device__ constexpr int bwd_ldx() { return bwd_qswz<T, VAR>() ? 16 : 16 + 16 / (int)sizeof(T); }
+// ... and S, dS' of the block: unpadded rows with the hswz128 swizzle at
+// bf16 d = 128, padded rows otherwise
+template <typename T, int D, int VAR>
+__host__ __device__ constexpr bool bwd_sx_hswz() { return bwd_qswz<T, VAR>() && D == 128; }
+template <typename T, int D, int VAR>
+__host__ __device__ constexpr int bwd_ldsx() { return bwd_sx_hswz<T, D, VAR>() ? D : D + 16 / (int)sizeof(T); }
+
 template <typename T, int D, int RP, int VAR>
 __host__ __device__ constexpr BwdLds bwd_lds() {
   BwdLds l{};
@@ -257,9 +276,10 @@ __host__ __device__ constexpr BwdLds bwd_lds() {
   constexpr size_t LDD = D + PAD, LDR = RF + PAD, LDB = 16 + PAD;
   constexpr size_t NS = bwd_stage_tiles(SW);
   size_t off = 0;
+  constexpr size_t LDK = bwd_ldk<T, D, VAR>(), LDX = bwd_ldx<T, VAR>(), LDSX = bwd_ldsx<T, D, VAR>();
   l.F = off;     off += lds_round(RF * LDD * e);
-  l.VbT = off;   off += lds_round(RP * LDD * e);
-  l.VwT = off;   off += lds_round((RF - RP) * LDD * e);
+  l.VbT = off;   off += lds_round(RP * LDK * e);
+  l.VwT = off;   off += lds_round((RF - RP) * LDK * e);
   l.Tau = off;   off += lds_round(16 * LDR * e);
   l.Tm = off;    off += lds_round(16 * LDB * e);
   l.P = off;     off += lds_round(16 * LDB * e);
@@ -268,17 +288,17 @@ __host__ __device__ constexpr BwdLds bwd_lds() {
   l.Dbeta = off; off += lds_round(NW * 16 * 4);
   l.Dwx = off;   off += SW ? lds_round(NW * 16 * 4) : 0;
   l.Inv = off;   off += (VAR & kVarAct) ? lds_round(2 * 16 * 4) : 0;
-  l.Kt = off;    off += lds_round(16 * LDD * e);
-  l.Qt = off;    off += lds_round(16 * LDD * e);
-  l.Ki = off;    off += lds_round(16 * LDD * e);
-  l.Sx = off;    off += lds_round(D * LDD * e);
+  l.Kt = off;    off += lds_round(16 * LDK * e);
+  l.Qt = off;    off += lds_round(16 * LDK * e);
+  l.Ki = off;    off += lds_round(16 * LDK * e);
+  l.Sx = off;    off += lds_round(D * LDSX * e);
   constexpr size_t LDF = RF + 4;
-  l.dSx = off;   off += lds_round(D * lds_max(LDD, 2 * LDF) * e);
+  l.dSx = off;   off += lds_round(D * lds_max(LDSX, 2 * LDF) * e);
   l.Stage = off;
-  l.dOT = off;   off += lds_round(D * LDB * e);
-  l.uT = off;    off += lds_round(D * LDB * e);
-  l.dRT = off;   off += lds_round(D * LDB * e);
-  l.dzwT = off;  off += lds_round(D * LDB * e);
+  l.dOT = off;   off += lds_round(D * LDX * e);
+  l.uT = off;    off += lds_round(D * LDX * e);
+  l.dRT = off;   off += lds_round(D * LDX * e);
+  l.dzwT = off;  off += lds_round(D * LDX * e);
   {
     const size_t garea = l.Stage + lds_round(NS * 16 * D * e);     // g, or f then Gate
     l.Gate = garea + lds_round(16 * D * e);
