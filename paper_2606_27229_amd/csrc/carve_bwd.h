@@ -100,15 +100,6 @@ __device__ __forceinline__ int acquire_ready(const int* rdy, const int need) {
 // hoisted above the previous one (bounds the number of live operand registers).
 #define CARVE_SEQ() asm volatile("" ::: "memory")
 
-// Transposing read of the S or dS' tile of a block (rows r0 + 4 g + c / 4,
-// columns c0 + 4 (c % 4)): with the hswz128 layout (SXH) from the lane's
-// precomputed offset sxo (row 4 g + c / 4, its swizzle term), else plain.
-template <bool SXH, typename T, int LDSX>
-__device__ __forceinline__ typename Quad<T>::q ld_sx_tile(const T* buf, int r0, int sxo, int c0, int g, int c) {
-  if constexpr (SXH) return Quad<T>::ld_tr_at(buf + r0 * LDSX + sxo);
-  else return Quad<T>::ld_tr(buf, LDSX, r0, c0, g, c);
-}
-
 // Adjoint of (batch, head) bh.  ready[bh * nch + ch] is raised when chunk ch's
 // record is complete; smem is the workgroup's dynamic LDS (BwdLds layout).
 // GATED: g is formed from its staged raw logit f (Eq. decay_gate); the kernel
@@ -618,7 +609,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         // is read from LDS once
         // S, dS' rows 32 kp + 4 g + c / 4 (+ 16): the swizzle term is that of
         // row 4 g + c / 4 for every kp
-        const int sxo = SXH ? (4 * g + (c >> 2)) * LDSX + ((16 * w + 4 * (c & 3)) ^ hswz128(4 * g + (c >> 2))) : 0;
+        const int sxo = SXH ? sx_lane_offset(16 * w, g, c) : 0;
 #define CARVE_LDSX(B_, R0_) ld_sx_tile<SXH, T, LDSX>(B_, R0_, sxo, 16 * w, g, c)
         for (int kp = 0; kp < NJT / 2; ++kp) {
           CARVE_SEQ();

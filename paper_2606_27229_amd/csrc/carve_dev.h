@@ -193,6 +193,20 @@ __device__ __forceinline__ int qswz(int r) {
 __device__ __forceinline__ int hswz128(int r) {
   return (((r & 1) ? 4 : 0) ^ ((r & 2) ? 8 : 0) ^ ((r & 4) ? 17 : 0) ^ ((r & 8) ? 2 : 0)) << 2;
 }
+// Transposing read (rows r0 + 4 g + c / 4, columns c0 + 4 (c % 4), r0 a
+// multiple of 16) of a tile laid out with hswz128 (SXH: rows of LD = 128
+// elements; sxo = the lane's offset of row 4 g + c / 4 with its swizzle term,
+// computed once), or of a plain padded tile.
+template <bool SXH, typename T, int LD>
+__device__ __forceinline__ typename Quad<T>::q ld_sx_tile(const T* buf, int r0, int sxo, int c0, int g, int c) {
+  if constexpr (SXH) return Quad<T>::ld_tr_at(buf + r0 * LD + sxo);
+  else return Quad<T>::ld_tr(buf, LD, r0, c0, g, c);
+}
+// sxo of ld_sx_tile for the column block c0
+__device__ __forceinline__ int sx_lane_offset(int c0, int g, int c) {
+  const int r = 4 * g + (c >> 2);
+  return r * 128 + ((c0 + 4 * (c & 3)) ^ hswz128(r));
+}
 
 // global 4-element vector of the token dtype <-> f32x4
 __device__ __forceinline__ f32x4 gload4(const bf16_t* p) {
