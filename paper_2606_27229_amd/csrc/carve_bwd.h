@@ -445,14 +445,12 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       // value-side step may overwrite the staging region
       quad kq, qq, lbx, vq, wxq, dOq, ltq[NRB];
       quad vraw;  // ACT: the raw value quad (for SiLU' of dv)
-      quad lfq;   // GATED: f (row t = c, key channels 16 w + 4 g + e)
       f32x4 lg;
       {
         const int by = (16 * w + 4 * g) * (int)sizeof(T);
         const int off = ((((by >> 4) ^ (c & (NC - 1))) << 4) | (by & 15)) / (int)sizeof(T);
         if constexpr (GATED) {
-          lfq = Qd::ld(sFs + c * D + off);
-          const f32x4 fv = Qd::f32(lfq);
+          const f32x4 fv = Qd::f32(Qd::ld(sFs + c * D + off));
           const f32x4 na = *reinterpret_cast<const f32x4*>(sGate + 16 * w + 4 * g);
           const f32x4 tf = *reinterpret_cast<const f32x4*>(sGate + D + 16 * w + 4 * g);
           for (int i = 0; i < 4; ++i) lg[i] = na[i] * softplus_f(fv[i] + tf[i]);
@@ -701,8 +699,10 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         Qd::st(dk + e0, Qd::cvt(dkv));
         if constexpr (GATED) {
           // through Eq. decay_gate: df = dg (-exp(A)) sigmoid(f + tau_f); dA and
-          // dtau collect dg g and df
-          const f32x4 fv = Qd::f32(lfq);
+          // dtau collect dg g and df.  f is read again from its staged tile
+          // (the exchange tiles end before it), not kept in registers
+          const int byf = (16 * w + 4 * g) * (int)sizeof(T);
+          const f32x4 fv = Qd::f32(Qd::ld(sFs + c * D + (((((byf >> 4) ^ (c & (NC - 1))) << 4) | (byf & 15)) / (int)sizeof(T))));
           const f32x4 na = *reinterpret_cast<const f32x4*>(sGate + 16 * w + 4 * g);
           const f32x4 tf = *reinterpret_cast<const f32x4*>(sGate + D + 16 * w + 4 * g);
           f32x4 dfv;

@@ -247,10 +247,13 @@ struct BwdLds {
 __host__ __device__ constexpr int bwd_stage_tiles(bool SW) { return SW ? 5 : 6; }
 
 // Whether the adjoint lays its bf16 operand tiles out bank-conflict-free (the
-// quad swizzle qswz).  Not in the gated kernels: their extra live state leaves
-// no registers for it (it raises their spills and costs more than it saves).
+// quad swizzle qswz).  Not in the gated kernel with the per-channel write
+// gate: its extra live state leaves no registers for the swizzle's address
+// terms (they raise its spills and cost more than the conflicts they remove).
 template <typename T, int VAR>
-__host__ __device__ constexpr bool bwd_qswz() { return sizeof(T) == 2 && !(VAR & kVarGated); }
+__host__ __device__ constexpr bool bwd_qswz() {
+  return sizeof(T) == 2 && (VAR & (kVarGated | kVarScalarW)) != kVarGated;
+}
 // Row strides (elements): Kt, Qt, Ki, VbT, VwT (the quad swizzle needs a stride
 // of 4 (mod 8) quads; otherwise a 16-byte pad) ...
 template <typename T, int D, int VAR>
