@@ -123,6 +123,17 @@ def test_bf16_single_chunk():
     check_bwd(w, make_inputs(w, seed=64, dS_T=True))
 
 
+@pytest.mark.parametrize("R", [16, 20])
+def test_bf16_d128_padded_rank(R):
+    """d = 128 with a gate rank below the 32 fold rows a tile holds (R = 16, and
+    R = 20 with 12 zero rows): the fold, Vb^T / Vw^T operand tiles and the
+    dtau path with padding rows, content projections at 15x the paper's
+    initialisation scale so that the content gates matter."""
+    w = _w(Dk=128, Dv=128, L=64, T=128, R=R, dtype="bf16", mu=3.0, s0=0.2, u_std=0.3)
+    print(f"case bf16 D=128 R={R}", flush=True)
+    check_bwd(w, make_inputs(w, seed=128 + R, dS_T=True))
+
+
 def test_bf16_odd_shape():
     """Odd batch, heads and rank, T of three 16-token chunks at d = 64: every
     (batch, head) offset, the rank padding (R = 7 of 32) and a chunk count
