@@ -361,8 +361,8 @@ def main():
     if act:
         bwd_names.append("carve_act_bwd_kernel")
     kernels_ms = {"carve_chain_fwd_kernel": avg(ev_f, 0)}
-    for i, name in enumerate(bwd_names):
-        kernels_ms[name] = avg(ev_b, i)
+    for i, kname in enumerate(bwd_names):
+        kernels_ms[kname] = avg(ev_b, i)
     fwd_ms = kernels_ms["carve_chain_fwd_kernel"]
     bwd_ms = sum(r[0].elapsed_time(r[NB - 1]) for r in ev_b) / args.steps
     tokens = B * T
