@@ -65,7 +65,7 @@ def test_fp32_ranks(R):
     check_bwd(w, make_inputs(w, seed=R, dS_T=True))
 
 
-@pytest.mark.parametrize("L", [16, 64, 128])
+@pytest.mark.parametrize("L", [16, 32, 64, 128])
 def test_bf16_d128(L):
     w = _w(Dk=128, Dv=128, L=L, T=256, R=32, dtype="bf16", mu=3.0, s0=0.0)
     print(f"case bf16 D=128 L={L}", flush=True)
