@@ -71,7 +71,7 @@ def test_act_fp32_d64():
     check(w, make_inputs(w, seed=5, dS_T=True, act=True))
 
 
-@pytest.mark.parametrize("L", [64, 128])
+@pytest.mark.parametrize("L", [16, 64, 128])
 def test_act_bf16_d128(L):
     w = _w(Dk=128, Dv=128, L=L, T=256, R=32, dtype="bf16", mu=3.0, s0=0.0, u_std=0.02)
     print(f"case act bf16 D=128 L={L}", flush=True)

@@ -87,7 +87,7 @@ def test_sw_fp32_rank_over_32():
     check(w, make_inputs(w, seed=40, dS_T=True, scalar_write=True))
 
 
-@pytest.mark.parametrize("L,gated", [(64, False), (128, True)])
+@pytest.mark.parametrize("L,gated", [(32, False), (64, False), (128, True)])
 def test_sw_bf16_d128(L, gated):
     w = _w(Dk=128, Dv=128, L=L, T=256, R=32, dtype="bf16", mu=3.0, s0=0.0, u_std=0.02)
     print(f"case sw bf16 D=128 L={L} gated={gated}", flush=True)
