@@ -90,14 +90,19 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   constexpr int R2 = fold_rows(RP, VAR);   // rows of the fold
   constexpr int NRT = R2 / 16;
   constexpr int NRB = RP / 16;
-  constexpr int PAD = 16 / sizeof(T);
-  constexpr int LDD = D + PAD, LDR = R2 + PAD, LDW = WB + PAD, LDB = 16 + PAD;
+  // bf16 operand tiles: rows of 16 (mod 32) elements with quad q of row r at
+  // q ^ ((r >> 2) & 3) (qswz; CARVE_QX below), bank-conflict-free for their
+  // row-wise, paired row-wise and transposing reads and their quad writes;
+  // f32 tiles: 16-byte row pad, no swizzle
+  constexpr int LDD = fwd_qstride<T>(D), LDR = fwd_qstride<T>(R2), LDW = fwd_qstride<T>(WB),
+                LDB = fwd_qstride<T>(16);
   constexpr int NTA = NB * (NB - 1) / 2;   // off-diagonal tiles of A
   constexpr int NTP = NB * (NB + 1) / 2;   // tiles of P
   static_assert(NW == NJT && NW >= 2, "one wave per 16-wide tile, at least two waves");
   static_assert(D % 32 == 0, "K32 steps over the key / value axis");
 
   const int tid = threadIdx.x, lane = tid & 63;
+#define CARVE_QX(R_) qswz<T>(R_)
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
   const int g = lane >> 4, c = lane & 15;
   const int H = a.H, Tn = a.T, L = a.L, R = a.R;
@@ -148,7 +153,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     float u = 0.0f;
     if (rr < R) u = a.Ub[rr * D + i];
     else if (!SW && rr >= RP && rr < RP + R) u = a.Uw[(rr - RP) * D + i];
-    sU[rr * LDD + i] = (T)u;
+    sU[rr * LDD + (i ^ CARVE_QX(rr))] = (T)u;
   }
   // Vb / Vw operand quads, lane (g, c): V[16 w + c][16 ks + 4 g + e]
   quad fVb[NRB], fVw[NRB];
@@ -270,7 +275,12 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       if (NVX % NT != 0 && x_ >= NVX) break;                                       \
       u32x4 r_ = (SRC_)[u_];                                                       \
       if constexpr (L2_) r_ = act_chunk<T>(r_, act_row_inv_norm<T, D / VEC>(r_));  \
-      *reinterpret_cast<u32x4*>((DST_) + (x_ / (D / VEC)) * LDD + (x_ % (D / VEC)) * VEC) = r_; \
+      const int row_ = x_ / (D / VEC), q2_ = (x_ % (D / VEC)) * 2;                 \
+      /* the chunk's quads 2m, 2m + 1 go to quads (2m, 2m + 1) ^ h: the pair    \
+         moves by h & 2 and its halves swap when h & 1 (bf16, VEC = 8) */       \
+      const int h_ = CARVE_QX(row_) >> 2;                                          \
+      if (sizeof(T) == 2 && (h_ & 1)) r_ = u32x4{r_[2], r_[3], r_[0], r_[1]};      \
+      *reinterpret_cast<u32x4*>((DST_) + row_ * LDD + (sizeof(T) == 2 ? ((q2_ ^ (h_ & 2)) * 4) : q2_ * 2)) = r_; \
     }                                                                              \
   } while (0)
   CARVE_PREFETCH_Q(0);
@@ -318,7 +328,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     } while (0)
     vm_wait_all();
     if (cstart) {
-      for (int jt = 0; jt < NJT; ++jt) Qd::st(sS + (16 * w + c) * LDD + 16 * jt + 4 * g, Qd::cvt(St[jt]));
+      for (int jt = 0; jt < NJT; ++jt) Qd::st(sS + (16 * w + c) * LDD + 16 * jt + ((4 * g) ^ CARVE_QX(c)), Qd::cvt(St[jt]));
     }
     CARVE_STAGE_ROWS(sQ, cq, ACT);
     if (w == 0 && lane < WB) {
@@ -340,12 +350,12 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       for (int rt = 0; rt < NRT; ++rt) {
         f32x4 acc = zero4();
         for (int vp = 0; vp < D / 32; ++vp) {
-          const quad a0 = Qd::ld_tr(sS, LDD, 32 * vp, 16 * w, g, c);
-          const quad a1 = Qd::ld_tr(sS, LDD, 32 * vp + 16, 16 * w, g, c);
-          const T* ur = sU + (16 * rt + c) * LDD + 32 * vp + 4 * g;
+          const quad a0 = Qd::ld_tr_sw(sS, LDD, 32 * vp, 16 * w, g, c);
+          const quad a1 = Qd::ld_tr_sw(sS, LDD, 32 * vp + 16, 16 * w, g, c);
+          const T* ur = sU + (16 * rt + c) * LDD + 32 * vp + ((4 * g) ^ CARVE_QX(c));
           acc = Qd::mma32(a0, a1, Qd::ld(ur), Qd::ld(ur + 16), acc);
         }
-        Qd::st(sF + (16 * rt + c) * LDD + 16 * w + 4 * g, Qd::cvt(acc));
+        Qd::st(sF + (16 * rt + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c)), Qd::cvt(acc));
       }
       __syncthreads();
     }
@@ -363,12 +373,12 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       const int rt = x % NRT, bb = x / NRT;
       f32x4 acc = zero4();
       for (int jp = 0; jp < D / 32; ++jp) {
-        const T* fr = sF + (16 * rt + c) * LDD + 32 * jp + 4 * g;
-        const T* qr = sQ + (16 * bb + c) * LDD + 32 * jp + 4 * g;
+        const T* fr = sF + (16 * rt + c) * LDD + 32 * jp + ((4 * g) ^ CARVE_QX(c));
+        const T* qr = sQ + (16 * bb + c) * LDD + 32 * jp + ((4 * g) ^ CARVE_QX(c));
         acc = Qd::mma32(Qd::ld(fr), Qd::ld(fr + 16), Qd::ld(qr), Qd::ld(qr + 16), acc);
       }
       for (int e = 0; e < 4; ++e) acc[e] = tanh_f(acc[e]);
-      Qd::st(sTau + (16 * bb + c) * LDR + 16 * rt + 4 * g, Qd::cvt(acc));
+      Qd::st(sTau + (16 * bb + c) * LDR + 16 * rt + ((4 * g) ^ CARVE_QX(c)), Qd::cvt(acc));
     }
     __syncthreads();
 
@@ -381,8 +391,8 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       for (int bb = 0; bb < NB; ++bb) {
         f32x4 z = zero4();
         for (int ks = 0; ks < NRB; ++ks)
-          z = Qd::mma16(fVb[ks], Qd::ld(sTau + (16 * bb + c) * LDR + 16 * ks + 4 * g), z);
-        const f32x4 bxv = Qd::f32(Qd::ld(sBx + (16 * bb + c) * LDD + 16 * w + 4 * g));
+          z = Qd::mma16(fVb[ks], Qd::ld(sTau + (16 * bb + c) * LDR + 16 * ks + ((4 * g) ^ CARVE_QX(c))), z);
+        const f32x4 bxv = Qd::f32(Qd::ld(sBx + (16 * bb + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c))));
         f32x4 gv;
         if constexpr (GATED) {
           const f32x4 fv = Qd::f32(pf[bb]);
@@ -405,9 +415,9 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
         fill[e] = fast_exp(-rho[e]);   // e^{lam_{-1} - rho}, lam_{-1} = 0
       }
       for (int bb = 0; bb < NB; ++bb) {
-        T* kp = sKi + (16 * bb + c) * LDD + 16 * w + 4 * g;
+        T* kp = sKi + (16 * bb + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c));
         const f32x4 kv = Qd::f32(Qd::ld(kp));
-        T* qp = sQ + (16 * bb + c) * LDD + 16 * w + 4 * g;
+        T* qp = sQ + (16 * bb + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c));
         const f32x4 qv = Qd::f32(Qd::ld(qp));
         f32x4 kt, qt, ki;
         for (int e = 0; e < 4; ++e) {
@@ -418,7 +428,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
           ki[e] = kv[e] * Ei;
           fill[e] = row_bcast15(E);
         }
-        Qd::st(sKt + (16 * bb + c) * LDD + 16 * w + 4 * g, Qd::cvt(kt));
+        Qd::st(sKt + (16 * bb + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c)), Qd::cvt(kt));
         Qd::st(qp, Qd::cvt(qt));
         Qd::st(kp, Qd::cvt(ki));
       }
@@ -446,7 +456,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       } else {
         f32x4 z = zero4();
         for (int ks = 0; ks < NRB; ++ks)
-          z = Qd::mma16(Qd::ld(sTau + (16 * bb + c) * LDR + RP + 16 * ks + 4 * g), fVw[ks], z);
+          z = Qd::mma16(Qd::ld(sTau + (16 * bb + c) * LDR + RP + 16 * ks + ((4 * g) ^ CARVE_QX(c))), fVw[ks], z);
         z = Qd::mma16(wxq, fI, z);                     // + wx, moved into this layout
         for (int e = 0; e < 4; ++e) wv[bb][e] = sigmoid_f(z[e]) * vv[e];
       }
@@ -475,8 +485,8 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       typedef Quad<float> Qf;
       for (int i = NW - 1 - w; i < NB; i += NDW) {
         f32x4 acc = zero4(), accT = zero4();
-        const T* kr = sKt + (16 * i + c) * LDD + 4 * g;
-        const T* ir = sKi + (16 * i + c) * LDD + 4 * g;
+        const T* kr = sKt + (16 * i + c) * LDD + ((4 * g) ^ CARVE_QX(c));
+        const T* ir = sKi + (16 * i + c) * LDD + ((4 * g) ^ CARVE_QX(c));
         for (int jp = 0; jp < D / 32; ++jp) {
           const quad k0 = Qd::ld(kr + 32 * jp), k1 = Qd::ld(kr + 32 * jp + 16);
           const quad i0 = Qd::ld(ir + 32 * jp), i1 = Qd::ld(ir + 32 * jp + 16);
@@ -500,7 +510,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
         const f32x4 W2 = Qf::mma16(M2t + I4, W, zero4());        // (I + M^2) W
         const f32x4 Ti = Qf::mma16(mA + I4, W2, zero4());        // (I + M) W2
         // T_ii[t = 4g + e][s = c] at (s, t) of sTmT
-        Qd::st(sTmT + (i * 16 + c) * LDB + 4 * g, Qd::cvt(Ti));
+        Qd::st(sTmT + (i * 16 + c) * LDB + ((4 * g) ^ CARVE_QX(c)), Qd::cvt(Ti));
       }
     }
     if (NOW == NW || w < NOW) {
@@ -514,8 +524,8 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
         const int y = isA ? x : x - NTA;
         const int i = tri_row(y, isA), j = tri_col(y, isA);
         // acc[e] = Ki_{s = 16 j + 4 g + e} . X_{t = 16 i + c}, X = Kt (A) or Qt (P)
-        const T* ar = sKi + (16 * j + ct) * LDD + 4 * gt;
-        const T* br = (isA ? sKt : sQ) + (16 * i + ct) * LDD + 4 * gt;
+        const T* ar = sKi + (16 * j + ct) * LDD + ((4 * gt) ^ CARVE_QX(ct));
+        const T* br = (isA ? sKt : sQ) + (16 * i + ct) * LDD + ((4 * gt) ^ CARVE_QX(ct));
         f32x4 acc = zero4();
         for (int jp = 0; jp < D / 32; ++jp)
           acc = Qd::mma32(Qd::ld(ar + 32 * jp), Qd::ld(ar + 32 * jp + 16), Qd::ld(br + 32 * jp),
@@ -524,10 +534,10 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
         if (isA) {
           const float bt = bcur[16 * i + ct];
           for (int e = 0; e < 4; ++e) val[e] = -bt * acc[e];
-          Qd::st(sA + (16 * i + ct) * LDW + 16 * j + 4 * gt, Qd::cvt(val));
+          Qd::st(sA + (16 * i + ct) * LDW + 16 * j + ((4 * gt) ^ CARVE_QX(ct)), Qd::cvt(val));
         } else {
           for (int e = 0; e < 4; ++e) val[e] = (i > j || 4 * gt + e <= ct) ? acc[e] : 0.0f;
-          Qd::st(sP + (16 * i + ct) * LDW + 16 * j + 4 * gt, Qd::cvt(val));
+          Qd::st(sP + (16 * i + ct) * LDW + 16 * j + ((4 * gt) ^ CARVE_QX(ct)), Qd::cvt(val));
         }
       }
     }
@@ -541,8 +551,8 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       for (int bb = 0; bb < NB; ++bb) {
         f32x4 xk = zero4();
         XQ[bb] = zero4();
-        const T* kr = sKt + (16 * bb + c) * LDD + 4 * g;
-        const T* qr = sQ + (16 * bb + c) * LDD + 4 * g;
+        const T* kr = sKt + (16 * bb + c) * LDD + ((4 * g) ^ CARVE_QX(c));
+        const T* qr = sQ + (16 * bb + c) * LDD + ((4 * g) ^ CARVE_QX(c));
         for (int jp = 0; jp < NJT / 2; ++jp) {
           xk = Qd::mma32(Qd::ld(kr + 32 * jp), Qd::ld(kr + 32 * jp + 16), sb[2 * jp], sb[2 * jp + 1], xk);
           XQ[bb] = Qd::mma32(Qd::ld(qr + 32 * jp), Qd::ld(qr + 32 * jp + 16), sb[2 * jp], sb[2 * jp + 1], XQ[bb]);
@@ -558,20 +568,20 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     quad uq[NB];
     for (int i = 0; i < NB; ++i) {
       f32x4 r = RH[i];
-      for (int j = 0; j < i; ++j) r = Qd::mma16(Qd::ld(sA + (16 * i + c) * LDW + 16 * j + 4 * g), uq[j], r);
-      const f32x4 u = Qd::mma16(Qd::ld_tr(sTmT + i * 16 * LDB, LDB, 0, 0, g, c), Qd::cvt(r), zero4());
+      for (int j = 0; j < i; ++j) r = Qd::mma16(Qd::ld(sA + (16 * i + c) * LDW + 16 * j + ((4 * g) ^ CARVE_QX(c))), uq[j], r);
+      const f32x4 u = Qd::mma16(Qd::ld_tr_sw(sTmT + i * 16 * LDB, LDB, 0, 0, g, c), Qd::cvt(r), zero4());
       uq[i] = Qd::cvt(u);
       f32x4 O = XQ[i];
-      for (int j = 0; j <= i; ++j) O = Qd::mma16(Qd::ld(sP + (16 * i + c) * LDW + 16 * j + 4 * g), uq[j], O);
+      for (int j = 0; j <= i; ++j) O = Qd::mma16(Qd::ld(sP + (16 * i + c) * LDW + 16 * j + ((4 * g) ^ CARVE_QX(c))), uq[j], O);
       oq[i] = Qd::cvt(Qd::mma16(Qd::cvt(O), fI, zero4()));
     }
     for (int jt = 0; jt < NJT; ++jt) {
       const f32x4 er = *reinterpret_cast<const f32x4*>(sRho + 16 * jt + 4 * g);
       f32x4 acc = St[jt] * er;
       for (int kp = 0; kp < NB / 2; ++kp)
-        acc = Qd::mma32(Qd::ld_tr(sKi, LDD, 32 * kp, 16 * jt, g, c), Qd::ld_tr(sKi, LDD, 32 * kp + 16, 16 * jt, g, c),
+        acc = Qd::mma32(Qd::ld_tr_sw(sKi, LDD, 32 * kp, 16 * jt, g, c), Qd::ld_tr_sw(sKi, LDD, 32 * kp + 16, 16 * jt, g, c),
                         uq[2 * kp], uq[2 * kp + 1], acc);
-      if (NB & 1) acc = Qd::mma16(Qd::ld_tr(sKi, LDD, 16 * (NB - 1), 16 * jt, g, c), uq[NB - 1], acc);
+      if (NB & 1) acc = Qd::mma16(Qd::ld_tr_sw(sKi, LDD, 16 * (NB - 1), 16 * jt, g, c), uq[NB - 1], acc);
       St[jt] = acc * er;
     }
     oprev = t0;
@@ -588,6 +598,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
 #undef CARVE_STORE_S
 #undef CARVE_STAGE_VW
 #undef CARVE_STAGE_ROWS
+#undef CARVE_QX
 }
 
 // ---------------------------------------------------------------------------

@@ -145,6 +145,14 @@ struct ChainLds {
   size_t U, X, Kt, Bx, Ki, F, Q, Tau, A, P, TmT, VW, Rho, Beta, Gate, total;
 };
 
+// Row stride (elements) of a forward operand tile with n columns: bf16 tiles
+// take the quad swizzle qswz and need a stride of 16 (mod 32) elements (4 (mod
+// 8) quads); f32 tiles keep a 16-byte pad.
+template <typename T>
+__host__ __device__ constexpr int fwd_qstride(int n) {
+  return sizeof(T) == 2 ? (n % 32 == 16 ? n : n + 16) : n + 16 / (int)sizeof(T);
+}
+
 template <typename T, int D, int WB, int RP, int VAR, bool VW>
 __host__ __device__ constexpr ChainLds chain_lds_v() {
   ChainLds l{};
@@ -152,8 +160,8 @@ __host__ __device__ constexpr ChainLds chain_lds_v() {
   constexpr bool SW = (VAR & kVarScalarW) != 0;
   constexpr size_t RF = fold_rows(RP, VAR);
   constexpr size_t NB = WB / 16;
-  constexpr size_t PAD = 16 / sizeof(T);
-  constexpr size_t LDD = D + PAD, LDR = RF + PAD, LDW = WB + PAD, LDB = 16 + PAD;
+  constexpr size_t LDD = fwd_qstride<T>(D), LDR = fwd_qstride<T>(RF), LDW = fwd_qstride<T>(WB),
+                   LDB = fwd_qstride<T>(16);
   size_t off = 0;
   l.U = off;    off += lds_round(RF * LDD * e);
   l.X = off;    off += lds_round(lds_max(D * LDD * e, 2 * lds_round(WB * LDD * e)));
