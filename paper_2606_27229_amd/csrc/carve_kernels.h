@@ -132,7 +132,8 @@ __host__ __device__ constexpr RecLds rec_lds() {
 
 // LDS layout of the chain forward for one WY block of WB tokens (NB = WB / 16
 // token tiles); SW: the scalar write gate (RP fold rows instead of 2RP).  Rows
-// are padded by 16 bytes.  Region X holds the chunk start
+// of n columns take fwd_qstride(n) elements (bf16: 16 (mod 32), the quad
+// swizzle qswz; f32: a 16-byte pad).  Region X holds the chunk start
 // state while the fold reads it, then the block's raw erase logits (Bx) and the
 // decayed keys Kt; Ki holds the block's raw keys until the gates turn them
 // into Ki in place.
