@@ -300,3 +300,38 @@ def bwd_act(inp, L, dO, dS_T=None, nthreads=None):
     out["dk"] = act_qk_bwd(inp["k"], out["dk"])
     out["dv"] = out["dv"] * silu_grad(inp["v"])
     return out
+
+
+# ---- output RMS normalisation (the step that closes Alg. carve_fwd:
+# y = W_O RMSNorm(reshape(o)); W_O is a plain GEMM and not part of this) ----
+RMSNORM_EPS = 1e-6   # the paper gives no epsilon
+
+
+def rmsnorm(o, weight, eps=RMSNORM_EPS):
+    """RMSNorm of reshape(o): every token's H*Dv values (o [B,T,H,Dv]) divided by
+    their root mean square sqrt(mean(x^2) + eps), times weight [H*Dv]."""
+    o = _f64(o)
+    B, T, H, Dv = o.shape
+    x = o.reshape(B, T, H * Dv)
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    y = x / np.sqrt(ms + eps) * _f64(weight)
+    return y.reshape(B, T, H, Dv)
+
+
+def rmsnorm_bwd(o, weight, dy, eps=RMSNORM_EPS):
+    """Reverse mode of ``rmsnorm`` for the loss <dy, y>, derived from the
+    definition: with r = (mean(x^2) + eps)^(-1/2), n = x r and dn = dy * weight,
+    dr/dx_i = -r^3 x_i / N, so d_o = r dn - x r^3 <dn, x> / N = r (dn - n <dn, n> / N);
+    dweight = sum over the rows of dy * n.  Returns (d_o, dweight)."""
+    o = _f64(o)
+    B, T, H, Dv = o.shape
+    N = H * Dv
+    x = o.reshape(-1, N)
+    g = _f64(dy).reshape(-1, N)
+    w = _f64(weight)
+    r = 1.0 / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)
+    n = x * r
+    dn = g * w
+    dx = r * (dn - n * np.sum(dn * n, axis=-1, keepdims=True) / N)
+    dw = np.sum(g * n, axis=0)
+    return dx.reshape(B, T, H, Dv), dw

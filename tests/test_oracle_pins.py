@@ -722,3 +722,114 @@ def test_act_backward_coordinates_of_q_k_v():
             fd = (_act_loss(xp, 4) - _act_loss(xm, 4)) / (2 * h)
             an = gr[gname].reshape(-1)[idx]
             assert abs(fd - an) <= 1e-6 * max(abs(an), 1e-2), (name, idx, fd, an)
+
+
+# --------------------------------------------------------------------------
+# pin P8 at the paper's head size: central differences of the backward on a
+# T = 128 slice of the fp32 layer workload (d = 64, r = 16, L = 64,
+# S0 ~ N(0, 0.1^2)), directional for every input and at 40 coordinates
+# --------------------------------------------------------------------------
+def _config1_slice():
+    w = WORKLOADS["layer_fp32"].with_(B=1, H=1, T=128)
+    return w, _f64(make_inputs(w, seed=1, dS_T=True))
+
+
+def test_backward_finite_differences_config1_slice_directional():
+    w, inp = _config1_slice()
+    gr = orc.bwd(inp, w.L, inp["dO"], inp["dS_T"])
+    rng = np.random.default_rng(128)
+    h = 1e-6
+    for name, gname in GRADS:
+        dirn = rng.standard_normal(inp[name].shape)
+        xp = dict(inp); xp[name] = inp[name] + h * dirn
+        xm = dict(inp); xm[name] = inp[name] - h * dirn
+        fd = (_loss(xp, w.L) - _loss(xm, w.L)) / (2 * h)
+        an = float(np.sum(gr[gname] * dirn))
+        assert abs(fd - an) <= 1e-6 * abs(an), (name, fd, an)
+
+
+def test_backward_finite_differences_config1_slice_coordinates():
+    w, inp = _config1_slice()
+    gr = orc.bwd(inp, w.L, inp["dO"], inp["dS_T"])
+    rng = np.random.default_rng(64)
+    h = 1e-5
+    # rounding floor of a central difference: a few ulps of the loss over 2h
+    floor = 50 * np.finfo(np.float64).eps * abs(_loss(inp, w.L)) / (2 * h)
+    checked = 0
+    for name, gname in GRADS:
+        flat = inp[name].reshape(-1)
+        for idx in rng.choice(flat.size, size=min(4, flat.size), replace=False):
+            xp = dict(inp); xp[name] = inp[name].copy(); xp[name].reshape(-1)[idx] += h
+            xm = dict(inp); xm[name] = inp[name].copy(); xm[name].reshape(-1)[idx] -= h
+            fd = (_loss(xp, w.L) - _loss(xm, w.L)) / (2 * h)
+            an = gr[gname].reshape(-1)[idx]
+            assert abs(fd - an) <= max(1e-6 * abs(an), floor), (name, idx, fd, an)
+            checked += 1
+    assert checked >= 40
+
+
+# --------------------------------------------------------------------------
+# output RMS normalisation (Alg. carve_fwd: y = W_O RMSNorm(reshape(o)))
+# --------------------------------------------------------------------------
+def test_rmsnorm_closed_form_and_unit_rms():
+    # one token, two heads of one value each: the row (3, 4) has mean square 12.5
+    o = np.array([3.0, 4.0]).reshape(1, 1, 2, 1)
+    y = orc.rmsnorm(o, np.ones(2), eps=0.0)
+    assert np.allclose(y.reshape(-1), [3 / math.sqrt(12.5), 4 / math.sqrt(12.5)], rtol=0, atol=1e-15)
+    # eps enters under the root: (3, 4) with eps = 3.5 divides by sqrt(16) = 4
+    y = orc.rmsnorm(o, np.ones(2), eps=3.5)
+    assert np.array_equal(y.reshape(-1), [0.75, 1.0])
+    # unit weight, eps = 0: every row of H * Dv values has mean square 1
+    rng = np.random.default_rng(0)
+    o = rng.standard_normal((2, 5, 3, 8)) * rng.uniform(0.1, 10, size=(2, 5, 1, 1))
+    y = orc.rmsnorm(o, np.ones(24), eps=0.0)
+    assert np.allclose(np.mean(y.reshape(10, 24) ** 2, axis=-1), 1.0, rtol=0, atol=1e-13)
+
+
+def test_rmsnorm_scale_invariance_and_weight():
+    rng = np.random.default_rng(1)
+    o = rng.standard_normal((1, 4, 2, 16))
+    w = rng.standard_normal(32)
+    y = orc.rmsnorm(o, w, eps=0.0)
+    # positive scaling of a token's row leaves it unchanged (eps = 0); the norm
+    # spans all heads of the token, so scaling one head alone does change it
+    assert _rel(orc.rmsnorm(7.5 * o, w, eps=0.0), y) < 1e-14
+    o2 = o.copy(); o2[:, :, 0] *= 3.0
+    assert _rel(orc.rmsnorm(o2, w, eps=0.0), y) > 1e-2
+    # the weight multiplies column i of the flattened row
+    y1 = orc.rmsnorm(o, np.ones(32), eps=0.0)
+    assert _rel(y, y1 * w.reshape(1, 1, 2, 16)) < 1e-15
+
+
+def test_rmsnorm_backward_finite_differences():
+    rng = np.random.default_rng(2)
+    for eps in (1e-6, 0.3):
+        o = rng.standard_normal((2, 3, 2, 8))
+        w = rng.standard_normal(16)
+        dy = rng.standard_normal(o.shape)
+        do_, dw = orc.rmsnorm_bwd(o, w, dy, eps=eps)
+        loss = lambda o_, w_: float(np.sum(orc.rmsnorm(o_, w_, eps=eps) * dy))
+        h = 1e-6
+        for _ in range(3):
+            d1 = rng.standard_normal(o.shape)
+            fd = (loss(o + h * d1, w) - loss(o - h * d1, w)) / (2 * h)
+            assert abs(fd - np.sum(do_ * d1)) <= 1e-7 * max(abs(fd), 1.0)
+            d2 = rng.standard_normal(w.shape)
+            fd = (loss(o, w + h * d2) - loss(o, w - h * d2)) / (2 * h)
+            assert abs(fd - np.sum(dw * d2)) <= 1e-7 * max(abs(fd), 1.0)
+        for idx in rng.choice(o.size, size=12, replace=False):
+            e = np.zeros(o.size); e[idx] = h
+            e = e.reshape(o.shape)
+            fd = (loss(o + e, w) - loss(o - e, w)) / (2 * h)
+            assert abs(fd - do_.reshape(-1)[idx]) <= 1e-7 * max(abs(fd), 1.0)
+
+
+def test_rmsnorm_gradient_is_orthogonal_to_the_row_without_eps():
+    """With eps = 0 the norm is invariant to scaling a row, so the gradient with
+    respect to each row is orthogonal to that row."""
+    rng = np.random.default_rng(3)
+    o = rng.standard_normal((2, 6, 4, 8))
+    do_, _ = orc.rmsnorm_bwd(o, rng.standard_normal(32), rng.standard_normal(o.shape), eps=0.0)
+    dots = np.sum((do_ * o).reshape(12, 32), axis=-1)
+    norms = np.linalg.norm(do_.reshape(12, 32), axis=-1) * np.linalg.norm(o.reshape(12, 32), axis=-1)
+    assert np.all(np.abs(dots) <= 1e-14 * norms)
