@@ -600,7 +600,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       CARVE_BWD_LOADS(gb > 0 ? gb - 1 : 0);
       f32x4 dqp;
       {
-        const f32x4 kv = Qd::f32(kq), qv = Qd::f32(qq), E = Qd::f32(Eq), Ei = Qd::f32(Eiq), sig = Qd::f32(sigq);
+        const f32x4 E = Qd::f32(Eq), Ei = Qd::f32(Eiq), sig = Qd::f32(sigq);
         f32x4 dKt = zero4(), dQt = zero4(), dKi = zero4(), dA = zero4(), dP = zero4();
         float dgs = 0.0f;   // sum_v dS'[v][j] S[v][j] for j = 16 w + c (partial over this lane's v)
         // one pass over the value axis (32 values per step): every operand tile
@@ -633,11 +633,19 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         const float bc_ = sBeta[c];
         const f32x4 bq = *reinterpret_cast<const f32x4*>(sBeta + 4 * g);
         const f32x4 gmj = *reinterpret_cast<const f32x4*>(sGam + 16 * w + 4 * g);
+        // The factors Kt, Qt, Ki that multiply their gradients in dlam (and Ki in
+        // dgam) are the token-dtype values of the operand tiles, exactly as the
+        // products above consumed them.  The pair terms of A and P (and the u^T Ki
+        // term of the state carry) enter dlam twice with opposite signs and cancel
+        // in the suffix sums; with one factor rounded and the other not, the
+        // rounding residue of those large terms would not cancel (bf16: about 1 %
+        // of dl instead of 0.2 %).
+        const int rok = c * LDK + 16 * w + ((4 * g) ^ CARVE_QX(c));
+        const f32x4 kiM = Qd::f32(Qd::ld(sKi + rok));
         f32x4 bdA, dgg;
         for (int i = 0; i < 4; ++i) {
           // dgam gam = gam (sum_v dS' S + sum_s Ki_s (dS'^T u_s)), reduced over s = the row
-          const float kis = kv[i] * Ei[i];
-          const float ds = row_scan(kis * dKi[i]);
+          const float ds = row_scan(kiM[i] * dKi[i]);
           dgg[i] = gmj[i] * (__shfl(dgs, 4 * g + i) + __shfl(ds, (lane & 48) | 15));
           dKt[i] = -bc_ * dKt[i];
           dKi[i] *= gmj[i];
@@ -684,17 +692,19 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         dQt = Qd::mma16(KiT, dPT, dQt);
         // elementwise: lane (g, c) holds j = 16 w + 4 g + i, t = c
         f32x4 dzb, dgv, dkv;
+        {
+        const f32x4 ktM = Qd::f32(Qd::ld(sKt + rok)), qtM = Qd::f32(Qd::ld(sQt + rok));
         for (int i = 0; i < 4; ++i) {
           const float Ep = row_shr1(E[i], 1.0f);
-          const float kt = kv[i] * Ep, qt = qv[i] * E[i], ki = kv[i] * Ei[i];
-          const float nxt = row_shl1(dKt[i] * kt, 0.0f);
-          float dlam = dQt[i] * qt - dKi[i] * ki + nxt;
+          const float nxt = row_shl1(dKt[i] * ktM[i], 0.0f);
+          float dlam = dQt[i] * qtM[i] - dKi[i] * kiM[i] + nxt;
           if (c == 15) dlam += dgg[i];
           const float dl = row_suffix(dlam);
           dgv[i] = dl;
           dzb[i] = -dl * sig[i];
           dkv[i] = dKt[i] * Ep + dKi[i] * Ei[i];
           dqp[i] = dQt[i] * E[i];
+        }
         }
         Qd::st(dk + e0, Qd::cvt(dkv));
         if constexpr (GATED) {

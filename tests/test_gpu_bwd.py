@@ -85,15 +85,32 @@ def test_layer_fp32_workload():
     check_bwd(w, make_inputs(w, seed=1))
 
 
-def test_bf16_content_dominant():
+# Gradients that are sums over the whole call (the shared parameters) or that
+# carry the content chain back through every chunk (dS0)
+CHAIN_SUMS = ("dUb", "dUw", "dVb", "dVw", "dS0")
+
+
+@pytest.mark.parametrize("seed", [21, 22, 23])
+def test_bf16_content_dominant(seed):
     """Stress case outside the paper's regime: content projections of std 1
     (50x the initialisation scale) make the gate logits O(1) functions of the
-    state, so bf16 rounding of the state and of the gradient operands is
-    amplified through the content chain.  Bar 3e-2 (the 2e-2 bar applies to
-    the paper-shaped workloads above)."""
+    state, so bf16 rounding of the state, of the fold and of the gradient
+    operands is amplified through the content chain.  The token gradients are
+    held to the 2e-2 bar.  The parameter gradients and dS0 sum these
+    amplified errors over the call with cancellation (their measured max-rel
+    is 0.012-0.026 over the three seeds) and are held to 3e-2: this case is
+    outside the bf16 contract, which is stated for the paper-shaped inputs
+    (initialisation scale 0.02, and 0.3 in the content-amplified cases)."""
     w = _w(Dk=128, Dv=128, L=64, T=128, R=32, dtype="bf16", mu=3.0, s0=0.3, u_std=1.0)
-    print("case bf16 content-dominant", flush=True)
-    check_bwd(w, make_inputs(w, seed=21, dS_T=True), tol=3e-2)
+    print(f"case bf16 content-dominant seed={seed}", flush=True)
+    inp = make_inputs(w, seed=seed, dS_T=True)
+    ref = orc.bwd(inp, w.L, inp["dO"], inp["dS_T"])
+    got = run_gpu(w, inp)
+    errs = {key: max_rel(got[key], ref[key]) for key in GRADS}
+    print("max-rel errors:", {key: float("%.3g" % e) for key, e in errs.items()}, flush=True)
+    for key in GRADS:
+        assert np.all(np.isfinite(got[key])), key
+        assert errs[key] <= (3e-2 if key in CHAIN_SUMS else TOL["bf16"]), (key, errs)
 
 
 def test_backward_deterministic():

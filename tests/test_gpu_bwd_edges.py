@@ -1,0 +1,158 @@
+"""Backward parity at the numerical edges of the paper's regime, through the C
+ABI, against the CPU oracle's exact reverse mode.
+
+- Erase-heavy inputs: erase logits bx ~ N(0, 1) instead of N(-mu, 1), about
+  -0.96 of log retention per token (Lambda over a 64-token chunk near -61,
+  near -123 over 128 tokens), with the content projections at 15x the paper's
+  initialisation scale so that the content gates matter; the default layer and
+  the gate-in-kernel variant, d = 128, L = 64 and 128.
+- Every gradient output is overwritten: buffers poisoned with NaN and with 7.0
+  before the call give finite, identical results.
+- Gate ranks above the 32 fold rows of one tile (R = 48, 64: two tiles of fold
+  rows per gate side) at d = 64, forward and backward.
+
+Bar: bf16 inputs with f32 state and accumulation, max-rel <= 2e-2 per tensor.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as orc
+from paper_2606_27229_amd import carve
+from paper_2606_27229_amd.inputs import Workload, make_inputs
+from tests.gpu_util import host, max_rel, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+GRADS = ("dq", "dk", "dv", "dbeta", "dg", "dbx", "dwx", "dUb", "dUw", "dVb", "dVw", "dS0")
+GATED_GRADS = ("dq", "dk", "dv", "dbeta", "df", "dA", "dtau", "dbx", "dwx", "dUb", "dUw", "dVb", "dVw", "dS0")
+
+
+def _w(**kw):
+    base = dict(name="edge", B=1, H=2, T=256, Dk=128, Dv=128, L=64, R=32, dtype="bf16", mu=3.0, s0=0.0,
+                u_std=0.3)
+    base.update(kw)
+    return Workload(**base)
+
+
+def _report(errs, got):
+    for key, val in got.items():
+        assert np.all(np.isfinite(val)), key
+    print("max-rel errors:", {k: float("%.3g" % e) for k, e in errs.items()}, flush=True)
+    bad = {k: e for k, e in errs.items() if not e <= TOL}
+    assert not bad, bad
+
+
+@pytest.mark.parametrize("L", [64, 128])
+def test_bwd_erase_heavy(L):
+    w = _w(L=L)
+    print(f"case erase-heavy bf16 D=128 L={L}", flush=True)
+    inp = make_inputs(w, seed=70 + L, dS_T=True, bx_mean=0.0)
+    x = to_gpu(inp, torch.bfloat16)
+    o, S_T, S_chunks = carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"],
+                                       x["Ub"], x["Uw"], x["Vb"], x["Vw"], x["S0"], L=L)
+    gr = carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
+                         x["Vb"], x["Vw"], S_chunks, x["dO"], x["dS_T"], L=L)
+    torch.cuda.synchronize()
+    rf = orc.fwd_serial(inp, L, want_chunks=True)
+    rb = orc.bwd(inp, L, inp["dO"], inp["dS_T"])
+    got = {"o": host(o), "S_T": host(S_T), "S_chunks": host(S_chunks)}
+    got.update({k: host(gr[k]) for k in GRADS})
+    errs = {k: max_rel(got[k], rf[k]) for k in ("o", "S_T", "S_chunks")}
+    errs.update({k: max_rel(got[k], rb[k]) for k in GRADS})
+    _report(errs, got)
+
+
+@pytest.mark.parametrize("L", [64, 128])
+def test_bwd_erase_heavy_gated(L):
+    w = _w(L=L)
+    print(f"case erase-heavy gated bf16 D=128 L={L}", flush=True)
+    inp = make_inputs(w, seed=90 + L, dS_T=True, bx_mean=0.0, gated=True)
+    x = to_gpu(inp, torch.bfloat16)
+    args = (x["q"], x["k"], x["v"], x["beta"], x["f"], x["A"], x["tau_f"], x["bx"], x["wx"],
+            x["Ub"], x["Uw"], x["Vb"], x["Vw"])
+    o, S_T, S_chunks = carve.chunk_fwd_gated(*args, x["S0"], L=L)
+    gr = carve.chunk_bwd_gated(*args, S_chunks, x["dO"], x["dS_T"], L=L)
+    torch.cuda.synchronize()
+    rf = orc.fwd_gated(inp, L, want_chunks=True)
+    rb = orc.bwd_gated(inp, L, inp["dO"], inp["dS_T"])
+    got = {"o": host(o), "S_T": host(S_T), "S_chunks": host(S_chunks)}
+    got.update({k: host(gr[k]) for k in GATED_GRADS})
+    errs = {k: max_rel(got[k], rf[k]) for k in ("o", "S_T", "S_chunks")}
+    errs.update({k: max_rel(got[k], rb[k]) for k in GATED_GRADS})
+    _report(errs, got)
+
+
+def test_bwd_overwrites_poisoned_outputs():
+    """Every gradient output (token gradients, parameter gradients, dS0) is
+    written in full: results are finite and bitwise equal whether the output
+    buffers held NaN or 7.0 before the call."""
+    w = _w(B=2, T=128, L=64, s0=0.2)
+    print("case bwd poisoned outputs bf16 D=128", flush=True)
+    inp = make_inputs(w, seed=31, dS_T=True)
+    x = to_gpu(inp, torch.bfloat16)
+    o, S_T, S_chunks = carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"],
+                                       x["Ub"], x["Uw"], x["Vb"], x["Vw"], x["S0"], L=w.L)
+    B, T, H, D, R = w.B, w.T, w.H, w.Dk, w.R
+    bf, f32 = torch.bfloat16, torch.float32
+    shapes = {"dq": ((B, T, H, D), bf), "dk": ((B, T, H, D), bf), "dv": ((B, T, H, D), bf),
+              "dbeta": ((B, T, H), bf), "dg": ((B, T, H, D), f32), "dbx": ((B, T, H, D), bf),
+              "dwx": ((B, T, H, D), bf), "dUb": ((R, D), f32), "dUw": ((R, D), f32),
+              "dVb": ((D, R), f32), "dVw": ((D, R), f32), "dS0": ((B, H, D, D), f32)}
+    runs = []
+    for poison in (float("nan"), 7.0):
+        out = {k: torch.full(s, poison, dtype=dt, device="cuda") for k, (s, dt) in shapes.items()}
+        ws = torch.full((carve.workspace_size(carve.make_dims(B, T, H, D, D, R, w.L, bf), True),), 255,
+                        dtype=torch.uint8, device="cuda")
+        gr = carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
+                             x["Vb"], x["Vw"], S_chunks, x["dO"], x["dS_T"], L=w.L, out=out, workspace=ws)
+        torch.cuda.synchronize()
+        runs.append({k: host(v) for k, v in gr.items()})
+    for k in shapes:
+        assert np.all(np.isfinite(runs[0][k])), k
+        assert np.array_equal(runs[0][k], runs[1][k]), k
+    rb = orc.bwd(inp, w.L, inp["dO"], inp["dS_T"])
+    errs = {k: max_rel(runs[0][k], rb[k]) for k in shapes}
+    _report(errs, {})
+
+
+@pytest.mark.parametrize("R", [48, 64])
+def test_fwd_bwd_rank_above_one_tile_d64(R):
+    """R in 33..64 takes the kernels with 64 fold rows per gate side."""
+    w = _w(Dk=64, Dv=64, T=192, R=R, s0=0.2)
+    print(f"case bf16 D=64 R={R}", flush=True)
+    inp = make_inputs(w, seed=R, dS_T=True)
+    x = to_gpu(inp, torch.bfloat16)
+    o, S_T, S_chunks = carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"],
+                                       x["Ub"], x["Uw"], x["Vb"], x["Vw"], x["S0"], L=w.L)
+    gr = carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
+                         x["Vb"], x["Vw"], S_chunks, x["dO"], x["dS_T"], L=w.L)
+    torch.cuda.synchronize()
+    rf = orc.fwd_serial(inp, w.L, want_chunks=True)
+    rb = orc.bwd(inp, w.L, inp["dO"], inp["dS_T"])
+    got = {"o": host(o), "S_T": host(S_T), "S_chunks": host(S_chunks)}
+    got.update({k: host(gr[k]) for k in GRADS})
+    errs = {k: max_rel(got[k], rf[k]) for k in ("o", "S_T", "S_chunks")}
+    errs.update({k: max_rel(got[k], rb[k]) for k in GRADS})
+    _report(errs, got)
+
+
+def test_fwd_rank48_d128():
+    """bf16 d = 128 with R = 48: the forward takes the 64-row fold kernels (the
+    backward at this shape does not fit the LDS and is rejected)."""
+    w = _w(T=128, R=48, s0=0.2)
+    print("case bf16 D=128 R=48 forward", flush=True)
+    inp = make_inputs(w, seed=48)
+    x = to_gpu(inp, torch.bfloat16)
+    o, S_T, S_chunks = carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"],
+                                       x["Ub"], x["Uw"], x["Vb"], x["Vw"], x["S0"], L=w.L)
+    torch.cuda.synchronize()
+    rf = orc.fwd_serial(inp, w.L, want_chunks=True)
+    got = {"o": host(o), "S_T": host(S_T), "S_chunks": host(S_chunks)}
+    errs = {k: max_rel(got[k], rf[k]) for k in got}
+    _report(errs, got)
+    with pytest.raises(carve.CarveError) as err:
+        carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
+                        x["Vb"], x["Vw"], S_chunks, x["dO"], None, L=w.L)
+    assert err.value.status == -3

@@ -45,10 +45,14 @@ def _slice(inp, b, h):
     return out
 
 
-@pytest.mark.parametrize("name,L", CASES)
-def test_full_size_sampled(name, L):
+@pytest.mark.parametrize("name,L,u_std", [c + (None,) for c in CASES] + [("layer_1p3b_T4096", 64, 0.3)])
+def test_full_size_sampled(name, L, u_std):
+    """u_std = 0.3: the content projections at 15x the paper's initialisation
+    scale, so that a broken fold or glue shows at the 2e-2 bar."""
     w = WORKLOADS[name].with_(L=L)
-    print(f"case {name} L={L}: B={w.B} H={w.H} T={w.T}", flush=True)
+    if u_std is not None:
+        w = w.with_(u_std=u_std)
+    print(f"case {name} L={L}: B={w.B} H={w.H} T={w.T} u_std={w.u_std}", flush=True)
     inp = make_inputs(w, seed=100 + L, dS_T=True)
     samples = [(0, 0), (w.B - 1, w.H - 1)]
     keep = np.zeros((w.B, w.H), dtype=bool)
