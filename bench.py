@@ -8,6 +8,8 @@ line with tokens/s, the roofline of the dominant kernel and the CPU oracle
 timed on a bounded sample of the same workload.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--L 64]
+(defaults: 50 timed steps after 10 warm-up steps; the reported step time is
+the median of the steps' HIP-event times)
 """
 from __future__ import annotations
 
@@ -167,14 +169,46 @@ def counter_summary(run_dirs):
         print(json.dumps(rec), flush=True)
 
 
+def host_cpu():
+    """(cores of the host, cores this process may run on, CPU share of its
+    cgroup or None, CPU model) for the CPU baseline's record."""
+    host = os.cpu_count() or 1
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = host
+    share = None
+    try:
+        with open("/sys/fs/cgroup/cpu.max") as f:
+            quota, period = f.read().split()[:2]
+        if quota != "max":
+            share = max(1, int(int(quota) // int(period)))
+    except (OSError, ValueError):
+        pass
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return host, usable, share, model
+
+
 def cpu_baseline(w, L, seed, target_s=12.0, gated=False, sw=False, act=False):
     """Time the CPU oracle (token-serial forward + exact backward, double) on the
-    whole workload batch, repeated until about target_s seconds of CPU work."""
+    whole workload batch, repeated until about target_s seconds of CPU work.
+    One host thread per (batch, head) chain, up to the cores this process may
+    use (its affinity set, and its cgroup's CPU share where one is set)."""
     from oracle import oracle as orc
     from paper_2606_27229_amd.inputs import make_inputs
 
     inp = make_inputs(w, seed=seed, gated=gated, scalar_write=sw, act=act)
-    threads = max(1, min(16, os.cpu_count() or 1, w.B * w.H))
+    host, usable, share, model = host_cpu()
+    avail = min(usable, share) if share else usable
+    threads = max(1, min(avail, w.B * w.H))
     if act:
         fwd, bwd = orc.fwd_act, orc.bwd_act
     elif sw:
@@ -193,17 +227,20 @@ def cpu_baseline(w, L, seed, target_s=12.0, gated=False, sw=False, act=False):
         t_b += t2 - t1
         reps += 1
     tokens = reps * w.B * w.T   # layer tokens (all heads) processed
-    return {"value": tokens / (t_f + t_b), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+    return {"value": tokens / (t_f + t_b), "unit": "tokens/s", "cores": host, "threads": threads,
+            "usable_cores": usable, "cgroup_cpu_share": share, "cpu_model": model, "kind": "oracle",
             "sample": f"{reps} x the whole batch (B={w.B}, H={w.H}, T={w.T}, L={L}): token-serial forward + "
-                      f"exact reverse-mode backward in double on {threads} threads, fwd {t_f:.1f} s, "
-                      f"bwd {t_b:.1f} s"}
+                      f"exact reverse-mode backward in double, one thread per (batch, head) chain on "
+                      f"{threads} threads (host {host} cores, {usable} usable"
+                      + (f", cgroup share {share}" if share else "") + f"; {model}), "
+                      f"fwd {t_f:.1f} s, bwd {t_b:.1f} s"}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--L", type=int, default=64)
     ap.add_argument("--workload", default=None,
                     help="another bf16 workload of the layer to time (e.g. layer_1p3b_T2048, long_seq_T16384); "
@@ -218,6 +255,10 @@ def main():
     ap.add_argument("--scalar-write", action="store_true",
                     help="the scalar write gate: one write logit per token and head, no write-side "
                          "content (carve_chunk_fwd_sw / _bwd_sw; with --gated, the decay from f)")
+    ap.add_argument("--rmsnorm", action="store_true",
+                    help="also run the output RMS normalisation of the layer (carve_rmsnorm_fwd after the "
+                         "forward, carve_rmsnorm_bwd before the backward, whose d_o is the layer's dO) inside "
+                         "every timed step, and report its kernels next to the layer's")
     ap.add_argument("--traffic-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
                     help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of this benchmark and of "
                          "--copy-calibration into the traffic record read by the roofline (no GPU needed)")
@@ -304,7 +345,40 @@ def main():
     dims = carve.make_dims(B, T, H, d, d, R, L, bf)
     ws = torch.empty(max(carve.workspace_size(dims, True), 16), dtype=torch.uint8, device=dev)
 
+    norm = args.rmsnorm
+    if norm:
+        nw = torch.from_numpy((1.0 + 0.1 * np.random.default_rng(5).standard_normal(H * d)).astype(np.float32)).to(dev)
+        norm_y = torch.empty((B, T, H, d), dtype=bf, device=dev)
+        norm_out = {"d_o": torch.empty((B, T, H, d), dtype=bf, device=dev),
+                    "dweight": torch.empty((H * d,), dtype=f32, device=dev)}
+        norm_ws = torch.empty(max(int(carve.load_library().carve_rmsnorm_workspace_size(
+            carve.ctypes.byref(carve.make_dims(B, T, H, d, d, R, L, bf)))), 16), dtype=torch.uint8, device=dev)
+        norm_dy = x["dO"]       # upstream gradient of y; the norm's d_o feeds the layer backward
+        layer_dO = norm_out["d_o"]
+    else:
+        layer_dO = x["dO"]
+    ev_nf = ev_nb = None
+    cur = {"s": 0}
+
     def fwd():
+        _fwd_layer()
+        if norm:
+            if ev_nf is not None:
+                carve.profile_events(ev_nf[cur["s"]])
+            carve.rmsnorm_fwd(fwd_out["o"], nw, out=norm_y)
+
+    def bwd():
+        if norm:
+            if ev_nb is not None:
+                carve.profile_events(ev_nb[cur["s"]])
+            carve.rmsnorm_bwd(fwd_out["o"], nw, norm_dy, out=norm_out, workspace=norm_ws)
+            if ev_b_armed[0] is not None:
+                carve.profile_events(ev_b_armed[0])
+        _bwd_layer()
+
+    ev_b_armed = [None]
+
+    def _fwd_layer():
         if sw:
             carve.chunk_fwd_sw(x["q"], x["k"], x["v"], x["beta"], x["bx"], x["wx"], x["Ub"], x["Vb"], x["S0"],
                                L=L, out=fwd_out, **decay)
@@ -315,17 +389,17 @@ def main():
             carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
                             x["Vb"], x["Vw"], x["S0"], L=L, out=fwd_out, act=act)
 
-    def bwd():
+    def _bwd_layer():
         if sw:
             carve.chunk_bwd_sw(x["q"], x["k"], x["v"], x["beta"], x["bx"], x["wx"], x["Ub"], x["Vb"],
-                               fwd_out["S_chunks"], x["dO"], None, L=L, out=bwd_out, workspace=ws, **decay)
+                               fwd_out["S_chunks"], layer_dO, None, L=L, out=bwd_out, workspace=ws, **decay)
         elif gated:
             carve.chunk_bwd_gated(x["q"], x["k"], x["v"], x["beta"], x["f"], x["A"], x["tau_f"], x["bx"], x["wx"],
-                                  x["Ub"], x["Uw"], x["Vb"], x["Vw"], fwd_out["S_chunks"], x["dO"], None, L=L,
+                                  x["Ub"], x["Uw"], x["Vb"], x["Vw"], fwd_out["S_chunks"], layer_dO, None, L=L,
                                   out=bwd_out, workspace=ws)
         else:
             carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
-                            x["Vb"], x["Vw"], fwd_out["S_chunks"], x["dO"], None, L=L, out=bwd_out,
+                            x["Vb"], x["Vw"], fwd_out["S_chunks"], layer_dO, None, L=L, out=bwd_out,
                             workspace=ws, act=act)
 
     for _ in range(args.warmup):
@@ -338,18 +412,33 @@ def main():
     NF, NB = 2, (8 if (gated or act) else 7)
     ev_f = [[torch.cuda.Event(enable_timing=True) for _ in range(NF)] for _ in range(args.steps)]
     ev_b = [[torch.cuda.Event(enable_timing=True) for _ in range(NB)] for _ in range(args.steps)]
-    for e in [x for row in ev_f + ev_b for x in row]:
+    if norm:
+        ev_nf = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        ev_nb = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    for e in [x for row in ev_f + ev_b + (ev_nf or []) + (ev_nb or []) for x in row]:
         e.record(stream)            # create the device events up front
     torch.cuda.synchronize()
+    # a step: [forward layer, norm forward] then [norm backward, backward layer];
+    # the step's time runs from ev_f[s][0] to ev_b[s][-1] (with the norm, the
+    # layer backward's events are armed inside bwd(), after the norm backward)
     t0 = time.perf_counter()
     for s_ in range(args.steps):
+        cur["s"] = s_
         carve.profile_events(ev_f[s_])
         fwd()
-        carve.profile_events(ev_b[s_])
+        if norm:
+            ev_b_armed[0] = ev_b[s_]
+        else:
+            carve.profile_events(ev_b[s_])
         bwd()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_per_step = wall * 1e3 / args.steps
+    wall_ms_per_step = wall * 1e3 / args.steps
+    # a step's time: from the event before its forward's first launch to the
+    # event after its backward's last launch (the steps run back to back on
+    # one stream); the headline is the median over the timed steps
+    step_ms = sorted(ev_f[s_][0].elapsed_time(ev_b[s_][NB - 1]) for s_ in range(args.steps))
+    ms_per_step = (step_ms[(args.steps - 1) // 2] + step_ms[args.steps // 2]) / 2
 
     def avg(rows, i):
         return sum(r[i].elapsed_time(r[i + 1]) for r in rows) / len(rows)
@@ -363,6 +452,10 @@ def main():
     kernels_ms = {"carve_chain_fwd_kernel": avg(ev_f, 0)}
     for i, kname in enumerate(bwd_names):
         kernels_ms[kname] = avg(ev_b, i)
+    if norm:
+        kernels_ms["carve_rmsnorm_fwd_kernel"] = avg(ev_nf, 0)
+        kernels_ms["carve_rmsnorm_bwd_kernel"] = avg(ev_nb, 0)
+        kernels_ms["carve_rmsnorm_reduce_kernel"] = avg(ev_nb, 1)
     fwd_ms = kernels_ms["carve_chain_fwd_kernel"]
     bwd_ms = sum(r[0].elapsed_time(r[NB - 1]) for r in ev_b) / args.steps
     tokens = B * T
@@ -373,6 +466,14 @@ def main():
     dom_ms = kernels_ms[dominant]
     dom_bytes = alg[dominant]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    dom_flops = cnt["fwd_flops"] if dominant == "carve_chain_fwd_kernel" else cnt["bwd_flops"]
+    dom_mfma_frac = dom_flops / (dom_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS
+    # the roofline that binds the kernel's algorithmic counts (bytes / HBM peak
+    # against flops / MFMA peak); "limiter" says what the measured fractions
+    # show when both are far below 1
+    bound = "hbm" if dom_bytes / (HBM_PEAK_GBS * 1e9) >= dom_flops / (BF16_PEAK_TFLOPS * 1e12) else "mfma"
+    limiter = bound if max(achieved / HBM_PEAK_GBS, dom_mfma_frac) >= 0.5 else \
+        "latency: a dependent chain per (batch, head), far below both rooflines"
     # the counters were taken on the default variant
     traffic = None if (gated or sw or act or name != HEADLINE or L != 64) else load_traffic(dominant)
     layer_tflops = (cnt["fwd_flops"] + cnt["bwd_flops"]) / (ms_per_step * 1e-3) / 1e12
@@ -398,6 +499,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "ms_per_step_wall": wall_ms_per_step,
+        "step_ms_min_max": [step_ms[0], step_ms[-1]],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -407,12 +510,18 @@ def main():
                    "token_dtype": "bf16", "state_dtype": "f32",
                    "decay": "formed in the kernels from f, A, tau_f" if gated else "g input (f32)",
                    "write_gate": "scalar per token and head" if sw else "per value channel, content-aware",
-                   "qkv": "raw projections, activations in the kernels" if act else "activated inputs"},
-        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                   "qkv": "raw projections, activations in the kernels" if act else "activated inputs",
+                   "output_norm": "RMSNorm over the H*Dv values of a token (fwd and bwd in every step)"
+                                  if norm else "none (the layer's o)"},
+        "roofline": {"bound": bound, "kernel": dominant,
+                     "achieved": achieved if bound == "hbm" else dom_mfma_frac * BF16_PEAK_TFLOPS,
+                     "peak": HBM_PEAK_GBS if bound == "hbm" else BF16_PEAK_TFLOPS,
+                     "unit": "GB/s" if bound == "hbm" else "TFLOP/s",
+                     "frac": achieved / HBM_PEAK_GBS if bound == "hbm" else dom_mfma_frac,
                      "traffic": None if traffic is None else traffic / (dom_ms * 1e-3) / 1e9,
                      "traffic_bytes_per_launch": traffic,
-                     "algorithmic_bytes_per_launch": dom_bytes, "avg_launch_ms": dom_ms},
+                     "algorithmic_bytes_per_launch": dom_bytes, "avg_launch_ms": dom_ms,
+                     "mfma_frac": dom_mfma_frac, "limiter": limiter},
         "kernels_ms": kernels_ms,
         "fwd_call_ms": fwd_ms,
         "bwd_call_ms": bwd_ms,
