@@ -84,7 +84,7 @@ enum {
   CARVE_ERR_ALIGN = -4,       /* a pointer is not 16-byte aligned */
   CARVE_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than carve_workspace_size */
   CARVE_ERR_HIP = -6,         /* a HIP runtime call failed */
-  CARVE_ERR_ARG = -7          /* both of two alternative inputs given (g and f) */
+  CARVE_ERR_ARG = -7          /* conflicting or invalid argument values (g and f both given; eps) */
 };
 
 /* Bytes of device workspace the forward (for_backward = 0) or the backward
@@ -217,14 +217,53 @@ int carve_chunk_bwd_act(const carve_dims_t* d, const void* q, const void* k, con
                         float* dUw, float* dVb, float* dVw, float* dS0, void* workspace,
                         size_t workspace_bytes, hipStream_t stream);
 
+/* Output RMS normalisation, the step that closes Alg. carve_fwd:
+ *     y = W_O RMSNorm(reshape(o)),
+ * without W_O (a plain GEMM outside the recurrence).  Alg. megakernel runs it
+ * as one hoisted launch over the assembled o, and Alg. megakernel_bwd mirrors
+ * it with one hoisted launch of its gradient; these entry points are those
+ * launches.  A token's row is reshape(o)[b, t, :], the N = H * Dv values of
+ * all its heads ([B, T, H, Dv] row-major viewed as [B*T, N]):
+ *     y[row, i] = o[row, i] / sqrt(mean_i o[row, i]^2 + eps) * weight[i]
+ * The paper gives no eps; the Python binding passes 1e-6.
+ * Only B, T, H, Dv and dtype of d are read (Dk, R and L are not; T need not be
+ * a multiple of L).  Supported: N a multiple of 8 (bf16) or 4 (f32) with
+ * N <= 4096 (bf16) or 2048 (f32), else CARVE_ERR_UNSUPPORTED; eps finite and
+ * >= 0, else CARVE_ERR_ARG.  A row of zeros with eps = 0 gives NaN.
+ * In:  o [B,T,H,Dv] in the call's dtype (as written by carve_chunk_fwd);
+ *      weight [H*Dv] f32.
+ * Out: y [B,T,H,Dv] in the call's dtype (must not overlap o or weight).
+ * One launch; asynchronous on stream. */
+int carve_rmsnorm_fwd(const carve_dims_t* d, const void* o, const float* weight, float eps, void* y,
+                      hipStream_t stream);
+
+/* Bytes of device workspace carve_rmsnorm_bwd needs for these dims (one f32
+ * partial row of dweight per workgroup of its first launch, at most 1024);
+ * 0 for dims that fail validation. */
+size_t carve_rmsnorm_workspace_size(const carve_dims_t* d);
+
+/* Backward of carve_rmsnorm_fwd for loss <dy, y>:
+ *     r = 1 / sqrt(mean_i o_i^2 + eps),  n = o r,  dn = dy * weight,
+ *     d_o = r (dn - n mean_i(dn_i n_i)),  dweight = sum over rows of dy * n.
+ * In:  o, weight, eps as given to the forward; dy [B,T,H,Dv] in the call's dtype.
+ * Out: d_o [B,T,H,Dv] in the call's dtype; dweight [H*Dv] f32 (overwritten,
+ *      reduced over the rows in a fixed order: reruns are bitwise identical).
+ * workspace: at least carve_rmsnorm_workspace_size(d) bytes, else
+ * CARVE_ERR_WORKSPACE.  Two launches (the rows, then the fixed-order sum of
+ * the workgroups' dweight partials); no output may overlap an input or the
+ * workspace. */
+int carve_rmsnorm_bwd(const carve_dims_t* d, const void* o, const float* weight, float eps, const void* dy,
+                      void* d_o, float* dweight, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Measurement hook (not part of the computation).  Arms the next
- * carve_chunk_fwd / carve_chunk_bwd call made on the calling thread to record
+ * carve_chunk_* or carve_rmsnorm_* call made on the calling thread to record
  * events[0] on its stream before its first kernel launch and events[i] after
  * its i-th launch (the forward makes 1 launch; the backward 6: clear of the
  * chunk ready flags, chunk recompute fused with the adjoint, dVb/dVw
  * partials, d[Ub;Uw] partials, two fixed-order reductions; the gated backward
  * a 7th, the reduction of dA, dtau over the batch; the backward with the
- * input activations a 7th, the activation gradient of dq, dk),
+ * input activations a 7th, the activation gradient of dq, dk; the norm's
+ * forward 1, its backward 2),
  * up to `capacity` events.  `events` are hipEvent_t handles created by the
  * caller (hipEventCreate) and owned by the caller; the handles are copied
  * here (the array may be freed after this call) and the events are only

@@ -18,7 +18,7 @@ LIB = os.path.join(HERE, "libcarve.so")
 # layer variant (decay given / formed in the kernels x full / scalar write
 # gate, and the input activations inside the layer)
 SOURCES = [("carve_abi.hip", "carve_abi", []), ("carve_fwd_chain.hip", "carve_fwd_chain", []),
-           ("carve_bwd.hip", "carve_bwd", [])] + [
+           ("carve_bwd.hip", "carve_bwd", []), ("carve_norm.hip", "carve_norm", [])] + [
     ("carve_variant.hip", f"carve_variant{v}", [f"-DCARVE_VARIANT={v}"]) for v in range(5)]
 
 BUILD = os.path.join(HERE, "_build")

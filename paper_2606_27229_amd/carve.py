@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libcarve.so")
 CARVE_F32, CARVE_BF16 = 0, 1
 SYMBOLS = ("carve_chunk_fwd", "carve_chunk_bwd", "carve_chunk_fwd_gated", "carve_chunk_bwd_gated",
            "carve_chunk_fwd_sw", "carve_chunk_bwd_sw", "carve_chunk_fwd_act", "carve_chunk_bwd_act",
+           "carve_rmsnorm_fwd", "carve_rmsnorm_bwd", "carve_rmsnorm_workspace_size",
            "carve_workspace_size", "carve_status_string", "carve_profile_events")
 
 
@@ -68,6 +69,12 @@ def load_library(path: str = LIB_PATH):
     lib.carve_chunk_fwd_act.restype = ctypes.c_int
     lib.carve_chunk_bwd_act.argtypes = lib.carve_chunk_bwd.argtypes
     lib.carve_chunk_bwd_act.restype = ctypes.c_int
+    lib.carve_rmsnorm_fwd.argtypes = [D, vp, fp, ctypes.c_float, vp, vp]
+    lib.carve_rmsnorm_fwd.restype = ctypes.c_int
+    lib.carve_rmsnorm_bwd.argtypes = [D, vp, fp, ctypes.c_float, vp, vp, fp, vp, sz, vp]
+    lib.carve_rmsnorm_bwd.restype = ctypes.c_int
+    lib.carve_rmsnorm_workspace_size.argtypes = [D]
+    lib.carve_rmsnorm_workspace_size.restype = sz
     lib.carve_profile_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]
     lib.carve_profile_events.restype = ctypes.c_int
     if path == LIB_PATH:
@@ -349,3 +356,52 @@ def chunk_bwd_sw(q, k, v, beta, bx, wx, Ub, Vb, S_chunks, dO, dS_T=None, *, g=No
         ws_ptr, ws_len, _stream(stream))
     _check("carve_chunk_bwd_sw", st)
     return res
+
+
+RMSNORM_EPS = 1e-6
+
+
+def _norm_dims(o):
+    B, T, H, Dv = o.shape
+    # only B, T, H, Dv and dtype are read by the norm entry points
+    return make_dims(B, T, H, Dv, Dv, 1, 1, o.dtype)
+
+
+def rmsnorm_fwd(o, weight, *, eps=RMSNORM_EPS, out=None, stream=None):
+    """Output RMS normalisation of the layer output o [B,T,H,Dv] over each
+    token's H*Dv values (Alg. carve_fwd's last step, without W_O):
+    y = o / sqrt(mean(o^2) + eps) * weight, weight [H*Dv] f32."""
+    lib = load_library()
+    B, T, H, Dv = o.shape
+    dims = _norm_dims(o)
+    y = out if out is not None else torch.empty_like(o)
+    st = lib.carve_rmsnorm_fwd(ctypes.byref(dims), _ptr(o, "o", o.dtype, (B, T, H, Dv)),
+                               _ptr(weight, "weight", torch.float32, (H * Dv,)), float(eps),
+                               _ptr(y, "y", o.dtype, (B, T, H, Dv)), _stream(stream))
+    _check("carve_rmsnorm_fwd", st)
+    return y
+
+
+def rmsnorm_bwd(o, weight, dy, *, eps=RMSNORM_EPS, out=None, workspace=None, stream=None):
+    """Backward of ``rmsnorm_fwd`` for loss <dy, y>: returns (d_o, dweight)."""
+    lib = load_library()
+    B, T, H, Dv = o.shape
+    dims = _norm_dims(o)
+    res = dict(out or {})
+    d_o = res.get("d_o")
+    if d_o is None:
+        d_o = torch.empty_like(o)
+    dw = res.get("dweight")
+    if dw is None:
+        dw = torch.empty((H * Dv,), dtype=torch.float32, device=o.device)
+    ws_bytes = int(lib.carve_rmsnorm_workspace_size(ctypes.byref(dims)))
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=o.device)
+    ws_len = workspace.numel() * workspace.element_size()
+    st = lib.carve_rmsnorm_bwd(ctypes.byref(dims), _ptr(o, "o", o.dtype, (B, T, H, Dv)),
+                               _ptr(weight, "weight", torch.float32, (H * Dv,)), float(eps),
+                               _ptr(dy, "dy", o.dtype, (B, T, H, Dv)), _ptr(d_o, "d_o", o.dtype, (B, T, H, Dv)),
+                               _ptr(dw, "dweight", torch.float32, (H * Dv,)), _ptr(workspace, "workspace"),
+                               ws_len, _stream(stream))
+    _check("carve_rmsnorm_bwd", st)
+    return d_o, dw

@@ -139,7 +139,7 @@ const char* carve_status_string(int status) {
     case CARVE_ERR_ALIGN: return "a pointer is not 16-byte aligned";
     case CARVE_ERR_WORKSPACE: return "workspace missing or too small";
     case CARVE_ERR_HIP: return "HIP runtime error";
-    case CARVE_ERR_ARG: return "conflicting arguments (both or neither of two alternative inputs given)";
+    case CARVE_ERR_ARG: return "conflicting or invalid argument values (both of two alternative inputs given, or eps)";
     default: return "unknown status";
   }
 }
@@ -445,6 +445,86 @@ int carve_chunk_bwd_act(const carve_dims_t* d, const void* q, const void* k, con
   return bwd_impl(d, q, k, v, beta, Decay{g, nullptr, nullptr, nullptr}, bx, wx, Ub, Uw, Vb, Vw, S_chunks, dO,
                   dS_T, dq, dk, dv, dbeta, DecayGrad{dg, nullptr, nullptr, nullptr}, dbx, dwx, dUb, dUw, dVb,
                   dVw, dS0, workspace, workspace_bytes, false, true, stream);
+}
+
+}  // extern "C"
+
+// ---- output RMS normalisation (Alg. carve_fwd output step, hoisted) --------
+
+namespace {
+
+// rows and row length of reshape(o) [B*T, H*Dv]; only B, T, H, Dv and dtype
+// of the dims are read
+int norm_dims(const carve_dims_t* d, long* rows, int* N) {
+  if (!d) return CARVE_ERR_NULL;
+  if (d->B <= 0 || d->T <= 0 || d->H <= 0 || d->Dv <= 0) return CARVE_ERR_SHAPE;
+  if (d->dtype != CARVE_F32 && d->dtype != CARVE_BF16) return CARVE_ERR_UNSUPPORTED;
+  const long long n = (long long)d->H * d->Dv;
+  if (n > (1 << 20) || !rmsnorm_supported(d->dtype, (int)n)) return CARVE_ERR_UNSUPPORTED;
+  const long long r = (long long)d->B * d->T;
+  if (r * n >= (1LL << 62)) return CARVE_ERR_UNSUPPORTED;
+  *rows = (long)r;
+  *N = (int)n;
+  return CARVE_OK;
+}
+
+bool eps_ok(float eps) { return eps >= 0.0f && eps <= 3.0e38f; }   // false for NaN and +Inf
+
+}  // namespace
+
+extern "C" {
+
+size_t carve_rmsnorm_workspace_size(const carve_dims_t* d) {
+  long rows = 0;
+  int N = 0;
+  if (norm_dims(d, &rows, &N) != CARVE_OK) return 0;
+  return align256((size_t)rmsnorm_bwd_groups(rows) * N * sizeof(float));
+}
+
+int carve_rmsnorm_fwd(const carve_dims_t* d, const void* o, const float* weight, float eps, void* y,
+                      hipStream_t stream) {
+  ProfClear pc;
+  long rows = 0;
+  int N = 0;
+  int st = norm_dims(d, &rows, &N);
+  if (st) return st;
+  if (!o || !weight || !y) return CARVE_ERR_NULL;
+  if (!eps_ok(eps)) return CARVE_ERR_ARG;
+  if (!aligned16(o) || !aligned16(weight) || !aligned16(y)) return CARVE_ERR_ALIGN;
+  const size_t es = esize(d->dtype);
+  const Range ins[] = {{o, (size_t)rows * N * es}, {weight, (size_t)N * 4}};
+  const Range outs[] = {{y, (size_t)rows * N * es}};
+  if (any_overlap(outs, 1, ins, 2)) return CARVE_ERR_UNSUPPORTED;
+  prof_mark(stream);
+  st = launch_rmsnorm_fwd(o, weight, y, rows, N, eps, d->dtype, stream);
+  prof_mark(stream);
+  return st;
+}
+
+int carve_rmsnorm_bwd(const carve_dims_t* d, const void* o, const float* weight, float eps, const void* dy,
+                      void* d_o, float* dweight, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  ProfClear pc;
+  long rows = 0;
+  int N = 0;
+  int st = norm_dims(d, &rows, &N);
+  if (st) return st;
+  if (!o || !weight || !dy || !d_o || !dweight) return CARVE_ERR_NULL;
+  if (!eps_ok(eps)) return CARVE_ERR_ARG;
+  const void* ptrs[] = {o, weight, dy, d_o, dweight, workspace};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return CARVE_ERR_ALIGN;
+  const size_t need = carve_rmsnorm_workspace_size(d);
+  if (!workspace || workspace_bytes < need) return CARVE_ERR_WORKSPACE;
+  const size_t es = esize(d->dtype);
+  const size_t nx = (size_t)rows * N * es;
+  const Range ins[] = {{o, nx}, {weight, (size_t)N * 4}, {dy, nx}, {workspace, need}};
+  const Range outs[] = {{d_o, nx}, {dweight, (size_t)N * 4}};
+  if (any_overlap(outs, 2, ins, 4)) return CARVE_ERR_UNSUPPORTED;
+  prof_mark(stream);
+  st = launch_rmsnorm_bwd(o, weight, dy, d_o, reinterpret_cast<float*>(workspace), dweight, rows, N, eps, d->dtype,
+                          stream, prof_mark);
+  prof_mark(stream);
+  return st;
 }
 
 }  // extern "C"

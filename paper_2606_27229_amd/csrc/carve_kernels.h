@@ -358,6 +358,18 @@ int launch_param_reduce(const float* part, int nparts, size_t half, float* dst0,
 int launch_act_bwd(const void* q_raw, const void* k_raw, void* dq, void* dk, size_t rows, int D, int dtype,
                    hipStream_t s);
 
+// Output RMS normalisation over rows of N = H * Dv values (carve_norm.hip).
+// The backward's workgroups (at most kNormBwdGroups) each write one f32
+// partial row of dweight, summed in order by a second launch; mark (if not
+// NULL) is called between the two launches.
+constexpr int kNormBwdGroups = 1024;
+bool rmsnorm_supported(int dtype, int N);
+int rmsnorm_bwd_groups(long rows);
+int launch_rmsnorm_fwd(const void* x, const float* wt, void* y, long rows, int N, float eps, int dtype,
+                       hipStream_t s);
+int launch_rmsnorm_bwd(const void* x, const float* wt, const void* dy, void* dx, float* partial, float* dw, long rows,
+                       int N, float eps, int dtype, hipStream_t s, void (*mark)(hipStream_t));
+
 // floats of one partial-gradient record: d[Ub; Uw] ([R][D] twice) or dVb, dVw ([D][R] twice)
 __host__ __device__ constexpr size_t part_floats(int R, int D) { return (size_t)2 * R * D; }
 

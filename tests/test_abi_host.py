@@ -202,3 +202,24 @@ def test_backward_workspace_holds_the_chunk_records(D, R, L, dt):
     RP = (R + 31) // 32 * 32
     per = 2 * RP * D * e + L * 2 * RP * e + (L // 16) * D * D * e + 2 * RP * D * 4
     assert lib.carve_workspace_size(ctypes.byref(d), 1) >= B * H * (T // L) * per
+
+
+def test_rmsnorm_validation():
+    lib = carve.load_library()
+    fake = ctypes.c_void_p(4096)
+    d = _dims(H=64, Dv=128)            # N = 8192 bf16: too long a row
+    assert lib.carve_rmsnorm_fwd(ctypes.byref(d), fake, fake, 1e-6, fake, None) == -3
+    assert lib.carve_rmsnorm_workspace_size(ctypes.byref(d)) == 0
+    d = _dims(T=100)                   # T need not be a multiple of L for the norm
+    assert lib.carve_rmsnorm_workspace_size(ctypes.byref(d)) > 0
+    assert lib.carve_rmsnorm_fwd(ctypes.byref(d), None, fake, 1e-6, fake, None) == -1
+    assert lib.carve_rmsnorm_fwd(ctypes.byref(d), fake, fake, -1.0, fake, None) == -7
+    assert lib.carve_rmsnorm_fwd(ctypes.byref(d), fake, fake, float("nan"), fake, None) == -7
+    assert lib.carve_rmsnorm_fwd(ctypes.byref(d), ctypes.c_void_p(4098), fake, 1e-6, fake, None) == -4
+    assert lib.carve_rmsnorm_fwd(ctypes.byref(d), fake, fake, 1e-6, fake, None) == -3   # y aliases o
+    ws = lib.carve_rmsnorm_workspace_size(ctypes.byref(d))
+    assert lib.carve_rmsnorm_bwd(ctypes.byref(d), ctypes.c_void_p(1 << 20), ctypes.c_void_p(2 << 20), 1e-6,
+                                 ctypes.c_void_p(3 << 20), ctypes.c_void_p(4 << 20), ctypes.c_void_p(5 << 20),
+                                 ctypes.c_void_p(6 << 20), ws - 1, None) == -5
+    d = _dims(B=0)
+    assert lib.carve_rmsnorm_fwd(ctypes.byref(d), fake, fake, 1e-6, ctypes.c_void_p(8192), None) == -2
