@@ -255,6 +255,21 @@ size_t carve_rmsnorm_workspace_size(const carve_dims_t* d);
 int carve_rmsnorm_bwd(const carve_dims_t* d, const void* o, const float* weight, float eps, const void* dy,
                       void* d_o, float* dweight, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* carve_rmsnorm_bwd without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  It allocates nothing: the dweight
+ * partials go to a static device array of the library, 16 MiB (1024 partial
+ * rows of up to 4096 floats), which every supported shape fits; each GPU the
+ * library runs on holds its own copy until the process ends.  Its device
+ * address is looked up once per device, on the first call made with that
+ * device current (CARVE_ERR_HIP if the lookup fails).  Arguments, outputs and
+ * errors are those of carve_rmsnorm_bwd; the results are bitwise those of
+ * carve_rmsnorm_bwd.  Every call on one GPU shares that GPU's array: calls
+ * that overlap in time on one GPU (different streams, or different threads
+ * without ordering) race on it and must not be made. */
+int carve_rmsnorm_bwd_noalloc(const carve_dims_t* d, const void* o, const float* weight, float eps,
+                              const void* dy, void* d_o, float* dweight, hipStream_t stream);
+
 /* Measurement hook (not part of the computation).  Arms the next
  * carve_chunk_* or carve_rmsnorm_* call made on the calling thread to record
  * events[0] on its stream before its first kernel launch and events[i] after

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libcarve.so")
 CARVE_F32, CARVE_BF16 = 0, 1
 SYMBOLS = ("carve_chunk_fwd", "carve_chunk_bwd", "carve_chunk_fwd_gated", "carve_chunk_bwd_gated",
            "carve_chunk_fwd_sw", "carve_chunk_bwd_sw", "carve_chunk_fwd_act", "carve_chunk_bwd_act",
-           "carve_rmsnorm_fwd", "carve_rmsnorm_bwd", "carve_rmsnorm_workspace_size",
+           "carve_rmsnorm_fwd", "carve_rmsnorm_bwd", "carve_rmsnorm_workspace_size", "carve_rmsnorm_bwd_noalloc",
            "carve_workspace_size", "carve_status_string", "carve_profile_events")
 
 
@@ -73,6 +73,8 @@ def load_library(path: str = LIB_PATH):
     lib.carve_rmsnorm_fwd.restype = ctypes.c_int
     lib.carve_rmsnorm_bwd.argtypes = [D, vp, fp, ctypes.c_float, vp, vp, fp, vp, sz, vp]
     lib.carve_rmsnorm_bwd.restype = ctypes.c_int
+    lib.carve_rmsnorm_bwd_noalloc.argtypes = [D, vp, fp, ctypes.c_float, vp, vp, fp, vp]
+    lib.carve_rmsnorm_bwd_noalloc.restype = ctypes.c_int
     lib.carve_rmsnorm_workspace_size.argtypes = [D]
     lib.carve_rmsnorm_workspace_size.restype = sz
     lib.carve_profile_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]
@@ -405,3 +407,19 @@ def rmsnorm_bwd(o, weight, dy, *, eps=RMSNORM_EPS, out=None, workspace=None, str
                                ws_len, _stream(stream))
     _check("carve_rmsnorm_bwd", st)
     return d_o, dw
+
+
+def rmsnorm_bwd_noalloc(o, weight, dy, d_o, dweight, *, eps=RMSNORM_EPS, stream=None):
+    """``rmsnorm_bwd`` through the entry point that allocates nothing (its
+    scratch is the library's static per-device array): the caller passes the
+    outputs d_o (like o) and dweight ([H*Dv] f32)."""
+    lib = load_library()
+    B, T, H, Dv = o.shape
+    dims = _norm_dims(o)
+    st = lib.carve_rmsnorm_bwd_noalloc(ctypes.byref(dims), _ptr(o, "o", o.dtype, (B, T, H, Dv)),
+                                       _ptr(weight, "weight", torch.float32, (H * Dv,)), float(eps),
+                                       _ptr(dy, "dy", o.dtype, (B, T, H, Dv)),
+                                       _ptr(d_o, "d_o", o.dtype, (B, T, H, Dv)),
+                                       _ptr(dweight, "dweight", torch.float32, (H * Dv,)), _stream(stream))
+    _check("carve_rmsnorm_bwd_noalloc", st)
+    return d_o, dweight

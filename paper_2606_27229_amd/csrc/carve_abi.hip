@@ -501,6 +501,29 @@ int carve_rmsnorm_fwd(const carve_dims_t* d, const void* o, const float* weight,
   return st;
 }
 
+int carve_rmsnorm_bwd_noalloc(const carve_dims_t* d, const void* o, const float* weight, float eps, const void* dy,
+                              void* d_o, float* dweight, hipStream_t stream) {
+  long rows = 0;
+  int N = 0;
+  int st = norm_dims(d, &rows, &N);
+  if (st) {
+    ProfClear pc;
+    return st;
+  }
+  const size_t need = carve_rmsnorm_workspace_size(d);
+  if (need > kNormScratchBytes) {
+    ProfClear pc;
+    return CARVE_ERR_WORKSPACE;
+  }
+  float* ws = nullptr;
+  st = norm_scratch(&ws);
+  if (st) {
+    ProfClear pc;
+    return st;
+  }
+  return carve_rmsnorm_bwd(d, o, weight, eps, dy, d_o, dweight, ws, kNormScratchBytes, stream);
+}
+
 int carve_rmsnorm_bwd(const carve_dims_t* d, const void* o, const float* weight, float eps, const void* dy,
                       void* d_o, float* dweight, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   ProfClear pc;

@@ -363,6 +363,12 @@ int launch_act_bwd(const void* q_raw, const void* k_raw, void* dq, void* dk, siz
 // partial row of dweight, summed in order by a second launch; mark (if not
 // NULL) is called between the two launches.
 constexpr int kNormBwdGroups = 1024;
+// carve_rmsnorm_bwd_noalloc: bytes of the per-device static scratch (every
+// supported row length: kNormBwdGroups partial rows of up to 4096 floats) and
+// the devices it can address
+constexpr size_t kNormScratchBytes = (size_t)kNormBwdGroups * 4096 * sizeof(float);
+constexpr int kMaxNormDevices = 64;
+int norm_scratch(float** ptr);
 bool rmsnorm_supported(int dtype, int N);
 int rmsnorm_bwd_groups(long rows);
 int launch_rmsnorm_fwd(const void* x, const float* wt, void* y, long rows, int N, float eps, int dtype,

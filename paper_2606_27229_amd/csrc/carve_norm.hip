@@ -17,7 +17,16 @@
 // and keeps its share of dweight in registers; the workgroup sums its waves in
 // order into one partial row, and a second kernel sums the partials in order,
 // so reruns are bitwise identical.
+#include <mutex>
+
 #include "carve_kernels.h"
+
+// Scratch of carve_rmsnorm_bwd_noalloc, for callers that cannot allocate: the
+// dweight partial rows of the backward (at most kNormBwdGroups rows of at most
+// 4096 floats).  Each GPU the library runs on holds its own copy until the
+// process ends.  Host code never uses this name as an address: the device
+// address comes from hipGetSymbolAddress, once per device (norm_scratch).
+static __device__ __align__(256) float scratch[carve::kNormScratchBytes / sizeof(float)];
 
 namespace carve {
 
@@ -266,6 +275,27 @@ int launch_rmsnorm_bwd(const void* x, const float* wt, const void* dy, void* dx,
   hipLaunchKernelGGL(carve_rmsnorm_reduce_kernel, dim3((unsigned)((N + 63) / 64)), dim3(64 * kNormReduceGroups), 0, s,
                      partial, nwg, N, dw);
   return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
+}
+
+}  // namespace carve
+
+namespace carve {
+
+// The device address of this device's scratch array (looked up on the first
+// call made with the device current, then cached), or CARVE_ERR_HIP.
+int norm_scratch(float** ptr) {
+  static std::mutex mu;
+  static float* addr[kMaxNormDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxNormDevices) return CARVE_ERR_HIP;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return CARVE_ERR_HIP;
+    addr[dev] = reinterpret_cast<float*>(p);
+  }
+  *ptr = addr[dev];
+  return CARVE_OK;
 }
 
 }  // namespace carve
