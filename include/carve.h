@@ -55,9 +55,10 @@
  *     range (log retention l = g - softplus(z_b) per key channel): the
  *     forward evaluates WY blocks of up to 64 tokens of a chunk with factors
  *     up to e^{|sum of l over the block| / 2}, so that sum must stay above
- *     about -170; the backward evaluates 16-token tiles with factors up to
- *     e^{|sum of l over the tile|}, so any 16 consecutive tokens must sum
- *     above about -80.
+ *     about -170; the backward evaluates the 16-token blocks of each chunk
+ *     relative to the middle of their log-retention range, with factors up
+ *     to e^{|sum of l over the block| / 2}, so each such block must sum above
+ *     about -170.
  */
 #ifndef CARVE_H
 #define CARVE_H

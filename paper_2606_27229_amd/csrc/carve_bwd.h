@@ -23,21 +23,30 @@
 //
 // Adjoint of one 16-token block (wave w owns value tile w and key tile w; the
 // state gradient dS lives in registers as dS^T tiles, rows = key index j,
-// columns = the wave's 16 value rows).  With S the block start state, dS' the
-// gradient of the block end state S' = (S + u^T Ki) diag(gam), and lam, Kt, Qt,
-// Ki, A, P, T, R, u as in the forward:
+// columns = the wave's 16 value rows).  The block is evaluated relative to the
+// per-key-channel reference rho = lam_15 / 2, the middle of its log-retention
+// range: with Sr = S diag(e^{rho}) the block start state as the chunk record
+// holds it, gam = e^{lam_15 - rho} (= e^{rho}), dS' the gradient of the block
+// end state (Sr + u^T Ki) diag(gam), and lam, Kt, Qt, Ki (relative to rho), A,
+// P, T, R, u as in the recompute:
 //   dM   = dS' diag(gam)
 //   du   = Ki dM^T + P^T dO             (du_s = dM Ki_s + sum_t P_ts dO_t)
 //   dR   = T^T du,  dX = -beta dR,  d(w v) = beta dR
-//   dS   = dM + dO^T Qt + dX^T Kt       (state gradient at the block start)
-//   dKt  = dX S + beta dA Ki             dA = -dR u^T (s < t)
-//   dQt  = dO S + dP Ki                  dP = dO u^T  (s <= t)
+//   dS   = (dM + dO^T Qt + dX^T Kt) diag(e^{rho})   (state gradient at the block start)
+//   dKt  = dX Sr + beta dA Ki            dA = -dR u^T (s < t)
+//   dQt  = dO Sr + dP Ki                 dP = dO u^T  (s <= t)
 //   dKi  = diag(gam) dS'^T u + (beta dA)^T Kt + dP^T Qt
 //   dbeta = rowsum(dR (w v - S Kt)) + rowsum(dA A0)    (A0 = Kt Ki^T)
-//   dgam gam = sum_v dS' S'  = gam (diag(dS'^T S) + sum_s Ki_s (dS'^T u_s))
+//   dgam gam = gam (diag(dS'^T Sr) + sum_s Ki_s (dS'^T u_s))
 //   dlam_t = dQt_t Qt_t - dKi_t Ki_t + dKt_{t+1} Kt_{t+1} + [t = 15] dgam gam
 //   dl = suffix sums of dlam;  dg = dl;  dz_b = -dl b
-//   dk = dKt e^{lam_{t-1}} + dKi e^{-lam_t},  dq = dQt e^{lam_t} + dY F
+//   dk = dKt e^{lam_{t-1} - rho} + dKi e^{rho - lam_t},  dq = dQt e^{lam_t - rho} + dY F
+// rho is a constant of the block (the block's result does not depend on it), so
+// the gradients through lam are those above with rho held fixed.  No factor
+// exceeds e^{|lam_15| / 2}.  This kernel takes rho from its own prefix sums; the
+// recompute scaled the record's Sr by its own, equal up to the rounding of the
+// two evaluations of the same sums (a relative difference of order 1e-6 in the
+// factors, far below the token dtype's rounding).
 //   dv = d(wv) w,  dz_w = d(wv) v w (1 - w)
 //   dtau = [dz_b Vb, dz_w Vw],  dY = dtau (1 - tau^2),  dF += dY^T q
 // and at the chunk start the folded read-out closes the chain ("glue"):
@@ -148,7 +157,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   T* sTau = reinterpret_cast<T*>(smem + lay.Tau);    // [16][LDR]    tau of the block
   T* sTm = reinterpret_cast<T*>(smem + lay.Tm);      // [16][LDB]    T of the block
   T* sP = reinterpret_cast<T*>(smem + lay.P);        // [16][LDB]    P of the block
-  float* sGam = reinterpret_cast<float*>(smem + lay.Gam);      // [D]
+  float* sGam = reinterpret_cast<float*>(smem + lay.Gam);      // [D] gam = e^{rho} of the block
   float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);    // [16] beta, then [16] sigmoid(wx) (SW)
   float* sDbeta = reinterpret_cast<float*>(smem + lay.Dbeta);  // [NW][16]
   float* sDwx = reinterpret_cast<float*>(smem + lay.Dwx);      // [NW][16] (SW)
@@ -242,7 +251,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   constexpr int NGC = D / 4;                     // 16-byte chunks per g row
   static_assert(16 * NGC == NT, "one g vector per thread");
   quad ptm, ppm, psbq[NJT];
-  f32x4 pgam, pg;
+  f32x4 pg;
   u32x4 pfv;        // a 16-byte vector of the block's f rows (GATED)
   T pbeta = (T)0.0f, pws = (T)0.0f;   // beta and (SW) the write logit of token tid
   // The prefetch of a block is issued in two parts during the previous block's
@@ -272,7 +281,6 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       ptm = Qd::ld(reinterpret_cast<const T*>(rc_ + cr.Tm) + bc_ * 256 + 4 * tid);            \
       ppm = Qd::ld(reinterpret_cast<const T*>(rc_ + cr.P) + bc_ * 256 + 4 * tid);             \
     }                                                                                         \
-    if (tid < D / 4) pgam = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(rc_ + cr.Gam) + bc_ * D + 4 * tid); \
     if (tid < 16) {                                                                           \
       pbeta = beta[(tb_ + tid) * H];                                                          \
       if constexpr (SW) pws = wx[(tb_ + tid) * H];                                            \
@@ -369,7 +377,6 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       u32x4 ltau[NTV];
       for (int u = 0; u < NTV; ++u) ltau[u] = ptau[u];
       const quad ltm = ptm, lpm = ppm;
-      const f32x4 lgam = pgam;
       const T lbeta = pbeta, lws = pws;
       quad sbq[NJT];   // block start state, wave layout: S[16 w + c][16 jt + 4 g + e]
       for (int jt = 0; jt < NJT; ++jt) sbq[jt] = psbq[jt];
@@ -408,7 +415,6 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         Qd::st(sTm + t * LDB + s4, ltm);
         Qd::st(sP + t * LDB + s4, lpm);
       }
-      if (tid < D / 4) *reinterpret_cast<f32x4*>(sGam + 4 * tid) = lgam;
       if (tid < 16) {
         sBeta[tid] = (float)lbeta;
         if constexpr (SW) sBeta[16 + tid] = sigmoid_f((float)lws);
@@ -479,18 +485,22 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         for (int ks = 0; ks < NRB; ++ks) z = Qd::mma16(CARVE_FVB(ks), ltq[ks], z);
         const f32x4 bxv = Qd::f32(lbx);
         const f32x4 kv = Qd::f32(kq), qv = Qd::f32(qq);
-        f32x4 kt, qt, ki, E, Ei, sig;
+        f32x4 kt, qt, ki, E, Ei, sig, gp;
         for (int i = 0; i < 4; ++i) {
           float sp, sg;
           softplus_sigmoid(z[i] + bxv[i], sp, sg);
           sig[i] = sg;
           const float lam = row_scan(lg[i] - sp);
-          E[i] = fast_exp(lam);
-          Ei[i] = fast_exp(-lam);
-          kt[i] = kv[i] * row_shr1(E[i], 1.0f);
+          const float rho = 0.5f * row_bcast15(lam);
+          E[i] = fast_exp(lam - rho);
+          Ei[i] = fast_exp(rho - lam);
+          // e^{lam_{-1} - rho} = e^{-rho} = Ei of the last token
+          kt[i] = kv[i] * row_shr1(E[i], row_bcast15(Ei[i]));
           qt[i] = qv[i] * E[i];
           ki[i] = kv[i] * Ei[i];
+          gp[i] = row_bcast15(E[i]);   // gam = e^{lam_15 - rho} = e^{rho}
         }
+        if (c == 0) *reinterpret_cast<f32x4*>(sGam + 16 * w + 4 * g) = gp;
         Eq = Qd::cvt(E);
         Eiq = Qd::cvt(Ei);
         sigq = Qd::cvt(sig);
@@ -662,8 +672,11 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
           for (int jp = 0; jp < NJT / 2; ++jp)
             A0 = Qd::mma32(Qd::ld(kr + 32 * jp), Qd::ld(kr + 32 * jp + 16), Qd::ld(kir + 32 * jp),
                            Qd::ld(kir + 32 * jp + 16), A0);
+          // (A0 over the whole tile: its entries above the diagonal are products of
+          // factors that may not exist in f32, so they are selected away, not
+          // multiplied by the zeros of dA there)
           f32x4 db;
-          for (int i = 0; i < 4; ++i) db[i] = row_scan(dA[i] * A0[i]);
+          for (int i = 0; i < 4; ++i) db[i] = row_scan(c < 4 * g + i ? dA[i] * A0[i] : 0.0f);
           if (c == 15) {
             for (int ww = 0; ww < NW; ++ww) {
               const f32x4 pv = *reinterpret_cast<const f32x4*>(sDbeta + ww * 16 + 4 * g);
@@ -695,7 +708,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         {
         const f32x4 ktM = Qd::f32(Qd::ld(sKt + rok)), qtM = Qd::f32(Qd::ld(sQt + rok));
         for (int i = 0; i < 4; ++i) {
-          const float Ep = row_shr1(E[i], 1.0f);
+          const float Ep = row_shr1(E[i], row_bcast15(Ei[i]));
           const float nxt = row_shl1(dKt[i] * ktM[i], 0.0f);
           float dlam = dQt[i] * qtM[i] - dKi[i] * kiM[i] + nxt;
           if (c == 15) dlam += dgg[i];
@@ -754,6 +767,9 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         for (int i = 0; i < 4; ++i) acc[i] *= 1.0f - tau[i] * tau[i];
         Qd::st(sdY + c * LDR + ro, Qd::cvt(acc));
       }
+      // the value-side step took the state gradient with respect to Sr; with
+      // respect to S it carries the factor e^{rho}
+      for (int jt = 0; jt < NJT; ++jt) dSt[jt] *= *reinterpret_cast<const f32x4*>(sGam + 16 * jt + 4 * g);
       __syncthreads();
 
       // BQ of this block runs at the top of the next block (or before the glue)

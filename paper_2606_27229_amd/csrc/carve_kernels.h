@@ -46,13 +46,14 @@ struct FwdArgs {
 //   Tau [L][RF]    token dtype   tanh(q F^T)
 //   Tm  [L/16][16][16]           T = (I + A)^{-1} of every 16-token block
 //   P   [L/16][16][16]           P of every block
-//   Gam [L/16][D]  f32           block retention e^{lam_15}
-//   S   [L/16][D/16][threads][4]  block start states: quad jt of thread tid
-//                                 (S[16 w + c][16 jt + 4 g + e]), contiguous over threads
+//   S   [L/16][D/16][threads][4]  block start states scaled by the block's reference,
+//                                 Sr = S diag(e^{rho}) with rho = lam_15 / 2 per key
+//                                 channel: quad jt of thread tid
+//                                 (Sr[16 w + c][16 jt + 4 g + e]), contiguous over threads
 //   dF  [D][RF]    f32           written by the adjoint: the chunk's gradient of F,
 //                                 stored transposed (dF[r][j] at (j, r))
 struct ChunkRec {
-  size_t F, Tau, Tm, P, Gam, S, dF, total;
+  size_t F, Tau, Tm, P, S, dF, total;
 };
 __host__ __device__ constexpr size_t rec_align(size_t x) { return (x + 255) & ~(size_t)255; }
 __host__ __device__ constexpr ChunkRec chunk_rec(size_t e, int D, int L, int RF) {
@@ -63,7 +64,6 @@ __host__ __device__ constexpr ChunkRec chunk_rec(size_t e, int D, int L, int RF)
   r.Tau = off; off += rec_align((size_t)L * RF * e);
   r.Tm = off;  off += rec_align(nbc * 256 * e);
   r.P = off;   off += rec_align(nbc * 256 * e);
-  r.Gam = off; off += rec_align(nbc * D * 4);
   r.S = off;   off += rec_align(nbc * (size_t)D * D * e);
   r.dF = off;  off += rec_align((size_t)RF * D * 4);
   r.total = off;
@@ -248,8 +248,8 @@ constexpr int kUSplit = 16;
 // Inv (kVarAct) holds the inverse L2 norms of the block's activated keys and
 // queries.
 struct BwdLds {
-  size_t F, VbT, VwT, Tau, Tm, P, Gam, Beta, Dbeta, Dwx, Inv, Kt, Qt, Ki, Sx, dSx, dOT, uT, dRT, dzwT, Stage, Gate,
-      dzb, dY, total;
+  size_t F, VbT, VwT, Tau, Tm, P, Gam, Beta, Dbeta, Dwx, Inv, Kt, Qt, Ki, Sx, dSx, dOT, uT, dRT, dzwT, Stage,
+      Gate, dzb, dY, total;
 };
 
 // token tiles the adjoint stages per block

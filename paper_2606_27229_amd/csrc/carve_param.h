@@ -8,7 +8,8 @@
 namespace carve {
 
 // d[Ub; Uw][r][v] = sum over the chunks of one split of sum_j dF[r][j] S_hat[v][j];
-// wave w owns value tile w (S_hat read in the thread layout of the chunk record).
+// wave w owns value tile w (S_hat read from S_chunks, lane (g, c) holding
+// S_hat[16 w + c][16 jt + 4 g + e]).
 // Per chunk, dF (parked as [j][r] f32) is read once with whole-row 16-byte loads
 // and staged in LDS as a high and a low token-dtype part ([j][r], padded rows);
 // the matrix-core operand dF[r][j] is then read with the transposing LDS load.
@@ -47,10 +48,10 @@ __device__ __forceinline__ void uparam_item(const BwdArgs& a, const int item, ch
   const int c0 = split * per, c1 = c0 + per < nch ? c0 + per : nch;
   for (int ch = c0; ch < c1; ++ch) {
     const char* rc = recb + (size_t)ch * cr.total;
-    const T* sv = reinterpret_cast<const T*>(rc + cr.S) + (size_t)tid * 4;
+    const float* sv = a.S_chunks + ((size_t)bh * nch + ch) * D * D + (size_t)(16 * w + c) * D + 4 * g;
     const float* dFr = reinterpret_cast<const float*>(rc + cr.dF);
     quad sb[NJT];
-    for (int jt = 0; jt < NJT; ++jt) sb[jt] = Qd::ld(sv + (size_t)jt * NT * 4);
+    for (int jt = 0; jt < NJT; ++jt) sb[jt] = Qd::cvt(gload4(sv + 16 * jt));
     for (int u = 0; u < NV / NT; ++u) {
       const int x = tid + u * NT;
       const int j = x / (R2 / 4), r4 = (x % (R2 / 4)) * 4;

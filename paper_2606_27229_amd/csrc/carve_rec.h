@@ -19,14 +19,18 @@
 //   l = g - softplus(z_b) = log(exp(g) (1 - b)), w = sigmoid(z_w)
 // and then, for consecutive 16-token blocks (the WY form of Sec. 6.2 applied
 // block by block; every block of the chunk uses the same F), with lam = prefix
-// sums of l inside the block (lam_{-1} = 0), state S at the block start and u
-// the WY "pseudo values":
-//   Kt_t = k_t e^{lam_{t-1}},  Ki_s = k_s e^{-lam_s},  Qt_t = q_t e^{lam_t}
+// sums of l inside the block (lam_{-1} = 0), the block reference
+// rho = lam_15 / 2 per key channel (the middle of the block's log-retention
+// range), state S at the block start and u the WY "pseudo values":
+//   Kt_t = k_t e^{lam_{t-1} - rho},  Ki_s = k_s e^{rho - lam_s},  Qt_t = q_t e^{lam_t - rho}
+//   S' = S diag(e^{rho})
 //   A_ts = beta_t Kt_t . Ki_s (s < t),  P_ts = Qt_t . Ki_s (s <= t)
-//   T = (I + A)^{-1},  R_t = beta_t (w_t * v_t - S Kt_t),  u = T R
-//   S <- (S + sum_s u_s Ki_s^T) diag(e^{lam_15})
-// which is the recurrence of Eq. carve_state rewritten exactly.  A 16-token
-// block keeps every factor within e^{-(16-token log retention)}.
+//   T = (I + A)^{-1},  R_t = beta_t (w_t * v_t - S' Kt_t),  u = T R
+//   S <- (S' + sum_s u_s Ki_s^T) diag(e^{lam_15 - rho})    (e^{lam_15 - rho} = e^{rho})
+// which is the recurrence of Eq. carve_state rewritten exactly (every pair of
+// factors multiplies to e^{lam_a - lam_b} with a >= b).  No factor exceeds
+// e^{|lam_15| / 2}.  The record keeps, per block, T, P and the scaled start
+// state S' (the adjoint evaluates the block with the same reference).
 //
 // With the scalar write gate (kVarScalarW) F = Ub S_hat has R rows and
 // w_t = sigmoid(wx_t) is one scalar per token and head, staged with beta.
@@ -35,8 +39,8 @@
 // through LDS (each wave holds 16 of its channels); v is SiLU(raw).
 //
 // Precondition (not checked): within any 16-token block the log retention
-// summed over the block stays above about -80 per key channel, so that
-// e^{-(block log retention)} is finite in f32.
+// summed over the block stays above about -170 per key channel, so that
+// e^{|block log retention| / 2} is finite in f32 and bf16.
 #pragma once
 #include "carve_kernels.h"
 
@@ -87,7 +91,7 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
   T* sKt = reinterpret_cast<T*>(smem + lay.Kt);    // [LW][LDD]
   T* sQt = reinterpret_cast<T*>(smem + lay.Qt);    // [LW][LDD]
   T* sKi = reinterpret_cast<T*>(smem + lay.Ki);    // [LW][LDD]
-  float* sGam = reinterpret_cast<float*>(smem + lay.Gam);  // [NB][D]     e^{lam_15}
+  float* sGam = reinterpret_cast<float*>(smem + lay.Gam);  // [NB][D]     e^{rho} = e^{lam_15 / 2}
   float* sAT = reinterpret_cast<float*>(smem + lay.AT);    // [NB][16][20] A^T per block
   T* sTm = reinterpret_cast<T*>(smem + lay.Tm);            // [NB][16][LDB] T per block
   float* sGate = reinterpret_cast<float*>(smem + lay.Gate);  // [2][D] -exp(A), tau_f (GATED)
@@ -273,25 +277,24 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
         gv = pg[bb];
       }
       const f32x4 qv = Qd::f32(Qd::ld(sQ + (16 * bb + c) * LDD + 16 * w + 4 * g));
-      f32x4 kt, qt, ki, gam;
+      f32x4 kt, qt, ki, erho;
       for (int i = 0; i < 4; ++i) {
         const float ell = gv[i] - softplus_f(z[i] + bxv[i]);
         const float lam = row_scan(ell);
-        const float E = fast_exp(lam);
-        const float Ep = row_shr1(E, 1.0f);
-        kt[i] = kv[i] * Ep;
+        const float rho = 0.5f * row_bcast15(lam);
+        const float E = fast_exp(lam - rho);
+        const float Ei = fast_exp(rho - lam);
+        // e^{lam_{-1} - rho} = e^{-rho} = Ei of the last token
+        kt[i] = kv[i] * row_shr1(E, row_bcast15(Ei));
         qt[i] = qv[i] * E;
-        ki[i] = kv[i] * fast_exp(-lam);
-        gam[i] = E;
+        ki[i] = kv[i] * Ei;
+        erho[i] = row_bcast15(E);   // e^{lam_15 - rho} = e^{rho}
       }
       const int ro = (16 * bb + c) * LDD + 16 * w + 4 * g;
       Qd::st(sKt + ro, Qd::cvt(kt));
       Qd::st(sQt + ro, Qd::cvt(qt));
       Qd::st(sKi + ro, Qd::cvt(ki));
-      if (c == 15) {
-        *reinterpret_cast<f32x4*>(sGam + bb * D + 16 * w + 4 * g) = gam;
-        *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(rec + cr.Gam) + (m * NB + bb) * D + 16 * w + 4 * g) = gam;
-      }
+      if (c == 15) *reinterpret_cast<f32x4*>(sGam + bb * D + 16 * w + 4 * g) = erho;
     }
     // value side, value tile w: rows t = 16 bb + 4 g + i, column v = 16 w + c
     f32x4 wv[NB];
@@ -337,8 +340,10 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
     __syncthreads();
 
     // ---- P5: T = (I + A)^{-1} per block; first block's state products ------------
+    // sb: S' = S diag(e^{rho}) of the block in the token dtype, the prediction's
+    // operand and the record's block start state
     quad sb[NJT];
-    for (int jt = 0; jt < NJT; ++jt) sb[jt] = Qd::cvt(St[jt]);
+    for (int jt = 0; jt < NJT; ++jt) sb[jt] = Qd::cvt(St[jt] * *reinterpret_cast<const f32x4*>(sGam + 16 * jt + 4 * g));
     f32x4 XK = zero4();
 #define CARVE_REC_XK(BB_)                                                                \
   do {                                                                                   \
@@ -390,10 +395,11 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
       const f32x4 u = Qd::mma16(Qd::ld(sTm + (bb * 16 + c) * LDB + 4 * g), Qd::cvt(rr), zero4());
       const quad uq = Qd::cvt(u);
       for (int jt = 0; jt < NJT; ++jt) {
-        const f32x4 acc = Qd::mma16(Qd::ld_tr(sKi, LDD, 16 * bb, 16 * jt, g, c), uq, St[jt]);
-        const f32x4 gm = *reinterpret_cast<const f32x4*>(sGam + bb * D + 16 * jt + 4 * g);
-        for (int i = 0; i < 4; ++i) St[jt][i] = acc[i] * gm[i];
-        sb[jt] = Qd::cvt(St[jt]);
+        // S <- (S' + u^T Ki) diag(e^{rho})
+        const f32x4 er = *reinterpret_cast<const f32x4*>(sGam + bb * D + 16 * jt + 4 * g);
+        const f32x4 acc = Qd::mma16(Qd::ld_tr(sKi, LDD, 16 * bb, 16 * jt, g, c), uq, St[jt] * er);
+        for (int i = 0; i < 4; ++i) St[jt][i] = acc[i] * er[i];
+        if (bb + 1 < NB) sb[jt] = Qd::cvt(St[jt] * *reinterpret_cast<const f32x4*>(sGam + (bb + 1) * D + 16 * jt + 4 * g));
       }
     }
 #undef CARVE_REC_XK

@@ -19,7 +19,7 @@ import torch
 
 from oracle import oracle as orc
 from paper_2606_27229_amd import carve
-from paper_2606_27229_amd.inputs import Workload, make_inputs
+from paper_2606_27229_amd.inputs import Workload, make_inputs, round_bf16
 from tests.gpu_util import host, max_rel, to_gpu
 
 pytestmark = pytest.mark.gpu
@@ -156,3 +156,35 @@ def test_fwd_rank48_d128():
         carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
                         x["Vb"], x["Vw"], S_chunks, x["dO"], None, L=w.L)
     assert err.value.status == -3
+
+
+def _hard_erase(inp, w, seed, nch=16):
+    """Erase logits near +8 on nch of the key channels (about -8 of log retention
+    per token there: -128 over 16 tokens, -512 over 64), the rest unchanged."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    chans = rng.choice(w.Dk, size=nch, replace=False)
+    out = dict(inp)
+    bx = np.array(inp["bx"], dtype=np.float32, copy=True)
+    bx[..., chans] = (8.0 + 0.5 * rng.standard_normal(bx[..., chans].shape)).astype(np.float32)
+    out["bx"] = round_bf16(bx) if w.dtype == "bf16" else bx
+    return out
+
+
+@pytest.mark.parametrize("L", [64, 128])
+def test_bwd_hard_erase_channels(L):
+    """The backward on inputs whose 16-token blocks lose about 128 of log
+    retention on some key channels.  The chunk-start states come from the
+    oracle, so this checks the recompute and the adjoint alone."""
+    w = _w(L=L, s0=0.2)
+    print(f"case hard-erase backward bf16 D=128 L={L}", flush=True)
+    inp = _hard_erase(make_inputs(w, seed=300 + L, dS_T=True), w, seed=L)
+    rf = orc.fwd_serial(inp, L, want_chunks=True)
+    x = to_gpu(inp, torch.bfloat16)
+    S_chunks = torch.from_numpy(np.ascontiguousarray(rf["S_chunks"], dtype=np.float32)).cuda()
+    gr = carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
+                         x["Vb"], x["Vw"], S_chunks, x["dO"], x["dS_T"], L=L)
+    torch.cuda.synchronize()
+    rb = orc.bwd(inp, L, inp["dO"], inp["dS_T"])
+    got = {k: host(gr[k]) for k in GRADS}
+    errs = {k: max_rel(got[k], rb[k]) for k in GRADS}
+    _report(errs, got)
