@@ -53,12 +53,15 @@
  *   - Every pointer must be 16-byte aligned (CARVE_ERR_ALIGN).
  *   - Inputs are assumed finite with g <= 0; NaN/Inf propagate.  Numerical
  *     range (log retention l = g - softplus(z_b) per key channel): the
- *     forward evaluates WY blocks of up to 64 tokens of a chunk with factors
- *     up to e^{|sum of l over the block| / 2}, so that sum must stay above
- *     about -170; the backward evaluates the 16-token blocks of each chunk
- *     relative to the middle of their log-retention range, with factors up
- *     to e^{|sum of l over the block| / 2}, so each such block must sum above
- *     about -170.
+ *     forward evaluates WY blocks of up to 64 tokens; a key channel whose
+ *     sum of l over a block stays above -160 is taken relative to the middle
+ *     of that block's range, any other channel relative to the middle of
+ *     each 16-token tile's range, with the products across tiles formed from
+ *     operands no larger than the raw token values.  The sum of l over every
+ *     16-token tile must stay above about -150 (-170 where a block is a
+ *     single tile).  The backward evaluates 16-token blocks relative to the
+ *     middle of their range, with factors up to e^{|sum of l over the block|
+ *     / 2}, so each such block must sum above about -170.
  */
 #ifndef CARVE_H
 #define CARVE_H

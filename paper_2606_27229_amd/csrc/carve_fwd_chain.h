@@ -10,17 +10,29 @@
 //   z_b = bx + tau_b Vb^T,  z_w = wx + tau_w Vw^T            (Eq. erase_gate)
 //   l = g - softplus(z_b) = log(exp(g) (1 - sigmoid(z_b))),   w = sigmoid(z_w)
 // Inside a block, with lam the prefix sums of l from the block start (lam_{-1}
-// = 0), S the block start state and the WY form of Sec. WY-form intra-chunk
-// solve re-derived from the recurrence of Eq. carve_state, every exponential
-// is taken relative to the per-key-channel reference rho = lam_end / 2 (the
-// middle of the block's log-retention range), so no factor exceeds
-// e^{|lam_end| / 2}:
-//   Kt_t = k_t e^{lam_{t-1} - rho},  Qt_t = q_t e^{lam_t - rho},  Ki_s = k_s e^{rho - lam_s}
-//   A_ts = beta_t Kt_t . Ki_s (s < t),  P_ts = Qt_t . Ki_s (s <= t)
-//   S' = S diag(e^{rho})
-//   u = (I + A)^{-1} beta (w * v - Kt S'^T)                  (corrected values)
-//   o = Qt S'^T + P u
-//   S <- (S' + u^T Ki) diag(e^{rho})          (= S diag(e^{lam_end}) + sum_s u_s k_s^T e^{lam_end - lam_s})
+// = 0), c_i = lam at the end of 16-token tile i (c_{-1} = 0), S the block start
+// state and the WY form of Sec. WY-form intra-chunk solve re-derived from the
+// recurrence of Eq. carve_state, the exponentials of a token in tile i are
+// taken relative to a per-key-channel reference m_i:
+//   Kt_t = k_t e^{lam_{t-1} - m_i},  Qt_t = q_t e^{lam_t - m_i},  Ki_t = k_t e^{m_i - lam_t}
+//   A_ts = beta_t Kt_t . Ki_s e^{m_i - m_j},  P_ts = Qt_t . Ki_s e^{m_i - m_j}   (s in tile j)
+//   u = (I + A)^{-1} beta (w * v - Kt diag(e^{m_i}) S^T)          (corrected values)
+//   o = Qt diag(e^{m_i}) S^T + P u
+//   S <- S diag(e^{lam_end}) + sum_s u_s (Ki_s e^{lam_end - m_j})^T
+// (= S diag(e^{lam_end}) + sum_s u_s k_s^T e^{lam_end - lam_s}).
+// A key channel that keeps lam_end >= -kWideLog over the block takes one
+// reference for every tile, m_i = lam_end / 2 (the middle of the block's
+// log-retention range; no factor exceeds e^{kWideLog / 2}); any other channel
+// takes the middle of each tile's own range, m_i = (c_{i-1} + c_i) / 2.  While
+// every channel of the block has one reference (a flag per wave, combined
+// across the workgroup after a barrier) the pair factors are 1, the state
+// factors the one e^{lam_end / 2}, and the products run on the stored
+// operands.  Otherwise every product across tiles is formed from operands that
+// do not exceed the raw token values: for i > j, Ki_s e^{c_j - m_j} against
+// Kt_t (Qt_t) e^{m_i - c_j} (the latter e^{c_i - m_i} for adjacent tiles), and
+// the state update scales Ki_s by e^{lam_end - m_j}; these factors are 1 on
+// one-reference channels.  The factors are per-channel tables in LDS
+// (fwd_tab_rows).
 // The unit-lower-triangular solve is blocked over 16-token tiles: the diagonal
 // tiles are inverted by substitution, the off-diagonal coupling is applied on
 // the matrix cores while walking the tiles in order.
@@ -44,9 +56,11 @@
 // raw: the rows of q and k are staged as SiLU(raw) / |SiLU(raw)| (the norm
 // summed over the row's lanes while staging), v as SiLU(raw).
 //
-// Precondition (not checked): inside one WY block the log retention summed
-// over the block stays above about -170 per key channel (factors up to
-// e^{|lam_end| / 2} are formed in f32).
+// Precondition (not checked): the log retention summed over every 16-token
+// tile stays above about -150 per key channel (blocks of a single tile: -170).
+// Tile factors up to e^{|tile sum| / 2} are formed in f32 and the token dtype;
+// where e^{m_i} S falls below the normal range, what is lost is below
+// e^{|tile sum| / 2 - 87} of the state's contribution.
 #pragma once
 #include "carve_kernels.h"
 
@@ -72,6 +86,12 @@ __host__ __device__ constexpr int tri_col(int x, bool strict) {
 }
 static_assert(tri_row(0, true) == 1 && tri_col(0, true) == 0 && tri_row(5, true) == 3 && tri_col(5, true) == 2, "");
 static_assert(tri_row(0, false) == 0 && tri_row(2, false) == 1 && tri_col(2, false) == 1 && tri_col(9, false) == 3, "");
+
+// q * f (per-element factors at p), rounded back to the operand type
+template <typename T>
+__device__ __forceinline__ typename Quad<T>::q scale_q(typename Quad<T>::q q, const float* p) {
+  return Quad<T>::cvt(Quad<T>::f32(q) * *reinterpret_cast<const f32x4*>(p));
+}
 
 // GATED: the decay g is formed in the kernel from its raw logit f (token
 // dtype) as -exp(A) softplus(f + tau_f) (Eq. decay_gate, Sec. decay_gate),
@@ -122,7 +142,15 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
   T* sA = reinterpret_cast<T*>(smem + lay.A);      // [WB][LDW]   -A[t][s] (off-diagonal tiles)
   T* sP = reinterpret_cast<T*>(smem + lay.P);      // [WB][LDW]   P[t][s]
   T* sTmT = reinterpret_cast<T*>(smem + lay.TmT);          // [NB][16][LDB] T_ii[t][s] at (s, t)
-  float* sRho = reinterpret_cast<float*>(smem + lay.Rho);  // [D] e^{rho} = e^{lam_end / 2}
+  // factor tables [fwd_tab_rows(NB)][D]: rows kTabSt + i = e^{m_i}, kTabUp + i =
+  // e^{lam_end - m_i}, kTabHalf + i = e^{c_i - m_i}, kTabEnd = e^{lam_end},
+  // kTabGap + (i - 2)(i - 1) / 2 + j = e^{m_i - c_j} (i >= j + 2); a block with
+  // one reference per channel writes only row kTabSt
+  float* sTab = reinterpret_cast<float*>(smem + lay.Tab);
+  constexpr int kTabSt = 0, kTabUp = NB, kTabHalf = 2 * NB, kTabEnd = 3 * NB, kTabGap = 3 * NB + 1;
+  constexpr int NTAB = fwd_tab_rows(NB);
+  static_assert(NTAB <= 16, "one table row per lane of a 16-lane row");
+  int* sFlag = reinterpret_cast<int*>(smem + lay.Flag);   // [NW]
   float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);  // [2][WB] (block parity)
   float* sWs = sBeta + 2 * WB;                     // [2][WB] sigmoid(wx) (SW; block parity)
   constexpr bool SVW = chain_stage_vw<T, D, WB, RP, VAR>();
@@ -408,31 +436,100 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
           carry[e] = row_bcast15(lam[bb][e]);
         }
       }
-      f32x4 rho, eRho, fill;
+    }
+    // lam at the end of tile i, c_i, is lane 15 of the row (row_bcast15).  A key
+    // channel whose block retention falls below e^{-kWideLog} takes per-tile
+    // references; the wave's vote goes to LDS for the products after the next
+    // barrier.
+    {
+      bool wch[4];
+      bool mine = false;
       for (int e = 0; e < 4; ++e) {
-        rho[e] = 0.5f * carry[e];
-        eRho[e] = fast_exp(rho[e]);
-        fill[e] = fast_exp(-rho[e]);   // e^{lam_{-1} - rho}, lam_{-1} = 0
+        wch[e] = NB > 1 && row_bcast15(lam[NB - 1][e]) < -kWideLog;
+        mine = mine || wch[e];
       }
-      for (int bb = 0; bb < NB; ++bb) {
-        T* kp = sKi + (16 * bb + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c));
-        const f32x4 kv = Qd::f32(Qd::ld(kp));
-        T* qp = sQ + (16 * bb + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c));
-        const f32x4 qv = Qd::f32(Qd::ld(qp));
-        f32x4 kt, qt, ki;
-        for (int e = 0; e < 4; ++e) {
-          const float E = fast_exp(lam[bb][e] - rho[e]);
-          const float Ei = fast_exp(rho[e] - lam[bb][e]);
-          kt[e] = kv[e] * row_shr1(E, fill[e]);
-          qt[e] = qv[e] * E;
-          ki[e] = kv[e] * Ei;
-          fill[e] = row_bcast15(E);
+      const bool wave_wide = __any(mine) != 0;
+      if (NB > 1 && lane == 0) sFlag[w] = wave_wide ? 1 : 0;
+      f32x4 fill, cprev = zero4();   // e^{lam_{t-1} - m} for the first token of tile bb; c_{bb-1}
+      // factor tables: lane c of the row forms row c for the row's 4 channels
+      // (one reference: e^{rho} in rows St, Up; 1 in Half, Gap; e^{lam_end} in End).
+      // Row c as a linear form in the tile ends: exponent sum_i tc[i] c_i on
+      // per-tile references, tn lam_end on one reference.  The lane index is
+      // taken opaque here so that no lane mask is hoisted out of the blocks.
+      float tc[NB], tn = 0.0f;
+      {
+        int cr = c;
+        asm volatile("" : "+v"(cr));
+        for (int i = 0; i < NB; ++i) tc[i] = 0.0f;
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+          const float h = (cr == kTabSt + i) ? 0.5f : 0.0f;     // m_i = (c_{i-1} + c_i) / 2
+          const float u = (cr == kTabUp + i) ? 0.5f : 0.0f;     // lam_end - m_i
+          const float f = (cr == kTabHalf + i) ? 0.5f : 0.0f;   // c_i - m_i
+          tc[i] += h - u + f;
+          if (i > 0) tc[i - 1] += h - u - f;
+          tc[NB - 1] += 2.0f * u;
+          tn += h + u;
+#pragma unroll
+          for (int j = 0; j + 2 <= i; ++j) {
+            const float q = (cr == kTabGap + (i - 2) * (i - 1) / 2 + j) ? 0.5f : 0.0f;   // m_i - c_j
+            tc[i] += q;
+            tc[i - 1] += q;
+            tc[j] -= 2.0f * q;
+          }
         }
-        Qd::st(sKt + (16 * bb + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c)), Qd::cvt(kt));
-        Qd::st(qp, Qd::cvt(qt));
-        Qd::st(kp, Qd::cvt(ki));
+        if (cr == kTabEnd) {
+          tc[NB - 1] += 1.0f;
+          tn = 1.0f;
+        }
       }
-      if (c == 0) *reinterpret_cast<f32x4*>(sRho + 16 * w + 4 * g) = eRho;
+      f32x4 x;
+      for (int e = 0; e < 4; ++e) {
+        const float lend = row_bcast15(lam[NB - 1][e]);
+        float xw = 0.0f;
+        for (int i = 0; i < NB; ++i) xw = fmaf(tc[i], row_bcast15(lam[i][e]), xw);
+        x[e] = fast_exp(wch[e] ? xw : tn * lend);
+        fill[e] = fast_exp(-0.5f * lend);
+      }
+      if (c < NTAB) *reinterpret_cast<f32x4*>(sTab + c * D + 16 * w + 4 * g) = x;
+      // decayed operands of the key tile: Kt = k e^{lam_{t-1} - m}, Qt = q e^{lam - m},
+      // Ki = k e^{m - lam}; PER_CHANNEL_: the channels flagged in wch take per-tile
+      // references (the branch is taken by waves with such a channel)
+#define CARVE_GATE_OPERANDS(PER_CHANNEL_)                                                          \
+  for (int bb = 0; bb < NB; ++bb) {                                                                \
+    T* kp = sKi + (16 * bb + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c));                          \
+    const f32x4 kv = Qd::f32(Qd::ld(kp));                                                          \
+    T* qp = sQ + (16 * bb + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c));                           \
+    const f32x4 qv = Qd::f32(Qd::ld(qp));                                                          \
+    f32x4 kt, qt, ki;                                                                              \
+    for (int e = 0; e < 4; ++e) {                                                                  \
+      float m = 0.5f * row_bcast15(lam[NB - 1][e]), f0 = fill[e];                                   \
+      if (PER_CHANNEL_) {                                                                          \
+        /* per-tile reference: e^{c_{bb-1} - m} = e^{m - c_bb} */                                  \
+        const float ce = row_bcast15(lam[bb][e]);                                                  \
+        const float mt = 0.5f * (cprev[e] + ce);                                                   \
+        const float eb = row_bcast15(fast_exp(mt - lam[bb][e]));                                    \
+        m = wch[e] ? mt : m;                                                                       \
+        f0 = wch[e] ? eb : f0;                                                                     \
+        cprev[e] = ce;                                                                             \
+      }                                                                                            \
+      const float E = fast_exp(lam[bb][e] - m);                                                    \
+      const float Ei = fast_exp(m - lam[bb][e]);                                                   \
+      kt[e] = kv[e] * row_shr1(E, f0);                                                             \
+      qt[e] = qv[e] * E;                                                                           \
+      ki[e] = kv[e] * Ei;                                                                          \
+      fill[e] = row_bcast15(E); /* one reference: E of the tile's last token */                    \
+    }                                                                                              \
+    Qd::st(sKt + (16 * bb + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c)), Qd::cvt(kt));             \
+    Qd::st(qp, Qd::cvt(qt));                                                                       \
+    Qd::st(kp, Qd::cvt(ki));                                                                       \
+  }
+      if (wave_wide) {
+        CARVE_GATE_OPERANDS(true)
+      } else {
+        CARVE_GATE_OPERANDS(false)
+      }
+#undef CARVE_GATE_OPERANDS
     }
     // value side, value tile w: rows t = 16 bb + 4 g + e, column v = 16 w + c
     f32x4 wv[NB];
@@ -468,6 +565,12 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     __syncthreads();
 
     // ---- coupling tiles, diagonal inverses, state products ---------------------
+    bool wide = false;   // some key channel of the block on per-tile references
+    if constexpr (NB > 1) {
+      int f = 0;
+      for (int x = 0; x < NW; ++x) f |= sFlag[x];
+      wide = __builtin_amdgcn_readfirstlane(f) != 0;
+    }
     CARVE_STORE_S(NJT / 2, NJT);
     CARVE_PREFETCH_G(blk + 1 < nblk ? blk + 1 : blk);
     const float* bcur = sBeta + par * WB;
@@ -527,9 +630,23 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
         const T* ar = sKi + (16 * j + ct) * LDD + ((4 * gt) ^ CARVE_QX(ct));
         const T* br = (isA ? sKt : sQ) + (16 * i + ct) * LDD + ((4 * gt) ^ CARVE_QX(ct));
         f32x4 acc = zero4();
-        for (int jp = 0; jp < D / 32; ++jp)
-          acc = Qd::mma32(Qd::ld(ar + 32 * jp), Qd::ld(ar + 32 * jp + 16), Qd::ld(br + 32 * jp),
-                          Qd::ld(br + 32 * jp + 16), acc);
+        if (wide && i > j) {
+          // per-tile references: Ki e^{c_j - m_j} against X e^{m_i - c_j}; lane
+          // quads hold channels 32 jp + 4 g .. + 3 and 16 further
+          const float* fa = sTab + (kTabHalf + j) * D + 4 * gt;
+          const float* fb = sTab + (i == j + 1 ? kTabHalf + i : kTabGap + (i - 2) * (i - 1) / 2 + j) * D + 4 * gt;
+          for (int jp = 0; jp < D / 32; ++jp) {
+            const quad a0 = scale_q<T>(Qd::ld(ar + 32 * jp), fa + 32 * jp);
+            const quad a1 = scale_q<T>(Qd::ld(ar + 32 * jp + 16), fa + 32 * jp + 16);
+            const quad b0 = scale_q<T>(Qd::ld(br + 32 * jp), fb + 32 * jp);
+            const quad b1 = scale_q<T>(Qd::ld(br + 32 * jp + 16), fb + 32 * jp + 16);
+            acc = Qd::mma32(a0, a1, b0, b1, acc);
+          }
+        } else {
+          for (int jp = 0; jp < D / 32; ++jp)
+            acc = Qd::mma32(Qd::ld(ar + 32 * jp), Qd::ld(ar + 32 * jp + 16), Qd::ld(br + 32 * jp),
+                            Qd::ld(br + 32 * jp + 16), acc);
+        }
         f32x4 val;
         if (isA) {
           const float bt = bcur[16 * i + ct];
@@ -544,10 +661,10 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     // on the value tile (rows t = 16 bb + 4 g + e, column v): XQ = Qt S^T and the
     // right-hand side R = beta (w * v - Kt S^T)
     f32x4 RH[NB], XQ[NB];
-    {
-      quad sb[NJT];   // S' = S diag(e^{rho}) as the B operand
+    if (!wide) {
+      quad sb[NJT];   // S diag(e^{rho}) as the B operand
       for (int jt = 0; jt < NJT; ++jt)
-        sb[jt] = Qd::cvt(St[jt] * *reinterpret_cast<const f32x4*>(sRho + 16 * jt + 4 * g));
+        sb[jt] = Qd::cvt(St[jt] * *reinterpret_cast<const f32x4*>(sTab + kTabSt * D + 16 * jt + 4 * g));
       for (int bb = 0; bb < NB; ++bb) {
         f32x4 xk = zero4();
         XQ[bb] = zero4();
@@ -556,6 +673,23 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
         for (int jp = 0; jp < NJT / 2; ++jp) {
           xk = Qd::mma32(Qd::ld(kr + 32 * jp), Qd::ld(kr + 32 * jp + 16), sb[2 * jp], sb[2 * jp + 1], xk);
           XQ[bb] = Qd::mma32(Qd::ld(qr + 32 * jp), Qd::ld(qr + 32 * jp + 16), sb[2 * jp], sb[2 * jp + 1], XQ[bb]);
+        }
+        const f32x4 bt = *reinterpret_cast<const f32x4*>(bcur + 16 * bb + 4 * g);
+        for (int e = 0; e < 4; ++e) RH[bb][e] = bt[e] * (wv[bb][e] - xk[e]);
+      }
+    } else {
+      // S diag(e^{m_bb}) formed per tile, two state columns at a time
+      for (int bb = 0; bb < NB; ++bb) {
+        f32x4 xk = zero4();
+        XQ[bb] = zero4();
+        const T* kr = sKt + (16 * bb + c) * LDD + ((4 * g) ^ CARVE_QX(c));
+        const T* qr = sQ + (16 * bb + c) * LDD + ((4 * g) ^ CARVE_QX(c));
+        const float* fs = sTab + (kTabSt + bb) * D + 4 * g;
+        for (int jp = 0; jp < NJT / 2; ++jp) {
+          const quad s0 = Qd::cvt(St[2 * jp] * *reinterpret_cast<const f32x4*>(fs + 32 * jp));
+          const quad s1 = Qd::cvt(St[2 * jp + 1] * *reinterpret_cast<const f32x4*>(fs + 32 * jp + 16));
+          xk = Qd::mma32(Qd::ld(kr + 32 * jp), Qd::ld(kr + 32 * jp + 16), s0, s1, xk);
+          XQ[bb] = Qd::mma32(Qd::ld(qr + 32 * jp), Qd::ld(qr + 32 * jp + 16), s0, s1, XQ[bb]);
         }
         const f32x4 bt = *reinterpret_cast<const f32x4*>(bcur + 16 * bb + 4 * g);
         for (int e = 0; e < 4; ++e) RH[bb][e] = bt[e] * (wv[bb][e] - xk[e]);
@@ -575,14 +709,36 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       for (int j = 0; j <= i; ++j) O = Qd::mma16(Qd::ld(sP + (16 * i + c) * LDW + 16 * j + ((4 * g) ^ CARVE_QX(c))), uq[j], O);
       oq[i] = Qd::cvt(Qd::mma16(Qd::cvt(O), fI, zero4()));
     }
-    for (int jt = 0; jt < NJT; ++jt) {
-      const f32x4 er = *reinterpret_cast<const f32x4*>(sRho + 16 * jt + 4 * g);
-      f32x4 acc = St[jt] * er;
-      for (int kp = 0; kp < NB / 2; ++kp)
-        acc = Qd::mma32(Qd::ld_tr_sw(sKi, LDD, 32 * kp, 16 * jt, g, c), Qd::ld_tr_sw(sKi, LDD, 32 * kp + 16, 16 * jt, g, c),
-                        uq[2 * kp], uq[2 * kp + 1], acc);
-      if (NB & 1) acc = Qd::mma16(Qd::ld_tr_sw(sKi, LDD, 16 * (NB - 1), 16 * jt, g, c), uq[NB - 1], acc);
-      St[jt] = acc * er;
+    if (!wide) {
+      // S <- (S e^{rho} + u^T Ki) e^{rho}, rho = lam_end / 2
+      for (int jt = 0; jt < NJT; ++jt) {
+        const f32x4 er = *reinterpret_cast<const f32x4*>(sTab + kTabSt * D + 16 * jt + 4 * g);
+        f32x4 acc = St[jt] * er;
+        for (int kp = 0; kp < NB / 2; ++kp)
+          acc = Qd::mma32(Qd::ld_tr_sw(sKi, LDD, 32 * kp, 16 * jt, g, c), Qd::ld_tr_sw(sKi, LDD, 32 * kp + 16, 16 * jt, g, c),
+                          uq[2 * kp], uq[2 * kp + 1], acc);
+        if (NB & 1) acc = Qd::mma16(Qd::ld_tr_sw(sKi, LDD, 16 * (NB - 1), 16 * jt, g, c), uq[NB - 1], acc);
+        St[jt] = acc * er;
+      }
+    } else {
+      // S <- S e^{lam_end} + u^T (Ki_s e^{lam_end - m_j}) (the transposed Ki quads
+      // hold one channel, 16 jt + c, and four tokens of tile j)
+      for (int jt = 0; jt < NJT; ++jt) {
+        f32x4 acc = St[jt] * *reinterpret_cast<const f32x4*>(sTab + kTabEnd * D + 16 * jt + 4 * g);
+        for (int kp = 0; kp < NB / 2; ++kp) {
+          const quad k0 = Qd::cvt(Qd::f32(Qd::ld_tr_sw(sKi, LDD, 32 * kp, 16 * jt, g, c)) *
+                                  sTab[(kTabUp + 2 * kp) * D + 16 * jt + c]);
+          const quad k1 = Qd::cvt(Qd::f32(Qd::ld_tr_sw(sKi, LDD, 32 * kp + 16, 16 * jt, g, c)) *
+                                  sTab[(kTabUp + 2 * kp + 1) * D + 16 * jt + c]);
+          acc = Qd::mma32(k0, k1, uq[2 * kp], uq[2 * kp + 1], acc);
+        }
+        if (NB & 1) {
+          const quad k0 = Qd::cvt(Qd::f32(Qd::ld_tr_sw(sKi, LDD, 16 * (NB - 1), 16 * jt, g, c)) *
+                                  sTab[(kTabUp + NB - 1) * D + 16 * jt + c]);
+          acc = Qd::mma16(k0, uq[NB - 1], acc);
+        }
+        St[jt] = acc;
+      }
     }
     oprev = t0;
   }

@@ -141,10 +141,25 @@ __host__ __device__ constexpr RecLds rec_lds() {
 // tiles (v, wx: WB rows each, unpadded, 16-byte chunks XOR-swizzled by row) from
 // the first barrier of a block to its gates; it overlays A .. TmT, which are
 // written only after the gates.  Without VW those tiles are read per wave.
+// Tab holds the block's per-channel factor tables, Flag one word per wave
+// (whether one of its key channels needs per-tile references).
 // Beta holds beta and (scalar write gate) w of the block, for two blocks.
 struct ChainLds {
-  size_t U, X, Kt, Bx, Ki, F, Q, Tau, A, P, TmT, VW, Rho, Beta, Gate, total;
+  size_t U, X, Kt, Bx, Ki, F, Q, Tau, A, P, TmT, VW, Tab, Flag, Beta, Gate, total;
 };
+
+// Per-channel factor tables of a forward WY block of NB 16-token tiles
+// (carve_fwd_chain.h), m_i the reference of tile i and c_i the log retention
+// at its end: e^{m_i} (NB rows), e^{lam_end - m_i} (NB), e^{c_i - m_i} (NB),
+// e^{lam_end} (1) and e^{m_i - c_j} for i >= j + 2 ((NB - 1) (NB - 2) / 2).  A
+// block of one tile needs only e^{m_0}.
+// A forward block takes one reference per key channel while every channel's
+// log retention over the block stays above -kWideLog (factors up to
+// e^{kWideLog / 2}), per-tile references otherwise.
+constexpr float kWideLog = 160.0f;
+__host__ __device__ constexpr int fwd_tab_rows(int NB) {
+  return NB == 1 ? 1 : 3 * NB + 1 + (NB - 1) * (NB - 2) / 2;
+}
 
 // Row stride (elements) of a forward operand tile with n columns: bf16 tiles
 // take the quad swizzle qswz and need a stride of 16 (mod 32) elements (4 (mod
@@ -177,7 +192,8 @@ __host__ __device__ constexpr ChainLds chain_lds_v() {
   l.TmT = off;  off += lds_round(NB * 16 * LDB * e);
   l.VW = l.A;
   if (VW) off = lds_max(off, l.VW + lds_round(2 * WB * (size_t)D * e));
-  l.Rho = off;  off += lds_round(D * 4);
+  l.Tab = off;  off += lds_round((size_t)fwd_tab_rows((int)NB) * D * 4);
+  l.Flag = off; off += lds_round(16 * 4);   // one word per wave
   l.Beta = off; off += lds_round((SW ? 4 : 2) * WB * 4);
   l.Gate = off; off += lds_round(2 * D * 4);   // -exp(A), tau_f of the head (gated)
   l.total = off;
