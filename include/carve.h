@@ -292,6 +292,31 @@ int carve_rmsnorm_bwd_noalloc(const carve_dims_t* d, const void* o, const float*
  * negative capacity, CARVE_ERR_UNSUPPORTED for capacity > 16. */
 int carve_profile_events(hipEvent_t* events, int capacity);
 
+/* Diagnostic of the backward's wait for the chunk records (not part of the
+ * computation).  In carve_chunk_bwd and its variants, each adjoint wave waits
+ * for the records of the next chunks with a bounded poll of their ready flags
+ * (by default 2^20 polls, about a second; a correct launch never reaches it,
+ * since a chunk is recomputed in tens of microseconds by a workgroup that is
+ * already running).  If the bound runs out, the wave fills its state gradient
+ * with NaN, so the gradients of all earlier tokens come out NaN, waits no
+ * more, and sets a timeout word in the workspace's synchronisation area.  The
+ * call itself still returns CARVE_OK, as kernel completion is asynchronous.
+ * This reads that word for the last backward enqueued with `workspace` and
+ * the same dims `d`: *timed_out = 1 if a wait ran out, 0 otherwise.  The word
+ * is cleared at the start of every backward.  It copies 4 bytes to the host on
+ * `stream` and synchronises `stream`: the only call of this library that
+ * synchronises.  Errors: CARVE_ERR_NULL for a NULL argument;
+ * CARVE_ERR_SHAPE / CARVE_ERR_UNSUPPORTED for dims no backward accepts;
+ * CARVE_ERR_HIP if the copy fails. */
+int carve_bwd_wait_status(const carve_dims_t* d, const void* workspace, hipStream_t stream, int* timed_out);
+
+/* Test hook for the timeout path above: sets the bound of that wait, in polls,
+ * for the backward calls made on the calling thread from then on.  0 makes
+ * every wait give up at once (the kernels still run to completion and the
+ * results are NaN); a negative value restores the default.  Returns the
+ * previous bound.  Not for production use. */
+int carve_set_ready_wait_limit(int polls);
+
 /* Static description of a status code. */
 const char* carve_status_string(int status);
 

@@ -20,7 +20,8 @@ CARVE_F32, CARVE_BF16 = 0, 1
 SYMBOLS = ("carve_chunk_fwd", "carve_chunk_bwd", "carve_chunk_fwd_gated", "carve_chunk_bwd_gated",
            "carve_chunk_fwd_sw", "carve_chunk_bwd_sw", "carve_chunk_fwd_act", "carve_chunk_bwd_act",
            "carve_rmsnorm_fwd", "carve_rmsnorm_bwd", "carve_rmsnorm_workspace_size", "carve_rmsnorm_bwd_noalloc",
-           "carve_workspace_size", "carve_status_string", "carve_profile_events")
+           "carve_workspace_size", "carve_status_string", "carve_profile_events", "carve_bwd_wait_status",
+           "carve_set_ready_wait_limit")
 
 
 class Dims(ctypes.Structure):
@@ -79,6 +80,10 @@ def load_library(path: str = LIB_PATH):
     lib.carve_rmsnorm_workspace_size.restype = sz
     lib.carve_profile_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]
     lib.carve_profile_events.restype = ctypes.c_int
+    lib.carve_bwd_wait_status.argtypes = [D, vp, vp, ctypes.POINTER(ctypes.c_int)]
+    lib.carve_bwd_wait_status.restype = ctypes.c_int
+    lib.carve_set_ready_wait_limit.argtypes = [ctypes.c_int]
+    lib.carve_set_ready_wait_limit.restype = ctypes.c_int
     if path == LIB_PATH:
         _lib = lib
     return lib
@@ -94,6 +99,21 @@ def profile_events(events) -> None:
     only).  The events must already exist on the device (record each once)."""
     arr = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
     _check("carve_profile_events", load_library().carve_profile_events(arr, len(events)))
+
+
+def bwd_wait_status(dims: Dims, workspace, stream=None) -> bool:
+    """Whether an adjoint wave's bounded wait for a chunk record ran out in the
+    last backward made with this workspace (synchronises the stream)."""
+    out = ctypes.c_int(0)
+    _check("carve_bwd_wait_status", load_library().carve_bwd_wait_status(
+        ctypes.byref(dims), _ptr(workspace, "workspace"), _stream(stream), ctypes.byref(out)))
+    return bool(out.value)
+
+
+def set_ready_wait_limit(polls: int) -> int:
+    """Test hook: the bound of the backward's record wait for calls on this
+    thread (negative: the default).  Returns the previous bound."""
+    return int(load_library().carve_set_ready_wait_limit(int(polls)))
 
 
 def make_dims(B, T, H, Dk, Dv, R, L, dtype) -> Dims:

@@ -105,6 +105,10 @@ struct ProfClear {
   ~ProfClear() { g_prof_capacity = 0; }
 };
 
+// bound of the backward's wait for a chunk record, for the calls made on this
+// thread (carve_set_ready_wait_limit)
+thread_local int g_wait_limit = kReadySpinLimit;
+
 struct Range {
   const void* p;
   size_t bytes;
@@ -151,6 +155,27 @@ int carve_profile_events(hipEvent_t* events, int capacity) {
   for (int i = 0; i < capacity; ++i) g_prof_events[i] = events[i];
   g_prof_capacity = capacity;
   g_prof_count = 0;
+  return CARVE_OK;
+}
+
+int carve_set_ready_wait_limit(int polls) {
+  const int prev = g_wait_limit;
+  g_wait_limit = polls < 0 ? kReadySpinLimit : polls;
+  return prev;
+}
+
+int carve_bwd_wait_status(const carve_dims_t* d, const void* workspace, hipStream_t stream, int* timed_out) {
+  if (!d || !workspace || !timed_out) return CARVE_ERR_NULL;
+  int st = check_dims(d);
+  if (st) return st;
+  if (!pick_lw(d)) return CARVE_ERR_UNSUPPORTED;
+  const BwdWs wl = bwd_workspace_layout(d);
+  const int* word = reinterpret_cast<const int*>(reinterpret_cast<const char*>(workspace) + wl.sync) +
+                    sync_timeout_word((size_t)d->B * d->H, (size_t)(d->T / d->L));
+  int h = 0;
+  if (hipMemcpyAsync(&h, word, sizeof(int), hipMemcpyDeviceToHost, stream) != hipSuccess) return CARVE_ERR_HIP;
+  if (hipStreamSynchronize(stream) != hipSuccess) return CARVE_ERR_HIP;
+  *timed_out = h != 0 ? 1 : 0;
   return CARVE_OK;
 }
 
@@ -294,6 +319,7 @@ int bwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v,
   a.partG = reinterpret_cast<float*>(wsb + wl.partG);
   a.rec = wsb + wl.rec;
   a.B = d->B; a.T = d->T; a.H = d->H; a.R = d->R; a.RP = RP; a.L = d->L;
+  a.wait_limit = g_wait_limit;
   int* sync = reinterpret_cast<int*>(wsb + wl.sync);
   prof_mark(stream);
   st = launch_sync_clear(sync, sync_ints((size_t)d->B * d->H, (size_t)(d->T / d->L)), stream);

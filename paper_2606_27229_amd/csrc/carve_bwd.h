@@ -65,12 +65,15 @@
 
 namespace carve {
 
-// Bound of the ready-flag wait: 2^20 polls (each a few device-scope loads and a
-// short sleep; about a second in all).  A chunk is recomputed in tens of
-// microseconds by a workgroup that never waits, so the bound is not reached in
-// a correct launch; if it is, the waiting wave poisons its state gradient with
-// NaN (every gradient of earlier tokens then comes out NaN) and waits no more.
-constexpr int kReadySpinLimit = 1 << 20;
+// Bound of the ready-flag wait: 2^20 polls (each a few device-scope
+// loads and a short sleep; about a second in all).  A chunk is recomputed in
+// tens of microseconds by a workgroup that never waits, so the bound is not
+// reached in a correct launch; if it is, the waiting wave poisons its state
+// gradient with NaN (every gradient of earlier tokens then comes out NaN),
+// sets the wait-timeout word of the synchronisation area and waits no more.
+// The bound is a kernel argument (BwdArgs::wait_limit, kReadySpinLimit unless
+// a test sets it) so that tests can make the wait give up from the host while
+// every kernel still runs to completion.
 // chunks whose flags one wait inspects (need, need - 1, ...)
 constexpr int kReadyWindow = 8;
 
@@ -79,9 +82,9 @@ constexpr int kReadyWindow = 8;
 // chunks lo .. need, within a window of kReadyWindow chunks, were all seen
 // raised; one acquire fence then covers all of them, so a wave pays for one
 // cache invalidation per window instead of one per chunk.  Every lane reads
-// every flag itself.  Returns need + 1 if the bound ran out.
-__device__ __forceinline__ int acquire_ready(const int* rdy, const int need) {
-  for (int n = 0; n < kReadySpinLimit; ++n) {
+// every flag itself.  Returns need + 1 if the bound (`limit` polls) ran out.
+__device__ __forceinline__ int acquire_ready(const int* rdy, const int need, const int limit) {
+  for (int n = 0; n < limit; ++n) {
     // unconditional loads from clamped indices (issued back to back), masked after
     int f[kReadyWindow];
 #pragma unroll
@@ -116,7 +119,8 @@ __device__ __forceinline__ int acquire_ready(const int* rdy, const int need) {
 // and dtau = df over its tokens (per lane in registers, reduced once at the
 // end) into a per-(batch, head) partial.
 template <typename T, int D, int RP, int VAR>
-__device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char* smem, const int* ready) {
+__device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char* smem, const int* ready,
+                                            int* timeout_word) {
   typedef Quad<T> Qd;
   typedef typename Qd::q quad;
   typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
@@ -327,9 +331,11 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
 #define CARVE_BWD_READY(CH_)                                                                  \
   do {                                                                                        \
     if ((CH_) < acq_lo) {                                                                     \
-      const int lo_ = acquire_ready(rdy, (CH_));                                              \
+      const int lo_ = acquire_ready(rdy, (CH_), a.wait_limit);                                \
       if (lo_ > (CH_)) {                                                                      \
         acq_lo = -1;                                                                          \
+        if ((threadIdx.x & 63) == 0)                                                          \
+          __hip_atomic_store(timeout_word, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);    \
         for (int jt_ = 0; jt_ < NJT; ++jt_) dSt[jt_] = f32x4{__builtin_nanf(""), __builtin_nanf(""), \
                                                              __builtin_nanf(""), __builtin_nanf("")}; \
       } else {                                                                                \
@@ -881,7 +887,7 @@ carve_bwd_fused_kernel(FwdArgs f, BwdArgs a, int nrec, int* sync) {
         __hip_atomic_store(ready + (size_t)bh * nch + ch, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     }
   } else {
-    bwd_adjoint<T, D, RP, VAR>(a, ticket - nrec, smem, ready);
+    bwd_adjoint<T, D, RP, VAR>(a, ticket - nrec, smem, ready, sync + sync_timeout_word(nbh, nch));
   }
 }
 

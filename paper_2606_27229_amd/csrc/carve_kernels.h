@@ -241,6 +241,7 @@ struct BwdArgs {
   float* partV;   // per-(b,h,split) partial dVb, dVw (workspace)
   const void* rec;  // chunk records of the recompute (workspace)
   int B, T, H, R, RP, L;
+  int wait_limit;   // polls of the adjoint's bounded wait for a chunk record
 };
 
 // token splits of the Vb / Vw gradient kernel and chunk splits of the [Ub; Uw]
@@ -361,8 +362,12 @@ int launch_sync_clear(int* sync, size_t n, hipStream_t s);
 // recompute sub-chunks (2RP fold rows)
 size_t bwd_lds_bytes(int dtype, int D, int LW, int RP);
 // ints of the synchronisation area: one ready flag per chunk, the ticket
-// counter that assigns the workgroup roles, padding
+// counter that assigns the workgroup roles, the wait-timeout word (nonzero once
+// an adjoint wave's bounded wait for a record ran out), padding
 __host__ __device__ constexpr size_t sync_ints(size_t nbh, size_t nch) { return nbh * nch + 4; }
+__host__ __device__ constexpr size_t sync_timeout_word(size_t nbh, size_t nch) { return nbh * nch + 1; }
+// default bound of that wait, in polls (carve_bwd.h)
+constexpr int kReadySpinLimit = 1 << 20;
 // sw: the scalar write gate (dVb, dUb only; the records hold RP fold rows)
 int launch_bwd_vparam(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s);
 int launch_bwd_uparam(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s);

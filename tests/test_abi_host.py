@@ -107,6 +107,27 @@ def test_profile_hook_validation():
     assert lib.carve_profile_events(None, 0) == 0
 
 
+def test_wait_hooks_host():
+    """The wait-bound test hook round-trips on the calling thread (negative:
+    the default, 2^20 polls); the timeout status query rejects NULL arguments
+    and dims no backward accepts before any HIP call."""
+    lib = carve.load_library()
+    default = 1 << 20
+    assert lib.carve_set_ready_wait_limit(0) == default
+    assert lib.carve_set_ready_wait_limit(7) == 0
+    assert lib.carve_set_ready_wait_limit(-1) == 7
+    assert lib.carve_set_ready_wait_limit(-5) == default
+    assert lib.carve_set_ready_wait_limit(-1) == default
+    d = _dims()
+    out = ctypes.c_int(5)
+    fake = ctypes.c_void_p(4096)
+    assert lib.carve_bwd_wait_status(None, fake, None, ctypes.byref(out)) == -1
+    assert lib.carve_bwd_wait_status(ctypes.byref(d), None, None, ctypes.byref(out)) == -1
+    assert lib.carve_bwd_wait_status(ctypes.byref(d), fake, None, None) == -1
+    assert lib.carve_bwd_wait_status(ctypes.byref(_dims(T=100)), fake, None, ctypes.byref(out)) == -2
+    assert out.value == 5
+
+
 def test_gated_forward_validation():
     """carve_chunk_fwd_gated: NULL f / A / tau_f, bad shapes and misalignment
     are rejected before any HIP call."""

@@ -188,3 +188,42 @@ def test_bwd_hard_erase_channels(L):
     got = {k: host(gr[k]) for k in GRADS}
     errs = {k: max_rel(got[k], rb[k]) for k in GRADS}
     _report(errs, got)
+
+
+def test_bwd_wait_timeout_is_reported():
+    """The adjoint's bounded wait for the chunk records, made to give up from
+    the host (a bound of 0 polls): every kernel still runs to completion, the
+    workspace's timeout word reads 1 and the carried state gradient is NaN;
+    with the default bound the next call on the same workspace reads 0 and is
+    bitwise equal to a call made before."""
+    w = _w(B=1, T=128, L=64, s0=0.2)
+    print("case bwd wait timeout bf16 D=128 T=128", flush=True)
+    inp = make_inputs(w, seed=41, dS_T=True)
+    x = to_gpu(inp, torch.bfloat16)
+    o, S_T, S_chunks = carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"],
+                                       x["Ub"], x["Uw"], x["Vb"], x["Vw"], x["S0"], L=w.L)
+    dims = carve.make_dims(w.B, w.T, w.H, w.Dk, w.Dv, w.R, w.L, torch.bfloat16)
+    ws = torch.empty(carve.workspace_size(dims, True), dtype=torch.uint8, device="cuda")
+
+    def bwd():
+        gr = carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
+                             x["Vb"], x["Vw"], S_chunks, x["dO"], x["dS_T"], L=w.L, workspace=ws)
+        torch.cuda.synchronize()
+        return {k: host(v) for k, v in gr.items()}
+
+    ref = bwd()
+    assert not carve.bwd_wait_status(dims, ws)
+    prev = carve.set_ready_wait_limit(0)
+    try:
+        got = bwd()
+        timed_out = carve.bwd_wait_status(dims, ws)
+    finally:
+        carve.set_ready_wait_limit(-1)
+    assert prev == 1 << 20
+    assert timed_out
+    assert np.all(np.isnan(got["dS0"]))
+    again = bwd()
+    assert not carve.bwd_wait_status(dims, ws)
+    for key, val in ref.items():
+        assert np.all(np.isfinite(val)), key
+        assert np.array_equal(again[key], val), key
