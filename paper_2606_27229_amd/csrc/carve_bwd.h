@@ -155,6 +155,10 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
 
   constexpr BwdLds lay = bwd_lds<T, D, RP, VAR>();
   constexpr int NS = bwd_stage_tiles(SW);             // staged token tiles per block
+  // the key-side factors of a block (E and the erase gate) come from the
+  // chunk record, staged in place of g and bx; GATED kernels recompute them
+  // from f, bx and tau
+  constexpr bool KREC = !GATED;
   T* sF = reinterpret_cast<T*>(smem + lay.F);        // [R2][LDD]    F of the chunk
   T* sVbT = reinterpret_cast<T*>(smem + lay.VbT);    // [RP][LDK]    Vb^T (quad-swizzled)
   T* sVwT = reinterpret_cast<T*>(smem + lay.VwT);    // [RP][LDK]    Vw^T (not SW; quad-swizzled)
@@ -243,15 +247,17 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   constexpr int NTV = (NTAU + NT - 1) / NT;
   constexpr int NFV = (R2 * D / VEC + NT - 1) / NT;   // 16-byte vectors of F per thread
   u32x4 ptau[NTV], pF[NFV];
-  // token tiles k, q, bx, v, dO and (not SW) wx of a block: NS * 16 rows of D
-  // elements read as 16-byte vectors (whole rows, coalesced) and staged through LDS
+  // token tiles k, q, bx (KREC: the recorded erase gate), v, dO and (not SW) wx
+  // of a block: NS * 16 rows of D elements read as 16-byte vectors (whole rows,
+  // coalesced) and staged through LDS
   constexpr int NC = D / VEC;                    // 16-byte chunks per row
   constexpr int NSV = NS * 16 * NC;              // vectors of the tiles
   constexpr int NSTG = (NSV + NT - 1) / NT;      // per thread
   static_assert((16 * NC) % 64 == 0 || NSV % NT == 0, "tile index uniform per wave");
   static_assert(!ACT || (16 * NC) % 64 == 0, "a staged row's chunks in one wave (row sums over lanes)");
   u32x4 pstg[NSTG];
-  // g of a block: 16 rows of D floats, one 16-byte vector per thread
+  // g (KREC: the recorded E) of a block: 16 rows of D floats, one 16-byte
+  // vector per thread
   constexpr int NGC = D / 4;                     // 16-byte chunks per g row
   static_assert(16 * NGC == NT, "one g vector per thread");
   quad ptm, ppm, psbq[NJT];
@@ -293,13 +299,21 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       const int x_ = tid + u_ * NT;                                                           \
       if (NSV % NT != 0 && x_ >= NSV) break;                                                  \
       const int s_ = x_ / (16 * NC), t_ = (x_ / NC) % 16, k_ = x_ % NC;                       \
-      const T* src_ = s_ == 0 ? k : s_ == 1 ? q : s_ == 2 ? bx : s_ == 3 ? v : s_ == 4 ? dO : wx; \
-      pstg[u_] = *reinterpret_cast<const u32x4*>(src_ + (tb_ + t_) * rs + k_ * VEC);           \
+      if (KREC && s_ == 2) {                                                                  \
+        /* the recorded erase gate of the block (rows of D) in place of bx */                 \
+        pstg[u_] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(rc_ + cr.Sig) +   \
+                                                   (16 * bc_ + t_) * D + k_ * VEC);            \
+      } else {                                                                                \
+        const T* src_ = s_ == 0 ? k : s_ == 1 ? q : s_ == 2 ? bx : s_ == 3 ? v : s_ == 4 ? dO : wx; \
+        pstg[u_] = *reinterpret_cast<const u32x4*>(src_ + (tb_ + t_) * rs + k_ * VEC);         \
+      }                                                                                       \
     }                                                                                         \
     if constexpr (GATED) {                                                                    \
       if (tid < 16 * NC) pfv = *reinterpret_cast<const u32x4*>(fl + (tb_ + tid / NC) * rs + (tid % NC) * VEC); \
     } else {                                                                                  \
-      pg = *reinterpret_cast<const f32x4*>(gl + (tb_ + tid / NGC) * rs + 4 * (tid % NGC));    \
+      /* the recorded E of the block in place of g */                                          \
+      pg = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(rc_ + cr.E) +         \
+                                           (16 * bc_ + tid / NGC) * D + 4 * (tid % NGC));      \
     }                                                                                         \
     (void)e_;                                                                                 \
   } while (0)
@@ -482,24 +496,37 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
           vraw = vq;
           vq = Qd::cvt(silu4(Qd::f32(vq)));
         }
-        for (int ks = 0; ks < NRB; ++ks) ltq[ks] = Qd::ld(sTau + c * LDR + 16 * ks + 4 * g);
+        if constexpr (!KREC)
+          for (int ks = 0; ks < NRB; ++ks) ltq[ks] = Qd::ld(sTau + c * LDR + 16 * ks + 4 * g);
       }
       // key-side factors kept for the adjoint in the token dtype (quads)
       quad Eq, Eiq, sigq;
       {
-        f32x4 z = zero4();
-        for (int ks = 0; ks < NRB; ++ks) z = Qd::mma16(CARVE_FVB(ks), ltq[ks], z);
-        const f32x4 bxv = Qd::f32(lbx);
         const f32x4 kv = Qd::f32(kq), qv = Qd::f32(qq);
         f32x4 kt, qt, ki, E, Ei, sig, gp;
+        if constexpr (KREC) {
+          // E and the erase gate as the recompute formed them (staged in place
+          // of g and bx); Ei from E as there, so every tile matches its T and P
+          sig = Qd::f32(lbx);
+          for (int i = 0; i < 4; ++i) {
+            E[i] = lg[i];
+            Ei[i] = fast_rcp(E[i]);
+          }
+        } else {
+          f32x4 z = zero4();
+          for (int ks = 0; ks < NRB; ++ks) z = Qd::mma16(CARVE_FVB(ks), ltq[ks], z);
+          const f32x4 bxv = Qd::f32(lbx);
+          for (int i = 0; i < 4; ++i) {
+            float sp, sg;
+            softplus_sigmoid(z[i] + bxv[i], sp, sg);
+            sig[i] = sg;
+            const float lam = row_scan(lg[i] - sp);
+            const float rho = 0.5f * row_bcast15(lam);
+            E[i] = fast_exp(lam - rho);
+            Ei[i] = fast_exp(rho - lam);
+          }
+        }
         for (int i = 0; i < 4; ++i) {
-          float sp, sg;
-          softplus_sigmoid(z[i] + bxv[i], sp, sg);
-          sig[i] = sg;
-          const float lam = row_scan(lg[i] - sp);
-          const float rho = 0.5f * row_bcast15(lam);
-          E[i] = fast_exp(lam - rho);
-          Ei[i] = fast_exp(rho - lam);
           // e^{lam_{-1} - rho} = e^{-rho} = Ei of the last token
           kt[i] = kv[i] * row_shr1(E[i], row_bcast15(Ei[i]));
           qt[i] = qv[i] * E[i];

@@ -50,10 +50,14 @@ struct FwdArgs {
 //                                 Sr = S diag(e^{rho}) with rho = lam_15 / 2 per key
 //                                 channel: quad jt of thread tid
 //                                 (Sr[16 w + c][16 jt + 4 g + e]), contiguous over threads
+//   E   [L/16][16][D]  f32       e^{lam_t - rho} of every token and key channel (its
+//                                 block's reference; not written by the GATED kernels)
+//   Sig [L/16][16][D]  token dtype  sigma(z_b) of every token and key channel (the
+//                                 erase gate b; not written by the GATED kernels)
 //   dF  [D][RF]    f32           written by the adjoint: the chunk's gradient of F,
 //                                 stored transposed (dF[r][j] at (j, r))
 struct ChunkRec {
-  size_t F, Tau, Tm, P, S, dF, total;
+  size_t F, Tau, Tm, P, S, E, Sig, dF, total;
 };
 __host__ __device__ constexpr size_t rec_align(size_t x) { return (x + 255) & ~(size_t)255; }
 __host__ __device__ constexpr ChunkRec chunk_rec(size_t e, int D, int L, int RF) {
@@ -65,6 +69,8 @@ __host__ __device__ constexpr ChunkRec chunk_rec(size_t e, int D, int L, int RF)
   r.Tm = off;  off += rec_align(nbc * 256 * e);
   r.P = off;   off += rec_align(nbc * 256 * e);
   r.S = off;   off += rec_align(nbc * (size_t)D * D * e);
+  r.E = off;   off += rec_align(nbc * 16 * (size_t)D * 4);
+  r.Sig = off; off += rec_align(nbc * 16 * (size_t)D * e);
   r.dF = off;  off += rec_align((size_t)RF * D * 4);
   r.total = off;
   return r;
@@ -256,7 +262,8 @@ constexpr int kUSplit = 16;
 // unless the write gate is scalar, wx, in the token dtype, then g in f32: 16
 // rows each, unpadded, 16-byte chunks XOR-swizzled by row) are staged there
 // (Stage), so the region holds at least 6 (5) * 16 * D elements plus 16 * D
-// floats.  At a chunk start the glue reuses dSx for dF as a high and a low
+// floats.  Except in gated kernels, the bx and g slots hold the block's erase
+// gate and retention factors E from the chunk record instead.  At a chunk start the glue reuses dSx for dF as a high and a low
 // part ([D][LDF] each).
 // Gated kernels stage the decay logit f (token dtype) in place of g and keep
 // -exp(A), tau_f of the head (Gate) behind it, inside the area g would take

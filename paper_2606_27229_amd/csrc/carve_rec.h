@@ -2,8 +2,9 @@
 //
 // rec_chunk() recomputes one gate chunk of one (batch, head) from its start
 // state (S_chunks, written by the forward) and writes the chunk record that the
-// adjoint reads (ChunkRec): the fold F, tau, and T, P, the retention and the
-// start state of every 16-token WY block.  Every chunk is independent, so the
+// adjoint reads (ChunkRec): the fold F, tau, and T, P and the scaled start
+// state of every 16-token WY block, and (except with the decay formed in the
+// kernels) the retention factors E and the erase gate of every token.  Every chunk is independent, so the
 // recompute is chunk-parallel.  Wave w of the workgroup owns the 16-wide tile w
 // of the value axis and the 16-wide tile w of the key axis:
 //   * the state lives in registers as S^T tiles (rows = key index j, columns =
@@ -277,23 +278,35 @@ __device__ __forceinline__ void rec_chunk(const FwdArgs& a, const int bh, const 
         gv = pg[bb];
       }
       const f32x4 qv = Qd::f32(Qd::ld(sQ + (16 * bb + c) * LDD + 16 * w + 4 * g));
-      f32x4 kt, qt, ki, erho;
+      f32x4 kt, qt, ki, erho, ev, sgv;
       for (int i = 0; i < 4; ++i) {
-        const float ell = gv[i] - softplus_f(z[i] + bxv[i]);
+        float sp, sg;
+        softplus_sigmoid(z[i] + bxv[i], sp, sg);
+        const float ell = gv[i] - sp;
         const float lam = row_scan(ell);
         const float rho = 0.5f * row_bcast15(lam);
         const float E = fast_exp(lam - rho);
-        const float Ei = fast_exp(rho - lam);
+        // the adjoint forms Ei from the recorded E the same way (GATED: it
+        // recomputes both from the gates)
+        const float Ei = GATED ? fast_exp(rho - lam) : fast_rcp(E);
         // e^{lam_{-1} - rho} = e^{-rho} = Ei of the last token
         kt[i] = kv[i] * row_shr1(E, row_bcast15(Ei));
         qt[i] = qv[i] * E;
         ki[i] = kv[i] * Ei;
         erho[i] = row_bcast15(E);   // e^{lam_15 - rho} = e^{rho}
+        ev[i] = E;
+        sgv[i] = sg;
       }
       const int ro = (16 * bb + c) * LDD + 16 * w + 4 * g;
       Qd::st(sKt + ro, Qd::cvt(kt));
       Qd::st(sQt + ro, Qd::cvt(qt));
       Qd::st(sKi + ro, Qd::cvt(ki));
+      if constexpr (!GATED) {
+        // E and the erase gate of the block's tokens for the adjoint: rows of D
+        const size_t re = ((size_t)(m * NB + bb) * 16 + c) * D + 16 * w + 4 * g;
+        *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(rec + cr.E) + re) = ev;
+        Qd::st(reinterpret_cast<T*>(rec + cr.Sig) + re, Qd::cvt(sgv));
+      }
       if (c == 15) *reinterpret_cast<f32x4*>(sGam + bb * D + 16 * w + 4 * g) = erho;
     }
     // value side, value tile w: rows t = 16 bb + 4 g + i, column v = 16 w + c
