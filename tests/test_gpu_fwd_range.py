@@ -15,7 +15,8 @@ cases drive the second mode:
   an erase logit of 40 (about -40 each, -120 per tile, at random positions);
 - mixed blocks: erase logits swinging between 1.9 and 2.7 on 16 channels put
   the block sums of those channels on both sides of -160, so blocks of both
-  modes follow each other along the sequence (checked on the oracle's gates).
+  modes follow each other along the sequence (checked on the oracle's gates);
+- hard erase at the headline launch (B=4 H=16 T=4096), on sampled slices.
 
 Bar: bf16 inputs with f32 state and accumulation, max-rel <= 2e-2 per tensor.
 """
@@ -153,3 +154,50 @@ def test_fwd_bwd_mixed_blocks():
     print("block minima over channels:", np.round(sums, 1).tolist(), flush=True)
     assert np.any(sums < -165) and np.any(sums > -155), "the inputs do not mix both block modes"
     _check_default(inp, w.L, rf=rf)
+
+
+def test_fwd_bwd_hard_erase_full_size_sampled():
+    """The headline launch (B=4 H=16 T=4096 d=128 r=32 L=64) with hard-erase
+    channels in every (batch, head), every block on per-tile references;
+    checked on two sampled (batch, head) slices, the parameter gradients with
+    the upstream gradients zeroed outside them (so the full-size sums must
+    equal the oracle's sums over the samples)."""
+    from paper_2606_27229_amd.inputs import WORKLOADS
+    from tests.test_gpu_fullsize import PARAM_GRADS, TOKEN_GRADS, _slice
+    w = WORKLOADS["layer_1p3b_T4096"].with_(L=64)
+    print(f"case forward hard erase full size B={w.B} H={w.H} T={w.T}", flush=True)
+    inp = _hard_erase(make_inputs(w, seed=490, dS_T=True), w, seed=491)
+    samples = [(0, 0), (w.B - 1, w.H - 1)]
+    keep = np.zeros((w.B, w.H), dtype=bool)
+    for b, h in samples:
+        keep[b, h] = True
+    inp["dO"] = inp["dO"] * keep[:, None, :, None]
+    inp["dS_T"] = inp["dS_T"] * keep[:, :, None, None]
+    x = to_gpu(inp, torch.bfloat16)
+    o, S_T, S_chunks = carve.chunk_fwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"],
+                                       x["Uw"], x["Vb"], x["Vw"], x["S0"], L=w.L)
+    gr = carve.chunk_bwd(x["q"], x["k"], x["v"], x["beta"], x["g"], x["bx"], x["wx"], x["Ub"], x["Uw"],
+                         x["Vb"], x["Vw"], S_chunks, x["dO"], x["dS_T"], L=w.L)
+    torch.cuda.synchronize()
+    del x
+    ref_params = {key: 0.0 for key in PARAM_GRADS}
+    errs, got = {}, {}
+    for b, h in samples:
+        s = _slice(inp, b, h)
+        rf = orc.fwd_serial(s, w.L, want_chunks=True)
+        rb = orc.bwd(s, w.L, s["dO"], s["dS_T"])
+        for key, val in (("o", o[b:b + 1, :, h:h + 1]), ("S_T", S_T[b:b + 1, h:h + 1]),
+                         ("S_chunks", S_chunks[b:b + 1, h:h + 1])):
+            got[f"{key}[{b},{h}]"] = host(val)
+            errs[f"{key}[{b},{h}]"] = max_rel(got[f"{key}[{b},{h}]"], rf[key])
+        for key in TOKEN_GRADS:
+            got[f"{key}[{b},{h}]"] = host(gr[key][b:b + 1, :, h:h + 1])
+            errs[f"{key}[{b},{h}]"] = max_rel(got[f"{key}[{b},{h}]"], rb[key])
+        got[f"dS0[{b},{h}]"] = host(gr["dS0"][b:b + 1, h:h + 1])
+        errs[f"dS0[{b},{h}]"] = max_rel(got[f"dS0[{b},{h}]"], rb["dS0"])
+        for key in PARAM_GRADS:
+            ref_params[key] = ref_params[key] + rb[key]
+    for key in PARAM_GRADS:
+        got[key] = host(gr[key])
+        errs[key] = max_rel(got[key], ref_params[key])
+    _report(errs, got)
