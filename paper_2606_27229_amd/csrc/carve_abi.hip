@@ -339,10 +339,8 @@ int bwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v,
   // 5. fixed-order reductions of the partials
   const int nbh = d->B * d->H;
   const size_t RD = (size_t)d->R * d->Dk;
-  st = launch_param_reduce(a.part, nbh * kUSplit, RD, dUb, sw ? nullptr : dUw, stream);
-  if (st) return st;
-  prof_mark(stream);
-  st = launch_param_reduce(a.partV, nbh * kVSplit, RD, dVb, sw ? nullptr : dVw, stream);
+  st = launch_param_reduce(a.part, nbh * kUSplit, a.partV, nbh * kVSplit, RD, dUb, sw ? nullptr : dUw, dVb,
+                           sw ? nullptr : dVw, stream);
   if (st) return st;
   prof_mark(stream);
   // 6. (gated) dA, dtau summed over the batch

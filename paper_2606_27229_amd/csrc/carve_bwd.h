@@ -76,6 +76,11 @@ namespace carve {
 // every kernel still runs to completion.
 // chunks whose flags one wait inspects (need, need - 1, ...)
 constexpr int kReadyWindow = 8;
+// how many chunks ahead of the adjoint the recompute works, and the bound of
+// its wait for the adjoint's position (2^16 polls of a few hundred cycles:
+// milliseconds, far beyond a chunk's time)
+constexpr int kRecomputeLead = 4;
+constexpr int kLeadSpinLimit = 1 << 16;
 
 // Wait until chunk `need`'s flag is raised (flags are raised with release
 // stores at agent scope) and return the lowest chunk lo such that the flags of
@@ -120,7 +125,7 @@ __device__ __forceinline__ int acquire_ready(const int* rdy, const int need, con
 // end) into a per-(batch, head) partial.
 template <typename T, int D, int RP, int VAR>
 __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char* smem, const int* ready,
-                                            int* timeout_word) {
+                                            int* timeout_word, int* pos) {
   typedef Quad<T> Qd;
   typedef typename Qd::q quad;
   typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
@@ -466,6 +471,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         *reinterpret_cast<f32x4*>(sGs + t * D + 4 * (kk ^ (t & (NGC - 1)))) = lg_row;
       }
       __syncthreads();
+      // the chunks started so far, for the pacing of the recompute
+      if (bc == nbc - 1 && tid == 0) __hip_atomic_store(pos, nch - ch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       // this wave's quads of the token tiles (row t = c, elements 16 w + 4 g ..
       // + 3) and of tau_b; read before the barrier that ends this step, so the
       // value-side step may overwrite the staging region
@@ -888,23 +895,40 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
 // waits, so every flag an adjoint workgroup waits for is raised in finite time
 // whatever order the hardware dispatches the grid in.  Recompute items are
 // taken latest chunk first (the order in which the adjoint needs them): item
-// i is chunk nch - 1 - i / (B*H) of (batch, head) i % (B*H).
+// i is chunk nch - 1 - i / (B*H) of (batch, head) i % (B*H).  With lead > 0 a
+// recompute workgroup starts that chunk only once the adjoint of its (batch,
+// head) has started the chunk lead places before it (a bounded wait: the
+// recompute still never waits for long): records are then written shortly
+// before they are read, and the recompute's stores do not all come at once.
+// Measured at the headline shape, a lead of 3-4 chunks takes the fused
+// launch from 2.01 to 1.90 ms; 1 chunk starves the adjoint.
 template <typename T, int D, int LW, int RP, int VAR>
 __global__ void __launch_bounds__(bwd_threads(D)) __attribute__((amdgpu_waves_per_eu(1, 2)))
-carve_bwd_fused_kernel(FwdArgs f, BwdArgs a, int nrec, int* sync) {
+carve_bwd_fused_kernel(FwdArgs f, BwdArgs a, int nrec, int* sync, int lead) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int nbh = a.B * a.H, nch = a.T / a.L;
   const int nitems = nbh * nch;
   int* ready = sync;
   if (threadIdx.x == 0)
     reinterpret_cast<int*>(smem)[0] =
-        __hip_atomic_fetch_add(sync + nitems, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_add(sync + sync_ticket(nbh, nch), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   const int ticket = __builtin_amdgcn_readfirstlane(reinterpret_cast<const int*>(smem)[0]);
   __syncthreads();
   if (ticket < nrec) {
     for (int item = ticket; item < nitems; item += nrec) {
       const int ch = nch - 1 - item / nbh, bh = item % nbh;
+      const int row = item / nbh;   // chunks after ch
+      if (lead > 0 && row >= lead) {
+        if (threadIdx.x == 0) {
+          const int* p = sync + sync_adjoint_pos(nbh, nch) + bh;
+          for (int n = 0; n < kLeadSpinLimit; ++n) {
+            if (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) > row - lead) break;
+            __builtin_amdgcn_s_sleep(4);
+          }
+        }
+        __syncthreads();
+      }
       rec_chunk<T, D, LW, RP, VAR>(f, bh, ch, smem);
       // every wave's record stores are complete before the barrier; the
       // release store (agent scope) then writes them back for other XCDs
@@ -914,7 +938,8 @@ carve_bwd_fused_kernel(FwdArgs f, BwdArgs a, int nrec, int* sync) {
         __hip_atomic_store(ready + (size_t)bh * nch + ch, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     }
   } else {
-    bwd_adjoint<T, D, RP, VAR>(a, ticket - nrec, smem, ready, sync + sync_timeout_word(nbh, nch));
+    bwd_adjoint<T, D, RP, VAR>(a, ticket - nrec, smem, ready, sync + sync_timeout_word(nbh, nch),
+                               sync + sync_adjoint_pos(nbh, nch) + (ticket - nrec));
   }
 }
 
@@ -944,7 +969,11 @@ static int launch_fused_t(const FwdArgs& f, const BwdArgs& a, int* sync, int cus
     if (nrec < cus / 4) nrec = cus;
     if (nrec > nitems) nrec = nitems;
     if (nrec < 1) nrec = 1;
-    hipLaunchKernelGGL(kern, dim3((unsigned)(nrec + nbh)), dim3(bwd_threads(D)), lds, stream, f, a, (int)nrec, sync);
+    // pace the recompute only when every workgroup of the grid can be resident
+    // at once (one per compute unit), so that the adjoints it follows run
+    const int lead = nrec + nbh <= cus ? kRecomputeLead : 0;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(nrec + nbh)), dim3(bwd_threads(D)), lds, stream, f, a, (int)nrec, sync,
+                       lead);
     return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
   }
 }

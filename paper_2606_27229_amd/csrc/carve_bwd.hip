@@ -23,11 +23,19 @@ __global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_vparam_kernel(BwdArg
 // (x, y) of a 64 x 16 block sums records y, y + 16, ... of element x (four
 // loads in flight), then the sixteen partial sums are added in order
 // y = 0..15.  Elements x < cnt are summed (cnt = 2 * half, or half when there
-// is no dst1).
+// is no second half).  blockIdx.y selects the d[Ub; Uw] (0) or the dVb, dVw
+// (1) partials, so both reductions share one launch.
 constexpr int kReduceGroups = 16;
-__global__ void __launch_bounds__(64 * kReduceGroups) carve_param_reduce_kernel(const float* __restrict__ part,
-                                                                                int nparts, size_t half, size_t cnt,
-                                                                                float* dst0, float* dst1) {
+__global__ void __launch_bounds__(64 * kReduceGroups) carve_param_reduce_kernel(const float* __restrict__ partU,
+                                                                                int npartU,
+                                                                                const float* __restrict__ partV,
+                                                                                int npartV, size_t half, size_t cnt,
+                                                                                float* dU0, float* dU1, float* dV0,
+                                                                                float* dV1) {
+  const float* part = blockIdx.y == 0 ? partU : partV;
+  const int nparts = blockIdx.y == 0 ? npartU : npartV;
+  float* dst0 = blockIdx.y == 0 ? dU0 : dV0;
+  float* dst1 = blockIdx.y == 0 ? dU1 : dV1;
   __shared__ float red[kReduceGroups][64];
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   const size_t x = (size_t)blockIdx.x * 64 + tx;
@@ -255,11 +263,12 @@ int launch_bwd_uparam(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s
   return launch_uparam_d<float>(a, D, sw, s);
 }
 
-int launch_param_reduce(const float* part, int nparts, size_t half, float* dst0, float* dst1, hipStream_t s) {
-  const size_t cnt = dst1 ? 2 * half : half;
+int launch_param_reduce(const float* partU, int npartU, const float* partV, int npartV, size_t half, float* dU0,
+                        float* dU1, float* dV0, float* dV1, hipStream_t s) {
+  const size_t cnt = dU1 ? 2 * half : half;
   const int blocks = (int)((cnt + 63) / 64);
-  hipLaunchKernelGGL(carve_param_reduce_kernel, dim3(blocks), dim3(64 * kReduceGroups), 0, s, part, nparts, half, cnt,
-                     dst0, dst1);
+  hipLaunchKernelGGL(carve_param_reduce_kernel, dim3(blocks, 2), dim3(64 * kReduceGroups), 0, s, partU, npartU, partV,
+                     npartV, half, cnt, dU0, dU1, dV0, dV1);
   return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
 }
 

@@ -370,17 +370,23 @@ int launch_sync_clear(int* sync, size_t n, hipStream_t s);
 size_t bwd_lds_bytes(int dtype, int D, int LW, int RP);
 // ints of the synchronisation area: one ready flag per chunk, the ticket
 // counter that assigns the workgroup roles, the wait-timeout word (nonzero once
-// an adjoint wave's bounded wait for a record ran out), padding
-__host__ __device__ constexpr size_t sync_ints(size_t nbh, size_t nch) { return nbh * nch + 4; }
+// an adjoint wave's bounded wait for a record ran out), padding, then per
+// (batch, head) the adjoint's position (chunks it has started, counted from the
+// last), which paces the recompute
+__host__ __device__ constexpr size_t sync_ints(size_t nbh, size_t nch) { return nbh * nch + 4 + nbh; }
+__host__ __device__ constexpr size_t sync_ticket(size_t nbh, size_t nch) { return nbh * nch; }
 __host__ __device__ constexpr size_t sync_timeout_word(size_t nbh, size_t nch) { return nbh * nch + 1; }
+__host__ __device__ constexpr size_t sync_adjoint_pos(size_t nbh, size_t nch) { return nbh * nch + 4; }
 // default bound of that wait, in polls (carve_bwd.h)
 constexpr int kReadySpinLimit = 1 << 20;
 // sw: the scalar write gate (dVb, dUb only; the records hold RP fold rows)
 int launch_bwd_vparam(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s);
 int launch_bwd_uparam(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s);
-// sum nparts records of 2 * half floats into dst0 (first half) and dst1; with
-// dst1 == NULL only the first half is summed
-int launch_param_reduce(const float* part, int nparts, size_t half, float* dst0, float* dst1, hipStream_t s);
+// in one launch: sum npartU records of 2 * half floats at partU into dU0 (first
+// half) and dU1, and npartV records at partV into dV0 and dV1; with dU1 == dV1
+// == NULL only the first halves are summed
+int launch_param_reduce(const float* partU, int npartU, const float* partV, int npartV, size_t half, float* dU0,
+                        float* dU1, float* dV0, float* dV1, hipStream_t s);
 // kVarAct: turn dq, dk (gradients of the activated q, k, in place, [rows][D]) into
 // the gradients of the raw projections q_raw, k_raw
 int launch_act_bwd(const void* q_raw, const void* k_raw, void* dq, void* dk, size_t rows, int D, int dtype,
