@@ -56,11 +56,16 @@ int check_dims(const carve_dims_t* d) {
   return CARVE_OK;
 }
 
-// largest recompute sub-chunk (<= 64 tokens, dividing L) for which the LDS
-// layout of the fused recompute + adjoint launch fits
+// largest recompute sub-chunk (<= 32 tokens, dividing L) for which the LDS
+// layout of the fused recompute + adjoint launch fits.  32-token sub-chunks
+// keep the recompute's registers within the file (64-token ones spill 64 of
+// them) and recompute fastest: measured against 64 and 16 tokens, the fused
+// launch took 1.32 against 1.49 and 1.41 ms at B = 8, H = 16, T = 2048 (where
+// the recompute bounds it) and 1.885 against 1.90 and 1.884 ms at the
+// 1.3B-scale T = 4096 layer (where the adjoint does)
 int pick_lw(const carve_dims_t* d) {
   const int RP = round_rp(d->R);
-  for (int lw = 64; lw >= 16; lw /= 2) {
+  for (int lw = 32; lw >= 16; lw /= 2) {
     if (lw > d->L || d->L % lw) continue;
     if (bwd_lds_bytes(d->dtype, d->Dk, lw, RP) <= kMaxLds) return lw;
   }

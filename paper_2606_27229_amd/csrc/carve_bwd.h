@@ -982,7 +982,6 @@ template <typename T, int D, int RP, int VAR>
 static int launch_fused_l(const FwdArgs& f, const BwdArgs& a, int* sync, int cus, int LW, hipStream_t s) {
   if (LW == 16) return launch_fused_t<T, D, 16, RP, VAR>(f, a, sync, cus, s);
   if (LW == 32) return launch_fused_t<T, D, 32, RP, VAR>(f, a, sync, cus, s);
-  if (LW == 64) return launch_fused_t<T, D, 64, RP, VAR>(f, a, sync, cus, s);
   return CARVE_ERR_UNSUPPORTED;
 }
 

@@ -175,7 +175,6 @@ template <typename T, int D, int RP>
 static size_t fused_lds_l(int LW) {
   if (LW == 16) return fused_lds<T, D, 16, RP, 0>();
   if (LW == 32) return fused_lds<T, D, 32, RP, 0>();
-  if (LW == 64) return fused_lds<T, D, 64, RP, 0>();
   return (size_t)-1;
 }
 
