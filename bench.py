@@ -407,10 +407,10 @@ def main():
         bwd()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    # launch-boundary events recorded by the library: forward 1 kernel, backward 5
-    # (6 with the gate-in-kernel decay: the reduction of dA, dtau; or with the
+    # launch-boundary events recorded by the library: forward 1 kernel, backward 4
+    # (5 with the gate-in-kernel decay: the reduction of dA, dtau; or with the
     # input activations: their backward)
-    NF, NB = 2, (7 if (gated or act) else 6)
+    NF, NB = 2, (6 if (gated or act) else 5)
     ev_f = [[torch.cuda.Event(enable_timing=True) for _ in range(NF)] for _ in range(args.steps)]
     ev_b = [[torch.cuda.Event(enable_timing=True) for _ in range(NB)] for _ in range(args.steps)]
     if norm:
@@ -444,8 +444,8 @@ def main():
     def avg(rows, i):
         return sum(r[i].elapsed_time(r[i + 1]) for r in rows) / len(rows)
 
-    bwd_names = ["carve_sync_clear_kernel", "carve_bwd_fused_kernel", "carve_bwd_vparam_kernel",
-                 "carve_bwd_uparam_kernel", "carve_param_reduce_kernel"]
+    bwd_names = ["carve_sync_clear_kernel", "carve_bwd_fused_kernel", "carve_bwd_param_kernel",
+                 "carve_param_reduce_kernel"]
     if gated:
         bwd_names.append("carve_gate_reduce_kernel")
     if act:

@@ -333,28 +333,25 @@ int bwd_impl(const carve_dims_t* d, const void* q, const void* k, const void* v,
   st = launch_bwd_fused(f, a, sync, cus, d->dtype, d->Dk, lw, variant_of(dc, sw, act), stream);
   if (st) return st;
   prof_mark(stream);
-  // 3. dVb, dVw from dbx, dwx and tau (dVb only with the scalar write gate)
-  st = launch_bwd_vparam(a, d->dtype, d->Dk, sw, stream);
+  // 3. in one launch: d[Ub; Uw] from the per-chunk dF, dVb, dVw from dbx, dwx
+  //    and tau (dUb, dVb only with the scalar write gate)
+  st = launch_bwd_param(a, d->dtype, d->Dk, sw, stream);
   if (st) return st;
   prof_mark(stream);
-  // 4. d[Ub; Uw] from the per-chunk dF (dUb only with the scalar write gate)
-  st = launch_bwd_uparam(a, d->dtype, d->Dk, sw, stream);
-  if (st) return st;
-  prof_mark(stream);
-  // 5. fixed-order reductions of the partials
+  // 4. fixed-order reductions of the partials
   const int nbh = d->B * d->H;
   const size_t RD = (size_t)d->R * d->Dk;
   st = launch_param_reduce(a.part, nbh * kUSplit, a.partV, nbh * kVSplit, RD, dUb, sw ? nullptr : dUw, dVb,
                            sw ? nullptr : dVw, stream);
   if (st) return st;
   prof_mark(stream);
-  // 6. (gated) dA, dtau summed over the batch
+  // 5. (gated) dA, dtau summed over the batch
   if (dc.gated()) {
     st = launch_gate_reduce(a.partG, d->B, d->H, d->Dk, dd.dA, dd.dtau, stream);
     if (st) return st;
     prof_mark(stream);
   }
-  // 7. (input activations) dq, dk through the L2 normalisation and SiLU
+  // 6. (input activations) dq, dk through the L2 normalisation and SiLU
   if (act) {
     st = launch_act_bwd(q, k, dq, dk, (size_t)d->B * d->T * d->H, d->Dk, d->dtype, stream);
     prof_mark(stream);

@@ -14,11 +14,10 @@
 //      walk the chunks and their 16-token blocks in reverse, carry the state
 //      gradient and wait for a chunk's flag before reading its record, so the
 //      recompute runs on the compute units the adjoint leaves idle, ahead of it;
-//   3. carve_bwd_vparam_kernel: dVb, dVw from dbx, dwx and tau, split over
-//      tokens;
-//   4. carve_bwd_uparam_kernel: d[Ub; Uw] from the per-chunk dF (parked in the
-//      chunk records by step 2) and the chunk start states, split over chunks;
-//   5. carve_param_reduce_kernel: fixed-order sums of the parameter partials,
+//   3. carve_bwd_param_kernel: d[Ub; Uw] from the per-chunk dF (parked in the
+//      chunk records by step 2) and the chunk start states, split over
+//      chunks, and dVb, dVw from dbx, dwx and tau, split over tokens;
+//   4. carve_param_reduce_kernel: fixed-order sums of the parameter partials,
 //      so reruns are bitwise identical.
 //
 // Adjoint of one 16-token block (wave w owns value tile w and key tile w; the
@@ -828,7 +827,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
     CARVE_BWD_BQ();
 
     // ---- glue: dS += [Ub; Uw]^T dF; dF is parked in the chunk record for
-    // d[Ub; Uw] += dF S_hat^T (carve_bwd_uparam_kernel).  dF enters the product
+    // d[Ub; Uw] += dF S_hat^T (carve_bwd_param_kernel).  dF enters the product
     // as a high and a low part so that its f32 accumulation is not rounded away.
     {
       constexpr int LDF = R2 + 4;   // row stride of the dF parts (LDS layout)

@@ -5,18 +5,17 @@
 
 namespace carve {
 
-// The parameter-gradient partials as launches of their own (one item per
-// workgroup), used when the fused launch does not run them itself.
+// The parameter-gradient partials in one launch, one item per workgroup: the
+// d[Ub; Uw] items (the heavier ones) first, then the dVb, dVw items, so that
+// the second kind fills the compute units the first leaves at its tail.
 template <typename T, int D, int RP, bool SW>
-__global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_uparam_kernel(BwdArgs a) {
+__global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_param_kernel(BwdArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  uparam_item<T, D, RP, SW>(a, blockIdx.x, smem);
-}
-
-template <typename T, int D, int RP, bool SW>
-__global__ void __launch_bounds__(bwd_threads(D)) carve_bwd_vparam_kernel(BwdArgs a) {
-  extern __shared__ __attribute__((aligned(16))) char smem[];
-  vparam_item<T, D, RP, SW>(a, blockIdx.x, smem);
+  const int nu = a.B * a.H * kUSplit;
+  if ((int)blockIdx.x < nu)
+    uparam_item<T, D, RP, SW>(a, blockIdx.x, smem);
+  else
+    vparam_item<T, D, RP, SW>(a, blockIdx.x - nu, smem);
 }
 
 // Sum nparts partial records (2 * half floats each) in a fixed order: thread
@@ -196,70 +195,41 @@ size_t bwd_lds_bytes(int dtype, int D, int LW, int RP) {
   return dtype == CARVE_BF16 ? fused_lds_d<bf16_t>(D, LW, RP) : fused_lds_d<float>(D, LW, RP);
 }
 
-template <typename T, int D, int RP>
-static int launch_vparam_t(const BwdArgs& a, bool sw, hipStream_t s) {
-  if (sw)
-    hipLaunchKernelGGL((carve_bwd_vparam_kernel<T, D, RP, true>), dim3(a.B * a.H * kVSplit), dim3(bwd_threads(D)),
-                       (vparam_lds<T, D, RP, true>()), s, a);
-  else
-    hipLaunchKernelGGL((carve_bwd_vparam_kernel<T, D, RP, false>), dim3(a.B * a.H * kVSplit), dim3(bwd_threads(D)),
-                       (vparam_lds<T, D, RP, false>()), s, a);
-  return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
-}
-
-template <typename T>
-static int launch_vparam_d(const BwdArgs& a, int D, bool sw, hipStream_t s) {
-  if (a.RP == 32) {
-    if (D == 32) return launch_vparam_t<T, 32, 32>(a, sw, s);
-    if (D == 64) return launch_vparam_t<T, 64, 32>(a, sw, s);
-    if (D == 128) return launch_vparam_t<T, 128, 32>(a, sw, s);
-  } else if (a.RP == 64) {
-    if (D == 32) return launch_vparam_t<T, 32, 64>(a, sw, s);
-    if (D == 64) return launch_vparam_t<T, 64, 64>(a, sw, s);
-    if (D == 128) return launch_vparam_t<T, 128, 64>(a, sw, s);
-  }
-  return CARVE_ERR_UNSUPPORTED;
-}
-
-int launch_bwd_vparam(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s) {
-  if (dtype == CARVE_BF16) return launch_vparam_d<bf16_t>(a, D, sw, s);
-  return launch_vparam_d<float>(a, D, sw, s);
-}
-
 template <typename T, int D, int RP, bool SW>
-static int launch_uparam_s(const BwdArgs& a, hipStream_t s) {
-  constexpr size_t lds = uparam_lds<T, D, SW ? RP : 2 * RP>();
+static int launch_param_s(const BwdArgs& a, hipStream_t s) {
+  constexpr size_t lu = uparam_lds<T, D, SW ? RP : 2 * RP>(), lv = vparam_lds<T, D, RP, SW>();
+  constexpr size_t lds = lu > lv ? lu : lv;
   if constexpr (lds > 64 * 1024) {
     return CARVE_ERR_UNSUPPORTED;   // only shapes the fused launch rejects first
   } else {
-    hipLaunchKernelGGL((carve_bwd_uparam_kernel<T, D, RP, SW>), dim3(a.B * a.H * kUSplit), dim3(bwd_threads(D)), lds,
-                       s, a);
+    hipLaunchKernelGGL((carve_bwd_param_kernel<T, D, RP, SW>), dim3(a.B * a.H * (kUSplit + kVSplit)),
+                       dim3(bwd_threads(D)), lds, s, a);
     return hipGetLastError() == hipSuccess ? CARVE_OK : CARVE_ERR_HIP;
   }
 }
 
 template <typename T, int D, int RP>
-static int launch_uparam_t(const BwdArgs& a, bool sw, hipStream_t s) {
-  return sw ? launch_uparam_s<T, D, RP, true>(a, s) : launch_uparam_s<T, D, RP, false>(a, s);
+static int launch_param_t(const BwdArgs& a, bool sw, hipStream_t s) {
+  return sw ? launch_param_s<T, D, RP, true>(a, s) : launch_param_s<T, D, RP, false>(a, s);
 }
 
 template <typename T>
-static int launch_uparam_d(const BwdArgs& a, int D, bool sw, hipStream_t s) {
+static int launch_param_d(const BwdArgs& a, int D, bool sw, hipStream_t s) {
   if (a.RP == 32) {
-    if (D == 32) return launch_uparam_t<T, 32, 32>(a, sw, s);
-    if (D == 64) return launch_uparam_t<T, 64, 32>(a, sw, s);
-    if (D == 128) return launch_uparam_t<T, 128, 32>(a, sw, s);
+    if (D == 32) return launch_param_t<T, 32, 32>(a, sw, s);
+    if (D == 64) return launch_param_t<T, 64, 32>(a, sw, s);
+    if (D == 128) return launch_param_t<T, 128, 32>(a, sw, s);
   } else if (a.RP == 64) {
-    if (D == 32) return launch_uparam_t<T, 32, 64>(a, sw, s);
-    if (D == 64) return launch_uparam_t<T, 64, 64>(a, sw, s);
-    if (D == 128) return launch_uparam_t<T, 128, 64>(a, sw, s);
+    if (D == 32) return launch_param_t<T, 32, 64>(a, sw, s);
+    if (D == 64) return launch_param_t<T, 64, 64>(a, sw, s);
+    if (D == 128) return launch_param_t<T, 128, 64>(a, sw, s);
   }
   return CARVE_ERR_UNSUPPORTED;
 }
 
-int launch_bwd_uparam(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s) {
-  if (dtype == CARVE_BF16) return launch_uparam_d<bf16_t>(a, D, sw, s);
-  return launch_uparam_d<float>(a, D, sw, s);
+int launch_bwd_param(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s) {
+  if (dtype == CARVE_BF16) return launch_param_d<bf16_t>(a, D, sw, s);
+  return launch_param_d<float>(a, D, sw, s);
 }
 
 int launch_param_reduce(const float* partU, int npartU, const float* partV, int npartV, size_t half, float* dU0,

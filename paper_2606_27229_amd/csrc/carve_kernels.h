@@ -379,9 +379,10 @@ __host__ __device__ constexpr size_t sync_timeout_word(size_t nbh, size_t nch) {
 __host__ __device__ constexpr size_t sync_adjoint_pos(size_t nbh, size_t nch) { return nbh * nch + 4; }
 // default bound of that wait, in polls (carve_bwd.h)
 constexpr int kReadySpinLimit = 1 << 20;
-// sw: the scalar write gate (dVb, dUb only; the records hold RP fold rows)
-int launch_bwd_vparam(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s);
-int launch_bwd_uparam(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s);
+// d[Ub; Uw] over chunk splits and dVb, dVw over token splits (carve_param.h),
+// one launch; sw: the scalar write gate (dVb, dUb only; the records hold RP
+// fold rows)
+int launch_bwd_param(const BwdArgs& a, int dtype, int D, bool sw, hipStream_t s);
 // in one launch: sum npartU records of 2 * half floats at partU into dU0 (first
 // half) and dU1, and npartV records at partV into dV0 and dV1; with dU1 == dV1
 // == NULL only the first halves are summed
