@@ -855,7 +855,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         }
         dSt[jt] = acc;
       }
-      __syncthreads();
+      // (no barrier: the next block writes sdSx only after its first barrier,
+      // and what it stages before that barrier does not overlap the dF parts)
     }
     }
   }  // blocks (reverse)
