@@ -227,9 +227,10 @@ __device__ __forceinline__ float row_shl1(float x, float fill) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, fill), __builtin_bit_cast(int, x),
                                                                0x101, 0xf, 0xf, false));
 }
-// x of lane 15 of the row, in every lane of the row
+// x of lane 15 of the row, in every lane of the row (every lane is written, so
+// no old value is needed)
 __device__ __forceinline__ float row_bcast15(float x) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x15F, 0xf, 0xf, false));
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x15F, 0xf, 0xf, false));
 }
 // x of the neighbouring lane (lane ^ 1)
 __device__ __forceinline__ float lane_xor1(float x) {
@@ -294,15 +295,18 @@ __device__ __forceinline__ void store_tile_t(float* buf, int ld, int r0, int c0,
 __device__ __forceinline__ float fast_exp(float x) { return __expf(x); }
 __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 __device__ __forceinline__ float sigmoid_f(float z) { return fast_rcp(1.0f + fast_exp(-z)); }
+// natural log of x in [1, 2]: the hardware log2 and one product (no range
+// reduction or denormal scaling is needed there)
+__device__ __forceinline__ float log_1to2(float x) { return __builtin_amdgcn_logf(x) * 0.693147180559945f; }
 // log(1 + e^z) without overflow
 __device__ __forceinline__ float softplus_f(float z) {
-  return fmaxf(z, 0.0f) + __logf(1.0f + fast_exp(-fabsf(z)));
+  return fmaxf(z, 0.0f) + log_1to2(1.0f + fast_exp(-fabsf(z)));
 }
 // softplus(z) = log(1 + e^z) and sigmoid(z) from one exponential
 __device__ __forceinline__ void softplus_sigmoid(float z, float& sp, float& sig) {
   const float e = fast_exp(-fabsf(z));
   const float r = fast_rcp(1.0f + e);
-  sp = fmaxf(z, 0.0f) + __logf(1.0f + e);
+  sp = fmaxf(z, 0.0f) + log_1to2(1.0f + e);
   sig = z >= 0.0f ? r : e * r;
 }
 // tanh with a short odd series near 0 (the exp form cancels there)
