@@ -375,16 +375,20 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
 
     // ---- fold F^T[j][r] = sum_v S_hat[v][j] U[r][v] (key tile w) --------------
     if (cstart) {
-      for (int rt = 0; rt < NRT; ++rt) {
-        f32x4 acc = zero4();
-        for (int vp = 0; vp < D / 32; ++vp) {
-          const quad a0 = Qd::ld_tr_sw(sS, LDD, 32 * vp, 16 * w, g, c);
-          const quad a1 = Qd::ld_tr_sw(sS, LDD, 32 * vp + 16, 16 * w, g, c);
+      // the state's column block (this wave's key tile) is read once per
+      // 32-value step and serves every fold row tile
+      f32x4 acc[NRT];
+      for (int rt = 0; rt < NRT; ++rt) acc[rt] = zero4();
+      for (int vp = 0; vp < D / 32; ++vp) {
+        const quad a0 = Qd::ld_tr_sw(sS, LDD, 32 * vp, 16 * w, g, c);
+        const quad a1 = Qd::ld_tr_sw(sS, LDD, 32 * vp + 16, 16 * w, g, c);
+        for (int rt = 0; rt < NRT; ++rt) {
           const T* ur = sU + (16 * rt + c) * LDD + 32 * vp + ((4 * g) ^ CARVE_QX(c));
-          acc = Qd::mma32(a0, a1, Qd::ld(ur), Qd::ld(ur + 16), acc);
+          acc[rt] = Qd::mma32(a0, a1, Qd::ld(ur), Qd::ld(ur + 16), acc[rt]);
         }
-        Qd::st(sF + (16 * rt + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c)), Qd::cvt(acc));
       }
+      for (int rt = 0; rt < NRT; ++rt)
+        Qd::st(sF + (16 * rt + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c)), Qd::cvt(acc[rt]));
       __syncthreads();
     }
     // raw erase logits into region X (the fold is done with the state)
@@ -397,16 +401,36 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     }
 
     // ---- tau^T[r][t] = tanh(F[r] . q_t) -> sTau[t][r] ---------------------------
-    for (int x = w; x < NRT * NB; x += NW) {
-      const int rt = x % NRT, bb = x / NRT;
-      f32x4 acc = zero4();
+    if constexpr (NW % NRT == 0) {
+      // every tile of this wave has the same fold rows: read them once
+      const int rt = w % NRT;
+      quad fq[D / 16];
       for (int jp = 0; jp < D / 32; ++jp) {
         const T* fr = sF + (16 * rt + c) * LDD + 32 * jp + ((4 * g) ^ CARVE_QX(c));
-        const T* qr = sQ + (16 * bb + c) * LDD + 32 * jp + ((4 * g) ^ CARVE_QX(c));
-        acc = Qd::mma32(Qd::ld(fr), Qd::ld(fr + 16), Qd::ld(qr), Qd::ld(qr + 16), acc);
+        fq[2 * jp] = Qd::ld(fr);
+        fq[2 * jp + 1] = Qd::ld(fr + 16);
       }
-      for (int e = 0; e < 4; ++e) acc[e] = tanh_f(acc[e]);
-      Qd::st(sTau + (16 * bb + c) * LDR + 16 * rt + ((4 * g) ^ CARVE_QX(c)), Qd::cvt(acc));
+      for (int bb = w / NRT; bb < NB; bb += NW / NRT) {
+        f32x4 acc = zero4();
+        for (int jp = 0; jp < D / 32; ++jp) {
+          const T* qr = sQ + (16 * bb + c) * LDD + 32 * jp + ((4 * g) ^ CARVE_QX(c));
+          acc = Qd::mma32(fq[2 * jp], fq[2 * jp + 1], Qd::ld(qr), Qd::ld(qr + 16), acc);
+        }
+        for (int e = 0; e < 4; ++e) acc[e] = tanh_f(acc[e]);
+        Qd::st(sTau + (16 * bb + c) * LDR + 16 * rt + ((4 * g) ^ CARVE_QX(c)), Qd::cvt(acc));
+      }
+    } else {
+      for (int x = w; x < NRT * NB; x += NW) {
+        const int rt = x % NRT, bb = x / NRT;
+        f32x4 acc = zero4();
+        for (int jp = 0; jp < D / 32; ++jp) {
+          const T* fr = sF + (16 * rt + c) * LDD + 32 * jp + ((4 * g) ^ CARVE_QX(c));
+          const T* qr = sQ + (16 * bb + c) * LDD + 32 * jp + ((4 * g) ^ CARVE_QX(c));
+          acc = Qd::mma32(Qd::ld(fr), Qd::ld(fr + 16), Qd::ld(qr), Qd::ld(qr + 16), acc);
+        }
+        for (int e = 0; e < 4; ++e) acc[e] = tanh_f(acc[e]);
+        Qd::st(sTau + (16 * bb + c) * LDR + 16 * rt + ((4 * g) ^ CARVE_QX(c)), Qd::cvt(acc));
+      }
     }
     __syncthreads();
 
