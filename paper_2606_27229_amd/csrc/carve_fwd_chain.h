@@ -510,9 +510,14 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       f32x4 x;
       for (int e = 0; e < 4; ++e) {
         const float lend = row_bcast15(lam[NB - 1][e]);
-        float xw = 0.0f;
-        for (int i = 0; i < NB; ++i) xw = fmaf(tc[i], row_bcast15(lam[i][e]), xw);
-        x[e] = fast_exp(wch[e] ? xw : tn * lend);
+        float xe = tn * lend;
+        if (wave_wide) {
+          // (the per-tile forms only where a channel of this wave needs them)
+          float xw = 0.0f;
+          for (int i = 0; i < NB; ++i) xw = fmaf(tc[i], row_bcast15(lam[i][e]), xw);
+          xe = wch[e] ? xw : xe;
+        }
+        x[e] = fast_exp(xe);
         fill[e] = fast_exp(-0.5f * lend);
       }
       if (c < NTAB) *reinterpret_cast<f32x4*>(sTab + c * D + 16 * w + 4 * g) = x;
