@@ -294,6 +294,12 @@ __device__ __forceinline__ void store_tile_t(float* buf, int ld, int r0, int c0,
 // ---- elementwise math (f32, hardware exp2/log2/rcp) -----------------------
 __device__ __forceinline__ float fast_exp(float x) { return __expf(x); }
 __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+// e^x and e^-x from one scaling to base 2 (each the same value fast_exp gives)
+__device__ __forceinline__ void exp_pm(float x, float& ep, float& em) {
+  const float y = x * 1.44269504088896341f;
+  ep = __builtin_amdgcn_exp2f(y);
+  em = __builtin_amdgcn_exp2f(-y);
+}
 __device__ __forceinline__ float sigmoid_f(float z) { return fast_rcp(1.0f + fast_exp(-z)); }
 // natural log of x in [1, 2]: the hardware log2 and one product (no range
 // reduction or denormal scaling is needed there)

@@ -542,8 +542,8 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
         f0 = wch[e] ? eb : f0;                                                                     \
         cprev[e] = ce;                                                                             \
       }                                                                                            \
-      const float E = fast_exp(lam[bb][e] - m);                                                    \
-      const float Ei = fast_exp(m - lam[bb][e]);                                                   \
+      float E, Ei;                                                                                 \
+      exp_pm(lam[bb][e] - m, E, Ei);                                                               \
       kt[e] = kv[e] * row_shr1(E, f0);                                                             \
       qt[e] = qv[e] * E;                                                                           \
       ki[e] = kv[e] * Ei;                                                                          \
