@@ -294,13 +294,21 @@ __device__ __forceinline__ void store_tile_t(float* buf, int ld, int r0, int c0,
 // ---- elementwise math (f32, hardware exp2/log2/rcp) -----------------------
 __device__ __forceinline__ float fast_exp(float x) { return __expf(x); }
 __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
-// e^x and e^-x from one scaling to base 2 (each the same value fast_exp gives)
-__device__ __forceinline__ void exp_pm(float x, float& ep, float& em) {
-  const float y = x * 1.44269504088896341f;
+__device__ __forceinline__ float sigmoid_f(float z) { return fast_rcp(1.0f + fast_exp(-z)); }
+// base-2 forms for code that keeps log retentions in units of log 2 (every
+// exponential then is one hardware exp2, with no scaling product)
+constexpr float kLog2e = 1.44269504088896341f;
+__device__ __forceinline__ float exp2_f(float y) { return __builtin_amdgcn_exp2f(y); }
+// 2^y and 2^-y
+__device__ __forceinline__ void exp2_pm(float y, float& ep, float& em) {
   ep = __builtin_amdgcn_exp2f(y);
   em = __builtin_amdgcn_exp2f(-y);
 }
-__device__ __forceinline__ float sigmoid_f(float z) { return fast_rcp(1.0f + fast_exp(-z)); }
+// softplus(z) / log 2 = log2(1 + e^z) without overflow (the log2 argument is
+// in [1, 2])
+__device__ __forceinline__ float softplus2_f(float z) {
+  return fmaf(fmaxf(z, 0.0f), kLog2e, __builtin_amdgcn_logf(1.0f + __builtin_amdgcn_exp2f(-fabsf(z) * kLog2e)));
+}
 // natural log of x in [1, 2]: the hardware log2 and one product (no range
 // reduction or denormal scaling is needed there)
 __device__ __forceinline__ float log_1to2(float x) { return __builtin_amdgcn_logf(x) * 0.693147180559945f; }

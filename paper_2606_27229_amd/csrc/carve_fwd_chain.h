@@ -436,7 +436,9 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
 
     // ---- gates ------------------------------------------------------------------
     // key side, key tile w: lane (g, c) of tile bb holds token 16 bb + c and keys
-    // j = 16 w + 4 g + e; prefix sums run along the 16 lanes of a row
+    // j = 16 w + 4 g + e; prefix sums run along the 16 lanes of a row.  Log
+    // retentions are kept in units of log 2 here (lam below is lam / log 2), so
+    // that every exponential of this step is one exp2.
     f32x4 lam[NB];
     {
       f32x4 carry = zero4();
@@ -450,13 +452,14 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
           const f32x4 fv = Qd::f32(pf[bb]);
           const f32x4 na = *reinterpret_cast<const f32x4*>(sGate + 16 * w + 4 * g);
           const f32x4 tf = *reinterpret_cast<const f32x4*>(sGate + D + 16 * w + 4 * g);
-          for (int e = 0; e < 4; ++e) gv[e] = na[e] * softplus_f(fv[e] + tf[e]);
+          for (int e = 0; e < 4; ++e) gv[e] = na[e] * softplus2_f(fv[e] + tf[e]);   // g / log 2
         } else {
           gv = pg[bb];
         }
         for (int e = 0; e < 4; ++e) {
-          const float ell = gv[e] - softplus_f(z[e] + bxv[e]);
-          lam[bb][e] = carry[e] + row_scan(ell);
+          const float sp = softplus2_f(z[e] + bxv[e]);
+          const float ell = GATED ? gv[e] - sp : fmaf(gv[e], kLog2e, -sp);
+          lam[bb][e] = bb == 0 ? row_scan(ell) : carry[e] + row_scan(ell);
           carry[e] = row_bcast15(lam[bb][e]);
         }
       }
@@ -469,7 +472,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       bool wch[4];
       bool mine = false;
       for (int e = 0; e < 4; ++e) {
-        wch[e] = NB > 1 && row_bcast15(lam[NB - 1][e]) < -kWideLog;
+        wch[e] = NB > 1 && row_bcast15(lam[NB - 1][e]) < -kWideLog * kLog2e;
         mine = mine || wch[e];
       }
       const bool wave_wide = __any(mine) != 0;
@@ -517,13 +520,14 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
           for (int i = 0; i < NB; ++i) xw = fmaf(tc[i], row_bcast15(lam[i][e]), xw);
           xe = wch[e] ? xw : xe;
         }
-        x[e] = fast_exp(xe);
-        fill[e] = fast_exp(-0.5f * lend);
+        x[e] = exp2_f(xe);
+        fill[e] = exp2_f(-0.5f * lend);
       }
       if (c < NTAB) *reinterpret_cast<f32x4*>(sTab + c * D + 16 * w + 4 * g) = x;
       // decayed operands of the key tile: Kt = k e^{lam_{t-1} - m}, Qt = q e^{lam - m},
-      // Ki = k e^{m - lam}; PER_CHANNEL_: the channels flagged in wch take per-tile
-      // references (the branch is taken by waves with such a channel)
+      // Ki = k e^{m - lam} (each one exp2 of the scaled exponents); PER_CHANNEL_:
+      // the channels flagged in wch take per-tile references (the branch is
+      // taken by waves with such a channel)
 #define CARVE_GATE_OPERANDS(PER_CHANNEL_)                                                          \
   for (int bb = 0; bb < NB; ++bb) {                                                                \
     T* kp = sKi + (16 * bb + c) * LDD + 16 * w + ((4 * g) ^ CARVE_QX(c));                          \
@@ -537,13 +541,13 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
         /* per-tile reference: e^{c_{bb-1} - m} = e^{m - c_bb} */                                  \
         const float ce = row_bcast15(lam[bb][e]);                                                  \
         const float mt = 0.5f * (cprev[e] + ce);                                                   \
-        const float eb = row_bcast15(fast_exp(mt - lam[bb][e]));                                    \
+        const float eb = row_bcast15(exp2_f(mt - lam[bb][e]));                                      \
         m = wch[e] ? mt : m;                                                                       \
         f0 = wch[e] ? eb : f0;                                                                     \
         cprev[e] = ce;                                                                             \
       }                                                                                            \
       float E, Ei;                                                                                 \
-      exp_pm(lam[bb][e] - m, E, Ei);                                                               \
+      exp2_pm(lam[bb][e] - m, E, Ei);                                                              \
       kt[e] = kv[e] * row_shr1(E, f0);                                                             \
       qt[e] = qv[e] * E;                                                                           \
       ki[e] = kv[e] * Ei;                                                                          \
