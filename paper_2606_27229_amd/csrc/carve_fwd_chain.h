@@ -617,6 +617,9 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     // (all waves when each has a diagonal tile) the off-diagonal ones.
     constexpr int NDW = NB < NW ? NB : NW;
     constexpr int NOW = NW > NDW ? NW - NDW : NW;   // off-diagonal workers
+    // The off-diagonal workers carry the step's longest chains: they take issue
+    // priority over the diagonal-inverse wave on their SIMD until the barrier.
+    if (NOW < NW && w < NOW) __builtin_amdgcn_s_setprio(2);
     if (w >= NW - NDW) {
       typedef Quad<float> Qf;
       for (int i = NW - 1 - w; i < NB; i += NDW) {
@@ -728,6 +731,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
         for (int e = 0; e < 4; ++e) RH[bb][e] = bt[e] * (wv[bb][e] - xk[e]);
       }
     }
+    __builtin_amdgcn_s_setprio(0);
     __syncthreads();
 
     // ---- value tile: blocked substitution for u, outputs, state carry ---------------
