@@ -564,8 +564,12 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       }
 #undef CARVE_GATE_OPERANDS
     }
-    // value side, value tile w: rows t = 16 bb + 4 g + e, column v = 16 w + c
-    f32x4 wv[NB];
+    // value side, value tile w: rows t = 16 bb + 4 g + e, column v = 16 w + c.
+    // The operand quads are taken here (the staged rows share LDS with the
+    // coupling tiles); the write gate w and w * v are formed after the barrier,
+    // at the start of the coupling step: the gate step is bound by the SIMDs'
+    // VALU issue, the coupling step by its matrix-core and LDS chains.
+    quad vqs[NB], wxqs[NB];
     for (int bb = 0; bb < NB; ++bb) {
       quad vq = pv[bb], wxq;
       if constexpr (!SW) wxq = pwx[bb];
@@ -578,18 +582,8 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       } else if constexpr (ACT) {
         vq = Qd::cvt(silu4(Qd::f32(vq)));
       }
-      const f32x4 vv = Qd::mma16(vq, fI, zero4());
-      if constexpr (SW) {
-        // one gate per token: rows t = 16 bb + 4 g + e
-        const f32x4 ws = *reinterpret_cast<const f32x4*>(sWs + par * WB + 16 * bb + 4 * g);
-        for (int e = 0; e < 4; ++e) wv[bb][e] = ws[e] * vv[e];
-      } else {
-        f32x4 z = zero4();
-        for (int ks = 0; ks < NRB; ++ks)
-          z = Qd::mma16(Qd::ld(sTau + (16 * bb + c) * LDR + RP + 16 * ks + ((4 * g) ^ CARVE_QX(c))), fVw[ks], z);
-        z = Qd::mma16(wxq, fI, z);                     // + wx, moved into this layout
-        for (int e = 0; e < 4; ++e) wv[bb][e] = sigmoid_f(z[e]) * vv[e];
-      }
+      vqs[bb] = vq;
+      if constexpr (!SW) wxqs[bb] = wxq;
     }
     {
       const int nx = blk + 1 < nblk ? blk + 1 : blk;
@@ -603,6 +597,22 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       int f = 0;
       for (int x = 0; x < NW; ++x) f |= sFlag[x];
       wide = __builtin_amdgcn_readfirstlane(f) != 0;
+    }
+    // w * v of each tile (the write gate from tau_w Vw^T + wx, or the token's
+    // scalar gate)
+    f32x4 wv[NB];
+    for (int bb = 0; bb < NB; ++bb) {
+      const f32x4 vv = Qd::mma16(vqs[bb], fI, zero4());
+      if constexpr (SW) {
+        const f32x4 ws = *reinterpret_cast<const f32x4*>(sWs + par * WB + 16 * bb + 4 * g);
+        for (int e = 0; e < 4; ++e) wv[bb][e] = ws[e] * vv[e];
+      } else {
+        f32x4 z = zero4();
+        for (int ks = 0; ks < NRB; ++ks)
+          z = Qd::mma16(Qd::ld(sTau + (16 * bb + c) * LDR + RP + 16 * ks + ((4 * g) ^ CARVE_QX(c))), fVw[ks], z);
+        z = Qd::mma16(wxqs[bb], fI, z);                // + wx, moved into this layout
+        for (int e = 0; e < 4; ++e) wv[bb][e] = sigmoid_f(z[e]) * vv[e];
+      }
     }
     CARVE_STORE_S(NJT / 2, NJT);
     CARVE_PREFETCH_G(blk + 1 < nblk ? blk + 1 : blk);
