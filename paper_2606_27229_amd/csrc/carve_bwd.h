@@ -695,7 +695,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         for (int i = 0; i < 4; ++i) {
           // dgam gam = gam (sum_v dS' S + sum_s Ki_s (dS'^T u_s)), reduced over s = the row
           const float ds = row_scan(kiM[i] * dKi[i]);
-          dgg[i] = gmj[i] * (__shfl(dgs, 4 * g + i) + __shfl(ds, (lane & 48) | 15));
+          dgg[i] = gmj[i] * (__shfl(dgs, 4 * g + i) + row_bcast15(ds));
           dKt[i] = -bc_ * dKt[i];
           dKi[i] *= gmj[i];
           const bool lowA = c < 4 * g + i, lowP = c <= 4 * g + i;
