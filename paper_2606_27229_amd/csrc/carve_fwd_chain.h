@@ -118,6 +118,11 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
                 LDB = fwd_qstride<T>(16);
   constexpr int NTA = NB * (NB - 1) / 2;   // off-diagonal tiles of A
   constexpr int NTP = NB * (NB + 1) / 2;   // tiles of P
+  // coupling step: NDW waves (one per SIMD) take the diagonal inverses, NOW
+  // waves the off-diagonal tiles (all waves when each has a diagonal tile)
+  constexpr int NDW = NB < NW ? NB : NW;
+  constexpr int NOW = NW > NDW ? NW - NDW : NW;
+  constexpr bool kSplitRoles = NOW < NW;
   static_assert(NW == NJT && NW >= 2, "one wave per 16-wide tile, at least two waves");
   static_assert(D % 32 == 0, "K32 steps over the key / value axis");
 
@@ -368,7 +373,10 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
       CARVE_PREFETCH_Q(nx);
     }
     __syncthreads();
-    CARVE_STORE_S(0, NJT / 2);
+    // the chunk start state goes out in two halves, the second during the
+    // coupling step; the off-diagonal workers, whose chains bound that step,
+    // store all of theirs here
+    CARVE_STORE_S(0, kSplitRoles && w < NOW ? NJT : NJT / 2);
     // raw keys of the block into free LDS (read by the gates)
     CARVE_STAGE_ROWS(sKi, ck, ACT);
     if constexpr (SVW) CARVE_STAGE_VW();
@@ -614,7 +622,7 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
         for (int e = 0; e < 4; ++e) wv[bb][e] = sigmoid_f(z[e]) * vv[e];
       }
     }
-    CARVE_STORE_S(NJT / 2, NJT);
+    if (!(kSplitRoles && w < NOW)) CARVE_STORE_S(NJT / 2, NJT);
     CARVE_PREFETCH_G(blk + 1 < nblk ? blk + 1 : blk);
     const float* bcur = sBeta + par * WB;
     // Diagonal 16 x 16 tiles: T_ii = (I + A_ii)^{-1}.  A_ii is strictly lower
@@ -625,11 +633,9 @@ __global__ void __launch_bounds__(fwd_threads(D)) carve_chain_fwd_kernel(FwdArgs
     // is held as its transpose in the result layout, so each power is formed
     // both ways.  NDW waves (one per SIMD) take the diagonal tiles, the others
     // (all waves when each has a diagonal tile) the off-diagonal ones.
-    constexpr int NDW = NB < NW ? NB : NW;
-    constexpr int NOW = NW > NDW ? NW - NDW : NW;   // off-diagonal workers
     // The off-diagonal workers carry the step's longest chains: they take issue
     // priority over the diagonal-inverse wave on their SIMD until the barrier.
-    if (NOW < NW && w < NOW) __builtin_amdgcn_s_setprio(2);
+    if (kSplitRoles && w < NOW) __builtin_amdgcn_s_setprio(2);
     if (w >= NW - NDW) {
       typedef Quad<float> Qf;
       for (int i = NW - 1 - w; i < NB; i += NDW) {
