@@ -404,6 +404,13 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       const T lbeta = pbeta, lws = pws;
       quad sbq[NJT];   // block start state, wave layout: S[16 w + c][16 jt + 4 g + e]
       for (int jt = 0; jt < NJT; ++jt) sbq[jt] = psbq[jt];
+      {
+        // S of the block into its own region now (the last block's key side,
+        // its only reader, ended two barriers ago); dS' waits for the first
+        // barrier (its region holds the glue's dF parts until then)
+        const int hx = SXH ? hswz128(c) : 0;
+        for (int jt = 0; jt < NJT; ++jt) Qd::st(sSx + (16 * w + c) * LDSX + ((16 * jt + 4 * g) ^ hx), sbq[jt]);
+      }
       u32x4 lstg[NSTG];
       for (int u = 0; u < NSTG; ++u) lstg[u] = pstg[u];
       const f32x4 lg_row = pg;   // a row vector of g (staged below)
@@ -553,7 +560,6 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         const int hx = SXH ? hswz128(c) : 0;
         for (int jt = 0; jt < NJT; ++jt) {
           const int o = (16 * w + c) * LDSX + ((16 * jt + 4 * g) ^ hx);
-          Qd::st(sSx + o, sbq[jt]);
           Qd::st(sdSx + o, Qd::cvt(dSt[jt]));
         }
       }
