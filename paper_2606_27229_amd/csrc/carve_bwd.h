@@ -171,7 +171,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   T* sP = reinterpret_cast<T*>(smem + lay.P);        // [16][LDB]    P of the block
   float* sGam = reinterpret_cast<float*>(smem + lay.Gam);      // [D] gam = e^{rho} of the block
   float* sBeta = reinterpret_cast<float*>(smem + lay.Beta);    // [16] beta, then [16] sigmoid(wx) (SW)
-  float* sDbeta = reinterpret_cast<float*>(smem + lay.Dbeta);  // [NW][16]
+  float* sDbeta = reinterpret_cast<float*>(smem + lay.Dbeta);  // [NW + 1][16]
   float* sDwx = reinterpret_cast<float*>(smem + lay.Dwx);      // [NW][16] (SW)
   float* sInv = reinterpret_cast<float*>(smem + lay.Inv);      // [2][16] 1/|SiLU(k)|, 1/|SiLU(q)| (ACT)
   T* sKt = reinterpret_cast<T*>(smem + lay.Kt);      // [16][LDK]    (quad-swizzled)
@@ -380,6 +380,12 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
     const quad qT_ = Qd::cvt(Qd::mma16(pqq, CARVE_FI(), zero4()));   /* q[t = 4g + i][j = 16 w + c] */ \
     for (int rt = 0; rt < NRT; ++rt) dF[rt] = Qd::mma16(Qd::ld_tr(sdY, LDR, 0, 16 * rt, g, c), qT_, dF[rt]); \
   } while (0)
+#define CARVE_BWD_GAM()                                                                       \
+  do {                                                                                        \
+    f32x4 gm_[NJT];                                                                           \
+    for (int jt_ = 0; jt_ < NJT; ++jt_) gm_[jt_] = *reinterpret_cast<const f32x4*>(sGam + 16 * jt_ + 4 * g); \
+    for (int jt_ = 0; jt_ < NJT; ++jt_) dSt[jt_] *= gm_[jt_];                                 \
+  } while (0)
 #pragma unroll 1
   for (int gb = ngb - 1; gb >= 0; --gb) {
     const int ch = gb / nbc, bc = gb % nbc;
@@ -476,6 +482,10 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         const int t = tid / NGC, kk = tid % NGC;
         *reinterpret_cast<f32x4*>(sGs + t * D + 4 * (kk ^ (t & (NGC - 1)))) = lg_row;
       }
+      // the previous block's state gradient with respect to S (the factor
+      // e^{rho} of its sGam, which the form step below rewrites); deferred
+      // from that block's end, where its loads would wait one by one
+      if (bc < nbc - 1) CARVE_BWD_GAM();
       __syncthreads();
       // the chunks started so far, for the pacing of the recompute
       if (bc == nbc - 1 && tid == 0) __hip_atomic_store(pos, nch - ch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -563,6 +573,15 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
           Qd::st(sdSx + o, Qd::cvt(dSt[jt]));
         }
       }
+      if constexpr (KREC) {
+        // dS' becomes dM = dS' diag(gam) in place, gam = e^{rho} = E of the
+        // block's last token (row 15 of the staged record: the same values
+        // the form step above writes to sGam for its own key tile)
+        f32x4 gm[NJT];
+        for (int jt = 0; jt < NJT; ++jt)
+          gm[jt] = *reinterpret_cast<const f32x4*>(sGs + 15 * D + 4 * ((4 * jt + g) ^ (15 & (NGC - 1))));
+        for (int jt = 0; jt < NJT; ++jt) dSt[jt] *= gm[jt];
+      }
       __syncthreads();
 
       // -- BV: value-side adjoint (value tile w, rows t = 4 g + i, column v = 16 w + c)
@@ -597,9 +616,10 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         // du = Ki dM^T + P^T dO with dM = dS' diag(gam)
         f32x4 du = zero4();
         const T* kir = sKi + c * LDK + ((4 * g) ^ CARVE_QX(c));
-        // dS' (already in LDS for the key side) becomes dM in place: both du and
-        // the state gradient below use dM only
-        for (int jt = 0; jt < NJT; ++jt) dSt[jt] *= *reinterpret_cast<const f32x4*>(sGam + 16 * jt + 4 * g);
+        // dS' (already in LDS for the key side) becomes dM in place (KREC: in
+        // the form step): both du and the state gradient below use dM only
+        if constexpr (!KREC)
+          for (int jt = 0; jt < NJT; ++jt) dSt[jt] *= *reinterpret_cast<const f32x4*>(sGam + 16 * jt + 4 * g);
         for (int jp = 0; jp < NJT / 2; ++jp)
           du = Qd::mma32(Qd::ld(kir + 32 * jp), Qd::ld(kir + 32 * jp + 16), Qd::cvt(dSt[2 * jp]),
                          Qd::cvt(dSt[2 * jp + 1]), du);
@@ -722,24 +742,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
           // multiplied by the zeros of dA there)
           f32x4 db;
           for (int i = 0; i < 4; ++i) db[i] = row_scan(c < 4 * g + i ? dA[i] * A0[i] : 0.0f);
-          if (c == 15) {
-            for (int ww = 0; ww < NW; ++ww) {
-              const f32x4 pv = *reinterpret_cast<const f32x4*>(sDbeta + ww * 16 + 4 * g);
-              for (int i = 0; i < 4; ++i) db[i] += pv[i];
-            }
-            for (int i = 0; i < 4; ++i) dbeta[(tb + 4 * g + i) * H] = (T)db[i];
-          }
-        }
-        if constexpr (SW) {
-          // the write-logit gradient: the waves' partials over the value axis, in order
-          if (w == 1 && c == 15) {
-            f32x4 dw = zero4();
-            for (int ww = 0; ww < NW; ++ww) {
-              const f32x4 pv = *reinterpret_cast<const f32x4*>(sDwx + ww * 16 + 4 * g);
-              for (int i = 0; i < 4; ++i) dw[i] += pv[i];
-            }
-            for (int i = 0; i < 4; ++i) dwx[(tb + 4 * g + i) * H] = (T)dw[i];
-          }
+          // (summed with the value partials by the last wave in the dtau step)
+          if (c == 15) *reinterpret_cast<f32x4*>(sDbeta + NW * 16 + 4 * g) = db;
         }
         const quad bdAT = Qd::cvt(Qd::mma16(Qd::cvt(bdA), CARVE_FI(), zero4()));   // rows s, columns t
         const quad dPT = Qd::cvt(Qd::mma16(Qd::cvt(dP), CARVE_FI(), zero4()));
@@ -812,9 +816,29 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         for (int i = 0; i < 4; ++i) acc[i] *= 1.0f - tau[i] * tau[i];
         Qd::st(sdY + c * LDR + ro, Qd::cvt(acc));
       }
+      // beta gradient: the A part plus the value partials, in that order; and
+      // (scalar write gate) the write-logit gradient from its value partials.
+      // The last wave has no dtau tile at d = 128.
+      if (w == NW - 1 && c == 15) {
+        f32x4 db = *reinterpret_cast<const f32x4*>(sDbeta + NW * 16 + 4 * g);
+        for (int ww = 0; ww < NW; ++ww) {
+          const f32x4 pv = *reinterpret_cast<const f32x4*>(sDbeta + ww * 16 + 4 * g);
+          for (int i = 0; i < 4; ++i) db[i] += pv[i];
+        }
+        for (int i = 0; i < 4; ++i) dbeta[(tb + 4 * g + i) * H] = (T)db[i];
+        if constexpr (SW) {
+          f32x4 dw = zero4();
+          for (int ww = 0; ww < NW; ++ww) {
+            const f32x4 pv = *reinterpret_cast<const f32x4*>(sDwx + ww * 16 + 4 * g);
+            for (int i = 0; i < 4; ++i) dw[i] += pv[i];
+          }
+          for (int i = 0; i < 4; ++i) dwx[(tb + 4 * g + i) * H] = (T)dw[i];
+        }
+      }
       // the value-side step took the state gradient with respect to Sr; with
-      // respect to S it carries the factor e^{rho}
-      for (int jt = 0; jt < NJT; ++jt) dSt[jt] *= *reinterpret_cast<const f32x4*>(sGam + 16 * jt + 4 * g);
+      // respect to S it carries the factor e^{rho}: applied here before the
+      // glue, otherwise at the next block's staging
+      if (bc == 0) CARVE_BWD_GAM();
       __syncthreads();
 
       // BQ of this block runs at the top of the next block (or before the glue)
@@ -868,6 +892,7 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
   }  // blocks (reverse)
 
 #undef CARVE_BWD_BQ
+#undef CARVE_BWD_GAM
 #undef CARVE_QX
 #undef CARVE_LDTR
 #undef CARVE_LDSX

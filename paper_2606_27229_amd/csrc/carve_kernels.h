@@ -321,7 +321,7 @@ __host__ __device__ constexpr BwdLds bwd_lds() {
   l.P = off;     off += lds_round(16 * LDB * e);
   l.Gam = off;   off += lds_round(D * 4);
   l.Beta = off;  off += lds_round((SW ? 32 : 16) * 4);
-  l.Dbeta = off; off += lds_round(NW * 16 * 4);
+  l.Dbeta = off; off += lds_round((NW + 1) * 16 * 4);   // NW value partials + the A part
   l.Dwx = off;   off += SW ? lds_round(NW * 16 * 4) : 0;
   l.Inv = off;   off += (VAR & kVarAct) ? lds_round(2 * 16 * 4) : 0;
   l.Kt = off;    off += lds_round(16 * LDK * e);
