@@ -877,11 +877,19 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
       __syncthreads();
       for (int jt = 0; jt < NJT; ++jt) {
         CARVE_SEQ();
+        // the tile's dF parts in one batch of LDS reads ahead of its products
+        quad fh[R2 / 16], fl[R2 / 16];
+        for (int rq = 0; rq < R2 / 16; ++rq) {
+          const int o = (16 * jt + c) * LDF + 16 * rq + 4 * g;
+          fh[rq] = Qd::ld(sdFh + o);
+          fl[rq] = Qd::ld(sdFl + o);
+        }
+        if constexpr (R2 == 64)
+          asm volatile("" : "+v"(fh[0]), "+v"(fh[1]), "+v"(fh[2]), "+v"(fh[3]), "+v"(fl[0]), "+v"(fl[1]), "+v"(fl[2]), "+v"(fl[3]));
         f32x4 acc = dSt[jt];
         for (int rp = 0; rp < R2 / 32; ++rp) {
-          const int o = (16 * jt + c) * LDF + 32 * rp + 4 * g;
-          acc = Qd::mma32(Qd::ld(sdFh + o), Qd::ld(sdFh + o + 16), fU[2 * rp], fU[2 * rp + 1], acc);
-          acc = Qd::mma32(Qd::ld(sdFl + o), Qd::ld(sdFl + o + 16), fU[2 * rp], fU[2 * rp + 1], acc);
+          acc = Qd::mma32(fh[2 * rp], fh[2 * rp + 1], fU[2 * rp], fU[2 * rp + 1], acc);
+          acc = Qd::mma32(fl[2 * rp], fl[2 * rp + 1], fU[2 * rp], fU[2 * rp + 1], acc);
         }
         dSt[jt] = acc;
       }
