@@ -703,6 +703,10 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
           const f32x4 x0 = Qd::f32(a0), x1 = Qd::f32(a1), y0 = Qd::f32(s0), y1 = Qd::f32(s1);
           for (int e = 0; e < 4; ++e) dgs += x0[e] * y0[e] + x1[e] * y1[e];
         }
+        // the transposed operand tiles of the products after the elementwise
+        // gradients, read now: their LDS latency overlaps the permutes below
+        const quad KiT = CARVE_LDTR(sKi, LDK, 0, 16 * w);
+        const quad KtT = CARVE_LDTR(sKt, LDK, 0, 16 * w), QtT = CARVE_LDTR(sQt, LDK, 0, 16 * w);
         dgs += __shfl_xor(dgs, 16);
         dgs += __shfl_xor(dgs, 32);
         const float bc_ = sBeta[c];
@@ -747,10 +751,8 @@ __device__ __forceinline__ void bwd_adjoint(const BwdArgs& a, const int bh, char
         }
         const quad bdAT = Qd::cvt(Qd::mma16(Qd::cvt(bdA), CARVE_FI(), zero4()));   // rows s, columns t
         const quad dPT = Qd::cvt(Qd::mma16(Qd::cvt(dP), CARVE_FI(), zero4()));
-        const quad KiT = CARVE_LDTR(sKi, LDK, 0, 16 * w);
         dKt = Qd::mma16(KiT, bdAT, dKt);
-        dKi = Qd::mma32(CARVE_LDTR(sKt, LDK, 0, 16 * w), CARVE_LDTR(sQt, LDK, 0, 16 * w), Qd::cvt(bdA),
-                        Qd::cvt(dP), dKi);
+        dKi = Qd::mma32(KtT, QtT, Qd::cvt(bdA), Qd::cvt(dP), dKi);
         dQt = Qd::mma16(KiT, dPT, dQt);
         // elementwise: lane (g, c) holds j = 16 w + 4 g + i, t = c
         f32x4 dzb, dgv, dkv;
